@@ -1,0 +1,372 @@
+/*
+ * CPU oracle for the Hadamard-domain INT8 linear operator (HaTQ).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or call
+ * this file; only the tests, the smoke check and the benchmark's CPU-baseline leg
+ * do.  It shares no code, header, table or helper with the HIP library: every
+ * step is re-derived here from the paper in the plainest form available
+ * (dense matrices, direct loops, fp64 sums, IEEE fp32 division, RNE rounding).
+ *
+ * Notation (paper): Y = X W^T + b (Eq. supp_linear_operator); a Sylvester matrix
+ * H~_m with H~ H~^T = m I (Eq. supp_hadamard_properties, Eq. supp_sylvester);
+ * symmetric quantizer with q_max = 127 and s = ||x||_inf / 127 (Eq. symmetric_q,
+ * Eq. current_scale); INT32 accumulation (Eq. integer_accumulation); accumulator
+ * scale s_x s_w,c (Eq. accumulator_scale); DH and WH forms (Eq.
+ * double_hadamard_quantization, Eq. weight_only_hadamard_quantization, and their
+ * padded versions Eq. supp_padded_dh, Eq. supp_padded_wh).
+ *
+ * Readings taken where the paper is silent (each listed in the design notes):
+ *  - round() is IEEE round-half-to-even; x/s is an IEEE fp32 division.
+ *  - The transform is the block-diagonal B_C = I_{C_pad/b} (x) H~_b, unnormalized;
+ *    the 1/sqrt(b) normalizations of both sides are absorbed into the dequant
+ *    scale as one exact factor 1/b (Sec. IV-B "absorbed into fixed-point
+ *    requantization"; Supplementary "Deployment Realization").
+ *  - One activation scale per sample (per input tensor at inference).
+ *  - An all-zero tensor or weight row gets scale 1 and all-zero codes.
+ *  - Bias is added in fp32 after dequantization, in the accumulator basis
+ *    (transformed for WH, Eq. supp_padded_wh_parameters), before the WH
+ *    output-basis restore; per-channel scales are applied before that restore
+ *    (Supplementary "General Nonlinearities", ordering rule).
+ *
+ * Built with -O2 -fopenmp -ffp-contract=off (no fast-math): every fp32 product
+ * and quotient below is a single correctly rounded IEEE operation.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+static int is_pow2(int b) { return b >= 1 && (b & (b - 1)) == 0; }
+static int round_up(int v, int m) { return (v + m - 1) / m * m; }
+
+/* ------------------------------------------------------------------------- */
+/* O1. Sylvester matrix by its recursion (Eq. supp_sylvester):                */
+/*     H~_1 = [1],  H~_2m = [[H~_m, H~_m], [H~_m, -H~_m]].                   */
+/* H is b*b, row-major.  Returns 0, or -1 when b is not a power of two.       */
+/* ------------------------------------------------------------------------- */
+int orc_sylvester(int b, int8_t *H)
+{
+    if (!is_pow2(b)) return -1;
+    H[0] = 1;
+    for (int m = 1; m < b; m *= 2)
+        for (int i = 0; i < m; ++i)
+            for (int j = 0; j < m; ++j) {
+                int8_t v = H[i * b + j];
+                H[i * b + (j + m)] = v;
+                H[(i + m) * b + j] = v;
+                H[(i + m) * b + (j + m)] = (int8_t)-v;
+            }
+    return 0;
+}
+
+/* Dense block-diagonal transform along the last axis, fp64 in and out:       */
+/*   out[r, blk*b + i] = sum_j H~_b[i][j] * in[r, blk*b + j]                   */
+/* for width = nblk*b.  Summation runs over j in natural order.               */
+static void block_transform_f64(const int8_t *H, int b, const double *in, double *out,
+                                int64_t rows, int width)
+{
+    const int nblk = width / b;
+    for (int64_t r = 0; r < rows; ++r)
+        for (int blk = 0; blk < nblk; ++blk)
+            for (int i = 0; i < b; ++i) {
+                double acc = 0.0;
+                for (int j = 0; j < b; ++j)
+                    acc += (double)H[i * b + j] * in[r * width + blk * b + j];
+                out[r * width + blk * b + i] = acc;
+            }
+}
+
+/* Public wrapper: fp64 block transform of `rows` rows of width `width`. */
+int orc_block_transform_f64(int b, const double *in, double *out, int64_t rows, int width)
+{
+    if (!is_pow2(b) || width % b) return -1;
+    int8_t *H = (int8_t *)malloc((size_t)b * b);
+    orc_sylvester(b, H);
+    block_transform_f64(H, b, in, out, rows, width);
+    free(H);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* O3. Activation operand.  DH: S = fl32(B_C x_pad) per pixel, computed in    */
+/* fp64 with one rounding (Eq. input_hadamard_transform, Eq. supp_padded_     */
+/* transforms: zero-pad C to C_pad = b*ceil(C/b)).  WH: b = 1, S = x.         */
+/* x is [P, C] fp32 (P pixels), S is [P, C_pad] fp32.                         */
+/* ------------------------------------------------------------------------- */
+int orc_activation_transform(const float *x, int64_t P, int C, int b, float *S)
+{
+    if (!is_pow2(b) || C <= 0) return -1;
+    const int Cp = round_up(C, b);
+    int8_t *H = (int8_t *)malloc((size_t)b * b);
+    orc_sylvester(b, H);
+    #pragma omp parallel
+    {
+        double *in = (double *)malloc(sizeof(double) * Cp);
+        double *out = (double *)malloc(sizeof(double) * Cp);
+        #pragma omp for schedule(static)
+        for (int64_t p = 0; p < P; ++p) {
+            for (int c = 0; c < Cp; ++c) in[c] = c < C ? (double)x[p * C + c] : 0.0;
+            block_transform_f64(H, b, in, out, 1, Cp);
+            for (int c = 0; c < Cp; ++c) S[p * Cp + c] = (float)out[c];
+        }
+        free(in);
+        free(out);
+    }
+    free(H);
+    return 0;
+}
+
+/* Symmetric per-tensor quantizer (Eq. symmetric_q, Eq. current_scale), one    */
+/* scale per sample.  S is [nsamp, per] fp32.                                 */
+/*   A = max |S|;  s = fl32(A / 127) (A > 0), else s = 1;                      */
+/*   q = clamp(rne(fl32(S / s)), -127, 127).                                   */
+void orc_quantize_symmetric(const float *S, int64_t nsamp, int64_t per, int8_t *q, float *scale)
+{
+    for (int64_t n = 0; n < nsamp; ++n) {
+        const float *s_n = S + n * per;
+        float A = 0.0f;
+        for (int64_t i = 0; i < per; ++i) {
+            float a = fabsf(s_n[i]);
+            if (a > A) A = a;
+        }
+        const float s = A > 0.0f ? A / 127.0f : 1.0f;
+        scale[n] = s;
+        #pragma omp parallel for schedule(static)
+        for (int64_t i = 0; i < per; ++i) {
+            float t = nearbyintf(s_n[i] / s);
+            if (t > 127.0f) t = 127.0f;
+            if (t < -127.0f) t = -127.0f;
+            q[n * per + i] = (int8_t)t;
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------- */
+/* O2. Weight preparation (offline).                                          */
+/* Input: PyTorch layout, OIHW [cout][cin][k][k] for a convolution, IOHW      */
+/* [cin][cout][k][k] for a transposed one.  Output canonical layout OHWI:     */
+/* wq[cout_pad][k][k][cin_pad], w_scale[cout_pad], w_bias[cout_pad].          */
+/* The contraction index of one output is d = (kh*K + kw)*cin_pad + ci, the   */
+/* Kronecker order I_{KhKw} (x) H of Eq. input_hadamard_transform.            */
+/*  DH (form 0): each (co, tap) row is multiplied by B_Cin (cin padded to b); */
+/*               bias untransformed.                                          */
+/*  WH (form 1): each (tap, ci) column is multiplied by B_Cout (cout padded   */
+/*               to b); bias b~ = B_Cout [b; 0] (Eq. supp_padded_wh_params).  */
+/* Transforms in fp64 with one rounding to fp32; then per output channel      */
+/* s_w = fl32(max|W'| / 127) (1 for an all-zero row) and                      */
+/* wq = clamp(rne(fl32(W'/s_w)), -127, 127).  w_real (nullable) receives the  */
+/* unquantized fp32 W' in the same layout.                                    */
+/* ------------------------------------------------------------------------- */
+int orc_prepare_weights(int cin, int cout, int k, int transposed, int hblock, int form,
+                        const float *w, const float *bias,
+                        int8_t *wq, float *w_scale, float *w_bias, float *w_real)
+{
+    if (!is_pow2(hblock) || cin <= 0 || cout <= 0 || k <= 0 || (form != 0 && form != 1))
+        return -1;
+    const int cin_p = form == 0 ? round_up(cin, hblock) : cin;
+    const int cout_p = form == 1 ? round_up(cout, hblock) : cout;
+    const int taps = k * k;
+    const int64_t per_co = (int64_t)taps * cin_p;
+    double *W0 = (double *)calloc((size_t)cout_p * per_co, sizeof(double));
+    float *W1 = (float *)malloc(sizeof(float) * (size_t)cout_p * per_co);
+    int8_t *H = (int8_t *)malloc((size_t)hblock * hblock);
+    orc_sylvester(hblock, H);
+
+    /* canonical fp64 copy, zero padded */
+    for (int co = 0; co < cout; ++co)
+        for (int kh = 0; kh < k; ++kh)
+            for (int kw = 0; kw < k; ++kw)
+                for (int ci = 0; ci < cin; ++ci) {
+                    float v = transposed ? w[(((int64_t)ci * cout + co) * k + kh) * k + kw]
+                                         : w[(((int64_t)co * cin + ci) * k + kh) * k + kw];
+                    W0[(int64_t)co * per_co + (kh * k + kw) * cin_p + ci] = v;
+                }
+
+    if (form == 0) {
+        double *out = (double *)malloc(sizeof(double) * cin_p);
+        for (int co = 0; co < cout_p; ++co)
+            for (int t = 0; t < taps; ++t) {
+                const double *row = W0 + (int64_t)co * per_co + (int64_t)t * cin_p;
+                block_transform_f64(H, hblock, row, out, 1, cin_p);
+                for (int ci = 0; ci < cin_p; ++ci)
+                    W1[(int64_t)co * per_co + (int64_t)t * cin_p + ci] = (float)out[ci];
+            }
+        free(out);
+    } else {
+        double *col = (double *)malloc(sizeof(double) * cout_p);
+        double *out = (double *)malloc(sizeof(double) * cout_p);
+        for (int64_t d = 0; d < per_co; ++d) {
+            for (int co = 0; co < cout_p; ++co) col[co] = W0[(int64_t)co * per_co + d];
+            block_transform_f64(H, hblock, col, out, 1, cout_p);
+            for (int co = 0; co < cout_p; ++co) W1[(int64_t)co * per_co + d] = (float)out[co];
+        }
+        free(col);
+        free(out);
+    }
+
+    if (w_real) memcpy(w_real, W1, sizeof(float) * (size_t)cout_p * per_co);
+    for (int co = 0; co < cout_p; ++co) {
+        const float *row = W1 + (int64_t)co * per_co;
+        float A = 0.0f;
+        for (int64_t d = 0; d < per_co; ++d)
+            if (fabsf(row[d]) > A) A = fabsf(row[d]);
+        const float s = A > 0.0f ? A / 127.0f : 1.0f;
+        w_scale[co] = s;
+        for (int64_t d = 0; d < per_co; ++d) {
+            float t = nearbyintf(row[d] / s);
+            if (t > 127.0f) t = 127.0f;
+            if (t < -127.0f) t = -127.0f;
+            wq[(int64_t)co * per_co + d] = (int8_t)t;
+        }
+    }
+
+    if (form == 0) {
+        for (int co = 0; co < cout_p; ++co) w_bias[co] = (bias && co < cout) ? bias[co] : 0.0f;
+    } else {
+        double *bb = (double *)calloc(cout_p, sizeof(double));
+        double *out = (double *)malloc(sizeof(double) * cout_p);
+        for (int co = 0; co < cout; ++co) bb[co] = bias ? bias[co] : 0.0;
+        block_transform_f64(H, hblock, bb, out, 1, cout_p);
+        for (int co = 0; co < cout_p; ++co) w_bias[co] = (float)out[co];
+        free(bb);
+        free(out);
+    }
+    free(W0);
+    free(W1);
+    free(H);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Output size of a convolution or transposed convolution.                    */
+/* ------------------------------------------------------------------------- */
+int orc_out_size(int in, int k, int stride, int pad, int transposed, int out_pad)
+{
+    if (transposed) return (in - 1) * stride - 2 * pad + k + out_pad;
+    return (in + 2 * pad - k) / stride + 1;
+}
+
+/* Input row feeding output row o through tap i, or -1 when the tap lands on   */
+/* zero padding.  Direct form: ih = o*s - p + i.  Transposed (gather) form:   */
+/* t = o + p - i, used iff t >= 0, t % s == 0 and t/s < in.                   */
+static int src_index(int o, int i, int in, int stride, int pad, int transposed)
+{
+    if (!transposed) {
+        int ih = o * stride - pad + i;
+        return (ih >= 0 && ih < in) ? ih : -1;
+    }
+    int t = o + pad - i;
+    if (t < 0 || t % stride) return -1;
+    t /= stride;
+    return t < in ? t : -1;
+}
+
+/* ------------------------------------------------------------------------- */
+/* O4. INT8 convolution with INT32 accumulation (Eq. integer_accumulation with */
+/* zero points 0; Eq. linear_operator unfolded): a direct seven-loop sum.     */
+/* xq: [n][h][w][cin_p] int8, wq: [cout_p][k][k][cin_p] int8 (OHWI),          */
+/* acc: [n][ho][wo][cout_p] int32.  Out-of-range taps contribute 0.           */
+/* ------------------------------------------------------------------------- */
+void orc_conv_int8(const int8_t *xq, int n, int h, int w, int cin_p,
+                   const int8_t *wq, int cout_p, int k, int stride, int pad,
+                   int transposed, int out_pad, int32_t *acc)
+{
+    const int ho = orc_out_size(h, k, stride, pad, transposed, out_pad);
+    const int wo = orc_out_size(w, k, stride, pad, transposed, out_pad);
+    #pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int b = 0; b < n; ++b)
+        for (int oh = 0; oh < ho; ++oh)
+            for (int ow = 0; ow < wo; ++ow)
+                for (int co = 0; co < cout_p; ++co) {
+                    int32_t a = 0;
+                    for (int kh = 0; kh < k; ++kh) {
+                        const int ih = src_index(oh, kh, h, stride, pad, transposed);
+                        if (ih < 0) continue;
+                        for (int kw = 0; kw < k; ++kw) {
+                            const int iw = src_index(ow, kw, w, stride, pad, transposed);
+                            if (iw < 0) continue;
+                            const int8_t *xp = xq + (((int64_t)b * h + ih) * w + iw) * cin_p;
+                            const int8_t *wp = wq + (((int64_t)co * k + kh) * k + kw) * cin_p;
+                            for (int ci = 0; ci < cin_p; ++ci)
+                                a += (int32_t)xp[ci] * (int32_t)wp[ci];
+                        }
+                    }
+                    acc[(((int64_t)b * ho + oh) * wo + ow) * cout_p + co] = a;
+                }
+}
+
+/* Same loops in fp64 on real values: used for the unquantized function-       */
+/* preservation checks.  x: [n][h][w][cin], wf: [cout][k][k][cin] (OHWI).     */
+void orc_conv_f64(const double *x, int n, int h, int w, int cin,
+                  const double *wf, int cout, int k, int stride, int pad,
+                  int transposed, int out_pad, double *y)
+{
+    const int ho = orc_out_size(h, k, stride, pad, transposed, out_pad);
+    const int wo = orc_out_size(w, k, stride, pad, transposed, out_pad);
+    #pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int b = 0; b < n; ++b)
+        for (int oh = 0; oh < ho; ++oh)
+            for (int ow = 0; ow < wo; ++ow)
+                for (int co = 0; co < cout; ++co) {
+                    double a = 0.0;
+                    for (int kh = 0; kh < k; ++kh) {
+                        const int ih = src_index(oh, kh, h, stride, pad, transposed);
+                        if (ih < 0) continue;
+                        for (int kw = 0; kw < k; ++kw) {
+                            const int iw = src_index(ow, kw, w, stride, pad, transposed);
+                            if (iw < 0) continue;
+                            const double *xp = x + (((int64_t)b * h + ih) * w + iw) * cin;
+                            const double *wp = wf + (((int64_t)co * k + kh) * k + kw) * cin;
+                            for (int ci = 0; ci < cin; ++ci) a += xp[ci] * wp[ci];
+                        }
+                    }
+                    y[(((int64_t)b * ho + oh) * wo + ow) * cout + co] = a;
+                }
+}
+
+/* ------------------------------------------------------------------------- */
+/* O5. Epilogues.  acc: [n][pix][cout_p] int32, sx[n], sw[cout_p], bias.       */
+/* DH: y = fma(float(acc), t_c, bias_c),  t_c = fl(fl(sx*sw_c) * 2^-log2(b)),  */
+/*     for c < cout (output in the original basis, Eq. supp_padded_dh).       */
+/* WH: z_c = fma(float(acc_c), fl(sx*sw_c), b~_c) for every c < cout_p (scale  */
+/*     aligned before the basis change), then y = fl32(B_Cout z / b) with a   */
+/*     dense fp64 multiply, truncated to cout (Eq. supp_padded_wh).           */
+/* ------------------------------------------------------------------------- */
+int orc_epilogue(const int32_t *acc, int n, int64_t pix, int cout, int cout_p, int form,
+                 int hblock, const float *sx, const float *sw, const float *bias, float *y)
+{
+    if (!is_pow2(hblock) || (form == 1 && cout_p % hblock)) return -1;
+    const float inv_b = 1.0f / (float)hblock; /* exact: power of two */
+    int8_t *H = NULL;
+    if (form == 1) {
+        H = (int8_t *)malloc((size_t)hblock * hblock);
+        orc_sylvester(hblock, H);
+    }
+    for (int b = 0; b < n; ++b) {
+        #pragma omp parallel
+        {
+            double *z = (double *)malloc(sizeof(double) * cout_p);
+            double *out = (double *)malloc(sizeof(double) * cout_p);
+            #pragma omp for schedule(static)
+            for (int64_t p = 0; p < pix; ++p) {
+                const int32_t *a = acc + ((int64_t)b * pix + p) * cout_p;
+                float *yo = y + ((int64_t)b * pix + p) * cout;
+                if (form == 0) {
+                    for (int c = 0; c < cout; ++c) {
+                        const float t = (sx[b] * sw[c]) * inv_b;
+                        yo[c] = fmaf((float)a[c], t, bias[c]);
+                    }
+                } else {
+                    for (int c = 0; c < cout_p; ++c)
+                        z[c] = (double)fmaf((float)a[c], sx[b] * sw[c], bias[c]);
+                    block_transform_f64(H, hblock, z, out, 1, cout_p);
+                    for (int c = 0; c < cout; ++c) yo[c] = (float)(out[c] / (double)hblock);
+                }
+            }
+            free(z);
+            free(out);
+        }
+    }
+    free(H);
+    return 0;
+}
