@@ -1,0 +1,190 @@
+/*
+ * hatq.h -- C ABI of the MI355X (gfx950) Hadamard-domain INT8 linear operator.
+ *
+ * The operator is the inference-time layer of HaTQ ("Hadamard-Domain Model
+ * Quantization for Learned Image Coding"): a convolution or fully connected
+ * layer Y = X W^T + b (Eq. supp_linear_operator) evaluated with INT8 operands in
+ * a Hadamard domain, in one of two per-layer forms (Sec. IV-B):
+ *
+ *   DH (double-Hadamard, Eq. double_hadamard_quantization): activations and
+ *      weights are both transformed along the contracted input channels,
+ *      Y = Q(X T_in) Q(W T_in)^T.
+ *   WH (weight-only Hadamard, Eq. weight_only_hadamard_quantization): weights
+ *      are transformed along output channels, activations are quantized in the
+ *      original domain, and the accumulator is mapped back,
+ *      Y = [Q(X) Q(T_out^T W)^T + b~] T_out^T   (Eq. supp_padded_wh).
+ *
+ * Transforms are block diagonal, B_C = I_{C/b} (x) H~_b, with H~_b the
+ * unnormalized Sylvester matrix of order b (Eq. supp_sylvester, natural order).
+ * The normalization 1/sqrt(b) of each side is folded into the dequantization
+ * scale as one exact factor 1/b (Supplementary, "Deployment Realization").
+ *
+ * Quantization is symmetric INT8 with codes in [-127, 127] (Eq. symmetric_q):
+ * per-sample dynamic activation scale s_x = ||S||_inf / 127 (Eq. current_scale)
+ * and per-output-channel weight scale; rounding is round-half-to-even and x/s is
+ * an IEEE fp32 division.  The INT8 x INT8 products accumulate in INT32
+ * (Eq. integer_accumulation); the accumulator of channel c has scale
+ * s_x * s_w,c (Eq. accumulator_scale).
+ *
+ * Conventions for every entry point:
+ *  - Tensors are NHWC, row-major, densely packed.  All tensor pointers are
+ *    DEVICE pointers owned by the caller; the library never allocates, frees or
+ *    synchronizes, and keeps no global state.  Calls are reentrant; calls on one
+ *    stream execute in order.
+ *  - `stream` is a hipStream_t (NULL = the default stream).
+ *  - Arguments are validated on the host before any launch.  On error nothing
+ *    is launched and outputs are untouched.  A launch failure is reported as
+ *    HATQ_EHIP; faults inside kernels surface at the caller's next
+ *    synchronization.  Nothing is printed and no C++ exception crosses the ABI.
+ *  - Unless noted, no entry point reads device memory on the host.
+ */
+#ifndef HATQ_H
+#define HATQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    HATQ_OK = 0,
+    HATQ_EINVAL = 1,        /* bad argument: null pointer, bad size, form mismatch */
+    HATQ_EUNSUPPORTED = 2,  /* valid operator outside the kernels' supported geometry */
+    HATQ_EWORKSPACE = 3,    /* caller-provided buffer too small */
+    HATQ_EHIP = 4           /* a HIP launch or runtime call failed */
+} hatq_status;
+
+typedef enum { HATQ_DH = 0, HATQ_WH = 1 } hatq_form;
+
+typedef enum {
+    HATQ_OUT_I32 = 0,       /* raw INT32 accumulators [n][ho][wo][cout_pad], no bias;
+                               WH accumulators stay in the output Hadamard basis */
+    HATQ_OUT_F32 = 1        /* dequantized fp32 output [n][ho][wo][cout], original basis */
+} hatq_out_mode;
+
+/* One layer's geometry.  Square kernels only.
+ *   conv:        ho = (h + 2*pad - k)/stride + 1
+ *   transposed:  ho = (h - 1)*stride - 2*pad + k + out_pad
+ * hblock: Sylvester block size b, a power of two in [1, 128]; it acts on cin
+ * for DH and on cout for WH.  b = 1 means no transform. */
+typedef struct {
+    int32_t cin, cout;
+    int32_t k;
+    int32_t stride, pad, out_pad;
+    int32_t transposed;     /* 0: convolution, 1: transposed convolution */
+    int32_t hblock;
+} hatq_conv_desc;
+
+/* Prepared weights: a plain view into the caller's device buffer, filled by
+ * hatq_prepare_weights.  Layout of wq: [cout_pad][k_stride] int8, row co holds
+ * the contraction index d = (kh*k + kw)*cin_pad + ci (the Kronecker order
+ * I_{KhKw} (x) H of Eq. input_hadamard_transform); bytes d >= k_total are 0.
+ * For a transposed convolution (kh, kw) index the kernel as stored in PyTorch
+ * (weight[ci][co][kh][kw]).  w_scale and bias are fp32 [cout_pad]; for WH the
+ * bias is the transformed b~ = B_Cout [b; 0] (Eq. supp_padded_wh_parameters). */
+typedef struct {
+    hatq_conv_desc d;
+    int32_t form;           /* hatq_form, fixed for the layer's lifetime (Sec. IV-C) */
+    int32_t cin_pad;        /* cin (DH: rounded up to hblock) */
+    int32_t cout_pad;       /* cout (WH: rounded up to hblock) */
+    int32_t k_total;        /* k*k*cin_pad */
+    int32_t k_stride;       /* k_total rounded up to 64 */
+    int8_t *wq;
+    float *w_scale;
+    float *bias;
+} hatq_weights;
+
+/* Static description of a status code.  Never NULL. */
+const char *hatq_status_string(int32_t status);
+
+/* Output spatial size of `d` for an input of h x w.  HATQ_EINVAL if the result
+ * would be empty. Host only. */
+int32_t hatq_conv_out_hw(const hatq_conv_desc *d, int32_t h, int32_t w, int32_t *ho, int32_t *wo);
+
+/* Bytes of device memory hatq_prepare_weights needs for `d` in form `form`
+ * (0 for an invalid descriptor). */
+size_t hatq_weights_bytes(const hatq_conv_desc *d, int32_t form);
+
+/* Offline weight preparation (Eq. hadamard_linear_equivalence and
+ * Eq. weight_only_hadamard_equivalence with the padded forms of the
+ * supplementary; per-channel symmetric quantization, Eq. symmetric_q).
+ *   w:    device fp32 weights in PyTorch layout, OIHW [cout][cin][k][k] for a
+ *         convolution, IOHW [cin][cout][k][k] for a transposed convolution.
+ *   bias: device fp32 [cout], or NULL for no bias.
+ *   dst:  device buffer of at least hatq_weights_bytes(d, form) bytes; it holds
+ *         wq, w_scale and bias afterwards.  `out` (host struct) receives the
+ *         view into it.
+ * The transform is evaluated in fp64 and rounded once to fp32; then
+ * s_w,c = fl32(max|W'_c| / 127) (1 for an all-zero row) and
+ * wq = clamp(rne(fl32(W'/s_w,c)), -127, 127).  Runs on `stream`.
+ * Supported: DH needs cin % hblock == 0, WH needs cout % hblock == 0. */
+int32_t hatq_prepare_weights(const hatq_conv_desc *d, int32_t form, const float *w,
+                             const float *bias, void *dst, size_t dst_bytes,
+                             hatq_weights *out, void *stream);
+
+/* Workspace bytes hatq_fwht_quant_act needs for a batch of n samples. */
+size_t hatq_fwht_quant_ws_bytes(int32_t n);
+
+/* Activation transform and quantization, steps a2-a4 of one layer
+ * (Eq. input_hadamard_transform, Eq. symmetric_q, Eq. current_scale):
+ *   S[p] = B_c x[p] along channels (hblock = 1: S = x),
+ *   s_x[i] = fl32(max |S over sample i| / 127)  (1 if that max is 0),
+ *   xq = clamp(rne(fl32(S / s_x[i])), -127, 127).
+ *   x:        device fp32 [n][h][w][c].
+ *   absmax:   NULL, or device fp32 [n] holding max |S| per sample already (as
+ *             produced by hatq_conv_int8's next_absmax); then the input is read
+ *             once instead of twice.
+ *   xq:       device int8 [n][h][w][c].
+ *   act_scale: device fp32 [n], receives s_x (unnormalized-domain scale).
+ *   ws:       device workspace of hatq_fwht_quant_ws_bytes(n) bytes (unused
+ *             when absmax is given).
+ * Supported: c % hblock == 0, and c % 4 == 0 or hblock == 1. */
+int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int32_t c,
+                            int32_t hblock, const float *absmax, int8_t *xq, float *act_scale,
+                            void *ws, size_t ws_bytes, void *stream);
+
+/* INT8 convolution with INT32 accumulation and the fused epilogue, steps a5-a6
+ * (Eq. integer_accumulation, Eq. accumulator_scale, Table I).
+ *   xq:        device int8 [n][h][w][cin_pad] (codes from hatq_fwht_quant_act).
+ *   act_scale: device fp32 [n].
+ *   mode HATQ_OUT_I32: y is int32 [n][ho][wo][cout_pad], raw accumulators.
+ *   mode HATQ_OUT_F32: y is fp32 [n][ho][wo][cout]:
+ *     DH: y = fma(float(acc), fl(s_x*s_w,c) * (1/b), bias_c);
+ *     WH: z_c = fma(float(acc), fl(s_x*s_w,c), b~_c) (scale before the basis
+ *         change, Supplementary "General Nonlinearities"), y = (B_Cout z)/b,
+ *         truncated to cout.
+ *   next_hblock / next_absmax (F32 mode only): if next_absmax is non-NULL it
+ *     receives, per sample, max |B_{next} y| with block size next_hblock (1: max
+ *     |y|), the exact value hatq_fwht_quant_act would compute from y; the next
+ *     layer can then quantize y reading it once.  It is overwritten, not
+ *     accumulated.
+ * Supported: cin_pad % 64 == 0 (any k), or cin_pad <= 8 with k*k*cin_pad <= 128;
+ * cout_pad % 64 == 0.  Transposed: stride 2. */
+int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act_scale,
+                       int32_t n, int32_t h, int32_t w, int32_t out_mode, void *y,
+                       int32_t next_hblock, float *next_absmax, void *stream);
+
+/* Workspace bytes of hatq_layer_forward for an input of n x h x w. */
+size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w);
+
+/* One whole layer (step a7): hatq_fwht_quant_act then hatq_conv_int8 in F32
+ * mode, with the transform of the layer's own form (DH: hblock on cin; WH: none
+ * on the activations).
+ *   form:      must equal W->form (the per-layer form flag), else HATQ_EINVAL.
+ *   x:         device fp32 [n][h][w][cin].
+ *   x_absmax:  NULL, or per-sample max |T_in x| already known (see above).
+ *   y:         device fp32 [n][ho][wo][cout].
+ *   act_scale: NULL, or device fp32 [n] receiving s_x.
+ *   next_hblock, next_absmax: as in hatq_conv_int8.
+ *   ws:        at least hatq_layer_ws_bytes(W, n, h, w) bytes of device memory. */
+int32_t hatq_layer_forward(const hatq_weights *W, int32_t form, const float *x, int32_t n,
+                           int32_t h, int32_t w, const float *x_absmax, float *y,
+                           float *act_scale, int32_t next_hblock, float *next_absmax,
+                           void *ws, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HATQ_H */

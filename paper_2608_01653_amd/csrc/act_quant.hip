@@ -1,0 +1,263 @@
+// Activation transform + per-sample absmax + INT8 quantization (steps a2-a4).
+//
+// The input of one sample is a flat fp32 array of E = h*w*c elements (NHWC).
+// With c % b == 0 every Hadamard block (b consecutive channels of one pixel) is
+// b-aligned in the flat array, so the kernel tiles the array into "items" of
+// I = max(64, b) consecutive floats without looking at pixel boundaries.
+//
+// One quad (4 lanes) owns one item.  Lane t of the quad holds the channels
+// c = 16*i + 4*t + j (j = 0..3 inside a float4, i = 0..I/16-1): bits 0-1 of
+// the channel index are inside a float4, bits 2-3 are the lane, bits 4+ are the
+// register index.  Loads are 64 contiguous bytes per quad per instruction.
+//
+// Two kernels:
+//   absmax_kernel: transform, max |S| per sample (one atomic per block).
+//   quant_kernel : transform again, quantize with s = fl32(A / 127), store codes.
+// When the producer of x already computed A (next_absmax of the convolution),
+// only quant_kernel runs and x is read once.
+#include "hatq_device.h"
+#include "hatq_launch.h"
+
+namespace hatq {
+
+__global__ void fill_u32_kernel(uint32_t *p, int n, uint32_t v) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = v;
+}
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kQuadsPerBlock = kThreads / 4;
+
+template <int B>
+struct ItemShape {
+    static constexpr int I = B > 64 ? B : 64;   // floats per item
+    static constexpr int R = I / 16;            // float4 registers per lane
+    static constexpr int LOG = B == 1 ? 0 : B == 2 ? 1 : B == 4 ? 2 : B == 8 ? 3 : B == 16 ? 4
+                               : B == 32 ? 5 : B == 64 ? 6 : 7;
+};
+
+// Transform of one item held as v[4*i + j] (lane t = quad position).
+// Returns sigma, the sign of the values held relative to the true transform.
+template <int B, int R4>
+__device__ __forceinline__ float fwht_item(float (&v)[R4], int t) {
+    constexpr int LOG = ItemShape<B>::LOG;
+    float sigma = 1.0f;
+    if constexpr (LOG >= 1) reg_stage<1>(v);                 // channel bit 0
+    if constexpr (LOG >= 2) reg_stage<2>(v);                 // channel bit 1
+    if constexpr (LOG >= 3) {                                 // channel bit 2: lane ^ 1
+        const float c = (t & 1) ? -1.0f : 1.0f;
+        cross_stage<1>(v, c);
+        sigma *= c;
+    }
+    if constexpr (LOG >= 4) {                                 // channel bit 3: lane ^ 2
+        const float c = (t & 2) ? -1.0f : 1.0f;
+        cross_stage<2>(v, c);
+        sigma *= c;
+    }
+    if constexpr (LOG >= 5) reg_stage<4>(v);                 // channel bit 4: register ^ 1
+    if constexpr (LOG >= 6) reg_stage<8>(v);                 // channel bit 5
+    if constexpr (LOG >= 7) reg_stage<16>(v);                // channel bit 6
+    return sigma;
+}
+
+template <int B>
+__device__ __forceinline__ void load_item(const float *xs, int64_t base, int64_t E, int t,
+                                          float (&v)[4 * ItemShape<B>::R]) {
+    constexpr int R = ItemShape<B>::R;
+    constexpr int I = ItemShape<B>::I;
+    const bool full = base + I <= E;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const int64_t off = base + 16 * i + 4 * t;
+        float4 f = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (full || off < E) f = *reinterpret_cast<const float4 *>(xs + off);
+        v[4 * i + 0] = f.x;
+        v[4 * i + 1] = f.y;
+        v[4 * i + 2] = f.z;
+        v[4 * i + 3] = f.w;
+    }
+}
+
+template <int B>
+__global__ void __launch_bounds__(kThreads) absmax_kernel(const float *__restrict__ x, int64_t E,
+                                                          float *__restrict__ absmax) {
+    constexpr int R = ItemShape<B>::R;
+    constexpr int I = ItemShape<B>::I;
+    const int n = blockIdx.y;
+    const float *xs = x + (int64_t)n * E;
+    const int t = threadIdx.x & 3;
+    const int64_t items = (E + I - 1) / I;
+    float m = 0.0f;
+    for (int64_t it = (int64_t)blockIdx.x * kQuadsPerBlock + (threadIdx.x >> 2); it < items;
+         it += (int64_t)gridDim.x * kQuadsPerBlock) {
+        float v[4 * R];
+        load_item<B>(xs, it * I, E, t, v);
+        fwht_item<B>(v, t);
+#pragma unroll
+        for (int r = 0; r < 4 * R; ++r) m = fmaxf(m, fabsf(v[r]));
+    }
+    m = wave_max(m);
+    __shared__ float red[kThreads / 64];
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float b = red[0];
+#pragma unroll
+        for (int k = 1; k < kThreads / 64; ++k) b = fmaxf(b, red[k]);
+        atomic_max_nonneg(absmax + n, b);
+    }
+}
+
+template <int B>
+__global__ void __launch_bounds__(kThreads) quant_kernel(const float *__restrict__ x, int64_t E,
+                                                         const float *__restrict__ absmax,
+                                                         int8_t *__restrict__ xq,
+                                                         float *__restrict__ act_scale) {
+    constexpr int R = ItemShape<B>::R;
+    constexpr int I = ItemShape<B>::I;
+    const int n = blockIdx.y;
+    const float *xs = x + (int64_t)n * E;
+    int8_t *qs = xq + (int64_t)n * E;
+    const int t = threadIdx.x & 3;
+    const float s = act_scale_from_absmax(absmax[n]);
+    if (blockIdx.x == 0 && threadIdx.x == 0) act_scale[n] = s;
+    const float r = 1.0f / s;
+    // The fast path needs r and every t finite and normal-range; a scale below
+    // 2^-125 or above 2^125 takes the exact division for every element.
+    const bool fast_ok = s >= 0x1p-125f && s <= 0x1p125f;
+    const int64_t items = (E + I - 1) / I;
+    for (int64_t it = (int64_t)blockIdx.x * kQuadsPerBlock + (threadIdx.x >> 2); it < items;
+         it += (int64_t)gridDim.x * kQuadsPerBlock) {
+        const int64_t base = it * I;
+        float v[4 * R];
+        load_item<B>(xs, base, E, t, v);
+        const float sigma = fwht_item<B>(v, t);
+        const float rs = sigma * r;
+        uint32_t u[4 * R];
+        bool near = !fast_ok;
+#pragma unroll
+        for (int k = 0; k < 4 * R; ++k) {
+            const float tq = clamp127(v[k] * rs);
+            const float uf = tq + HATQ_MAGIC;
+            const float kf = uf - HATQ_MAGIC;
+            near |= fabsf(tq - kf) > HATQ_NEAR_TIE;
+            u[k] = __float_as_uint(uf);
+        }
+        if (near) {
+#pragma unroll
+            for (int k = 0; k < 4 * R; ++k) {
+                const float q = rintf(clamp127((sigma * v[k]) / s));
+                u[k] = __float_as_uint(q + HATQ_MAGIC);
+            }
+        }
+        const bool full = base + I <= E;
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const int64_t off = base + 16 * i + 4 * t;
+            if (full || off < E)
+                *reinterpret_cast<uint32_t *>(qs + off) =
+                    pack_low_bytes(u[4 * i], u[4 * i + 1], u[4 * i + 2], u[4 * i + 3]);
+        }
+    }
+}
+
+// Elementwise path for b <= 2 when E is not a multiple of 4 (float4 alignment
+// of every sample cannot be assumed).  Element pairs never straddle a pixel
+// because c % b == 0.
+template <int B, bool QUANT>
+__global__ void __launch_bounds__(kThreads) scalar_kernel(const float *__restrict__ x, int64_t E,
+                                                          float *__restrict__ absmax,
+                                                          int8_t *__restrict__ xq,
+                                                          float *__restrict__ act_scale) {
+    const int n = blockIdx.y;
+    const float *xs = x + (int64_t)n * E;
+    float s = 1.0f;
+    if constexpr (QUANT) {
+        s = act_scale_from_absmax(absmax[n]);
+        if (blockIdx.x == 0 && threadIdx.x == 0) act_scale[n] = s;
+    }
+    float m = 0.0f;
+    const int64_t groups = E / B;
+    for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < groups;
+         g += (int64_t)gridDim.x * kThreads) {
+        float v[B];
+#pragma unroll
+        for (int j = 0; j < B; ++j) v[j] = xs[g * B + j];
+        if constexpr (B == 2) {
+            const float a = v[0], c = v[1];
+            v[0] = a + c;
+            v[1] = a - c;
+        }
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            if constexpr (QUANT) xq[(int64_t)n * E + g * B + j] = (int8_t)(int)rintf(clamp127(v[j] / s));
+            else m = fmaxf(m, fabsf(v[j]));
+        }
+    }
+    if constexpr (!QUANT) {
+        m = wave_max(m);
+        if ((threadIdx.x & 63) == 0) atomic_max_nonneg(absmax + n, m);
+    }
+}
+
+int grid_x(int64_t work_units, int per_block, int n) {
+    int64_t want = (work_units + per_block - 1) / per_block;
+    int64_t cap = (2048 + n - 1) / n;   // about 8 blocks per CU over the whole batch
+    if (cap < 1) cap = 1;
+    if (want > cap) want = cap;
+    return (int)(want < 1 ? 1 : want);
+}
+
+template <int B>
+hipError_t launch_vector(const float *x, int n, int64_t E, const float *absmax_in, float *ws_absmax,
+                         int8_t *xq, float *act_scale, hipStream_t st) {
+    constexpr int I = ItemShape<B>::I;
+    const int64_t items = (E + I - 1) / I;
+    dim3 grid(grid_x(items, kQuadsPerBlock, n), n);
+    const float *A = absmax_in;
+    if (!A) {
+        fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(ws_absmax), n, 0u);
+        absmax_kernel<B><<<grid, kThreads, 0, st>>>(x, E, ws_absmax);
+        A = ws_absmax;
+    }
+    quant_kernel<B><<<grid, kThreads, 0, st>>>(x, E, A, xq, act_scale);
+    return hipGetLastError();
+}
+
+template <int B>
+hipError_t launch_scalar(const float *x, int n, int64_t E, const float *absmax_in, float *ws_absmax,
+                         int8_t *xq, float *act_scale, hipStream_t st) {
+    dim3 grid(grid_x(E / B, kThreads, n), n);
+    const float *A = absmax_in;
+    if (!A) {
+        fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(ws_absmax), n, 0u);
+        scalar_kernel<B, false><<<grid, kThreads, 0, st>>>(x, E, ws_absmax, nullptr, nullptr);
+        A = ws_absmax;
+    }
+    scalar_kernel<B, true><<<grid, kThreads, 0, st>>>(x, E, const_cast<float *>(A), xq, act_scale);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,
+                            float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st) {
+    if (E % 4 != 0) {
+        if (hblock == 1) return launch_scalar<1>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        return launch_scalar<2>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+    }
+    switch (hblock) {
+        case 1: return launch_vector<1>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        case 2: return launch_vector<2>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        case 4: return launch_vector<4>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        case 8: return launch_vector<8>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        case 16: return launch_vector<16>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        case 32: return launch_vector<32>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        case 64: return launch_vector<64>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        case 128: return launch_vector<128>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace hatq

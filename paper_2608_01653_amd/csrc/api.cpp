@@ -1,0 +1,336 @@
+// C-ABI entry points of libhatq: host-side validation and launch orchestration.
+// Every argument check runs before the first HIP call, so invalid calls launch
+// nothing, touch no output and need no GPU.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+
+#include "../../include/hatq.h"
+#include "hatq_launch.h"
+
+namespace {
+
+bool is_pow2(int v) { return v >= 1 && (v & (v - 1)) == 0; }
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+int32_t check_desc(const hatq_conv_desc *d, int32_t form) {
+    if (!d) return HATQ_EINVAL;
+    if (form != HATQ_DH && form != HATQ_WH) return HATQ_EINVAL;
+    if (d->cin <= 0 || d->cout <= 0 || d->k <= 0 || d->stride <= 0 || d->pad < 0 || d->out_pad < 0)
+        return HATQ_EINVAL;
+    if (!is_pow2(d->hblock) || d->hblock > 128) return HATQ_EINVAL;
+    if (d->transposed != 0 && d->transposed != 1) return HATQ_EINVAL;
+    if (d->transposed && d->out_pad >= d->stride) return HATQ_EINVAL;
+    return HATQ_OK;
+}
+
+struct Dims {
+    int32_t cin_p, cout_p, k_total, k_stride;
+};
+
+Dims dims_of(const hatq_conv_desc *d, int32_t form) {
+    Dims r;
+    r.cin_p = (int32_t)(form == HATQ_DH ? round_up(d->cin, d->hblock) : d->cin);
+    r.cout_p = (int32_t)(form == HATQ_WH ? round_up(d->cout, d->hblock) : d->cout);
+    r.k_total = d->k * d->k * r.cin_p;
+    r.k_stride = (int32_t)round_up(r.k_total, 64);
+    return r;
+}
+
+int32_t out_hw(const hatq_conv_desc *d, int32_t h, int32_t w, int32_t *ho, int32_t *wo) {
+    int64_t a, b;
+    if (d->transposed) {
+        a = (int64_t)(h - 1) * d->stride - 2 * d->pad + d->k + d->out_pad;
+        b = (int64_t)(w - 1) * d->stride - 2 * d->pad + d->k + d->out_pad;
+    } else {
+        if (h + 2 * d->pad < d->k || w + 2 * d->pad < d->k) return HATQ_EINVAL;
+        a = (h + 2 * d->pad - d->k) / d->stride + 1;
+        b = (w + 2 * d->pad - d->k) / d->stride + 1;
+    }
+    if (a <= 0 || b <= 0 || a > INT32_MAX || b > INT32_MAX) return HATQ_EINVAL;
+    *ho = (int32_t)a;
+    *wo = (int32_t)b;
+    return HATQ_OK;
+}
+
+int32_t hip_status(hipError_t e) { return e == hipSuccess ? HATQ_OK : HATQ_EHIP; }
+
+// Kernel geometry the conv kernels implement.
+int32_t check_conv_supported(const hatq_weights *W) {
+    const hatq_conv_desc &d = W->d;
+    const bool small = W->cin_pad <= 4 && W->k_total <= 128;
+    if (!small && W->cin_pad % 64 != 0) return HATQ_EUNSUPPORTED;
+    if (W->cout_pad % 64 != 0) return HATQ_EUNSUPPORTED;
+    if (d.k * d.k > hatq::kMaxTaps) return HATQ_EUNSUPPORTED;
+    if (d.transposed && (d.stride != 2 || small)) return HATQ_EUNSUPPORTED;
+    if (d.k > 64 || d.pad > 64 || d.stride > 64) return HATQ_EUNSUPPORTED;
+    // the WH restore runs inside one wave: the block must tile the wave's columns
+    const int tiles[] = {64, 128, 192, 256, 320};
+    bool fixed = false;
+    for (int t : tiles) fixed |= (W->cout_pad == t);
+    const int bn = fixed ? W->cout_pad : 64;
+    if (W->form == HATQ_WH && bn % W->d.hblock != 0) return HATQ_EUNSUPPORTED;
+    return HATQ_OK;
+}
+
+int32_t check_weights(const hatq_weights *W) {
+    if (!W) return HATQ_EINVAL;
+    if (check_desc(&W->d, W->form) != HATQ_OK) return HATQ_EINVAL;
+    const Dims dm = dims_of(&W->d, W->form);
+    if (dm.cin_p != W->cin_pad || dm.cout_p != W->cout_pad || dm.k_total != W->k_total ||
+        dm.k_stride != W->k_stride)
+        return HATQ_EINVAL;
+    if (!W->wq || !W->w_scale || !W->bias) return HATQ_EINVAL;
+    if (!aligned(W->wq, 16) || !aligned(W->w_scale, 4) || !aligned(W->bias, 4)) return HATQ_EINVAL;
+    return HATQ_OK;
+}
+
+int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next_absmax) {
+    if (!next_absmax) return HATQ_OK;
+    if (!is_pow2(next_hblock) || next_hblock > 128) return HATQ_EINVAL;
+    if (W->d.cout % next_hblock != 0) return HATQ_EUNSUPPORTED;
+    const int tiles[] = {64, 128, 192, 256, 320};
+    bool fixed = false;
+    for (int t : tiles) fixed |= (W->cout_pad == t);
+    const int bn = fixed ? W->cout_pad : 64;
+    if (bn % next_hblock != 0 && next_hblock > 1) return HATQ_EUNSUPPORTED;
+    if (!aligned(next_absmax, 4)) return HATQ_EINVAL;
+    return HATQ_OK;
+}
+
+// Fill the tap table of one GEMM launch.  Regular convolution: one launch over
+// the output grid, taps (kh, kw).  Transposed convolution with stride 2: one
+// launch per output phase (ph, pw) over the points (i, j) with
+// oh = 2i + ph; tap kh is used iff (oh + pad - kh) is even, and then reads input
+// row i + (ph + pad - kh)/2 (gather form of the transposed convolution).
+int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, int32_t n,
+                      int32_t h, int32_t w, int32_t mode, void *y, int32_t next_hblock,
+                      float *next_absmax, hipStream_t st) {
+    const hatq_conv_desc &d = W->d;
+    int32_t ho, wo;
+    if (out_hw(&d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
+    hatq::ConvArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.xq = xq;
+    a.wq = W->wq;
+    a.sx = sx;
+    a.w_scale = W->w_scale;
+    a.bias = W->bias;
+    a.y = y;
+    a.next_absmax = next_absmax;
+    a.n = n;
+    a.h = h;
+    a.w = w;
+    a.cin_p = W->cin_pad;
+    a.ho = ho;
+    a.wo = wo;
+    a.k_total = W->k_total;
+    a.k_stride = W->k_stride;
+    a.cout = d.cout;
+    a.cout_pad = W->cout_pad;
+    a.form = W->form;
+    a.mode = mode;
+    a.hblock = d.hblock;
+    a.next_hblock = next_absmax ? next_hblock : 0;
+    const bool small = W->cin_pad <= 4 && W->k_total <= 128;
+    if (!d.transposed) {
+        a.gh = ho;
+        a.gw = wo;
+        a.sa = d.stride;
+        a.bah = -d.pad;
+        a.baw = -d.pad;
+        a.so = 1;
+        a.boh = 0;
+        a.bow = 0;
+        a.ntaps = d.k * d.k;
+        for (int kh = 0; kh < d.k; ++kh)
+            for (int kw = 0; kw < d.k; ++kw) {
+                const int t = kh * d.k + kw;
+                a.dh[t] = (int8_t)kh;
+                a.dw[t] = (int8_t)kw;
+                a.wtap[t] = (int16_t)t;
+            }
+        a.nksteps = small ? (W->k_total + 63) / 64 : a.ntaps * (W->cin_pad / 64);
+        a.M = (int64_t)n * a.gh * a.gw;
+        return hip_status(hatq::launch_conv(a, true, st));
+    }
+    // transposed, stride 2: four phases
+    bool first = true;
+    for (int ph = 0; ph < 2; ++ph)
+        for (int pw = 0; pw < 2; ++pw) {
+            hatq::ConvArgs b = a;
+            b.gh = (ho - ph + 1) / 2;
+            b.gw = (wo - pw + 1) / 2;
+            if (b.gh <= 0 || b.gw <= 0) continue;
+            b.sa = 1;
+            b.bah = 0;
+            b.baw = 0;
+            b.so = 2;
+            b.boh = ph;
+            b.bow = pw;
+            int nt = 0;
+            for (int kh = 0; kh < d.k; ++kh) {
+                if (((ph + d.pad - kh) % 2 + 2) % 2) continue;
+                for (int kw = 0; kw < d.k; ++kw) {
+                    if (((pw + d.pad - kw) % 2 + 2) % 2) continue;
+                    b.dh[nt] = (int8_t)((ph + d.pad - kh) / 2);
+                    b.dw[nt] = (int8_t)((pw + d.pad - kw) / 2);
+                    b.wtap[nt] = (int16_t)(kh * d.k + kw);
+                    ++nt;
+                }
+            }
+            b.ntaps = nt;
+            b.nksteps = nt * (W->cin_pad / 64);
+            b.M = (int64_t)n * b.gh * b.gw;
+            if (nt == 0) continue;   // cannot happen for k >= 2
+            // next_absmax is cleared by the first phase and accumulated by the rest
+            if (hatq::launch_conv(b, first, st) != hipSuccess) return HATQ_EHIP;
+            first = false;
+        }
+    return HATQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *hatq_status_string(int32_t s) {
+    switch (s) {
+        case HATQ_OK: return "ok";
+        case HATQ_EINVAL: return "invalid argument";
+        case HATQ_EUNSUPPORTED: return "unsupported geometry";
+        case HATQ_EWORKSPACE: return "workspace too small";
+        case HATQ_EHIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+int32_t hatq_conv_out_hw(const hatq_conv_desc *d, int32_t h, int32_t w, int32_t *ho, int32_t *wo) {
+    if (!d || !ho || !wo || h <= 0 || w <= 0) return HATQ_EINVAL;
+    if (check_desc(d, HATQ_DH) != HATQ_OK) return HATQ_EINVAL;
+    return out_hw(d, h, w, ho, wo);
+}
+
+size_t hatq_weights_bytes(const hatq_conv_desc *d, int32_t form) {
+    if (check_desc(d, form) != HATQ_OK) return 0;
+    const Dims dm = dims_of(d, form);
+    return align256((size_t)dm.cout_p * dm.k_stride) + 2 * align256((size_t)dm.cout_p * 4);
+}
+
+int32_t hatq_prepare_weights(const hatq_conv_desc *d, int32_t form, const float *w, const float *bias,
+                             void *dst, size_t dst_bytes, hatq_weights *out, void *stream) {
+    if (check_desc(d, form) != HATQ_OK || !w || !dst || !out) return HATQ_EINVAL;
+    if (form == HATQ_DH && d->cin % d->hblock) return HATQ_EUNSUPPORTED;
+    if (form == HATQ_WH && d->cout % d->hblock) return HATQ_EUNSUPPORTED;
+    if (!aligned(dst, 256) || !aligned(w, 4) || (bias && !aligned(bias, 4))) return HATQ_EINVAL;
+    const size_t need = hatq_weights_bytes(d, form);
+    if (dst_bytes < need) return HATQ_EWORKSPACE;
+    const Dims dm = dims_of(d, form);
+    hatq_weights W;
+    W.d = *d;
+    W.form = form;
+    W.cin_pad = dm.cin_p;
+    W.cout_pad = dm.cout_p;
+    W.k_total = dm.k_total;
+    W.k_stride = dm.k_stride;
+    int8_t *base = static_cast<int8_t *>(dst);
+    W.wq = base;
+    W.w_scale = reinterpret_cast<float *>(base + align256((size_t)dm.cout_p * dm.k_stride));
+    W.bias = reinterpret_cast<float *>(reinterpret_cast<int8_t *>(W.w_scale) + align256((size_t)dm.cout_p * 4));
+    hatq::PrepArgs a;
+    a.w = w;
+    a.bias = bias;
+    a.wq = W.wq;
+    a.w_scale = W.w_scale;
+    a.w_bias = W.bias;
+    a.cin = d->cin;
+    a.cout = d->cout;
+    a.k = d->k;
+    a.transposed = d->transposed;
+    a.hblock = d->hblock;
+    a.form = form;
+    a.cin_p = dm.cin_p;
+    a.cout_p = dm.cout_p;
+    a.k_total = dm.k_total;
+    a.k_stride = dm.k_stride;
+    const int32_t st = hip_status(hatq::launch_prepare(a, static_cast<hipStream_t>(stream)));
+    if (st == HATQ_OK) *out = W;
+    return st;
+}
+
+size_t hatq_fwht_quant_ws_bytes(int32_t n) { return n > 0 ? align256((size_t)n * 4) : 0; }
+
+int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
+                            const float *absmax, int8_t *xq, float *act_scale, void *ws, size_t ws_bytes,
+                            void *stream) {
+    if (!x || !xq || !act_scale || n <= 0 || h <= 0 || w <= 0 || c <= 0) return HATQ_EINVAL;
+    if (!is_pow2(hblock) || hblock > 128) return HATQ_EINVAL;
+    if (c % hblock) return HATQ_EUNSUPPORTED;
+    if (!aligned(x, 16) || !aligned(xq, 4) || !aligned(act_scale, 4)) return HATQ_EINVAL;
+    if (absmax && !aligned(absmax, 4)) return HATQ_EINVAL;
+    if (!absmax) {
+        if (!ws) return HATQ_EINVAL;
+        if (ws_bytes < hatq_fwht_quant_ws_bytes(n) || !aligned(ws, 4)) return HATQ_EWORKSPACE;
+    }
+    const int64_t E = (int64_t)h * w * c;
+    return hip_status(hatq::launch_act_quant(x, n, E, hblock, absmax, static_cast<float *>(ws), xq,
+                                             act_scale, static_cast<hipStream_t>(stream)));
+}
+
+int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act_scale, int32_t n, int32_t h,
+                       int32_t w, int32_t out_mode, void *y, int32_t next_hblock, float *next_absmax,
+                       void *stream) {
+    int32_t s = check_weights(W);
+    if (s != HATQ_OK) return s;
+    if (!xq || !act_scale || !y || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
+    if (out_mode != HATQ_OUT_I32 && out_mode != HATQ_OUT_F32) return HATQ_EINVAL;
+    if (out_mode == HATQ_OUT_I32 && next_absmax) return HATQ_EINVAL;
+    if (!aligned(xq, 16) || !aligned(y, 4) || !aligned(act_scale, 4)) return HATQ_EINVAL;
+    if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    if ((s = check_next(W, next_hblock, next_absmax)) != HATQ_OK) return s;
+    int32_t ho, wo;
+    if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
+    return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, next_hblock, next_absmax,
+                         static_cast<hipStream_t>(stream));
+}
+
+size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w) {
+    if (check_weights(W) != HATQ_OK || n <= 0 || h <= 0 || w <= 0) return 0;
+    const size_t codes = (size_t)n * h * w * W->cin_pad;
+    return align256(codes) + align256((size_t)n * 4) + hatq_fwht_quant_ws_bytes(n);
+}
+
+int32_t hatq_layer_forward(const hatq_weights *W, int32_t form, const float *x, int32_t n, int32_t h, int32_t w,
+                           const float *x_absmax, float *y, float *act_scale, int32_t next_hblock,
+                           float *next_absmax, void *ws, size_t ws_bytes, void *stream) {
+    int32_t s = check_weights(W);
+    if (s != HATQ_OK) return s;
+    if (form != W->form) return HATQ_EINVAL;
+    if (!x || !y || !ws || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
+    if (!aligned(x, 16) || !aligned(y, 4) || !aligned(ws, 256)) return HATQ_EINVAL;
+    if (act_scale && !aligned(act_scale, 4)) return HATQ_EINVAL;
+    if (x_absmax && !aligned(x_absmax, 4)) return HATQ_EINVAL;
+    if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    if ((s = check_next(W, next_hblock, next_absmax)) != HATQ_OK) return s;
+    const int hb_act = form == HATQ_DH ? W->d.hblock : 1;
+    if (W->cin_pad != W->d.cin) return HATQ_EUNSUPPORTED;   // activation padding not supported
+    if (W->d.cin % hb_act) return HATQ_EUNSUPPORTED;
+    int32_t ho, wo;
+    if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
+    const size_t need = hatq_layer_ws_bytes(W, n, h, w);
+    if (ws_bytes < need) return HATQ_EWORKSPACE;
+    int8_t *xq = static_cast<int8_t *>(ws);
+    float *ws_sx = reinterpret_cast<float *>(xq + align256((size_t)n * h * w * W->cin_pad));
+    float *amax = reinterpret_cast<float *>(reinterpret_cast<int8_t *>(ws_sx) + align256((size_t)n * 4));
+    float *sx = act_scale ? act_scale : ws_sx;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int64_t E = (int64_t)h * w * W->d.cin;
+    if (hatq::launch_act_quant(x, n, E, hb_act, x_absmax, amax, xq, sx, st) != hipSuccess) return HATQ_EHIP;
+    return conv_launches(W, xq, sx, n, h, w, HATQ_OUT_F32, y, next_hblock, next_absmax, st);
+}
+
+}  // extern "C"

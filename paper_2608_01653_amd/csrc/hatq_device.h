@@ -1,0 +1,119 @@
+// Device-side helpers shared by the HatQ HIP kernels (gfx950 only).
+//
+// Fast Walsh-Hadamard butterflies.  The unnormalized Sylvester transform of
+// order b = 2^L (Supplementary S-I, butterfly structure) is computed as L radix-2
+// stages in ascending bit order: stage k pairs channel i with i ^ (1 << k) and
+// maps (a, c) -> (a + c, a - c).  Every kernel that transforms the same data uses
+// this order, so their fp32 results are bit-identical.
+//
+// Stages whose bit lies in the lane index use DPP lane moves and one FMA with a
+// per-lane +/-1 coefficient instead of an add and a subtract.  The lane with the
+// bit clear computes v + p, the lane with the bit set computes v - p = -(p - v):
+// both are single correctly rounded operations, and the second carries a known
+// sign flip.  The flips are tracked as a per-lane sign sigma = (-1)^(number of
+// cross-lane stages in which the lane had its bit set) and removed at the end
+// (or ignored where only |value| matters).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hatq {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// ---- DPP lane exchanges inside a 16-lane row ---------------------------------
+// quad_perm [1,0,3,2]
+__device__ __forceinline__ float lane_xor1(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, true));
+}
+// quad_perm [2,3,0,1]
+__device__ __forceinline__ float lane_xor2(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, true));
+}
+// row_half_mirror (i -> 7-i inside 8 lanes) then quad_perm [3,2,1,0] (i -> i^3):
+// 7 - (i ^ 3) = i ^ 4 for i in 0..7.
+__device__ __forceinline__ float lane_xor4(float v) {
+    int m = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x141, 0xF, 0xF, true);
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(m, 0x1B, 0xF, 0xF, true));
+}
+// row_ror:8 (i -> (i + 8) mod 16)
+__device__ __forceinline__ float lane_xor8(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x128, 0xF, 0xF, true));
+}
+
+template <int MASK>
+__device__ __forceinline__ float lane_xor(float v) {
+    static_assert(MASK == 1 || MASK == 2 || MASK == 4 || MASK == 8, "lane mask");
+    if constexpr (MASK == 1) return lane_xor1(v);
+    else if constexpr (MASK == 2) return lane_xor2(v);
+    else if constexpr (MASK == 4) return lane_xor4(v);
+    else return lane_xor8(v);
+}
+
+// One cross-lane butterfly stage on R registers: partner lane = lane ^ MASK.
+// coef = -1 on lanes with the bit set, +1 otherwise.
+template <int MASK, int R>
+__device__ __forceinline__ void cross_stage(float (&v)[R], float coef) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) v[r] = __builtin_fmaf(coef, lane_xor<MASK>(v[r]), v[r]);
+}
+
+// One in-register butterfly stage on registers whose index bit STRIDE differs.
+template <int STRIDE, int R>
+__device__ __forceinline__ void reg_stage(float (&v)[R]) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        if (r & STRIDE) continue;
+        const float a = v[r], c = v[r + STRIDE];
+        v[r] = a + c;
+        v[r + STRIDE] = a - c;
+    }
+}
+
+// ---- symmetric INT8 quantizer -----------------------------------------------
+// s = fl32(A / 127), or 1 for A == 0 (IEEE division; HIP's default float
+// division on gfx950 is correctly rounded).
+__device__ __forceinline__ float act_scale_from_absmax(float A) {
+    return A > 0.0f ? A / 127.0f : 1.0f;
+}
+
+// Magic constant 1.5 * 2^23: for |t| < 2^22, t + MAGIC rounds t to the nearest
+// integer with ties to even (the hardware's default rounding of the add) and the
+// low bits of the sum's encoding are that integer in two's complement.
+#define HATQ_MAGIC 12582912.0f
+
+// Exactness of the fast path: with r = fl(1/s), t = fl(v * r) differs from the
+// correctly rounded quotient fl(v / s) by at most |v/s| * (3 * 2^-24 + 2^-48)
+// <= 2.3e-5 for |v/s| <= 128, s a normal number.  When t lies farther than
+// 0.5 - 2^-14 from the nearest integer k, fl(v / s) lies strictly inside
+// (k - 1/2, k + 1/2) and rne(fl(v / s)) = k.  Elements closer to a half-integer
+// take the exact path, an IEEE division.
+#define HATQ_NEAR_TIE (0.5f - 0x1p-14f)
+
+// Clamp to [-127, 127].
+__device__ __forceinline__ float clamp127(float t) { return __builtin_amdgcn_fmed3f(t, -127.0f, 127.0f); }
+
+// Pack the low bytes of four 32-bit words into one word (byte 0 from a).
+__device__ __forceinline__ uint32_t pack_low_bytes(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+    const uint32_t lo = __builtin_amdgcn_perm(b, a, 0x0C0C0400u);   // [a0, b0, 0, 0]
+    const uint32_t hi = __builtin_amdgcn_perm(d, c, 0x0C0C0400u);   // [c0, d0, 0, 0]
+    return __builtin_amdgcn_perm(hi, lo, 0x05040100u);               // [a0, b0, c0, d0]
+}
+
+// Order-preserving float max for non-negative values through 32-bit atomics.
+__device__ __forceinline__ void atomic_max_nonneg(float *addr, float v) {
+    atomicMax(reinterpret_cast<unsigned int *>(addr), __float_as_uint(v));
+}
+
+__device__ __forceinline__ float wave_max(float m) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    return m;
+}
+
+// Fill n 32-bit words with a value (used instead of hipMemsetAsync so the
+// sequence stays graph-capture friendly).
+__global__ void fill_u32_kernel(uint32_t *p, int n, uint32_t v);
+
+}  // namespace hatq

@@ -1,0 +1,61 @@
+// Internal launchers of the HatQ kernels (host side, gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hatq {
+
+// Activation transform + quantization of n samples of E floats each.
+// absmax_in == nullptr: two passes through ws_absmax (n floats of scratch).
+hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,
+                            float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st);
+
+constexpr int kMaxTaps = 32;
+
+// Geometry and operands of one implicit-GEMM launch.  GEMM rows are the points
+// (nb, gi, gj) of an n x gh x gw grid.  Input anchor of a point:
+// (gi*sa + bah, gj*sa + baw); tap t reads the input pixel anchor + (dh[t], dw[t])
+// with weight tap wtap[t] (kh*k + kw).  Output pixel: (gi*so + boh, gj*so + bow).
+struct ConvArgs {
+    const int8_t *xq;
+    const int8_t *wq;
+    const float *sx;
+    const float *w_scale;
+    const float *bias;
+    void *y;
+    float *next_absmax;
+    int64_t M;             // n * gh * gw
+    int32_t n, h, w, cin_p;
+    int32_t gh, gw;
+    int32_t sa, bah, baw;
+    int32_t ho, wo, so, boh, bow;
+    int32_t ntaps, nksteps;
+    int32_t k_total, k_stride;
+    int32_t cout, cout_pad;
+    int32_t form;          // 0 DH, 1 WH
+    int32_t mode;          // 0 I32, 1 F32
+    int32_t hblock;        // the layer's block size
+    int32_t next_hblock;   // 0 = no next-operand absmax
+    int32_t tiles_m, tiles_n;
+    int8_t dh[kMaxTaps], dw[kMaxTaps];
+    int16_t wtap[kMaxTaps];
+};
+
+// clear_next: zero next_absmax before the launch (false to keep accumulating
+// across the phase launches of one transposed convolution).
+hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st);
+
+// Weight preparation: transform, per-channel scale, codes, bias.
+struct PrepArgs {
+    const float *w;        // PyTorch layout
+    const float *bias;     // may be null
+    int8_t *wq;
+    float *w_scale;
+    float *w_bias;
+    int32_t cin, cout, k, transposed, hblock, form;
+    int32_t cin_p, cout_p, k_total, k_stride;
+};
+hipError_t launch_prepare(const PrepArgs &a, hipStream_t st);
+
+}  // namespace hatq

@@ -1,0 +1,87 @@
+// Offline weight preparation on the device (step a1).
+//
+// DH (Eq. hadamard_linear_equivalence, Eq. supp_padded_dh): every (co, tap) row
+// of the contraction is multiplied by B_Cin = I (x) H~_b.  WH (Eq.
+// weight_only_hadamard_equivalence, Eq. supp_padded_wh_parameters): every (tap, ci)
+// column is multiplied by B_Cout, and the bias becomes b~ = B_Cout [b; 0].
+// Each transformed value is an fp64 sum over j = 0..b-1 in ascending order of
+// (-1)^popcount(i & j) * w_j (products with +-1 are exact), rounded once to fp32.
+// Then per output channel s_w = fl32(max|W'| / 127) (1 if the row is zero) and
+// q = clamp(rne(fl32(W' / s_w)), -127, 127) with IEEE fp32 division
+// (Eq. symmetric_q, per-output-channel weights).
+#include "hatq_device.h"
+#include "hatq_launch.h"
+
+namespace hatq {
+namespace {
+
+constexpr int kThreads = 256;
+
+// Original weight W0[co][kh][kw][ci] read from the PyTorch layout, 0 outside.
+__device__ __forceinline__ double w_orig(const PrepArgs &a, int co, int tap, int ci) {
+    if (co >= a.cout || ci >= a.cin) return 0.0;
+    const int kh = tap / a.k, kw = tap - kh * a.k;
+    const int64_t idx = a.transposed ? (((int64_t)ci * a.cout + co) * a.k + kh) * a.k + kw
+                                     : (((int64_t)co * a.cin + ci) * a.k + kh) * a.k + kw;
+    return (double)a.w[idx];
+}
+
+__device__ __forceinline__ double hsign(int i, int j) { return (__popc(i & j) & 1) ? -1.0 : 1.0; }
+
+// Transformed weight W'[co][d], d = tap*cin_p + ci.
+__device__ float w_prime(const PrepArgs &a, int co, int d) {
+    const int tap = d / a.cin_p, ci = d - tap * a.cin_p;
+    const int b = a.hblock;
+    double acc = 0.0;
+    if (a.form == 0) {
+        const int blk = ci / b * b, i = ci - blk;
+        for (int j = 0; j < b; ++j) acc += hsign(i, j) * w_orig(a, co, tap, blk + j);
+    } else {
+        const int blk = co / b * b, i = co - blk;
+        for (int j = 0; j < b; ++j) acc += hsign(i, j) * w_orig(a, blk + j, tap, ci);
+    }
+    return (float)acc;
+}
+
+__global__ void __launch_bounds__(kThreads) prepare_kernel(const PrepArgs a) {
+    const int co = blockIdx.x;
+    float m = 0.0f;
+    for (int d = threadIdx.x; d < a.k_total; d += kThreads) m = fmaxf(m, fabsf(w_prime(a, co, d)));
+    m = wave_max(m);
+    __shared__ float red[kThreads / 64];
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    float A = red[0];
+#pragma unroll
+    for (int k = 1; k < kThreads / 64; ++k) A = fmaxf(A, red[k]);
+    const float s = A > 0.0f ? A / 127.0f : 1.0f;
+    int8_t *row = a.wq + (int64_t)co * a.k_stride;
+    for (int d = threadIdx.x; d < a.k_stride; d += kThreads) {
+        int8_t q = 0;
+        if (d < a.k_total) q = (int8_t)(int)rintf(clamp127(w_prime(a, co, d) / s));
+        row[d] = q;
+    }
+    if (threadIdx.x == 0) {
+        a.w_scale[co] = s;
+        double bv = 0.0;
+        if (a.bias) {
+            if (a.form == 0) {
+                bv = co < a.cout ? (double)a.bias[co] : 0.0;
+            } else {
+                const int b = a.hblock, blk = co / b * b, i = co - blk;
+                for (int j = 0; j < b; ++j)
+                    bv += hsign(i, j) * (blk + j < a.cout ? (double)a.bias[blk + j] : 0.0);
+            }
+        }
+        a.w_bias[co] = (float)bv;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_prepare(const PrepArgs &a, hipStream_t st) {
+    prepare_kernel<<<a.cout_p, kThreads, 0, st>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace hatq

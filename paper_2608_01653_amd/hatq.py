@@ -1,0 +1,227 @@
+"""Thin Python binding of libhatq (ctypes).
+
+Argument marshalling only: every step of the operator runs in the library's HIP
+kernels.  PyTorch supplies device memory (tensors passed by ``data_ptr()``) and
+the stream (``torch.cuda.current_stream()``).  There is no fallback: if the
+library is missing or cannot be loaded, every call raises.
+
+The function names mirror the C ABI in ``include/hatq.h``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+import torch
+
+from . import build as _build
+
+HATQ_OK, HATQ_EINVAL, HATQ_EUNSUPPORTED, HATQ_EWORKSPACE, HATQ_EHIP = range(5)
+HATQ_DH, HATQ_WH = 0, 1
+HATQ_OUT_I32, HATQ_OUT_F32 = 0, 1
+FORMS = {"DH": HATQ_DH, "WH": HATQ_WH}
+
+
+class HatqError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [("cin", ctypes.c_int32), ("cout", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("stride", ctypes.c_int32), ("pad", ctypes.c_int32), ("out_pad", ctypes.c_int32),
+                ("transposed", ctypes.c_int32), ("hblock", ctypes.c_int32)]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [("d", ConvDesc), ("form", ctypes.c_int32), ("cin_pad", ctypes.c_int32),
+                ("cout_pad", ctypes.c_int32), ("k_total", ctypes.c_int32),
+                ("k_stride", ctypes.c_int32), ("wq", ctypes.c_void_p),
+                ("w_scale", ctypes.c_void_p), ("bias", ctypes.c_void_p)]
+
+
+EXPORTS = ["hatq_status_string", "hatq_conv_out_hw", "hatq_weights_bytes", "hatq_prepare_weights",
+           "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act", "hatq_conv_int8",
+           "hatq_layer_ws_bytes", "hatq_layer_forward"]
+
+_lib = None
+
+
+def lib_path() -> str:
+    return _build.LIB
+
+
+def load(build_if_missing: bool = False):
+    """Load libhatq.so; raise if it is absent (no silent fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = lib_path()
+    if not os.path.exists(path):
+        if not build_if_missing:
+            raise RuntimeError(f"libhatq.so not built ({path}); run __graft_entry__.build()")
+        _build.build()
+    L = ctypes.CDLL(path)
+    P, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    L.hatq_status_string.argtypes = [i32]
+    L.hatq_status_string.restype = ctypes.c_char_p
+    L.hatq_conv_out_hw.argtypes = [ctypes.POINTER(ConvDesc), i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    L.hatq_conv_out_hw.restype = i32
+    L.hatq_weights_bytes.argtypes = [ctypes.POINTER(ConvDesc), i32]
+    L.hatq_weights_bytes.restype = sz
+    L.hatq_prepare_weights.argtypes = [ctypes.POINTER(ConvDesc), i32, P, P, P, sz, ctypes.POINTER(Weights), P]
+    L.hatq_prepare_weights.restype = i32
+    L.hatq_fwht_quant_ws_bytes.argtypes = [i32]
+    L.hatq_fwht_quant_ws_bytes.restype = sz
+    L.hatq_fwht_quant_act.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P, sz, P]
+    L.hatq_fwht_quant_act.restype = i32
+    L.hatq_conv_int8.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, i32, P, P]
+    L.hatq_conv_int8.restype = i32
+    L.hatq_layer_ws_bytes.argtypes = [ctypes.POINTER(Weights), i32, i32, i32]
+    L.hatq_layer_ws_bytes.restype = sz
+    L.hatq_layer_forward.argtypes = [ctypes.POINTER(Weights), i32, P, i32, i32, i32, P, P, P, i32, P, P,
+                                     sz, P]
+    L.hatq_layer_forward.restype = i32
+    _lib = L
+    return L
+
+
+def status_string(s: int) -> str:
+    return load().hatq_status_string(int(s)).decode()
+
+
+def _check(status: int, where: str):
+    if status != HATQ_OK:
+        raise HatqError(status, where)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("device tensor expected")
+    if not t.is_contiguous():
+        raise ValueError("contiguous tensor expected")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def desc(cin, cout, k, stride, pad, hblock, transposed=False, out_pad=0) -> ConvDesc:
+    return ConvDesc(int(cin), int(cout), int(k), int(stride), int(pad), int(out_pad),
+                    int(bool(transposed)), int(hblock))
+
+
+def hatq_conv_out_hw(d: ConvDesc, h: int, w: int) -> Tuple[int, int]:
+    ho, wo = ctypes.c_int32(), ctypes.c_int32()
+    _check(load().hatq_conv_out_hw(ctypes.byref(d), h, w, ctypes.byref(ho), ctypes.byref(wo)),
+           "hatq_conv_out_hw")
+    return ho.value, wo.value
+
+
+def hatq_weights_bytes(d: ConvDesc, form) -> int:
+    return int(load().hatq_weights_bytes(ctypes.byref(d), FORMS.get(form, form)))
+
+
+@dataclass
+class PreparedLayer:
+    """Prepared weights of one layer: the device buffer and the C view into it."""
+    buf: torch.Tensor
+    w: Weights
+    form: int
+
+    @property
+    def cout_pad(self) -> int:
+        return self.w.cout_pad
+
+    @property
+    def cin_pad(self) -> int:
+        return self.w.cin_pad
+
+    @property
+    def k_stride(self) -> int:
+        return self.w.k_stride
+
+    def wq(self) -> torch.Tensor:
+        """int8 [cout_pad, k_stride] view of the packed codes."""
+        n = self.w.cout_pad * self.w.k_stride
+        return self.buf[:n].view(self.w.cout_pad, self.w.k_stride)
+
+    def w_scale(self) -> torch.Tensor:
+        off = self.w.w_scale - self.buf.data_ptr()
+        return self.buf[off:off + 4 * self.w.cout_pad].view(torch.float32)
+
+    def bias(self) -> torch.Tensor:
+        off = self.w.bias - self.buf.data_ptr()
+        return self.buf[off:off + 4 * self.w.cout_pad].view(torch.float32)
+
+
+def hatq_prepare_weights(d: ConvDesc, form, w: torch.Tensor, bias: Optional[torch.Tensor] = None,
+                         stream=None) -> PreparedLayer:
+    f = FORMS.get(form, form)
+    nbytes = hatq_weights_bytes(d, f)
+    if nbytes == 0:
+        raise HatqError(HATQ_EINVAL, "hatq_weights_bytes")
+    buf = torch.zeros(nbytes, dtype=torch.int8, device=w.device)
+    out = Weights()
+    w = w.contiguous().float()
+    b = None if bias is None else bias.contiguous().float()
+    _check(load().hatq_prepare_weights(ctypes.byref(d), f, _ptr(w), _ptr(b), _ptr(buf), nbytes,
+                                       ctypes.byref(out), _stream(stream)), "hatq_prepare_weights")
+    return PreparedLayer(buf, out, f)
+
+
+def hatq_fwht_quant_act(x: torch.Tensor, hblock: int, absmax: Optional[torch.Tensor] = None,
+                        stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """x fp32 NHWC -> (int8 codes NHWC, per-sample scale fp32 [n])."""
+    n, h, w, c = x.shape
+    xq = torch.empty((n, h, w, c), dtype=torch.int8, device=x.device)
+    sc = torch.empty(n, dtype=torch.float32, device=x.device)
+    wsb = int(load().hatq_fwht_quant_ws_bytes(n))
+    ws = torch.empty(max(wsb, 4), dtype=torch.int8, device=x.device)
+    _check(load().hatq_fwht_quant_act(_ptr(x), n, h, w, c, int(hblock), _ptr(absmax), _ptr(xq), _ptr(sc),
+                                      _ptr(ws), wsb, _stream(stream)), "hatq_fwht_quant_act")
+    return xq, sc
+
+
+def hatq_conv_int8(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tensor, out_mode=HATQ_OUT_F32,
+                   next_hblock: int = 0, next_absmax: Optional[torch.Tensor] = None, y=None, stream=None):
+    n, h, w, _ = xq.shape
+    ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
+    if y is None:
+        if out_mode == HATQ_OUT_I32:
+            y = torch.empty((n, ho, wo, layer.w.cout_pad), dtype=torch.int32, device=xq.device)
+        else:
+            y = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.float32, device=xq.device)
+    _check(load().hatq_conv_int8(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), n, h, w, int(out_mode),
+                                 _ptr(y), int(next_hblock), _ptr(next_absmax), _stream(stream)),
+           "hatq_conv_int8")
+    return y
+
+
+def hatq_layer_ws_bytes(layer: PreparedLayer, n: int, h: int, w: int) -> int:
+    return int(load().hatq_layer_ws_bytes(ctypes.byref(layer.w), n, h, w))
+
+
+def hatq_layer_forward(layer: PreparedLayer, form, x: torch.Tensor, x_absmax: Optional[torch.Tensor] = None,
+                       next_hblock: int = 0, next_absmax: Optional[torch.Tensor] = None,
+                       act_scale: Optional[torch.Tensor] = None, y: Optional[torch.Tensor] = None,
+                       ws: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    n, h, w, _ = x.shape
+    ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
+    if y is None:
+        y = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.float32, device=x.device)
+    need = hatq_layer_ws_bytes(layer, n, h, w)
+    if ws is None:
+        ws = torch.empty(max(need, 256), dtype=torch.int8, device=x.device)
+    _check(load().hatq_layer_forward(ctypes.byref(layer.w), FORMS.get(form, form), _ptr(x), n, h, w,
+                                     _ptr(x_absmax), _ptr(y), _ptr(act_scale), int(next_hblock),
+                                     _ptr(next_absmax), _ptr(ws), ws.numel(), _stream(stream)),
+           "hatq_layer_forward")
+    return y

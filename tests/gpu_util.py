@@ -1,0 +1,66 @@
+"""Helpers for the GPU parity tests: device transfer and the parity rules.
+
+Parity bar (fixed by the target specification of this operator):
+  * INT8 codes: bit-exact when both sides see identical fp32 transform outputs
+    (inputs whose transform is exact in fp32, or no transform); otherwise at most
+    1 LSB apart on at most 1e-4 of the elements.
+  * INT32 accumulators: bit-exact.
+  * Dequantized fp32 outputs: max |diff| <= 1e-6 * max |reference| per tensor
+    (range-relative; per-element relative error is undefined near zero).
+Data only flows oracle -> GPU (the GPU stage may consume the oracle's
+intermediates), never GPU -> oracle.
+"""
+import numpy as np
+import torch
+
+DEV = "cuda:0"
+CODE_FLIP_FRACTION = 1e-4
+FP32_RANGE_REL = 1e-6
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def assert_codes(q_gpu, q_ref, exact=False, what="codes"):
+    d = np.abs(q_gpu.astype(np.int32) - q_ref.astype(np.int32))
+    if exact:
+        assert d.max() == 0, f"{what}: {np.count_nonzero(d)} of {d.size} differ (max {d.max()})"
+    else:
+        frac = np.count_nonzero(d) / d.size
+        assert d.max() <= 1 and frac <= CODE_FLIP_FRACTION, \
+            f"{what}: max diff {d.max()}, fraction {frac:.3g}"
+    assert np.abs(q_gpu.astype(np.int32)).max() <= 127
+
+
+def assert_range_rel(y, ref, tol=FP32_RANGE_REL, what="y"):
+    scale = float(np.abs(ref).max())
+    err = float(np.abs(y.astype(np.float64) - ref.astype(np.float64)).max())
+    assert err <= tol * scale, f"{what}: max err {err:.3g} vs tol {tol * scale:.3g}"
+
+
+def assert_scale_ulp(s_gpu, s_ref, ulps=1):
+    a = s_gpu.astype(np.float32).view(np.int32).astype(np.int64)
+    b = s_ref.astype(np.float32).view(np.int32).astype(np.int64)
+    assert np.abs(a - b).max() <= ulps, (s_gpu, s_ref)
+
+
+def set_codes(layer, wq_ohwi):
+    """Overwrite a prepared layer's codes with given OHWI codes (zero K padding)."""
+    cout_p, ks = layer.w.cout_pad, layer.w.k_stride
+    kt = layer.w.k_total
+    buf = np.zeros((cout_p, ks), np.int8)
+    buf[:, :kt] = wq_ohwi.reshape(cout_p, kt)
+    layer.wq().copy_(dev(buf))
+
+
+def unpack_codes(layer, k, cin_p):
+    w = host(layer.wq())
+    kt = layer.w.k_total
+    assert not w[:, kt:].any(), "K padding must be zero"
+    return w[:, :kt].reshape(layer.w.cout_pad, k, k, cin_p)

@@ -1,0 +1,136 @@
+"""CPU-side checks of the C ABI: the library loads, exports every symbol the
+header declares, and rejects bad arguments on the host before any launch (so
+these run without a GPU; the pointers below are never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_01653_amd import hatq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = ctypes.c_void_p(0x10000)   # aligned, never dereferenced: validation fails first
+
+# These calls pass fake device pointers that validation must reject.  Never run
+# them where a GPU is visible: a validation bug would then launch on garbage.
+try:
+    import torch
+    _HAS_GPU = torch.cuda.device_count() > 0
+except Exception:  # pragma: no cover
+    _HAS_GPU = False
+pytestmark = pytest.mark.skipif(_HAS_GPU, reason="fake-pointer validation tests run on CPU-only hosts")
+
+
+@pytest.fixture(scope="module")
+def L():
+    return hatq.load(build_if_missing=True)
+
+
+def declared_symbols():
+    txt = open(os.path.join(ROOT, "include", "hatq.h")).read()
+    return sorted(set(re.findall(r"^\S.*?\b(hatq_\w+)\s*\(", txt, re.M)))
+
+
+def test_exports_every_declared_symbol(L):
+    syms = declared_symbols()
+    assert len(syms) >= 9
+    for s in syms:
+        assert hasattr(L, s), s
+    assert set(syms) == set(hatq.EXPORTS)
+
+
+def test_status_strings(L):
+    for s in range(5):
+        assert hatq.status_string(s)
+    assert hatq.status_string(99) == "unknown status"
+
+
+@pytest.mark.parametrize("args,exp", [
+    ((192, 192, 5, 2, 2, 64), (128, 128)),
+    ((128, 128, 1, 1, 0, 128), (64, 64)),
+    ((3, 192, 5, 2, 2, 64), (128, 128)),
+])
+def test_out_hw(L, args, exp):
+    assert hatq.hatq_conv_out_hw(hatq.desc(*args), 256 if args[3] == 2 else 64,
+                                 256 if args[3] == 2 else 64) == exp
+
+
+def test_out_hw_transposed(orc):
+    d = hatq.desc(192, 192, 5, 2, 2, 64, transposed=True, out_pad=1)
+    assert hatq.hatq_conv_out_hw(d, 64, 96) == (orc.out_size(64, 5, 2, 2, True, 1),
+                                                orc.out_size(96, 5, 2, 2, True, 1)) == (128, 192)
+
+
+def test_weights_bytes(L):
+    assert hatq.hatq_weights_bytes(hatq.desc(192, 192, 5, 2, 2, 64), "DH") >= 192 * 4800 + 2 * 192 * 4
+    assert hatq.hatq_weights_bytes(hatq.desc(3, 192, 5, 2, 2, 64), "WH") >= 192 * 128
+    assert hatq.hatq_weights_bytes(hatq.desc(192, 192, 5, 2, 2, 48), "DH") == 0    # not a power of two
+    assert hatq.hatq_weights_bytes(hatq.desc(192, 192, 5, 2, 2, 256), "DH") == 0   # above 128
+    assert hatq.hatq_weights_bytes(hatq.desc(192, 192, 5, 2, 2, 64), 7) == 0
+
+
+def test_prepare_rejects_before_launch(L):
+    out = hatq.Weights()
+    d = hatq.desc(192, 192, 5, 2, 2, 64)
+    f = L.hatq_prepare_weights
+    assert f(ctypes.byref(d), 0, None, None, FAKE, 1 << 30, ctypes.byref(out), None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(d), 0, FAKE, None, FAKE, 16, ctypes.byref(out), None) == hatq.HATQ_EWORKSPACE
+    d2 = hatq.desc(96, 192, 5, 2, 2, 64)       # DH needs cin % hblock == 0
+    assert f(ctypes.byref(d2), 0, FAKE, None, FAKE, 1 << 30, ctypes.byref(out), None) == hatq.HATQ_EUNSUPPORTED
+    d3 = hatq.desc(192, 96, 5, 2, 2, 64)       # WH needs cout % hblock == 0
+    assert f(ctypes.byref(d3), 1, FAKE, None, FAKE, 1 << 30, ctypes.byref(out), None) == hatq.HATQ_EUNSUPPORTED
+    assert f(ctypes.byref(d), 0, FAKE, None, ctypes.c_void_p(0x10010), 1 << 30, ctypes.byref(out),
+             None) == hatq.HATQ_EINVAL    # dst not 256-aligned
+
+
+def test_fwht_quant_rejects_before_launch(L):
+    f = L.hatq_fwht_quant_act
+    assert f(None, 1, 4, 4, 64, 64, None, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 1, 4, 4, 64, 48, None, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 1, 4, 4, 96, 64, None, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EUNSUPPORTED
+    assert f(FAKE, 2, 4, 4, 64, 64, None, FAKE, FAKE, FAKE, 0, None) == hatq.HATQ_EWORKSPACE
+    assert f(FAKE, 2, 4, 4, 64, 64, None, FAKE, FAKE, None, 0, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.c_void_p(0x10004), 1, 4, 4, 64, 64, None, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 0, 4, 4, 64, 64, None, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EINVAL
+
+
+def _fake_weights(cin=192, cout=192, k=5, s=2, p=2, hb=64, form=0, transposed=0, out_pad=0):
+    d = hatq.desc(cin, cout, k, s, p, hb, transposed, out_pad)
+    cin_p = -(-cin // hb) * hb if form == 0 else cin
+    cout_p = -(-cout // hb) * hb if form == 1 else cout
+    kt = k * k * cin_p
+    return hatq.Weights(d, form, cin_p, cout_p, kt, -(-kt // 64) * 64, 0x10000, 0x20000, 0x30000)
+
+
+def test_conv_rejects_before_launch(L):
+    f = L.hatq_conv_int8
+    W = _fake_weights()
+    assert f(None, FAKE, FAKE, 1, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 5, FAKE, 0, None, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 0, FAKE, 64, FAKE, None) == hatq.HATQ_EINVAL  # I32 + absmax
+    bad = _fake_weights()
+    bad.k_total += 1                                   # inconsistent view
+    assert f(ctypes.byref(bad), FAKE, FAKE, 1, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EINVAL
+    W32 = _fake_weights(cin=32, hb=32)                 # cin_pad 32: neither small nor a multiple of 64
+    assert f(ctypes.byref(W32), FAKE, FAKE, 1, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EUNSUPPORTED
+    Wt3 = _fake_weights(transposed=1, s=3, out_pad=1)  # transposed needs stride 2
+    assert f(ctypes.byref(Wt3), FAKE, FAKE, 1, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EUNSUPPORTED
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 1, FAKE, 128, FAKE, None) == hatq.HATQ_EUNSUPPORTED
+    W0 = _fake_weights(p=0)                            # 5x5, no padding: a 2x2 input gives no output
+    assert f(ctypes.byref(W0), FAKE, FAKE, 1, 2, 2, 1, FAKE, 0, None, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 0, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EINVAL
+
+
+def test_layer_forward_form_flag_and_workspace(L):
+    f = L.hatq_layer_forward
+    W = _fake_weights()
+    # the per-layer form flag must match the prepared weights
+    assert f(ctypes.byref(W), 1, FAKE, 1, 16, 16, None, FAKE, None, 0, None, FAKE, 1 << 30,
+             None) == hatq.HATQ_EINVAL
+    need = L.hatq_layer_ws_bytes(ctypes.byref(W), 1, 16, 16)
+    assert need >= 16 * 16 * 192
+    assert f(ctypes.byref(W), 0, FAKE, 1, 16, 16, None, FAKE, None, 0, None, FAKE, need - 1,
+             None) == hatq.HATQ_EWORKSPACE
+    assert f(ctypes.byref(W), 0, FAKE, 1, 16, 16, None, FAKE, None, 0, None, None, need,
+             None) == hatq.HATQ_EINVAL
