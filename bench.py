@@ -1,0 +1,241 @@
+#!/usr/bin/env python3
+"""Benchmark of the Hadamard-domain INT8 operator on one MI355X.
+
+One step = one pass of the whole hot path over one batch: the four-layer
+analysis stack (5x5 stride-2 convolutions 3->192->192->192->320, per-layer forms
+WH, DH, DH, WH, Sylvester blocks of 64) at batch 16 on 1024x1024 RGB inputs.
+Per layer: activation transform + per-sample absmax + INT8 quantization, INT8
+implicit-GEMM convolution with INT32 accumulation, fused dequant/bias/WH-restore
+epilogue; each convolution's epilogue also produces the next layer's per-sample
+absmax, so layers 2-4 read their fp32 input once.  Inputs and prepared weights
+are resident in HBM before timing.  Data: synthetic, seeded (uniform RGB,
+Student-t weights).
+
+Prints one JSON line.  ``value`` is the whole step's algorithmic INT8 conv
+throughput (TOP/s, dense taps, 2 ops per MAC); per-layer time, TOP/s, GB/s and
+Mpixel/s are under ``layers``.  ``roofline`` is for the dominant kernel (layer-2
+convolution, INT8 MFMA bound); ``roofline_act_quant`` for layer 2's fused
+transform+quantization pass (HBM bound).  ``cpu_baseline`` times the CPU oracle
+on one sample of the batch (rank 0, N = 1 only).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, GB/s
+PEAK_INT8_TOPS = 5000.0      # MI355X dense INT8 MFMA, TOP/s
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cfg4.json")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("act_quant.hip", "conv_i8.hip", "hatq_device.h", "hatq_launch.h", "api.cpp"):
+        h.update(open(os.path.join(ROOT, "paper_2608_01653_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(key: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources; else None."""
+    try:
+        d = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if d.get("source_hash") != kernel_source_hash():
+        return None
+    return d.get("kernels", {}).get(key)
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(wl, x_np, params):
+    """The oracle, as it stands, on sample 0 of the batch (1/n of a step)."""
+    import numpy as np
+    import oracle
+    from paper_2608_01653_amd import workloads
+
+    oracle.lib()
+    x = x_np[:1]
+    ops = 0
+    dt = 0.0
+    for i, L in enumerate(wl.layers):
+        w, b = params[i]
+        pw = oracle.prepare_weights(w, b, cin=L.cin, cout=L.cout, k=L.k, stride=L.stride, pad=L.pad,
+                                    form=L.form, hblock=L.hblock, transposed=L.transposed,
+                                    out_pad=L.out_pad)           # offline, not timed (as on the GPU)
+        t0 = time.perf_counter()
+        r = oracle.layer_forward(x, pw)
+        dt += time.perf_counter() - t0
+        x = r.y
+        ops += workloads.conv_ops(wl, i) // wl.input_shape[0]
+        log(f"cpu baseline: layer {i + 1} done ({dt:.1f} s so far)")
+    cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
+    return {"value": ops / dt / 1e12, "unit": "TOP/s", "cores": cores, "kind": "oracle",
+            "seconds": round(dt, 3),
+            "sample": f"sample 0 of the batch (1/{wl.input_shape[0]} of one step): the same four "
+                      f"layers on [1,{wl.input_shape[1]},{wl.input_shape[2]},3]; weight "
+                      "preparation untimed, as on the GPU"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="cfg4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this operator is measured on one GPU only; --gpus must be 1 "
+              f"(got {args.gpus}). Batch sharding across GPUs needs no communication and is "
+              "described in DESIGN.md, but is not run here.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2608_01653_amd import build, hatq, workloads
+
+    if build.stale() and not os.path.exists(build.LIB):
+        build.build()
+    hatq.load()
+    wl = workloads.ALL[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    x_np, params = wl.generate()
+    log(f"inputs generated: {wl.name} {wl.input_shape}")
+    shapes = wl.shapes()
+    n = wl.input_shape[0]
+    x0 = torch.from_numpy(x_np).to(dev)
+    layers = []
+    for L, (w, b) in zip(wl.layers, params):
+        d = hatq.desc(L.cin, L.cout, L.k, L.stride, L.pad, L.hblock, L.transposed, L.out_pad)
+        layers.append(hatq.hatq_prepare_weights(d, L.form, torch.from_numpy(w).to(dev),
+                                                torch.from_numpy(b).to(dev)))
+    # buffers, all allocated before timing
+    xq, sc, amax, ys = [], [], [], []
+    for (ishape, oshape) in shapes:
+        xq.append(torch.empty(ishape, dtype=torch.int8, device=dev))
+        sc.append(torch.empty(n, dtype=torch.float32, device=dev))
+        amax.append(torch.empty(n, dtype=torch.float32, device=dev))
+        ys.append(torch.empty(oshape, dtype=torch.float32, device=dev))
+    ws = torch.empty(int(hatq.load().hatq_fwht_quant_ws_bytes(n)), dtype=torch.int8, device=dev)
+    act_hb = [L.hblock if L.form == "DH" else 1 for L in wl.layers]
+    nL = len(wl.layers)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nL + 1)]
+          for _ in range(args.steps)]
+
+    def step(events=None):
+        x = x0
+        for i in range(nL):
+            if events:
+                events[2 * i].record()
+            # layer 1 has no producer: two-pass absmax; later layers use the
+            # absmax the previous epilogue produced
+            hatq.hatq_fwht_quant_act(x, act_hb[i], absmax=None if i == 0 else amax[i - 1],
+                                     xq=xq[i], scale=sc[i], ws=ws)
+            if events:
+                events[2 * i + 1].record()
+            nxt = i + 1 < nL
+            hatq.hatq_conv_int8(layers[i], xq[i], sc[i], hatq.HATQ_OUT_F32,
+                                next_hblock=act_hb[i + 1] if nxt else 0,
+                                next_absmax=amax[i] if nxt else None, y=ys[i])
+            x = ys[i]
+        if events:
+            events[2 * nL].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record()
+    for k in range(args.steps):
+        step(ev[k])
+    t_end.record()
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    log(f"timed {args.steps} steps: {total_ms / args.steps:.3f} ms/step")
+    ms_step = total_ms / args.steps
+
+    def avg_ms(a, b):
+        return sum(ev[k][a].elapsed_time(ev[k][b]) for k in range(args.steps)) / args.steps
+
+    total_ops = sum(workloads.conv_ops(wl, i) for i in range(nL))
+    img_pix = n * wl.input_shape[1] * wl.input_shape[2]
+    per_layer = []
+    for i, L in enumerate(wl.layers):
+        (ishape, oshape) = shapes[i]
+        tq = avg_ms(2 * i, 2 * i + 1)
+        tc = avg_ms(2 * i + 1, 2 * i + 2)
+        elems = int(np.prod(ishape))
+        ops = workloads.conv_ops(wl, i)
+        out_pix = oshape[0] * oshape[1] * oshape[2]
+        conv_bytes = elems + layers[i].cout_pad * layers[i].k_stride + out_pix * L.cout * 4
+        per_layer.append({
+            "layer": f"L{i + 1} {L.form} {L.cin}->{L.cout} k{L.k}s{L.stride}",
+            "act_quant_us": round(tq * 1e3, 2),
+            "act_quant_passes": 2 if i == 0 else 1,
+            "act_quant_gbs_alg": round(elems * 5 / (tq * 1e-3) / 1e9, 1),
+            "conv_us": round(tc * 1e3, 2),
+            "conv_tops": round(ops / (tc * 1e-3) / 1e12, 1),
+            "conv_mfma_frac": round(ops / (tc * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4),
+            "conv_gbs_alg": round(conv_bytes / (tc * 1e-3) / 1e9, 1),
+            "mpix_per_s_image": round(img_pix / ((tq + tc) * 1e-3) / 1e6, 1),
+            "mpix_per_s_output": round(out_pix / ((tq + tc) * 1e-3) / 1e6, 1),
+        })
+
+    # dominant kernel: the layer-2 convolution (INT8 MFMA bound)
+    t_conv2 = avg_ms(3, 4) * 1e-3
+    ops2 = workloads.conv_ops(wl, 1)
+    ach = ops2 / t_conv2 / 1e12
+    roof = {"kernel": "conv_kernel<256,192,0> (layer 2, DH 192->192 k5s2)", "bound": "mfma",
+            "achieved": round(ach, 1), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+            "frac": round(ach / PEAK_INT8_TOPS, 4), "traffic": measured_traffic("conv_l2"),
+            "avg_us": round(t_conv2 * 1e6, 2),
+            "work": f"{ops2} ops per launch = 2 x {n}x256x256 outputs x 192 x 5x5x192"}
+    t_q2 = avg_ms(2, 3) * 1e-3
+    e2 = int(np.prod(shapes[1][0]))
+    achq = e2 * 5 / t_q2 / 1e9
+    roof_q = {"kernel": "quant_kernel<64> (layer 2, single read)", "bound": "hbm",
+              "achieved": round(achq, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+              "frac": round(achq / PEAK_HBM_GBS, 4), "traffic": measured_traffic("quant_l2"),
+              "avg_us": round(t_q2 * 1e6, 2),
+              "work": f"{e2 * 5} bytes per launch = {e2} elements x (4 B fp32 in + 1 B int8 out)"}
+
+    out = {
+        "metric": "Hadamard-INT8 conv TOPS + Mpixel/s per layer; % of INT8 MFMA / HBM peak",
+        "value": round(total_ops / (ms_step * 1e-3) / 1e12, 2),
+        "unit": "TOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic (seeded uniform RGB input, Student-t weights)",
+        "config": {"workload": wl.name, "input": list(wl.input_shape),
+                   "layers": [f"{L.form} {L.cin}->{L.cout} k{L.k}s{L.stride} b{L.hblock}"
+                              for L in wl.layers],
+                   "form_mask": ",".join(L.form for L in wl.layers), "parallelism": "none"},
+        "mpix_per_s": round(img_pix / (ms_step * 1e-3) / 1e6, 1),
+        "layers": per_layer,
+        "roofline": roof,
+        "roofline_act_quant": roof_q,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, x_np, params)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

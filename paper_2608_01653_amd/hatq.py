@@ -178,13 +178,18 @@ def hatq_prepare_weights(d: ConvDesc, form, w: torch.Tensor, bias: Optional[torc
 
 
 def hatq_fwht_quant_act(x: torch.Tensor, hblock: int, absmax: Optional[torch.Tensor] = None,
-                        stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """x fp32 NHWC -> (int8 codes NHWC, per-sample scale fp32 [n])."""
+                        xq: Optional[torch.Tensor] = None, scale: Optional[torch.Tensor] = None,
+                        ws: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """x fp32 NHWC -> (int8 codes NHWC, per-sample scale fp32 [n]).  Output and
+    workspace tensors may be passed in to avoid allocation."""
     n, h, w, c = x.shape
-    xq = torch.empty((n, h, w, c), dtype=torch.int8, device=x.device)
-    sc = torch.empty(n, dtype=torch.float32, device=x.device)
+    if xq is None:
+        xq = torch.empty((n, h, w, c), dtype=torch.int8, device=x.device)
+    sc = scale if scale is not None else torch.empty(n, dtype=torch.float32, device=x.device)
     wsb = int(load().hatq_fwht_quant_ws_bytes(n))
-    ws = torch.empty(max(wsb, 4), dtype=torch.int8, device=x.device)
+    if ws is None:
+        ws = torch.empty(max(wsb, 4), dtype=torch.int8, device=x.device)
+    wsb = ws.numel()
     _check(load().hatq_fwht_quant_act(_ptr(x), n, h, w, c, int(hblock), _ptr(absmax), _ptr(xq), _ptr(sc),
                                       _ptr(ws), wsb, _stream(stream)), "hatq_fwht_quant_act")
     return xq, sc
