@@ -30,38 +30,6 @@ constexpr int kThreads = 256;
 constexpr int kQuadsPerBlock = kThreads / 4;
 
 template <int B>
-struct ItemShape {
-    static constexpr int I = B > 64 ? B : 64;   // floats per item
-    static constexpr int R = I / 16;            // float4 registers per lane
-    static constexpr int LOG = B == 1 ? 0 : B == 2 ? 1 : B == 4 ? 2 : B == 8 ? 3 : B == 16 ? 4
-                               : B == 32 ? 5 : B == 64 ? 6 : 7;
-};
-
-// Transform of one item held as v[4*i + j] (lane t = quad position).
-// Returns sigma, the sign of the values held relative to the true transform.
-template <int B, int R4>
-__device__ __forceinline__ float fwht_item(float (&v)[R4], int t) {
-    constexpr int LOG = ItemShape<B>::LOG;
-    float sigma = 1.0f;
-    if constexpr (LOG >= 1) reg_stage<1>(v);                 // channel bit 0
-    if constexpr (LOG >= 2) reg_stage<2>(v);                 // channel bit 1
-    if constexpr (LOG >= 3) {                                 // channel bit 2: lane ^ 1
-        const float c = (t & 1) ? -1.0f : 1.0f;
-        cross_stage<1>(v, c);
-        sigma *= c;
-    }
-    if constexpr (LOG >= 4) {                                 // channel bit 3: lane ^ 2
-        const float c = (t & 2) ? -1.0f : 1.0f;
-        cross_stage<2>(v, c);
-        sigma *= c;
-    }
-    if constexpr (LOG >= 5) reg_stage<4>(v);                 // channel bit 4: register ^ 1
-    if constexpr (LOG >= 6) reg_stage<8>(v);                 // channel bit 5
-    if constexpr (LOG >= 7) reg_stage<16>(v);                // channel bit 6
-    return sigma;
-}
-
-template <int B>
 __device__ __forceinline__ void load_item(const float *xs, int64_t base, int64_t E, int t,
                                           float (&v)[4 * ItemShape<B>::R]) {
     constexpr int R = ItemShape<B>::R;

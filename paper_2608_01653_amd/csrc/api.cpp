@@ -73,7 +73,7 @@ int32_t check_conv_supported(const hatq_weights *W) {
     bool fixed = false;
     for (int t : tiles) fixed |= (W->cout_pad == t);
     const int bn = fixed ? W->cout_pad : 64;
-    if (W->form == HATQ_WH && bn % W->d.hblock != 0) return HATQ_EUNSUPPORTED;
+    if (W->form == HATQ_WH && (bn % W->d.hblock != 0 || W->d.hblock > 64)) return HATQ_EUNSUPPORTED;
     return HATQ_OK;
 }
 
@@ -85,7 +85,7 @@ int32_t check_weights(const hatq_weights *W) {
         dm.k_stride != W->k_stride)
         return HATQ_EINVAL;
     if (!W->wq || !W->w_scale || !W->bias) return HATQ_EINVAL;
-    if (!aligned(W->wq, 16) || !aligned(W->w_scale, 4) || !aligned(W->bias, 4)) return HATQ_EINVAL;
+    if (!aligned(W->wq, 16) || !aligned(W->w_scale, 16) || !aligned(W->bias, 16)) return HATQ_EINVAL;
     return HATQ_OK;
 }
 
@@ -97,7 +97,7 @@ int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next
     bool fixed = false;
     for (int t : tiles) fixed |= (W->cout_pad == t);
     const int bn = fixed ? W->cout_pad : 64;
-    if (bn % next_hblock != 0 && next_hblock > 1) return HATQ_EUNSUPPORTED;
+    if (next_hblock > 64 || (bn % next_hblock != 0 && next_hblock > 1)) return HATQ_EUNSUPPORTED;
     if (!aligned(next_absmax, 4)) return HATQ_EINVAL;
     return HATQ_OK;
 }
@@ -289,7 +289,7 @@ int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act
     if (!xq || !act_scale || !y || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
     if (out_mode != HATQ_OUT_I32 && out_mode != HATQ_OUT_F32) return HATQ_EINVAL;
     if (out_mode == HATQ_OUT_I32 && next_absmax) return HATQ_EINVAL;
-    if (!aligned(xq, 16) || !aligned(y, 4) || !aligned(act_scale, 4)) return HATQ_EINVAL;
+    if (!aligned(xq, 16) || !aligned(y, 16) || !aligned(act_scale, 4)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
     if ((s = check_next(W, next_hblock, next_absmax)) != HATQ_OK) return s;
     int32_t ho, wo;
@@ -311,7 +311,7 @@ int32_t hatq_layer_forward(const hatq_weights *W, int32_t form, const float *x, 
     if (s != HATQ_OK) return s;
     if (form != W->form) return HATQ_EINVAL;
     if (!x || !y || !ws || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
-    if (!aligned(x, 16) || !aligned(y, 4) || !aligned(ws, 256)) return HATQ_EINVAL;
+    if (!aligned(x, 16) || !aligned(y, 16) || !aligned(ws, 256)) return HATQ_EINVAL;
     if (act_scale && !aligned(act_scale, 4)) return HATQ_EINVAL;
     if (x_absmax && !aligned(x_absmax, 4)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;

@@ -112,6 +112,42 @@ __device__ __forceinline__ float wave_max(float m) {
     return m;
 }
 
+template <int B>
+struct ItemShape {
+    static constexpr int I = B > 64 ? B : 64;   // floats per item
+    static constexpr int R = I / 16;            // float4 registers per lane
+    static constexpr int LOG = B == 1 ? 0 : B == 2 ? 1 : B == 4 ? 2 : B == 8 ? 3 : B == 16 ? 4
+                               : B == 32 ? 5 : B == 64 ? 6 : 7;
+};
+
+// Quad layout: one quad (4 consecutive lanes) owns an item of I = max(64, b)
+// consecutive floats; lane t of the quad holds channels 16*i + 4*t + j in
+// v[4*i + j].  Channel bits 0-1 (j) and 4+ (i) are inside the thread, bits 2-3
+// are the quad lane.  fwht_item applies the ascending-bit butterfly of order B to
+// every B-block of the item and returns sigma, the per-lane sign of the values
+// held relative to the true transform.
+template <int B, int R4>
+__device__ __forceinline__ float fwht_item(float (&v)[R4], int t) {
+    constexpr int LOG = ItemShape<B>::LOG;
+    float sigma = 1.0f;
+    if constexpr (LOG >= 1) reg_stage<1>(v);                 // channel bit 0
+    if constexpr (LOG >= 2) reg_stage<2>(v);                 // channel bit 1
+    if constexpr (LOG >= 3) {                                 // channel bit 2: lane ^ 1
+        const float c = (t & 1) ? -1.0f : 1.0f;
+        cross_stage<1>(v, c);
+        sigma *= c;
+    }
+    if constexpr (LOG >= 4) {                                 // channel bit 3: lane ^ 2
+        const float c = (t & 2) ? -1.0f : 1.0f;
+        cross_stage<2>(v, c);
+        sigma *= c;
+    }
+    if constexpr (LOG >= 5) reg_stage<4>(v);                 // channel bit 4: register ^ 1
+    if constexpr (LOG >= 6) reg_stage<8>(v);                 // channel bit 5
+    if constexpr (LOG >= 7) reg_stage<16>(v);                // channel bit 6
+    return sigma;
+}
+
 // Fill n 32-bit words with a value (used instead of hipMemsetAsync so the
 // sequence stays graph-capture friendly).
 __global__ void fill_u32_kernel(uint32_t *p, int n, uint32_t v);

@@ -14,7 +14,7 @@ hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const 
 constexpr int kMaxTaps = 32;
 
 // Geometry and operands of one implicit-GEMM launch.  GEMM rows are the points
-// (nb, gi, gj) of an n x gh x gw grid.  Input anchor of a point:
+// (nb, gi, gj) of an n x gh x gw grid, processed in 2-D tiles of TH x TW points.  Input anchor of a point:
 // (gi*sa + bah, gj*sa + baw); tap t reads the input pixel anchor + (dh[t], dw[t])
 // with weight tap wtap[t] (kh*k + kw).  Output pixel: (gi*so + boh, gj*so + bow).
 struct ConvArgs {
@@ -37,7 +37,7 @@ struct ConvArgs {
     int32_t mode;          // 0 I32, 1 F32
     int32_t hblock;        // the layer's block size
     int32_t next_hblock;   // 0 = no next-operand absmax
-    int32_t tiles_m, tiles_n;
+    int32_t tiles_h, tiles_w, tiles_n;   // 2-D tiles of grid points per sample; column tiles
     int8_t dh[kMaxTaps], dw[kMaxTaps];
     int16_t wtap[kMaxTaps];
 };
