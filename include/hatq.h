@@ -83,7 +83,11 @@ typedef struct {
  * I_{KhKw} (x) H of Eq. input_hadamard_transform); bytes d >= k_total are 0.
  * For a transposed convolution (kh, kw) index the kernel as stored in PyTorch
  * (weight[ci][co][kh][kw]).  w_scale and bias are fp32 [cout_pad]; for WH the
- * bias is the transformed b~ = B_Cout [b; 0] (Eq. supp_padded_wh_parameters). */
+ * bias is the transformed b~ = B_Cout [b; 0] (Eq. supp_padded_wh_parameters).
+ * wpack holds the same codes again in the order the convolution kernels stream
+ * them (K-blocked: [pack_stride/64][cout_pad][64], contiguous per 64-deep
+ * contraction step); it is library-internal and callers must not depend on
+ * its order.  hatq_prepare_weights fills both copies. */
 typedef struct {
     hatq_conv_desc d;
     int32_t form;           /* hatq_form, fixed for the layer's lifetime (Sec. IV-C) */
@@ -94,6 +98,8 @@ typedef struct {
     int8_t *wq;
     float *w_scale;
     float *bias;
+    int8_t *wpack;          /* kernel-order copy of wq (see above) */
+    int32_t pack_stride;    /* contraction bytes per output channel in wpack */
 } hatq_weights;
 
 /* Static description of a status code.  Never NULL. */
@@ -123,6 +129,13 @@ size_t hatq_weights_bytes(const hatq_conv_desc *d, int32_t form);
 int32_t hatq_prepare_weights(const hatq_conv_desc *d, int32_t form, const float *w,
                              const float *bias, void *dst, size_t dst_bytes,
                              hatq_weights *out, void *stream);
+
+/* Rebuild W->wpack from the codes in W->wq, for callers that write codes into
+ * wq themselves (codes quantized elsewhere, e.g. loaded from a deployment
+ * checkpoint, with w_scale and bias filled to match).  W must be a view returned
+ * by hatq_prepare_weights (same geometry); wq bytes past k_total must be 0.
+ * Runs on `stream`. */
+int32_t hatq_pack_weights(const hatq_weights *W, void *stream);
 
 /* Workspace bytes hatq_fwht_quant_act needs for a batch of n samples. */
 size_t hatq_fwht_quant_ws_bytes(int32_t n);

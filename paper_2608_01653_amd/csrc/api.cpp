@@ -29,8 +29,16 @@ int32_t check_desc(const hatq_conv_desc *d, int32_t form) {
 }
 
 struct Dims {
-    int32_t cin_p, cout_p, k_total, k_stride;
+    int32_t cin_p, cout_p, k_total, k_stride, pack_stride;
+    bool rowrun;
 };
+
+// Row-run geometry: a regular convolution with a few input channels whose taps
+// along one kernel row are k*cin_p <= 16 consecutive bytes of the NHWC input;
+// its kernel contracts 16 bytes per kernel row (d' = 16*kh + kw*cin_p + ci).
+bool rowrun_geometry(const hatq_conv_desc *d, int32_t cin_p) {
+    return !d->transposed && cin_p <= 4 && d->k * cin_p <= 16 && d->k <= 8 && d->stride <= 2;
+}
 
 Dims dims_of(const hatq_conv_desc *d, int32_t form) {
     Dims r;
@@ -38,6 +46,8 @@ Dims dims_of(const hatq_conv_desc *d, int32_t form) {
     r.cout_p = (int32_t)(form == HATQ_WH ? round_up(d->cout, d->hblock) : d->cout);
     r.k_total = d->k * d->k * r.cin_p;
     r.k_stride = (int32_t)round_up(r.k_total, 64);
+    r.rowrun = rowrun_geometry(d, r.cin_p);
+    r.pack_stride = r.rowrun ? (int32_t)round_up(16 * d->k, 64) : r.k_stride;
     return r;
 }
 
@@ -65,7 +75,8 @@ int32_t check_conv_supported(const hatq_weights *W) {
     const bool small = W->cin_pad <= 4 && W->k_total <= 128;
     if (!small && W->cin_pad % 64 != 0) return HATQ_EUNSUPPORTED;
     if (W->cout_pad % 64 != 0) return HATQ_EUNSUPPORTED;
-    if (d.k * d.k > hatq::kMaxTaps) return HATQ_EUNSUPPORTED;
+    const bool rowrun = rowrun_geometry(&d, W->cin_pad);
+    if (!rowrun && d.k * d.k > hatq::kMaxTaps) return HATQ_EUNSUPPORTED;   // tap table
     if (d.transposed && (d.stride != 2 || small)) return HATQ_EUNSUPPORTED;
     if (d.k > 64 || d.pad > 64 || d.stride > 64) return HATQ_EUNSUPPORTED;
     // the WH restore runs inside one wave: the block must tile the wave's columns
@@ -82,10 +93,11 @@ int32_t check_weights(const hatq_weights *W) {
     if (check_desc(&W->d, W->form) != HATQ_OK) return HATQ_EINVAL;
     const Dims dm = dims_of(&W->d, W->form);
     if (dm.cin_p != W->cin_pad || dm.cout_p != W->cout_pad || dm.k_total != W->k_total ||
-        dm.k_stride != W->k_stride)
+        dm.k_stride != W->k_stride || dm.pack_stride != W->pack_stride)
         return HATQ_EINVAL;
-    if (!W->wq || !W->w_scale || !W->bias) return HATQ_EINVAL;
-    if (!aligned(W->wq, 16) || !aligned(W->w_scale, 16) || !aligned(W->bias, 16)) return HATQ_EINVAL;
+    if (!W->wq || !W->w_scale || !W->bias || !W->wpack) return HATQ_EINVAL;
+    if (!aligned(W->wq, 16) || !aligned(W->w_scale, 16) || !aligned(W->bias, 16) || !aligned(W->wpack, 16))
+        return HATQ_EINVAL;
     return HATQ_OK;
 }
 
@@ -116,7 +128,7 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
     hatq::ConvArgs a;
     std::memset(&a, 0, sizeof(a));
     a.xq = xq;
-    a.wq = W->wq;
+    a.wp = W->wpack;
     a.sx = sx;
     a.w_scale = W->w_scale;
     a.bias = W->bias;
@@ -128,8 +140,10 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
     a.cin_p = W->cin_pad;
     a.ho = ho;
     a.wo = wo;
+    a.k = d.k;
     a.k_total = W->k_total;
-    a.k_stride = W->k_stride;
+    a.pack_stride = W->pack_stride;
+    a.rowrun = rowrun_geometry(&d, W->cin_pad);
     a.cout = d.cout;
     a.cout_pad = W->cout_pad;
     a.form = W->form;
@@ -147,14 +161,14 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
         a.boh = 0;
         a.bow = 0;
         a.ntaps = d.k * d.k;
-        for (int kh = 0; kh < d.k; ++kh)
+        for (int kh = 0; kh < d.k && d.k * d.k <= hatq::kMaxTaps; ++kh)   // (row-run needs no table)
             for (int kw = 0; kw < d.k; ++kw) {
                 const int t = kh * d.k + kw;
                 a.dh[t] = (int8_t)kh;
                 a.dw[t] = (int8_t)kw;
                 a.wtap[t] = (int16_t)t;
             }
-        a.nksteps = small ? (W->k_total + 63) / 64 : a.ntaps * (W->cin_pad / 64);
+        a.nksteps = small ? W->pack_stride / 64 : a.ntaps * (W->cin_pad / 64);
         a.M = (int64_t)n * a.gh * a.gw;
         return hip_status(hatq::launch_conv(a, true, st));
     }
@@ -218,7 +232,8 @@ int32_t hatq_conv_out_hw(const hatq_conv_desc *d, int32_t h, int32_t w, int32_t 
 size_t hatq_weights_bytes(const hatq_conv_desc *d, int32_t form) {
     if (check_desc(d, form) != HATQ_OK) return 0;
     const Dims dm = dims_of(d, form);
-    return align256((size_t)dm.cout_p * dm.k_stride) + 2 * align256((size_t)dm.cout_p * 4);
+    return align256((size_t)dm.cout_p * dm.k_stride) + 2 * align256((size_t)dm.cout_p * 4) +
+           align256((size_t)dm.cout_p * dm.pack_stride);
 }
 
 int32_t hatq_prepare_weights(const hatq_conv_desc *d, int32_t form, const float *w, const float *bias,
@@ -241,6 +256,8 @@ int32_t hatq_prepare_weights(const hatq_conv_desc *d, int32_t form, const float 
     W.wq = base;
     W.w_scale = reinterpret_cast<float *>(base + align256((size_t)dm.cout_p * dm.k_stride));
     W.bias = reinterpret_cast<float *>(reinterpret_cast<int8_t *>(W.w_scale) + align256((size_t)dm.cout_p * 4));
+    W.wpack = reinterpret_cast<int8_t *>(W.bias) + align256((size_t)dm.cout_p * 4);
+    W.pack_stride = dm.pack_stride;
     hatq::PrepArgs a;
     a.w = w;
     a.bias = bias;
@@ -257,9 +274,29 @@ int32_t hatq_prepare_weights(const hatq_conv_desc *d, int32_t form, const float 
     a.cout_p = dm.cout_p;
     a.k_total = dm.k_total;
     a.k_stride = dm.k_stride;
+    a.wpack = W.wpack;
+    a.pack_stride = dm.pack_stride;
+    a.rowrun = dm.rowrun;
     const int32_t st = hip_status(hatq::launch_prepare(a, static_cast<hipStream_t>(stream)));
     if (st == HATQ_OK) *out = W;
     return st;
+}
+
+int32_t hatq_pack_weights(const hatq_weights *W, void *stream) {
+    const int32_t s = check_weights(W);
+    if (s != HATQ_OK) return s;
+    hatq::PrepArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.wq = W->wq;
+    a.wpack = W->wpack;
+    a.k = W->d.k;
+    a.cin_p = W->cin_pad;
+    a.cout_p = W->cout_pad;
+    a.k_total = W->k_total;
+    a.k_stride = W->k_stride;
+    a.pack_stride = W->pack_stride;
+    a.rowrun = rowrun_geometry(&W->d, W->cin_pad);
+    return hip_status(hatq::launch_pack(a, static_cast<hipStream_t>(stream)));
 }
 
 size_t hatq_fwht_quant_ws_bytes(int32_t n) { return n > 0 ? align256((size_t)n * 4) : 0; }

@@ -12,17 +12,12 @@
 // (i, j) holds channel 16*j + 4*(l/16) + r of pixel 16*i + l%16, i.e. four
 // consecutive channels of one pixel.
 //
-// Epilogue, per 16-pixel group, through a wave-private LDS staging area:
-//   1. dequantize (DH: y = fma(float(acc), fl(s_x*s_w,c)*(1/b), bias_c);
-//      WH: z = fma(float(acc), fl(s_x*s_w,c), b~_c); I32: raw) and write 16 B
-//      per lane into staged rows of BN floats (float4 columns XOR-swizzled by
-//      the row so both access patterns below are bank-conflict free);
-//   2. re-read in the quad layout of the activation kernels (one quad per
-//      64-channel block of one pixel) for the WH output-basis restore (b-point
-//      FWHT, times 1/b) and for the next layer's per-sample max |B_next y|, with
-//      the very butterfly the activation kernels use, so the max equals what
-//      they would compute from the stored y;
-//   3. store every staged row as one contiguous run of 16-B lanes.
+// Epilogue, in registers: a 64-channel block of one pixel lies in four lanes
+// (see fwht_acc), so the dequantization (DH: y = fma(float(acc),
+// fl(s_x*s_w,c)*(1/b), bias_c); WH: z = fma(float(acc), fl(s_x*s_w,c), b~_c);
+// I32: raw), the WH output-basis restore (b-point FWHT times 1/b) and the next
+// layer's per-sample max |B_next y| run on the accumulators with no LDS round
+// trip, and each lane stores 16 B of one pixel.
 #include <utility>
 
 #include "hatq_device.h"
@@ -35,31 +30,6 @@ constexpr int kThreads = 256;
 
 // 16-B chunk swizzle of a 64-B LDS operand row (A and B tiles).
 __device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
-
-// float4-column swizzle of a staged epilogue row: a bijection of the low four
-// bits of the column, different for each of 16 consecutive rows.
-__device__ __forceinline__ int stg_swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
-
-// Quad-layout butterfly of runtime order b <= 64 (wave-uniform branches): the
-// same stages in the same order as fwht_item<b>, hence the same fp32 results.
-__device__ __forceinline__ float fwht16(float (&v)[16], int b, int qt) {
-    float sigma = 1.0f;
-    if (b >= 2) reg_stage<1>(v);
-    if (b >= 4) reg_stage<2>(v);
-    if (b >= 8) {
-        const float c = (qt & 1) ? -1.0f : 1.0f;
-        cross_stage<1>(v, c);
-        sigma *= c;
-    }
-    if (b >= 16) {
-        const float c = (qt & 2) ? -1.0f : 1.0f;
-        cross_stage<2>(v, c);
-        sigma *= c;
-    }
-    if (b >= 32) reg_stage<4>(v);
-    if (b >= 64) reg_stage<8>(v);
-    return sigma;
-}
 
 // A block's tile: sample nb, first grid point (gi0, gj0); local row m is the
 // point (gi0 + m / TW, gj0 + m % TW).  Tiles never straddle samples.
@@ -85,126 +55,6 @@ __device__ __forceinline__ int64_t out_pixel(const ConvArgs &a, int nb, int gi, 
     return ((int64_t)nb * a.ho + gi * a.so + a.boh) * a.wo + gj * a.so + a.bow;
 }
 
-struct EpiCtx {
-    Tile t;
-    int lane, ycols, ncols;
-    bool f32, wh, want_abs;
-    float inv_b;
-    const float *col_t;   // LDS: per column, fl(s_x*s_w,c) (WH) or fl(fl(s_x*s_w,c)/b) (DH)
-    const float *col_b;   // LDS: per column bias
-};
-
-// One 16-point group (local rows row0 + 16*I ... + 15: one tile row segment,
-// since 16 divides TW) of a wave's accumulator tile.
-template <int I, int TW, int FM, int FN>
-__device__ __forceinline__ void epilogue_group(const ConvArgs &a, const EpiCtx &e, const v4i (&acc)[FM][FN],
-                                               int row0, float *stg, float &wave_m) {
-    constexpr int BN = 16 * FN;
-    constexpr int NBLK = BN / 64;
-    static_assert(TW % 16 == 0, "a 16-point group must lie in one tile row");
-    const int lane = e.lane;
-    const int pl = lane & 15, cg = lane >> 4;
-    const int qrow = lane >> 2, qt = lane & 3;
-    const int n0 = e.t.n0;
-    const int m0 = row0 + 16 * I;                 // first local row of the group
-    const int gi = e.t.gi0 + m0 / TW;             // its grid row (same for all 16)
-    const int gj0 = e.t.gj0 + m0 % TW;            // grid column of row 0 of the group
-    const bool row_ok = gi < a.gh;
-    // 1. dequantize into the staged rows
-    {
-        float *srow = stg + pl * BN;
-        const int sw_row = stg_swz(pl);
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int cl = 16 * j + 4 * cg;   // column inside the tile
-            float4 o;
-            if (!e.f32) {
-                o = make_float4(__int_as_float(acc[I][j][0]), __int_as_float(acc[I][j][1]),
-                                __int_as_float(acc[I][j][2]), __int_as_float(acc[I][j][3]));
-            } else {
-                const float4 t4 = *reinterpret_cast<const float4 *>(e.col_t + cl);
-                const float4 b4 = *reinterpret_cast<const float4 *>(e.col_b + cl);
-                o.x = __builtin_fmaf((float)acc[I][j][0], t4.x, b4.x);
-                o.y = __builtin_fmaf((float)acc[I][j][1], t4.y, b4.y);
-                o.z = __builtin_fmaf((float)acc[I][j][2], t4.z, b4.z);
-                o.w = __builtin_fmaf((float)acc[I][j][3], t4.w, b4.w);
-            }
-            const int q = 4 * j + cg;   // float4 column
-            *reinterpret_cast<float4 *>(srow + 4 * (q ^ sw_row)) = o;
-        }
-    }
-    // 2. WH restore and next-operand absmax in the quad layout (same wave: its
-    //    LDS writes above are ordered before these reads)
-    if (e.wh || e.want_abs) {
-        const bool rvalid = row_ok && gj0 + qrow < a.gw;
-        float *srow = stg + qrow * BN;
-        const int sw_row = stg_swz(qrow);
-        for (int k = 0; k < NBLK; ++k) {
-            float v[16];
-#pragma unroll
-            for (int ii = 0; ii < 4; ++ii) {
-                const int q = 16 * k + 4 * ii + qt;
-                const float4 f = *reinterpret_cast<const float4 *>(srow + 4 * (q ^ sw_row));
-                v[4 * ii] = f.x;
-                v[4 * ii + 1] = f.y;
-                v[4 * ii + 2] = f.z;
-                v[4 * ii + 3] = f.w;
-            }
-            if (e.wh) {
-                const float sg = fwht16(v, a.hblock, qt) * e.inv_b;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) v[r] *= sg;
-#pragma unroll
-                for (int ii = 0; ii < 4; ++ii) {
-                    const int q = 16 * k + 4 * ii + qt;
-                    *reinterpret_cast<float4 *>(srow + 4 * (q ^ sw_row)) =
-                        make_float4(v[4 * ii], v[4 * ii + 1], v[4 * ii + 2], v[4 * ii + 3]);
-                }
-            }
-            if (e.want_abs) {
-                // channels past cout and rows past M are not part of the next operand
-#pragma unroll
-                for (int ii = 0; ii < 4; ++ii)
-#pragma unroll
-                    for (int jj = 0; jj < 4; ++jj) {
-                        const int ch = n0 + 64 * k + 16 * ii + 4 * qt + jj;
-                        if (!rvalid || ch >= a.cout) v[4 * ii + jj] = 0.0f;
-                    }
-                fwht16(v, a.next_hblock, qt);
-                float m = 0.0f;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) m = fmaxf(m, fabsf(v[r]));
-                wave_m = fmaxf(wave_m, m);
-            }
-        }
-    }
-    // 3. each staged row is one contiguous run of y
-    if (!row_ok) return;
-    const bool vec = (e.ycols & 3) == 0;
-    float *y0 = reinterpret_cast<float *>(a.y) + out_pixel(a, e.t.nb, gi, gj0) * e.ycols + n0;
-    const int64_t ystep = (int64_t)a.so * e.ycols;   // consecutive grid columns
-    for (int r = 0; r < 16; ++r) {
-        if (gj0 + r >= a.gw) break;
-        float *yr = y0 + r * ystep;
-        const float *srow = stg + r * BN;
-        const int sw_row = stg_swz(r);
-        if (vec) {
-            for (int q = lane; 4 * q < e.ncols; q += 64)
-                *reinterpret_cast<float4 *>(yr + 4 * q) =
-                    *reinterpret_cast<const float4 *>(srow + 4 * (q ^ sw_row));
-        } else {
-            for (int c = lane; c < e.ncols; c += 64) yr[c] = srow[4 * ((c >> 2) ^ sw_row) + (c & 3)];
-        }
-    }
-}
-
-template <int TW, int FM, int FN, int... Is>
-__device__ __forceinline__ void epilogue_groups(const ConvArgs &a, const EpiCtx &e, const v4i (&acc)[FM][FN],
-                                                int row0, float *stg, float &wave_m,
-                                                std::integer_sequence<int, Is...>) {
-    (epilogue_group<Is, TW, FM, FN>(a, e, acc, row0, stg, wave_m), ...);
-}
-
 // Per-tile column factors of the dequantization (the tile is one sample, so
 // s_x is uniform): col_t[c] = fl(s_x*s_w,c) for WH, fl(fl(s_x*s_w,c) * (1/b))
 // for DH (exact power of two); col_b[c] = bias.  Written by the whole block.
@@ -218,29 +68,159 @@ __device__ __forceinline__ void column_factors(const ConvArgs &a, const Tile &t,
     }
 }
 
-// row0: the wave's first local row in the tile.  col_t / col_b: LDS column
-// factors (column_factors, followed by a block barrier).
+// ---- register epilogue ------------------------------------------------------
+// Channel c = n0 + 64*k + 16*jj + 4*q + r of the pixel of lane p + 16*q lies in
+// acc[i][4*k + jj][r].  Inside a 64-channel block, channel bits 0-1 are the
+// register r, bits 2-3 the lane bits 4-5 (q) and bits 4-5 the fragment jj: the
+// quad layout of the activation kernels with the lane bits moved.  fwht_acc
+// applies the same ascending-bit butterflies as fwht_item and produces the same
+// fp32 values: every stage output is a correctly rounded a + c or a - c.
+
+// Pair swap across lane bit 4 (MASK 16: odd 16-lane rows of x with even rows of
+// y) or bit 5 (MASK 32: upper half of x with lower half of y).
+template <int MASK>
+__device__ __forceinline__ void pair_swap(float &x, float &y) {
+    const unsigned xi = __float_as_uint(x), yi = __float_as_uint(y);
+    if constexpr (MASK == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(xi, yi, false, false);
+        x = __uint_as_float(r[0]);
+        y = __uint_as_float(r[1]);
+    } else {
+        static_assert(MASK == 32, "lane bit 4 or 5");
+        const auto r = __builtin_amdgcn_permlane32_swap(xi, yi, false, false);
+        x = __uint_as_float(r[0]);
+        y = __uint_as_float(r[1]);
+    }
+}
+
+// Butterfly across lane bit MASK on two registers at once: after one pair swap
+// every lane holds both partners (a: bit clear, c: bit set) of one pair, of x in
+// the lanes with the bit clear and of y in the others; a + c and a - c are
+// formed in-lane and a second swap puts them back in place.
+template <int MASK>
+__device__ __forceinline__ void cross_pair(float &x, float &y) {
+    pair_swap<MASK>(x, y);
+    const float s = x + y, d = x - y;
+    x = s;
+    y = d;
+    pair_swap<MASK>(x, y);
+}
+
+// Runtime block size b <= 64 (wave-uniform branches).  All lanes of the wave
+// must be active.
+__device__ __forceinline__ void fwht_acc(float (&v)[16], int b) {
+    if (b >= 2) reg_stage<1>(v);
+    if (b >= 4) reg_stage<2>(v);
+    if (b >= 8) {
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) cross_pair<16>(v[r], v[r + 1]);
+    }
+    if (b >= 16) {
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) cross_pair<32>(v[r], v[r + 1]);
+    }
+    if (b >= 32) reg_stage<4>(v);
+    if (b >= 64) reg_stage<8>(v);
+}
+
+// row0: the wave's first local row in the tile (local row m = row0 + 16*i + p is
+// grid point (gi0 + m / TW, gj0 + m % TW)).  col_t / col_b: LDS column factors
+// (column_factors, followed by a block barrier).
 template <int TW, int FM, int FN>
-__device__ __forceinline__ void epilogue(const ConvArgs &a, const v4i (&acc)[FM][FN], const Tile &t, int row0,
-                                         int lane, float *stg, const float *col_t, const float *col_b) {
-    constexpr int BN = 16 * FN;
-    static_assert(BN % 64 == 0, "staging needs whole 64-channel blocks");
-    EpiCtx e;
-    e.t = t;
-    e.lane = lane;
-    e.f32 = a.mode != 0;
-    e.wh = e.f32 && a.form == 1;
-    e.want_abs = e.f32 && a.next_absmax != nullptr && a.next_hblock > 0;
-    e.inv_b = 1.0f / (float)a.hblock;
-    e.ycols = e.f32 ? a.cout : a.cout_pad;
-    e.ncols = e.ycols - t.n0 < BN ? e.ycols - t.n0 : BN;
-    e.col_t = col_t;
-    e.col_b = col_b;
+__device__ __forceinline__ void epilogue_regs(const ConvArgs &a, const v4i (&acc)[FM][FN], const Tile &t,
+                                              int row0, int lane, const float *col_t, const float *col_b) {
+    static_assert(FN % 4 == 0, "whole 64-channel blocks");
+    constexpr int NBLK = FN / 4;
+    const int p = lane & 15, q = lane >> 4;
+    const bool f32 = a.mode != 0;
+    const bool wh = f32 && a.form == 1;
+    const bool want_abs = f32 && a.next_absmax != nullptr && a.next_hblock > 0;
+    const float inv_b = 1.0f / (float)a.hblock;
+    const int ycols = f32 ? a.cout : a.cout_pad;
+    const int ncols = ycols - t.n0 < 16 * FN ? ycols - t.n0 : 16 * FN;
+    const bool vec = (ycols & 3) == 0;
+    // the whole tile inside the grid (wave-uniform): no row masking needed
+    const bool full = t.gi0 + (row0 + 16 * FM - 1) / TW < a.gh && t.gj0 + TW <= a.gw;
     float wave_m = 0.0f;
-    epilogue_groups<TW, FM, FN>(a, e, acc, row0, stg, wave_m, std::make_integer_sequence<int, FM>{});
-    if (e.want_abs) {
+    // published running maximum of this sample, read early (used at the end)
+    float seen = -1.0f;
+    if (want_abs && lane == 0)
+        seen = __uint_as_float(__hip_atomic_load(reinterpret_cast<unsigned int *>(a.next_absmax + t.nb),
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int m = row0 + 16 * i + p;
+        const int gi = t.gi0 + m / TW, gj = t.gj0 + m % TW;
+        const bool valid = gi < a.gh && gj < a.gw;
+        float *yp = reinterpret_cast<float *>(a.y) + (valid ? out_pixel(a, t.nb, gi, gj) * ycols + t.n0 : 0);
+#pragma unroll
+        for (int k = 0; k < NBLK; ++k) {
+            float v[16];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const v4i c4 = acc[i][4 * k + jj];
+                if (!f32) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) v[4 * jj + r] = __int_as_float(c4[r]);
+                } else {
+                    const int cl = 64 * k + 16 * jj + 4 * q;
+                    const float4 t4 = *reinterpret_cast<const float4 *>(col_t + cl);
+                    const float4 b4 = *reinterpret_cast<const float4 *>(col_b + cl);
+                    v[4 * jj + 0] = __builtin_fmaf((float)c4[0], t4.x, b4.x);
+                    v[4 * jj + 1] = __builtin_fmaf((float)c4[1], t4.y, b4.y);
+                    v[4 * jj + 2] = __builtin_fmaf((float)c4[2], t4.z, b4.z);
+                    v[4 * jj + 3] = __builtin_fmaf((float)c4[3], t4.w, b4.w);
+                }
+            }
+            if (wh) {
+                fwht_acc(v, a.hblock);
+#pragma unroll
+                for (int r = 0; r < 16; ++r) v[r] *= inv_b;
+            }
+            if (want_abs) {
+                // rows past the grid and channels past cout are not part of the next operand
+                float u[16];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) u[r] = v[r];
+                if (!full || t.n0 + 64 * k + 64 > a.cout) {
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int ch = t.n0 + 64 * k + 16 * jj + 4 * q + r;
+                            if (!valid || ch >= a.cout) u[4 * jj + r] = 0.0f;
+                        }
+                }
+                fwht_acc(u, a.next_hblock);
+                float mm = 0.0f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(u[r]));
+                wave_m = fmaxf(wave_m, mm);
+            }
+            if (valid) {
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int cl = 64 * k + 16 * jj + 4 * q;
+                    if (vec) {
+                        if (cl < ncols)
+                            *reinterpret_cast<float4 *>(yp + cl) =
+                                make_float4(v[4 * jj], v[4 * jj + 1], v[4 * jj + 2], v[4 * jj + 3]);
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (cl + r < ncols) yp[cl + r] = v[4 * jj + r];
+                    }
+                }
+            }
+        }
+    }
+    if (want_abs) {
         wave_m = wave_max(wave_m);
-        if (lane == 0) atomic_max_nonneg(a.next_absmax + t.nb, wave_m);
+        // The running maximum only grows, so a wave whose maximum does not exceed
+        // a value already published skips its atomic (the read may be stale, which
+        // costs at most an unneeded atomic).  Device-scope atomics on one address
+        // serialize, and most waves of a layer end up skipping.
+        if (lane == 0 && wave_m > seen) atomic_max_nonneg(a.next_absmax + t.nb, wave_m);
     }
 }
 
@@ -252,6 +232,162 @@ __device__ __forceinline__ int xcd_logical_tile() {
     const int bid = blockIdx.x;
     const int xcd = bid & 7, q8 = nt >> 3, rmd = nt & 7;
     return xcd * q8 + (xcd < rmd ? xcd : rmd) + (bid >> 3);
+}
+
+// ---------------------------------------------------------------------------
+// Row-run path (regular convolution, cin_p <= 4, k*cin_p <= 16, k <= 8,
+// stride <= 2): in NHWC the taps kw = 0..k-1 of one kernel row kh are k*cin_p
+// consecutive input bytes, so the contraction is taken as one 16-byte run per
+// kernel row, d' = 16*kh + (kw*cin_p + ci) (weights zero past k*cin_p and past
+// kh = k-1).  A block stages its input patch (zero outside the image) and the
+// whole weight tile in LDS; lane group g of a fragment holds the run of kernel
+// row 4*ks + g, read unaligned from the patch with byte funnel shifts.
+// Accumulators stay small (two 16-point groups per wave) so two blocks share a
+// CU and one block's stores overlap the other's loads and MFMAs.
+// ---------------------------------------------------------------------------
+template <int TH, int TW, int BN, int CIN>
+__global__ void __launch_bounds__(kThreads, 2) conv_rowrun_kernel(const ConvArgs a) {
+    constexpr int BM = TH * TW;
+    constexpr int TM = BM / 4;
+    constexpr int FM = TM / 16;
+    constexpr int FN = BN / 16;
+    constexpr int PH = (TH - 1) * 2 + 8;                 // patch rows (stride <= 2, k <= 8)
+    constexpr int PWB = ((TW - 1) * 2 + 8) * CIN;        // patch bytes per row
+    constexpr int RS = (PWB + 3 + 20 + 15) / 16 * 16;    // LDS row stride: alignment shift + 20-byte reads
+    constexpr int RW = RS / 4;
+    constexpr int PWORDS = PH * RW;
+    constexpr int PIT = (PWORDS + kThreads - 1) / kThreads;
+    constexpr int BIT = 2 * BN * 4 / kThreads;
+    static_assert(TM % 16 == 0 && TW % 16 == 0 && BN % 64 == 0 && 2 * BN * 4 % kThreads == 0, "tile");
+    __shared__ __attribute__((aligned(16))) int8_t s_b[2 * BN * 64];
+    __shared__ uint32_t s_patch[PWORDS];
+    __shared__ __attribute__((aligned(16))) float s_col[2 * BN];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const Tile tile = block_tile(a, xcd_logical_tile(), TH, TW, BN);
+    const int nks = a.nksteps;   // 1 or 2 (pack_stride / 64)
+    const int ih0 = tile.gi0 * a.sa + a.bah, iw0 = tile.gj0 * a.sa + a.baw;
+    const int prow = (TH - 1) * a.sa + a.k;   // patch rows in use
+    const int pcols = (TW - 1) * a.sa + a.k;  // patch columns in use
+    // Patch row r holds the input bytes of row ih0 + r from the 4-aligned address
+    // at or below its first byte (pixel iw0), so it is fetched as aligned dwords;
+    // the row's alignment shift is (first byte address) mod 4.  Buffer offsets
+    // below 0 or past the input wrap or exceed num_records and read 0; every
+    // byte outside the image is masked to 0 anyway.
+    auto row_shift = [&](int r) -> int {
+        const uint32_t g = ((uint32_t)(tile.nb * a.h + ih0 + r) * (uint32_t)a.w + (uint32_t)iw0) * (uint32_t)CIN;
+        return (int)(g & 3u);
+    };
+
+    // ---- every global load of the prologue is issued before the first wait ----
+    v4i wb[BIT];
+#pragma unroll
+    for (int it = 0; it < BIT; ++it) {
+        const int pc = tid + it * kThreads;
+        const int ks = pc / (BN * 4), rem = pc - ks * (BN * 4);
+        wb[it] = v4i{0, 0, 0, 0};
+        if (ks < nks)
+            wb[it] = *reinterpret_cast<const v4i *>(a.wp + ((int64_t)ks * a.cout_pad + tile.n0 + (rem >> 2)) * 64 +
+                                                    16 * (rem & 3));
+    }
+    const int64_t in_bytes = (int64_t)a.n * a.h * a.w * CIN;
+    const __amdgpu_buffer_rsrc_t rx =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t *>(a.xq), (short)0, (int)in_bytes, 0x00020000);
+    uint32_t pwd[PIT];
+#pragma unroll
+    for (int it = 0; it < PIT; ++it) {
+        const int e4 = tid + it * kThreads;
+        const int r = e4 / RW, wi = e4 - r * RW;
+        const int ih = ih0 + r;
+        pwd[it] = 0;
+        if (e4 < PWORDS && r < prow && (unsigned)ih < (unsigned)a.h) {
+            const int sh = row_shift(r);
+            const int64_t ga = ((int64_t)(tile.nb * a.h + ih) * a.w + iw0) * CIN - sh + 4 * wi;
+            uint32_t word;
+            if (ga + 4 <= in_bytes) {
+                word = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rx, (int)(uint32_t)ga, 0, 0);
+            } else {
+                // the dword straddling the end of the input (the range check would
+                // drop all of it): its bytes one by one
+                word = 0;
+                for (int e = 0; e < 4; ++e)
+                    if (ga + e >= 0 && ga + e < in_bytes) word |= (uint32_t)(uint8_t)a.xq[ga + e] << (8 * e);
+            }
+            uint32_t mask = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int rel = 4 * wi + e - sh;   // byte index from pixel iw0
+                const int c = rel / CIN;
+                if (rel >= 0 && c < pcols && (unsigned)(iw0 + c) < (unsigned)a.w) mask |= 0xFFu << (8 * e);
+            }
+            pwd[it] = word & mask;
+        }
+    }
+    float colv_t = 0.0f, colv_b = 0.0f;
+    if (tid < BN) {
+        const float f = a.form == 1 ? 1.0f : 1.0f / (float)a.hblock;
+        colv_t = (a.sx[tile.nb] * a.w_scale[tile.n0 + tid]) * f;
+        colv_b = a.bias[tile.n0 + tid];
+    }
+    // ---- LDS ----
+#pragma unroll
+    for (int it = 0; it < BIT; ++it) {
+        const int pc = tid + it * kThreads;
+        const int ks = pc / (BN * 4), rem = pc - ks * (BN * 4);
+        const int nn = rem >> 2, g = rem & 3;
+        *reinterpret_cast<v4i *>(s_b + ks * BN * 64 + nn * 64 + 16 * (g ^ swz(nn))) = wb[it];
+    }
+#pragma unroll
+    for (int it = 0; it < PIT; ++it) {
+        const int e4 = tid + it * kThreads;
+        if (e4 < PWORDS) s_patch[e4] = pwd[it];
+    }
+    static_assert(BN <= kThreads, "one column per thread");
+    if (tid < BN) {
+        s_col[tid] = colv_t;
+        s_col[BN + tid] = colv_b;
+    }
+    __syncthreads();
+
+    const int fr = lane & 15, fg = lane >> 4;
+    int poff[FM];   // patch byte of the run of kernel row 0 for this lane's points
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int m = wave * TM + 16 * i + fr;
+        const int ohl = m / TW, owl = m - ohl * TW;
+        poff[i] = a.sa * ohl * RS + a.sa * owl * CIN;   // + row shift, added per kernel row below
+    }
+    v4i acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+    for (int ks = 0; ks < nks; ++ks) {
+        // kernel row 4*ks + fg <= 7 stays inside the patch; rows >= k meet zero weights
+        const int kh = 4 * ks + fg;
+        v4i fa[FM];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int m = wave * TM + 16 * i + fr;
+            const int off = poff[i] + kh * RS + row_shift(a.sa * (m / TW) + kh);
+            const uint32_t *pw = s_patch + (off >> 2);
+            const uint32_t sh = off & 3;
+            const uint32_t d0 = pw[0], d1 = pw[1], d2 = pw[2], d3 = pw[3], d4 = pw[4];
+            fa[i] = v4i{(int)__builtin_amdgcn_alignbyte(d1, d0, sh), (int)__builtin_amdgcn_alignbyte(d2, d1, sh),
+                        (int)__builtin_amdgcn_alignbyte(d3, d2, sh), (int)__builtin_amdgcn_alignbyte(d4, d3, sh)};
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int nn = 16 * j + fr;
+            const v4i fb = *reinterpret_cast<const v4i *>(s_b + ks * BN * 64 + nn * 64 + 16 * (fg ^ swz(nn)));
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fb, fa[i], acc[i][j], 0, 0, 0);
+        }
+    }
+    epilogue_regs<TW, FM, FN>(a, acc, tile, wave * TM, lane, s_col, s_col + BN);
 }
 
 // ---------------------------------------------------------------------------
@@ -268,8 +404,8 @@ __global__ void __launch_bounds__(kThreads, 1) conv_gather_kernel(const ConvArgs
     constexpr int A_PIECES = BM * 4 / kThreads;
     constexpr int B_PIECES = BN * 4 / kThreads;
     constexpr int BUF = (BM + BN) * 64;
-    constexpr int EPI_BYTES = (4 * 16 + 2) * BN * 4;   // staging + column factors
-    constexpr int LDS_BYTES = 2 * BUF > EPI_BYTES ? 2 * BUF : EPI_BYTES;
+    constexpr int LDS_BYTES = 2 * BUF;
+    static_assert(LDS_BYTES >= 2 * BN * 4, "column factors fit");
     static_assert(BM * 4 % kThreads == 0 && BN * 4 % kThreads == 0, "tile");
     __shared__ __attribute__((aligned(16))) int8_t lds[LDS_BYTES];
     __shared__ int s_lut_off[128];
@@ -344,7 +480,7 @@ __global__ void __launch_bounds__(kThreads, 1) conv_gather_kernel(const ConvArgs
 #pragma unroll
         for (int p = 0; p < B_PIECES; ++p) {
             const int nn = (tid >> 2) + 64 * p;
-            rb[p] = *reinterpret_cast<const v4i *>(a.wq + (int64_t)(n0 + nn) * a.k_stride + d0);
+            rb[p] = *reinterpret_cast<const v4i *>(a.wp + ((int64_t)ks * a.cout_pad + n0 + nn) * 64 + g * 16);
         }
     };
     auto lds_store = [&](int buf) {
@@ -395,11 +531,10 @@ __global__ void __launch_bounds__(kThreads, 1) conv_gather_kernel(const ConvArgs
         if (ks + 1 < nks) lds_store(buf ^ 1);
         __syncthreads();
     }
-    float *col = reinterpret_cast<float *>(lds) + 4 * 16 * BN;
+    float *col = reinterpret_cast<float *>(lds);
     column_factors<BN>(a, tile, col, col + BN);
     __syncthreads();
-    epilogue<TW, FM, FN>(a, acc, tile, wave * TM, lane, reinterpret_cast<float *>(lds) + wave * 16 * BN, col,
-                         col + BN);
+    epilogue_regs<TW, FM, FN>(a, acc, tile, wave * TM, lane, col, col + BN);
 }
 
 // Fill the tile counts of a launch over TH x TW tiles; returns the block count.
@@ -408,6 +543,23 @@ int64_t set_tiles(ConvArgs &b, int TH, int TW, int BN) {
     b.tiles_w = (b.gw + TW - 1) / TW;
     b.tiles_n = b.cout_pad / BN;
     return (int64_t)b.n * b.tiles_h * b.tiles_w * b.tiles_n;
+}
+
+template <int TH, int TW, int BN, int CS>
+hipError_t launch_rowrun(const ConvArgs &a, hipStream_t st) {
+    ConvArgs b = a;
+    const int64_t tiles = set_tiles(b, TH, TW, BN);
+    if (tiles <= 0 || tiles >= ((int64_t)1 << 31) || b.nksteps < 1 || b.nksteps > 2 || b.sa > 2)
+        return hipErrorInvalidValue;
+    conv_rowrun_kernel<TH, TW, BN, CS><<<(unsigned)tiles, kThreads, 0, st>>>(b);
+    return hipGetLastError();
+}
+
+template <int CS>
+hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
+    if (a.cout_pad % 192 == 0) return launch_rowrun<2, 64, 192, CS>(a, st);
+    if (a.cout_pad % 128 == 0) return launch_rowrun<2, 64, 128, CS>(a, st);
+    return launch_rowrun<2, 64, 64, CS>(a, st);
 }
 
 template <int TH, int TW, int BN, int CS>
@@ -469,7 +621,6 @@ __global__ void __launch_bounds__(kThreads, 1) conv_pipe_kernel(const ConvArgs a
     constexpr int PER_STAGE = A_INSTR + B_INSTR;
     constexpr int STAGE_BYTES = (BM + BN) * 64;
     static_assert(BM % 64 == 0 && BN % 64 == 0 && STAGES >= 3, "tile");
-    static_assert(STAGES * STAGE_BYTES >= (4 * 16 + 2) * BN * 4, "epilogue staging fits in the ring");
     __shared__ __attribute__((aligned(1024))) int8_t lds[STAGES * STAGE_BYTES];
 
     const int tid = threadIdx.x;
@@ -483,7 +634,7 @@ __global__ void __launch_bounds__(kThreads, 1) conv_pipe_kernel(const ConvArgs a
     const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int8_t *>(a.xq), (short)0, (int)((int64_t)a.n * a.h * a.w * cin_p), 0x00020000);
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<int8_t *>(a.wq), (short)0, (int)((int64_t)a.cout_pad * a.k_stride), 0x00020000);
+        const_cast<int8_t *>(a.wp), (short)0, (int)((int64_t)a.cout_pad * a.pack_stride), 0x00020000);
 
     // A rows this lane fetches: instruction j covers rows 16*(wave + 4j) + lane/4
     int a_off[A_INSTR], a_ih0[A_INSTR], a_iw0[A_INSTR];
@@ -507,7 +658,7 @@ __global__ void __launch_bounds__(kThreads, 1) conv_pipe_kernel(const ConvArgs a
     for (int j = 0; j < B_INSTR; ++j) {
         const int nn = 16 * (wave + 4 * j) + (lane >> 2);
         const int g = (lane & 3) ^ swz(nn);
-        b_off[j] = (uint32_t)((n0 + nn) * a.k_stride + 16 * g);
+        b_off[j] = (uint32_t)((n0 + nn) * 64 + 16 * g);
     }
 
     auto issue = [&](int ks) {
@@ -522,7 +673,8 @@ __global__ void __launch_bounds__(kThreads, 1) conv_pipe_kernel(const ConvArgs a
             const bool in = (unsigned)ih < (unsigned)a.h && (unsigned)iw < (unsigned)a.w;
             dma16(rx, sb + 1024 * (wave + 4 * j), in ? (uint32_t)(a_off[j] + doff) : kOobOffset);
         }
-        const uint32_t woff = (uint32_t)(a.wtap[tap] * cin_p + chunk * 64);
+        // K-blocked weights: this step's BN rows are one contiguous run
+        const uint32_t woff = (uint32_t)((a.wtap[tap] * nchunks + chunk) * a.cout_pad * 64);
 #pragma unroll
         for (int j = 0; j < B_INSTR; ++j) dma16(rw, sb + BM * 64 + 1024 * (wave + 4 * j), b_off[j] + woff);
     };
@@ -593,12 +745,11 @@ __global__ void __launch_bounds__(kThreads, 1) conv_pipe_kernel(const ConvArgs a
 #pragma unroll
         for (int i = 0; i < FM; ++i) fa0[i] = fa1[i];
     }
-    __syncthreads();   // every wave is done with the ring; reuse it as staging
-    float *col = reinterpret_cast<float *>(lds) + 4 * 16 * BN;
+    __syncthreads();   // every wave is done with the ring; reuse it for the column factors
+    float *col = reinterpret_cast<float *>(lds);
     column_factors<BN>(a, tile, col, col + BN);
     __syncthreads();
-    epilogue<TW, FM, FN>(a, acc, tile, wave * TM, lane, reinterpret_cast<float *>(lds) + wave * 16 * BN, col,
-                         col + BN);
+    epilogue_regs<TW, FM, FN>(a, acc, tile, wave * TM, lane, col, col + BN);
 }
 
 template <int TH, int TW, int BN, int STAGES>
@@ -608,7 +759,7 @@ hipError_t launch_pipe(const ConvArgs &a, hipStream_t st) {
     const int64_t per_sample = (int64_t)a.h * a.w * a.cin_p;
     int64_t group = ((int64_t)1 << 31) / per_sample;
     if (group < 1) return hipErrorInvalidValue;
-    if ((int64_t)a.cout_pad * a.k_stride >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    if ((int64_t)a.cout_pad * a.pack_stride >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     for (int64_t s0 = 0; s0 < a.n; s0 += group) {
         ConvArgs b = a;
         const int gn = (int)(a.n - s0 < group ? a.n - s0 : group);
@@ -641,10 +792,10 @@ hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
                 case 320: return launch_pipe<4, 32, 320, 5>(a, st);
                 default: return launch_pipe<8, 32, 64, 5>(a, st);
             }
-        case 1: return launch_gather_n<1>(a, st);
-        case 2: return launch_gather_n<2>(a, st);
-        case 3: return launch_gather_n<3>(a, st);
-        case 4: return launch_gather_n<4>(a, st);
+        case 1: return a.rowrun ? launch_rowrun_n<1>(a, st) : launch_gather_n<1>(a, st);
+        case 2: return a.rowrun ? launch_rowrun_n<2>(a, st) : launch_gather_n<2>(a, st);
+        case 3: return a.rowrun ? launch_rowrun_n<3>(a, st) : launch_gather_n<3>(a, st);
+        case 4: return a.rowrun ? launch_rowrun_n<4>(a, st) : launch_gather_n<4>(a, st);
         default: return hipErrorInvalidValue;
     }
 }

@@ -19,7 +19,7 @@ constexpr int kMaxTaps = 32;
 // with weight tap wtap[t] (kh*k + kw).  Output pixel: (gi*so + boh, gj*so + bow).
 struct ConvArgs {
     const int8_t *xq;
-    const int8_t *wq;
+    const int8_t *wp;      // K-blocked weights [pack_stride/64][cout_pad][64]
     const float *sx;
     const float *w_scale;
     const float *bias;
@@ -30,8 +30,9 @@ struct ConvArgs {
     int32_t gh, gw;
     int32_t sa, bah, baw;
     int32_t ho, wo, so, boh, bow;
-    int32_t ntaps, nksteps;
-    int32_t k_total, k_stride;
+    int32_t k, ntaps, nksteps;   // kernel size; taps and K-steps of this launch
+    int32_t k_total, pack_stride;
+    int32_t rowrun;        // small-cin layer contracted per kernel row (16 B each)
     int32_t cout, cout_pad;
     int32_t form;          // 0 DH, 1 WH
     int32_t mode;          // 0 I32, 1 F32
@@ -53,9 +54,12 @@ struct PrepArgs {
     int8_t *wq;
     float *w_scale;
     float *w_bias;
+    int8_t *wpack;         // K-blocked copy of wq in the kernels' contraction order
     int32_t cin, cout, k, transposed, hblock, form;
-    int32_t cin_p, cout_p, k_total, k_stride;
+    int32_t cin_p, cout_p, k_total, k_stride, pack_stride, rowrun;
 };
 hipError_t launch_prepare(const PrepArgs &a, hipStream_t st);
+// Rebuild wpack from wq (geometry fields, wq and wpack are used).
+hipError_t launch_pack(const PrepArgs &a, hipStream_t st);
 
 }  // namespace hatq

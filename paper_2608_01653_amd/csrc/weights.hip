@@ -43,6 +43,25 @@ __device__ float w_prime(const PrepArgs &a, int co, int d) {
     return (float)acc;
 }
 
+// K-blocked copy of one channel's codes: contraction byte d' goes to
+// wpack[d'/64][co][d'%64].  Natural order d' = d, except for row-run layers,
+// whose kernel contracts one 16-byte run per kernel row: d' = 16*kh + j holds
+// d = kh*k*cin_p + j for j < k*cin_p and 0 otherwise.
+__device__ void pack_row(const PrepArgs &a, int co, const int8_t *row) {
+    for (int dp = threadIdx.x; dp < a.pack_stride; dp += kThreads) {
+        int d = dp;
+        if (a.rowrun) {
+            const int kh = dp >> 4, j = dp & 15;
+            d = (kh < a.k && j < a.k * a.cin_p) ? kh * a.k * a.cin_p + j : a.k_stride;
+        }
+        a.wpack[((int64_t)(dp >> 6) * a.cout_p + co) * 64 + (dp & 63)] = d < a.k_stride ? row[d] : (int8_t)0;
+    }
+}
+
+__global__ void __launch_bounds__(kThreads) pack_kernel(const PrepArgs a) {
+    pack_row(a, blockIdx.x, a.wq + (int64_t)blockIdx.x * a.k_stride);
+}
+
 __global__ void __launch_bounds__(kThreads) prepare_kernel(const PrepArgs a) {
     const int co = blockIdx.x;
     float m = 0.0f;
@@ -61,6 +80,8 @@ __global__ void __launch_bounds__(kThreads) prepare_kernel(const PrepArgs a) {
         if (d < a.k_total) q = (int8_t)(int)rintf(clamp127(w_prime(a, co, d) / s));
         row[d] = q;
     }
+    __syncthreads();   // this block's wq row is complete
+    pack_row(a, co, row);
     if (threadIdx.x == 0) {
         a.w_scale[co] = s;
         double bv = 0.0;
@@ -81,6 +102,11 @@ __global__ void __launch_bounds__(kThreads) prepare_kernel(const PrepArgs a) {
 
 hipError_t launch_prepare(const PrepArgs &a, hipStream_t st) {
     prepare_kernel<<<a.cout_p, kThreads, 0, st>>>(a);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack(const PrepArgs &a, hipStream_t st) {
+    pack_kernel<<<a.cout_p, kThreads, 0, st>>>(a);
     return hipGetLastError();
 }
 

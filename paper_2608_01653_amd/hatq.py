@@ -40,11 +40,12 @@ class Weights(ctypes.Structure):
     _fields_ = [("d", ConvDesc), ("form", ctypes.c_int32), ("cin_pad", ctypes.c_int32),
                 ("cout_pad", ctypes.c_int32), ("k_total", ctypes.c_int32),
                 ("k_stride", ctypes.c_int32), ("wq", ctypes.c_void_p),
-                ("w_scale", ctypes.c_void_p), ("bias", ctypes.c_void_p)]
+                ("w_scale", ctypes.c_void_p), ("bias", ctypes.c_void_p),
+                ("wpack", ctypes.c_void_p), ("pack_stride", ctypes.c_int32)]
 
 
 EXPORTS = ["hatq_status_string", "hatq_conv_out_hw", "hatq_weights_bytes", "hatq_prepare_weights",
-           "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act", "hatq_conv_int8",
+           "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act", "hatq_conv_int8",
            "hatq_layer_ws_bytes", "hatq_layer_forward"]
 
 _lib = None
@@ -74,6 +75,8 @@ def load(build_if_missing: bool = False):
     L.hatq_weights_bytes.restype = sz
     L.hatq_prepare_weights.argtypes = [ctypes.POINTER(ConvDesc), i32, P, P, P, sz, ctypes.POINTER(Weights), P]
     L.hatq_prepare_weights.restype = i32
+    L.hatq_pack_weights.argtypes = [ctypes.POINTER(Weights), P]
+    L.hatq_pack_weights.restype = i32
     L.hatq_fwht_quant_ws_bytes.argtypes = [i32]
     L.hatq_fwht_quant_ws_bytes.restype = sz
     L.hatq_fwht_quant_act.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P, sz, P]
@@ -161,6 +164,12 @@ class PreparedLayer:
         off = self.w.bias - self.buf.data_ptr()
         return self.buf[off:off + 4 * self.w.cout_pad].view(torch.float32)
 
+    def wpack(self) -> torch.Tensor:
+        """int8 [pack_stride/64, cout_pad, 64] view of the kernel-order copy."""
+        off = self.w.wpack - self.buf.data_ptr()
+        n = self.w.cout_pad * self.w.pack_stride
+        return self.buf[off:off + n].view(self.w.pack_stride // 64, self.w.cout_pad, 64)
+
 
 def hatq_prepare_weights(d: ConvDesc, form, w: torch.Tensor, bias: Optional[torch.Tensor] = None,
                          stream=None) -> PreparedLayer:
@@ -175,6 +184,11 @@ def hatq_prepare_weights(d: ConvDesc, form, w: torch.Tensor, bias: Optional[torc
     _check(load().hatq_prepare_weights(ctypes.byref(d), f, _ptr(w), _ptr(b), _ptr(buf), nbytes,
                                        ctypes.byref(out), _stream(stream)), "hatq_prepare_weights")
     return PreparedLayer(buf, out, f)
+
+
+def hatq_pack_weights(layer: PreparedLayer, stream=None) -> None:
+    """Rebuild the kernel-order copy after codes were written into ``layer.wq()``."""
+    _check(load().hatq_pack_weights(ctypes.byref(layer.w), _stream(stream)), "hatq_pack_weights")
 
 
 def hatq_fwht_quant_act(x: torch.Tensor, hblock: int, absmax: Optional[torch.Tensor] = None,

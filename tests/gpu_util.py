@@ -13,6 +13,8 @@ intermediates), never GPU -> oracle.
 import numpy as np
 import torch
 
+from paper_2608_01653_amd import hatq
+
 DEV = "cuda:0"
 CODE_FLIP_FRACTION = 1e-4
 FP32_RANGE_REL = 1e-6
@@ -57,6 +59,21 @@ def set_codes(layer, wq_ohwi):
     buf = np.zeros((cout_p, ks), np.int8)
     buf[:, :kt] = wq_ohwi.reshape(cout_p, kt)
     layer.wq().copy_(dev(buf))
+    hatq.hatq_pack_weights(layer)   # the kernels read the K-blocked copy
+
+
+def expected_pack(wq_rows, k, cin_p, rowrun, pack_stride):
+    """The K-blocked kernel copy [pack_stride/64][cout_pad][64] of wq rows
+    [cout_pad][k_stride], built on the host from its definition in hatq.h."""
+    cout_p, ks = wq_rows.shape
+    rows = np.zeros((cout_p, pack_stride), np.int8)
+    if rowrun:
+        run = k * cin_p
+        for kh in range(k):
+            rows[:, 16 * kh:16 * kh + run] = wq_rows[:, kh * run:(kh + 1) * run]
+    else:
+        rows[:, :ks] = wq_rows
+    return rows.reshape(cout_p, pack_stride // 64, 64).transpose(1, 0, 2)
 
 
 def unpack_codes(layer, k, cin_p):

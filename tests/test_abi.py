@@ -100,7 +100,21 @@ def _fake_weights(cin=192, cout=192, k=5, s=2, p=2, hb=64, form=0, transposed=0,
     cin_p = -(-cin // hb) * hb if form == 0 else cin
     cout_p = -(-cout // hb) * hb if form == 1 else cout
     kt = k * k * cin_p
-    return hatq.Weights(d, form, cin_p, cout_p, kt, -(-kt // 64) * 64, 0x10000, 0x20000, 0x30000)
+    ks = -(-kt // 64) * 64
+    rowrun = not transposed and cin_p <= 4 and k * cin_p <= 16 and k <= 8 and s <= 2
+    ps = -(-16 * k // 64) * 64 if rowrun else ks
+    return hatq.Weights(d, form, cin_p, cout_p, kt, ks, 0x10000, 0x20000, 0x30000, 0x40000, ps)
+
+
+def test_pack_rejects_before_launch(L):
+    f = L.hatq_pack_weights
+    assert f(None, None) == hatq.HATQ_EINVAL
+    W = _fake_weights(cin=3, form=1)
+    W.pack_stride = W.k_stride + 64                    # inconsistent view
+    assert f(ctypes.byref(W), None) == hatq.HATQ_EINVAL
+    W = _fake_weights()
+    W.wpack = None
+    assert f(ctypes.byref(W), None) == hatq.HATQ_EINVAL
 
 
 def test_conv_rejects_before_launch(L):

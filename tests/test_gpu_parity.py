@@ -7,8 +7,8 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import (assert_codes, assert_range_rel, assert_scale_ulp, dev, host, set_codes,
-                      unpack_codes)
+from gpu_util import (assert_codes, assert_range_rel, assert_scale_ulp, dev, expected_pack, host,
+                      set_codes, unpack_codes)
 from paper_2608_01653_amd import hatq, synth
 
 pytestmark = pytest.mark.gpu
@@ -108,7 +108,15 @@ PREP = [  # (cin, cout, k, stride, pad, form, hblock, transposed, out_pad)
     (3, 192, 5, 2, 2, "WH", 64, False, 0),
     (192, 320, 5, 2, 2, "WH", 64, False, 0),
     (64, 64, 3, 2, 1, "WH", 16, True, 1),
+    (4, 128, 4, 2, 1, "DH", 4, False, 0),
+    (2, 128, 8, 2, 3, "WH", 64, False, 0),
+    (4, 64, 5, 2, 2, "WH", 64, False, 0),
 ]
+
+
+def _rowrun(cin_p, k, stride, transposed):
+    """Geometries whose kernel contracts one 16-byte run per kernel row."""
+    return not transposed and cin_p <= 4 and k * cin_p <= 16 and k <= 8 and stride <= 2
 
 
 @pytest.mark.parametrize("p", PREP, ids=[f"{p[0]}-{p[1]}-k{p[2]}-{p[5]}-b{p[6]}{'-T' if p[7] else ''}" for p in PREP])
@@ -122,6 +130,23 @@ def test_prepare_weights_bit_exact(orc, p):
     assert np.array_equal(unpack_codes(layer, k, ref.cin_p), ref.wq)
     assert np.array_equal(host(layer.w_scale()), ref.w_scale)
     assert np.array_equal(host(layer.bias()), ref.w_bias)
+    rr = _rowrun(ref.cin_p, k, s, tr)
+    assert layer.w.pack_stride == (-(-16 * k // 64) * 64 if rr else layer.w.k_stride)
+    assert np.array_equal(host(layer.wpack()),
+                          expected_pack(host(layer.wq()), k, ref.cin_p, rr, layer.w.pack_stride))
+
+
+def test_pack_weights_rebuilds_copy(orc):
+    """hatq_pack_weights after codes written into wq directly."""
+    p = PREP[4]
+    cin, cout, k, s, pad, form, hb, tr, op = p
+    rng = np.random.default_rng(5)
+    w, b = synth.layer_params(rng, cin, cout, k, tr)
+    layer = hatq.hatq_prepare_weights(hatq.desc(cin, cout, k, s, pad, hb, tr, op), form, dev(w), dev(b))
+    wq = synth.int8_codes(rng, (layer.cout_pad, k * k * layer.cin_pad))
+    set_codes(layer, wq)
+    assert np.array_equal(host(layer.wpack()),
+                          expected_pack(host(layer.wq()), k, layer.cin_pad, True, layer.w.pack_stride))
 
 
 # ----------------------------------------------------------------------- a5
@@ -135,6 +160,11 @@ CONV = [  # (n, h, w, cin, cout, k, stride, pad, transposed, out_pad, form, hblo
     (2, 5, 7, 64, 64, 5, 2, 2, True, 1, "WH", 64),
     (1, 19, 23, 64, 64, 3, 1, 1, False, 0, "DH", 64),
     (1, 17, 15, 64, 256, 3, 2, 1, False, 0, "DH", 64),
+    (1, 29, 31, 1, 64, 3, 1, 1, False, 0, "WH", 64),      # row-run, stride 1
+    (2, 20, 26, 4, 128, 4, 2, 1, False, 0, "DH", 4),      # row-run, 16-byte runs
+    (1, 23, 17, 2, 128, 8, 2, 3, False, 0, "WH", 64),     # row-run, two K-steps
+    (1, 21, 19, 3, 320, 5, 2, 2, False, 0, "WH", 64),     # row-run, 64-column tiles
+    (1, 18, 22, 4, 64, 5, 2, 2, False, 0, "WH", 64),      # byte-gather path (20-byte runs)
 ]
 CONV_IDS = [f"n{c[0]}-{c[1]}x{c[2]}-{c[3]}to{c[4]}-k{c[5]}s{c[6]}-{c[10]}{'-T' if c[8] else ''}" for c in CONV]
 
