@@ -14,8 +14,8 @@
 //
 // Epilogue, in registers: a 64-channel block of one pixel lies in four lanes
 // (see fwht_acc), so the dequantization (DH: y = fma(float(acc),
-// fl(s_x*s_w,c)*(1/b), bias_c); WH: z = fma(float(acc), fl(s_x*s_w,c), b~_c);
-// I32: raw), the WH output-basis restore (b-point FWHT times 1/b) and the next
+// fl(s_x*s_w,c)*(1/b), bias_c); WH: z/b = fma(float(acc), fl(s_x*s_w,c)*(1/b),
+// b~_c/b); I32: raw), the WH output-basis restore (b-point FWHT) and the next
 // layer's per-sample max |B_next y| run on the accumulators with no LDS round
 // trip, and each lane stores 16 B of one pixel.
 #include <utility>
@@ -56,16 +56,23 @@ __device__ __forceinline__ int64_t out_pixel(const ConvArgs &a, int nb, int gi, 
 }
 
 // Per-tile column factors of the dequantization (the tile is one sample, so
-// s_x is uniform): col_t[c] = fl(s_x*s_w,c) for WH, fl(fl(s_x*s_w,c) * (1/b))
-// for DH (exact power of two); col_b[c] = bias.  Written by the whole block.
+// s_x is uniform).  Both forms fold the exact factor 1/b in here:
+//   DH: y = fma(acc, t_c, bias_c)        with t_c = fl(fl(s_x*s_w,c) * (1/b));
+//   WH: z/b = fma(acc, t_c, b~_c * (1/b)), and y = B_Cout (z/b) = (B_Cout z)/b.
+// Scaling by a power of two commutes with every rounding (results far above
+// the subnormal range), so the WH output equals restoring z first and dividing
+// after, as the operator is defined.
+__device__ __forceinline__ void column_factor(const ConvArgs &a, float sxv, int c, float &t, float &b) {
+    const float inv_b = 1.0f / (float)a.hblock;
+    t = (sxv * a.w_scale[c]) * inv_b;
+    b = a.form == 1 ? a.bias[c] * inv_b : a.bias[c];
+}
+
+// Written by the whole block.
 template <int BN>
 __device__ __forceinline__ void column_factors(const ConvArgs &a, const Tile &t, float *col_t, float *col_b) {
     const float sxv = a.sx[t.nb];
-    const float f = a.form == 1 ? 1.0f : 1.0f / (float)a.hblock;
-    for (int c = threadIdx.x; c < BN; c += kThreads) {
-        col_t[c] = (sxv * a.w_scale[t.n0 + c]) * f;
-        col_b[c] = a.bias[t.n0 + c];
-    }
+    for (int c = threadIdx.x; c < BN; c += kThreads) column_factor(a, sxv, t.n0 + c, col_t[c], col_b[c]);
 }
 
 // ---- register epilogue ------------------------------------------------------
@@ -93,69 +100,179 @@ __device__ __forceinline__ void pair_swap(float &x, float &y) {
     }
 }
 
-// Butterfly across lane bit MASK on two registers at once: after one pair swap
-// every lane holds both partners (a: bit clear, c: bit set) of one pair, of x in
-// the lanes with the bit clear and of y in the others; a + c and a - c are
-// formed in-lane and a second swap puts them back in place.
-template <int MASK>
-__device__ __forceinline__ void cross_pair(float &x, float &y) {
-    pair_swap<MASK>(x, y);
-    const float s = x + y, d = x - y;
-    x = s;
-    y = d;
-    pair_swap<MASK>(x, y);
+// Butterfly across lane bit MASK on all 16 registers, taken two at a time:
+// after one pair swap every lane holds both partners (a: bit clear, c: bit
+// set) of one pair, of the first register in the lanes with the bit clear and
+// of the second in the others; a + c and a - c are formed in-lane.  With
+// RESTORE a second swap puts them back in place; without it the values stay
+// permuted among lanes and register pairs, which is enough where only their
+// maximum is needed (the later stages pair registers r and r+4, r+8 and lanes
+// l and l^32 in the same way in both layouts).
+template <int MASK, bool RESTORE>
+__device__ __forceinline__ void cross_stage_pairs(float (&v)[16]) {
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) pair_swap<MASK>(v[r], v[r + 1]);
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) {
+        const float s = v[r] + v[r + 1], d = v[r] - v[r + 1];
+        v[r] = s;
+        v[r + 1] = d;
+    }
+    if constexpr (RESTORE) {
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) pair_swap<MASK>(v[r], v[r + 1]);
+    }
 }
 
-// Runtime block size b <= 64 (wave-uniform branches).  All lanes of the wave
-// must be active.
+// Block size B <= 64 fixed at compile time (B = 1: no transform), so the
+// stages are straight-line code.  All lanes of the wave must be active.
+// B = -1: the block size b is taken at run time (wave-uniform branches); B = 0:
+// no transform.
+template <int B, bool RESTORE>
 __device__ __forceinline__ void fwht_acc(float (&v)[16], int b) {
-    if (b >= 2) reg_stage<1>(v);
-    if (b >= 4) reg_stage<2>(v);
-    if (b >= 8) {
-#pragma unroll
-        for (int r = 0; r < 16; r += 2) cross_pair<16>(v[r], v[r + 1]);
+    static_assert(B == -1 || B == 0 || (B >= 1 && B <= 64 && (B & (B - 1)) == 0), "block size");
+    if constexpr (B == -1) {
+        if (b >= 2) reg_stage<1>(v);
+        if (b >= 4) reg_stage<2>(v);
+        if (b >= 8) cross_stage_pairs<16, RESTORE>(v);
+        if (b >= 16) cross_stage_pairs<32, RESTORE>(v);
+        if (b >= 32) reg_stage<4>(v);
+        if (b >= 64) reg_stage<8>(v);
+    } else {
+        if constexpr (B >= 2) reg_stage<1>(v);
+        if constexpr (B >= 4) reg_stage<2>(v);
+        if constexpr (B >= 8) cross_stage_pairs<16, RESTORE>(v);
+        if constexpr (B >= 16) cross_stage_pairs<32, RESTORE>(v);
+        if constexpr (B >= 32) reg_stage<4>(v);
+        if constexpr (B >= 64) reg_stage<8>(v);
     }
-    if (b >= 16) {
-#pragma unroll
-        for (int r = 0; r < 16; r += 2) cross_pair<32>(v[r], v[r + 1]);
-    }
-    if (b >= 32) reg_stage<4>(v);
-    if (b >= 64) reg_stage<8>(v);
 }
 
 // row0: the wave's first local row in the tile (local row m = row0 + 16*i + p is
 // grid point (gi0 + m / TW, gj0 + m % TW)).  col_t / col_b: LDS column factors
 // (column_factors, followed by a block barrier).
-template <int TW, int FM, int FN>
-__device__ __forceinline__ void epilogue_regs(const ConvArgs &a, const v4i (&acc)[FM][FN], const Tile &t,
-                                              int row0, int lane, const float *col_t, const float *col_b) {
+// Epilogue variants, fixed per kernel instantiation so that each kernel holds
+// one straight-line body: WB is the block size of the WH restore (0: none) and
+// NB the block size of the next operand's absmax (0: not wanted), both for
+// fp32 output; WB = NB = -1 is the generic body, which takes the output mode,
+// form and block sizes from the arguments.
+template <int WB_, int NB_>
+struct Epi {
+    static constexpr int WB = WB_, NB = NB_;
+};
+using EpiGeneric = Epi<-1, -1>;
+
+// The variant a launch needs, or the generic one.
+template <typename E>
+bool epi_matches(const ConvArgs &a) {
+    if constexpr (E::WB == -1) {
+        return true;
+    } else {
+        const int wb = a.form == 1 ? a.hblock : 0;
+        const int nb = a.next_absmax != nullptr ? a.next_hblock : 0;
+        return a.mode == 1 && wb == E::WB && nb == E::NB;
+    }
+}
+
+// Values of one output row group after the epilogue arithmetic: out[i][k][*]
+// is the 64-channel block k of the lane's pixel in group i, in the accumulator
+// layout (v[4*jj + r]: channel 64*k + 16*jj + 4*q + r).
+template <int FM, int FN>
+using EpiVals = float[FM][FN / 4][16];
+
+template <typename E>
+struct EpiFlags {
+    static constexpr int WB = E::WB, NB = E::NB;
+    static constexpr bool generic = WB == -1;
+    bool f32, wh, want_abs;
+    __device__ explicit EpiFlags(const ConvArgs &a) {
+        f32 = generic ? a.mode != 0 : true;
+        wh = generic ? f32 && a.form == 1 : WB != 0;
+        want_abs = generic ? f32 && a.next_absmax != nullptr && a.next_hblock > 0 : NB != 0;
+    }
+};
+
+// Stores 64-channel block k of group i: each lane writes 16 B (four channels)
+// of its pixel per fragment.
+template <int TW, int FN, typename E>
+__device__ __forceinline__ void store_group_impl(const ConvArgs &a, const Tile &t, int row0, int lane, int i, int k,
+                                                 const float (&v)[16]) {
+    const int p = lane & 15, q = lane >> 4;
+    const EpiFlags<E> fl(a);
+    const int ycols = fl.f32 ? a.cout : a.cout_pad;
+    const int ncols = ycols - t.n0 < 16 * FN ? ycols - t.n0 : 16 * FN;
+    const int m = row0 + 16 * i + p;
+    const int gi = t.gi0 + m / TW, gj = t.gj0 + m % TW;
+    float *yp = reinterpret_cast<float *>(a.y) + out_pixel(a, t.nb, gi, gj) * ycols + t.n0;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+        const int cl = 64 * k + 16 * jj + 4 * q;
+        if ((ycols & 3) == 0) {
+            if (cl < ncols)
+                *reinterpret_cast<float4 *>(yp + cl) = make_float4(v[4 * jj], v[4 * jj + 1], v[4 * jj + 2], v[4 * jj + 3]);
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                if (cl + r < ncols) yp[cl + r] = v[4 * jj + r];
+        }
+    }
+}
+#define store_group(a, t, row0, lane, i, k, v) store_group_impl<TW, FN, E>(a, t, row0, lane, i, k, v)
+
+// The arithmetic: dequantization, WH restore, next-operand absmax (one atomic
+// per wave at most).  With STORE each group is stored as soon as it is final
+// (stores interleave with the arithmetic); without, out holds the values for
+// epilogue_store.
+template <int TW, int FM, int FN, typename E, bool STORE = false>
+__device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&acc)[FM][FN], const Tile &t,
+                                                 int row0, int lane, const float *col_t, const float *col_b,
+                                                 EpiVals<FM, FN> &out) {
     static_assert(FN % 4 == 0, "whole 64-channel blocks");
+    constexpr int WB = E::WB, NB = E::NB;
+    constexpr bool generic = WB == -1;
     constexpr int NBLK = FN / 4;
     const int p = lane & 15, q = lane >> 4;
-    const bool f32 = a.mode != 0;
-    const bool wh = f32 && a.form == 1;
-    const bool want_abs = f32 && a.next_absmax != nullptr && a.next_hblock > 0;
-    const float inv_b = 1.0f / (float)a.hblock;
-    const int ycols = f32 ? a.cout : a.cout_pad;
-    const int ncols = ycols - t.n0 < 16 * FN ? ycols - t.n0 : 16 * FN;
-    const bool vec = (ycols & 3) == 0;
+    const EpiFlags<E> fl(a);
+    const bool f32 = fl.f32, wh = fl.wh, want_abs = fl.want_abs;
     // the whole tile inside the grid (wave-uniform): no row masking needed
     const bool full = t.gi0 + (row0 + 16 * FM - 1) / TW < a.gh && t.gj0 + TW <= a.gw;
     float wave_m = 0.0f;
-    // published running maximum of this sample, read early (used at the end)
+    // Published running maximum of this sample (read once; a stale value only
+    // costs work).  A group whose rigorous upper bound on max |B_next y| stays
+    // below it cannot raise the maximum, so its exact transform is skipped.
     float seen = -1.0f;
-    if (want_abs && lane == 0)
-        seen = __uint_as_float(__hip_atomic_load(reinterpret_cast<unsigned int *>(a.next_absmax + t.nb),
-                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    if (want_abs) {
+        if (lane == 0)
+            seen = __uint_as_float(__hip_atomic_load(reinterpret_cast<unsigned int *>(a.next_absmax + t.nb),
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        seen = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(seen)));
+    }
+    const int nbk = generic ? a.next_hblock : NB;
+    // WH layer whose next operand uses the same blocks: B y = B (B z / b) = z
+    // exactly, so max|B y| <= max|z| (1 + 2 gamma_6 * 64) with gamma_6 the
+    // six-stage fp32 rounding factor (< 3.6e-7); 1 + 1e-4 covers it.
+    const bool z_bound = wh && (generic ? a.hblock == a.next_hblock : WB == NB);
+    bool valid[FM];
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
         const int m = row0 + 16 * i + p;
-        const int gi = t.gi0 + m / TW, gj = t.gj0 + m % TW;
-        const bool valid = gi < a.gh && gj < a.gw;
-        float *yp = reinterpret_cast<float *>(a.y) + (valid ? out_pixel(a, t.nb, gi, gj) * ycols + t.n0 : 0);
+        valid[i] = t.gi0 + m / TW < a.gh && t.gj0 + m % TW < a.gw;
+    }
+    // 64-channel blocks outermost: one set of column factors serves all FM groups
 #pragma unroll
-        for (int k = 0; k < NBLK; ++k) {
-            float v[16];
+    for (int k = 0; k < NBLK; ++k) {
+        float4 t4[4], b4[4];
+        if (f32) {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int cl = 64 * k + 16 * jj + 4 * q;
+                t4[jj] = *reinterpret_cast<const float4 *>(col_t + cl);
+                b4[jj] = *reinterpret_cast<const float4 *>(col_b + cl);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            float (&v)[16] = out[i][k];
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
                 const v4i c4 = acc[i][4 * k + jj];
@@ -163,22 +280,44 @@ __device__ __forceinline__ void epilogue_regs(const ConvArgs &a, const v4i (&acc
 #pragma unroll
                     for (int r = 0; r < 4; ++r) v[4 * jj + r] = __int_as_float(c4[r]);
                 } else {
-                    const int cl = 64 * k + 16 * jj + 4 * q;
-                    const float4 t4 = *reinterpret_cast<const float4 *>(col_t + cl);
-                    const float4 b4 = *reinterpret_cast<const float4 *>(col_b + cl);
-                    v[4 * jj + 0] = __builtin_fmaf((float)c4[0], t4.x, b4.x);
-                    v[4 * jj + 1] = __builtin_fmaf((float)c4[1], t4.y, b4.y);
-                    v[4 * jj + 2] = __builtin_fmaf((float)c4[2], t4.z, b4.z);
-                    v[4 * jj + 3] = __builtin_fmaf((float)c4[3], t4.w, b4.w);
+                    v[4 * jj + 0] = __builtin_fmaf((float)c4[0], t4[jj].x, b4[jj].x);
+                    v[4 * jj + 1] = __builtin_fmaf((float)c4[1], t4[jj].y, b4[jj].y);
+                    v[4 * jj + 2] = __builtin_fmaf((float)c4[2], t4[jj].z, b4[jj].z);
+                    v[4 * jj + 3] = __builtin_fmaf((float)c4[3], t4[jj].w, b4[jj].w);
                 }
             }
-            if (wh) {
-                fwht_acc(v, a.hblock);
+            // bound on this lane's share of max |B_next y| (see above)
+            float zmax = 0.0f;
+            if (want_abs && z_bound) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r) v[r] *= inv_b;
+                for (int r = 0; r < 16; ++r) zmax = fmaxf(zmax, fabsf(v[r]));
+                zmax *= (float)a.hblock;   // v holds z / b
             }
-            if (want_abs) {
-                // rows past the grid and channels past cout are not part of the next operand
+            if (wh) fwht_acc<WB, true>(v, a.hblock);   // the column factors carry the 1/b
+            if constexpr (STORE) {
+                if (valid[i]) store_group(a, t, row0, lane, i, k, v);
+            }
+            // (channels past cout are zeroed before the exact transform, which
+            // breaks B y = z for a block that holds some)
+            bool exact = want_abs;
+            if (want_abs && nbk > 1 && z_bound && t.n0 + 64 * k + 64 <= a.cout)
+                exact = __builtin_amdgcn_ballot_w64(zmax * 1.0001f + 1e-30f >= seen) != 0;
+            if (NB == 1 && exact) {
+                // no transform: the maximum of |y| over the valid values
+                const bool all = full && t.n0 + 64 * k + 64 <= a.cout;
+                float mm = 0.0f;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int ch = t.n0 + 64 * k + 16 * jj + 4 * q + r;
+                        const bool in = all || (valid[i] && ch < a.cout);
+                        mm = fmaxf(mm, in ? fabsf(v[4 * jj + r]) : 0.0f);
+                    }
+                wave_m = fmaxf(wave_m, mm);
+            } else if (exact) {
+                // Rows past the grid and channels past cout are not part of the
+                // next operand.
                 float u[16];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) u[r] = v[r];
@@ -188,40 +327,45 @@ __device__ __forceinline__ void epilogue_regs(const ConvArgs &a, const v4i (&acc
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             const int ch = t.n0 + 64 * k + 16 * jj + 4 * q + r;
-                            if (!valid || ch >= a.cout) u[4 * jj + r] = 0.0f;
+                            if (!valid[i] || ch >= a.cout) u[4 * jj + r] = 0.0f;
                         }
                 }
-                fwht_acc(u, a.next_hblock);
+                fwht_acc<NB, false>(u, a.next_hblock);
                 float mm = 0.0f;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(u[r]));
                 wave_m = fmaxf(wave_m, mm);
-            }
-            if (valid) {
-#pragma unroll
-                for (int jj = 0; jj < 4; ++jj) {
-                    const int cl = 64 * k + 16 * jj + 4 * q;
-                    if (vec) {
-                        if (cl < ncols)
-                            *reinterpret_cast<float4 *>(yp + cl) =
-                                make_float4(v[4 * jj], v[4 * jj + 1], v[4 * jj + 2], v[4 * jj + 3]);
-                    } else {
-#pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            if (cl + r < ncols) yp[cl + r] = v[4 * jj + r];
-                    }
-                }
             }
         }
     }
     if (want_abs) {
         wave_m = wave_max(wave_m);
         // The running maximum only grows, so a wave whose maximum does not exceed
-        // a value already published skips its atomic (the read may be stale, which
-        // costs at most an unneeded atomic).  Device-scope atomics on one address
-        // serialize, and most waves of a layer end up skipping.
+        // a value already published skips its atomic.  Device-scope atomics on
+        // one address serialize, and most waves of a layer end up skipping.
         if (lane == 0 && wave_m > seen) atomic_max_nonneg(a.next_absmax + t.nb, wave_m);
     }
+}
+
+// The stores of values computed by epilogue_compute without STORE.
+template <int TW, int FM, int FN, typename E>
+__device__ __forceinline__ void epilogue_store(const ConvArgs &a, const Tile &t, int row0, int lane,
+                                               const EpiVals<FM, FN> &out) {
+    const int p = lane & 15;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int m = row0 + 16 * i + p;
+        if (t.gi0 + m / TW >= a.gh || t.gj0 + m % TW >= a.gw) continue;
+#pragma unroll
+        for (int k = 0; k < FN / 4; ++k) store_group_impl<TW, FN, E>(a, t, row0, lane, i, k, out[i][k]);
+    }
+}
+
+template <int TW, int FM, int FN, typename E>
+__device__ __forceinline__ void epilogue_regs(const ConvArgs &a, const v4i (&acc)[FM][FN], const Tile &t,
+                                              int row0, int lane, const float *col_t, const float *col_b) {
+    EpiVals<FM, FN> out;
+    epilogue_compute<TW, FM, FN, E, true>(a, acc, t, row0, lane, col_t, col_b, out);
 }
 
 // Block index -> tile, XCD aware: blocks bid, bid+8, ... run on one XCD; each
@@ -239,155 +383,194 @@ __device__ __forceinline__ int xcd_logical_tile() {
 // stride <= 2): in NHWC the taps kw = 0..k-1 of one kernel row kh are k*cin_p
 // consecutive input bytes, so the contraction is taken as one 16-byte run per
 // kernel row, d' = 16*kh + (kw*cin_p + ci) (weights zero past k*cin_p and past
-// kh = k-1).  A block stages its input patch (zero outside the image) and the
-// whole weight tile in LDS; lane group g of a fragment holds the run of kernel
-// row 4*ks + g, read unaligned from the patch with byte funnel shifts.
-// Accumulators stay small (two 16-point groups per wave) so two blocks share a
-// CU and one block's stores overlap the other's loads and MFMAs.
+// kh = k-1).  Lane group g of a fragment holds the run of kernel row 4*ks + g,
+// read unaligned from an LDS copy of the input patch with byte funnel shifts.
+//
+// A block walks a run of RUN consecutive TH x TW tiles of one sample and one
+// column tile: the weight tile and the column factors are staged once, and the
+// next tile's patch is fetched while the current tile's epilogue runs (two
+// patch buffers).  Accumulators stay small (two 16-point groups per wave) so
+// two blocks share a CU.
 // ---------------------------------------------------------------------------
-template <int TH, int TW, int BN, int CIN>
+template <int TH, int TW, int CIN>
+struct RowRunPatch {
+    static constexpr int PH = (TH - 1) * 2 + 8;                 // patch rows (stride <= 2, k <= 8)
+    static constexpr int PWB = ((TW - 1) * 2 + 8) * CIN;        // patch bytes per row
+    static constexpr int RS = (PWB + 3 + 20 + 15) / 16 * 16;    // LDS row stride: alignment shift + 20-byte reads
+    static constexpr int RW = RS / 4;
+    static constexpr int WORDS = PH * RW;
+    static constexpr int PIT = (WORDS + kThreads - 1) / kThreads;
+};
+
+constexpr int kRowRunTiles = 4;   // tiles per block
+
+template <int TH, int TW, int BN, int CIN, typename E>
 __global__ void __launch_bounds__(kThreads, 2) conv_rowrun_kernel(const ConvArgs a) {
     constexpr int BM = TH * TW;
     constexpr int TM = BM / 4;
     constexpr int FM = TM / 16;
     constexpr int FN = BN / 16;
-    constexpr int PH = (TH - 1) * 2 + 8;                 // patch rows (stride <= 2, k <= 8)
-    constexpr int PWB = ((TW - 1) * 2 + 8) * CIN;        // patch bytes per row
-    constexpr int RS = (PWB + 3 + 20 + 15) / 16 * 16;    // LDS row stride: alignment shift + 20-byte reads
-    constexpr int RW = RS / 4;
-    constexpr int PWORDS = PH * RW;
-    constexpr int PIT = (PWORDS + kThreads - 1) / kThreads;
+    using P = RowRunPatch<TH, TW, CIN>;
+    constexpr int RS = P::RS, RW = P::RW, PWORDS = P::WORDS, PIT = P::PIT;
     constexpr int BIT = 2 * BN * 4 / kThreads;
     static_assert(TM % 16 == 0 && TW % 16 == 0 && BN % 64 == 0 && 2 * BN * 4 % kThreads == 0, "tile");
+    static_assert(BN <= kThreads, "one column per thread");
     __shared__ __attribute__((aligned(16))) int8_t s_b[2 * BN * 64];
-    __shared__ uint32_t s_patch[PWORDS];
+    __shared__ uint32_t s_patch[2][PWORDS];
     __shared__ __attribute__((aligned(16))) float s_col[2 * BN];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const Tile tile = block_tile(a, xcd_logical_tile(), TH, TW, BN);
     const int nks = a.nksteps;   // 1 or 2 (pack_stride / 64)
-    const int ih0 = tile.gi0 * a.sa + a.bah, iw0 = tile.gj0 * a.sa + a.baw;
-    const int prow = (TH - 1) * a.sa + a.k;   // patch rows in use
-    const int pcols = (TW - 1) * a.sa + a.k;  // patch columns in use
-    // Patch row r holds the input bytes of row ih0 + r from the 4-aligned address
-    // at or below its first byte (pixel iw0), so it is fetched as aligned dwords;
-    // the row's alignment shift is (first byte address) mod 4.  Buffer offsets
-    // below 0 or past the input wrap or exceed num_records and read 0; every
-    // byte outside the image is masked to 0 anyway.
-    auto row_shift = [&](int r) -> int {
-        const uint32_t g = ((uint32_t)(tile.nb * a.h + ih0 + r) * (uint32_t)a.w + (uint32_t)iw0) * (uint32_t)CIN;
-        return (int)(g & 3u);
+
+    // this block's run: sample nb, column tile n0, tiles t_first .. t_first+cnt-1
+    // of the sample (row-major over tiles_h x tiles_w)
+    const int per = a.tiles_h * a.tiles_w;
+    const int runs = (per + kRowRunTiles - 1) / kRowRunTiles;
+    const int logical = xcd_logical_tile();
+    const int rn = logical / a.tiles_n;
+    const int n0 = (logical - rn * a.tiles_n) * BN;
+    const int nb = rn / runs;
+    const int t_first = (rn - nb * runs) * kRowRunTiles;
+    const int cnt = per - t_first < kRowRunTiles ? per - t_first : kRowRunTiles;
+    auto tile_of = [&](int t) {
+        Tile tl;
+        tl.nb = nb;
+        tl.n0 = n0;
+        const int th = t / a.tiles_w;
+        tl.gi0 = th * TH;
+        tl.gj0 = (t - th * a.tiles_w) * TW;
+        return tl;
     };
 
-    // ---- every global load of the prologue is issued before the first wait ----
-    v4i wb[BIT];
-#pragma unroll
-    for (int it = 0; it < BIT; ++it) {
-        const int pc = tid + it * kThreads;
-        const int ks = pc / (BN * 4), rem = pc - ks * (BN * 4);
-        wb[it] = v4i{0, 0, 0, 0};
-        if (ks < nks)
-            wb[it] = *reinterpret_cast<const v4i *>(a.wp + ((int64_t)ks * a.cout_pad + tile.n0 + (rem >> 2)) * 64 +
-                                                    16 * (rem & 3));
-    }
+    const int prow = (TH - 1) * a.sa + a.k;   // patch rows in use
+    const int pcols = (TW - 1) * a.sa + a.k;  // patch columns in use
     const int64_t in_bytes = (int64_t)a.n * a.h * a.w * CIN;
     const __amdgpu_buffer_rsrc_t rx =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t *>(a.xq), (short)0, (int)in_bytes, 0x00020000);
-    uint32_t pwd[PIT];
+    // Patch row r of a tile holds the input bytes of row ih0 + r from the
+    // 4-aligned address at or below its first byte (pixel iw0), fetched as
+    // aligned dwords; the row's alignment shift is (first byte address) mod 4.
+    auto row_shift = [&](int ih, int iw0) -> int {
+        const uint32_t g = ((uint32_t)(nb * a.h + ih) * (uint32_t)a.w + (uint32_t)iw0) * (uint32_t)CIN;
+        return (int)(g & 3u);
+    };
+    // every load of a patch at once (no branches): rows outside the image use an
+    // out-of-range offset and read 0
+    auto patch_load = [&](const Tile &tl, uint32_t (&pwd)[PIT]) {
+        const int ih0 = tl.gi0 * a.sa + a.bah, iw0 = tl.gj0 * a.sa + a.baw;
 #pragma unroll
-    for (int it = 0; it < PIT; ++it) {
-        const int e4 = tid + it * kThreads;
-        const int r = e4 / RW, wi = e4 - r * RW;
-        const int ih = ih0 + r;
-        pwd[it] = 0;
-        if (e4 < PWORDS && r < prow && (unsigned)ih < (unsigned)a.h) {
-            const int sh = row_shift(r);
-            const int64_t ga = ((int64_t)(tile.nb * a.h + ih) * a.w + iw0) * CIN - sh + 4 * wi;
-            uint32_t word;
-            if (ga + 4 <= in_bytes) {
-                word = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rx, (int)(uint32_t)ga, 0, 0);
-            } else {
-                // the dword straddling the end of the input (the range check would
-                // drop all of it): its bytes one by one
-                word = 0;
-                for (int e = 0; e < 4; ++e)
-                    if (ga + e >= 0 && ga + e < in_bytes) word |= (uint32_t)(uint8_t)a.xq[ga + e] << (8 * e);
-            }
-            uint32_t mask = 0;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int rel = 4 * wi + e - sh;   // byte index from pixel iw0
-                const int c = rel / CIN;
-                if (rel >= 0 && c < pcols && (unsigned)(iw0 + c) < (unsigned)a.w) mask |= 0xFFu << (8 * e);
-            }
-            pwd[it] = word & mask;
+        for (int it = 0; it < PIT; ++it) {
+            const int e4 = tid + it * kThreads;
+            const int r = e4 / RW, wi = e4 - r * RW;
+            const int ih = ih0 + r;
+            const bool live = e4 < PWORDS && r < prow && (unsigned)ih < (unsigned)a.h;
+            const int64_t ga = ((int64_t)(nb * a.h + ih) * a.w + iw0) * CIN + 4 * wi - row_shift(ih, iw0);
+            pwd[it] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rx, (int)(live ? (uint32_t)ga : 0xFFFFFFFFu),
+                                                                     0, 0);
         }
-    }
-    float colv_t = 0.0f, colv_b = 0.0f;
-    if (tid < BN) {
-        const float f = a.form == 1 ? 1.0f : 1.0f / (float)a.hblock;
-        colv_t = (a.sx[tile.nb] * a.w_scale[tile.n0 + tid]) * f;
-        colv_b = a.bias[tile.n0 + tid];
-    }
-    // ---- LDS ----
+    };
+    // then the masks (bytes of columns inside both the patch and the image) and
+    // the LDS copy.  The range check drops the whole dword that straddles the end
+    // of the input; its bytes are read one by one.
+    auto patch_store = [&](const Tile &tl, uint32_t (&pwd)[PIT], uint32_t *dst) {
+        const int ih0 = tl.gi0 * a.sa + a.bah, iw0 = tl.gj0 * a.sa + a.baw;
+        const int vlo = (iw0 < 0 ? -iw0 : 0) * CIN;
+        const int vhi = (pcols < a.w - iw0 ? pcols : a.w - iw0) * CIN;
 #pragma unroll
-    for (int it = 0; it < BIT; ++it) {
-        const int pc = tid + it * kThreads;
-        const int ks = pc / (BN * 4), rem = pc - ks * (BN * 4);
-        const int nn = rem >> 2, g = rem & 3;
-        *reinterpret_cast<v4i *>(s_b + ks * BN * 64 + nn * 64 + 16 * (g ^ swz(nn))) = wb[it];
-    }
+        for (int it = 0; it < PIT; ++it) {
+            const int e4 = tid + it * kThreads;
+            const int r = e4 / RW, wi = e4 - r * RW;
+            const int ih = ih0 + r;
+            const bool live = e4 < PWORDS && r < prow && (unsigned)ih < (unsigned)a.h;
+            const int rel0 = 4 * wi - row_shift(ih, iw0);   // byte index of byte 0 from pixel iw0
+            const int64_t ga = ((int64_t)(nb * a.h + ih) * a.w + iw0) * CIN + rel0;
+            uint32_t word = pwd[it];
+            if (live && ga + 4 > in_bytes) {
+                word = 0;
+                for (int e = 0; e < 4 && ga + e < in_bytes; ++e)
+                    word |= (uint32_t)(uint8_t)a.xq[ga + e] << (8 * e);
+            }
+            const int lo = live ? min(max(vlo - rel0, 0), 4) : 4, hi = min(max(vhi - rel0, 0), 4);
+            const uint64_t keep = ((1ull << (8 * hi)) - 1) & ~((1ull << (8 * lo)) - 1);
+            if (e4 < PWORDS) dst[e4] = word & (uint32_t)keep;
+        }
+    };
+
+    // ---- once per block: weight tile, column factors, first patch ----
+    uint32_t pwd[PIT];
+    {
+        v4i wb[BIT];
 #pragma unroll
-    for (int it = 0; it < PIT; ++it) {
-        const int e4 = tid + it * kThreads;
-        if (e4 < PWORDS) s_patch[e4] = pwd[it];
-    }
-    static_assert(BN <= kThreads, "one column per thread");
-    if (tid < BN) {
-        s_col[tid] = colv_t;
-        s_col[BN + tid] = colv_b;
+        for (int it = 0; it < BIT; ++it) {
+            const int pc = tid + it * kThreads;
+            const int ks = pc / (BN * 4), rem = pc - ks * (BN * 4);
+            wb[it] = v4i{0, 0, 0, 0};
+            if (ks < nks)
+                wb[it] = *reinterpret_cast<const v4i *>(a.wp + ((int64_t)ks * a.cout_pad + n0 + (rem >> 2)) * 64 +
+                                                        16 * (rem & 3));
+        }
+        patch_load(tile_of(t_first), pwd);
+        float colv_t = 0.0f, colv_b = 0.0f;
+        if (tid < BN) column_factor(a, a.sx[nb], n0 + tid, colv_t, colv_b);
+#pragma unroll
+        for (int it = 0; it < BIT; ++it) {
+            const int pc = tid + it * kThreads;
+            const int ks = pc / (BN * 4), rem = pc - ks * (BN * 4);
+            const int nn = rem >> 2, g = rem & 3;
+            *reinterpret_cast<v4i *>(s_b + ks * BN * 64 + nn * 64 + 16 * (g ^ swz(nn))) = wb[it];
+        }
+        if (tid < BN) {
+            s_col[tid] = colv_t;
+            s_col[BN + tid] = colv_b;
+        }
+        patch_store(tile_of(t_first), pwd, s_patch[0]);
     }
     __syncthreads();
 
     const int fr = lane & 15, fg = lane >> 4;
-    int poff[FM];   // patch byte of the run of kernel row 0 for this lane's points
+    for (int it = 0; it < cnt; ++it) {
+        const Tile tile = tile_of(t_first + it);
+        const bool more = it + 1 < cnt;
+        if (more) patch_load(tile_of(t_first + it + 1), pwd);   // lands during this tile's work
+        const uint32_t *patch = s_patch[it & 1];
+        const int ih0 = tile.gi0 * a.sa + a.bah, iw0 = tile.gj0 * a.sa + a.baw;
+        v4i acc[FM][FN];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int m = wave * TM + 16 * i + fr;
-        const int ohl = m / TW, owl = m - ohl * TW;
-        poff[i] = a.sa * ohl * RS + a.sa * owl * CIN;   // + row shift, added per kernel row below
-    }
-    v4i acc[FM][FN];
+        for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+            for (int j = 0; j < FN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+        for (int ks = 0; ks < nks; ++ks) {
+            // kernel row 4*ks + fg <= 7 stays inside the patch; rows >= k meet zero weights
+            const int kh = 4 * ks + fg;
+            v4i fa[FM];
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
-    for (int ks = 0; ks < nks; ++ks) {
-        // kernel row 4*ks + fg <= 7 stays inside the patch; rows >= k meet zero weights
-        const int kh = 4 * ks + fg;
-        v4i fa[FM];
+            for (int i = 0; i < FM; ++i) {
+                const int m = wave * TM + 16 * i + fr;
+                const int ohl = m / TW, owl = m - ohl * TW;
+                const int row = a.sa * ohl + kh;
+                const int off = row * RS + a.sa * owl * CIN + row_shift(ih0 + row, iw0);
+                const uint32_t *pw = patch + (off >> 2);
+                const uint32_t sh = off & 3;
+                const uint32_t d0 = pw[0], d1 = pw[1], d2 = pw[2], d3 = pw[3], d4 = pw[4];
+                fa[i] = v4i{(int)__builtin_amdgcn_alignbyte(d1, d0, sh), (int)__builtin_amdgcn_alignbyte(d2, d1, sh),
+                            (int)__builtin_amdgcn_alignbyte(d3, d2, sh), (int)__builtin_amdgcn_alignbyte(d4, d3, sh)};
+            }
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            const int m = wave * TM + 16 * i + fr;
-            const int off = poff[i] + kh * RS + row_shift(a.sa * (m / TW) + kh);
-            const uint32_t *pw = s_patch + (off >> 2);
-            const uint32_t sh = off & 3;
-            const uint32_t d0 = pw[0], d1 = pw[1], d2 = pw[2], d3 = pw[3], d4 = pw[4];
-            fa[i] = v4i{(int)__builtin_amdgcn_alignbyte(d1, d0, sh), (int)__builtin_amdgcn_alignbyte(d2, d1, sh),
-                        (int)__builtin_amdgcn_alignbyte(d3, d2, sh), (int)__builtin_amdgcn_alignbyte(d4, d3, sh)};
+            for (int j = 0; j < FN; ++j) {
+                const int nn = 16 * j + fr;
+                const v4i fb = *reinterpret_cast<const v4i *>(s_b + ks * BN * 64 + nn * 64 + 16 * (fg ^ swz(nn)));
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fb, fa[i], acc[i][j], 0, 0, 0);
+            }
         }
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int nn = 16 * j + fr;
-            const v4i fb = *reinterpret_cast<const v4i *>(s_b + ks * BN * 64 + nn * 64 + 16 * (fg ^ swz(nn)));
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fb, fa[i], acc[i][j], 0, 0, 0);
-        }
+        epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, s_col, s_col + BN);
+        // the other buffer was last read before the previous barrier
+        if (more) patch_store(tile_of(t_first + it + 1), pwd, s_patch[(it + 1) & 1]);
+        __syncthreads();
     }
-    epilogue_regs<TW, FM, FN>(a, acc, tile, wave * TM, lane, s_col, s_col + BN);
 }
 
 // ---------------------------------------------------------------------------
@@ -395,7 +578,7 @@ __global__ void __launch_bounds__(kThreads, 2) conv_rowrun_kernel(const ConvArgs
 // values gathered byte by byte (tap / channel from a lookup table), through
 // registers into a double-buffered LDS tile.
 // ---------------------------------------------------------------------------
-template <int TH, int TW, int BN, int CIN_SMALL>
+template <int TH, int TW, int BN, int CIN_SMALL, typename E>
 __global__ void __launch_bounds__(kThreads, 1) conv_gather_kernel(const ConvArgs a) {
     constexpr int BM = TH * TW;
     constexpr int TM = BM / 4;
@@ -534,7 +717,7 @@ __global__ void __launch_bounds__(kThreads, 1) conv_gather_kernel(const ConvArgs
     float *col = reinterpret_cast<float *>(lds);
     column_factors<BN>(a, tile, col, col + BN);
     __syncthreads();
-    epilogue_regs<TW, FM, FN>(a, acc, tile, wave * TM, lane, col, col + BN);
+    epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, col, col + BN);
 }
 
 // Fill the tile counts of a launch over TH x TW tiles; returns the block count.
@@ -545,21 +728,47 @@ int64_t set_tiles(ConvArgs &b, int TH, int TW, int BN) {
     return (int64_t)b.n * b.tiles_h * b.tiles_w * b.tiles_n;
 }
 
-template <int TH, int TW, int BN, int CS>
+// Launch with the first epilogue variant of Es that matches (the last must be
+// EpiGeneric).
+template <typename E, typename... Es, typename L>
+hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
+    if constexpr (sizeof...(Es) == 0) {
+        static_assert(E::WB == -1, "the generic variant comes last");
+        return launch(E{});
+    } else {
+        if (epi_matches<E>(a)) return launch(E{});
+        return with_epilogue<Es...>(a, launch);
+    }
+}
+
+// Variants compiled for the layer shapes of the analysis transforms: DH or WH
+// blocks of 64, next operand blocked by 64 (DH next), 1 (WH next) or none.
+#define HATQ_HOT_EPILOGUES Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, EpiGeneric
+
+template <int TH, int TW, int BN, int CS, typename E>
 hipError_t launch_rowrun(const ConvArgs &a, hipStream_t st) {
     ConvArgs b = a;
     const int64_t tiles = set_tiles(b, TH, TW, BN);
-    if (tiles <= 0 || tiles >= ((int64_t)1 << 31) || b.nksteps < 1 || b.nksteps > 2 || b.sa > 2)
-        return hipErrorInvalidValue;
-    conv_rowrun_kernel<TH, TW, BN, CS><<<(unsigned)tiles, kThreads, 0, st>>>(b);
+    if (tiles <= 0 || b.nksteps < 1 || b.nksteps > 2 || b.sa > 2 || b.k > 8) return hipErrorInvalidValue;
+    // every byte offset of the input fits the 32-bit buffer range
+    if ((int64_t)b.n * b.h * b.w * CS >= ((int64_t)1 << 31) - 64) return hipErrorInvalidValue;
+    const int64_t per = (int64_t)b.tiles_h * b.tiles_w;
+    const int64_t blocks = (int64_t)b.n * ((per + kRowRunTiles - 1) / kRowRunTiles) * b.tiles_n;
+    if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    conv_rowrun_kernel<TH, TW, BN, CS, E><<<(unsigned)blocks, kThreads, 0, st>>>(b);
     return hipGetLastError();
 }
 
 template <int CS>
 hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
-    if (a.cout_pad % 192 == 0) return launch_rowrun<2, 64, 192, CS>(a, st);
-    if (a.cout_pad % 128 == 0) return launch_rowrun<2, 64, 128, CS>(a, st);
-    return launch_rowrun<2, 64, 64, CS>(a, st);
+    if (a.cout_pad % 192 == 0) {
+        if constexpr (CS == 3)
+            return with_epilogue<HATQ_HOT_EPILOGUES>(
+                a, [&](auto e) { return launch_rowrun<2, 64, 192, CS, decltype(e)>(a, st); });
+        return launch_rowrun<2, 64, 192, CS, EpiGeneric>(a, st);
+    }
+    if (a.cout_pad % 128 == 0) return launch_rowrun<2, 64, 128, CS, EpiGeneric>(a, st);
+    return launch_rowrun<2, 64, 64, CS, EpiGeneric>(a, st);
 }
 
 template <int TH, int TW, int BN, int CS>
@@ -567,7 +776,7 @@ hipError_t launch_gather(const ConvArgs &a, hipStream_t st) {
     ConvArgs b = a;
     const int64_t tiles = set_tiles(b, TH, TW, BN);
     if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-    conv_gather_kernel<TH, TW, BN, CS><<<(unsigned)tiles, kThreads, 0, st>>>(b);
+    conv_gather_kernel<TH, TW, BN, CS, EpiGeneric><<<(unsigned)tiles, kThreads, 0, st>>>(b);
     return hipGetLastError();
 }
 
@@ -610,7 +819,7 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | 0x70 | 0xF00 | ((N >> 4) << 14));
 }
 
-template <int TH, int TW, int BN, int STAGES>
+template <int TH, int TW, int BN, int STAGES, typename E>
 __global__ void __launch_bounds__(kThreads, 1) conv_pipe_kernel(const ConvArgs a) {
     constexpr int BM = TH * TW;
     constexpr int TM = BM / 4;
@@ -749,10 +958,10 @@ __global__ void __launch_bounds__(kThreads, 1) conv_pipe_kernel(const ConvArgs a
     float *col = reinterpret_cast<float *>(lds);
     column_factors<BN>(a, tile, col, col + BN);
     __syncthreads();
-    epilogue_regs<TW, FM, FN>(a, acc, tile, wave * TM, lane, col, col + BN);
+    epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, col, col + BN);
 }
 
-template <int TH, int TW, int BN, int STAGES>
+template <int TH, int TW, int BN, int STAGES, typename E>
 hipError_t launch_pipe(const ConvArgs &a, hipStream_t st) {
     // keep every buffer under 2 GiB (32-bit buffer offsets, kOobOffset out of
     // range): launch over groups of whole samples
@@ -772,7 +981,7 @@ hipError_t launch_pipe(const ConvArgs &a, hipStream_t st) {
         b.M = (int64_t)gn * a.gh * a.gw;
         const int64_t tiles = set_tiles(b, TH, TW, BN);
         if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-        conv_pipe_kernel<TH, TW, BN, STAGES><<<(unsigned)tiles, kThreads, 0, st>>>(b);
+        conv_pipe_kernel<TH, TW, BN, STAGES, E><<<(unsigned)tiles, kThreads, 0, st>>>(b);
     }
     return hipGetLastError();
 }
@@ -785,12 +994,16 @@ hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
     switch (a.cin_p <= 4 ? a.cin_p : 0) {
         case 0:
             switch (a.cout_pad) {
-                case 64: return launch_pipe<8, 32, 64, 5>(a, st);
-                case 128: return launch_pipe<8, 32, 128, 5>(a, st);
-                case 192: return launch_pipe<8, 32, 192, 5>(a, st);
-                case 256: return launch_pipe<4, 32, 256, 5>(a, st);
-                case 320: return launch_pipe<4, 32, 320, 5>(a, st);
-                default: return launch_pipe<8, 32, 64, 5>(a, st);
+                case 64: return launch_pipe<8, 32, 64, 5, EpiGeneric>(a, st);
+                case 128: return launch_pipe<8, 32, 128, 5, EpiGeneric>(a, st);
+                case 192:
+                    return with_epilogue<HATQ_HOT_EPILOGUES>(
+                        a, [&](auto e) { return launch_pipe<8, 32, 192, 5, decltype(e)>(a, st); });
+                case 256: return launch_pipe<4, 32, 256, 5, EpiGeneric>(a, st);
+                case 320:
+                    return with_epilogue<HATQ_HOT_EPILOGUES>(
+                        a, [&](auto e) { return launch_pipe<4, 32, 320, 5, decltype(e)>(a, st); });
+                default: return launch_pipe<8, 32, 64, 5, EpiGeneric>(a, st);
             }
         case 1: return a.rowrun ? launch_rowrun_n<1>(a, st) : launch_gather_n<1>(a, st);
         case 2: return a.rowrun ? launch_rowrun_n<2>(a, st) : launch_gather_n<2>(a, st);
