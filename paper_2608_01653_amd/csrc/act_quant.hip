@@ -77,13 +77,53 @@ __global__ void __launch_bounds__(kThreads) absmax_kernel(const float *__restric
     }
 }
 
+// Items per quad per loop iteration (all their loads issued before first use).
+template <int B>
+struct QuantUnroll {
+    static constexpr int UN = 1;   // more items in flight measured no faster
+};
+
+// Quantize one transformed item (s = act scale, r = fl(1/s)) and store its codes.
+template <int B>
+__device__ __forceinline__ void quant_store_item(const float (&vin)[4 * ItemShape<B>::R], int8_t *qs, int64_t base,
+                                                 int64_t E, int t, float s, float r, bool fast_ok, float sigma) {
+    constexpr int R = ItemShape<B>::R;
+    constexpr int I = ItemShape<B>::I;
+    const float rs = sigma * r;
+    uint32_t u[4 * R];
+    bool near = !fast_ok;
+#pragma unroll
+    for (int k = 0; k < 4 * R; ++k) {
+        const float tq = clamp127(vin[k] * rs);
+        const float uf = tq + HATQ_MAGIC;
+        const float kf = uf - HATQ_MAGIC;
+        near |= fabsf(tq - kf) > HATQ_NEAR_TIE;
+        u[k] = __float_as_uint(uf);
+    }
+    if (near) {
+#pragma unroll
+        for (int k = 0; k < 4 * R; ++k) {
+            const float q = rintf(clamp127((sigma * vin[k]) / s));
+            u[k] = __float_as_uint(q + HATQ_MAGIC);
+        }
+    }
+    const bool full = base + I <= E;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const int64_t off = base + 16 * i + 4 * t;
+        if (full || off < E)
+            *reinterpret_cast<uint32_t *>(qs + off) = pack_low_bytes(u[4 * i], u[4 * i + 1], u[4 * i + 2], u[4 * i + 3]);
+    }
+}
+
 template <int B>
 __global__ void __launch_bounds__(kThreads) quant_kernel(const float *__restrict__ x, int64_t E,
                                                          const float *__restrict__ absmax,
                                                          int8_t *__restrict__ xq,
                                                          float *__restrict__ act_scale) {
-    constexpr int R = ItemShape<B>::R;
     constexpr int I = ItemShape<B>::I;
+    constexpr int R = ItemShape<B>::R;
+    constexpr int UN = QuantUnroll<B>::UN;
     const int n = blockIdx.y;
     const float *xs = x + (int64_t)n * E;
     int8_t *qs = xq + (int64_t)n * E;
@@ -95,37 +135,21 @@ __global__ void __launch_bounds__(kThreads) quant_kernel(const float *__restrict
     // 2^-125 or above 2^125 takes the exact division for every element.
     const bool fast_ok = s >= 0x1p-125f && s <= 0x1p125f;
     const int64_t items = (E + I - 1) / I;
-    for (int64_t it = (int64_t)blockIdx.x * kQuadsPerBlock + (threadIdx.x >> 2); it < items;
-         it += (int64_t)gridDim.x * kQuadsPerBlock) {
-        const int64_t base = it * I;
-        float v[4 * R];
-        load_item<B>(xs, base, E, t, v);
-        const float sigma = fwht_item<B>(v, t);
-        const float rs = sigma * r;
-        uint32_t u[4 * R];
-        bool near = !fast_ok;
+    const int64_t step = (int64_t)gridDim.x * kQuadsPerBlock;
+    for (int64_t it0 = (int64_t)blockIdx.x * kQuadsPerBlock * UN + (threadIdx.x >> 2); it0 < items;
+         it0 += step * UN) {
+        float v[UN][4 * R];
 #pragma unroll
-        for (int k = 0; k < 4 * R; ++k) {
-            const float tq = clamp127(v[k] * rs);
-            const float uf = tq + HATQ_MAGIC;
-            const float kf = uf - HATQ_MAGIC;
-            near |= fabsf(tq - kf) > HATQ_NEAR_TIE;
-            u[k] = __float_as_uint(uf);
+        for (int u = 0; u < UN; ++u) {
+            const int64_t it = it0 + u * kQuadsPerBlock;
+            if (it < items) load_item<B>(xs, it * I, E, t, v[u]);
         }
-        if (near) {
 #pragma unroll
-            for (int k = 0; k < 4 * R; ++k) {
-                const float q = rintf(clamp127((sigma * v[k]) / s));
-                u[k] = __float_as_uint(q + HATQ_MAGIC);
-            }
-        }
-        const bool full = base + I <= E;
-#pragma unroll
-        for (int i = 0; i < R; ++i) {
-            const int64_t off = base + 16 * i + 4 * t;
-            if (full || off < E)
-                *reinterpret_cast<uint32_t *>(qs + off) =
-                    pack_low_bytes(u[4 * i], u[4 * i + 1], u[4 * i + 2], u[4 * i + 3]);
+        for (int u = 0; u < UN; ++u) {
+            const int64_t it = it0 + u * kQuadsPerBlock;
+            if (it >= items) break;
+            const float sigma = fwht_item<B>(v[u], t);
+            quant_store_item<B>(v[u], qs, it * I, E, t, s, r, fast_ok, sigma);
         }
     }
 }
@@ -169,9 +193,12 @@ __global__ void __launch_bounds__(kThreads) scalar_kernel(const float *__restric
     }
 }
 
-int grid_x(int64_t work_units, int per_block, int n) {
+// Blocks per sample: enough for the work, at most `total` over the whole batch.
+// The absmax kernels end in one same-address atomic per block, so they use a
+// smaller total than the quantization kernels.
+int grid_x(int64_t work_units, int per_block, int n, int total = 8192) {
     int64_t want = (work_units + per_block - 1) / per_block;
-    int64_t cap = (2048 + n - 1) / n;   // about 8 blocks per CU over the whole batch
+    int64_t cap = (total + n - 1) / n;
     if (cap < 1) cap = 1;
     if (want > cap) want = cap;
     return (int)(want < 1 ? 1 : want);
@@ -182,13 +209,14 @@ hipError_t launch_vector(const float *x, int n, int64_t E, const float *absmax_i
                          int8_t *xq, float *act_scale, hipStream_t st) {
     constexpr int I = ItemShape<B>::I;
     const int64_t items = (E + I - 1) / I;
-    dim3 grid(grid_x(items, kQuadsPerBlock, n), n);
     const float *A = absmax_in;
     if (!A) {
+        dim3 grid(grid_x(items, kQuadsPerBlock, n, 2048), n);
         fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(ws_absmax), n, 0u);
         absmax_kernel<B><<<grid, kThreads, 0, st>>>(x, E, ws_absmax);
         A = ws_absmax;
     }
+    dim3 grid(grid_x(items, kQuadsPerBlock * QuantUnroll<B>::UN, n), n);
     quant_kernel<B><<<grid, kThreads, 0, st>>>(x, E, A, xq, act_scale);
     return hipGetLastError();
 }
@@ -200,7 +228,8 @@ hipError_t launch_scalar(const float *x, int n, int64_t E, const float *absmax_i
     const float *A = absmax_in;
     if (!A) {
         fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(ws_absmax), n, 0u);
-        scalar_kernel<B, false><<<grid, kThreads, 0, st>>>(x, E, ws_absmax, nullptr, nullptr);
+        scalar_kernel<B, false><<<dim3(grid_x(E / B, kThreads, n, 2048), n), kThreads, 0, st>>>(x, E, ws_absmax,
+                                                                                              nullptr, nullptr);
         A = ws_absmax;
     }
     scalar_kernel<B, true><<<grid, kThreads, 0, st>>>(x, E, const_cast<float *>(A), xq, act_scale);

@@ -52,11 +52,12 @@ __device__ __forceinline__ float lane_xor(float v) {
 }
 
 // One cross-lane butterfly stage on R registers: partner lane = lane ^ MASK.
-// coef = -1 on lanes with the bit set, +1 otherwise.
+// coef = -1 on lanes with the bit set, +1 otherwise.  The partner value is the
+// first factor so the DPP move folds into the fused multiply-add.
 template <int MASK, int R>
 __device__ __forceinline__ void cross_stage(float (&v)[R], float coef) {
 #pragma unroll
-    for (int r = 0; r < R; ++r) v[r] = __builtin_fmaf(coef, lane_xor<MASK>(v[r]), v[r]);
+    for (int r = 0; r < R; ++r) v[r] = __builtin_fmaf(lane_xor<MASK>(v[r]), coef, v[r]);
 }
 
 // One in-register butterfly stage on registers whose index bit STRIDE differs.
