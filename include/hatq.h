@@ -173,7 +173,7 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
  *     |y|), the exact value hatq_fwht_quant_act would compute from y; the next
  *     layer can then quantize y reading it once.  It is overwritten, not
  *     accumulated.
- * Supported: cin_pad % 64 == 0 (any k), or cin_pad <= 4 with k*k*cin_pad <= 128;
+ * Supported: cin_pad % 64 == 0 with k <= 8, or cin_pad <= 4 with k*k*cin_pad <= 128;
  * cout_pad % 64 == 0; WH block and next_hblock at most 64.  Transposed: stride 2.
  * xq and y must be 16-byte aligned. */
 int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act_scale,

@@ -961,6 +961,249 @@ __global__ void __launch_bounds__(kThreads, 1) conv_pipe_kernel(const ConvArgs a
     epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, col, col + BN);
 }
 
+// ---------------------------------------------------------------------------
+// Halo path (regular convolution, stride 2, 4 <= k <= 6, cin_p % 64 == 0): the
+// input window of an 8 x 32 output tile for one 64-channel chunk, at most
+// 20 x 68 pixels, stays in LDS, so each input byte crosses the L2 once per block
+// instead of once per tap.  The window is split by row parity: with stride 2,
+// tap row kh reads window rows 2*oh + kh, all of parity kh & 1.  Each chunk runs
+// its odd-kh taps first, then its even-kh taps; while one parity half is being
+// read the other half is refilled for the next phase (even half of this chunk
+// during the odd taps, odd half of the next chunk during the even taps).
+// Column parity is split too, so the 16 consecutive output columns a fragment
+// reads are 16 consecutive 64-byte records (chunk-swizzled like the operand
+// tiles: conflict-free).  Weight tiles stream through a STAGES-deep ring as in
+// the pipelined path.
+// ---------------------------------------------------------------------------
+struct HaloGeom {
+    static constexpr int TH = 8, TW = 32;
+    static constexpr int HR = 10;                          // window rows per parity (k <= 6)
+    static constexpr int HCC = 34;                         // window columns per parity
+    static constexpr int RECS = HR * 2 * HCC;              // 64-byte records per half
+    static constexpr int INSTR = (RECS + 63) / 64;         // 1 KB DMA instructions per wave per half
+    static constexpr int HALF_BYTES = INSTR * 4 * 1024;
+};
+
+template <int BN, int STAGES, typename E>
+__global__ void __launch_bounds__(kThreads, 1) conv_halo_kernel(const ConvArgs a) {
+    using G = HaloGeom;
+    constexpr int TH = G::TH, TW = G::TW;
+    constexpr int BM = TH * TW;
+    constexpr int TM = BM / 4;
+    constexpr int FM = TM / 16;
+    constexpr int FN = BN / 16;
+    constexpr int PER = BN / 64;                           // weight DMA instructions per wave per step
+    constexpr int HB = G::INSTR;                           // window DMA instructions per wave per half
+    constexpr int B_BYTES = BN * 64;
+    static_assert(BN % 64 == 0 && STAGES >= 4, "tile");
+    __shared__ __attribute__((aligned(1024))) int8_t lds[2 * G::HALF_BYTES + STAGES * B_BYTES];
+    int8_t *const halo = lds;
+    int8_t *const bring = lds + 2 * G::HALF_BYTES;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const Tile tile = block_tile(a, xcd_logical_tile(), TH, TW, BN);
+    const int n0 = tile.n0;
+    const int cin_p = a.cin_p;
+    const int nchunks = cin_p >> 6;
+    const int k = a.k;
+    const int ntap = k * k;
+    const int nodd = (k >> 1) * k;                         // taps with odd kh
+    const int nks = nchunks * ntap;
+    const int rows_used = 2 * (TH - 1) + k, cols_used = 2 * (TW - 1) + k;
+    const int ih0 = tile.gi0 * 2 + a.bah, iw0 = tile.gj0 * 2 + a.baw;
+
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int8_t *>(a.xq), (short)0, (int)((int64_t)a.n * a.h * a.w * cin_p), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int8_t *>(a.wp), (short)0, (int)((int64_t)a.cout_pad * a.pack_stride), 0x00020000);
+
+    // window DMA: instruction j of this wave fills records 16*(wave + 4j) + lane/4
+    // of a half; record f = (rr*2 + cp)*HCC + cc is window row 2*rr + parity,
+    // column 2*cc + cp.  Offsets exclude the chunk; records outside the window or
+    // the image read zeros.
+    uint32_t h_off[2][HB];
+#pragma unroll
+    for (int hp = 0; hp < 2; ++hp)
+#pragma unroll
+        for (int j = 0; j < HB; ++j) {
+            const int f = 16 * (wave + 4 * j) + (lane >> 2);
+            const int g = (lane & 3) ^ swz(f);
+            const int rr = f / (2 * G::HCC), rem = f - rr * (2 * G::HCC);
+            const int cp = rem / G::HCC, cc = rem - cp * G::HCC;
+            const int row = 2 * rr + hp, col = 2 * cc + cp;
+            const int ih = ih0 + row, iw = iw0 + col;
+            const bool in = f < G::RECS && row < rows_used && col < cols_used && (unsigned)ih < (unsigned)a.h &&
+                            (unsigned)iw < (unsigned)a.w;
+            h_off[hp][j] = in ? (uint32_t)(((tile.nb * a.h + ih) * a.w + iw) * cin_p + 16 * g) : kOobOffset;
+        }
+    auto burst = [&](int hp, int chunk) {
+        int8_t *dst = halo + hp * G::HALF_BYTES;
+        const uint32_t coff = (uint32_t)(chunk * 64);
+#pragma unroll
+        for (int j = 0; j < HB; ++j)
+            dma16(rx, dst + 1024 * (wave + 4 * j), h_off[hp][j] == kOobOffset ? kOobOffset : h_off[hp][j] + coff);
+    };
+    uint32_t b_off[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int nn = 16 * (wave + 4 * j) + (lane >> 2);
+        const int g = (lane & 3) ^ swz(nn);
+        b_off[j] = (uint32_t)((n0 + nn) * 64 + 16 * g);
+    }
+    // step ks: chunk, then the odd-kh taps, then the even-kh taps
+    auto decode = [&](int ks, int &chunk, int &kh, int &kw) {
+        chunk = ks / ntap;
+        int j = ks - chunk * ntap;
+        int par = 1;
+        if (j >= nodd) {
+            j -= nodd;
+            par = 0;
+        }
+        const int q = j / k;
+        kh = 2 * q + par;
+        kw = j - q * k;
+    };
+    auto issue_b = [&](int ks) {
+        int chunk, kh, kw;
+        decode(ks, chunk, kh, kw);
+        const uint32_t woff = (uint32_t)(((kh * k + kw) * nchunks + chunk) * a.cout_pad * 64);
+        int8_t *sb = bring + (ks % STAGES) * B_BYTES;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) dma16(rw, sb + 1024 * (wave + 4 * j), b_off[j] + woff);
+    };
+    // window refills: even half of chunk c at its first (odd) step, odd half of
+    // chunk c+1 at chunk c's first even step; returns the half refilled or -1
+    auto burst_at = [&](int ks, int &chunk_out) -> int {
+        const int chunk = ks / ntap, j = ks - chunk * ntap;
+        if (j == 0 && chunk >= 1) {
+            chunk_out = chunk;
+            return 0;
+        }
+        if (j == nodd && chunk + 1 < nchunks) {
+            chunk_out = chunk + 1;
+            return 1;
+        }
+        return -1;
+    };
+
+    v4i acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+
+    const int fr = lane & 15, fg = lane >> 4;
+    int f_base[FM];   // window record of tap (0, 0) for this lane's points
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int m = wave * TM + 16 * i + fr;
+        const int oh = m / TW, ow = m - oh * TW;
+        f_base[i] = oh * 2 * G::HCC + ow;
+    }
+    int fb_off[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        const int nn = 16 * j + fr;
+        fb_off[j] = nn * 64 + 16 * (fg ^ swz(nn));
+    }
+    auto afrag = [&](int ks, int i) {
+        int chunk, kh, kw;
+        decode(ks, chunk, kh, kw);
+        const int f = f_base[i] + ((kh >> 1) * 2 + (kw & 1)) * G::HCC + (kw >> 1);
+        return *reinterpret_cast<const v4i *>(halo + (kh & 1) * G::HALF_BYTES + f * 64 + 16 * (fg ^ swz(f)));
+    };
+    auto bfrag = [&](int ks, int j) {
+        return *reinterpret_cast<const v4i *>(bring + (ks % STAGES) * B_BYTES + fb_off[j]);
+    };
+
+    // B fragments stream through a ring of RING registers (RING-1 reads ahead,
+    // continuing into step ks+1); step ks+1's A fragments go to the other A set.
+    // Reads past the last step hit stale, in-bounds LDS and are never used.
+    constexpr int RING = 4;
+    static_assert(FN % RING == 0 && FN >= RING, "ring");
+    v4i ring[RING];
+    v4i fa0[FM], fa1[FM];
+
+    // prologue: both halves of chunk 0, weight steps 0 .. STAGES-2
+    burst(1, 0);
+    burst(0, 0);
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (s < nks) issue_b(s);
+    if (STAGES - 1 <= nks) wait_vmcnt<(STAGES - 2) * PER>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa0[i] = afrag(0, i);
+#pragma unroll
+    for (int r = 0; r < RING - 1; ++r) ring[r] = bfrag(0, r);
+
+    int bc;
+    auto stage = [&](int ks, v4i (&acur)[FM], v4i (&anext)[FM]) {
+        // weight steps ks and ks+1 (and window halves read by them) must have
+        // landed: everything but the last two weight steps, plus any window burst
+        // issued after weight step ks+1
+        if (ks + STAGES - 2 < nks) {
+            const bool recent = (ks >= 1 && burst_at(ks - 1, bc) >= 0) || (ks >= 2 && burst_at(ks - 2, bc) >= 0);
+            if (recent) wait_vmcnt<(STAGES - 3) * PER + HB>();
+            else wait_vmcnt<(STAGES - 3) * PER>();
+        } else {
+            wait_vmcnt<0>();
+        }
+        __builtin_amdgcn_s_barrier();
+        const int hp = burst_at(ks, bc);
+        if (hp >= 0) burst(hp, bc);
+        if (ks + STAGES - 1 < nks) issue_b(ks + STAGES - 1);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int jj = j + RING - 1;
+            ring[jj % RING] = jj < FN ? bfrag(ks, jj) : bfrag(ks + 1, jj - FN);
+            if (j >= FN - FM) anext[j - (FN - FM)] = afrag(ks + 1, j - (FN - FM));
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ring[j % RING], acur[i], acc[i][j], 0, 0, 0);
+        }
+    };
+    for (int ks = 0; ks < nks; ++ks) {
+        stage(ks, fa0, fa1);
+#pragma unroll
+        for (int i = 0; i < FM; ++i) fa0[i] = fa1[i];
+    }
+    __syncthreads();   // every wave is done with the window and the ring
+    float *col = reinterpret_cast<float *>(lds);
+    column_factors<BN>(a, tile, col, col + BN);
+    __syncthreads();
+    epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, col, col + BN);
+}
+
+template <int BN, int STAGES, typename E>
+hipError_t launch_halo(const ConvArgs &a, hipStream_t st) {
+    // keep every buffer under 2 GiB (32-bit buffer offsets, kOobOffset out of
+    // range): launch over groups of whole samples
+    const int64_t per_sample = (int64_t)a.h * a.w * a.cin_p;
+    const int64_t group = ((int64_t)1 << 31) / per_sample;
+    if (group < 1) return hipErrorInvalidValue;
+    if ((int64_t)a.cout_pad * a.pack_stride >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    if (a.sa != 2 || a.so != 1 || a.k < 4 || a.k > 6 || a.cin_p % 64) return hipErrorInvalidValue;
+    for (int64_t s0 = 0; s0 < a.n; s0 += group) {
+        ConvArgs b = a;
+        const int gn = (int)(a.n - s0 < group ? a.n - s0 : group);
+        b.n = gn;
+        b.xq = a.xq + s0 * per_sample;
+        b.sx = a.sx + s0;
+        const int64_t out_per_sample = (int64_t)a.ho * a.wo * (a.mode == 0 ? a.cout_pad : a.cout);
+        b.y = (void *)((char *)a.y + s0 * out_per_sample * 4);
+        if (a.next_absmax) b.next_absmax = a.next_absmax + s0;
+        b.M = (int64_t)gn * a.gh * a.gw;
+        const int64_t tiles = set_tiles(b, HaloGeom::TH, HaloGeom::TW, BN);
+        if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+        conv_halo_kernel<BN, STAGES, E><<<(unsigned)tiles, kThreads, 0, st>>>(b);
+    }
+    return hipGetLastError();
+}
+
 template <int TH, int TW, int BN, int STAGES, typename E>
 hipError_t launch_pipe(const ConvArgs &a, hipStream_t st) {
     // keep every buffer under 2 GiB (32-bit buffer offsets, kOobOffset out of
@@ -997,6 +1240,9 @@ hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
                 case 64: return launch_pipe<8, 32, 64, 5, EpiGeneric>(a, st);
                 case 128: return launch_pipe<8, 32, 128, 5, EpiGeneric>(a, st);
                 case 192:
+                    if (a.sa == 2 && a.so == 1 && a.k >= 4 && a.k <= 6)
+                        return with_epilogue<HATQ_HOT_EPILOGUES>(
+                            a, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st); });
                     return with_epilogue<HATQ_HOT_EPILOGUES>(
                         a, [&](auto e) { return launch_pipe<8, 32, 192, 5, decltype(e)>(a, st); });
                 case 256: return launch_pipe<4, 32, 256, 5, EpiGeneric>(a, st);

@@ -11,7 +11,7 @@ namespace hatq {
 hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,
                             float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st);
 
-constexpr int kMaxTaps = 32;
+constexpr int kMaxTaps = 64;
 
 // Geometry and operands of one implicit-GEMM launch.  GEMM rows are the points
 // (nb, gi, gj) of an n x gh x gw grid, processed in 2-D tiles of TH x TW points.  Input anchor of a point:
