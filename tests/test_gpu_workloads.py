@@ -1,0 +1,122 @@
+"""GPU parity at the workload shapes.
+
+* cfg0-cfg3 (sizes the oracle finishes in seconds): every layer of the workload,
+  each GPU stage fed the oracle's own inputs (the oracle's fp32 output of the
+  previous layer, the oracle's codes and scales), so the comparison isolates each
+  stage: codes and scales of the activation pass, the fp32 output of the
+  convolution with its epilogue, and the fused next-layer absmax.
+* cfg4 (batch 16, 1024x1024; too large for the oracle): every convolution at its
+  full size, in the launch configuration the benchmark times, on random INT8
+  codes; sampled output pixels are recomputed by the oracle from their 5x5
+  input crop, and the fused absmax is checked against the two-pass activation
+  kernel run on the stored output (a property that holds at any size).
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import assert_codes, assert_range_rel, assert_scale_ulp, dev, host
+from paper_2608_01653_amd import hatq, synth, workloads
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    hatq.load()
+    torch.cuda.init()
+
+
+def _prepare(orc, L, w, b):
+    ref = orc.prepare_weights(w, b, cin=L.cin, cout=L.cout, k=L.k, stride=L.stride, pad=L.pad,
+                              form=L.form, hblock=L.hblock, transposed=L.transposed, out_pad=L.out_pad)
+    d = hatq.desc(L.cin, L.cout, L.k, L.stride, L.pad, L.hblock, L.transposed, L.out_pad)
+    return ref, hatq.hatq_prepare_weights(d, L.form, dev(w), dev(b))
+
+
+def _act_block(L):
+    return L.hblock if L.form == "DH" else 1
+
+
+@pytest.mark.parametrize("name", ["cfg0", "cfg1_dh", "cfg1_wh", "cfg2", "cfg3"])
+def test_workload_layers(orc, name):
+    wl = workloads.ALL[name]
+    x, params = wl.generate()
+    n = x.shape[0]
+    for i, L in enumerate(wl.layers):
+        w, b = params[i]
+        ref, layer = _prepare(orc, L, w, b)
+        r = orc.layer_forward(x, ref)
+        # a2-a4 on the oracle's layer input
+        q, s = hatq.hatq_fwht_quant_act(dev(x), _act_block(L))
+        assert_scale_ulp(host(s), r.sx)
+        assert_codes(host(q), r.xq, what=f"{name} layer {i + 1} codes")
+        # a5-a6 on the oracle's codes and scales, with the next layer's absmax
+        nxt = wl.layers[i + 1] if i + 1 < len(wl.layers) else None
+        nam = torch.full((n,), -1.0, device="cuda") if nxt else None
+        y = hatq.hatq_conv_int8(layer, dev(r.xq), dev(r.sx), hatq.HATQ_OUT_F32,
+                                next_hblock=_act_block(nxt) if nxt else 0, next_absmax=nam)
+        yh = host(y)
+        assert yh.shape == r.y.shape
+        if L.form == "DH":
+            assert np.array_equal(yh, r.y), f"{name} layer {i + 1} output"
+        else:
+            assert_range_rel(yh, r.y, what=f"{name} layer {i + 1} output")
+        if nxt:
+            S_ref = orc.activation_transform(r.y, _act_block(nxt)).reshape(n, -1)
+            A_ref = np.abs(S_ref.astype(np.float64)).max(1)
+            np.testing.assert_allclose(host(nam), A_ref, rtol=2e-6)
+        x = r.y   # the oracle's output feeds the next layer
+
+
+def _crop(xq, nb, ih0, iw0, k):
+    """k x k input window at (ih0, iw0) of sample nb, zero outside the image."""
+    _, h, w, c = xq.shape
+    out = np.zeros((1, k, k, c), np.int8)
+    r0, r1 = max(ih0, 0), min(ih0 + k, h)
+    c0, c1 = max(iw0, 0), min(iw0 + k, w)
+    out[0, r0 - ih0:r1 - ih0, c0 - iw0:c1 - iw0] = xq[nb, r0:r1, c0:c1]
+    return out
+
+
+@pytest.mark.parametrize("li", [0, 1, 2, 3], ids=["L1", "L2", "L3", "L4"])
+def test_cfg4_full_size_sampled(orc, li):
+    wl = workloads.CFG4
+    (ishape, oshape) = wl.shapes()[li]
+    L = wl.layers[li]
+    rng = np.random.default_rng(4000 + li)
+    w, b = synth.layer_params(rng, L.cin, L.cout, L.k, L.transposed)
+    ref, layer = _prepare(orc, L, w, b)
+    n, h, wd, _ = ishape
+    xq = synth.int8_codes(rng, (n, h, wd, ref.cin_p))
+    sx = rng.uniform(1e-3, 1e-2, n).astype(np.float32)
+    nxt = wl.layers[li + 1] if li + 1 < len(wl.layers) else None
+    nb = _act_block(nxt) if nxt else 0
+    nam = torch.full((n,), -1.0, device="cuda") if nxt else None
+    y = hatq.hatq_conv_int8(layer, dev(xq), dev(sx), hatq.HATQ_OUT_F32, next_hblock=nb, next_absmax=nam)
+    ho, wo = oshape[1], oshape[2]
+    # sampled pixels: the four corners of several samples plus random interior points
+    pts = [(s, oh, ow) for s in (0, n - 1) for oh in (0, ho - 1) for ow in (0, wo - 1)]
+    pts += [(int(rng.integers(n)), int(rng.integers(ho)), int(rng.integers(wo))) for _ in range(120)]
+    idx = torch.tensor(pts, device="cuda")
+    y_s = host(y[idx[:, 0], idx[:, 1], idx[:, 2]])
+    y_ref = np.empty_like(y_s)
+    for t, (s, oh, ow) in enumerate(pts):
+        crop = _crop(xq, s, oh * L.stride - L.pad, ow * L.stride - L.pad, L.k)
+        acc = orc.conv_int8(crop, ref.wq, stride=L.stride, pad=0)
+        y_ref[t] = orc.epilogue(acc, sx[s:s + 1], ref)[0, 0, 0]
+    if L.form == "DH":
+        assert np.array_equal(y_s, y_ref)
+    else:
+        assert_range_rel(y_s, y_ref)
+    if nxt:
+        # the fused absmax equals what the two-pass activation kernel computes from
+        # the stored output, and bounds the sampled pixels' transformed values
+        q1, s1 = hatq.hatq_fwht_quant_act(y, nb, absmax=nam)
+        q2, s2 = hatq.hatq_fwht_quant_act(y, nb)
+        assert torch.equal(s1, s2)
+        A = host(nam)
+        S_s = orc.activation_transform(y_ref.reshape(len(pts), 1, 1, -1), nb).reshape(len(pts), -1)
+        for t, (s, _, _) in enumerate(pts):
+            assert np.abs(S_s[t].astype(np.float64)).max() <= A[s] * (1 + 1e-5)
+        del q1, q2
