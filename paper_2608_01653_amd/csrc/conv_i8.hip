@@ -1052,40 +1052,32 @@ __global__ void __launch_bounds__(kThreads, 1) conv_halo_kernel(const ConvArgs a
         const int g = (lane & 3) ^ swz(nn);
         b_off[j] = (uint32_t)((n0 + nn) * 64 + 16 * g);
     }
-    // step ks: chunk, then the odd-kh taps, then the even-kh taps
-    auto decode = [&](int ks, int &chunk, int &kh, int &kw) {
-        chunk = ks / ntap;
-        int j = ks - chunk * ntap;
-        int par = 1;
-        if (j >= nodd) {
-            j -= nodd;
-            par = 0;
-        }
-        const int q = j / k;
-        kh = 2 * q + par;
-        kw = j - q * k;
+    // Position of a K-step in the order chunk, odd-kh taps, even-kh taps; the
+    // loop advances these incrementally (no divisions per step).
+    struct Pos {
+        int chunk, j, kh, kw, slot;   // slot: weight ring buffer (step % STAGES)
     };
-    auto issue_b = [&](int ks) {
-        int chunk, kh, kw;
-        decode(ks, chunk, kh, kw);
-        const uint32_t woff = (uint32_t)(((kh * k + kw) * nchunks + chunk) * a.cout_pad * 64);
-        int8_t *sb = bring + (ks % STAGES) * B_BYTES;
+    auto advance = [&](Pos &p) {
+        ++p.j;
+        if (++p.slot == STAGES) p.slot = 0;
+        if (p.j == ntap) {
+            p.j = 0;
+            ++p.chunk;
+            p.kh = 1;
+            p.kw = 0;
+        } else if (p.j == nodd) {
+            p.kh = 0;
+            p.kw = 0;
+        } else if (++p.kw == k) {
+            p.kw = 0;
+            p.kh += 2;
+        }
+    };
+    auto issue_b = [&](const Pos &p) {
+        const uint32_t woff = (uint32_t)(((p.kh * k + p.kw) * nchunks + p.chunk) * a.cout_pad * 64);
+        int8_t *sb = bring + p.slot * B_BYTES;
 #pragma unroll
         for (int j = 0; j < PER; ++j) dma16(rw, sb + 1024 * (wave + 4 * j), b_off[j] + woff);
-    };
-    // window refills: even half of chunk c at its first (odd) step, odd half of
-    // chunk c+1 at chunk c's first even step; returns the half refilled or -1
-    auto burst_at = [&](int ks, int &chunk_out) -> int {
-        const int chunk = ks / ntap, j = ks - chunk * ntap;
-        if (j == 0 && chunk >= 1) {
-            chunk_out = chunk;
-            return 0;
-        }
-        if (j == nodd && chunk + 1 < nchunks) {
-            chunk_out = chunk + 1;
-            return 1;
-        }
-        return -1;
     };
 
     v4i acc[FM][FN];
@@ -1108,14 +1100,12 @@ __global__ void __launch_bounds__(kThreads, 1) conv_halo_kernel(const ConvArgs a
         const int nn = 16 * j + fr;
         fb_off[j] = nn * 64 + 16 * (fg ^ swz(nn));
     }
-    auto afrag = [&](int ks, int i) {
-        int chunk, kh, kw;
-        decode(ks, chunk, kh, kw);
-        const int f = f_base[i] + ((kh >> 1) * 2 + (kw & 1)) * G::HCC + (kw >> 1);
-        return *reinterpret_cast<const v4i *>(halo + (kh & 1) * G::HALF_BYTES + f * 64 + 16 * (fg ^ swz(f)));
+    auto afrag = [&](const Pos &p, int i) {
+        const int f = f_base[i] + ((p.kh >> 1) * 2 + (p.kw & 1)) * G::HCC + (p.kw >> 1);
+        return *reinterpret_cast<const v4i *>(halo + (p.kh & 1) * G::HALF_BYTES + f * 64 + 16 * (fg ^ swz(f)));
     };
-    auto bfrag = [&](int ks, int j) {
-        return *reinterpret_cast<const v4i *>(bring + (ks % STAGES) * B_BYTES + fb_off[j]);
+    auto bfrag = [&](const Pos &p, int j) {
+        return *reinterpret_cast<const v4i *>(bring + p.slot * B_BYTES + fb_off[j]);
     };
 
     // B fragments stream through a ring of RING registers (RING-1 reads ahead,
@@ -1127,44 +1117,64 @@ __global__ void __launch_bounds__(kThreads, 1) conv_halo_kernel(const ConvArgs a
     v4i fa0[FM], fa1[FM];
 
     // prologue: both halves of chunk 0, weight steps 0 .. STAGES-2
+    Pos p_cur = {0, 0, 1, 0, 0};   // step ks (odd-kh taps first: kh = 1)
     burst(1, 0);
     burst(0, 0);
+    Pos p_iss = p_cur;            // next weight step to issue
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s)
-        if (s < nks) issue_b(s);
+        if (s < nks) {
+            issue_b(p_iss);
+            advance(p_iss);
+        }
     if (STAGES - 1 <= nks) wait_vmcnt<(STAGES - 2) * PER>();
     else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
 #pragma unroll
-    for (int i = 0; i < FM; ++i) fa0[i] = afrag(0, i);
+    for (int i = 0; i < FM; ++i) fa0[i] = afrag(p_cur, i);
 #pragma unroll
-    for (int r = 0; r < RING - 1; ++r) ring[r] = bfrag(0, r);
+    for (int r = 0; r < RING - 1; ++r) ring[r] = bfrag(p_cur, r);
 
-    int bc;
+    Pos p_nxt = p_cur;            // step ks+1
+    advance(p_nxt);
+    // at step t's wait, since_burst = t - 1 - (step of the last window burst)
+    int since_burst = 2;
     auto stage = [&](int ks, v4i (&acur)[FM], v4i (&anext)[FM]) {
         // weight steps ks and ks+1 (and window halves read by them) must have
-        // landed: everything but the last two weight steps, plus any window burst
-        // issued after weight step ks+1
+        // landed: everything but the last two weight steps, plus a window burst
+        // issued in either of the two previous steps (after weight step ks+1)
         if (ks + STAGES - 2 < nks) {
-            const bool recent = (ks >= 1 && burst_at(ks - 1, bc) >= 0) || (ks >= 2 && burst_at(ks - 2, bc) >= 0);
-            if (recent) wait_vmcnt<(STAGES - 3) * PER + HB>();
+            if (since_burst <= 1) wait_vmcnt<(STAGES - 3) * PER + HB>();
             else wait_vmcnt<(STAGES - 3) * PER>();
         } else {
             wait_vmcnt<0>();
         }
         __builtin_amdgcn_s_barrier();
-        const int hp = burst_at(ks, bc);
-        if (hp >= 0) burst(hp, bc);
-        if (ks + STAGES - 1 < nks) issue_b(ks + STAGES - 1);
+        // window refills: even half of this chunk at its first (odd) step, odd
+        // half of the next chunk at this chunk's first even step
+        ++since_burst;
+        if (p_cur.j == 0 && p_cur.chunk >= 1) {
+            burst(0, p_cur.chunk);
+            since_burst = 0;
+        } else if (p_cur.j == nodd && p_cur.chunk + 1 < nchunks) {
+            burst(1, p_cur.chunk + 1);
+            since_burst = 0;
+        }
+        if (ks + STAGES - 1 < nks) {
+            issue_b(p_iss);
+            advance(p_iss);
+        }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
             const int jj = j + RING - 1;
-            ring[jj % RING] = jj < FN ? bfrag(ks, jj) : bfrag(ks + 1, jj - FN);
-            if (j >= FN - FM) anext[j - (FN - FM)] = afrag(ks + 1, j - (FN - FM));
+            ring[jj % RING] = jj < FN ? bfrag(p_cur, jj) : bfrag(p_nxt, jj - FN);
+            if (j >= FN - FM) anext[j - (FN - FM)] = afrag(p_nxt, j - (FN - FM));
 #pragma unroll
             for (int i = 0; i < FM; ++i)
                 acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ring[j % RING], acur[i], acc[i][j], 0, 0, 0);
         }
+        p_cur = p_nxt;
+        advance(p_nxt);
     };
     for (int ks = 0; ks < nks; ++ks) {
         stage(ks, fa0, fa1);
