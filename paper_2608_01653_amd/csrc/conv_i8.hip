@@ -984,25 +984,53 @@ struct HaloGeom {
     static constexpr int HALF_BYTES = INSTR * 4 * 1024;
 };
 
+// Window and weight records use the 16-B chunk swizzle q ^ ((f >> 2) & 3)
+// (conflict-free for any 16 consecutive records).  With a = byte offset of
+// record f (bits 4-9 of every half's base are zero), the physical address of
+// chunk q is aq ^ ((aq >> 4) & 0x30) with aq = a + 16*q, so a fragment address
+// is one add and two bit operations per tap.
+__device__ __forceinline__ int swz_win(int f) { return (f >> 2) & 3; }
+__device__ __forceinline__ uint32_t win_addr(uint32_t aq) { return aq ^ ((aq >> 4) & 0x30u); }
+
+// Eight waves (two per SIMD, so one wave's MFMAs run while the other waits
+// on LDS), each owning one 32-pixel output row of the tile by all BN channels.
+constexpr int kHaloWaves = 8;
+constexpr int kHaloThreads = 64 * kHaloWaves;
+
+// DMA block bi (1 KB) of a region of nblk >= kHaloWaves blocks, as issued by
+// instruction j of a wave: blocks past the end repeat the wave's previous block
+// (same bytes to the same place), so every wave issues the same number of
+// instructions and the per-wave wait counts stay uniform.
+__device__ __forceinline__ int halo_block(int wave, int j, int nblk) {
+    const int bi = wave + kHaloWaves * j;
+    return bi < nblk ? bi : bi - kHaloWaves;
+}
+
 template <int BN, int STAGES, typename E>
-__global__ void __launch_bounds__(kThreads, 1) conv_halo_kernel(const ConvArgs a) {
+__global__ void __launch_bounds__(kHaloThreads, 1) conv_halo_kernel(const ConvArgs a) {
     using G = HaloGeom;
     constexpr int TH = G::TH, TW = G::TW;
     constexpr int BM = TH * TW;
-    constexpr int TM = BM / 4;
+    constexpr int TM = BM / kHaloWaves;
     constexpr int FM = TM / 16;
     constexpr int FN = BN / 16;
-    constexpr int PER = BN / 64;                           // weight DMA instructions per wave per step
-    constexpr int HB = G::INSTR;                           // window DMA instructions per wave per half
+    constexpr int B_BLK = BN / 16;                                   // 1 KB blocks per weight step
+    constexpr int PER = (B_BLK + kHaloWaves - 1) / kHaloWaves;       // weight DMA instructions per wave per step
+    constexpr int W_BLK = (G::RECS + 15) / 16;                       // 1 KB blocks per window half
+    constexpr int HB = (W_BLK + kHaloWaves - 1) / kHaloWaves;        // window DMA instructions per wave per half
     constexpr int B_BYTES = BN * 64;
-    static_assert(BN % 64 == 0 && STAGES >= 4, "tile");
+    constexpr uint32_t RING_BASE = 2 * G::HALF_BYTES;
+    static_assert(BN % 64 == 0 && STAGES == 5, "tile");
+    static_assert(FM == 2 && TM == TW, "one output row per wave");
+    static_assert(B_BLK >= kHaloWaves && W_BLK >= kHaloWaves && W_BLK * 1024 <= G::HALF_BYTES, "DMA blocks");
+    static_assert((G::HALF_BYTES & 0x3F0) == 0 && (RING_BASE & 0x3F0) == 0 && (B_BYTES & 0x3F0) == 0, "swizzle bits");
     __shared__ __attribute__((aligned(1024))) int8_t lds[2 * G::HALF_BYTES + STAGES * B_BYTES];
     int8_t *const halo = lds;
-    int8_t *const bring = lds + 2 * G::HALF_BYTES;
+    int8_t *const bring = lds + RING_BASE;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const Tile tile = block_tile(a, xcd_logical_tile(), TH, TW, BN);
     const int n0 = tile.n0;
     const int cin_p = a.cin_p;
@@ -1019,17 +1047,17 @@ __global__ void __launch_bounds__(kThreads, 1) conv_halo_kernel(const ConvArgs a
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int8_t *>(a.wp), (short)0, (int)((int64_t)a.cout_pad * a.pack_stride), 0x00020000);
 
-    // window DMA: instruction j of this wave fills records 16*(wave + 4j) + lane/4
-    // of a half; record f = (rr*2 + cp)*HCC + cc is window row 2*rr + parity,
-    // column 2*cc + cp.  Offsets exclude the chunk; records outside the window or
-    // the image read zeros.
+    // window DMA: instruction j of this wave fills block halo_block(wave, j) of
+    // a half, records 16*block + lane/4; record f = (rr*2 + cp)*HCC + cc is
+    // window row 2*rr + parity, column 2*cc + cp.  Offsets exclude the chunk;
+    // records outside the window or the image read zeros.
     uint32_t h_off[2][HB];
 #pragma unroll
     for (int hp = 0; hp < 2; ++hp)
 #pragma unroll
         for (int j = 0; j < HB; ++j) {
-            const int f = 16 * (wave + 4 * j) + (lane >> 2);
-            const int g = (lane & 3) ^ swz(f);
+            const int f = 16 * halo_block(wave, j, W_BLK) + (lane >> 2);
+            const int g = (lane & 3) ^ swz_win(f);
             const int rr = f / (2 * G::HCC), rem = f - rr * (2 * G::HCC);
             const int cp = rem / G::HCC, cc = rem - cp * G::HCC;
             const int row = 2 * rr + hp, col = 2 * cc + cp;
@@ -1043,41 +1071,56 @@ __global__ void __launch_bounds__(kThreads, 1) conv_halo_kernel(const ConvArgs a
         const uint32_t coff = (uint32_t)(chunk * 64);
 #pragma unroll
         for (int j = 0; j < HB; ++j)
-            dma16(rx, dst + 1024 * (wave + 4 * j), h_off[hp][j] == kOobOffset ? kOobOffset : h_off[hp][j] + coff);
+            dma16(rx, dst + 1024 * halo_block(wave, j, W_BLK),
+                  h_off[hp][j] == kOobOffset ? kOobOffset : h_off[hp][j] + coff);
     };
     uint32_t b_off[PER];
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-        const int nn = 16 * (wave + 4 * j) + (lane >> 2);
-        const int g = (lane & 3) ^ swz(nn);
+        const int nn = 16 * halo_block(wave, j, B_BLK) + (lane >> 2);
+        const int g = (lane & 3) ^ swz_win(nn);
         b_off[j] = (uint32_t)((n0 + nn) * 64 + 16 * g);
     }
-    // Position of a K-step in the order chunk, odd-kh taps, even-kh taps; the
-    // loop advances these incrementally (no divisions per step).
-    struct Pos {
-        int chunk, j, kh, kw, slot;   // slot: weight ring buffer (step % STAGES)
+
+    // K-steps run chunk by chunk, odd-kh taps first, then even-kh taps.  A
+    // cursor follows one step: tap index j in that order, column kw, chunk, and
+    // an offset that advances with the taps (branch-free selects):
+    //  * window cursors: byte offset of the tap's window records,
+    //    (kh & 1)*HALF_BYTES + ((kh >> 1)*2*HCC + (kw & 1)*HCC + (kw >> 1))*64;
+    //  * weight cursors: weight K-block offset ((kh*k + kw)*nchunks + chunk)*cout_pad*64.
+    struct Cursor {
+        int j, kw, chunk;
+        uint32_t off, row_off;
     };
-    auto advance = [&](Pos &p) {
-        ++p.j;
-        if (++p.slot == STAGES) p.slot = 0;
-        if (p.j == ntap) {
-            p.j = 0;
-            ++p.chunk;
-            p.kh = 1;
-            p.kw = 0;
-        } else if (p.j == nodd) {
-            p.kh = 0;
-            p.kw = 0;
-        } else if (++p.kw == k) {
-            p.kw = 0;
-            p.kh += 2;
-        }
+    const uint32_t cp64 = (uint32_t)a.cout_pad * 64u;
+    const uint32_t tap_w = (uint32_t)nchunks * cp64;
+    auto next_win = [&](Cursor &c) {
+        const bool end_tap = c.j + 1 == ntap, end_odd = c.j + 1 == nodd, end_row = c.kw + 1 == k;
+        const uint32_t in_row = c.off + ((c.kw & 1) ? (uint32_t)(64 - G::HCC * 64) : (uint32_t)(G::HCC * 64));
+        const uint32_t new_row = end_tap ? (uint32_t)G::HALF_BYTES : end_odd ? 0u : c.row_off + 2u * G::HCC * 64u;
+        c.off = end_row ? new_row : in_row;
+        c.row_off = end_row ? new_row : c.row_off;
+        c.kw = end_row ? 0 : c.kw + 1;
+        c.chunk += end_tap ? 1 : 0;
+        c.j = end_tap ? 0 : c.j + 1;
     };
-    auto issue_b = [&](const Pos &p) {
-        const uint32_t woff = (uint32_t)(((p.kh * k + p.kw) * nchunks + p.chunk) * a.cout_pad * 64);
-        int8_t *sb = bring + p.slot * B_BYTES;
+    auto next_w = [&](Cursor &c) {
+        const bool end_tap = c.j + 1 == ntap, end_odd = c.j + 1 == nodd, end_row = c.kw + 1 == k;
+        const uint32_t new_row = end_tap ? (uint32_t)k * tap_w + (uint32_t)(c.chunk + 1) * cp64
+                                         : end_odd ? (uint32_t)c.chunk * cp64 : c.row_off + 2u * (uint32_t)k * tap_w;
+        c.off = end_row ? new_row : c.off + tap_w;
+        c.row_off = end_row ? new_row : c.row_off;
+        c.kw = end_row ? 0 : c.kw + 1;
+        c.chunk += end_tap ? 1 : 0;
+        c.j = end_tap ? 0 : c.j + 1;
+    };
+    // weight step of cursor c into ring slot `slot`; steps past the last one
+    // read zeros into a slot no remaining step uses (uniform wait counts)
+    auto issue_b = [&](const Cursor &c, int slot, bool real) {
+        int8_t *sb = bring + slot * B_BYTES;
 #pragma unroll
-        for (int j = 0; j < PER; ++j) dma16(rw, sb + 1024 * (wave + 4 * j), b_off[j] + woff);
+        for (int j = 0; j < PER; ++j)
+            dma16(rw, sb + 1024 * halo_block(wave, j, B_BLK), real ? b_off[j] + c.off : kOobOffset);
     };
 
     v4i acc[FM][FN];
@@ -1086,101 +1129,105 @@ __global__ void __launch_bounds__(kThreads, 1) conv_halo_kernel(const ConvArgs a
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
+    // fragment bases: this wave's pixels are output row `wave`, columns
+    // 16*i + fr (A rows i = 0, 1 are 16 window records apart: same swizzle,
+    // +1024 B); B column groups j are 1024 B apart
     const int fr = lane & 15, fg = lane >> 4;
-    int f_base[FM];   // window record of tap (0, 0) for this lane's points
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int m = wave * TM + 16 * i + fr;
-        const int oh = m / TW, ow = m - oh * TW;
-        f_base[i] = oh * 2 * G::HCC + ow;
-    }
-    int fb_off[FN];
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-        const int nn = 16 * j + fr;
-        fb_off[j] = nn * 64 + 16 * (fg ^ swz(nn));
-    }
-    auto afrag = [&](const Pos &p, int i) {
-        const int f = f_base[i] + ((p.kh >> 1) * 2 + (p.kw & 1)) * G::HCC + (p.kw >> 1);
-        return *reinterpret_cast<const v4i *>(halo + (p.kh & 1) * G::HALF_BYTES + f * 64 + 16 * (fg ^ swz(f)));
-    };
-    auto bfrag = [&](const Pos &p, int j) {
-        return *reinterpret_cast<const v4i *>(bring + p.slot * B_BYTES + fb_off[j]);
-    };
+    const uint32_t la0 = (uint32_t)((wave * 2 * G::HCC + fr) * 64 + 16 * fg);
+    const uint32_t lb = RING_BASE + (uint32_t)(fr * 64 + 16 * (fg ^ swz_win(fr)));
+    auto lds_v4 = [&](uint32_t addr) { return *reinterpret_cast<const v4i *>(lds + addr); };
 
-    // B fragments stream through a ring of RING registers (RING-1 reads ahead,
-    // continuing into step ks+1); step ks+1's A fragments go to the other A set.
-    // Reads past the last step hit stale, in-bounds LDS and are never used.
     constexpr int RING = 4;
-    static_assert(FN % RING == 0 && FN >= RING, "ring");
+    static_assert(FN % RING == 0 && FN >= RING && 2 * FM <= FN, "ring");
     v4i ring[RING];
     v4i fa0[FM], fa1[FM];
 
     // prologue: both halves of chunk 0, weight steps 0 .. STAGES-2
-    Pos p_cur = {0, 0, 1, 0, 0};   // step ks (odd-kh taps first: kh = 1)
+    Cursor c_cur = {0, 0, 0, (uint32_t)G::HALF_BYTES, (uint32_t)G::HALF_BYTES};   // step ks (kh = 1 first)
+    Cursor c_iss = {0, 0, 0, (uint32_t)k * tap_w, (uint32_t)k * tap_w};          // next weight step to issue
     burst(1, 0);
     burst(0, 0);
-    Pos p_iss = p_cur;            // next weight step to issue
 #pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s)
-        if (s < nks) {
-            issue_b(p_iss);
-            advance(p_iss);
-        }
-    if (STAGES - 1 <= nks) wait_vmcnt<(STAGES - 2) * PER>();
-    else wait_vmcnt<0>();
+    for (int s = 0; s < STAGES - 1; ++s) {
+        issue_b(c_iss, s, s < nks);
+        next_w(c_iss);
+    }
+    int iss_step = STAGES - 1;
+    wait_vmcnt<(STAGES - 2) * PER>();
     __builtin_amdgcn_s_barrier();
+    {
+        const uint32_t a0 = win_addr(la0 + c_cur.off);
+        fa0[0] = lds_v4(a0);
+        fa0[1] = lds_v4(a0 + 1024);
 #pragma unroll
-    for (int i = 0; i < FM; ++i) fa0[i] = afrag(p_cur, i);
-#pragma unroll
-    for (int r = 0; r < RING - 1; ++r) ring[r] = bfrag(p_cur, r);
-
-    Pos p_nxt = p_cur;            // step ks+1
-    advance(p_nxt);
+        for (int r = 0; r < RING - 1; ++r) ring[r] = lds_v4(lb + r * 1024);
+    }
+    Cursor c_nxt = c_cur;          // step ks+1
+    next_win(c_nxt);
+    int slot = 0;                  // ring slot of step ks
     // at step t's wait, since_burst = t - 1 - (step of the last window burst)
     int since_burst = 2;
-    auto stage = [&](int ks, v4i (&acur)[FM], v4i (&anext)[FM]) {
-        // weight steps ks and ks+1 (and window halves read by them) must have
+    auto stage = [&](v4i (&acur)[FM], v4i (&anext)[FM]) {
+        // weight steps ks and ks+1 (and the window halves they read) must have
         // landed: everything but the last two weight steps, plus a window burst
         // issued in either of the two previous steps (after weight step ks+1)
-        if (ks + STAGES - 2 < nks) {
-            if (since_burst <= 1) wait_vmcnt<(STAGES - 3) * PER + HB>();
-            else wait_vmcnt<(STAGES - 3) * PER>();
-        } else {
-            wait_vmcnt<0>();
-        }
+        if (since_burst <= 1) wait_vmcnt<(STAGES - 3) * PER + HB>();
+        else wait_vmcnt<(STAGES - 3) * PER>();
         __builtin_amdgcn_s_barrier();
         // window refills: even half of this chunk at its first (odd) step, odd
         // half of the next chunk at this chunk's first even step
         ++since_burst;
-        if (p_cur.j == 0 && p_cur.chunk >= 1) {
-            burst(0, p_cur.chunk);
+        // (the distinct asm markers keep the two branches from being merged
+        // into one path that selects its operands on every step)
+        if (c_cur.j == 0 && c_cur.chunk >= 1) {
+            burst(0, c_cur.chunk);
             since_burst = 0;
-        } else if (p_cur.j == nodd && p_cur.chunk + 1 < nchunks) {
-            burst(1, p_cur.chunk + 1);
+            asm volatile("; window refill, even rows" ::: "memory");
+        } else if (c_cur.j == nodd && c_cur.chunk + 1 < nchunks) {
+            burst(1, c_cur.chunk + 1);
             since_burst = 0;
+            asm volatile("; window refill, odd rows" ::: "memory");
         }
-        if (ks + STAGES - 1 < nks) {
-            issue_b(p_iss);
-            advance(p_iss);
-        }
+        const int slot_nxt = slot == STAGES - 1 ? 0 : slot + 1;
+        const int slot_iss = slot == 0 ? STAGES - 1 : slot - 1;
+        issue_b(c_iss, slot_iss, iss_step < nks);
+        next_w(c_iss);
+        ++iss_step;
+        const uint32_t bcur = lb + (uint32_t)(slot * B_BYTES), bnxt = lb + (uint32_t)(slot_nxt * B_BYTES);
+        const uint32_t a0 = win_addr(la0 + c_nxt.off);
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
             const int jj = j + RING - 1;
-            ring[jj % RING] = jj < FN ? bfrag(p_cur, jj) : bfrag(p_nxt, jj - FN);
-            if (j >= FN - FM) anext[j - (FN - FM)] = afrag(p_nxt, j - (FN - FM));
+            ring[jj % RING] = jj < FN ? lds_v4(bcur + jj * 1024) : lds_v4(bnxt + (jj - FN) * 1024);
+            if ((j & 1) && j < 2 * FM) anext[j >> 1] = lds_v4(a0 + (j >> 1) * 1024);
 #pragma unroll
             for (int i = 0; i < FM; ++i)
                 acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ring[j % RING], acur[i], acc[i][j], 0, 0, 0);
         }
-        p_cur = p_nxt;
-        advance(p_nxt);
-    };
-    for (int ks = 0; ks < nks; ++ks) {
-        stage(ks, fa0, fa1);
+        // keep the reads RING-1 fragments ahead of the MFMAs that use them
 #pragma unroll
-        for (int i = 0; i < FM; ++i) fa0[i] = fa1[i];
+        for (int j = 0; j < FM; ++j) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, FM, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, FM, 0);
+        }
+#pragma unroll
+        for (int j = 2 * FM; j < FN; ++j) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, FM, 0);
+        }
+        c_cur = c_nxt;
+        next_win(c_nxt);
+        slot = slot_nxt;
+    };
+    int ks = 0;
+    for (; ks + 1 < nks; ks += 2) {
+        stage(fa0, fa1);
+        stage(fa1, fa0);
     }
+    if (ks < nks) stage(fa0, fa1);
+    wait_vmcnt<0>();   // no DMA may still be writing LDS
     __syncthreads();   // every wave is done with the window and the ring
     float *col = reinterpret_cast<float *>(lds);
     column_factors<BN>(a, tile, col, col + BN);
@@ -1209,7 +1256,7 @@ hipError_t launch_halo(const ConvArgs &a, hipStream_t st) {
         b.M = (int64_t)gn * a.gh * a.gw;
         const int64_t tiles = set_tiles(b, HaloGeom::TH, HaloGeom::TW, BN);
         if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-        conv_halo_kernel<BN, STAGES, E><<<(unsigned)tiles, kThreads, 0, st>>>(b);
+        conv_halo_kernel<BN, STAGES, E><<<(unsigned)tiles, kHaloThreads, 0, st>>>(b);
     }
     return hipGetLastError();
 }
