@@ -28,8 +28,11 @@ namespace {
 
 constexpr int kThreads = 256;
 
-// 16-B chunk swizzle of a 64-B LDS operand row (A and B tiles).
-__device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
+// 16-B chunk swizzle of a 64-B LDS operand row (A and B tiles): chunk q of row
+// f sits at position q ^ ((f >> 1) & 3).  A ds_read_b128 serves 8 lanes per
+// pass from 32 banks; 8 consecutive rows then cover all 32 banks once, from any
+// starting row, so fragment reads of consecutive rows are conflict-free.
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 3; }
 
 // A block's tile: sample nb, first grid point (gi0, gj0); local row m is the
 // point (gi0 + m / TW, gj0 + m % TW).  Tiles never straddle samples.
@@ -811,6 +814,12 @@ constexpr uint32_t kOobOffset = 0x80000000u;   // beyond every buffer (< 2 GiB e
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, int8_t *lds_dst, uint32_t off) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, HATQ_LDS_PTR(lds_dst), 16, off, 0, 0, 0);
 }
+// The same with a wave-uniform offset added in the scalar offset field (the
+// per-lane part off stays loop-invariant; an off past num_records still reads
+// zeros).
+__device__ __forceinline__ void dma16s(__amdgpu_buffer_rsrc_t r, int8_t *lds_dst, uint32_t off, uint32_t soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, HATQ_LDS_PTR(lds_dst), 16, off, soff, 0, 0);
+}
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -984,13 +993,11 @@ struct HaloGeom {
     static constexpr int HALF_BYTES = INSTR * 4 * 1024;
 };
 
-// Window and weight records use the 16-B chunk swizzle q ^ ((f >> 2) & 3)
-// (conflict-free for any 16 consecutive records).  With a = byte offset of
-// record f (bits 4-9 of every half's base are zero), the physical address of
-// chunk q is aq ^ ((aq >> 4) & 0x30) with aq = a + 16*q, so a fragment address
+// Window and weight records use the operand swizzle.  With a = byte offset of
+// record f (bits 0-8 of every region's base are zero), the physical address of
+// chunk q is aq ^ ((aq >> 3) & 0x30) with aq = a + 16*q, so a fragment address
 // is one add and two bit operations per tap.
-__device__ __forceinline__ int swz_win(int f) { return (f >> 2) & 3; }
-__device__ __forceinline__ uint32_t win_addr(uint32_t aq) { return aq ^ ((aq >> 4) & 0x30u); }
+__device__ __forceinline__ uint32_t win_addr(uint32_t aq) { return aq ^ ((aq >> 3) & 0x30u); }
 
 // Eight waves (two per SIMD, so one wave's MFMAs run while the other waits
 // on LDS), each owning one 32-pixel output row of the tile by all BN channels.
@@ -1023,7 +1030,7 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo_kernel(const ConvAr
     static_assert(BN % 64 == 0 && STAGES == 5, "tile");
     static_assert(FM == 2 && TM == TW, "one output row per wave");
     static_assert(B_BLK >= kHaloWaves && W_BLK >= kHaloWaves && W_BLK * 1024 <= G::HALF_BYTES, "DMA blocks");
-    static_assert((G::HALF_BYTES & 0x3F0) == 0 && (RING_BASE & 0x3F0) == 0 && (B_BYTES & 0x3F0) == 0, "swizzle bits");
+    static_assert((G::HALF_BYTES & 0x1FF) == 0 && (RING_BASE & 0x1FF) == 0 && (B_BYTES & 0x1FF) == 0, "swizzle bits");
     __shared__ __attribute__((aligned(1024))) int8_t lds[2 * G::HALF_BYTES + STAGES * B_BYTES];
     int8_t *const halo = lds;
     int8_t *const bring = lds + RING_BASE;
@@ -1057,7 +1064,7 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo_kernel(const ConvAr
 #pragma unroll
         for (int j = 0; j < HB; ++j) {
             const int f = 16 * halo_block(wave, j, W_BLK) + (lane >> 2);
-            const int g = (lane & 3) ^ swz_win(f);
+            const int g = (lane & 3) ^ swz(f);
             const int rr = f / (2 * G::HCC), rem = f - rr * (2 * G::HCC);
             const int cp = rem / G::HCC, cc = rem - cp * G::HCC;
             const int row = 2 * rr + hp, col = 2 * cc + cp;
@@ -1078,7 +1085,7 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo_kernel(const ConvAr
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
         const int nn = 16 * halo_block(wave, j, B_BLK) + (lane >> 2);
-        const int g = (lane & 3) ^ swz_win(nn);
+        const int g = (lane & 3) ^ swz(nn);
         b_off[j] = (uint32_t)((n0 + nn) * 64 + 16 * g);
     }
 
@@ -1134,7 +1141,7 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo_kernel(const ConvAr
     // +1024 B); B column groups j are 1024 B apart
     const int fr = lane & 15, fg = lane >> 4;
     const uint32_t la0 = (uint32_t)((wave * 2 * G::HCC + fr) * 64 + 16 * fg);
-    const uint32_t lb = RING_BASE + (uint32_t)(fr * 64 + 16 * (fg ^ swz_win(fr)));
+    const uint32_t lb = RING_BASE + (uint32_t)(fr * 64 + 16 * (fg ^ swz(fr)));
     auto lds_v4 = [&](uint32_t addr) { return *reinterpret_cast<const v4i *>(lds + addr); };
 
     constexpr int RING = 4;
@@ -1235,8 +1242,232 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo_kernel(const ConvAr
     epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, col, col + BN);
 }
 
+// Compile-time unrolling: f(integral_constant<int, J>) for J = 0 .. N-1.
+template <typename F, int... J>
+__device__ __forceinline__ void unroll_seq(F &&f, std::integer_sequence<int, J...>) {
+    (f(std::integral_constant<int, J>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void unroll(F &&f) {
+    unroll_seq(f, std::make_integer_sequence<int, N>{});
+}
+
+// The 5 x 5 window conv with every K-step of a chunk unrolled: 25 steps per
+// chunk and a 5-slot weight ring, so a step's ring slot, tap, window offset
+// and wait count are compile-time constants.  The per-lane fragment addresses
+// of the 15 distinct tap offsets are computed once per block, both window
+// refills are issued every chunk (the odd-row refill after the last chunk
+// reads zeros into rows no later step uses), and the even half of chunk 0 is
+// loaded at the first step like every other chunk's.
+template <int BN, typename E>
+__global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvArgs a) {
+    using G = HaloGeom;
+    constexpr int K = 5, NTAP = K * K, NODD = (K >> 1) * K, SLOTS = 5;
+    static_assert(NTAP % SLOTS == 0, "ring slot of a step is fixed within a chunk");
+    constexpr int TH = G::TH, TW = G::TW;
+    constexpr int BM = TH * TW;
+    constexpr int TM = BM / kHaloWaves;
+    constexpr int FM = TM / 16;
+    constexpr int FN = BN / 16;
+    constexpr int B_BLK = BN / 16;
+    constexpr int PER = (B_BLK + kHaloWaves - 1) / kHaloWaves;
+    constexpr int W_BLK = (G::RECS + 15) / 16;
+    constexpr int HB = (W_BLK + kHaloWaves - 1) / kHaloWaves;
+    constexpr int B_BYTES = BN * 64;
+    constexpr uint32_t RING_BASE = 2 * G::HALF_BYTES;
+    static_assert(BN % 64 == 0 && FM == 2 && TM == TW, "tile");
+    static_assert(B_BLK >= kHaloWaves && W_BLK >= kHaloWaves && W_BLK * 1024 <= G::HALF_BYTES, "DMA blocks");
+    static_assert((G::HALF_BYTES & 0x1FF) == 0 && (RING_BASE & 0x1FF) == 0 && (B_BYTES & 0x1FF) == 0, "swizzle bits");
+    static_assert(G::HALF_BYTES + 1024 < 65536 && (SLOTS - 1) * B_BYTES + (FN - 1) * 1024 < 65536, "read offsets");
+    static_assert(2 * (TH - 1) + K <= 2 * G::HR && 2 * (TW - 1) + K <= 2 * G::HCC, "window size");
+    __shared__ __attribute__((aligned(1024))) int8_t lds[2 * G::HALF_BYTES + SLOTS * B_BYTES];
+    int8_t *const halo = lds;
+    int8_t *const bring = lds + RING_BASE;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const Tile tile = block_tile(a, xcd_logical_tile(), TH, TW, BN);
+    const int cin_p = a.cin_p;
+    const int nchunks = cin_p >> 6;
+    const int rows_used = 2 * (TH - 1) + K, cols_used = 2 * (TW - 1) + K;
+    const int ih0 = tile.gi0 * 2 + a.bah, iw0 = tile.gj0 * 2 + a.baw;
+
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int8_t *>(a.xq), (short)0, (int)((int64_t)a.n * a.h * a.w * cin_p), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int8_t *>(a.wp), (short)0, (int)((int64_t)a.cout_pad * a.pack_stride), 0x00020000);
+
+    // window DMA offsets (as in conv_halo_kernel)
+    uint32_t h_off[2][HB];
+#pragma unroll
+    for (int hp = 0; hp < 2; ++hp)
+#pragma unroll
+        for (int j = 0; j < HB; ++j) {
+            const int f = 16 * halo_block(wave, j, W_BLK) + (lane >> 2);
+            const int g = (lane & 3) ^ swz(f);
+            const int rr = f / (2 * G::HCC), rem = f - rr * (2 * G::HCC);
+            const int cp = rem / G::HCC, cc = rem - cp * G::HCC;
+            const int row = 2 * rr + hp, col = 2 * cc + cp;
+            const int ih = ih0 + row, iw = iw0 + col;
+            const bool in = f < G::RECS && row < rows_used && col < cols_used && (unsigned)ih < (unsigned)a.h &&
+                            (unsigned)iw < (unsigned)a.w;
+            h_off[hp][j] = in ? (uint32_t)(((tile.nb * a.h + ih) * a.w + iw) * cin_p + 16 * g) : kOobOffset;
+        }
+    // refill of window half hp with chunk c; zero_fill: the same number of
+    // DMAs reading zeros
+    auto burst = [&](int hp, int chunk) {
+        int8_t *dst = halo + hp * G::HALF_BYTES;
+#pragma unroll
+        for (int j = 0; j < HB; ++j) dma16s(rx, dst + 1024 * halo_block(wave, j, W_BLK), h_off[hp][j], (uint32_t)chunk * 64u);
+    };
+    auto zero_fill = [&](int hp) {
+        int8_t *dst = halo + hp * G::HALF_BYTES;
+#pragma unroll
+        for (int j = 0; j < HB; ++j) dma16s(rx, dst + 1024 * halo_block(wave, j, W_BLK), kOobOffset, 0u);
+    };
+    uint32_t b_off[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int nn = 16 * halo_block(wave, j, B_BLK) + (lane >> 2);
+        const int g = (lane & 3) ^ swz(nn);
+        b_off[j] = (uint32_t)((tile.n0 + nn) * 64 + 16 * g);
+    }
+    const uint32_t cp64 = (uint32_t)a.cout_pad * 64u;
+    const uint32_t tap_w = (uint32_t)nchunks * cp64;
+    // Step j of a chunk: odd kernel rows first (kh = 1, 3), then even (0, 2, 4).
+    auto step_kh = [](int j) { return j < NODD ? 1 + 2 * (j / K) : 2 * ((j - NODD) / K); };
+    auto step_kw = [](int j) { return j < NODD ? j % K : (j - NODD) % K; };
+    // weight step J of the chunk at chunk_off into its slot; or zeros into it
+    auto issue_b = [&](auto Jc, uint32_t chunk_off) {
+        constexpr int J = decltype(Jc)::value;
+        constexpr int TAP = step_kh(J) * K + step_kw(J);
+        int8_t *sb = bring + (J % SLOTS) * B_BYTES;
+        const uint32_t woff = (uint32_t)TAP * tap_w + chunk_off;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) dma16s(rw, sb + 1024 * halo_block(wave, j, B_BLK), b_off[j], woff);
+    };
+    auto issue_zero = [&](auto Jc) {
+        constexpr int J = decltype(Jc)::value;
+        int8_t *sb = bring + (J % SLOTS) * B_BYTES;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) dma16s(rw, sb + 1024 * halo_block(wave, j, B_BLK), kOobOffset, 0u);
+    };
+
+    // per-lane A fragment addresses of the 15 window offsets (kh >> 1, kw):
+    // s = (kh >> 1)*2*HCC + (kw & 1)*HCC + (kw >> 1) records; the parity half
+    // and the second fragment (+16 records, same swizzle) are immediates
+    const int fr = lane & 15, fg = lane >> 4;
+    const uint32_t la0 = (uint32_t)((wave * 2 * G::HCC + fr) * 64 + 16 * fg);
+    uint32_t pa[3 * K];
+#pragma unroll
+    for (int r = 0; r < 3; ++r)
+#pragma unroll
+        for (int kw = 0; kw < K; ++kw)
+            pa[r * K + kw] = win_addr(la0 + (uint32_t)((r * 2 * G::HCC + (kw & 1) * G::HCC + (kw >> 1)) * 64));
+    uint32_t lb = RING_BASE + (uint32_t)(fr * 64 + 16 * (fg ^ swz(fr)));
+    // opaque bases: with known low bits the compiler would turn base + offset
+    // into an or and keep one register per constant offset instead of using
+    // the read's offset field
+    asm volatile("" : "+v"(lb));
+#pragma unroll
+    for (int r = 0; r < 3 * K; ++r) asm volatile("" : "+v"(pa[r]));
+    auto lds_v4 = [&](uint32_t addr) { return *reinterpret_cast<const v4i *>(lds + addr); };
+    auto afrag = [&](auto Jc, int i) {
+        constexpr int J = decltype(Jc)::value;
+        constexpr int KH = step_kh(J % NTAP), KW = step_kw(J % NTAP);
+        return lds_v4(pa[(KH >> 1) * K + KW] + (KH & 1) * G::HALF_BYTES + i * 1024);
+    };
+    auto bfrag = [&](auto Jc, int jj) {
+        constexpr int J = decltype(Jc)::value;
+        return lds_v4(lb + (J % SLOTS) * B_BYTES + jj * 1024);
+    };
+
+    v4i acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+
+    constexpr int RING = 4;
+    static_assert(FN % RING == 0 && 2 * FM <= FN, "ring");
+    v4i ring[RING];
+    v4i fa0[FM], fa1[FM];
+
+    // prologue: odd half of chunk 0, weight steps 0 .. 3
+    static_assert(SLOTS - 1 <= NTAP, "prologue within chunk 0");
+    burst(1, 0);
+    unroll<SLOTS - 1>([&](auto Jc) { issue_b(Jc, 0u); });
+    wait_vmcnt<(SLOTS - 2) * PER>();
+    __builtin_amdgcn_s_barrier();
+    fa0[0] = afrag(std::integral_constant<int, 0>{}, 0);
+    fa0[1] = afrag(std::integral_constant<int, 0>{}, 1);
+#pragma unroll
+    for (int r = 0; r < RING - 1; ++r) ring[r] = bfrag(std::integral_constant<int, 0>{}, r);
+
+    for (int c = 0; c < nchunks; ++c) {
+        const uint32_t coff = (uint32_t)c * cp64, coff1 = coff + cp64;
+        const bool more = c + 1 < nchunks;
+        unroll<NTAP>([&](auto Jc) {
+            constexpr int J = decltype(Jc)::value;
+            v4i(&acur)[FM] = (J & 1) ? fa1 : fa0;
+            v4i(&anext)[FM] = (J & 1) ? fa0 : fa1;
+            // weight step J+1 (and the window halves read by steps J, J+1)
+            // landed: all but the last two weight steps, plus a refill issued
+            // in either of the two previous steps
+            if constexpr (J == 1 || J == 2 || J == NODD + 1 || J == NODD + 2)
+                wait_vmcnt<(SLOTS - 3) * PER + HB>();
+            else
+                wait_vmcnt<(SLOTS - 3) * PER>();
+            __builtin_amdgcn_s_barrier();
+            if constexpr (J == 0) burst(0, c);   // even rows of this chunk
+            if constexpr (J == NODD) {          // odd rows of the next chunk
+                if (more) burst(1, c + 1);
+                else zero_fill(1);
+            }
+            if constexpr (J + SLOTS - 1 < NTAP) {
+                issue_b(std::integral_constant<int, J + SLOTS - 1>{}, coff);
+            } else {
+                if (more) issue_b(std::integral_constant<int, J + SLOTS - 1 - NTAP>{}, coff1);
+                else issue_zero(std::integral_constant<int, J + SLOTS - 1 - NTAP>{});
+            }
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int jj = j + RING - 1;
+                ring[jj % RING] = jj < FN ? bfrag(Jc, jj) : bfrag(std::integral_constant<int, J + 1>{}, jj - FN);
+                if ((j & 1) && j < 2 * FM) anext[j >> 1] = afrag(std::integral_constant<int, J + 1>{}, j >> 1);
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ring[j % RING], acur[i], acc[i][j], 0, 0, 0);
+            }
+#pragma unroll
+            for (int j = 0; j < FM; ++j) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, FM, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, FM, 0);
+            }
+#pragma unroll
+            for (int j = 2 * FM; j < FN; ++j) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, FM, 0);
+            }
+        });
+        // NTAP is odd: the next chunk's first A fragments are in fa1
+#pragma unroll
+        for (int i = 0; i < FM; ++i) fa0[i] = fa1[i];
+    }
+    wait_vmcnt<0>();   // no DMA may still be writing LDS
+    __syncthreads();   // every wave is done with the window and the ring
+    float *col = reinterpret_cast<float *>(lds);
+    column_factors<BN>(a, tile, col, col + BN);
+    __syncthreads();
+    epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, col, col + BN);
+}
+
 template <int BN, int STAGES, typename E>
 hipError_t launch_halo(const ConvArgs &a, hipStream_t st) {
+    static_assert(STAGES == 5, "ring");
     // keep every buffer under 2 GiB (32-bit buffer offsets, kOobOffset out of
     // range): launch over groups of whole samples
     const int64_t per_sample = (int64_t)a.h * a.w * a.cin_p;
@@ -1256,7 +1487,8 @@ hipError_t launch_halo(const ConvArgs &a, hipStream_t st) {
         b.M = (int64_t)gn * a.gh * a.gw;
         const int64_t tiles = set_tiles(b, HaloGeom::TH, HaloGeom::TW, BN);
         if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-        conv_halo_kernel<BN, STAGES, E><<<(unsigned)tiles, kHaloThreads, 0, st>>>(b);
+        if (a.k == 5) conv_halo5_kernel<BN, E><<<(unsigned)tiles, kHaloThreads, 0, st>>>(b);
+        else conv_halo_kernel<BN, STAGES, E><<<(unsigned)tiles, kHaloThreads, 0, st>>>(b);
     }
     return hipGetLastError();
 }
