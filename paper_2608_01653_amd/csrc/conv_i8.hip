@@ -827,6 +827,12 @@ __device__ __forceinline__ void wait_vmcnt() {
     // s_waitcnt simm16 (gfx9): vmcnt[3:0], expcnt[6:4]=7, lgkmcnt[11:8]=15, vmcnt_hi[15:14]
     __builtin_amdgcn_s_waitcnt((N & 15) | 0x70 | 0xF00 | ((N >> 4) << 14));
 }
+// The same, and this wave's LDS accesses done (lgkmcnt 0).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lds() {
+    static_assert(N >= 0 && N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 15) | 0x70 | ((N >> 4) << 14));
+}
 
 template <int TH, int TW, int BN, int STAGES, typename E>
 __global__ void __launch_bounds__(kThreads, 1) conv_pipe_kernel(const ConvArgs a) {
@@ -1280,9 +1286,12 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     static_assert((G::HALF_BYTES & 0x1FF) == 0 && (RING_BASE & 0x1FF) == 0 && (B_BYTES & 0x1FF) == 0, "swizzle bits");
     static_assert(G::HALF_BYTES + 1024 < 65536 && (SLOTS - 1) * B_BYTES + (FN - 1) * 1024 < 65536, "read offsets");
     static_assert(2 * (TH - 1) + K <= 2 * G::HR && 2 * (TW - 1) + K <= 2 * G::HCC, "window size");
-    __shared__ __attribute__((aligned(1024))) int8_t lds[2 * G::HALF_BYTES + SLOTS * B_BYTES];
+    // one LDS object (window halves, weight ring, the tile's column factors):
+    // a second one makes the compiler wait for every LDS DMA before each read
+    __shared__ __attribute__((aligned(1024))) int8_t lds[2 * G::HALF_BYTES + SLOTS * B_BYTES + 2 * BN * 4];
     int8_t *const halo = lds;
     int8_t *const bring = lds + RING_BASE;
+    float *const s_col = reinterpret_cast<float *>(lds + RING_BASE + SLOTS * B_BYTES);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -1398,7 +1407,9 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     static_assert(SLOTS - 1 <= NTAP, "prologue within chunk 0");
     burst(1, 0);
     unroll<SLOTS - 1>([&](auto Jc) { issue_b(Jc, 0u); });
-    wait_vmcnt<(SLOTS - 2) * PER>();
+    // the epilogue's column factors, while the first DMAs are in flight
+    column_factors<BN>(a, tile, s_col, s_col + BN);
+    wait_vmcnt_lds<(SLOTS - 2) * PER>();
     __builtin_amdgcn_s_barrier();
     fa0[0] = afrag(std::integral_constant<int, 0>{}, 0);
     fa0[1] = afrag(std::integral_constant<int, 0>{}, 1);
@@ -1457,12 +1468,8 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
 #pragma unroll
         for (int i = 0; i < FM; ++i) fa0[i] = fa1[i];
     }
-    wait_vmcnt<0>();   // no DMA may still be writing LDS
-    __syncthreads();   // every wave is done with the window and the ring
-    float *col = reinterpret_cast<float *>(lds);
-    column_factors<BN>(a, tile, col, col + BN);
-    __syncthreads();
-    epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, col, col + BN);
+    wait_vmcnt<0>();   // no DMA may still be writing LDS when the block ends
+    epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, s_col, s_col + BN);
 }
 
 template <int BN, int STAGES, typename E>
