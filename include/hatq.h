@@ -61,7 +61,9 @@ typedef enum { HATQ_DH = 0, HATQ_WH = 1 } hatq_form;
 typedef enum {
     HATQ_OUT_I32 = 0,       /* raw INT32 accumulators [n][ho][wo][cout_pad], no bias;
                                WH accumulators stay in the output Hadamard basis */
-    HATQ_OUT_F32 = 1        /* dequantized fp32 output [n][ho][wo][cout], original basis */
+    HATQ_OUT_F32 = 1,       /* dequantized fp32 output [n][ho][wo][cout], original basis */
+    HATQ_OUT_I8 = 2         /* the next operand's INT8 codes [n][ho][wo][cout]: produced by
+                               hatq_conv_int8_requant (hatq_conv_int8 rejects this mode) */
 } hatq_out_mode;
 
 /* One layer's geometry.  Square kernels only.
@@ -172,13 +174,35 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
  *     receives, per sample, max |B_{next} y| with block size next_hblock (1: max
  *     |y|), the exact value hatq_fwht_quant_act would compute from y; the next
  *     layer can then quantize y reading it once.  It is overwritten, not
- *     accumulated.
+ *     accumulated.  y may be NULL in F32 mode when next_absmax is given: the
+ *     call then only produces next_absmax (the first pass of
+ *     hatq_conv_int8_requant's dynamic scale).
  * Supported: cin_pad % 64 == 0 with k <= 8, or cin_pad <= 4 with k*k*cin_pad <= 128;
  * cout_pad % 64 == 0; WH block and next_hblock at most 64.  Transposed: stride 2.
  * xq and y must be 16-byte aligned. */
 int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act_scale,
                        int32_t n, int32_t h, int32_t w, int32_t out_mode, void *y,
                        int32_t next_hblock, float *next_absmax, void *stream);
+
+/* INT8 convolution with the requantizing epilogue (step a6, I8 output; Eq.
+ * integer_requantization with the dynamic per-tensor scale of Eq. symmetric_q):
+ * the layer's fp32 output y (as hatq_conv_int8 computes it in F32 mode) is
+ * transformed for the next layer, y' = B_next y with blocks of next_hblock (1:
+ * y' = y, the WH input case), and quantized in registers,
+ *   yq = clamp(rne(fl(y' / s)), -127, 127),
+ * exactly as hatq_fwht_quant_act(y, ..., next_hblock, absmax = next_absmax)
+ * would from y; y itself is never written.
+ *   next_absmax: device fp32 [n] with max |B_next y| per sample (from an
+ *     earlier hatq_conv_int8 call with y = NULL, or an upper bound of it); the
+ *     scale is then s = fl32(next_absmax / 127) (1 if it is 0) and is written to
+ *     next_scale.  NULL: next_scale [n] is an input, a static scale.
+ *   next_scale: device fp32 [n], the next layer's act_scale.
+ *   yq:        device int8 [n][ho][wo][cout], the next layer's xq.
+ * Supported: as hatq_conv_int8, with cout % 4 == 0 and cout % next_hblock == 0. */
+int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const float *act_scale,
+                               int32_t n, int32_t h, int32_t w, int32_t next_hblock,
+                               const float *next_absmax, float *next_scale, int8_t *yq,
+                               void *stream);
 
 /* Workspace bytes of hatq_layer_forward for an input of n x h x w. */
 size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w);

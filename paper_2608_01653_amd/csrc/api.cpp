@@ -121,7 +121,8 @@ int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next
 // row i + (ph + pad - kh)/2 (gather form of the transposed convolution).
 int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, int32_t n,
                       int32_t h, int32_t w, int32_t mode, void *y, int32_t next_hblock,
-                      float *next_absmax, hipStream_t st) {
+                      float *next_absmax, hipStream_t st, const float *q_absmax = nullptr,
+                      float *q_scale = nullptr) {
     const hatq_conv_desc &d = W->d;
     int32_t ho, wo;
     if (out_hw(&d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
@@ -134,6 +135,8 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
     a.bias = W->bias;
     a.y = y;
     a.next_absmax = next_absmax;
+    a.q_absmax = q_absmax;
+    a.q_scale = q_scale;
     a.n = n;
     a.h = h;
     a.w = w;
@@ -149,7 +152,7 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
     a.form = W->form;
     a.mode = mode;
     a.hblock = d.hblock;
-    a.next_hblock = next_absmax ? next_hblock : 0;
+    a.next_hblock = (next_absmax || mode == HATQ_OUT_I8) ? next_hblock : 0;
     const bool small = W->cin_pad <= 4 && W->k_total <= 128;
     if (!d.transposed) {
         a.gh = ho;
@@ -323,16 +326,38 @@ int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act
                        void *stream) {
     int32_t s = check_weights(W);
     if (s != HATQ_OK) return s;
-    if (!xq || !act_scale || !y || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
+    if (!xq || !act_scale || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
     if (out_mode != HATQ_OUT_I32 && out_mode != HATQ_OUT_F32) return HATQ_EINVAL;
     if (out_mode == HATQ_OUT_I32 && next_absmax) return HATQ_EINVAL;
-    if (!aligned(xq, 16) || !aligned(y, 16) || !aligned(act_scale, 4)) return HATQ_EINVAL;
+    // y may be NULL only when the call is for next_absmax alone
+    if (!y && !(out_mode == HATQ_OUT_F32 && next_absmax)) return HATQ_EINVAL;
+    if (!aligned(xq, 16) || (y && !aligned(y, 16)) || !aligned(act_scale, 4)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
     if ((s = check_next(W, next_hblock, next_absmax)) != HATQ_OK) return s;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
     return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, next_hblock, next_absmax,
                          static_cast<hipStream_t>(stream));
+}
+
+int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const float *act_scale, int32_t n,
+                               int32_t h, int32_t w, int32_t next_hblock, const float *next_absmax,
+                               float *next_scale, int8_t *yq, void *stream) {
+    int32_t s = check_weights(W);
+    if (s != HATQ_OK) return s;
+    if (!xq || !act_scale || !next_scale || !yq || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
+    if (!aligned(xq, 16) || !aligned(yq, 4) || !aligned(act_scale, 4) || !aligned(next_scale, 4))
+        return HATQ_EINVAL;
+    if (next_absmax && !aligned(next_absmax, 4)) return HATQ_EINVAL;
+    if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    // the transform and the code layout follow the next operand's blocks
+    const float *probe = next_absmax ? next_absmax : next_scale;
+    if ((s = check_next(W, next_hblock, probe)) != HATQ_OK) return s;
+    if (W->d.cout % 4) return HATQ_EUNSUPPORTED;
+    int32_t ho, wo;
+    if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
+    return conv_launches(W, xq, act_scale, n, h, w, HATQ_OUT_I8, yq, next_hblock, nullptr,
+                         static_cast<hipStream_t>(stream), next_absmax, next_scale);
 }
 
 size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w) {

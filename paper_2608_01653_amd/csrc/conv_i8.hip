@@ -187,11 +187,13 @@ template <typename E>
 struct EpiFlags {
     static constexpr int WB = E::WB, NB = E::NB;
     static constexpr bool generic = WB == -1;
-    bool f32, wh, want_abs;
+    bool f32, wh, want_abs, i8, store;
     __device__ explicit EpiFlags(const ConvArgs &a) {
-        f32 = generic ? a.mode != 0 : true;
+        f32 = generic ? a.mode != 0 : true;   // the fp32 arithmetic (F32 and I8 modes)
         wh = generic ? f32 && a.form == 1 : WB != 0;
-        want_abs = generic ? f32 && a.next_absmax != nullptr && a.next_hblock > 0 : NB != 0;
+        want_abs = generic ? a.mode == 1 && a.next_absmax != nullptr && a.next_hblock > 0 : NB != 0;
+        i8 = generic && a.mode == 2;
+        store = !i8 && a.y != nullptr;        // I32 / F32 values
     }
 };
 
@@ -222,11 +224,34 @@ __device__ __forceinline__ void store_group_impl(const ConvArgs &a, const Tile &
 }
 #define store_group(a, t, row0, lane, i, k, v) store_group_impl<TW, FN, E>(a, t, row0, lane, i, k, v)
 
+// Codes of 16 values as the activation quantizer rounds them: t = fl(u * r)
+// rounded with the magic constant, and the IEEE quotient fl(u / s) for every
+// value of a lane that has one near a half-integer (or when the scale is out of
+// the fast path's range); w[jj] packs the codes of registers 4*jj .. 4*jj+3.
+__device__ __forceinline__ void quant16(const float (&u)[16], float s, float r, bool fast_ok, uint32_t (&w)[4]) {
+    uint32_t c[16];
+    bool near = !fast_ok;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const float tq = clamp127(u[k] * r);
+        const float uf = tq + HATQ_MAGIC;
+        const float kf = uf - HATQ_MAGIC;
+        near |= fabsf(tq - kf) > HATQ_NEAR_TIE;
+        c[k] = __float_as_uint(uf);
+    }
+    if (near) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) c[k] = __float_as_uint(rintf(clamp127(u[k] / s)) + HATQ_MAGIC);
+    }
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) w[jj] = pack_low_bytes(c[4 * jj], c[4 * jj + 1], c[4 * jj + 2], c[4 * jj + 3]);
+}
+
 // The arithmetic: dequantization, WH restore, next-operand absmax (one atomic
-// per wave at most).  With STORE each group is stored as soon as it is final
-// (stores interleave with the arithmetic); without, out holds the values for
-// epilogue_store.
-template <int TW, int FM, int FN, typename E, bool STORE = false>
+// per wave at most) or, in I8 mode, the next operand's codes.  Each group is
+// stored as soon as it is final (stores interleave with the arithmetic); out
+// is the per-group working storage.
+template <int TW, int FM, int FN, typename E>
 __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&acc)[FM][FN], const Tile &t,
                                                  int row0, int lane, const float *col_t, const float *col_b,
                                                  EpiVals<FM, FN> &out) {
@@ -236,7 +261,7 @@ __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&
     constexpr int NBLK = FN / 4;
     const int p = lane & 15, q = lane >> 4;
     const EpiFlags<E> fl(a);
-    const bool f32 = fl.f32, wh = fl.wh, want_abs = fl.want_abs;
+    const bool f32 = fl.f32, wh = fl.wh, want_abs = fl.want_abs, i8 = fl.i8, store = fl.store;
     // the whole tile inside the grid (wave-uniform): no row masking needed
     const bool full = t.gi0 + (row0 + 16 * FM - 1) / TW < a.gh && t.gj0 + TW <= a.gw;
     float wave_m = 0.0f;
@@ -255,6 +280,16 @@ __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&
     // exactly, so max|B y| <= max|z| (1 + 2 gamma_6 * 64) with gamma_6 the
     // six-stage fp32 rounding factor (< 3.6e-7); 1 + 1e-4 covers it.
     const bool z_bound = wh && (generic ? a.hblock == a.next_hblock : WB == NB);
+    // I8 mode: the sample's scale (from the absmax as the activation quantizer
+    // derives it, or given), published by the sample's first tile
+    float qs = 1.0f, qr = 1.0f;
+    bool q_fast = true;
+    if (i8) {
+        qs = a.q_absmax ? act_scale_from_absmax(a.q_absmax[t.nb]) : a.q_scale[t.nb];
+        qr = 1.0f / qs;
+        q_fast = qs >= 0x1p-125f && qs <= 0x1p125f;
+        if (a.q_absmax && t.gi0 == 0 && t.gj0 == 0 && t.n0 == 0 && row0 == 0 && lane == 0) a.q_scale[t.nb] = qs;
+    }
     bool valid[FM];
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
@@ -273,6 +308,7 @@ __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&
                 b4[jj] = *reinterpret_cast<const float4 *>(col_b + cl);
             }
         }
+        const bool blk_full = t.n0 + 64 * k + 64 <= a.cout;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
             float (&v)[16] = out[i][k];
@@ -296,18 +332,17 @@ __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&
                 for (int r = 0; r < 16; ++r) zmax = fmaxf(zmax, fabsf(v[r]));
                 zmax *= (float)a.hblock;   // v holds z / b
             }
-            if (wh) fwht_acc<WB, true>(v, a.hblock);   // the column factors carry the 1/b
-            if constexpr (STORE) {
-                if (valid[i]) store_group(a, t, row0, lane, i, k, v);
-            }
             // (channels past cout are zeroed before the exact transform, which
             // breaks B y = z for a block that holds some)
             bool exact = want_abs;
-            if (want_abs && nbk > 1 && z_bound && t.n0 + 64 * k + 64 <= a.cout)
+            if (want_abs && nbk > 1 && z_bound && blk_full)
                 exact = __builtin_amdgcn_ballot_w64(zmax * 1.0001f + 1e-30f >= seen) != 0;
+            // the restored values are needed for a store, an exact maximum or codes
+            if (wh && (store || exact || i8)) fwht_acc<WB, true>(v, a.hblock);   // the column factors carry the 1/b
+            if (store && valid[i]) store_group(a, t, row0, lane, i, k, v);
             if (NB == 1 && exact) {
                 // no transform: the maximum of |y| over the valid values
-                const bool all = full && t.n0 + 64 * k + 64 <= a.cout;
+                const bool all = full && blk_full;
                 float mm = 0.0f;
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj)
@@ -318,13 +353,13 @@ __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&
                         mm = fmaxf(mm, in ? fabsf(v[4 * jj + r]) : 0.0f);
                     }
                 wave_m = fmaxf(wave_m, mm);
-            } else if (exact) {
+            } else if (exact || i8) {
                 // Rows past the grid and channels past cout are not part of the
                 // next operand.
                 float u[16];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) u[r] = v[r];
-                if (!full || t.n0 + 64 * k + 64 > a.cout) {
+                if (!full || !blk_full) {
 #pragma unroll
                     for (int jj = 0; jj < 4; ++jj)
 #pragma unroll
@@ -333,11 +368,28 @@ __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&
                             if (!valid[i] || ch >= a.cout) u[4 * jj + r] = 0.0f;
                         }
                 }
-                fwht_acc<NB, false>(u, a.next_hblock);
-                float mm = 0.0f;
+                if (i8) {
+                    // codes of B_next y in channel order (restoring butterflies)
+                    fwht_acc<NB, true>(u, a.next_hblock);
+                    uint32_t w[4];
+                    quant16(u, qs, qr, q_fast, w);
+                    if (valid[i]) {
+                        const int m = row0 + 16 * i + p;
+                        int8_t *yq = reinterpret_cast<int8_t *>(a.y) +
+                                     out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW) * a.cout + t.n0;
 #pragma unroll
-                for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(u[r]));
-                wave_m = fmaxf(wave_m, mm);
+                        for (int jj = 0; jj < 4; ++jj) {
+                            const int cl = 64 * k + 16 * jj + 4 * q;
+                            if (t.n0 + cl < a.cout) *reinterpret_cast<uint32_t *>(yq + cl) = w[jj];
+                        }
+                    }
+                } else {
+                    fwht_acc<NB, false>(u, a.next_hblock);
+                    float mm = 0.0f;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(u[r]));
+                    wave_m = fmaxf(wave_m, mm);
+                }
             }
         }
     }
@@ -350,25 +402,11 @@ __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&
     }
 }
 
-// The stores of values computed by epilogue_compute without STORE.
-template <int TW, int FM, int FN, typename E>
-__device__ __forceinline__ void epilogue_store(const ConvArgs &a, const Tile &t, int row0, int lane,
-                                               const EpiVals<FM, FN> &out) {
-    const int p = lane & 15;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int m = row0 + 16 * i + p;
-        if (t.gi0 + m / TW >= a.gh || t.gj0 + m % TW >= a.gw) continue;
-#pragma unroll
-        for (int k = 0; k < FN / 4; ++k) store_group_impl<TW, FN, E>(a, t, row0, lane, i, k, out[i][k]);
-    }
-}
-
 template <int TW, int FM, int FN, typename E>
 __device__ __forceinline__ void epilogue_regs(const ConvArgs &a, const v4i (&acc)[FM][FN], const Tile &t,
                                               int row0, int lane, const float *col_t, const float *col_b) {
     EpiVals<FM, FN> out;
-    epilogue_compute<TW, FM, FN, E, true>(a, acc, t, row0, lane, col_t, col_b, out);
+    epilogue_compute<TW, FM, FN, E>(a, acc, t, row0, lane, col_t, col_b, out);
 }
 
 // Block index -> tile, XCD aware: blocks bid, bid+8, ... run on one XCD; each

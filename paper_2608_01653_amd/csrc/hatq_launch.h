@@ -23,8 +23,10 @@ struct ConvArgs {
     const float *sx;
     const float *w_scale;
     const float *bias;
-    void *y;
+    void *y;               // NULL in F32 mode: only next_absmax is produced
     float *next_absmax;
+    const float *q_absmax; // I8 mode: per-sample max |B_next y| giving the scale, or NULL
+    float *q_scale;        // I8 mode: per-sample scale (written from q_absmax, else read)
     int64_t M;             // n * gh * gw
     int32_t n, h, w, cin_p;
     int32_t gh, gw;
@@ -35,7 +37,7 @@ struct ConvArgs {
     int32_t rowrun;        // small-cin layer contracted per kernel row (16 B each)
     int32_t cout, cout_pad;
     int32_t form;          // 0 DH, 1 WH
-    int32_t mode;          // 0 I32, 1 F32
+    int32_t mode;          // 0 I32, 1 F32, 2 I8 (codes of B_next y, next_hblock the block)
     int32_t hblock;        // the layer's block size
     int32_t next_hblock;   // 0 = no next-operand absmax
     int32_t tiles_h, tiles_w, tiles_n;   // 2-D tiles of grid points per sample; column tiles

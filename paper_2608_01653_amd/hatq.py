@@ -20,7 +20,7 @@ from . import build as _build
 
 HATQ_OK, HATQ_EINVAL, HATQ_EUNSUPPORTED, HATQ_EWORKSPACE, HATQ_EHIP = range(5)
 HATQ_DH, HATQ_WH = 0, 1
-HATQ_OUT_I32, HATQ_OUT_F32 = 0, 1
+HATQ_OUT_I32, HATQ_OUT_F32, HATQ_OUT_I8 = 0, 1, 2
 FORMS = {"DH": HATQ_DH, "WH": HATQ_WH}
 
 
@@ -46,6 +46,7 @@ class Weights(ctypes.Structure):
 
 EXPORTS = ["hatq_status_string", "hatq_conv_out_hw", "hatq_weights_bytes", "hatq_prepare_weights",
            "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act", "hatq_conv_int8",
+           "hatq_conv_int8_requant",
            "hatq_layer_ws_bytes", "hatq_layer_forward"]
 
 _lib = None
@@ -83,6 +84,8 @@ def load(build_if_missing: bool = False):
     L.hatq_fwht_quant_act.restype = i32
     L.hatq_conv_int8.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, i32, P, P]
     L.hatq_conv_int8.restype = i32
+    L.hatq_conv_int8_requant.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, P, P, P]
+    L.hatq_conv_int8_requant.restype = i32
     L.hatq_layer_ws_bytes.argtypes = [ctypes.POINTER(Weights), i32, i32, i32]
     L.hatq_layer_ws_bytes.restype = sz
     L.hatq_layer_forward.argtypes = [ctypes.POINTER(Weights), i32, P, i32, i32, i32, P, P, P, i32, P, P,
@@ -210,9 +213,16 @@ def hatq_fwht_quant_act(x: torch.Tensor, hblock: int, absmax: Optional[torch.Ten
 
 
 def hatq_conv_int8(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tensor, out_mode=HATQ_OUT_F32,
-                   next_hblock: int = 0, next_absmax: Optional[torch.Tensor] = None, y=None, stream=None):
+                   next_hblock: int = 0, next_absmax: Optional[torch.Tensor] = None, y=None, stream=None,
+                   absmax_only: bool = False):
+    """absmax_only: F32 mode with y = NULL, producing next_absmax alone (returns None)."""
     n, h, w, _ = xq.shape
     ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
+    if absmax_only:
+        _check(load().hatq_conv_int8(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), n, h, w, int(out_mode),
+                                     None, int(next_hblock), _ptr(next_absmax), _stream(stream)),
+               "hatq_conv_int8")
+        return None
     if y is None:
         if out_mode == HATQ_OUT_I32:
             y = torch.empty((n, ho, wo, layer.w.cout_pad), dtype=torch.int32, device=xq.device)
@@ -222,6 +232,23 @@ def hatq_conv_int8(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tens
                                  _ptr(y), int(next_hblock), _ptr(next_absmax), _stream(stream)),
            "hatq_conv_int8")
     return y
+
+
+def hatq_conv_int8_requant(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tensor, next_hblock: int,
+                           next_absmax: Optional[torch.Tensor] = None, next_scale: Optional[torch.Tensor] = None,
+                           yq: Optional[torch.Tensor] = None, stream=None):
+    """Conv with the requantizing epilogue: returns (yq, next_scale), the next layer's codes and scale."""
+    n, h, w, _ = xq.shape
+    ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
+    if yq is None:
+        yq = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.int8, device=xq.device)
+    if next_scale is None:
+        next_scale = torch.empty((n,), dtype=torch.float32, device=xq.device)
+    _check(load().hatq_conv_int8_requant(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), n, h, w,
+                                         int(next_hblock), _ptr(next_absmax), _ptr(next_scale), _ptr(yq),
+                                         _stream(stream)),
+           "hatq_conv_int8_requant")
+    return yq, next_scale
 
 
 def hatq_layer_ws_bytes(layer: PreparedLayer, n: int, h: int, w: int) -> int:

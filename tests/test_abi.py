@@ -136,6 +136,28 @@ def test_conv_rejects_before_launch(L):
     assert f(ctypes.byref(W), FAKE, FAKE, 0, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EINVAL
 
 
+def test_conv_absmax_only_needs_next_absmax(L):
+    f = L.hatq_conv_int8
+    W = _fake_weights()
+    # y = NULL is only the absmax-only F32 call
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 1, None, 0, None, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 0, None, 0, None, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, hatq.HATQ_OUT_I8, FAKE, 0, None, None) == hatq.HATQ_EINVAL
+
+
+def test_requant_rejects_before_launch(L):
+    f = L.hatq_conv_int8_requant
+    W = _fake_weights()
+    assert f(None, FAKE, FAKE, 1, 8, 8, 64, FAKE, FAKE, FAKE, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 64, FAKE, None, FAKE, None) == hatq.HATQ_EINVAL   # no scale
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 64, FAKE, FAKE, None, None) == hatq.HATQ_EINVAL   # no output
+    assert f(ctypes.byref(W), FAKE, FAKE, 0, 8, 8, 64, FAKE, FAKE, FAKE, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 3, FAKE, FAKE, FAKE, None) == hatq.HATQ_EINVAL    # block 3
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 128, FAKE, FAKE, FAKE, None) == hatq.HATQ_EUNSUPPORTED
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 64, ctypes.c_void_p(FAKE.value + 2), FAKE, FAKE, None) \
+        == hatq.HATQ_EINVAL                                                                           # misaligned
+
+
 def test_layer_forward_form_flag_and_workspace(L):
     f = L.hatq_layer_forward
     W = _fake_weights()

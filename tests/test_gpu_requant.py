@@ -1,0 +1,91 @@
+"""GPU parity of the requantizing epilogue (step a6 with I8 output,
+hatq_conv_int8_requant) and of the absmax-only F32 call (y = NULL) that gives
+its dynamic scale.
+
+* Against the oracle: the oracle's own layer (codes, scales, fp32 output y_ref)
+  fixes S_ref = B_next y_ref and its codes and per-sample scale (Eq.
+  symmetric_q); the GPU, fed the oracle's codes and scales, must produce the
+  same scale within 1 ulp and the same codes under the INT8 rule (bit-exact
+  where both sides see identical fp32 values: DH layers with next block 1).
+* Against the two-kernel GPU path: the codes equal, bit for bit, what the
+  activation kernel computes from the stored F32 output with the same absmax
+  (same fp32 butterfly, same rounding), and the absmax-only call matches the
+  F32 call's fused absmax exactly.
+* A static scale (next_absmax = NULL) gives the oracle's codes for that scale.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import assert_codes, assert_scale_ulp, dev, host
+from paper_2608_01653_amd import hatq, synth
+from test_gpu_parity import CONV, CONV_IDS, _layer
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    hatq.load()
+    torch.cuda.init()
+
+
+def _oracle_next(orc, r, next_b):
+    S_ref = orc.activation_transform(r.y, next_b)
+    q_ref, s_ref = orc.quantize_symmetric(S_ref)
+    return q_ref, s_ref
+
+
+@pytest.mark.parametrize("c", CONV, ids=CONV_IDS)
+@pytest.mark.parametrize("next_b", [1, 64])
+def test_requant_codes(orc, c, next_b):
+    n, h, w, cin, cout, k, s, p, tr, op, form, hb = c
+    rng, wt, b, ref, layer = _layer(orc, c, 81)
+    x = synth.heavy_tailed_activations(rng, (n, h, w, cin))
+    r = orc.layer_forward(x, ref)
+    q_ref, s_ref = _oracle_next(orc, r, next_b)
+    xq, sx = dev(r.xq), dev(r.sx)
+    # pass 1: the absmax alone; pass 2: the codes
+    nam = torch.full((n,), -1.0, device="cuda")
+    assert hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=next_b, next_absmax=nam,
+                               absmax_only=True) is None
+    yq, sq = hatq.hatq_conv_int8_requant(layer, xq, sx, next_b, next_absmax=nam)
+    assert yq.shape == q_ref.shape and yq.dtype == torch.int8
+    assert_scale_ulp(host(sq), s_ref)
+    exact = form == "DH" and next_b == 1
+    assert_codes(host(yq), q_ref, exact=exact, what=f"requant codes next_b={next_b}")
+    # the two-kernel GPU path on the stored output: identical absmax, scale, codes
+    nam2 = torch.full((n,), -1.0, device="cuda")
+    y = hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=next_b, next_absmax=nam2)
+    assert torch.equal(nam, nam2)
+    q2, s2 = hatq.hatq_fwht_quant_act(y, next_b, absmax=nam2)
+    assert torch.equal(sq, s2)
+    assert torch.equal(yq, q2)
+
+
+@pytest.mark.parametrize("ci", [1, 2, 4, 5, 16], ids=[CONV_IDS[i] for i in (1, 2, 4, 5, 16)])
+def test_requant_static_scale(orc, ci):
+    c = CONV[ci]
+    n, h, w, cin, cout, k, s, p, tr, op, form, hb = c
+    rng, wt, b, ref, layer = _layer(orc, c, 82)
+    x = synth.heavy_tailed_activations(rng, (n, h, w, cin))
+    r = orc.layer_forward(x, ref)
+    q_ref, s_ref = _oracle_next(orc, r, 64)
+    sc = dev(s_ref.copy())
+    yq, sq = hatq.hatq_conv_int8_requant(layer, dev(r.xq), dev(r.sx), 64, next_absmax=None, next_scale=sc)
+    assert np.array_equal(host(sq), s_ref)      # an input: left as given
+    assert_codes(host(yq), q_ref, what="requant codes, static scale")
+
+
+def test_requant_zero_output():
+    """All-zero codes and bias: absmax 0 gives scale 1 and all-zero codes."""
+    c = CONV[1]
+    n, h, w, cin, cout, k, s, p, tr, op, form, hb = c
+    layer = hatq.hatq_prepare_weights(hatq.desc(cin, cout, k, s, p, hb, tr, op), form,
+                                      torch.randn(cout, cin, k, k, device="cuda"), torch.zeros(cout, device="cuda"))
+    xq = torch.zeros((n, h, w, cin), dtype=torch.int8, device="cuda")
+    sx = torch.ones(n, device="cuda")
+    nam = torch.full((n,), -1.0, device="cuda")
+    hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=64, next_absmax=nam, absmax_only=True)
+    yq, sq = hatq.hatq_conv_int8_requant(layer, xq, sx, 64, next_absmax=nam)
+    assert torch.all(nam == 0) and torch.all(sq == 1) and not torch.any(yq)
