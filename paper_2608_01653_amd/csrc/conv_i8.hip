@@ -159,9 +159,10 @@ __device__ __forceinline__ void fwht_acc(float (&v)[16], int b) {
 // NB the block size of the next operand's absmax (0: not wanted), both for
 // fp32 output; WB = NB = -1 is the generic body, which takes the output mode,
 // form and block sizes from the arguments.
-template <int WB_, int NB_>
+// Q = 1: I8 output (the next operand's codes, NB its transform block).
+template <int WB_, int NB_, int Q_ = 0>
 struct Epi {
-    static constexpr int WB = WB_, NB = NB_;
+    static constexpr int WB = WB_, NB = NB_, Q = Q_;
 };
 using EpiGeneric = Epi<-1, -1>;
 
@@ -172,6 +173,7 @@ bool epi_matches(const ConvArgs &a) {
         return true;
     } else {
         const int wb = a.form == 1 ? a.hblock : 0;
+        if (E::Q) return a.mode == 2 && wb == E::WB && a.next_hblock == E::NB;
         const int nb = a.next_absmax != nullptr ? a.next_hblock : 0;
         return a.mode == 1 && wb == E::WB && nb == E::NB;
     }
@@ -191,8 +193,8 @@ struct EpiFlags {
     __device__ explicit EpiFlags(const ConvArgs &a) {
         f32 = generic ? a.mode != 0 : true;   // the fp32 arithmetic (F32 and I8 modes)
         wh = generic ? f32 && a.form == 1 : WB != 0;
-        want_abs = generic ? a.mode == 1 && a.next_absmax != nullptr && a.next_hblock > 0 : NB != 0;
-        i8 = generic && a.mode == 2;
+        want_abs = generic ? a.mode == 1 && a.next_absmax != nullptr && a.next_hblock > 0 : E::Q == 0 && NB != 0;
+        i8 = generic ? a.mode == 2 : E::Q != 0;
         store = !i8 && a.y != nullptr;        // I32 / F32 values
     }
 };
@@ -804,7 +806,7 @@ template <int CS>
 hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
     if (a.cout_pad % 192 == 0) {
         if constexpr (CS == 3)
-            return with_epilogue<HATQ_HOT_EPILOGUES>(
+            return with_epilogue<Epi<64, 64, 1>, HATQ_HOT_EPILOGUES>(
                 a, [&](auto e) { return launch_rowrun<2, 64, 192, CS, decltype(e)>(a, st); });
         return launch_rowrun<2, 64, 192, CS, EpiGeneric>(a, st);
     }

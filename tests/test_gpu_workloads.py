@@ -120,3 +120,47 @@ def test_cfg4_full_size_sampled(orc, li):
         for t, (s, _, _) in enumerate(pts):
             assert np.abs(S_s[t].astype(np.float64)).max() <= A[s] * (1 + 1e-5)
         del q1, q2
+
+
+def test_cfg4_layer1_requant_full_size(orc):
+    """The benchmark's layer-1 -> layer-2 transition at full size: the absmax-only
+    pass and the requantizing epilogue give bit for bit the scale and codes that
+    the F32 output followed by the activation kernel gives (a property that holds
+    at any size), and sampled pixels match the oracle's quantization of its own
+    layer output under the INT8 rule."""
+    wl = workloads.CFG4
+    (ishape, oshape) = wl.shapes()[0]
+    L, nxt = wl.layers[0], wl.layers[1]
+    rng = np.random.default_rng(4100)
+    w, b = synth.layer_params(rng, L.cin, L.cout, L.k, L.transposed)
+    ref, layer = _prepare(orc, L, w, b)
+    n = ishape[0]
+    xq = synth.int8_codes(rng, ishape)
+    sx = rng.uniform(1e-3, 1e-2, n).astype(np.float32)
+    nb = _act_block(nxt)
+    xq_d, sx_d = dev(xq), dev(sx)
+    nam = torch.full((n,), -1.0, device="cuda")
+    hatq.hatq_conv_int8(layer, xq_d, sx_d, hatq.HATQ_OUT_F32, next_hblock=nb, next_absmax=nam, absmax_only=True)
+    yq, sq = hatq.hatq_conv_int8_requant(layer, xq_d, sx_d, nb, next_absmax=nam)
+    nam2 = torch.full((n,), -1.0, device="cuda")
+    y = hatq.hatq_conv_int8(layer, xq_d, sx_d, hatq.HATQ_OUT_F32, next_hblock=nb, next_absmax=nam2)
+    assert torch.equal(nam, nam2)
+    q2, s2 = hatq.hatq_fwht_quant_act(y, nb, absmax=nam2)
+    assert torch.equal(sq, s2) and torch.equal(yq, q2)
+    # oracle on sampled pixels, with the GPU's scale (checked against the fused
+    # absmax just above): codes of B_next y_ref
+    ho, wo = oshape[1], oshape[2]
+    pts = [(int(rng.integers(n)), int(rng.integers(ho)), int(rng.integers(wo))) for _ in range(64)]
+    pts += [(0, 0, 0), (n - 1, ho - 1, wo - 1)]
+    sh = host(sq)
+    got = host(yq[torch.tensor([p[0] for p in pts]), torch.tensor([p[1] for p in pts]),
+                  torch.tensor([p[2] for p in pts])])
+    exp = np.empty_like(got)
+    for t, (s_, oh, ow) in enumerate(pts):
+        crop = _crop(xq, s_, oh * L.stride - L.pad, ow * L.stride - L.pad, L.k)
+        acc = orc.conv_int8(crop, ref.wq, stride=L.stride, pad=0)
+        y_ref = orc.epilogue(acc, sx[s_:s_ + 1], ref)[0, 0, 0]
+        S = orc.activation_transform(y_ref.reshape(1, 1, 1, -1), nb).reshape(-1).astype(np.float64)
+        exp[t] = np.clip(np.rint(S.astype(np.float32) / sh[s_]), -127, 127).astype(np.int8)
+    assert_codes(got, exp, what="cfg4 layer-1 requant codes vs oracle")
+    del y, q2
