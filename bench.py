@@ -232,7 +232,7 @@ def main():
     t_conv2 = avg_ms(3, 4) * 1e-3
     ops2 = workloads.conv_ops(wl, 1)
     ach = ops2 / t_conv2 / 1e12
-    roof = {"kernel": "conv_halo_kernel<192,5,Epi<0,64>> (layer 2, DH 192->192 k5s2)", "bound": "mfma",
+    roof = {"kernel": "conv_halo5_kernel<192,Epi<0,64>> (layer 2, DH 192->192 k5s2)", "bound": "mfma",
             "achieved": round(ach, 1), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
             "frac": round(ach / PEAK_INT8_TOPS, 4), "traffic": traffic_bytes("conv_l2"),
             "traffic_detail": measured_traffic("conv_l2"),

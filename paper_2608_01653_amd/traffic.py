@@ -7,10 +7,12 @@ pass (FETCH_SIZE or WRITE_SIZE, in KiB per dispatch).  The two calibration
 passes profile ``bench.py --calibrate-copy`` (1 GiB device copies); the ratio of
 the known copy size to what each counter reads scales the bench's counters to
 bytes.  Launches are identified by their order within one step of the
-four-layer stack: the first ``quant_kernel<64>`` and the first
-``conv_halo_kernel<192, 5, ...>`` after the row-run convolution (layer 1) are
-layer 2's quantization and convolution.  The output JSON carries a hash of the kernel sources;
-bench.py reports the traffic only while the sources are unchanged.
+four-layer stack: layer 1 runs the row-run convolution (an absmax pass, then the
+requantizing pass that writes layer 2's codes), so the first window
+convolution after a row-run launch is layer 2's convolution and the first
+``quant_kernel<64>`` after it is layer 3's quantization.  The output JSON
+carries a hash of the kernel sources; bench.py reports the traffic only while
+the sources are unchanged.
 """
 from __future__ import annotations
 
@@ -41,22 +43,24 @@ def copy_factor(d):
 
 
 def per_launch(d, factor):
-    """KiB counter -> bytes, median over the steps, for the layer-2 kernels."""
+    """KiB counter -> bytes, median over the steps, for the layer-2 conv and the
+    layer-3 quantization."""
     conv, quant = [], []
     want_q = want_c = False
     for r in rows(d):
         name = r["Kernel_Name"]
         v = float(r["Counter_Value"]) * factor * 1024
         if "conv_rowrun_kernel" in name:
-            want_q = want_c = True
+            want_c = True
+        elif "conv_halo5_kernel<192" in name and want_c:
+            conv.append(v)
+            want_c = False
+            want_q = True
         elif "quant_kernel<64>" in name and want_q:
             quant.append(v)
             want_q = False
-        elif "conv_halo_kernel<192, 5" in name and want_c:
-            conv.append(v)
-            want_c = False
     return {"conv_l2": statistics.median(conv) if conv else None,
-            "quant_l2": statistics.median(quant) if quant else None}
+            "quant_l3": statistics.median(quant) if quant else None}
 
 
 def main():
