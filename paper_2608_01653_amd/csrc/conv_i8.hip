@@ -230,6 +230,8 @@ __device__ __forceinline__ void store_group_impl(const ConvArgs &a, const Tile &
 // rounded with the magic constant, and the IEEE quotient fl(u / s) for every
 // value of a lane that has one near a half-integer (or when the scale is out of
 // the fast path's range); w[jj] packs the codes of registers 4*jj .. 4*jj+3.
+// (A per-register exact path behind a wave vote was measured slower: the
+// branches split the straight-line code.)
 __device__ __forceinline__ void quant16(const float (&u)[16], float s, float r, bool fast_ok, uint32_t (&w)[4]) {
     uint32_t c[16];
     bool near = !fast_ok;
@@ -585,6 +587,34 @@ __global__ void __launch_bounds__(kThreads, 2) conv_rowrun_kernel(const ConvArgs
 #pragma unroll
             for (int j = 0; j < FN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
         for (int ks = 0; ks < nks; ++ks) {
+            if (ks == 1 && a.k <= 6) {
+                // Kernel rows 4 and 5 hold the only nonzero weights of this K-step:
+                // a 32-deep MFMA (8 contraction bytes per lane, lane group fg ->
+                // row 4 + fg/2, bytes 8*(fg&1) .. +7) does it at half the cost.
+                const int kh = 4 + (fg >> 1), b0 = 8 * (fg & 1);
+                long fa[FM];
+#pragma unroll
+                for (int i = 0; i < FM; ++i) {
+                    const int m = wave * TM + 16 * i + fr;
+                    const int ohl = m / TW, owl = m - ohl * TW;
+                    const int row = a.sa * ohl + kh;
+                    const int off = row * RS + a.sa * owl * CIN + b0 + row_shift(ih0 + row, iw0);
+                    const uint32_t *pw = patch + (off >> 2);
+                    const uint32_t sh = off & 3;
+                    const uint32_t d0 = pw[0], d1 = pw[1], d2 = pw[2];
+                    const uint32_t lo = __builtin_amdgcn_alignbyte(d1, d0, sh), hi = __builtin_amdgcn_alignbyte(d2, d1, sh);
+                    fa[i] = (long)(((uint64_t)hi << 32) | lo);
+                }
+#pragma unroll
+                for (int j = 0; j < FN; ++j) {
+                    const int nn = 16 * j + fr;
+                    const long fb = *reinterpret_cast<const long *>(s_b + BN * 64 + nn * 64 + 16 * ((fg >> 1) ^ swz(nn)) + b0);
+#pragma unroll
+                    for (int i = 0; i < FM; ++i)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x32_i8(fb, fa[i], acc[i][j], 0, 0, 0);
+                }
+                continue;
+            }
             // kernel row 4*ks + fg <= 7 stays inside the patch; rows >= k meet zero weights
             const int kh = 4 * ks + fg;
             v4i fa[FM];

@@ -87,10 +87,10 @@ __device__ __forceinline__ float act_scale_from_absmax(float A) {
 // Exactness of the fast path: with r = fl(1/s), t = fl(v * r) differs from the
 // correctly rounded quotient fl(v / s) by at most |v/s| * (3 * 2^-24 + 2^-48)
 // <= 2.3e-5 for |v/s| <= 128, s a normal number.  When t lies farther than
-// 0.5 - 2^-14 from the nearest integer k, fl(v / s) lies strictly inside
-// (k - 1/2, k + 1/2) and rne(fl(v / s)) = k.  Elements closer to a half-integer
-// take the exact path, an IEEE division.
-#define HATQ_NEAR_TIE (0.5f - 0x1p-14f)
+// 0.5 - 2^-15 (2^-15 > 3.0e-5) from the nearest integer k, fl(v / s) lies
+// strictly inside (k - 1/2, k + 1/2) and rne(fl(v / s)) = k.  Elements closer
+// to a half-integer take the exact path, an IEEE division.
+#define HATQ_NEAR_TIE (0.5f - 0x1p-15f)
 
 // Clamp to [-127, 127].
 __device__ __forceinline__ float clamp127(float t) { return __builtin_amdgcn_fmed3f(t, -127.0f, 127.0f); }
