@@ -179,11 +179,6 @@ bool epi_matches(const ConvArgs &a) {
     }
 }
 
-// Values of one output row group after the epilogue arithmetic: out[i][k][*]
-// is the 64-channel block k of the lane's pixel in group i, in the accumulator
-// layout (v[4*jj + r]: channel 64*k + 16*jj + 4*q + r).
-template <int FM, int FN>
-using EpiVals = float[FM][FN / 4][16];
 
 template <typename E>
 struct EpiFlags {
@@ -253,56 +248,69 @@ __device__ __forceinline__ void quant16(const float (&u)[16], float s, float r, 
 
 // The arithmetic: dequantization, WH restore, next-operand absmax (one atomic
 // per wave at most) or, in I8 mode, the next operand's codes.  Each group is
-// stored as soon as it is final (stores interleave with the arithmetic); out
-// is the per-group working storage.
+// stored as soon as it is final (stores interleave with the arithmetic).  The
+// work is split into the per-tile setup (constructor), one call per 64-channel
+// block of the accumulators (block(acc, k), any order) and finish(), so a
+// kernel can run a block's epilogue while later blocks' MFMAs are in flight.
 template <int TW, int FM, int FN, typename E>
-__device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&acc)[FM][FN], const Tile &t,
-                                                 int row0, int lane, const float *col_t, const float *col_b,
-                                                 EpiVals<FM, FN> &out) {
+struct Epilogue {
     static_assert(FN % 4 == 0, "whole 64-channel blocks");
-    constexpr int WB = E::WB, NB = E::NB;
-    constexpr bool generic = WB == -1;
-    constexpr int NBLK = FN / 4;
-    const int p = lane & 15, q = lane >> 4;
-    const EpiFlags<E> fl(a);
-    const bool f32 = fl.f32, wh = fl.wh, want_abs = fl.want_abs, i8 = fl.i8, store = fl.store;
-    // the whole tile inside the grid (wave-uniform): no row masking needed
-    const bool full = t.gi0 + (row0 + 16 * FM - 1) / TW < a.gh && t.gj0 + TW <= a.gw;
-    float wave_m = 0.0f;
-    // Published running maximum of this sample (read once; a stale value only
-    // costs work).  A group whose rigorous upper bound on max |B_next y| stays
-    // below it cannot raise the maximum, so its exact transform is skipped.
-    float seen = -1.0f;
-    if (want_abs) {
-        if (lane == 0)
-            seen = __uint_as_float(__hip_atomic_load(reinterpret_cast<unsigned int *>(a.next_absmax + t.nb),
-                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-        seen = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(seen)));
-    }
-    const int nbk = generic ? a.next_hblock : NB;
-    // WH layer whose next operand uses the same blocks: B y = B (B z / b) = z
-    // exactly, so max|B y| <= max|z| (1 + 2 gamma_6 * 64) with gamma_6 the
-    // six-stage fp32 rounding factor (< 3.6e-7); 1 + 1e-4 covers it.
-    const bool z_bound = wh && (generic ? a.hblock == a.next_hblock : WB == NB);
-    // I8 mode: the sample's scale (from the absmax as the activation quantizer
-    // derives it, or given), published by the sample's first tile
-    float qs = 1.0f, qr = 1.0f;
-    bool q_fast = true;
-    if (i8) {
-        qs = a.q_absmax ? act_scale_from_absmax(a.q_absmax[t.nb]) : a.q_scale[t.nb];
-        qr = 1.0f / qs;
-        q_fast = qs >= 0x1p-125f && qs <= 0x1p125f;
-        if (a.q_absmax && t.gi0 == 0 && t.gj0 == 0 && t.n0 == 0 && row0 == 0 && lane == 0) a.q_scale[t.nb] = qs;
-    }
+    static constexpr int WB = E::WB, NB = E::NB;
+    static constexpr bool generic = WB == -1;
+    static constexpr int NBLK = FN / 4;
+    const ConvArgs &a;
+    const Tile &t;
+    const int row0, lane, p, q;
+    const float *col_t, *col_b;
+    const EpiFlags<E> fl;
+    bool full, z_bound, q_fast;
+    float wave_m, seen, qs, qr;
+    int nbk;
     bool valid[FM];
+
+    __device__ __forceinline__ Epilogue(const ConvArgs &a_, const Tile &t_, int row0_, int lane_, const float *col_t_,
+                                        const float *col_b_)
+        : a(a_), t(t_), row0(row0_), lane(lane_), p(lane_ & 15), q(lane_ >> 4), col_t(col_t_), col_b(col_b_),
+          fl(a_) {
+        // the whole tile inside the grid (wave-uniform): no row masking needed
+        full = t.gi0 + (row0 + 16 * FM - 1) / TW < a.gh && t.gj0 + TW <= a.gw;
+        wave_m = 0.0f;
+        // Published running maximum of this sample (read once; a stale value only
+        // costs work).  A group whose rigorous upper bound on max |B_next y| stays
+        // below it cannot raise the maximum, so its exact transform is skipped.
+        seen = -1.0f;
+        if (fl.want_abs) {
+            if (lane == 0)
+                seen = __uint_as_float(__hip_atomic_load(reinterpret_cast<unsigned int *>(a.next_absmax + t.nb),
+                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+            seen = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(seen)));
+        }
+        nbk = generic ? a.next_hblock : NB;
+        // WH layer whose next operand uses the same blocks: B y = B (B z / b) = z
+        // exactly, so max|B y| <= max|z| (1 + 2 gamma_6 * 64) with gamma_6 the
+        // six-stage fp32 rounding factor (< 3.6e-7); 1 + 1e-4 covers it.
+        z_bound = fl.wh && (generic ? a.hblock == a.next_hblock : WB == NB);
+        // I8 mode: the sample's scale (from the absmax as the activation quantizer
+        // derives it, or given), published by the sample's first tile
+        qs = 1.0f;
+        qr = 1.0f;
+        q_fast = true;
+        if (fl.i8) {
+            qs = a.q_absmax ? act_scale_from_absmax(a.q_absmax[t.nb]) : a.q_scale[t.nb];
+            qr = 1.0f / qs;
+            q_fast = qs >= 0x1p-125f && qs <= 0x1p125f;
+            if (a.q_absmax && t.gi0 == 0 && t.gj0 == 0 && t.n0 == 0 && row0 == 0 && lane == 0) a.q_scale[t.nb] = qs;
+        }
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int m = row0 + 16 * i + p;
-        valid[i] = t.gi0 + m / TW < a.gh && t.gj0 + m % TW < a.gw;
+        for (int i = 0; i < FM; ++i) {
+            const int m = row0 + 16 * i + p;
+            valid[i] = t.gi0 + m / TW < a.gh && t.gj0 + m % TW < a.gw;
+        }
     }
-    // 64-channel blocks outermost: one set of column factors serves all FM groups
-#pragma unroll
-    for (int k = 0; k < NBLK; ++k) {
+
+    // 64-channel block k of every row group (one set of column factors serves all)
+    __device__ __forceinline__ void block(const v4i (&acc)[FM][FN], int k) {
+        const bool f32 = fl.f32, wh = fl.wh, want_abs = fl.want_abs, i8 = fl.i8, store = fl.store;
         float4 t4[4], b4[4];
         if (f32) {
 #pragma unroll
@@ -315,7 +323,7 @@ __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&
         const bool blk_full = t.n0 + 64 * k + 64 <= a.cout;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
-            float (&v)[16] = out[i][k];
+            float v[16];
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
                 const v4i c4 = acc[i][4 * k + jj];
@@ -360,23 +368,20 @@ __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&
             } else if (exact || i8) {
                 // Rows past the grid and channels past cout are not part of the
                 // next operand.
-                float u[16];
-#pragma unroll
-                for (int r = 0; r < 16; ++r) u[r] = v[r];
                 if (!full || !blk_full) {
 #pragma unroll
                     for (int jj = 0; jj < 4; ++jj)
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             const int ch = t.n0 + 64 * k + 16 * jj + 4 * q + r;
-                            if (!valid[i] || ch >= a.cout) u[4 * jj + r] = 0.0f;
+                            if (!valid[i] || ch >= a.cout) v[4 * jj + r] = 0.0f;
                         }
                 }
                 if (i8) {
                     // codes of B_next y in channel order (restoring butterflies)
-                    fwht_acc<NB, true>(u, a.next_hblock);
+                    fwht_acc<NB, true>(v, a.next_hblock);
                     uint32_t w[4];
-                    quant16(u, qs, qr, q_fast, w);
+                    quant16(v, qs, qr, q_fast, w);
                     if (valid[i]) {
                         const int m = row0 + 16 * i + p;
                         int8_t *yq = reinterpret_cast<int8_t *>(a.y) +
@@ -388,29 +393,34 @@ __device__ __forceinline__ void epilogue_compute(const ConvArgs &a, const v4i (&
                         }
                     }
                 } else {
-                    fwht_acc<NB, false>(u, a.next_hblock);
+                    fwht_acc<NB, false>(v, a.next_hblock);
                     float mm = 0.0f;
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(u[r]));
+                    for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(v[r]));
                     wave_m = fmaxf(wave_m, mm);
                 }
             }
         }
     }
-    if (want_abs) {
-        wave_m = wave_max(wave_m);
-        // The running maximum only grows, so a wave whose maximum does not exceed
-        // a value already published skips its atomic.  Device-scope atomics on
-        // one address serialize, and most waves of a layer end up skipping.
-        if (lane == 0 && wave_m > seen) atomic_max_nonneg(a.next_absmax + t.nb, wave_m);
+
+    __device__ __forceinline__ void finish() {
+        if (fl.want_abs) {
+            const float m = wave_max(wave_m);
+            // The running maximum only grows, so a wave whose maximum does not exceed
+            // a value already published skips its atomic.  Device-scope atomics on
+            // one address serialize, and most waves of a layer end up skipping.
+            if (lane == 0 && m > seen) atomic_max_nonneg(a.next_absmax + t.nb, m);
+        }
     }
-}
+};
 
 template <int TW, int FM, int FN, typename E>
 __device__ __forceinline__ void epilogue_regs(const ConvArgs &a, const v4i (&acc)[FM][FN], const Tile &t,
                                               int row0, int lane, const float *col_t, const float *col_b) {
-    EpiVals<FM, FN> out;
-    epilogue_compute<TW, FM, FN, E>(a, acc, t, row0, lane, col_t, col_b, out);
+    Epilogue<TW, FM, FN, E> ep(a, t, row0, lane, col_t, col_b);
+#pragma unroll
+    for (int k = 0; k < FN / 4; ++k) ep.block(acc, k);
+    ep.finish();
 }
 
 // Block index -> tile, XCD aware: blocks bid, bid+8, ... run on one XCD; each
