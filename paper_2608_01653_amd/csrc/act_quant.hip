@@ -57,6 +57,9 @@ __global__ void __launch_bounds__(kThreads) absmax_kernel(const float *__restric
     const int t = threadIdx.x & 3;
     const int64_t items = (E + I - 1) / I;
     float m = 0.0f;
+    // (unrolled so the loads of several items are in flight together: the
+    // grid is small, so each quad walks several items)
+#pragma unroll 4
     for (int64_t it = (int64_t)blockIdx.x * kQuadsPerBlock + (threadIdx.x >> 2); it < items;
          it += (int64_t)gridDim.x * kQuadsPerBlock) {
         float v[4 * R];
