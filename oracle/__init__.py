@@ -66,6 +66,8 @@ def lib():
         L.orc_conv_f64.argtypes = [P, i32, i32, i32, i32, P, i32, i32, i32, i32, i32, i32, P]
         L.orc_conv_f64.restype = None
         L.orc_epilogue.argtypes = [P, i32, i64, i32, i32, i32, i32, P, P, P, P]
+        L.orc_int_requant_params.argtypes = [i32, ctypes.c_float, P, P, ctypes.c_float, i32, i32, i32, i32, P, P]
+        L.orc_int_transition.argtypes = [P, i64, i32, i32, P, P, i32, i32, i32, P]
         _lib = L
     return _lib
 
@@ -270,3 +272,41 @@ def float_layer(x: np.ndarray, w: np.ndarray, bias: Optional[np.ndarray], *, str
     if bias is not None:
         y = y + bias.astype(np.float64)
     return y
+
+
+# --------------------------------------------------------------------------
+# O7  Integer-only inter-layer transition (static scales)
+# --------------------------------------------------------------------------
+@dataclass
+class IntRequant:
+    M: np.ndarray       # [cout_p] int32 multipliers
+    b_int: np.ndarray   # [cout_p] int32 integer bias
+    shift: int          # shared right shift n
+
+
+def int_requant_params(pw: PreparedWeights, s_x: float, s_y: float, next_b: int) -> IntRequant:
+    """Eq. integer_accumulation (b_int), Eq. integer_fixed_point_scale (M, n) for
+    static input scale s_x and next-operand scale s_y (see the C source, O6)."""
+    K = pw.k * pw.k * pw.cin_p
+    gain = (pw.hblock if pw.form == "WH" else 1) * next_b
+    M = np.empty(pw.cout_p, np.int32)
+    b = np.empty(pw.cout_p, np.int32)
+    beta_in, beta_out = (pw.hblock, 1) if pw.form == "DH" else (1, pw.hblock)
+    n = lib().orc_int_requant_params(pw.cout_p, float(s_x), _p(pw.w_scale), _p(pw.w_bias), float(s_y),
+                                     beta_in, beta_out, K, gain, _p(M), _p(b))
+    if n < 0:
+        raise ValueError("no shift fits the multiplier and overflow bounds")
+    return IntRequant(M, b, int(n))
+
+
+def int_transition(acc: np.ndarray, pw: PreparedWeights, rq: IntRequant, next_b: int) -> np.ndarray:
+    """Eq. integer_hadamard_transition with phi = identity: the next layer's INT8
+    operand [.., cout] from the accumulators [.., cout_p]."""
+    acc = _c(acc, np.int32)
+    P = acc.size // pw.cout_p
+    q = np.empty(acc.shape[:-1] + (pw.cout,), np.int8)
+    wb = pw.hblock if pw.form == "WH" else 1
+    if lib().orc_int_transition(_p(acc), P, pw.cout, pw.cout_p, _p(_c(rq.M, np.int32)),
+                                _p(_c(rq.b_int, np.int32)), rq.shift, wb, next_b, _p(q)) != 0:
+        raise ValueError("bad transition geometry")
+    return q

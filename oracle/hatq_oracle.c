@@ -370,3 +370,107 @@ int orc_epilogue(const int32_t *acc, int n, int64_t pix, int cout, int cout_p, i
     free(H);
     return 0;
 }
+
+/* ------------------------------------------------------------------------- */
+/* O6. Integer-only inter-layer transition (Eq. integer_accumulation with    */
+/* zero points 0, Eq. integer_fixed_point_scale, Eq. integer_hadamard_        */
+/* transition, Table I), static scales.  In the unnormalized transforms used */
+/* throughout, one accumulator step of channel c is worth                     */
+/*   u_c = s_x s_w,c / beta_in    (beta_in = block of a DH layer's input       */
+/*                                 transform, 1 for WH),                      */
+/* and the output transform of a WH layer divides by its block beta_out      */
+/* (1 for DH), so the bias in accumulator steps and the scale ratio are       */
+/*   b_int,c = rne(b_c / u_c),  rho_c = u_c / (beta_out s_y),                 */
+/*   M_c = rne(2^n rho_c),                                                    */
+/* with the shared shift n the largest in [0, 62] that keeps every M_c at or  */
+/* below M_max = floor(2^62 / (A_max G)), A_max = K 127^2 + max|b_int| the    */
+/* accumulator bound and G the product of the transform gains (block size of  */
+/* the WH output transform, block size of the next DH input transform).       */
+/* Returns n, or -1 when no n >= 0 fits (or |b_int| >= 2^30).                 */
+/* ------------------------------------------------------------------------- */
+int orc_int_requant_params(int cout_p, float s_x, const float *s_w, const float *bias, float s_y,
+                           int beta_in, int beta_out, int K, int gain, int32_t *M, int32_t *b_int)
+{
+    if (beta_in < 1 || beta_out < 1 || gain < 1) return -1;
+    double bmax = 0.0;
+    for (int c = 0; c < cout_p; ++c) {
+        const double u = (double)s_x * (double)s_w[c] / (double)beta_in;   /* exact: product, power of two */
+        const double bi = rint((double)bias[c] / u);
+        if (fabs(bi) >= 1073741824.0) return -1;
+        b_int[c] = (int32_t)bi;
+        if (fabs(bi) > bmax) bmax = fabs(bi);
+    }
+    const double amax = (double)K * 127.0 * 127.0 + bmax;
+    double mmax = floor(4611686018427387904.0 / (amax * (double)gain));   /* 2^62 / (A_max G) */
+    if (mmax > 2147483647.0) mmax = 2147483647.0;
+    for (int n = 62; n >= 0; --n) {
+        int ok = 1;
+        for (int c = 0; c < cout_p && ok; ++c) {
+            const double rho = (double)s_x * (double)s_w[c] / ((double)beta_in * (double)beta_out * (double)s_y);
+            if (rint(ldexp(rho, n)) > mmax) ok = 0;
+        }
+        if (!ok) continue;
+        for (int c = 0; c < cout_p; ++c) {
+            const double rho = (double)s_x * (double)s_w[c] / ((double)beta_in * (double)beta_out * (double)s_y);
+            M[c] = (int32_t)rint(ldexp(rho, n));
+        }
+        return n;
+    }
+    return -1;
+}
+
+/* rne(w / 2^n) for an integer w: the exact quotient rounded half to even. */
+static int64_t rne_shift(int64_t w, int n)
+{
+    if (n == 0) return w;
+    const int64_t q = w >> n;                         /* floor */
+    const int64_t r = w - (q << n);                   /* 0 <= r < 2^n */
+    const int64_t half = (int64_t)1 << (n - 1);
+    if (r > half || (r == half && (q & 1))) return q + 1;
+    return q;
+}
+
+/* The transition itself on accumulators acc [P][cout_p]:                     */
+/*   a'  = acc + b_int;  v = H_out(M (.) a') (WH: blocks of wb over cout_p;    */
+/*   wb = 1: identity), truncated to cout;  w = H_in(v) (DH next: blocks of    */
+/*   nb over cout, cout % nb == 0; nb = 1: identity);                         */
+/*   q = clamp(rne(w / 2^n), -127, 127).  All in int64 with dense matrices.    */
+int orc_int_transition(const int32_t *acc, int64_t P, int cout, int cout_p, const int32_t *M,
+                       const int32_t *b_int, int n, int wb, int nb, int8_t *q)
+{
+    if (!is_pow2(wb) || !is_pow2(nb) || cout_p % wb || cout % nb || n < 0 || n > 62) return -1;
+    int8_t *Ho = (int8_t *)malloc((size_t)wb * wb);
+    int8_t *Hi = (int8_t *)malloc((size_t)nb * nb);
+    orc_sylvester(wb, Ho);
+    orc_sylvester(nb, Hi);
+    #pragma omp parallel
+    {
+        int64_t *p = (int64_t *)malloc(sizeof(int64_t) * cout_p);
+        int64_t *v = (int64_t *)malloc(sizeof(int64_t) * cout_p);
+        #pragma omp for schedule(static)
+        for (int64_t px = 0; px < P; ++px) {
+            const int32_t *a = acc + px * cout_p;
+            for (int c = 0; c < cout_p; ++c) p[c] = (int64_t)M[c] * ((int64_t)a[c] + b_int[c]);
+            for (int blk = 0; blk < cout_p; blk += wb)
+                for (int i = 0; i < wb; ++i) {
+                    int64_t s = 0;
+                    for (int j = 0; j < wb; ++j) s += Ho[i * wb + j] * p[blk + j];
+                    v[blk + i] = s;
+                }
+            for (int blk = 0; blk < cout; blk += nb)
+                for (int i = 0; i < nb; ++i) {
+                    int64_t s = 0;
+                    for (int j = 0; j < nb; ++j) s += Hi[i * nb + j] * v[blk + j];
+                    int64_t r = rne_shift(s, n);
+                    if (r > 127) r = 127;
+                    if (r < -127) r = -127;
+                    q[px * cout + blk + i] = (int8_t)r;
+                }
+        }
+        free(p);
+        free(v);
+    }
+    free(Ho);
+    free(Hi);
+    return 0;
+}
