@@ -93,6 +93,73 @@ def cpu_baseline(wl, x_np, params):
                       "preparation untimed, as on the GPU"}
 
 
+def measure_integer_stack(args, wl, layers, x0, xq, sc, ys, ws, act_hb, total_ops, img_pix):
+    """The same stack with integer-only transitions between layers (static
+    per-tensor scales, calibrated as the largest per-sample scale the dynamic
+    step just produced for each operand): one activation pass on the image, then
+    each conv writes the next layer's INT8 codes through the fixed-point
+    epilogue; the last layer writes fp32.  Timed separately from the step."""
+    import torch
+    from paper_2608_01653_amd import hatq
+    n = x0.shape[0]
+    nL = len(layers)
+    dev = x0.device
+    s_dyn = [float(sc[i].max()) for i in range(nL)]
+    # static input scale: every sample quantized with the batch's absmax
+    a0 = torch.full((n,), s_dyn[0] * 127.0, dtype=torch.float32, device=dev)
+    s0 = torch.empty(n, dtype=torch.float32, device=dev)
+    hatq.hatq_fwht_quant_act(x0, act_hb[0], absmax=a0, xq=xq[0], scale=s0, ws=ws)
+    s_x = [float(s0[0])] + s_dyn[1:]
+    tables, shifts = [], []
+    for i in range(nL - 1):
+        t, sh = hatq.hatq_int_transition_params(layers[i], s_x[i], s_x[i + 1], act_hb[i + 1], device=dev)
+        tables.append(t)
+        shifts.append(sh)
+    s_last = torch.full((n,), s_x[-1], dtype=torch.float32, device=dev)
+
+    def istep(events=None):
+        if events:
+            events[0].record()
+        hatq.hatq_fwht_quant_act(x0, act_hb[0], absmax=a0, xq=xq[0], scale=s0, ws=ws)
+        for i in range(nL - 1):
+            if events:
+                events[i + 1].record()
+            hatq.hatq_conv_int8_int_transition(layers[i], xq[i], act_hb[i + 1], tables[i], yq=xq[i + 1])
+        if events:
+            events[nL].record()
+        hatq.hatq_conv_int8(layers[-1], xq[-1], s_last, hatq.HATQ_OUT_F32, y=ys[-1])
+        if events:
+            events[nL + 1].record()
+
+    for _ in range(args.warmup):
+        istep()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(nL + 2)] for _ in range(args.steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for k in range(args.steps):
+        istep(ev[k])
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    log(f"integer stack: {ms:.3f} ms/step")
+
+    def avg_us(a, b):
+        return round(sum(ev[k][a].elapsed_time(ev[k][b]) for k in range(args.steps)) / args.steps * 1e3, 2)
+    stages = {"act_quant_l1": avg_us(0, 1)}
+    for i in range(nL - 1):
+        stages[f"conv_l{i + 1}_int_transition"] = avg_us(i + 1, i + 2)
+    stages[f"conv_l{nL}_f32"] = avg_us(nL, nL + 1)
+    return {"ms_per_step": round(ms, 4),
+            "tops": round(total_ops / (ms * 1e-3) / 1e12, 2),
+            "mpix_per_s": round(img_pix / (ms * 1e-3) / 1e6, 1),
+            "stages_us": stages,
+            "static_scales": [float(f"{v:.6g}") for v in s_x],
+            "shifts": shifts,
+            "note": "integer-only transitions (fixed-point multiplier, integer bias, int64 "
+                    "Hadamard transforms in the conv epilogue); static per-tensor scales"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -250,6 +317,8 @@ def main():
               "avg_us": round(t_q * 1e6, 2),
               "work": f"{eq * 5} bytes per launch = {eq} elements x (4 B fp32 in + 1 B int8 out)"}
 
+    integer_stack = measure_integer_stack(args, wl, layers, x0, xq, sc, ys, ws, act_hb, total_ops, img_pix)
+
     out = {
         "metric": "Hadamard-INT8 conv TOPS + Mpixel/s per layer; % of INT8 MFMA / HBM peak",
         "value": round(total_ops / (ms_step * 1e-3) / 1e12, 2),
@@ -267,6 +336,7 @@ def main():
         "layers": per_layer,
         "roofline": roof,
         "roofline_act_quant": roof_q,
+        "integer_stack": integer_stack,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, x_np, params)

@@ -204,6 +204,49 @@ int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const fl
                                const float *next_absmax, float *next_scale, int8_t *yq,
                                void *stream);
 
+/* Integer-only transition (Eq. integer_accumulation, Eq.
+ * integer_fixed_point_scale, Eq. integer_hadamard_transition, the integer
+ * column of Table I) with static per-tensor scales: the layer's INT32
+ * accumulators become the next layer's INT8 codes with no floating point.
+ *
+ * hatq_int_table_len: int32 entries of the parameter table of W (2*cout_pad + 1),
+ * 0 for invalid weights.
+ *
+ * hatq_int_transition_params: calibration step, fills the table on the device.
+ *   s_x:   the static scale of W's input codes (unnormalized domain).
+ *   s_y:   the static scale of the next operand's codes.
+ *   next_hblock: the next operand's transform block (1: none), a power of two
+ *          <= 64; the overflow bound depends on it, so the table serves only
+ *          calls with this next_hblock.
+ *   table: device int32 [2*cout_pad + 1], 16-byte aligned, written as
+ *     M[c]         = rne(2^n rho_c), rho_c = u_c / (beta_out s_y),
+ *     b_int[c]     = rne(b_c / u_c),  u_c = s_x s_w,c / beta_in,
+ *     table[2*cout_pad] = n,
+ *   with (beta_in, beta_out) = (hblock, 1) for DH and (1, hblock) for WH (one
+ *   accumulator step is worth u_c; the WH output transform divides by its
+ *   block), b the prepared bias (WH: in the output basis) and n the largest
+ *   shift in [0, 62] with every M_c <= floor(2^62 / (A_max G)) and < 2^31,
+ *   A_max = k*k*cin_pad*127^2 + max|b_int|, G = (WH: hblock) * next_hblock:
+ *   every int64 sum of the transition is then exact.  fp64 arithmetic with
+ *   correctly rounded division.
+ *   shift: NULL or host int32 receiving n.
+ *   Waits for the stream (the status depends on the result): HATQ_EUNSUPPORTED
+ *   if no shift fits (or |b_int| >= 2^30), then n = -1 in the table.
+ *
+ * hatq_conv_int8_int_transition: convolution plus the integer epilogue,
+ *   p = M (.) (acc + b_int) in int64, v = B_Cout p (WH; truncated to cout),
+ *   w = B_next v (blocks of next_hblock), yq = clamp(rne(w / 2^n), -127, 127)
+ *   with rne rounding exact halves to even; no act_scale (it is inside M).
+ *   table: as written by hatq_int_transition_params for W and next_hblock.
+ *   yq:    device int8 [n][ho][wo][cout], the next layer's codes.
+ *   Supported: as hatq_conv_int8_requant. */
+size_t hatq_int_table_len(const hatq_weights *W);
+int32_t hatq_int_transition_params(const hatq_weights *W, float s_x, float s_y, int32_t next_hblock,
+                                   int32_t *table, int32_t *shift, void *stream);
+int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, int32_t n, int32_t h,
+                                      int32_t w, int32_t next_hblock, const int32_t *table,
+                                      int8_t *yq, void *stream);
+
 /* Workspace bytes of hatq_layer_forward for an input of n x h x w. */
 size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w);
 

@@ -3,6 +3,7 @@
 // nothing, touch no output and need no GPU.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdint>
 #include <cstring>
 
@@ -122,7 +123,7 @@ int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next
 int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, int32_t n,
                       int32_t h, int32_t w, int32_t mode, void *y, int32_t next_hblock,
                       float *next_absmax, hipStream_t st, const float *q_absmax = nullptr,
-                      float *q_scale = nullptr) {
+                      float *q_scale = nullptr, const int32_t *rq_table = nullptr) {
     const hatq_conv_desc &d = W->d;
     int32_t ho, wo;
     if (out_hw(&d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
@@ -137,6 +138,7 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
     a.next_absmax = next_absmax;
     a.q_absmax = q_absmax;
     a.q_scale = q_scale;
+    a.rq_table = rq_table;
     a.n = n;
     a.h = h;
     a.w = w;
@@ -152,7 +154,7 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
     a.form = W->form;
     a.mode = mode;
     a.hblock = d.hblock;
-    a.next_hblock = (next_absmax || mode == HATQ_OUT_I8) ? next_hblock : 0;
+    a.next_hblock = (next_absmax || mode >= HATQ_OUT_I8) ? next_hblock : 0;
     const bool small = W->cin_pad <= 4 && W->k_total <= 128;
     if (!d.transposed) {
         a.gh = ho;
@@ -358,6 +360,55 @@ int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const fl
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
     return conv_launches(W, xq, act_scale, n, h, w, HATQ_OUT_I8, yq, next_hblock, nullptr,
                          static_cast<hipStream_t>(stream), next_absmax, next_scale);
+}
+
+size_t hatq_int_table_len(const hatq_weights *W) {
+    if (check_weights(W) != HATQ_OK) return 0;
+    return 2 * (size_t)W->cout_pad + 1;
+}
+
+int32_t hatq_int_transition_params(const hatq_weights *W, float s_x, float s_y, int32_t next_hblock,
+                                   int32_t *table, int32_t *shift, void *stream) {
+    int32_t s = check_weights(W);
+    if (s != HATQ_OK) return s;
+    if (!table || !aligned(table, 16)) return HATQ_EINVAL;
+    if (!(s_x > 0.0f) || !(s_y > 0.0f) || !std::isfinite(s_x) || !std::isfinite(s_y)) return HATQ_EINVAL;
+    if (!is_pow2(next_hblock) || next_hblock > 64) return HATQ_EINVAL;
+    const bool dh = W->form == HATQ_DH;
+    hatq::IntParamArgs a;
+    a.w_scale = W->w_scale;
+    a.bias = W->bias;
+    a.table = table;
+    a.s_x = s_x;
+    a.s_y = s_y;
+    a.cout_p = W->cout_pad;
+    a.beta_in = dh ? W->d.hblock : 1;
+    a.beta_out = dh ? 1 : W->d.hblock;
+    a.K = W->d.k * W->d.k * W->cin_pad;
+    a.gain = a.beta_out * next_hblock;
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    if (hatq::launch_int_params(a, st) != hipSuccess) return HATQ_EHIP;
+    int32_t n = -1;
+    if (hipMemcpyAsync(&n, table + 2 * W->cout_pad, sizeof(n), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+        return HATQ_EHIP;
+    if (shift) *shift = n;
+    return n >= 0 ? HATQ_OK : HATQ_EUNSUPPORTED;
+}
+
+int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, int32_t n, int32_t h, int32_t w,
+                                      int32_t next_hblock, const int32_t *table, int8_t *yq, void *stream) {
+    int32_t s = check_weights(W);
+    if (s != HATQ_OK) return s;
+    if (!xq || !table || !yq || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
+    if (!aligned(xq, 16) || !aligned(yq, 4) || !aligned(table, 16)) return HATQ_EINVAL;
+    if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    if ((s = check_next(W, next_hblock, reinterpret_cast<const float *>(table))) != HATQ_OK) return s;
+    if (W->d.cout % 4) return HATQ_EUNSUPPORTED;
+    int32_t ho, wo;
+    if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
+    return conv_launches(W, xq, nullptr, n, h, w, hatq::kModeIntTransition, yq, next_hblock, nullptr,
+                         static_cast<hipStream_t>(stream), nullptr, nullptr, table);
 }
 
 size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w) {

@@ -65,16 +65,28 @@ __device__ __forceinline__ int64_t out_pixel(const ConvArgs &a, int nb, int gi, 
 // Scaling by a power of two commutes with every rounding (results far above
 // the subnormal range), so the WH output equals restoring z first and dividing
 // after, as the operator is defined.
+// In the integer transition (mode 3) the two slots carry the bits of the
+// fixed-point multiplier M_c and of the integer bias b_int,c instead.
 __device__ __forceinline__ void column_factor(const ConvArgs &a, float sxv, int c, float &t, float &b) {
+    if (a.mode == kModeIntTransition) {
+        t = __int_as_float(a.rq_table[c]);
+        b = __int_as_float(a.rq_table[a.cout_pad + c]);
+        return;
+    }
     const float inv_b = 1.0f / (float)a.hblock;
     t = (sxv * a.w_scale[c]) * inv_b;
     b = a.form == 1 ? a.bias[c] * inv_b : a.bias[c];
 }
 
+// The tile's activation scale (the integer transition has none).
+__device__ __forceinline__ float tile_sx(const ConvArgs &a, int nb) {
+    return a.mode == kModeIntTransition ? 0.0f : a.sx[nb];
+}
+
 // Written by the whole block.
 template <int BN>
 __device__ __forceinline__ void column_factors(const ConvArgs &a, const Tile &t, float *col_t, float *col_b) {
-    const float sxv = a.sx[t.nb];
+    const float sxv = tile_sx(a, t.nb);
     for (int c = threadIdx.x; c < BN; c += kThreads) column_factor(a, sxv, t.n0 + c, col_t[c], col_b[c]);
 }
 
@@ -151,6 +163,65 @@ __device__ __forceinline__ void fwht_acc(float (&v)[16], int b) {
     }
 }
 
+// ---- integer transition: the same butterflies on int64 values ---------------
+// Integer butterflies are exact, so any stage order gives the Sylvester
+// transform of the block; the layout and the lane pairing are those above.
+template <int STRIDE>
+__device__ __forceinline__ void reg_stage_i64(int64_t (&v)[16]) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        if (r & STRIDE) continue;
+        const int64_t x = v[r], y = v[r + STRIDE];
+        v[r] = x + y;
+        v[r + STRIDE] = x - y;
+    }
+}
+
+template <int MASK>
+__device__ __forceinline__ void pair_swap_i64(int64_t &x, int64_t &y) {
+    float xl = __uint_as_float((uint32_t)x), xh = __uint_as_float((uint32_t)((uint64_t)x >> 32));
+    float yl = __uint_as_float((uint32_t)y), yh = __uint_as_float((uint32_t)((uint64_t)y >> 32));
+    pair_swap<MASK>(xl, yl);
+    pair_swap<MASK>(xh, yh);
+    x = (int64_t)(((uint64_t)__float_as_uint(xh) << 32) | __float_as_uint(xl));
+    y = (int64_t)(((uint64_t)__float_as_uint(yh) << 32) | __float_as_uint(yl));
+}
+
+template <int MASK>
+__device__ __forceinline__ void cross_stage_i64(int64_t (&v)[16]) {
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) pair_swap_i64<MASK>(v[r], v[r + 1]);
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) {
+        const int64_t x = v[r], y = v[r + 1];
+        v[r] = x + y;
+        v[r + 1] = x - y;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) pair_swap_i64<MASK>(v[r], v[r + 1]);
+}
+
+// B as in fwht_acc (B = -1: block size b at run time; 0 or 1: none).
+template <int B>
+__device__ __forceinline__ void fwht_acc_i64(int64_t (&v)[16], int b) {
+    const int bb = B == -1 ? b : B;
+    if (bb >= 2) reg_stage_i64<1>(v);
+    if (bb >= 4) reg_stage_i64<2>(v);
+    if (bb >= 8) cross_stage_i64<16>(v);
+    if (bb >= 16) cross_stage_i64<32>(v);
+    if (bb >= 32) reg_stage_i64<4>(v);
+    if (bb >= 64) reg_stage_i64<8>(v);
+}
+
+// clamp(rne(w / 2^n), -127, 127) for |w| < 2^62: adding 2^(n-1) - 1 plus the
+// parity of the floor quotient rounds exact halves to the even neighbour.
+__device__ __forceinline__ uint32_t int_code(int64_t w, int n, int64_t bias_m1) {
+    const int64_t odd = n ? (w >> n) & 1 : 0;
+    int64_t q = (w + bias_m1 + odd) >> n;
+    q = q > 127 ? 127 : (q < -127 ? -127 : q);
+    return (uint32_t)(int32_t)q;
+}
+
 // row0: the wave's first local row in the tile (local row m = row0 + 16*i + p is
 // grid point (gi0 + m / TW, gj0 + m % TW)).  col_t / col_b: LDS column factors
 // (column_factors, followed by a block barrier).
@@ -159,21 +230,23 @@ __device__ __forceinline__ void fwht_acc(float (&v)[16], int b) {
 // NB the block size of the next operand's absmax (0: not wanted), both for
 // fp32 output; WB = NB = -1 is the generic body, which takes the output mode,
 // form and block sizes from the arguments.
-// Q = 1: I8 output (the next operand's codes, NB its transform block).
+// Q = 1: I8 output (the next operand's codes, NB its transform block); Q = 2:
+// the same codes by the integer transition (mode 3).
 template <int WB_, int NB_, int Q_ = 0>
 struct Epi {
     static constexpr int WB = WB_, NB = NB_, Q = Q_;
 };
 using EpiGeneric = Epi<-1, -1>;
+using EpiGenericInt = Epi<-1, -1, 2>;   // the integer transition, blocks at run time
 
 // The variant a launch needs, or the generic one.
 template <typename E>
 bool epi_matches(const ConvArgs &a) {
     if constexpr (E::WB == -1) {
-        return true;
+        return (a.mode == kModeIntTransition) == (E::Q == 2);
     } else {
         const int wb = a.form == 1 ? a.hblock : 0;
-        if (E::Q) return a.mode == 2 && wb == E::WB && a.next_hblock == E::NB;
+        if (E::Q) return a.mode == (E::Q == 2 ? kModeIntTransition : 2) && wb == E::WB && a.next_hblock == E::NB;
         const int nb = a.next_absmax != nullptr ? a.next_hblock : 0;
         return a.mode == 1 && wb == E::WB && nb == E::NB;
     }
@@ -184,13 +257,14 @@ template <typename E>
 struct EpiFlags {
     static constexpr int WB = E::WB, NB = E::NB;
     static constexpr bool generic = WB == -1;
-    bool f32, wh, want_abs, i8, store;
+    bool f32, wh, want_abs, i8, iq, store;
     __device__ explicit EpiFlags(const ConvArgs &a) {
-        f32 = generic ? a.mode != 0 : true;   // the fp32 arithmetic (F32 and I8 modes)
-        wh = generic ? f32 && a.form == 1 : WB != 0;
-        want_abs = generic ? a.mode == 1 && a.next_absmax != nullptr && a.next_hblock > 0 : E::Q == 0 && NB != 0;
-        i8 = generic ? a.mode == 2 : E::Q != 0;
-        store = !i8 && a.y != nullptr;        // I32 / F32 values
+        iq = E::Q == 2;   // integer transition (its own variants, generic ones included)
+        f32 = !iq && (generic ? a.mode != 0 : true);   // the fp32 arithmetic (F32 and I8 modes)
+        wh = generic ? a.mode != 0 && a.form == 1 : WB != 0;
+        want_abs = !iq && (generic ? a.mode == 1 && a.next_absmax != nullptr && a.next_hblock > 0 : E::Q == 0 && NB != 0);
+        i8 = !iq && (generic ? a.mode == 2 : E::Q == 1);
+        store = !i8 && !iq && a.y != nullptr;   // I32 / F32 values
     }
 };
 
@@ -265,7 +339,8 @@ struct Epilogue {
     const EpiFlags<E> fl;
     bool full, z_bound, q_fast;
     float wave_m, seen, qs, qr;
-    int nbk;
+    int nbk, rq_n;
+    int64_t rq_bias;
     bool valid[FM];
 
     __device__ __forceinline__ Epilogue(const ConvArgs &a_, const Tile &t_, int row0_, int lane_, const float *col_t_,
@@ -301,6 +376,14 @@ struct Epilogue {
             q_fast = qs >= 0x1p-125f && qs <= 0x1p125f;
             if (a.q_absmax && t.gi0 == 0 && t.gj0 == 0 && t.n0 == 0 && row0 == 0 && lane == 0) a.q_scale[t.nb] = qs;
         }
+        // integer transition: the shared shift n (in [0, 62]) after the two tables
+        rq_n = 0;
+        rq_bias = 0;
+        if (fl.iq) {
+            rq_n = __builtin_amdgcn_readfirstlane(a.rq_table[2 * a.cout_pad]);
+            rq_n = rq_n < 0 ? 0 : (rq_n > 62 ? 62 : rq_n);   // the parameter call keeps n in [0, 62]
+            rq_bias = rq_n ? ((int64_t)1 << (rq_n - 1)) - 1 : 0;
+        }
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
             const int m = row0 + 16 * i + p;
@@ -308,8 +391,55 @@ struct Epilogue {
         }
     }
 
+    // Integer transition of block k: p = M (.) (acc + b_int) in int64, the WH
+    // output transform, the next operand's transform, then the codes
+    // clamp(rne(w / 2^n)).  Rows do not mix (the butterflies pair lanes of one
+    // pixel), and channels past cout only meet channels past cout in the next
+    // transform (cout is a multiple of its block), so neither needs masking.
+    __device__ __forceinline__ void block_int(const v4i (&acc)[FM][FN], int k) {
+        v4i m4[4], b4[4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            const int cl = 64 * k + 16 * jj + 4 * q;
+            m4[jj] = *reinterpret_cast<const v4i *>(col_t + cl);
+            b4[jj] = *reinterpret_cast<const v4i *>(col_b + cl);
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            int64_t v[16];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const v4i c4 = acc[i][4 * k + jj];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[4 * jj + r] = (int64_t)m4[jj][r] * (int64_t)(c4[r] + b4[jj][r]);
+            }
+            if (fl.wh) fwht_acc_i64<WB>(v, a.hblock);
+            fwht_acc_i64<NB>(v, a.next_hblock);
+            if (valid[i]) {
+                uint32_t w[4];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+                    w[jj] = pack_low_bytes(int_code(v[4 * jj], rq_n, rq_bias), int_code(v[4 * jj + 1], rq_n, rq_bias),
+                                           int_code(v[4 * jj + 2], rq_n, rq_bias),
+                                           int_code(v[4 * jj + 3], rq_n, rq_bias));
+                const int m = row0 + 16 * i + p;
+                int8_t *yq = reinterpret_cast<int8_t *>(a.y) +
+                             out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW) * a.cout + t.n0;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int cl = 64 * k + 16 * jj + 4 * q;
+                    if (t.n0 + cl < a.cout) *reinterpret_cast<uint32_t *>(yq + cl) = w[jj];
+                }
+            }
+        }
+    }
+
     // 64-channel block k of every row group (one set of column factors serves all)
     __device__ __forceinline__ void block(const v4i (&acc)[FM][FN], int k) {
+        if (fl.iq) {
+            block_int(acc, k);
+            return;
+        }
         const bool f32 = fl.f32, wh = fl.wh, want_abs = fl.want_abs, i8 = fl.i8, store = fl.store;
         float4 t4[4], b4[4];
         if (f32) {
@@ -568,7 +698,7 @@ __global__ void __launch_bounds__(kThreads, 2) conv_rowrun_kernel(const ConvArgs
         }
         patch_load(tile_of(t_first), pwd);
         float colv_t = 0.0f, colv_b = 0.0f;
-        if (tid < BN) column_factor(a, a.sx[nb], n0 + tid, colv_t, colv_b);
+        if (tid < BN) column_factor(a, tile_sx(a, nb), n0 + tid, colv_t, colv_b);
 #pragma unroll
         for (int it = 0; it < BIT; ++it) {
             const int pc = tid + it * kThreads;
@@ -812,11 +942,11 @@ int64_t set_tiles(ConvArgs &b, int TH, int TW, int BN) {
 }
 
 // Launch with the first epilogue variant of Es that matches (the last must be
-// EpiGeneric).
+// EpiGeneric, taken for anything the others do not match).
 template <typename E, typename... Es, typename L>
 hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
     if constexpr (sizeof...(Es) == 0) {
-        static_assert(E::WB == -1, "the generic variant comes last");
+        static_assert(E::WB == -1 && E::Q == 0, "the generic variant comes last");
         return launch(E{});
     } else {
         if (epi_matches<E>(a)) return launch(E{});
@@ -826,7 +956,9 @@ hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
 
 // Variants compiled for the layer shapes of the analysis transforms: DH or WH
 // blocks of 64, next operand blocked by 64 (DH next), 1 (WH next) or none.
-#define HATQ_HOT_EPILOGUES Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, EpiGeneric
+#define HATQ_GENERIC_EPILOGUES EpiGenericInt, EpiGeneric
+#define HATQ_HOT_EPILOGUES \
+    Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_GENERIC_EPILOGUES
 
 template <int TH, int TW, int BN, int CS, typename E>
 hipError_t launch_rowrun(const ConvArgs &a, hipStream_t st) {
@@ -846,12 +978,16 @@ template <int CS>
 hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
     if (a.cout_pad % 192 == 0) {
         if constexpr (CS == 3)
-            return with_epilogue<Epi<64, 64, 1>, HATQ_HOT_EPILOGUES>(
+            return with_epilogue<Epi<64, 64, 1>, Epi<64, 64, 2>, HATQ_HOT_EPILOGUES>(
                 a, [&](auto e) { return launch_rowrun<2, 64, 192, CS, decltype(e)>(a, st); });
-        return launch_rowrun<2, 64, 192, CS, EpiGeneric>(a, st);
+        return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+            a, [&](auto e) { return launch_rowrun<2, 64, 192, CS, decltype(e)>(a, st); });
     }
-    if (a.cout_pad % 128 == 0) return launch_rowrun<2, 64, 128, CS, EpiGeneric>(a, st);
-    return launch_rowrun<2, 64, 64, CS, EpiGeneric>(a, st);
+    if (a.cout_pad % 128 == 0)
+        return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+            a, [&](auto e) { return launch_rowrun<2, 64, 128, CS, decltype(e)>(a, st); });
+    return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+        a, [&](auto e) { return launch_rowrun<2, 64, 64, CS, decltype(e)>(a, st); });
 }
 
 template <int TH, int TW, int BN, int CS>
@@ -859,8 +995,10 @@ hipError_t launch_gather(const ConvArgs &a, hipStream_t st) {
     ConvArgs b = a;
     const int64_t tiles = set_tiles(b, TH, TW, BN);
     if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-    conv_gather_kernel<TH, TW, BN, CS, EpiGeneric><<<(unsigned)tiles, kThreads, 0, st>>>(b);
-    return hipGetLastError();
+    return with_epilogue<HATQ_GENERIC_EPILOGUES>(b, [&](auto e) {
+        conv_gather_kernel<TH, TW, BN, CS, decltype(e)><<<(unsigned)tiles, kThreads, 0, st>>>(b);
+        return hipGetLastError();
+    });
 }
 
 template <int CS>
@@ -1552,6 +1690,22 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, s_col, s_col + BN);
 }
 
+// The arguments of the launch over samples [s0, s0 + gn) of a.
+ConvArgs sample_group(const ConvArgs &a, int64_t s0, int gn) {
+    ConvArgs b = a;
+    b.n = gn;
+    b.xq = a.xq + s0 * ((int64_t)a.h * a.w * a.cin_p);
+    if (a.sx) b.sx = a.sx + s0;
+    const int64_t out_per_sample = (int64_t)a.ho * a.wo * (a.mode == 0 ? a.cout_pad : a.cout);
+    const int64_t elem_bytes = a.mode >= 2 ? 1 : 4;   // I8 codes, else 32-bit values
+    if (a.y) b.y = (void *)((char *)a.y + s0 * out_per_sample * elem_bytes);
+    if (a.next_absmax) b.next_absmax = a.next_absmax + s0;
+    if (a.q_absmax) b.q_absmax = a.q_absmax + s0;
+    if (a.q_scale) b.q_scale = a.q_scale + s0;
+    b.M = (int64_t)gn * a.gh * a.gw;
+    return b;
+}
+
 template <int BN, int STAGES, typename E>
 hipError_t launch_halo(const ConvArgs &a, hipStream_t st) {
     static_assert(STAGES == 5, "ring");
@@ -1563,15 +1717,8 @@ hipError_t launch_halo(const ConvArgs &a, hipStream_t st) {
     if ((int64_t)a.cout_pad * a.pack_stride >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     if (a.sa != 2 || a.so != 1 || a.k < 4 || a.k > 6 || a.cin_p % 64) return hipErrorInvalidValue;
     for (int64_t s0 = 0; s0 < a.n; s0 += group) {
-        ConvArgs b = a;
         const int gn = (int)(a.n - s0 < group ? a.n - s0 : group);
-        b.n = gn;
-        b.xq = a.xq + s0 * per_sample;
-        b.sx = a.sx + s0;
-        const int64_t out_per_sample = (int64_t)a.ho * a.wo * (a.mode == 0 ? a.cout_pad : a.cout);
-        b.y = (void *)((char *)a.y + s0 * out_per_sample * 4);
-        if (a.next_absmax) b.next_absmax = a.next_absmax + s0;
-        b.M = (int64_t)gn * a.gh * a.gw;
+        ConvArgs b = sample_group(a, s0, gn);
         const int64_t tiles = set_tiles(b, HaloGeom::TH, HaloGeom::TW, BN);
         if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
         if (a.k == 5) conv_halo5_kernel<BN, E><<<(unsigned)tiles, kHaloThreads, 0, st>>>(b);
@@ -1589,15 +1736,8 @@ hipError_t launch_pipe(const ConvArgs &a, hipStream_t st) {
     if (group < 1) return hipErrorInvalidValue;
     if ((int64_t)a.cout_pad * a.pack_stride >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     for (int64_t s0 = 0; s0 < a.n; s0 += group) {
-        ConvArgs b = a;
         const int gn = (int)(a.n - s0 < group ? a.n - s0 : group);
-        b.n = gn;
-        b.xq = a.xq + s0 * per_sample;
-        b.sx = a.sx + s0;
-        const int64_t out_per_sample = (int64_t)a.ho * a.wo * (a.mode == 0 ? a.cout_pad : a.cout);
-        b.y = (void *)((char *)a.y + s0 * out_per_sample * 4);
-        if (a.next_absmax) b.next_absmax = a.next_absmax + s0;
-        b.M = (int64_t)gn * a.gh * a.gw;
+        ConvArgs b = sample_group(a, s0, gn);
         const int64_t tiles = set_tiles(b, TH, TW, BN);
         if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
         conv_pipe_kernel<TH, TW, BN, STAGES, E><<<(unsigned)tiles, kThreads, 0, st>>>(b);
@@ -1613,19 +1753,23 @@ hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
     switch (a.cin_p <= 4 ? a.cin_p : 0) {
         case 0:
             switch (a.cout_pad) {
-                case 64: return launch_pipe<8, 32, 64, 5, EpiGeneric>(a, st);
-                case 128: return launch_pipe<8, 32, 128, 5, EpiGeneric>(a, st);
+                case 64: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+                        a, [&](auto e) { return launch_pipe<8, 32, 64, 5, decltype(e)>(a, st); });
+                case 128: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+                        a, [&](auto e) { return launch_pipe<8, 32, 128, 5, decltype(e)>(a, st); });
                 case 192:
                     if (a.sa == 2 && a.so == 1 && a.k >= 4 && a.k <= 6)
                         return with_epilogue<HATQ_HOT_EPILOGUES>(
                             a, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st); });
                     return with_epilogue<HATQ_HOT_EPILOGUES>(
                         a, [&](auto e) { return launch_pipe<8, 32, 192, 5, decltype(e)>(a, st); });
-                case 256: return launch_pipe<4, 32, 256, 5, EpiGeneric>(a, st);
+                case 256: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+                        a, [&](auto e) { return launch_pipe<4, 32, 256, 5, decltype(e)>(a, st); });
                 case 320:
                     return with_epilogue<HATQ_HOT_EPILOGUES>(
                         a, [&](auto e) { return launch_pipe<4, 32, 320, 5, decltype(e)>(a, st); });
-                default: return launch_pipe<8, 32, 64, 5, EpiGeneric>(a, st);
+                default: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+                        a, [&](auto e) { return launch_pipe<8, 32, 64, 5, decltype(e)>(a, st); });
             }
         case 1: return a.rowrun ? launch_rowrun_n<1>(a, st) : launch_gather_n<1>(a, st);
         case 2: return a.rowrun ? launch_rowrun_n<2>(a, st) : launch_gather_n<2>(a, st);

@@ -12,6 +12,7 @@ hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const 
                             float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st);
 
 constexpr int kMaxTaps = 64;
+constexpr int kModeIntTransition = 3;   // ConvArgs::mode of the integer transition
 
 // Geometry and operands of one implicit-GEMM launch.  GEMM rows are the points
 // (nb, gi, gj) of an n x gh x gw grid, processed in 2-D tiles of TH x TW points.  Input anchor of a point:
@@ -27,6 +28,7 @@ struct ConvArgs {
     float *next_absmax;
     const float *q_absmax; // I8 mode: per-sample max |B_next y| giving the scale, or NULL
     float *q_scale;        // I8 mode: per-sample scale (written from q_absmax, else read)
+    const int32_t *rq_table;   // mode 3: M [cout_pad], b_int [cout_pad], shift n
     int64_t M;             // n * gh * gw
     int32_t n, h, w, cin_p;
     int32_t gh, gw;
@@ -37,7 +39,8 @@ struct ConvArgs {
     int32_t rowrun;        // small-cin layer contracted per kernel row (16 B each)
     int32_t cout, cout_pad;
     int32_t form;          // 0 DH, 1 WH
-    int32_t mode;          // 0 I32, 1 F32, 2 I8 (codes of B_next y, next_hblock the block)
+    int32_t mode;          // 0 I32, 1 F32, 2 I8 (codes of B_next y, next_hblock the block),
+                           // 3 the same codes by the integer transition (rq_table)
     int32_t hblock;        // the layer's block size
     int32_t next_hblock;   // 0 = no next-operand absmax
     int32_t tiles_h, tiles_w, tiles_n;   // 2-D tiles of grid points per sample; column tiles
@@ -63,5 +66,18 @@ struct PrepArgs {
 hipError_t launch_prepare(const PrepArgs &a, hipStream_t st);
 // Rebuild wpack from wq (geometry fields, wq and wpack are used).
 hipError_t launch_pack(const PrepArgs &a, hipStream_t st);
+
+// Fixed-point parameters of the integer transition from static scales.
+struct IntParamArgs {
+    const float *w_scale;  // [cout_p]
+    const float *bias;     // [cout_p], the prepared bias (WH: in the output basis)
+    int32_t *table;        // out: M [cout_p], b_int [cout_p], shift n (-1: none fits)
+    float s_x, s_y;
+    int32_t cout_p;
+    int32_t beta_in, beta_out;   // DH: (hblock, 1); WH: (1, hblock)
+    int32_t K;                   // contraction length k*k*cin_p
+    int32_t gain;                // WH output block times the next operand's block
+};
+hipError_t launch_int_params(const IntParamArgs &a, hipStream_t st);
 
 }  // namespace hatq

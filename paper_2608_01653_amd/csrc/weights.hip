@@ -98,7 +98,66 @@ __global__ void __launch_bounds__(kThreads) prepare_kernel(const PrepArgs a) {
     }
 }
 
+// Integer transition parameters (Eq. integer_accumulation, Eq.
+// integer_fixed_point_scale), one block.  One accumulator step of channel c is
+// u_c = s_x s_w,c / beta_in (exact: a product of two floats over a power of
+// two), so b_int,c = rne(b_c / u_c); the scale ratio rho_c = u_c / (beta_out
+// s_y) becomes M_c = rne(2^n rho_c) with the shared shift n, the largest in
+// [0, 62] that keeps every M_c at or below floor(2^62 / (A_max G)) (and below
+// 2^31), A_max = K 127^2 + max |b_int| bounding |acc + b_int| and G the gain of
+// the two transforms, so every int64 partial sum of the transition is exact.
+// fp64 with correctly rounded division throughout; |b_int| >= 2^30 or no
+// fitting n gives n = -1.
+__global__ void __launch_bounds__(kThreads) int_params_kernel(const IntParamArgs a) {
+    __shared__ double s_bmax[kThreads];
+    __shared__ int s_n[kThreads];
+    const int tid = threadIdx.x;
+    double bmax = 0.0;
+    for (int c = tid; c < a.cout_p; c += kThreads) {
+        const double u = (double)a.s_x * (double)a.w_scale[c] / (double)a.beta_in;
+        const double bi = rint((double)a.bias[c] / u);
+        const bool big = !(fabs(bi) < 1073741824.0);   // also catches NaN
+        a.table[a.cout_p + c] = big ? 0 : (int32_t)bi;
+        bmax = fmax(bmax, big ? INFINITY : fabs(bi));
+    }
+    s_bmax[tid] = bmax;
+    __syncthreads();
+    for (int h = kThreads / 2; h > 0; h >>= 1) {
+        if (tid < h) s_bmax[tid] = fmax(s_bmax[tid], s_bmax[tid + h]);
+        __syncthreads();
+    }
+    const double bm = s_bmax[0];
+    const double amax = (double)a.K * 127.0 * 127.0 + bm;
+    double mmax = floor(4611686018427387904.0 / (amax * (double)a.gain));
+    if (mmax > 2147483647.0) mmax = 2147483647.0;
+    const double den = (double)a.beta_in * (double)a.beta_out * (double)a.s_y;
+    int nmin = bm < 1073741824.0 ? 62 : -1;
+    for (int c = tid; c < a.cout_p; c += kThreads) {
+        const double rho = (double)a.s_x * (double)a.w_scale[c] / den;
+        int n = nmin;
+        while (n >= 0 && rint(ldexp(rho, n)) > mmax) --n;
+        nmin = n;
+    }
+    s_n[tid] = nmin;
+    __syncthreads();
+    for (int h = kThreads / 2; h > 0; h >>= 1) {
+        if (tid < h) s_n[tid] = min(s_n[tid], s_n[tid + h]);
+        __syncthreads();
+    }
+    const int n = s_n[0];
+    for (int c = tid; c < a.cout_p; c += kThreads) {
+        const double rho = (double)a.s_x * (double)a.w_scale[c] / den;
+        a.table[c] = n >= 0 ? (int32_t)rint(ldexp(rho, n)) : 0;
+    }
+    if (tid == 0) a.table[2 * a.cout_p] = n;
+}
+
 }  // namespace
+
+hipError_t launch_int_params(const IntParamArgs &a, hipStream_t st) {
+    int_params_kernel<<<1, kThreads, 0, st>>>(a);
+    return hipGetLastError();
+}
 
 hipError_t launch_prepare(const PrepArgs &a, hipStream_t st) {
     prepare_kernel<<<a.cout_p, kThreads, 0, st>>>(a);

@@ -46,7 +46,8 @@ class Weights(ctypes.Structure):
 
 EXPORTS = ["hatq_status_string", "hatq_conv_out_hw", "hatq_weights_bytes", "hatq_prepare_weights",
            "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act", "hatq_conv_int8",
-           "hatq_conv_int8_requant",
+           "hatq_conv_int8_requant", "hatq_int_table_len", "hatq_int_transition_params",
+           "hatq_conv_int8_int_transition",
            "hatq_layer_ws_bytes", "hatq_layer_forward"]
 
 _lib = None
@@ -86,6 +87,13 @@ def load(build_if_missing: bool = False):
     L.hatq_conv_int8.restype = i32
     L.hatq_conv_int8_requant.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, P, P, P]
     L.hatq_conv_int8_requant.restype = i32
+    L.hatq_int_table_len.argtypes = [ctypes.POINTER(Weights)]
+    L.hatq_int_table_len.restype = sz
+    L.hatq_int_transition_params.argtypes = [ctypes.POINTER(Weights), ctypes.c_float, ctypes.c_float, i32, P,
+                                             ctypes.POINTER(i32), P]
+    L.hatq_int_transition_params.restype = i32
+    L.hatq_conv_int8_int_transition.argtypes = [ctypes.POINTER(Weights), P, i32, i32, i32, i32, P, P, P]
+    L.hatq_conv_int8_int_transition.restype = i32
     L.hatq_layer_ws_bytes.argtypes = [ctypes.POINTER(Weights), i32, i32, i32]
     L.hatq_layer_ws_bytes.restype = sz
     L.hatq_layer_forward.argtypes = [ctypes.POINTER(Weights), i32, P, i32, i32, i32, P, P, P, i32, P, P,
@@ -249,6 +257,35 @@ def hatq_conv_int8_requant(layer: PreparedLayer, xq: torch.Tensor, act_scale: to
                                          _stream(stream)),
            "hatq_conv_int8_requant")
     return yq, next_scale
+
+
+def hatq_int_table_len(layer: PreparedLayer) -> int:
+    return int(load().hatq_int_table_len(ctypes.byref(layer.w)))
+
+
+def hatq_int_transition_params(layer: PreparedLayer, s_x: float, s_y: float, next_hblock: int,
+                               table: Optional[torch.Tensor] = None, device="cuda", stream=None):
+    """Integer transition table (M, b_int, shift) from static scales: returns (table, shift)."""
+    if table is None:
+        table = torch.empty((hatq_int_table_len(layer),), dtype=torch.int32, device=device)
+    n = ctypes.c_int32(-1)
+    _check(load().hatq_int_transition_params(ctypes.byref(layer.w), float(s_x), float(s_y), int(next_hblock),
+                                             _ptr(table), ctypes.byref(n), _stream(stream)),
+           "hatq_int_transition_params")
+    return table, int(n.value)
+
+
+def hatq_conv_int8_int_transition(layer: PreparedLayer, xq: torch.Tensor, next_hblock: int, table: torch.Tensor,
+                                  yq: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Conv with the integer-only epilogue: the next layer's codes."""
+    n, h, w, _ = xq.shape
+    ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
+    if yq is None:
+        yq = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.int8, device=xq.device)
+    _check(load().hatq_conv_int8_int_transition(ctypes.byref(layer.w), _ptr(xq), n, h, w, int(next_hblock),
+                                                _ptr(table), _ptr(yq), _stream(stream)),
+           "hatq_conv_int8_int_transition")
+    return yq
 
 
 def hatq_layer_ws_bytes(layer: PreparedLayer, n: int, h: int, w: int) -> int:

@@ -158,6 +158,31 @@ def test_requant_rejects_before_launch(L):
         == hatq.HATQ_EINVAL                                                                           # misaligned
 
 
+def test_int_transition_rejects_before_launch(L):
+    W = _fake_weights()
+    assert L.hatq_int_table_len(ctypes.byref(W)) == 2 * W.cout_pad + 1
+    assert L.hatq_int_table_len(None) == 0
+    p = L.hatq_int_transition_params
+    assert p(None, 0.1, 0.1, 64, FAKE, None, None) == hatq.HATQ_EINVAL
+    assert p(ctypes.byref(W), 0.0, 0.1, 64, FAKE, None, None) == hatq.HATQ_EINVAL           # s_x not positive
+    assert p(ctypes.byref(W), 0.1, float("inf"), 64, FAKE, None, None) == hatq.HATQ_EINVAL  # s_y not finite
+    assert p(ctypes.byref(W), 0.1, float("nan"), 64, FAKE, None, None) == hatq.HATQ_EINVAL
+    assert p(ctypes.byref(W), 0.1, 0.1, 3, FAKE, None, None) == hatq.HATQ_EINVAL            # block 3
+    assert p(ctypes.byref(W), 0.1, 0.1, 128, FAKE, None, None) == hatq.HATQ_EINVAL          # above 64
+    assert p(ctypes.byref(W), 0.1, 0.1, 64, None, None, None) == hatq.HATQ_EINVAL           # no table
+    assert p(ctypes.byref(W), 0.1, 0.1, 64, ctypes.c_void_p(FAKE.value + 4), None, None) \
+        == hatq.HATQ_EINVAL                                                                   # misaligned
+    c = L.hatq_conv_int8_int_transition
+    assert c(None, FAKE, 1, 8, 8, 64, FAKE, FAKE, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W), FAKE, 0, 8, 8, 64, FAKE, FAKE, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, None, FAKE, None) == hatq.HATQ_EINVAL      # no table
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, FAKE, None, None) == hatq.HATQ_EINVAL      # no output
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 3, FAKE, FAKE, None) == hatq.HATQ_EINVAL       # block 3
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 128, FAKE, FAKE, None) == hatq.HATQ_EUNSUPPORTED
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, ctypes.c_void_p(FAKE.value + 4), FAKE, None) \
+        == hatq.HATQ_EINVAL                                                                   # misaligned table
+
+
 def test_layer_forward_form_flag_and_workspace(L):
     f = L.hatq_layer_forward
     W = _fake_weights()
