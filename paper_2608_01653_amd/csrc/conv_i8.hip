@@ -222,6 +222,16 @@ __device__ __forceinline__ uint32_t int_code(int64_t w, int n, int64_t bias_m1) 
     return (uint32_t)(int32_t)q;
 }
 
+// The same for n = 32 + s, s in [0, 30]: floor(w / 2^n) is the high word
+// shifted right by s, so only the bias addition is 64-bit.
+__device__ __forceinline__ uint32_t int_code_hi(int64_t w, int s, int64_t bias_m1) {
+    const int32_t odd = ((int32_t)(w >> 32) >> s) & 1;
+    const int64_t u = w + bias_m1 + odd;
+    int32_t q = (int32_t)(u >> 32) >> s;
+    q = q > 127 ? 127 : (q < -127 ? -127 : q);
+    return (uint32_t)q;
+}
+
 // row0: the wave's first local row in the tile (local row m = row0 + 16*i + p is
 // grid point (gi0 + m / TW, gj0 + m % TW)).  col_t / col_b: LDS column factors
 // (column_factors, followed by a block barrier).
@@ -339,9 +349,9 @@ struct Epilogue {
     const EpiFlags<E> fl;
     bool full, z_bound, q_fast;
     float wave_m, seen, qs, qr;
-    int nbk, rq_n;
+    int nbk, rq_n, rq_pre;
     int64_t rq_bias;
-    bool valid[FM];
+    bool rq_pair, valid[FM];
 
     __device__ __forceinline__ Epilogue(const ConvArgs &a_, const Tile &t_, int row0_, int lane_, const float *col_t_,
                                         const float *col_b_)
@@ -376,13 +386,27 @@ struct Epilogue {
             q_fast = qs >= 0x1p-125f && qs <= 0x1p125f;
             if (a.q_absmax && t.gi0 == 0 && t.gj0 == 0 && t.n0 == 0 && row0 == 0 && lane == 0) a.q_scale[t.nb] = qs;
         }
-        // integer transition: the shared shift n (in [0, 62]) after the two tables
+        // Integer transition: the shared shift n (in [0, 62]) after the two
+        // tables.  A WH layer whose next operand uses the same blocks has
+        // B_next B_Cout = b I on every kept block (Sylvester blocks square to b
+        // times the identity; cout is a multiple of b, so truncation drops
+        // whole blocks), so w = b p exactly: both transforms are skipped and
+        // the shift absorbs log2(b) (a left shift rq_pre where n < log2(b)).
         rq_n = 0;
+        rq_pre = 0;
         rq_bias = 0;
+        rq_pair = false;
         if (fl.iq) {
-            rq_n = __builtin_amdgcn_readfirstlane(a.rq_table[2 * a.cout_pad]);
-            rq_n = rq_n < 0 ? 0 : (rq_n > 62 ? 62 : rq_n);   // the parameter call keeps n in [0, 62]
-            rq_bias = rq_n ? ((int64_t)1 << (rq_n - 1)) - 1 : 0;
+            int n = __builtin_amdgcn_readfirstlane(a.rq_table[2 * a.cout_pad]);
+            n = n < 0 ? 0 : (n > 62 ? 62 : n);   // the parameter call keeps n in [0, 62]
+            rq_pair = fl.wh && (generic ? a.hblock == a.next_hblock : WB == NB) && a.hblock > 1;
+            if (rq_pair) {
+                const int lg = 31 - __builtin_clz(a.hblock);
+                rq_pre = lg > n ? lg - n : 0;
+                n = lg > n ? 0 : n - lg;
+            }
+            rq_n = n;
+            rq_bias = n ? ((int64_t)1 << (n - 1)) - 1 : 0;
         }
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
@@ -413,15 +437,25 @@ struct Epilogue {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) v[4 * jj + r] = (int64_t)m4[jj][r] * (int64_t)(c4[r] + b4[jj][r]);
             }
-            if (fl.wh) fwht_acc_i64<WB>(v, a.hblock);
-            fwht_acc_i64<NB>(v, a.next_hblock);
+            if (rq_pair) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) v[r] = (int64_t)((uint64_t)v[r] << rq_pre);
+            } else {
+                if (fl.wh) fwht_acc_i64<WB>(v, a.hblock);
+                fwht_acc_i64<NB>(v, a.next_hblock);
+            }
             if (valid[i]) {
+                uint32_t c[16];
+                if (rq_n >= 32) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) c[r] = int_code_hi(v[r], rq_n - 32, rq_bias);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) c[r] = int_code(v[r], rq_n, rq_bias);
+                }
                 uint32_t w[4];
 #pragma unroll
-                for (int jj = 0; jj < 4; ++jj)
-                    w[jj] = pack_low_bytes(int_code(v[4 * jj], rq_n, rq_bias), int_code(v[4 * jj + 1], rq_n, rq_bias),
-                                           int_code(v[4 * jj + 2], rq_n, rq_bias),
-                                           int_code(v[4 * jj + 3], rq_n, rq_bias));
+                for (int jj = 0; jj < 4; ++jj) w[jj] = pack_low_bytes(c[4 * jj], c[4 * jj + 1], c[4 * jj + 2], c[4 * jj + 3]);
                 const int m = row0 + 16 * i + p;
                 int8_t *yq = reinterpret_cast<int8_t *>(a.y) +
                              out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW) * a.cout + t.n0;
@@ -1759,7 +1793,7 @@ hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
                         a, [&](auto e) { return launch_pipe<8, 32, 128, 5, decltype(e)>(a, st); });
                 case 192:
                     if (a.sa == 2 && a.so == 1 && a.k >= 4 && a.k <= 6)
-                        return with_epilogue<HATQ_HOT_EPILOGUES>(
+                        return with_epilogue<Epi<0, 64, 2>, Epi<0, 1, 2>, HATQ_HOT_EPILOGUES>(
                             a, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st); });
                     return with_epilogue<HATQ_HOT_EPILOGUES>(
                         a, [&](auto e) { return launch_pipe<8, 32, 192, 5, decltype(e)>(a, st); });

@@ -59,20 +59,30 @@ def test_int_transition_bit_exact(orc, c, next_b):
     assert np.abs(q_ref.astype(np.int32)).max() == 127        # the static scale reaches the range end
 
 
-def test_int_transition_saturates_and_reuses_table(orc):
-    """A smaller s_y pushes many codes past the range (clamped on both sides);
-    the same table serves a second, smaller input."""
+@pytest.mark.parametrize("next_b", [1, 64])
+@pytest.mark.parametrize("target", [None, 20, 3])
+def test_int_transition_small_shifts_and_reuse(orc, next_b, target):
+    """A smaller s_y pushes codes past the range (clamped on both sides) and
+    lowers the shift by log2 of the factor with the same multipliers: to 20
+    (the general rounding, below 32) and to 3 (below log2 of the block: the WH
+    layer whose next operand has the same blocks then shifts left); None
+    divides s_y by 8.  The same table serves a second, smaller input."""
     c = CONV[2]
-    ref, layer, xq, acc, s_x, s_y = _static_case(orc, c, 64, 92)
-    rq = orc.int_requant_params(ref, s_x, s_y / 8, 64)
-    table, _ = hatq.hatq_int_transition_params(layer, s_x, s_y / 8, 64)
-    q_ref = orc.int_transition(acc, ref, rq, 64)
+    ref, layer, xq, acc, s_x, s_y = _static_case(orc, c, next_b, 92)
+    n1 = orc.int_requant_params(ref, s_x, s_y, next_b).shift
+    shrink = 8.0 if target is None else 2.0 ** (n1 - target)
+    rq = orc.int_requant_params(ref, s_x, s_y / shrink, next_b)
+    assert target is None or rq.shift == target
+    table, n_shift = hatq.hatq_int_transition_params(layer, s_x, s_y / shrink, next_b)
+    assert n_shift == rq.shift
+    assert np.array_equal(host(table)[:layer.w.cout_pad], rq.M)
+    q_ref = orc.int_transition(acc, ref, rq, next_b)
     assert np.count_nonzero(np.abs(q_ref.astype(np.int32)) == 127) > 0.01 * q_ref.size
-    assert_codes(host(hatq.hatq_conv_int8_int_transition(layer, dev(xq), 64, table)), q_ref, exact=True)
+    assert_codes(host(hatq.hatq_conv_int8_int_transition(layer, dev(xq), next_b, table)), q_ref, exact=True)
     small = np.ascontiguousarray(xq[:1, :17, :11])
     acc_s = orc.conv_int8(small, ref.wq, stride=c[6], pad=c[7])
-    assert_codes(host(hatq.hatq_conv_int8_int_transition(layer, dev(small), 64, table)),
-                 orc.int_transition(acc_s, ref, rq, 64), exact=True)
+    assert_codes(host(hatq.hatq_conv_int8_int_transition(layer, dev(small), next_b, table)),
+                 orc.int_transition(acc_s, ref, rq, next_b), exact=True)
 
 
 def test_int_params_no_shift_fits(orc):
