@@ -11,6 +11,10 @@ the per-step functions in the order the paper gives them:
     INT8 x INT8 -> INT32 direct convolution              Eq. integer_accumulation
     dequant (s_x s_w,c / b), bias, WH basis restore      Eq. accumulator_scale,
                                                          Eq. supp_padded_dh, Eq. supp_padded_wh
+    integer-only transition (M, b_int, shift; int64)     Eq. integer_fixed_point_scale,
+                                                         Eq. integer_hadamard_transition
+    range-expansion statistic and the DH/WH rule         Eq. hadamard_sensitivity,
+                                                         Eq. layerwise_hadamard_selection
 
 Parity status: every function is pinned by the CPU tests (identities of the
 Hadamard matrix, a library special case for the convolution, function
@@ -68,6 +72,8 @@ def lib():
         L.orc_epilogue.argtypes = [P, i32, i64, i32, i32, i32, i32, P, P, P, P]
         L.orc_int_requant_params.argtypes = [i32, ctypes.c_float, P, P, ctypes.c_float, i32, i32, i32, i32, P, P]
         L.orc_int_transition.argtypes = [P, i64, i32, i32, P, P, i32, i32, i32, P]
+        L.orc_range_expansion.argtypes = [P, i32, i64, i32, i32, P, P, P]
+        L.orc_select_form.argtypes = [i64, i64, ctypes.c_double]
         _lib = L
     return _lib
 
@@ -310,3 +316,29 @@ def int_transition(acc: np.ndarray, pw: PreparedWeights, rq: IntRequant, next_b:
                                 _p(_c(rq.b_int, np.int32)), rq.shift, wb, next_b, _p(q)) != 0:
         raise ValueError("bad transition geometry")
     return q
+
+
+# --------------------------------------------------------------------------
+# O7  Range-expansion profiling and the form rule
+# --------------------------------------------------------------------------
+def range_expansion(x: np.ndarray, b: int):
+    """Per sample of x [n, ..., C]: (max |x|, max |fl32(B_C x_pad)|, expands)
+    with expands = max|S|^2 > b max|x|^2 (Eq. hadamard_sensitivity with the
+    orthonormal transform B / sqrt(b))."""
+    x = _c(x, np.float32)
+    n, C = x.shape[0], x.shape[-1]
+    P = x.size // (n * C)
+    ax = np.empty(n, np.float32)
+    ah = np.empty(n, np.float32)
+    fl = np.empty(n, np.int32)
+    if lib().orc_range_expansion(_p(x), n, P, C, b, _p(ax), _p(ah), _p(fl)) != 0:
+        raise ValueError("bad block size or shape")
+    return ax, ah, fl
+
+
+def select_form(expansions: int, images: int, tau: float = 0.8) -> str:
+    """Eq. layerwise_hadamard_selection: "WH" if expansions / images > tau, else "DH"."""
+    r = lib().orc_select_form(int(expansions), int(images), float(tau))
+    if r < 0:
+        raise ValueError("bad counts")
+    return "WH" if r else "DH"

@@ -474,3 +474,60 @@ int orc_int_transition(const int32_t *acc, int64_t P, int cout, int cout_p, cons
     free(Hi);
     return 0;
 }
+
+/* ------------------------------------------------------------------------- */
+/* O7. Range-expansion profiling (Eq. hadamard_sensitivity) and the form     */
+/* rule (Eq. layerwise_hadamard_selection).                                   */
+/* For sample k of x [n][P][C] (its pixels padded with zero channels to a     */
+/* multiple of b): ax[k] = max |x|, ah[k] = max |S| with S = fl32(B_C x_pad)  */
+/* as in O3 (the unnormalized transform the activation quantizer sees).  The */
+/* paper compares the orthonormal transform H = B / sqrt(b) against x, so    */
+/* the sample expands iff ah > sqrt(b) ax, decided exactly as                 */
+/*   ah^2 > b ax^2   in fp64 (squares of fp32 values and their products by a  */
+/*                    power of two are exact in fp64).                        */
+/* ------------------------------------------------------------------------- */
+int orc_range_expansion(const float *x, int n, int64_t P, int C, int b, float *ax, float *ah, int32_t *flags)
+{
+    if (!is_pow2(b) || C <= 0 || n <= 0 || P <= 0) return -1;
+    const int Cp = round_up(C, b);
+    int8_t *H = (int8_t *)malloc((size_t)b * b);
+    orc_sylvester(b, H);
+    for (int k = 0; k < n; ++k) {
+        const float *xs = x + (int64_t)k * P * C;
+        float mx = 0.0f, mh = 0.0f;
+        #pragma omp parallel reduction(max : mx, mh)
+        {
+            double *in = (double *)malloc(sizeof(double) * Cp);
+            double *out = (double *)malloc(sizeof(double) * Cp);
+            #pragma omp for schedule(static)
+            for (int64_t p = 0; p < P; ++p) {
+                for (int c = 0; c < Cp; ++c) {
+                    in[c] = c < C ? (double)xs[p * C + c] : 0.0;
+                    if (c < C && fabsf(xs[p * C + c]) > mx) mx = fabsf(xs[p * C + c]);
+                }
+                block_transform_f64(H, b, in, out, 1, Cp);
+                for (int c = 0; c < Cp; ++c) {
+                    const float v = fabsf((float)out[c]);
+                    if (v > mh) mh = v;
+                }
+            }
+            free(in);
+            free(out);
+        }
+        ax[k] = mx;
+        ah[k] = mh;
+        flags[k] = (double)mh * (double)mh > (double)b * ((double)mx * (double)mx);
+    }
+    free(H);
+    return 0;
+}
+
+/* pi = WH (1) if p = expansions / images > tau, else DH (0); p is the       */
+/* correctly rounded fp64 quotient.  -1 for images <= 0 or a count outside    */
+/* [0, images].                                                               */
+int orc_select_form(int64_t expansions, int64_t images, double tau)
+{
+    if (images <= 0 || expansions < 0 || expansions > images) return -1;
+    const double p = (double)expansions / (double)images;
+    return p > tau ? 1 : 0;
+}
