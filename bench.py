@@ -160,6 +160,54 @@ def measure_integer_stack(args, wl, layers, x0, xq, sc, ys, ws, act_hb, total_op
                     "Hadamard transforms in the conv epilogue); static per-tensor scales"}
 
 
+def measure_form_selection(args, wl, layers, x0, xq, sc, ys, tau=0.8):
+    """The profiling pass of the form rule on this batch: for each layer's fp32
+    input, the per-image range-expansion indicator with the layer's block, the
+    probability p_l over the batch's images and the form it selects.  The pass
+    over layer 2's input (the largest activation) is timed: it is one read of
+    the tensor, HBM bound."""
+    import torch
+    from paper_2608_01653_amd import hatq
+    n = x0.shape[0]
+    # layer 1's fp32 output (the stack itself only forms its codes), from
+    # dynamically quantized input codes
+    L1 = wl.layers[0]
+    hatq.hatq_fwht_quant_act(x0, L1.hblock if L1.form == "DH" else 1, xq=xq[0], scale=sc[0])
+    hatq.hatq_conv_int8(layers[0], xq[0], sc[0], hatq.HATQ_OUT_F32, y=ys[0])
+    inputs = [x0] + ys[:len(layers) - 1]
+    p, sel = [], []
+    amax = torch.empty(2 * n, dtype=torch.float32, device=x0.device)
+    flags = torch.empty(n, dtype=torch.int32, device=x0.device)
+    for L, xin in zip(wl.layers, inputs):
+        count = torch.zeros(1, dtype=torch.int32, device=x0.device)
+        hatq.hatq_range_expansion(xin, L.hblock, amax=amax, flags=flags, count=count)
+        k = int(count.item())
+        p.append(round(k / n, 4))
+        sel.append(hatq.hatq_select_form(k, n, tau))
+    x2 = inputs[1]
+    reps = max(args.steps, 5)
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    hatq.hatq_range_expansion(x2, wl.layers[1].hblock, amax=amax, flags=flags)
+    torch.cuda.synchronize()
+    t0.record()
+    for _ in range(reps):
+        hatq.hatq_range_expansion(x2, wl.layers[1].hblock, amax=amax, flags=flags)
+    t1.record()
+    torch.cuda.synchronize()
+    us = t0.elapsed_time(t1) / reps * 1e3
+    nbytes = x2.numel() * 4
+    gbs = nbytes / (us * 1e-6) / 1e9
+    log(f"form selection: p = {p}, selected {sel}; profiling pass {us:.1f} us")
+    return {"tau": tau, "images": n, "p": p, "selected": sel,
+            "configured": [L.form for L in wl.layers],
+            "profile_pass": {"kernel": f"range_kernel<{wl.layers[1].hblock}> (layer 2 input)",
+                             "us": round(us, 2), "bound": "hbm", "achieved": round(gbs, 1),
+                             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                             "work": f"{nbytes} bytes per call = {x2.numel()} fp32 elements read once"},
+            "note": "random-init weights and synthetic inputs: the selection shows the mechanism, "
+                    "not the paper's trained-model assignment"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -318,6 +366,7 @@ def main():
               "work": f"{eq * 5} bytes per launch = {eq} elements x (4 B fp32 in + 1 B int8 out)"}
 
     integer_stack = measure_integer_stack(args, wl, layers, x0, xq, sc, ys, ws, act_hb, total_ops, img_pix)
+    form_selection = measure_form_selection(args, wl, layers, x0, xq, sc, ys)
 
     out = {
         "metric": "Hadamard-INT8 conv TOPS + Mpixel/s per layer; % of INT8 MFMA / HBM peak",
@@ -337,6 +386,7 @@ def main():
         "roofline": roof,
         "roofline_act_quant": roof_q,
         "integer_stack": integer_stack,
+        "form_selection": form_selection,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, x_np, params)

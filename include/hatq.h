@@ -247,6 +247,29 @@ int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, i
                                       int32_t w, int32_t next_hblock, const int32_t *table,
                                       int8_t *yq, void *stream);
 
+/* Range-expansion profiling (Eq. hadamard_sensitivity): for each sample k of
+ * a layer's input x, whether the layer's input-side transform enlarges the
+ * range, ||H x_k||_inf > ||x_k||_inf with H = B_C / sqrt(hblock) orthonormal
+ * (B_C the block-diagonal Sylvester transform, channels zero-padded to a
+ * multiple of hblock).  Decided exactly as max|S|^2 > hblock * max|x|^2 in
+ * fp64, S the fp32 butterfly transform hatq_fwht_quant_act applies.
+ *   x:      device fp32 [n][h][w][c], 16-byte aligned; n <= 65535.
+ *   hblock: power of two <= 128 (1: no transform, never an expansion).
+ *   amax:   device fp32 [2n], written: max|x_k| at [k], max|S_k| at [n + k].
+ *   flags:  NULL, or device int32 [n] receiving 1 (expands) or 0.
+ *   count:  NULL, or device int32 [1] to which the number of expanding samples
+ *           is added (not overwritten: calls over the batches of a profiling
+ *           set accumulate).
+ * The probability p_l is *count / images over the profiling set. */
+int32_t hatq_range_expansion(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
+                             float *amax, int32_t *flags, int32_t *count, void *stream);
+
+/* Form rule (Eq. layerwise_hadamard_selection): *form = HATQ_WH if
+ * p = expansions / images (correctly rounded fp64) exceeds tau, else HATQ_DH.
+ * HATQ_EINVAL for images <= 0, expansions outside [0, images] or a non-finite
+ * tau.  Host only. */
+int32_t hatq_select_form(int64_t expansions, int64_t images, double tau, int32_t *form);
+
 /* Workspace bytes of hatq_layer_forward for an input of n x h x w. */
 size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w);
 

@@ -157,6 +157,105 @@ __global__ void __launch_bounds__(kThreads) quant_kernel(const float *__restrict
     }
 }
 
+// ---- range-expansion profiling (Eq. hadamard_sensitivity) -------------------
+// One read of x gives both maxima of each sample: max |x| (into amax[k]) and
+// max |S| of the same butterfly the quantizer applies (into amax[n + k]).
+template <int B>
+__global__ void __launch_bounds__(kThreads) range_kernel(const float *__restrict__ x, int64_t E,
+                                                         float *__restrict__ amax) {
+    constexpr int R = ItemShape<B>::R;
+    constexpr int I = ItemShape<B>::I;
+    const int k = blockIdx.y;
+    const float *xs = x + (int64_t)k * E;
+    const int t = threadIdx.x & 3;
+    const int64_t items = (E + I - 1) / I;
+    float mx = 0.0f, mh = 0.0f;
+#pragma unroll 4
+    for (int64_t it = (int64_t)blockIdx.x * kQuadsPerBlock + (threadIdx.x >> 2); it < items;
+         it += (int64_t)gridDim.x * kQuadsPerBlock) {
+        float v[4 * R];
+        load_item<B>(xs, it * I, E, t, v);
+#pragma unroll
+        for (int r = 0; r < 4 * R; ++r) mx = fmaxf(mx, fabsf(v[r]));
+        fwht_item<B>(v, t);
+#pragma unroll
+        for (int r = 0; r < 4 * R; ++r) mh = fmaxf(mh, fabsf(v[r]));
+    }
+    mx = wave_max(mx);
+    mh = wave_max(mh);
+    __shared__ float red[2][kThreads / 64];
+    if ((threadIdx.x & 63) == 0) {
+        red[0][threadIdx.x >> 6] = mx;
+        red[1][threadIdx.x >> 6] = mh;
+    }
+    __syncthreads();
+    if (threadIdx.x < 2) {
+        float b = red[threadIdx.x][0];
+#pragma unroll
+        for (int w = 1; w < kThreads / 64; ++w) b = fmaxf(b, red[threadIdx.x][w]);
+        atomic_max_nonneg(amax + (threadIdx.x ? gridDim.y : 0) + k, b);
+    }
+}
+
+// Channels not a multiple of the block (or a ragged sample): one thread per
+// (pixel, block), zero channels past C, the same ascending-bit butterfly in
+// registers.
+template <int B>
+__global__ void __launch_bounds__(kThreads) range_pad_kernel(const float *__restrict__ x, int64_t P, int C,
+                                                             float *__restrict__ amax) {
+    const int k = blockIdx.y;
+    const float *xs = x + (int64_t)k * P * C;
+    const int nblk = (C + B - 1) / B;
+    float mx = 0.0f, mh = 0.0f;
+    for (int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x; u < P * nblk; u += (int64_t)gridDim.x * kThreads) {
+        const int64_t px = u / nblk;
+        const int c0 = (int)(u - px * nblk) * B;
+        float v[B];
+#pragma unroll
+        for (int j = 0; j < B; ++j) {
+            v[j] = c0 + j < C ? xs[px * C + c0 + j] : 0.0f;
+            mx = fmaxf(mx, fabsf(v[j]));
+        }
+#pragma unroll
+        for (int h = 1; h < B; h <<= 1)
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                if (j & h) continue;
+                const float a = v[j], c = v[j + h];
+                v[j] = a + c;
+                v[j + h] = a - c;
+            }
+#pragma unroll
+        for (int j = 0; j < B; ++j) mh = fmaxf(mh, fabsf(v[j]));
+    }
+    mx = wave_max(mx);
+    mh = wave_max(mh);
+    __shared__ float red[2][kThreads / 64];
+    if ((threadIdx.x & 63) == 0) {
+        red[0][threadIdx.x >> 6] = mx;
+        red[1][threadIdx.x >> 6] = mh;
+    }
+    __syncthreads();
+    if (threadIdx.x < 2) {
+        float b = red[threadIdx.x][0];
+#pragma unroll
+        for (int w = 1; w < kThreads / 64; ++w) b = fmaxf(b, red[threadIdx.x][w]);
+        atomic_max_nonneg(amax + (threadIdx.x ? gridDim.y : 0) + k, b);
+    }
+}
+
+// The indicator of each sample: max|S|^2 > b max|x|^2, exact in fp64 (the
+// orthonormal transform is S / sqrt(b)); the expanding samples are counted.
+__global__ void expansion_flags_kernel(const float *__restrict__ amax, int n, int b, int32_t *flags,
+                                       int32_t *count) {
+    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= n) return;
+    const double mx = amax[k], mh = amax[n + k];
+    const int f = mh * mh > (double)b * (mx * mx);
+    if (flags) flags[k] = f;
+    if (count && f) atomicAdd(count, 1);
+}
+
 // Elementwise path for b <= 2 when E is not a multiple of 4 (float4 alignment
 // of every sample cannot be assumed).  Element pairs never straddle a pixel
 // because c % b == 0.
@@ -239,7 +338,41 @@ hipError_t launch_scalar(const float *x, int n, int64_t E, const float *absmax_i
     return hipGetLastError();
 }
 
+template <int B>
+hipError_t launch_range_b(const float *x, int n, int64_t P, int C, float *amax, hipStream_t st) {
+    const int64_t E = P * C;
+    if (C % B == 0 && E % 4 == 0) {
+        constexpr int I = ItemShape<B>::I;
+        const int64_t items = (E + I - 1) / I;
+        range_kernel<B><<<dim3(grid_x(items, kQuadsPerBlock, n, 2048), n), kThreads, 0, st>>>(x, E, amax);
+    } else {
+        const int64_t units = P * ((C + B - 1) / B);
+        range_pad_kernel<B><<<dim3(grid_x(units, kThreads, n, 2048), n), kThreads, 0, st>>>(x, P, C, amax);
+    }
+    return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_range_expansion(const float *x, int n, int64_t P, int C, int hblock, float *amax, int32_t *flags,
+                                  int32_t *count, hipStream_t st) {
+    fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(amax), 2 * n, 0u);
+    hipError_t e;
+    switch (hblock) {
+        case 1: e = launch_range_b<1>(x, n, P, C, amax, st); break;
+        case 2: e = launch_range_b<2>(x, n, P, C, amax, st); break;
+        case 4: e = launch_range_b<4>(x, n, P, C, amax, st); break;
+        case 8: e = launch_range_b<8>(x, n, P, C, amax, st); break;
+        case 16: e = launch_range_b<16>(x, n, P, C, amax, st); break;
+        case 32: e = launch_range_b<32>(x, n, P, C, amax, st); break;
+        case 64: e = launch_range_b<64>(x, n, P, C, amax, st); break;
+        case 128: e = launch_range_b<128>(x, n, P, C, amax, st); break;
+        default: return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
+    expansion_flags_kernel<<<(n + 255) / 256, 256, 0, st>>>(amax, n, hblock, flags, count);
+    return hipGetLastError();
+}
 
 hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,
                             float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st) {

@@ -411,6 +411,25 @@ int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, i
                          static_cast<hipStream_t>(stream), nullptr, nullptr, table);
 }
 
+int32_t hatq_range_expansion(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
+                             float *amax, int32_t *flags, int32_t *count, void *stream) {
+    if (!x || !amax || n <= 0 || n > 65535 || h <= 0 || w <= 0 || c <= 0) return HATQ_EINVAL;
+    if (!is_pow2(hblock) || hblock > 128) return HATQ_EINVAL;
+    if (!aligned(x, 16) || !aligned(amax, 4)) return HATQ_EINVAL;
+    if ((flags && !aligned(flags, 4)) || (count && !aligned(count, 4))) return HATQ_EINVAL;
+    const int64_t P = (int64_t)h * w;
+    if (P * c > ((int64_t)1 << 40)) return HATQ_EINVAL;
+    return hip_status(hatq::launch_range_expansion(x, n, P, c, hblock, amax, flags, count,
+                                                   static_cast<hipStream_t>(stream)));
+}
+
+int32_t hatq_select_form(int64_t expansions, int64_t images, double tau, int32_t *form) {
+    if (!form || images <= 0 || expansions < 0 || expansions > images || !std::isfinite(tau)) return HATQ_EINVAL;
+    const double p = (double)expansions / (double)images;
+    *form = p > tau ? HATQ_WH : HATQ_DH;
+    return HATQ_OK;
+}
+
 size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w) {
     if (check_weights(W) != HATQ_OK || n <= 0 || h <= 0 || w <= 0) return 0;
     const size_t codes = (size_t)n * h * w * W->cin_pad;

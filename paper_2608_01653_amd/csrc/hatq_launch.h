@@ -11,6 +11,13 @@ namespace hatq {
 hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,
                             float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st);
 
+// Range-expansion profiling of n samples of P pixels x C channels: amax[k] =
+// max |x|, amax[n + k] = max |S| (blocks of hblock, zero-padded), then the
+// per-sample indicator into flags (or NULL) and its count added to *count (or
+// NULL).  amax is 2n floats of caller memory.
+hipError_t launch_range_expansion(const float *x, int n, int64_t P, int C, int hblock, float *amax, int32_t *flags,
+                                  int32_t *count, hipStream_t st);
+
 constexpr int kMaxTaps = 64;
 constexpr int kModeIntTransition = 3;   // ConvArgs::mode of the integer transition
 

@@ -47,7 +47,7 @@ class Weights(ctypes.Structure):
 EXPORTS = ["hatq_status_string", "hatq_conv_out_hw", "hatq_weights_bytes", "hatq_prepare_weights",
            "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act", "hatq_conv_int8",
            "hatq_conv_int8_requant", "hatq_int_table_len", "hatq_int_transition_params",
-           "hatq_conv_int8_int_transition",
+           "hatq_conv_int8_int_transition", "hatq_range_expansion", "hatq_select_form",
            "hatq_layer_ws_bytes", "hatq_layer_forward"]
 
 _lib = None
@@ -94,6 +94,10 @@ def load(build_if_missing: bool = False):
     L.hatq_int_transition_params.restype = i32
     L.hatq_conv_int8_int_transition.argtypes = [ctypes.POINTER(Weights), P, i32, i32, i32, i32, P, P, P]
     L.hatq_conv_int8_int_transition.restype = i32
+    L.hatq_range_expansion.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P]
+    L.hatq_range_expansion.restype = i32
+    L.hatq_select_form.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_double, ctypes.POINTER(i32)]
+    L.hatq_select_form.restype = i32
     L.hatq_layer_ws_bytes.argtypes = [ctypes.POINTER(Weights), i32, i32, i32]
     L.hatq_layer_ws_bytes.restype = sz
     L.hatq_layer_forward.argtypes = [ctypes.POINTER(Weights), i32, P, i32, i32, i32, P, P, P, i32, P, P,
@@ -286,6 +290,27 @@ def hatq_conv_int8_int_transition(layer: PreparedLayer, xq: torch.Tensor, next_h
                                                 _ptr(table), _ptr(yq), _stream(stream)),
            "hatq_conv_int8_int_transition")
     return yq
+
+
+def hatq_range_expansion(x: torch.Tensor, hblock: int, amax: Optional[torch.Tensor] = None,
+                         flags: Optional[torch.Tensor] = None, count: Optional[torch.Tensor] = None,
+                         stream=None):
+    """Per-sample range-expansion indicator of x (fp32 NHWC): returns (amax [2n], flags [n]).
+    count, if given, accumulates the number of expanding samples."""
+    n, h, w, c = x.shape
+    if amax is None:
+        amax = torch.empty(2 * n, dtype=torch.float32, device=x.device)
+    if flags is None:
+        flags = torch.empty(n, dtype=torch.int32, device=x.device)
+    _check(load().hatq_range_expansion(_ptr(x), n, h, w, c, int(hblock), _ptr(amax), _ptr(flags), _ptr(count),
+                                       _stream(stream)), "hatq_range_expansion")
+    return amax, flags
+
+
+def hatq_select_form(expansions: int, images: int, tau: float = 0.8) -> str:
+    f = ctypes.c_int32(-1)
+    _check(load().hatq_select_form(int(expansions), int(images), float(tau), ctypes.byref(f)), "hatq_select_form")
+    return "WH" if f.value == HATQ_WH else "DH"
 
 
 def hatq_layer_ws_bytes(layer: PreparedLayer, n: int, h: int, w: int) -> int:

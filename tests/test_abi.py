@@ -183,6 +183,30 @@ def test_int_transition_rejects_before_launch(L):
         == hatq.HATQ_EINVAL                                                                   # misaligned table
 
 
+def test_range_expansion_rejects_before_launch(L):
+    f = L.hatq_range_expansion
+    assert f(None, 1, 4, 4, 64, 64, FAKE, None, None, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 1, 4, 4, 64, 64, None, None, None, None) == hatq.HATQ_EINVAL                 # no amax
+    assert f(FAKE, 0, 4, 4, 64, 64, FAKE, None, None, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 65536, 4, 4, 64, 64, FAKE, None, None, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 1, 4, 4, 0, 64, FAKE, None, None, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 1, 4, 4, 64, 48, FAKE, None, None, None) == hatq.HATQ_EINVAL                 # not a power of two
+    assert f(FAKE, 1, 4, 4, 64, 256, FAKE, None, None, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.c_void_p(FAKE.value + 4), 1, 4, 4, 64, 64, FAKE, None, None, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 1, 4, 4, 64, 64, FAKE, ctypes.c_void_p(FAKE.value + 2), None, None) == hatq.HATQ_EINVAL
+
+
+def test_select_form_matches_oracle(L, orc):
+    out = ctypes.c_int32(-1)
+    for k, m, tau in [(800, 1000, 0.8), (801, 1000, 0.8), (0, 1, 0.8), (1, 1, 0.8), (4, 5, 0.8), (5, 6, 0.8),
+                      (3, 10, 0.3), (4, 10, 0.3), (7, 7, 1.0), (0, 3, -0.5), (2, 3, 2.0 / 3.0)]:
+        assert L.hatq_select_form(k, m, tau, ctypes.byref(out)) == hatq.HATQ_OK
+        assert ("WH" if out.value == hatq.HATQ_WH else "DH") == orc.select_form(k, m, tau), (k, m, tau)
+    for k, m, tau in [(1, 0, 0.8), (-1, 4, 0.8), (5, 4, 0.8), (1, 2, float("nan")), (1, 2, float("inf"))]:
+        assert L.hatq_select_form(k, m, tau, ctypes.byref(out)) == hatq.HATQ_EINVAL
+    assert L.hatq_select_form(1, 2, 0.8, None) == hatq.HATQ_EINVAL
+
+
 def test_layer_forward_form_flag_and_workspace(L):
     f = L.hatq_layer_forward
     W = _fake_weights()
