@@ -8,6 +8,7 @@ the per-step functions in the order the paper gives them:
 
     activation operand (DH: S = B_C x; WH: S = x)       Eq. input_hadamard_transform
     per-sample symmetric INT8 quantization               Eq. symmetric_q, Eq. current_scale
+    (or affine: scale and zero point from min / max)     Eq. uniform_q, Eq. affine_q
     INT8 x INT8 -> INT32 direct convolution              Eq. integer_accumulation
     dequant (s_x s_w,c / b), bias, WH basis restore      Eq. accumulator_scale,
                                                          Eq. supp_padded_dh, Eq. supp_padded_wh
@@ -65,7 +66,8 @@ def lib():
         L.orc_quantize_symmetric.restype = None
         L.orc_prepare_weights.argtypes = [i32, i32, i32, i32, i32, i32, P, P, P, P, P, P]
         L.orc_out_size.argtypes = [i32, i32, i32, i32, i32, i32]
-        L.orc_conv_int8.argtypes = [P, i32, i32, i32, i32, P, i32, i32, i32, i32, i32, i32, P]
+        L.orc_conv_int8.argtypes = [P, P, i32, i32, i32, i32, P, i32, i32, i32, i32, i32, i32, P]
+        L.orc_quantize_affine.argtypes = [P, i64, i64, P, P, P]
         L.orc_conv_int8.restype = None
         L.orc_conv_f64.argtypes = [P, i32, i32, i32, i32, P, i32, i32, i32, i32, i32, i32, P]
         L.orc_conv_f64.restype = None
@@ -134,6 +136,18 @@ def quantize_symmetric(S: np.ndarray, per_sample: bool = True):
     return q, s
 
 
+def quantize_affine(S: np.ndarray, per_sample: bool = True):
+    """Codes, scale(s) and zero point(s) of Eq. affine_q / Eq. uniform_q on the
+    signed grid [-128, 127]; one (s, z) per leading-axis sample."""
+    S = _c(S, np.float32)
+    nsamp = S.shape[0] if per_sample else 1
+    q = np.empty(S.shape, np.int8)
+    s = np.empty(nsamp, np.float32)
+    z = np.empty(nsamp, np.int32)
+    lib().orc_quantize_affine(_p(S), nsamp, S.size // nsamp, _p(q), _p(s), _p(z))
+    return q, s, z
+
+
 def activation_operand(x: np.ndarray, form: str, hblock: int):
     """Steps a2-a4: (S, codes, per-sample scale)."""
     S = activation_transform(x, hblock if form == "DH" else 1)
@@ -189,8 +203,9 @@ def out_size(n_in, k, stride, pad, transposed=False, out_pad=0) -> int:
     return lib().orc_out_size(n_in, k, stride, pad, int(transposed), out_pad)
 
 
-def conv_int8(xq: np.ndarray, wq: np.ndarray, *, stride, pad, transposed=False, out_pad=0):
-    """Direct INT8 conv, INT32 accumulate.  xq NHWC [n,h,w,cin_p], wq OHWI."""
+def conv_int8(xq: np.ndarray, wq: np.ndarray, *, stride, pad, transposed=False, out_pad=0, zx=None):
+    """Direct INT8 conv, INT32 accumulate.  xq NHWC [n,h,w,cin_p], wq OHWI;
+    zx: per-sample activation zero points (affine codes), or None."""
     xq = _c(xq, np.int8)
     wq = _c(wq, np.int8)
     n, h, w, cin_p = xq.shape
@@ -199,7 +214,9 @@ def conv_int8(xq: np.ndarray, wq: np.ndarray, *, stride, pad, transposed=False, 
     ho = out_size(h, k, stride, pad, transposed, out_pad)
     wo = out_size(w, k, stride, pad, transposed, out_pad)
     acc = np.empty((n, ho, wo, cout_p), np.int32)
-    lib().orc_conv_int8(_p(xq), n, h, w, cin_p, _p(wq), cout_p, k, stride, pad,
+    zxa = None if zx is None else _c(zx, np.int32)
+    assert zxa is None or zxa.shape == (n,)
+    lib().orc_conv_int8(_p(xq), _p(zxa), n, h, w, cin_p, _p(wq), cout_p, k, stride, pad,
                         int(transposed), out_pad, _p(acc))
     return acc
 

@@ -141,6 +141,44 @@ void orc_quantize_symmetric(const float *S, int64_t nsamp, int64_t per, int8_t *
     }
 }
 
+/* Affine per-sample quantizer (Eq. uniform_q, Eq. affine_q) on the signed    */
+/* 8-bit grid [q_min, q_max] = [-128, 127] (the paper's unsigned grid [0, 255]  */
+/* shifted by -128: the same dequantized values, codes that a signed INT8      */
+/* product takes).  With xmin' = min(min S, 0) and xmax' = max(max S, 0):       */
+/*   r = fl32(xmax' - xmin');  s = fl32(r / 255) (r > 0), else s = 1, z = 0;   */
+/*   z = clamp(round(q_min - xmin'/s)) = clamp(rne(fl32(-xmin' / s)) - 128)    */
+/*       (q_min is an even integer, so rounding commutes with adding it);      */
+/*   q = clamp(rne(fl32(S / s)) + z, -128, 127).                               */
+void orc_quantize_affine(const float *S, int64_t nsamp, int64_t per, int8_t *q, float *scale, int32_t *zero)
+{
+    for (int64_t n = 0; n < nsamp; ++n) {
+        const float *s_n = S + n * per;
+        float lo = 0.0f, hi = 0.0f;
+        for (int64_t i = 0; i < per; ++i) {
+            if (s_n[i] < lo) lo = s_n[i];
+            if (s_n[i] > hi) hi = s_n[i];
+        }
+        const float r = hi - lo;
+        float s = 1.0f;
+        int z = 0;
+        if (r > 0.0f) {
+            s = r / 255.0f;
+            z = (int)nearbyintf(-lo / s) - 128;
+            if (z < -128) z = -128;
+            if (z > 127) z = 127;
+        }
+        scale[n] = s;
+        zero[n] = z;
+        #pragma omp parallel for schedule(static)
+        for (int64_t i = 0; i < per; ++i) {
+            float t = nearbyintf(s_n[i] / s) + (float)z;
+            if (t > 127.0f) t = 127.0f;
+            if (t < -128.0f) t = -128.0f;
+            q[n * per + i] = (int8_t)t;
+        }
+    }
+}
+
 /* ------------------------------------------------------------------------- */
 /* O2. Weight preparation (offline).                                          */
 /* Input: PyTorch layout, OIHW [cout][cin][k][k] for a convolution, IOHW      */
@@ -267,7 +305,10 @@ static int src_index(int o, int i, int in, int stride, int pad, int transposed)
 /* xq: [n][h][w][cin_p] int8, wq: [cout_p][k][k][cin_p] int8 (OHWI),          */
 /* acc: [n][ho][wo][cout_p] int32.  Out-of-range taps contribute 0.           */
 /* ------------------------------------------------------------------------- */
-void orc_conv_int8(const int8_t *xq, int n, int h, int w, int cin_p,
+/* zx: NULL, or one activation zero point per sample: the sum then runs over */
+/* the centered codes x - z_x (Eq. integer_accumulation with z_w = 0), and    */
+/* input pixels outside the image contribute nothing (the value zero).        */
+void orc_conv_int8(const int8_t *xq, const int32_t *zx, int n, int h, int w, int cin_p,
                    const int8_t *wq, int cout_p, int k, int stride, int pad,
                    int transposed, int out_pad, int32_t *acc)
 {
@@ -278,6 +319,7 @@ void orc_conv_int8(const int8_t *xq, int n, int h, int w, int cin_p,
         for (int oh = 0; oh < ho; ++oh)
             for (int ow = 0; ow < wo; ++ow)
                 for (int co = 0; co < cout_p; ++co) {
+                    const int32_t z = zx ? zx[b] : 0;
                     int32_t a = 0;
                     for (int kh = 0; kh < k; ++kh) {
                         const int ih = src_index(oh, kh, h, stride, pad, transposed);
@@ -288,7 +330,7 @@ void orc_conv_int8(const int8_t *xq, int n, int h, int w, int cin_p,
                             const int8_t *xp = xq + (((int64_t)b * h + ih) * w + iw) * cin_p;
                             const int8_t *wp = wq + (((int64_t)co * k + kh) * k + kw) * cin_p;
                             for (int ci = 0; ci < cin_p; ++ci)
-                                a += (int32_t)xp[ci] * (int32_t)wp[ci];
+                                a += ((int32_t)xp[ci] - z) * (int32_t)wp[ci];
                         }
                     }
                     acc[(((int64_t)b * ho + oh) * wo + ow) * cout_p + co] = a;
