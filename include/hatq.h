@@ -204,6 +204,42 @@ int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const fl
                                const float *next_absmax, float *next_scale, int8_t *yq,
                                void *stream);
 
+/* Affine activation quantization (Eq. affine_q, Eq. uniform_q), the dynamic
+ * per-sample form of the paper's PTQ setting, on the signed grid [-128, 127]
+ * (the paper's unsigned grid shifted by -128: the same dequantized values, codes
+ * that the signed INT8 product takes).  For S = the activation transform of
+ * each sample (as hatq_fwht_quant_act): with lo = max(-min S, 0), hi = max(max
+ * S, 0), r = fl32(hi + lo):
+ *   s = fl32(r / 255), z = clamp(rne(fl32(lo / s)) - 128, -128, 127); r = 0 gives
+ *   s = 1, z = 0;  xq = clamp(rne(fl32(S / s)) + z, -128, 127).
+ *   act_scale, act_zero: device fp32 / int32 [n], written.
+ *   ws: device workspace of hatq_fwht_quant_affine_ws_bytes(n) bytes.
+ * Supported: c % hblock == 0, h*w*c % 4 == 0, n <= 65535. */
+size_t hatq_fwht_quant_affine_ws_bytes(int32_t n);
+int32_t hatq_fwht_quant_act_affine(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
+                                   int8_t *xq, float *act_scale, int32_t *act_zero, void *ws, size_t ws_bytes,
+                                   void *stream);
+
+/* Weight sums for the zero-point correction: tapsum[t][c] = sum over ci of the
+ * code W_q[c][t][ci] for each tap t < k*k, then tapsum[k*k][c] = their total.
+ * hatq_tapsum_len gives the int32 entries ((k*k + 1) * cout_pad, 0 for invalid
+ * weights); tapsum is device memory, 16-byte aligned, written on the stream. */
+size_t hatq_tapsum_len(const hatq_weights *W);
+int32_t hatq_weight_tapsums(const hatq_weights *W, int32_t *tapsum, void *stream);
+
+/* INT8 convolution of affine codes (Eq. integer_accumulation with zero points
+ * z_x per sample and z_w = 0): the accumulator is the sum of (x - z_x) w over
+ * the input pixels inside the image (padding is the value zero), formed as the
+ * sum of x w minus z_x times the weight sum of the pixel's inside taps; then
+ * the same output modes as hatq_conv_int8 (HATQ_OUT_I32: these centered
+ * accumulators; HATQ_OUT_F32: the same epilogue with s_x = act_scale).
+ *   act_zero: device int32 [n] (from hatq_fwht_quant_act_affine).
+ *   tapsum:   from hatq_weight_tapsums for W.
+ * Supported: as hatq_conv_int8 (no next-operand absmax). */
+int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const float *act_scale,
+                              const int32_t *act_zero, const int32_t *tapsum, int32_t n, int32_t h, int32_t w,
+                              int32_t out_mode, void *y, void *stream);
+
 /* Integer-only transition (Eq. integer_accumulation, Eq.
  * integer_fixed_point_scale, Eq. integer_hadamard_transition, the integer
  * column of Table I) with static per-tensor scales: the layer's INT32

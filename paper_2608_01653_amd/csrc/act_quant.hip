@@ -157,6 +157,104 @@ __global__ void __launch_bounds__(kThreads) quant_kernel(const float *__restrict
     }
 }
 
+// ---- affine quantization (Eq. affine_q, Eq. uniform_q) ----------------------
+// Signed grid [-128, 127].  amax[k] = max(max S, 0), amax[n + k] = max(-min S, 0)
+// (both non-negative, so the order-preserving atomic serves both).
+template <int B>
+__global__ void __launch_bounds__(kThreads) minmax_kernel(const float *__restrict__ x, int64_t E,
+                                                          float *__restrict__ amax) {
+    constexpr int R = ItemShape<B>::R;
+    constexpr int I = ItemShape<B>::I;
+    const int k = blockIdx.y;
+    const float *xs = x + (int64_t)k * E;
+    const int t = threadIdx.x & 3;
+    const int64_t items = (E + I - 1) / I;
+    float hi = 0.0f, lo = 0.0f;   // max(S, 0) and max(-S, 0)
+#pragma unroll 4
+    for (int64_t it = (int64_t)blockIdx.x * kQuadsPerBlock + (threadIdx.x >> 2); it < items;
+         it += (int64_t)gridDim.x * kQuadsPerBlock) {
+        float v[4 * R];
+        load_item<B>(xs, it * I, E, t, v);
+        const float sigma = fwht_item<B>(v, t);
+#pragma unroll
+        for (int r = 0; r < 4 * R; ++r) {
+            const float sv = sigma * v[r];
+            hi = fmaxf(hi, sv);
+            lo = fmaxf(lo, -sv);
+        }
+    }
+    hi = wave_max(hi);
+    lo = wave_max(lo);
+    __shared__ float red[2][kThreads / 64];
+    if ((threadIdx.x & 63) == 0) {
+        red[0][threadIdx.x >> 6] = hi;
+        red[1][threadIdx.x >> 6] = lo;
+    }
+    __syncthreads();
+    if (threadIdx.x < 2) {
+        float b = red[threadIdx.x][0];
+#pragma unroll
+        for (int w = 1; w < kThreads / 64; ++w) b = fmaxf(b, red[threadIdx.x][w]);
+        atomic_max_nonneg(amax + (threadIdx.x ? gridDim.y : 0) + k, b);
+    }
+}
+
+// s = fl32(fl32(hi + lo) / 255) and z = clamp(rne(fl32(lo / s)) - 128) for a
+// nonzero range (hi + lo = xmax' - xmin'), else s = 1, z = 0.
+__device__ __forceinline__ void affine_params(float hi, float lo, float &s, int &z) {
+    const float r = hi + lo;
+    s = 1.0f;
+    z = 0;
+    if (r > 0.0f) {
+        s = r / 255.0f;
+        z = (int)rintf(lo / s) - 128;
+        z = z < -128 ? -128 : (z > 127 ? 127 : z);
+    }
+}
+
+// Codes q = clamp(rne(fl32(S / s)) + z, -128, 127), IEEE division per element.
+template <int B>
+__global__ void __launch_bounds__(kThreads) quant_affine_kernel(const float *__restrict__ x, int64_t E,
+                                                                const float *__restrict__ amax,
+                                                                int8_t *__restrict__ xq, float *__restrict__ act_scale,
+                                                                int32_t *__restrict__ act_zero) {
+    constexpr int I = ItemShape<B>::I;
+    constexpr int R = ItemShape<B>::R;
+    const int k = blockIdx.y;
+    const float *xs = x + (int64_t)k * E;
+    int8_t *qs = xq + (int64_t)k * E;
+    const int t = threadIdx.x & 3;
+    float s;
+    int z;
+    affine_params(amax[k], amax[gridDim.y + k], s, z);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        act_scale[k] = s;
+        act_zero[k] = z;
+    }
+    const float zf = (float)z;
+    const int64_t items = (E + I - 1) / I;
+    for (int64_t it = (int64_t)blockIdx.x * kQuadsPerBlock + (threadIdx.x >> 2); it < items;
+         it += (int64_t)gridDim.x * kQuadsPerBlock) {
+        float v[4 * R];
+        load_item<B>(xs, it * I, E, t, v);
+        const float sigma = fwht_item<B>(v, t);
+        uint32_t u[4 * R];
+#pragma unroll
+        for (int r = 0; r < 4 * R; ++r) {
+            const float q = __builtin_amdgcn_fmed3f(rintf((sigma * v[r]) / s) + zf, -128.0f, 127.0f);
+            u[r] = (uint32_t)(int32_t)q;
+        }
+        const int64_t base = it * I;
+        const bool full = base + I <= E;
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const int64_t off = base + 16 * i + 4 * t;
+            if (full || off < E)
+                *reinterpret_cast<uint32_t *>(qs + off) = pack_low_bytes(u[4 * i], u[4 * i + 1], u[4 * i + 2], u[4 * i + 3]);
+        }
+    }
+}
+
 // ---- range-expansion profiling (Eq. hadamard_sensitivity) -------------------
 // One read of x gives both maxima of each sample: max |x| (into amax[k]) and
 // max |S| of the same butterfly the quantizer applies (into amax[n + k]).
@@ -352,7 +450,35 @@ hipError_t launch_range_b(const float *x, int n, int64_t P, int C, float *amax, 
     return hipGetLastError();
 }
 
+template <int B>
+hipError_t launch_affine_b(const float *x, int n, int64_t E, float *ws, int8_t *xq, float *act_scale,
+                           int32_t *act_zero, hipStream_t st) {
+    constexpr int I = ItemShape<B>::I;
+    const int64_t items = (E + I - 1) / I;
+    fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(ws), 2 * n, 0u);
+    minmax_kernel<B><<<dim3(grid_x(items, kQuadsPerBlock, n, 2048), n), kThreads, 0, st>>>(x, E, ws);
+    quant_affine_kernel<B><<<dim3(grid_x(items, kQuadsPerBlock, n), n), kThreads, 0, st>>>(x, E, ws, xq, act_scale,
+                                                                                          act_zero);
+    return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_act_quant_affine(const float *x, int n, int64_t E, int hblock, float *ws, int8_t *xq,
+                                   float *act_scale, int32_t *act_zero, hipStream_t st) {
+    if (E % 4 != 0) return hipErrorInvalidValue;
+    switch (hblock) {
+        case 1: return launch_affine_b<1>(x, n, E, ws, xq, act_scale, act_zero, st);
+        case 2: return launch_affine_b<2>(x, n, E, ws, xq, act_scale, act_zero, st);
+        case 4: return launch_affine_b<4>(x, n, E, ws, xq, act_scale, act_zero, st);
+        case 8: return launch_affine_b<8>(x, n, E, ws, xq, act_scale, act_zero, st);
+        case 16: return launch_affine_b<16>(x, n, E, ws, xq, act_scale, act_zero, st);
+        case 32: return launch_affine_b<32>(x, n, E, ws, xq, act_scale, act_zero, st);
+        case 64: return launch_affine_b<64>(x, n, E, ws, xq, act_scale, act_zero, st);
+        case 128: return launch_affine_b<128>(x, n, E, ws, xq, act_scale, act_zero, st);
+        default: return hipErrorInvalidValue;
+    }
+}
 
 hipError_t launch_range_expansion(const float *x, int n, int64_t P, int C, int hblock, float *amax, int32_t *flags,
                                   int32_t *count, hipStream_t st) {

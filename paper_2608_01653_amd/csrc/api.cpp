@@ -123,7 +123,8 @@ int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next
 int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, int32_t n,
                       int32_t h, int32_t w, int32_t mode, void *y, int32_t next_hblock,
                       float *next_absmax, hipStream_t st, const float *q_absmax = nullptr,
-                      float *q_scale = nullptr, const int32_t *rq_table = nullptr) {
+                      float *q_scale = nullptr, const int32_t *rq_table = nullptr,
+                      const int32_t *zx = nullptr, const int32_t *tapsum = nullptr) {
     const hatq_conv_desc &d = W->d;
     int32_t ho, wo;
     if (out_hw(&d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
@@ -139,6 +140,8 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
     a.q_absmax = q_absmax;
     a.q_scale = q_scale;
     a.rq_table = rq_table;
+    a.zx = zx;
+    a.tapsum = tapsum;
     a.n = n;
     a.h = h;
     a.w = w;
@@ -360,6 +363,60 @@ int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const fl
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
     return conv_launches(W, xq, act_scale, n, h, w, HATQ_OUT_I8, yq, next_hblock, nullptr,
                          static_cast<hipStream_t>(stream), next_absmax, next_scale);
+}
+
+size_t hatq_fwht_quant_affine_ws_bytes(int32_t n) { return n > 0 ? align256((size_t)n * 8) : 0; }
+
+int32_t hatq_fwht_quant_act_affine(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
+                                   int8_t *xq, float *act_scale, int32_t *act_zero, void *ws, size_t ws_bytes,
+                                   void *stream) {
+    if (!x || !xq || !act_scale || !act_zero || !ws || n <= 0 || n > 65535 || h <= 0 || w <= 0 || c <= 0)
+        return HATQ_EINVAL;
+    if (!is_pow2(hblock) || hblock > 128) return HATQ_EINVAL;
+    if (!aligned(x, 16) || !aligned(xq, 4) || !aligned(act_scale, 4) || !aligned(act_zero, 4) || !aligned(ws, 4))
+        return HATQ_EINVAL;
+    if (ws_bytes < (size_t)n * 8) return HATQ_EWORKSPACE;
+    const int64_t E = (int64_t)h * w * c;
+    if (c % hblock != 0 || E % 4 != 0 || E > ((int64_t)1 << 40)) return HATQ_EUNSUPPORTED;
+    return hip_status(hatq::launch_act_quant_affine(x, n, E, hblock, static_cast<float *>(ws), xq, act_scale,
+                                                    act_zero, static_cast<hipStream_t>(stream)));
+}
+
+size_t hatq_tapsum_len(const hatq_weights *W) {
+    if (check_weights(W) != HATQ_OK) return 0;
+    return ((size_t)W->d.k * W->d.k + 1) * W->cout_pad;
+}
+
+int32_t hatq_weight_tapsums(const hatq_weights *W, int32_t *tapsum, void *stream) {
+    int32_t s = check_weights(W);
+    if (s != HATQ_OK) return s;
+    if (!tapsum || !aligned(tapsum, 16)) return HATQ_EINVAL;
+    hatq::PrepArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.wq = W->wq;
+    a.k = W->d.k;
+    a.cin_p = W->cin_pad;
+    a.cout_p = W->cout_pad;
+    a.k_total = W->k_total;
+    a.k_stride = W->k_stride;
+    return hip_status(hatq::launch_tapsums(a, tapsum, static_cast<hipStream_t>(stream)));
+}
+
+int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const float *act_scale,
+                              const int32_t *act_zero, const int32_t *tapsum, int32_t n, int32_t h, int32_t w,
+                              int32_t out_mode, void *y, void *stream) {
+    int32_t s = check_weights(W);
+    if (s != HATQ_OK) return s;
+    if (!xq || !act_scale || !act_zero || !tapsum || !y || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
+    if (out_mode != HATQ_OUT_I32 && out_mode != HATQ_OUT_F32) return HATQ_EINVAL;
+    if (!aligned(xq, 16) || !aligned(y, 16) || !aligned(act_scale, 4) || !aligned(act_zero, 4) ||
+        !aligned(tapsum, 16))
+        return HATQ_EINVAL;
+    if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    int32_t ho, wo;
+    if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
+    return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, 0, nullptr, static_cast<hipStream_t>(stream),
+                         nullptr, nullptr, nullptr, act_zero, tapsum);
 }
 
 size_t hatq_int_table_len(const hatq_weights *W) {

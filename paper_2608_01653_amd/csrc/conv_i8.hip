@@ -241,20 +241,23 @@ __device__ __forceinline__ uint32_t int_code_hi(int64_t w, int s, int64_t bias_m
 // fp32 output; WB = NB = -1 is the generic body, which takes the output mode,
 // form and block sizes from the arguments.
 // Q = 1: I8 output (the next operand's codes, NB its transform block); Q = 2:
-// the same codes by the integer transition (mode 3).
+// the same codes by the integer transition (mode 3); Q = 3 (generic only):
+// I32 / F32 output from affine activation codes.
 template <int WB_, int NB_, int Q_ = 0>
 struct Epi {
     static constexpr int WB = WB_, NB = NB_, Q = Q_;
 };
 using EpiGeneric = Epi<-1, -1>;
 using EpiGenericInt = Epi<-1, -1, 2>;   // the integer transition, blocks at run time
+using EpiGenericAffine = Epi<-1, -1, 3>;   // affine activations: zero-point correction
 
 // The variant a launch needs, or the generic one.
 template <typename E>
 bool epi_matches(const ConvArgs &a) {
     if constexpr (E::WB == -1) {
-        return (a.mode == kModeIntTransition) == (E::Q == 2);
+        return (a.mode == kModeIntTransition) == (E::Q == 2) && (a.zx != nullptr) == (E::Q == 3);
     } else {
+        if (a.zx) return false;
         const int wb = a.form == 1 ? a.hblock : 0;
         if (E::Q) return a.mode == (E::Q == 2 ? kModeIntTransition : 2) && wb == E::WB && a.next_hblock == E::NB;
         const int nb = a.next_absmax != nullptr ? a.next_hblock : 0;
@@ -267,8 +270,9 @@ template <typename E>
 struct EpiFlags {
     static constexpr int WB = E::WB, NB = E::NB;
     static constexpr bool generic = WB == -1;
-    bool f32, wh, want_abs, i8, iq, store;
+    bool f32, wh, want_abs, i8, iq, affine, store;
     __device__ explicit EpiFlags(const ConvArgs &a) {
+        affine = E::Q == 3;
         iq = E::Q == 2;   // integer transition (its own variants, generic ones included)
         f32 = !iq && (generic ? a.mode != 0 : true);   // the fp32 arithmetic (F32 and I8 modes)
         wh = generic ? a.mode != 0 && a.form == 1 : WB != 0;
@@ -349,9 +353,9 @@ struct Epilogue {
     const EpiFlags<E> fl;
     bool full, z_bound, q_fast;
     float wave_m, seen, qs, qr;
-    int nbk, rq_n, rq_pre;
+    int nbk, rq_n, rq_pre, zp;
     int64_t rq_bias;
-    bool rq_pair, valid[FM];
+    bool rq_pair, valid[FM], border[FM];
 
     __device__ __forceinline__ Epilogue(const ConvArgs &a_, const Tile &t_, int row0_, int lane_, const float *col_t_,
                                         const float *col_b_)
@@ -413,6 +417,59 @@ struct Epilogue {
             const int m = row0 + 16 * i + p;
             valid[i] = t.gi0 + m / TW < a.gh && t.gj0 + m % TW < a.gw;
         }
+        // Affine activations: the sample's zero point, and per row group whether
+        // any lane's pixel has a tap outside the image (wave-uniform).
+        zp = 0;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) border[i] = false;
+        if (fl.affine) {
+            zp = a.zx[t.nb];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int m = row0 + 16 * i + p;
+                const int ih0 = (t.gi0 + m / TW) * a.sa + a.bah, iw0 = (t.gj0 + m % TW) * a.sa + a.baw;
+                bool out = false;
+                for (int tp = 0; tp < a.ntaps; ++tp) {
+                    const int ih = ih0 + a.dh[tp], iw = iw0 + a.dw[tp];
+                    out |= ih < 0 || ih >= a.h || iw < 0 || iw >= a.w;
+                }
+                border[i] = __builtin_amdgcn_ballot_w64(valid[i] && out) != 0;
+            }
+        }
+    }
+
+    // Affine activations: codes outside the image read as 0, which stands for
+    // the value -z s, so the centered sum is acc - z T(p, c), T the weight sum
+    // over the launch's taps of pixel p that fall inside the image.  A launch
+    // with every tap (regular convolution) starts from the total and removes
+    // the outside taps of border pixels; a transposed phase adds its inside taps.
+    __device__ __forceinline__ void zero_point_fix(v4i (&cc)[4], int i, int k) const {
+        const int cl0 = t.n0 + 64 * k + 4 * q;
+        const bool all_taps = a.ntaps == a.k * a.k;
+        v4i T[4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) T[jj] = v4i{0, 0, 0, 0};
+        if (all_taps) {
+            const int32_t *full = a.tapsum + (int64_t)a.k * a.k * a.cout_pad + cl0;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) T[jj] = *reinterpret_cast<const v4i *>(full + 16 * jj);
+        }
+        if (border[i] || !all_taps) {
+            const int m = row0 + 16 * i + p;
+            const int ih0 = (t.gi0 + m / TW) * a.sa + a.bah, iw0 = (t.gj0 + m % TW) * a.sa + a.baw;
+            for (int tp = 0; tp < a.ntaps; ++tp) {
+                const int ih = ih0 + a.dh[tp], iw = iw0 + a.dw[tp];
+                const bool inside = ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+                if (inside != all_taps) {
+                    const int32_t *row = a.tapsum + (int64_t)a.wtap[tp] * a.cout_pad + cl0;
+                    const int sg = all_taps ? -1 : 1;
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj) T[jj] += sg * *reinterpret_cast<const v4i *>(row + 16 * jj);
+                }
+            }
+        }
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) cc[jj] -= zp * T[jj];
     }
 
     // Integer transition of block k: p = M (.) (acc + b_int) in int64, the WH
@@ -488,9 +545,13 @@ struct Epilogue {
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
             float v[16];
+            v4i cc[4];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) cc[jj] = acc[i][4 * k + jj];
+            if (fl.affine) zero_point_fix(cc, i, k);
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
-                const v4i c4 = acc[i][4 * k + jj];
+                const v4i c4 = cc[jj];
                 if (!f32) {
 #pragma unroll
                     for (int r = 0; r < 4; ++r) v[4 * jj + r] = __int_as_float(c4[r]);
@@ -990,7 +1051,7 @@ hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
 
 // Variants compiled for the layer shapes of the analysis transforms: DH or WH
 // blocks of 64, next operand blocked by 64 (DH next), 1 (WH next) or none.
-#define HATQ_GENERIC_EPILOGUES EpiGenericInt, EpiGeneric
+#define HATQ_GENERIC_EPILOGUES EpiGenericInt, EpiGenericAffine, EpiGeneric
 #define HATQ_HOT_EPILOGUES \
     Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_GENERIC_EPILOGUES
 
@@ -1736,6 +1797,7 @@ ConvArgs sample_group(const ConvArgs &a, int64_t s0, int gn) {
     if (a.next_absmax) b.next_absmax = a.next_absmax + s0;
     if (a.q_absmax) b.q_absmax = a.q_absmax + s0;
     if (a.q_scale) b.q_scale = a.q_scale + s0;
+    if (a.zx) b.zx = a.zx + s0;
     b.M = (int64_t)gn * a.gh * a.gw;
     return b;
 }

@@ -11,6 +11,12 @@ namespace hatq {
 hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,
                             float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st);
 
+// Affine activation quantization (signed grid [-128, 127]) of n samples of E
+// floats each (E % 4 == 0, the channel count a multiple of hblock): ws holds 2n
+// floats (per-sample max(S, 0), then max(-S, 0)); per-sample scale and zero point out.
+hipError_t launch_act_quant_affine(const float *x, int n, int64_t E, int hblock, float *ws, int8_t *xq,
+                                   float *act_scale, int32_t *act_zero, hipStream_t st);
+
 // Range-expansion profiling of n samples of P pixels x C channels: amax[k] =
 // max |x|, amax[n + k] = max |S| (blocks of hblock, zero-padded), then the
 // per-sample indicator into flags (or NULL) and its count added to *count (or
@@ -36,6 +42,8 @@ struct ConvArgs {
     const float *q_absmax; // I8 mode: per-sample max |B_next y| giving the scale, or NULL
     float *q_scale;        // I8 mode: per-sample scale (written from q_absmax, else read)
     const int32_t *rq_table;   // mode 3: M [cout_pad], b_int [cout_pad], shift n
+    const int32_t *zx;         // affine activations (modes 0, 1): per-sample zero point, or NULL
+    const int32_t *tapsum;     // with zx: weight sums [k*k + 1][cout_pad] (per tap, then all taps)
     int64_t M;             // n * gh * gw
     int32_t n, h, w, cin_p;
     int32_t gh, gw;
@@ -73,6 +81,9 @@ struct PrepArgs {
 hipError_t launch_prepare(const PrepArgs &a, hipStream_t st);
 // Rebuild wpack from wq (geometry fields, wq and wpack are used).
 hipError_t launch_pack(const PrepArgs &a, hipStream_t st);
+// Per-tap weight sums of the codes: tapsum[t][c] = sum_ci wq[c][t*cin_p + ci] for
+// t < k*k, and tapsum[k*k][c] = sum over all taps (geometry fields and wq used).
+hipError_t launch_tapsums(const PrepArgs &a, int32_t *tapsum, hipStream_t st);
 
 // Fixed-point parameters of the integer transition from static scales.
 struct IntParamArgs {

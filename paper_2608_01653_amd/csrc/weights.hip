@@ -152,7 +152,28 @@ __global__ void __launch_bounds__(kThreads) int_params_kernel(const IntParamArgs
     if (tid == 0) a.table[2 * a.cout_p] = n;
 }
 
+// One thread per output channel: the per-tap sums, then their total.
+__global__ void __launch_bounds__(kThreads) tapsum_kernel(const PrepArgs a, int32_t *tapsum) {
+    const int c = blockIdx.x * kThreads + threadIdx.x;
+    if (c >= a.cout_p) return;
+    const int taps = a.k * a.k;
+    const int8_t *row = a.wq + (int64_t)c * a.k_stride;
+    int32_t all = 0;
+    for (int t = 0; t < taps; ++t) {
+        int32_t sum = 0;
+        for (int ci = 0; ci < a.cin_p; ++ci) sum += row[t * a.cin_p + ci];
+        tapsum[(int64_t)t * a.cout_p + c] = sum;
+        all += sum;
+    }
+    tapsum[(int64_t)taps * a.cout_p + c] = all;
+}
+
 }  // namespace
+
+hipError_t launch_tapsums(const PrepArgs &a, int32_t *tapsum, hipStream_t st) {
+    tapsum_kernel<<<(a.cout_p + kThreads - 1) / kThreads, kThreads, 0, st>>>(a, tapsum);
+    return hipGetLastError();
+}
 
 hipError_t launch_int_params(const IntParamArgs &a, hipStream_t st) {
     int_params_kernel<<<1, kThreads, 0, st>>>(a);

@@ -48,6 +48,8 @@ EXPORTS = ["hatq_status_string", "hatq_conv_out_hw", "hatq_weights_bytes", "hatq
            "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act", "hatq_conv_int8",
            "hatq_conv_int8_requant", "hatq_int_table_len", "hatq_int_transition_params",
            "hatq_conv_int8_int_transition", "hatq_range_expansion", "hatq_select_form",
+           "hatq_fwht_quant_affine_ws_bytes", "hatq_fwht_quant_act_affine", "hatq_tapsum_len",
+           "hatq_weight_tapsums", "hatq_conv_int8_affine",
            "hatq_layer_ws_bytes", "hatq_layer_forward"]
 
 _lib = None
@@ -95,6 +97,16 @@ def load(build_if_missing: bool = False):
     L.hatq_conv_int8_int_transition.argtypes = [ctypes.POINTER(Weights), P, i32, i32, i32, i32, P, P, P]
     L.hatq_conv_int8_int_transition.restype = i32
     L.hatq_range_expansion.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P]
+    L.hatq_fwht_quant_affine_ws_bytes.argtypes = [i32]
+    L.hatq_fwht_quant_affine_ws_bytes.restype = sz
+    L.hatq_fwht_quant_act_affine.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P, sz, P]
+    L.hatq_fwht_quant_act_affine.restype = i32
+    L.hatq_tapsum_len.argtypes = [ctypes.POINTER(Weights)]
+    L.hatq_tapsum_len.restype = sz
+    L.hatq_weight_tapsums.argtypes = [ctypes.POINTER(Weights), P, P]
+    L.hatq_weight_tapsums.restype = i32
+    L.hatq_conv_int8_affine.argtypes = [ctypes.POINTER(Weights), P, P, P, P, i32, i32, i32, i32, P, P]
+    L.hatq_conv_int8_affine.restype = i32
     L.hatq_range_expansion.restype = i32
     L.hatq_select_form.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_double, ctypes.POINTER(i32)]
     L.hatq_select_form.restype = i32
@@ -290,6 +302,46 @@ def hatq_conv_int8_int_transition(layer: PreparedLayer, xq: torch.Tensor, next_h
                                                 _ptr(table), _ptr(yq), _stream(stream)),
            "hatq_conv_int8_int_transition")
     return yq
+
+
+def hatq_fwht_quant_act_affine(x: torch.Tensor, hblock: int, xq: Optional[torch.Tensor] = None,
+                               scale: Optional[torch.Tensor] = None, zero: Optional[torch.Tensor] = None,
+                               ws: Optional[torch.Tensor] = None, stream=None):
+    """x fp32 NHWC -> (int8 codes, per-sample scale fp32 [n], zero point int32 [n])."""
+    n, h, w, c = x.shape
+    if xq is None:
+        xq = torch.empty((n, h, w, c), dtype=torch.int8, device=x.device)
+    if scale is None:
+        scale = torch.empty(n, dtype=torch.float32, device=x.device)
+    if zero is None:
+        zero = torch.empty(n, dtype=torch.int32, device=x.device)
+    if ws is None:
+        ws = torch.empty(int(load().hatq_fwht_quant_affine_ws_bytes(n)), dtype=torch.int8, device=x.device)
+    _check(load().hatq_fwht_quant_act_affine(_ptr(x), n, h, w, c, int(hblock), _ptr(xq), _ptr(scale), _ptr(zero),
+                                             _ptr(ws), ws.numel(), _stream(stream)), "hatq_fwht_quant_act_affine")
+    return xq, scale, zero
+
+
+def hatq_weight_tapsums(layer: PreparedLayer, tapsum: Optional[torch.Tensor] = None, device="cuda", stream=None):
+    if tapsum is None:
+        tapsum = torch.empty(int(load().hatq_tapsum_len(ctypes.byref(layer.w))), dtype=torch.int32, device=device)
+    _check(load().hatq_weight_tapsums(ctypes.byref(layer.w), _ptr(tapsum), _stream(stream)), "hatq_weight_tapsums")
+    return tapsum
+
+
+def hatq_conv_int8_affine(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tensor, act_zero: torch.Tensor,
+                          tapsum: torch.Tensor, out_mode=HATQ_OUT_F32, y=None, stream=None) -> torch.Tensor:
+    n, h, w, _ = xq.shape
+    ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
+    if y is None:
+        if out_mode == HATQ_OUT_I32:
+            y = torch.empty((n, ho, wo, layer.w.cout_pad), dtype=torch.int32, device=xq.device)
+        else:
+            y = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.float32, device=xq.device)
+    _check(load().hatq_conv_int8_affine(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), _ptr(act_zero),
+                                        _ptr(tapsum), n, h, w, int(out_mode), _ptr(y), _stream(stream)),
+           "hatq_conv_int8_affine")
+    return y
 
 
 def hatq_range_expansion(x: torch.Tensor, hblock: int, amax: Optional[torch.Tensor] = None,
