@@ -208,6 +208,59 @@ def measure_form_selection(args, wl, layers, x0, xq, sc, ys, tau=0.8):
                     "not the paper's trained-model assignment"}
 
 
+def measure_affine_layer(args, wl, layers, xq, ys, per_layer, li=2):
+    """Layer 3 with affine dynamic activations (the paper's PTQ setting): the
+    min / max pass and the affine quantization of its fp32 input, then the
+    convolution with the zero-point correction, F32 output.  Timed on its own
+    after the step, beside the symmetric layer's figures from the step."""
+    import torch
+    from paper_2608_01653_amd import hatq, workloads
+    L = wl.layers[li]
+    x = ys[li - 1]
+    n = x.shape[0]
+    dev = x.device
+    hb = L.hblock if L.form == "DH" else 1
+    scale = torch.empty(n, dtype=torch.float32, device=dev)
+    zero = torch.empty(n, dtype=torch.int32, device=dev)
+    ws = torch.empty(int(hatq.load().hatq_fwht_quant_affine_ws_bytes(n)), dtype=torch.int8, device=dev)
+    tapsum = hatq.hatq_weight_tapsums(layers[li], device=dev)
+
+    def run(events=None):
+        if events:
+            events[0].record()
+        hatq.hatq_fwht_quant_act_affine(x, hb, xq=xq[li], scale=scale, zero=zero, ws=ws)
+        if events:
+            events[1].record()
+        hatq.hatq_conv_int8_affine(layers[li], xq[li], scale, zero, tapsum, hatq.HATQ_OUT_F32, y=ys[li])
+        if events:
+            events[2].record()
+
+    for _ in range(args.warmup):
+        run()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for k in range(args.steps):
+        run(ev[k])
+    torch.cuda.synchronize()
+    tq = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps * 1e3
+    tc = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps * 1e3
+    ops = workloads.conv_ops(wl, li)
+    elems = x.numel()
+    z = zero.cpu().tolist()
+    log(f"affine layer {li + 1}: quant {tq:.1f} us, conv {tc:.1f} us")
+    return {"layer": per_layer[li]["layer"],
+            "act_quant_affine_us": round(tq, 2),
+            "act_quant_affine_gbs_alg": round(elems * 5 / (tq * 1e-6) / 1e9, 1),
+            "act_quant_affine_passes": 2,
+            "conv_affine_us": round(tc, 2),
+            "conv_affine_tops": round(ops / (tc * 1e-6) / 1e12, 1),
+            "symmetric_act_quant_us": per_layer[li]["act_quant_us"],
+            "symmetric_conv_us": per_layer[li]["conv_us"],
+            "zero_points": [min(z), max(z)],
+            "note": "dynamic per-sample affine activations (min/max pass + quantization), "
+                    "zero-point correction in the conv epilogue"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -367,6 +420,7 @@ def main():
 
     integer_stack = measure_integer_stack(args, wl, layers, x0, xq, sc, ys, ws, act_hb, total_ops, img_pix)
     form_selection = measure_form_selection(args, wl, layers, x0, xq, sc, ys)
+    affine = measure_affine_layer(args, wl, layers, xq, ys, per_layer)
 
     out = {
         "metric": "Hadamard-INT8 conv TOPS + Mpixel/s per layer; % of INT8 MFMA / HBM peak",
@@ -387,6 +441,7 @@ def main():
         "roofline_act_quant": roof_q,
         "integer_stack": integer_stack,
         "form_selection": form_selection,
+        "affine_layer": affine,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, x_np, params)

@@ -207,6 +207,30 @@ def test_select_form_matches_oracle(L, orc):
     assert L.hatq_select_form(1, 2, 0.8, None) == hatq.HATQ_EINVAL
 
 
+def test_affine_rejects_before_launch(L):
+    q = L.hatq_fwht_quant_act_affine
+    assert L.hatq_fwht_quant_affine_ws_bytes(4) >= 32 and L.hatq_fwht_quant_affine_ws_bytes(0) == 0
+    assert q(None, 1, 4, 4, 64, 64, FAKE, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EINVAL
+    assert q(FAKE, 1, 4, 4, 64, 64, FAKE, FAKE, None, FAKE, 256, None) == hatq.HATQ_EINVAL     # no zero points
+    assert q(FAKE, 1, 4, 4, 64, 48, FAKE, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EINVAL
+    assert q(FAKE, 4, 4, 4, 64, 64, FAKE, FAKE, FAKE, FAKE, 16, None) == hatq.HATQ_EWORKSPACE
+    assert q(FAKE, 1, 4, 4, 48, 32, FAKE, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EUNSUPPORTED  # c % b
+    assert q(FAKE, 1, 3, 3, 3, 1, FAKE, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EUNSUPPORTED    # h*w*c % 4
+    W = _fake_weights()
+    assert L.hatq_tapsum_len(ctypes.byref(W)) == (W.d.k * W.d.k + 1) * W.cout_pad
+    assert L.hatq_tapsum_len(None) == 0
+    assert L.hatq_weight_tapsums(ctypes.byref(W), None, None) == hatq.HATQ_EINVAL
+    assert L.hatq_weight_tapsums(ctypes.byref(W), ctypes.c_void_p(FAKE.value + 4), None) == hatq.HATQ_EINVAL
+    c = L.hatq_conv_int8_affine
+    assert c(None, FAKE, FAKE, FAKE, FAKE, 1, 8, 8, 1, FAKE, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W), FAKE, FAKE, None, FAKE, 1, 8, 8, 1, FAKE, None) == hatq.HATQ_EINVAL   # no zero points
+    assert c(ctypes.byref(W), FAKE, FAKE, FAKE, None, 1, 8, 8, 1, FAKE, None) == hatq.HATQ_EINVAL   # no tap sums
+    assert c(ctypes.byref(W), FAKE, FAKE, FAKE, FAKE, 1, 8, 8, hatq.HATQ_OUT_I8, FAKE, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W), FAKE, FAKE, FAKE, FAKE, 0, 8, 8, 1, FAKE, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W), FAKE, FAKE, FAKE, ctypes.c_void_p(FAKE.value + 4), 1, 8, 8, 1, FAKE, None) \
+        == hatq.HATQ_EINVAL
+
+
 def test_layer_forward_form_flag_and_workspace(L):
     f = L.hatq_layer_forward
     W = _fake_weights()
