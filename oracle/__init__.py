@@ -16,6 +16,8 @@ the per-step functions in the order the paper gives them:
                                                          Eq. integer_hadamard_transition
     range-expansion statistic and the DH/WH rule         Eq. hadamard_sensitivity,
                                                          Eq. layerwise_hadamard_selection
+    Paley / Kronecker orders and the order rule          Eq. hadamard_order,
+                                                         Eq. supp_hadamard_order
 
 Parity status: every function is pinned by the CPU tests (identities of the
 Hadamard matrix, a library special case for the convolution, function
@@ -75,6 +77,10 @@ def lib():
         L.orc_int_requant_params.argtypes = [i32, ctypes.c_float, P, P, ctypes.c_float, i32, i32, i32, i32, P, P]
         L.orc_int_transition.argtypes = [P, i64, i32, i32, P, P, i32, i32, i32, P]
         L.orc_range_expansion.argtypes = [P, i32, i64, i32, i32, P, P, P]
+        L.orc_paley.argtypes = [i32, i32, P]
+        L.orc_hadamard.argtypes = [i32, P]
+        L.orc_hadamard_base.argtypes = [i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+        L.orc_order.argtypes = [i32, i32]
         L.orc_select_form.argtypes = [i64, i64, ctypes.c_double]
         _lib = L
     return _lib
@@ -283,7 +289,9 @@ def layer_unquantized(x: np.ndarray, pw: PreparedWeights) -> np.ndarray:
         y = acc / pw.hblock + pw.w_bias[: pw.cout].astype(np.float64)
     else:
         z = acc + pw.w_bias.astype(np.float64)
-        y = block_transform_f64(z, pw.hblock)[..., : pw.cout] / pw.hblock
+        # restore with B^T (B^T B = b I): row vectors times H
+        H = hadamard(pw.hblock).astype(np.float64)
+        y = (z.reshape(z.shape[:-1] + (-1, pw.hblock)) @ H).reshape(z.shape)[..., : pw.cout] / pw.hblock
     return y
 
 
@@ -359,3 +367,39 @@ def select_form(expansions: int, images: int, tau: float = 0.8) -> str:
     if r < 0:
         raise ValueError("bad counts")
     return "WH" if r else "DH"
+
+
+# --------------------------------------------------------------------------
+# O8  Hadamard orders beyond powers of two
+# --------------------------------------------------------------------------
+def paley(q: int, kind: int) -> np.ndarray:
+    """Paley-I (kind 1, q = 3 mod 4, order q + 1) or Paley-II (kind 2, q = 1 mod 4,
+    order 2(q + 1)) for a prime q."""
+    n = (q + 1) * (1 if kind == 1 else 2)
+    H = np.empty((n, n), np.int8)
+    if lib().orc_paley(q, kind, _p(H)) != 0:
+        raise ValueError("no Paley matrix of this kind for q")
+    return H
+
+
+def hadamard_base(m: int):
+    """(b, kind, q): the base order of the construction of order m (P_b (x) H~_(m/b))
+    and its Paley kind and prime (kind 0: b = 1, Sylvester); None if unsupported."""
+    kind, q = ctypes.c_int32(), ctypes.c_int32()
+    b = lib().orc_hadamard_base(m, ctypes.byref(kind), ctypes.byref(q))
+    return None if b < 0 else (int(b), int(kind.value), int(q.value))
+
+
+def hadamard(m: int) -> np.ndarray:
+    H = np.empty((m, m), np.int8)
+    if lib().orc_hadamard(m, _p(H)) != 0:
+        raise ValueError("unsupported order")
+    return H
+
+
+def order(C: int, mmax: int = 4096) -> int:
+    """Eq. hadamard_order: the smallest supported order >= 4 ceil(C / 4)."""
+    m = lib().orc_order(C, mmax)
+    if m < 0:
+        raise ValueError("no supported order below mmax")
+    return int(m)

@@ -59,6 +59,127 @@ int orc_sylvester(int b, int8_t *H)
     return 0;
 }
 
+/* Paley constructions (supplementary, Hadamard construction): chi is the     */
+/* quadratic character of the prime field F_q (chi(0) = 0) and Q the          */
+/* Jacobsthal matrix Q[i][j] = chi(j - i).                                    */
+/*  Paley-I  (q = 3 mod 4, order q + 1): H = I + [[0, 1^T], [-1, Q]].         */
+/*  Paley-II (q = 1 mod 4, order 2(q + 1)): with the symmetric conference     */
+/*           matrix C = [[0, 1^T], [1, Q]], every entry C[i][j] becomes the   */
+/*           2x2 block [[1, -1], [-1, -1]] where C[i][j] = 0 and              */
+/*           C[i][j] * [[1, 1], [1, -1]] otherwise.                           */
+/* Only prime q (no prime powers).  Returns 0, or -1 if q is not such a prime.*/
+static int is_prime(int q)
+{
+    if (q < 2) return 0;
+    for (int d = 2; d * d <= q; ++d)
+        if (q % d == 0) return 0;
+    return 1;
+}
+
+static int chi(int a, int q)
+{
+    a = ((a % q) + q) % q;
+    if (a == 0) return 0;
+    for (int x = 1; x < q; ++x)
+        if ((x * x) % q == a) return 1;
+    return -1;
+}
+
+int orc_paley(int q, int kind, int8_t *H)
+{
+    if (!is_prime(q) || q == 2) return -1;
+    const int n = q + 1;
+    if (kind == 1) {
+        if (q % 4 != 3) return -1;
+        for (int i = 0; i < n; ++i)
+            for (int j = 0; j < n; ++j) {
+                int s;
+                if (i == 0) s = j == 0 ? 0 : 1;
+                else if (j == 0) s = -1;
+                else s = chi(j - i, q);
+                H[i * n + j] = (int8_t)((i == j ? 1 : 0) + s);
+            }
+        return 0;
+    }
+    if (kind == 2) {
+        if (q % 4 != 1) return -1;
+        const int m = 2 * n;
+        for (int i = 0; i < n; ++i)
+            for (int j = 0; j < n; ++j) {
+                int c;
+                if (i == 0 || j == 0) c = (i == j) ? 0 : 1;
+                else c = chi(j - i, q);
+                for (int a = 0; a < 2; ++a)
+                    for (int b = 0; b < 2; ++b) {
+                        int v;
+                        if (c == 0) v = (a == 0 && b == 0) ? 1 : -1;
+                        else v = (a == 1 && b == 1) ? -c : c;
+                        H[(2 * i + a) * m + 2 * j + b] = (int8_t)v;
+                    }
+            }
+        return 0;
+    }
+    return -1;
+}
+
+/* Base orders of the supported set: 1 and the Paley orders (Paley-I first    */
+/* where both give the same order).  The construction of order m is          */
+/* P_b (x) H~_(m/b) with the smallest base b such that m/b is a power of two; */
+/* returns b and its construction (kind 0: b = 1, else the Paley kind and q), */
+/* or -1 when m is not in the supported set.                                  */
+int orc_hadamard_base(int m, int *kind, int *q)
+{
+    if (m < 1) return -1;
+    for (int b = 1; b <= m; ++b) {
+        if (m % b || !is_pow2(m / b)) continue;
+        if (b == 1) { *kind = 0; *q = 0; return 1; }
+        if (is_prime(b - 1) && (b - 1) % 4 == 3) { *kind = 1; *q = b - 1; return b; }
+        if (b % 2 == 0 && is_prime(b / 2 - 1) && (b / 2 - 1) % 4 == 1) { *kind = 2; *q = b / 2 - 1; return b; }
+    }
+    return -1;
+}
+
+/* The Hadamard matrix of order m (row-major m*m): the Kronecker product      */
+/* P_b (x) H~_(m/b), index (a, j) -> a * (m/b) + j.  -1 if unsupported.        */
+int orc_hadamard(int m, int8_t *H)
+{
+    int kind, q;
+    const int b = orc_hadamard_base(m, &kind, &q);
+    if (b < 0) return -1;
+    const int s = m / b;
+    int8_t *P = (int8_t *)malloc((size_t)b * b);
+    int8_t *S = (int8_t *)malloc((size_t)s * s);
+    if (kind == 0) P[0] = 1;
+    else orc_paley(q, kind, P);
+    orc_sylvester(s, S);
+    for (int a = 0; a < b; ++a)
+        for (int j = 0; j < s; ++j)
+            for (int c = 0; c < b; ++c)
+                for (int l = 0; l < s; ++l)
+                    H[(a * s + j) * m + c * s + l] = (int8_t)(P[a * b + c] * S[j * s + l]);
+    free(P);
+    free(S);
+    return 0;
+}
+
+/* Eq. hadamard_order: C_4 = 4 ceil(C / 4), m(C) = the smallest supported     */
+/* order >= C_4 (searched up to mmax; -1 if none).                            */
+int orc_order(int C, int mmax)
+{
+    if (C < 1) return -1;
+    const int c4 = 4 * ((C + 3) / 4);
+    int kind, q;
+    for (int m = c4; m <= mmax; ++m)
+        if (orc_hadamard_base(m, &kind, &q) > 0) return m;
+    return -1;
+}
+
+static int supported(int m)
+{
+    int kind, q;
+    return orc_hadamard_base(m, &kind, &q) > 0;
+}
+
 /* Dense block-diagonal transform along the last axis, fp64 in and out:       */
 /*   out[r, blk*b + i] = sum_j H~_b[i][j] * in[r, blk*b + j]                   */
 /* for width = nblk*b.  Summation runs over j in natural order.               */
@@ -79,9 +200,9 @@ static void block_transform_f64(const int8_t *H, int b, const double *in, double
 /* Public wrapper: fp64 block transform of `rows` rows of width `width`. */
 int orc_block_transform_f64(int b, const double *in, double *out, int64_t rows, int width)
 {
-    if (!is_pow2(b) || width % b) return -1;
+    if (!supported(b) || width % b) return -1;
     int8_t *H = (int8_t *)malloc((size_t)b * b);
-    orc_sylvester(b, H);
+    orc_hadamard(b, H);
     block_transform_f64(H, b, in, out, rows, width);
     free(H);
     return 0;
@@ -91,14 +212,15 @@ int orc_block_transform_f64(int b, const double *in, double *out, int64_t rows, 
 /* O3. Activation operand.  DH: S = fl32(B_C x_pad) per pixel, computed in    */
 /* fp64 with one rounding (Eq. input_hadamard_transform, Eq. supp_padded_     */
 /* transforms: zero-pad C to C_pad = b*ceil(C/b)).  WH: b = 1, S = x.         */
+/* b is any supported order (orc_hadamard), the power-of-two ones Sylvester.  */
 /* x is [P, C] fp32 (P pixels), S is [P, C_pad] fp32.                         */
 /* ------------------------------------------------------------------------- */
 int orc_activation_transform(const float *x, int64_t P, int C, int b, float *S)
 {
-    if (!is_pow2(b) || C <= 0) return -1;
+    if (!supported(b) || C <= 0) return -1;
     const int Cp = round_up(C, b);
     int8_t *H = (int8_t *)malloc((size_t)b * b);
-    orc_sylvester(b, H);
+    orc_hadamard(b, H);
     #pragma omp parallel
     {
         double *in = (double *)malloc(sizeof(double) * Cp);
@@ -199,7 +321,7 @@ int orc_prepare_weights(int cin, int cout, int k, int transposed, int hblock, in
                         const float *w, const float *bias,
                         int8_t *wq, float *w_scale, float *w_bias, float *w_real)
 {
-    if (!is_pow2(hblock) || cin <= 0 || cout <= 0 || k <= 0 || (form != 0 && form != 1))
+    if (!supported(hblock) || cin <= 0 || cout <= 0 || k <= 0 || (form != 0 && form != 1))
         return -1;
     const int cin_p = form == 0 ? round_up(cin, hblock) : cin;
     const int cout_p = form == 1 ? round_up(cout, hblock) : cout;
@@ -208,7 +330,7 @@ int orc_prepare_weights(int cin, int cout, int k, int transposed, int hblock, in
     double *W0 = (double *)calloc((size_t)cout_p * per_co, sizeof(double));
     float *W1 = (float *)malloc(sizeof(float) * (size_t)cout_p * per_co);
     int8_t *H = (int8_t *)malloc((size_t)hblock * hblock);
-    orc_sylvester(hblock, H);
+    orc_hadamard(hblock, H);
 
     /* canonical fp64 copy, zero padded */
     for (int co = 0; co < cout; ++co)
@@ -368,21 +490,27 @@ void orc_conv_f64(const double *x, int n, int h, int w, int cin,
 
 /* ------------------------------------------------------------------------- */
 /* O5. Epilogues.  acc: [n][pix][cout_p] int32, sx[n], sw[cout_p], bias.       */
-/* DH: y = fma(float(acc), t_c, bias_c),  t_c = fl(fl(sx*sw_c) * 2^-log2(b)),  */
-/*     for c < cout (output in the original basis, Eq. supp_padded_dh).       */
+/* DH: y = fma(float(acc), t_c, bias_c),  t_c = fl(fl(sx*sw_c) / b) (an exact */
+/*     scaling when b is a power of two), for c < cout (output in the         */
+/*     original basis, Eq. supp_padded_dh).                                   */
 /* WH: z_c = fma(float(acc_c), fl(sx*sw_c), b~_c) for every c < cout_p (scale  */
-/*     aligned before the basis change), then y = fl32(B_Cout z / b) with a   */
+/*     aligned before the basis change), then y = fl32(B_Cout^T z / b) with a */
 /*     dense fp64 multiply, truncated to cout (Eq. supp_padded_wh).           */
 /* ------------------------------------------------------------------------- */
 int orc_epilogue(const int32_t *acc, int n, int64_t pix, int cout, int cout_p, int form,
                  int hblock, const float *sx, const float *sw, const float *bias, float *y)
 {
-    if (!is_pow2(hblock) || (form == 1 && cout_p % hblock)) return -1;
-    const float inv_b = 1.0f / (float)hblock; /* exact: power of two */
+    if (!supported(hblock) || (form == 1 && cout_p % hblock)) return -1;
     int8_t *H = NULL;
     if (form == 1) {
+        /* the restore multiplies by the transpose (B^T B = b I; Sylvester   */
+        /* blocks are symmetric, Paley-I blocks are not)                      */
+        int8_t *Hf = (int8_t *)malloc((size_t)hblock * hblock);
         H = (int8_t *)malloc((size_t)hblock * hblock);
-        orc_sylvester(hblock, H);
+        orc_hadamard(hblock, Hf);
+        for (int i = 0; i < hblock; ++i)
+            for (int j = 0; j < hblock; ++j) H[i * hblock + j] = Hf[j * hblock + i];
+        free(Hf);
     }
     for (int b = 0; b < n; ++b) {
         #pragma omp parallel
@@ -395,7 +523,7 @@ int orc_epilogue(const int32_t *acc, int n, int64_t pix, int cout, int cout_p, i
                 float *yo = y + ((int64_t)b * pix + p) * cout;
                 if (form == 0) {
                     for (int c = 0; c < cout; ++c) {
-                        const float t = (sx[b] * sw[c]) * inv_b;
+                        const float t = (sx[b] * sw[c]) / (float)hblock;   /* exact scaling for 2^k */
                         yo[c] = fmaf((float)a[c], t, bias[c]);
                     }
                 } else {

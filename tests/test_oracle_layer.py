@@ -33,6 +33,10 @@ LAYERS = [  # (name, n, h, w, cin, cout, k, stride, pad, transposed, out_pad, fo
     ("rgb_wh_b64", 1, 12, 13, 3, 64, 5, 2, 2, False, 0, "WH", 64),
     ("pad_dh_c40", 1, 7, 6, 40, 16, 3, 1, 1, False, 0, "DH", 64),     # C_in padded 40 -> 64
     ("pad_wh_c40", 1, 7, 6, 16, 40, 3, 1, 1, False, 0, "WH", 64),     # C_out padded 40 -> 64
+    ("k5s2_dh_m192", 1, 9, 8, 192, 64, 5, 2, 2, False, 0, "DH", 192),  # H_12 (x) H~_16
+    ("k3_wh_m320", 1, 6, 7, 32, 320, 3, 1, 1, False, 0, "WH", 320),    # H_20 (x) H~_16
+    ("pad_dh_c17_m20", 1, 7, 6, 17, 8, 3, 1, 1, False, 0, "DH", 20),  # m(17) = 20: Paley-I
+    ("pad_wh_c10_m12", 1, 5, 6, 8, 10, 3, 1, 1, False, 0, "WH", 12),  # m(10) = 12
 ]
 
 
