@@ -69,8 +69,16 @@ typedef enum {
 /* One layer's geometry.  Square kernels only.
  *   conv:        ho = (h + 2*pad - k)/stride + 1
  *   transposed:  ho = (h - 1)*stride - 2*pad + k + out_pad
- * hblock: Sylvester block size b, a power of two in [1, 128]; it acts on cin
- * for DH and on cout for WH.  b = 1 means no transform. */
+ * hblock: block order b of the transform B = I (x) H_b; it acts on cin for DH
+ * and on cout for WH.  b = 1 means no transform.  A power of two in [1, 128]
+ * (Sylvester H~_b), or one of the orders m(C) of Eq. hadamard_order that the
+ * Sylvester family lacks, built as Kronecker products with a Paley-I factor
+ * (supplementary, Hadamard construction): 192 = P_12 (x) H~_16 and
+ * 320 = P_20 (x) H~_16, index a*16 + l (Paley index a, Sylvester index l).
+ * Those two are supported for DH layers in hatq_fwht_quant_act,
+ * hatq_prepare_weights, hatq_conv_int8 and hatq_layer_forward (the DH
+ * dequantization factor is fl(s_x s_w / b)); the requantizing, integer,
+ * affine and profiling entry points and WH layers take powers of two. */
 typedef struct {
     int32_t cin, cout;
     int32_t k;
@@ -155,7 +163,8 @@ size_t hatq_fwht_quant_ws_bytes(int32_t n);
  *   act_scale: device fp32 [n], receives s_x (unnormalized-domain scale).
  *   ws:       device workspace of hatq_fwht_quant_ws_bytes(n) bytes (unused
  *             when absmax is given).
- * Supported: c % hblock == 0, and c % 4 == 0 or hblock == 1. */
+ * Supported: c % hblock == 0, and c % 4 == 0 or hblock == 1; for the Kronecker
+ * orders 192 and 320, h*w*c % 4 == 0. */
 int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int32_t c,
                             int32_t hblock, const float *absmax, int8_t *xq, float *act_scale,
                             void *ws, size_t ws_bytes, void *stream);

@@ -515,6 +515,8 @@ hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const 
         case 32: return launch_vector<32>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
         case 64: return launch_vector<64>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
         case 128: return launch_vector<128>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        case 192: return launch_vector<192>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
+        case 320: return launch_vector<320>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
         default: return hipErrorInvalidValue;
     }
 }

@@ -18,12 +18,16 @@ bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
+// Transform orders the kernels implement: Sylvester blocks up to 128 and the
+// Kronecker orders 192 = P_12 (x) H~_16 and 320 = P_20 (x) H~_16.
+bool supported_order(int32_t b) { return (is_pow2(b) && b <= 128) || hatq::kron_q(b) != 0; }
+
 int32_t check_desc(const hatq_conv_desc *d, int32_t form) {
     if (!d) return HATQ_EINVAL;
     if (form != HATQ_DH && form != HATQ_WH) return HATQ_EINVAL;
     if (d->cin <= 0 || d->cout <= 0 || d->k <= 0 || d->stride <= 0 || d->pad < 0 || d->out_pad < 0)
         return HATQ_EINVAL;
-    if (!is_pow2(d->hblock) || d->hblock > 128) return HATQ_EINVAL;
+    if (!supported_order(d->hblock)) return HATQ_EINVAL;
     if (d->transposed != 0 && d->transposed != 1) return HATQ_EINVAL;
     if (d->transposed && d->out_pad >= d->stride) return HATQ_EINVAL;
     return HATQ_OK;
@@ -313,7 +317,7 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
                             const float *absmax, int8_t *xq, float *act_scale, void *ws, size_t ws_bytes,
                             void *stream) {
     if (!x || !xq || !act_scale || n <= 0 || h <= 0 || w <= 0 || c <= 0) return HATQ_EINVAL;
-    if (!is_pow2(hblock) || hblock > 128) return HATQ_EINVAL;
+    if (!supported_order(hblock)) return HATQ_EINVAL;
     if (c % hblock) return HATQ_EUNSUPPORTED;
     if (!aligned(x, 16) || !aligned(xq, 4) || !aligned(act_scale, 4)) return HATQ_EINVAL;
     if (absmax && !aligned(absmax, 4)) return HATQ_EINVAL;
@@ -355,6 +359,7 @@ int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const fl
         return HATQ_EINVAL;
     if (next_absmax && !aligned(next_absmax, 4)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    if (!is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
     // the transform and the code layout follow the next operand's blocks
     const float *probe = next_absmax ? next_absmax : next_scale;
     if ((s = check_next(W, next_hblock, probe)) != HATQ_OK) return s;
@@ -391,6 +396,7 @@ int32_t hatq_weight_tapsums(const hatq_weights *W, int32_t *tapsum, void *stream
     int32_t s = check_weights(W);
     if (s != HATQ_OK) return s;
     if (!tapsum || !aligned(tapsum, 16)) return HATQ_EINVAL;
+    if (W->d.k * W->d.k > 256) return HATQ_EUNSUPPORTED;   // one thread per tap
     hatq::PrepArgs a;
     std::memset(&a, 0, sizeof(a));
     a.wq = W->wq;
@@ -413,6 +419,7 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
         !aligned(tapsum, 16))
         return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    if (!is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
     return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, 0, nullptr, static_cast<hipStream_t>(stream),
@@ -431,6 +438,7 @@ int32_t hatq_int_transition_params(const hatq_weights *W, float s_x, float s_y, 
     if (!table || !aligned(table, 16)) return HATQ_EINVAL;
     if (!(s_x > 0.0f) || !(s_y > 0.0f) || !std::isfinite(s_x) || !std::isfinite(s_y)) return HATQ_EINVAL;
     if (!is_pow2(next_hblock) || next_hblock > 64) return HATQ_EINVAL;
+    if (!is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
     const bool dh = W->form == HATQ_DH;
     hatq::IntParamArgs a;
     a.w_scale = W->w_scale;
@@ -460,6 +468,7 @@ int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, i
     if (!xq || !table || !yq || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
     if (!aligned(xq, 16) || !aligned(yq, 4) || !aligned(table, 16)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    if (!is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
     if ((s = check_next(W, next_hblock, reinterpret_cast<const float *>(table))) != HATQ_OK) return s;
     if (W->d.cout % 4) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;

@@ -59,8 +59,9 @@ __device__ __forceinline__ int64_t out_pixel(const ConvArgs &a, int nb, int gi, 
 }
 
 // Per-tile column factors of the dequantization (the tile is one sample, so
-// s_x is uniform).  Both forms fold the exact factor 1/b in here:
-//   DH: y = fma(acc, t_c, bias_c)        with t_c = fl(fl(s_x*s_w,c) * (1/b));
+// s_x is uniform).  Both forms fold the factor 1/b in here:
+//   DH: y = fma(acc, t_c, bias_c)        with t_c = fl(fl(s_x*s_w,c) / b) (b may be
+//       a Kronecker order, 192 or 320; for a power of two this is exact scaling);
 //   WH: z/b = fma(acc, t_c, b~_c * (1/b)), and y = B_Cout (z/b) = (B_Cout z)/b.
 // Scaling by a power of two commutes with every rounding (results far above
 // the subnormal range), so the WH output equals restoring z first and dividing
@@ -73,9 +74,14 @@ __device__ __forceinline__ void column_factor(const ConvArgs &a, float sxv, int 
         b = __int_as_float(a.rq_table[a.cout_pad + c]);
         return;
     }
-    const float inv_b = 1.0f / (float)a.hblock;
-    t = (sxv * a.w_scale[c]) * inv_b;
-    b = a.form == 1 ? a.bias[c] * inv_b : a.bias[c];
+    if (a.form == 1) {
+        const float inv_b = 1.0f / (float)a.hblock;
+        t = (sxv * a.w_scale[c]) * inv_b;
+        b = a.bias[c] * inv_b;
+    } else {
+        t = (sxv * a.w_scale[c]) / (float)a.hblock;   // exact scaling for a power of two
+        b = a.bias[c];
+    }
 }
 
 // The tile's activation scale (the integer transition has none).

@@ -18,6 +18,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "hatq_launch.h"
+
 namespace hatq {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
@@ -113,13 +115,64 @@ __device__ __forceinline__ float wave_max(float m) {
     return m;
 }
 
+// ---- Hadamard orders beyond powers of two -------------------------------------
+// Paley-I matrix of order q + 1 (q prime, q = 3 mod 4): I + [[0, 1^T], [-1, Q]]
+// with the Jacobsthal matrix Q[i][j] = chi(j - i), chi the quadratic character
+// of F_q (chi(0) = 0).  The kernels support the Kronecker orders
+// 192 = P_12 (x) H~_16 and 320 = P_20 (x) H~_16 (channel a*16 + l: the Paley
+// factor on a, the Sylvester butterfly on l).
+constexpr int quad_char(int a, int q) {
+    a = ((a % q) + q) % q;
+    if (a == 0) return 0;
+    for (int x = 1; x < q; ++x)
+        if ((x * x) % q == a) return 1;
+    return -1;
+}
+
+constexpr int paley1_entry(int q, int i, int j) {
+    const int s = i == 0 ? (j == 0 ? 0 : 1) : (j == 0 ? -1 : quad_char(j - i, q));
+    return (i == j ? 1 : 0) + s;
+}
+
+template <int Q>
+struct Paley1Table {
+    int8_t s[Q + 1][Q + 1];
+    constexpr Paley1Table() : s() {
+        for (int i = 0; i <= Q; ++i)
+            for (int j = 0; j <= Q; ++j) s[i][j] = (int8_t)paley1_entry(Q, i, j);
+    }
+};
+
 template <int B>
 struct ItemShape {
-    static constexpr int I = B > 64 ? B : 64;   // floats per item
-    static constexpr int R = I / 16;            // float4 registers per lane
-    static constexpr int LOG = B == 1 ? 0 : B == 2 ? 1 : B == 4 ? 2 : B == 8 ? 3 : B == 16 ? 4
+    static constexpr bool KRON = kron_q(B) != 0;   // P_(B/16) (x) H~_16
+    static constexpr int I = B > 64 ? B : 64;      // floats per item
+    static constexpr int R = I / 16;               // float4 registers per lane
+    static constexpr int LOG = KRON ? 4 : B == 1 ? 0 : B == 2 ? 1 : B == 4 ? 2 : B == 8 ? 3 : B == 16 ? 4
                                : B == 32 ? 5 : B == 64 ? 6 : 7;
 };
+
+// The Paley factor of a Kronecker order on the register groups of an item:
+// out[a] = sum over c, ascending, of P[a][c] * v[c] for each of the four values
+// j of group c (v[4*c + j]).
+template <int Q, int R4>
+__device__ __forceinline__ void paley_stage(float (&v)[R4]) {
+    constexpr int P = Q + 1;
+    static_assert(R4 == 4 * P, "one register group per Paley index");
+    constexpr Paley1Table<Q> H{};
+    float out[R4];
+#pragma unroll
+    for (int a = 0; a < P; ++a)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float acc = H.s[a][0] > 0 ? v[j] : -v[j];
+#pragma unroll
+            for (int c = 1; c < P; ++c) acc = H.s[a][c] > 0 ? acc + v[4 * c + j] : acc - v[4 * c + j];
+            out[4 * a + j] = acc;
+        }
+#pragma unroll
+    for (int r = 0; r < R4; ++r) v[r] = out[r];
+}
 
 // Quad layout: one quad (4 consecutive lanes) owns an item of I = max(64, b)
 // consecutive floats; lane t of the quad holds channels 16*i + 4*t + j in
@@ -146,6 +199,7 @@ __device__ __forceinline__ float fwht_item(float (&v)[R4], int t) {
     if constexpr (LOG >= 5) reg_stage<4>(v);                 // channel bit 4: register ^ 1
     if constexpr (LOG >= 6) reg_stage<8>(v);                 // channel bit 5
     if constexpr (LOG >= 7) reg_stage<16>(v);                // channel bit 6
+    if constexpr (ItemShape<B>::KRON) paley_stage<kron_q(B)>(v);   // channel bits 4+: the Paley factor
     return sigma;
 }
 

@@ -24,6 +24,10 @@ hipError_t launch_act_quant_affine(const float *x, int n, int64_t E, int hblock,
 hipError_t launch_range_expansion(const float *x, int n, int64_t P, int C, int hblock, float *amax, int32_t *flags,
                                   int32_t *count, hipStream_t st);
 
+// Kronecker transform orders P_(m/16) (x) H~_16 the kernels implement, by the
+// prime q of their Paley-I factor (order q + 1); 0 for other orders.
+constexpr int kron_q(int m) { return m == 192 ? 11 : m == 320 ? 19 : 0; }
+
 constexpr int kMaxTaps = 64;
 constexpr int kModeIntTransition = 3;   // ConvArgs::mode of the integer transition
 

@@ -1,7 +1,8 @@
 // Offline weight preparation on the device (step a1).
 //
 // DH (Eq. hadamard_linear_equivalence, Eq. supp_padded_dh): every (co, tap) row
-// of the contraction is multiplied by B_Cin = I (x) H~_b.  WH (Eq.
+// of the contraction is multiplied by B_Cin = I (x) H~_b (H~_b Sylvester, or the
+// Kronecker order P (x) H~_16 for b = 192, 320; then W' = W B^T).  WH (Eq.
 // weight_only_hadamard_equivalence, Eq. supp_padded_wh_parameters): every (tap, ci)
 // column is multiplied by B_Cout, and the bias becomes b~ = B_Cout [b; 0].
 // Each transformed value is an fp64 sum over j = 0..b-1 in ascending order of
@@ -28,6 +29,14 @@ __device__ __forceinline__ double w_orig(const PrepArgs &a, int co, int tap, int
 
 __device__ __forceinline__ double hsign(int i, int j) { return (__popc(i & j) & 1) ? -1.0 : 1.0; }
 
+// Entry (i, j) of the order-b block: Sylvester for powers of two, else the
+// Kronecker order P (x) H~_16 (index a*16 + l).
+__device__ __forceinline__ double block_sign(int b, int i, int j) {
+    const int q = kron_q(b);
+    if (q == 0) return hsign(i, j);
+    return paley1_entry(q, i >> 4, j >> 4) * hsign(i & 15, j & 15);
+}
+
 // Transformed weight W'[co][d], d = tap*cin_p + ci.
 __device__ float w_prime(const PrepArgs &a, int co, int d) {
     const int tap = d / a.cin_p, ci = d - tap * a.cin_p;
@@ -35,10 +44,10 @@ __device__ float w_prime(const PrepArgs &a, int co, int d) {
     double acc = 0.0;
     if (a.form == 0) {
         const int blk = ci / b * b, i = ci - blk;
-        for (int j = 0; j < b; ++j) acc += hsign(i, j) * w_orig(a, co, tap, blk + j);
+        for (int j = 0; j < b; ++j) acc += block_sign(b, i, j) * w_orig(a, co, tap, blk + j);
     } else {
         const int blk = co / b * b, i = co - blk;
-        for (int j = 0; j < b; ++j) acc += hsign(i, j) * w_orig(a, blk + j, tap, ci);
+        for (int j = 0; j < b; ++j) acc += block_sign(b, i, j) * w_orig(a, blk + j, tap, ci);
     }
     return (float)acc;
 }
@@ -91,7 +100,7 @@ __global__ void __launch_bounds__(kThreads) prepare_kernel(const PrepArgs a) {
             } else {
                 const int b = a.hblock, blk = co / b * b, i = co - blk;
                 for (int j = 0; j < b; ++j)
-                    bv += hsign(i, j) * (blk + j < a.cout ? (double)a.bias[blk + j] : 0.0);
+                    bv += block_sign(b, i, j) * (blk + j < a.cout ? (double)a.bias[blk + j] : 0.0);
             }
         }
         a.w_bias[co] = (float)bv;
@@ -152,26 +161,32 @@ __global__ void __launch_bounds__(kThreads) int_params_kernel(const IntParamArgs
     if (tid == 0) a.table[2 * a.cout_p] = n;
 }
 
-// One thread per output channel: the per-tap sums, then their total.
+// One block per output channel, one thread per tap (k*k <= kMaxTaps <= the
+// block), then the block's total.
 __global__ void __launch_bounds__(kThreads) tapsum_kernel(const PrepArgs a, int32_t *tapsum) {
-    const int c = blockIdx.x * kThreads + threadIdx.x;
-    if (c >= a.cout_p) return;
+    __shared__ int32_t s_sum[kThreads];
+    const int c = blockIdx.x, t = threadIdx.x;
     const int taps = a.k * a.k;
-    const int8_t *row = a.wq + (int64_t)c * a.k_stride;
-    int32_t all = 0;
-    for (int t = 0; t < taps; ++t) {
-        int32_t sum = 0;
-        for (int ci = 0; ci < a.cin_p; ++ci) sum += row[t * a.cin_p + ci];
+    int32_t sum = 0;
+    if (t < taps) {
+        const int8_t *row = a.wq + (int64_t)c * a.k_stride + t * a.cin_p;
+        for (int ci = 0; ci < a.cin_p; ++ci) sum += row[ci];
         tapsum[(int64_t)t * a.cout_p + c] = sum;
-        all += sum;
     }
-    tapsum[(int64_t)taps * a.cout_p + c] = all;
+    s_sum[t] = sum;
+    __syncthreads();
+    for (int h = kThreads / 2; h > 0; h >>= 1) {
+        if (t < h) s_sum[t] += s_sum[t + h];
+        __syncthreads();
+    }
+    if (t == 0) tapsum[(int64_t)taps * a.cout_p + c] = s_sum[0];
 }
 
 }  // namespace
 
 hipError_t launch_tapsums(const PrepArgs &a, int32_t *tapsum, hipStream_t st) {
-    tapsum_kernel<<<(a.cout_p + kThreads - 1) / kThreads, kThreads, 0, st>>>(a, tapsum);
+    if (a.k * a.k > kThreads) return hipErrorInvalidValue;
+    tapsum_kernel<<<a.cout_p, kThreads, 0, st>>>(a, tapsum);
     return hipGetLastError();
 }
 
