@@ -261,6 +261,56 @@ def measure_affine_layer(args, wl, layers, xq, ys, per_layer, li=2):
                     "zero-point correction in the conv epilogue"}
 
 
+def measure_order_layer(args, wl, params, xq, sc, ys, per_layer, li=2):
+    """Layer 3 (DH, 192 input channels) with the paper's transform order
+    m(192) = 192 (one Kronecker block P_12 (x) H~_16 over all channels) in place
+    of blocks of 64: the two-pass activation quantization of its fp32 input and
+    the convolution, timed after the step beside the block-64 layer."""
+    import torch
+    from paper_2608_01653_amd import hatq, workloads
+    L = wl.layers[li]
+    m = 192
+    if L.form != "DH" or L.cin % m:
+        return None
+    dev = ys[0].device
+    w, b = params[li]
+    layer = hatq.hatq_prepare_weights(hatq.desc(L.cin, L.cout, L.k, L.stride, L.pad, m, L.transposed, L.out_pad),
+                                      "DH", torch.from_numpy(w).to(dev), torch.from_numpy(b).to(dev))
+    x = ys[li - 1]
+    n = x.shape[0]
+    ws = torch.empty(int(hatq.load().hatq_fwht_quant_ws_bytes(n)), dtype=torch.int8, device=dev)
+
+    def run(events=None):
+        if events:
+            events[0].record()
+        hatq.hatq_fwht_quant_act(x, m, xq=xq[li], scale=sc[li], ws=ws)
+        if events:
+            events[1].record()
+        hatq.hatq_conv_int8(layer, xq[li], sc[li], hatq.HATQ_OUT_F32, y=ys[li])
+        if events:
+            events[2].record()
+
+    for _ in range(args.warmup):
+        run()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for k in range(args.steps):
+        run(ev[k])
+    torch.cuda.synchronize()
+    tq = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps * 1e3
+    tc = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps * 1e3
+    elems = x.numel()
+    log(f"order-{m} layer {li + 1}: quant {tq:.1f} us, conv {tc:.1f} us")
+    return {"layer": per_layer[li]["layer"], "order": m, "construction": "P_12 (x) H~_16 (Paley-I q = 11)",
+            "act_quant_us": round(tq, 2), "act_quant_passes": 2,
+            "act_quant_gbs_alg": round(elems * 9 / (tq * 1e-6) / 1e9, 1),
+            "conv_us": round(tc, 2),
+            "conv_tops": round(workloads.conv_ops(wl, li) / (tc * 1e-6) / 1e12, 1),
+            "block64_act_quant_us": per_layer[li]["act_quant_us"], "block64_conv_us": per_layer[li]["conv_us"],
+            "note": "two-pass quantization (the fused next-operand absmax covers blocks up to 64); "
+                    "algorithmic bytes 4 B read twice + 1 B written per element"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -421,6 +471,7 @@ def main():
     integer_stack = measure_integer_stack(args, wl, layers, x0, xq, sc, ys, ws, act_hb, total_ops, img_pix)
     form_selection = measure_form_selection(args, wl, layers, x0, xq, sc, ys)
     affine = measure_affine_layer(args, wl, layers, xq, ys, per_layer)
+    order_m = measure_order_layer(args, wl, params, xq, sc, ys, per_layer)
 
     out = {
         "metric": "Hadamard-INT8 conv TOPS + Mpixel/s per layer; % of INT8 MFMA / HBM peak",
@@ -442,6 +493,7 @@ def main():
         "integer_stack": integer_stack,
         "form_selection": form_selection,
         "affine_layer": affine,
+        "paper_order_layer": order_m,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, x_np, params)
