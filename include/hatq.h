@@ -185,7 +185,10 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
  *     layer can then quantize y reading it once.  It is overwritten, not
  *     accumulated.  y may be NULL in F32 mode when next_absmax is given: the
  *     call then only produces next_absmax (the first pass of
- *     hatq_conv_int8_requant's dynamic scale).
+ *     hatq_conv_int8_requant's dynamic scale).  With y = NULL, a WH layer whose
+ *     block equals next_hblock (> 1) takes the maximum of |z| instead, z the
+ *     dequantized accumulators before the output restore: B_next y = z exactly
+ *     there (the two transforms cancel, Table I), and no butterfly runs.
  * Supported: cin_pad % 64 == 0 with k <= 8, or cin_pad <= 4 with k*k*cin_pad <= 128;
  * cout_pad % 64 == 0; WH block and next_hblock at most 64.  Transposed: stride 2.
  * xq and y must be 16-byte aligned. */
@@ -200,7 +203,11 @@ int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act
  * y' = y, the WH input case), and quantized in registers,
  *   yq = clamp(rne(fl(y' / s)), -127, 127),
  * exactly as hatq_fwht_quant_act(y, ..., next_hblock, absmax = next_absmax)
- * would from y; y itself is never written.
+ * would from y; y itself is never written.  A WH layer whose block equals
+ * next_hblock (> 1) quantizes z, the dequantized accumulators before the
+ * output restore, which equals B_next y exactly (Table I): the codes are those
+ * of z (no butterfly), and can differ from the two-kernel path's by its fp32
+ * rounding.
  *   next_absmax: device fp32 [n] with max |B_next y| per sample (from an
  *     earlier hatq_conv_int8 call with y = NULL, or an upper bound of it); the
  *     scale is then s = fl32(next_absmax / 127) (1 if it is 0) and is written to

@@ -78,6 +78,7 @@ def lib():
         L.orc_int_transition.argtypes = [P, i64, i32, i32, P, P, i32, i32, i32, P]
         L.orc_range_expansion.argtypes = [P, i32, i64, i32, i32, P, P, P]
         L.orc_paley.argtypes = [i32, i32, P]
+        L.orc_wh_z.argtypes = [P, i32, i64, i32, P, P, P, P]
         L.orc_hadamard.argtypes = [i32, P]
         L.orc_hadamard_base.argtypes = [i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
         L.orc_order.argtypes = [i32, i32]
@@ -258,6 +259,19 @@ def epilogue(acc: np.ndarray, sx: np.ndarray, pw: PreparedWeights) -> np.ndarray
     if rc != 0:
         raise ValueError("bad epilogue geometry")
     return y
+
+
+def wh_z(acc: np.ndarray, sx: np.ndarray, pw: PreparedWeights) -> np.ndarray:
+    """A WH layer's dequantized accumulators before the output restore
+    [.., cout_p]: the next operand when the next transform uses the same blocks
+    (B_next y = z exactly, Table I)."""
+    assert pw.form == "WH"
+    acc = _c(acc, np.int32)
+    n = acc.shape[0]
+    pix = acc.size // (n * pw.cout_p)
+    z = np.empty(acc.shape, np.float32)
+    lib().orc_wh_z(_p(acc), n, pix, pw.cout_p, _p(_c(sx, np.float32)), _p(pw.w_scale), _p(pw.w_bias), _p(z))
+    return z
 
 
 @dataclass

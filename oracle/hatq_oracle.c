@@ -541,6 +541,22 @@ int orc_epilogue(const int32_t *acc, int n, int64_t pix, int cout, int cout_p, i
     return 0;
 }
 
+/* The WH layer's dequantized accumulators before the output restore: O5's   */
+/* z_c = fma(float(acc_c), fl(sx*sw_c), b~_c) for every c < cout_p.  When the */
+/* next operand's transform uses the same blocks, B_next y = B B^T z / b = z  */
+/* on every kept block in exact arithmetic (Table I: the WH output transform  */
+/* and the next DH input transform cancel), so z is that next operand.        */
+void orc_wh_z(const int32_t *acc, int n, int64_t pix, int cout_p, const float *sx, const float *sw,
+              const float *bias, float *z)
+{
+    for (int b = 0; b < n; ++b)
+        for (int64_t p = 0; p < pix; ++p)
+            for (int c = 0; c < cout_p; ++c) {
+                const int64_t i = ((int64_t)b * pix + p) * cout_p + c;
+                z[i] = fmaf((float)acc[i], sx[b] * sw[c], bias[c]);
+            }
+}
+
 /* ------------------------------------------------------------------------- */
 /* O6. Integer-only inter-layer transition (Eq. integer_accumulation with    */
 /* zero points 0, Eq. integer_fixed_point_scale, Eq. integer_hadamard_        */

@@ -247,8 +247,9 @@ __device__ __forceinline__ uint32_t int_code_hi(int64_t w, int s, int64_t bias_m
 // fp32 output; WB = NB = -1 is the generic body, which takes the output mode,
 // form and block sizes from the arguments.
 // Q = 1: I8 output (the next operand's codes, NB its transform block); Q = 2:
-// the same codes by the integer transition (mode 3); Q = 3 (generic only):
-// I32 / F32 output from affine activation codes.
+// the same codes by the integer transition (mode 3); Q = 3: output from affine
+// activation codes (fixed variants: F32 with no next-operand absmax, NB = 0;
+// the generic one also I32).
 template <int WB_, int NB_, int Q_ = 0>
 struct Epi {
     static constexpr int WB = WB_, NB = NB_, Q = Q_;
@@ -263,7 +264,8 @@ bool epi_matches(const ConvArgs &a) {
     if constexpr (E::WB == -1) {
         return (a.mode == kModeIntTransition) == (E::Q == 2) && (a.zx != nullptr) == (E::Q == 3);
     } else {
-        if (a.zx) return false;
+        if ((a.zx != nullptr) != (E::Q == 3)) return false;
+        if (E::Q == 3) return a.mode == 1 && (a.form == 1 ? a.hblock : 0) == E::WB && a.next_absmax == nullptr;
         const int wb = a.form == 1 ? a.hblock : 0;
         if (E::Q) return a.mode == (E::Q == 2 ? kModeIntTransition : 2) && wb == E::WB && a.next_hblock == E::NB;
         const int nb = a.next_absmax != nullptr ? a.next_hblock : 0;
@@ -357,10 +359,11 @@ struct Epilogue {
     const int row0, lane, p, q;
     const float *col_t, *col_b;
     const EpiFlags<E> fl;
-    bool full, z_bound, q_fast;
+    bool full, z_bound, zpair, q_fast;
     float wave_m, seen, qs, qr;
     int nbk, rq_n, rq_pre, zp;
     int64_t rq_bias;
+    uint64_t tapmask[FM];   // affine: the taps whose weight sums the pixel adjusts
     bool rq_pair, valid[FM], border[FM];
 
     __device__ __forceinline__ Epilogue(const ConvArgs &a_, const Tile &t_, int row0_, int lane_, const float *col_t_,
@@ -385,6 +388,10 @@ struct Epilogue {
         // exactly, so max|B y| <= max|z| (1 + 2 gamma_6 * 64) with gamma_6 the
         // six-stage fp32 rounding factor (< 3.6e-7); 1 + 1e-4 covers it.
         z_bound = fl.wh && (generic ? a.hblock == a.next_hblock : WB == NB);
+        // With no fp32 output to store, the next operand of such a layer is z
+        // itself (B_next y = B B z / b = z in exact arithmetic): its maximum and
+        // its codes are taken from z, and neither butterfly runs.
+        zpair = !fl.affine && z_bound && !fl.store && nbk > 1 && (fl.want_abs || fl.i8);
         // I8 mode: the sample's scale (from the absmax as the activation quantizer
         // derives it, or given), published by the sample's first tile
         qs = 1.0f;
@@ -423,23 +430,31 @@ struct Epilogue {
             const int m = row0 + 16 * i + p;
             valid[i] = t.gi0 + m / TW < a.gh && t.gj0 + m % TW < a.gw;
         }
-        // Affine activations: the sample's zero point, and per row group whether
-        // any lane's pixel has a tap outside the image (wave-uniform).
+        // Affine activations: the sample's zero point and, per row group, the
+        // lane's taps to adjust (a launch with every tap: those outside the
+        // image, subtracted from the total; a transposed phase: those inside,
+        // added up), and whether any lane has one (wave-uniform).
         zp = 0;
 #pragma unroll
-        for (int i = 0; i < FM; ++i) border[i] = false;
+        for (int i = 0; i < FM; ++i) {
+            border[i] = false;
+            tapmask[i] = 0;
+        }
         if (fl.affine) {
             zp = a.zx[t.nb];
+            const bool all_taps = a.ntaps == a.k * a.k;
 #pragma unroll
             for (int i = 0; i < FM; ++i) {
                 const int m = row0 + 16 * i + p;
                 const int ih0 = (t.gi0 + m / TW) * a.sa + a.bah, iw0 = (t.gj0 + m % TW) * a.sa + a.baw;
-                bool out = false;
+                uint64_t mk = 0;
                 for (int tp = 0; tp < a.ntaps; ++tp) {
                     const int ih = ih0 + a.dh[tp], iw = iw0 + a.dw[tp];
-                    out |= ih < 0 || ih >= a.h || iw < 0 || iw >= a.w;
+                    const bool inside = ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
+                    if (inside != all_taps) mk |= (uint64_t)1 << tp;
                 }
-                border[i] = __builtin_amdgcn_ballot_w64(valid[i] && out) != 0;
+                tapmask[i] = valid[i] ? mk : 0;
+                border[i] = __builtin_amdgcn_ballot_w64(tapmask[i] != 0) != 0;
             }
         }
     }
@@ -460,18 +475,16 @@ struct Epilogue {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) T[jj] = *reinterpret_cast<const v4i *>(full + 16 * jj);
         }
-        if (border[i] || !all_taps) {
-            const int m = row0 + 16 * i + p;
-            const int ih0 = (t.gi0 + m / TW) * a.sa + a.bah, iw0 = (t.gj0 + m % TW) * a.sa + a.baw;
-            for (int tp = 0; tp < a.ntaps; ++tp) {
-                const int ih = ih0 + a.dh[tp], iw = iw0 + a.dw[tp];
-                const bool inside = ih >= 0 && ih < a.h && iw >= 0 && iw < a.w;
-                if (inside != all_taps) {
-                    const int32_t *row = a.tapsum + (int64_t)a.wtap[tp] * a.cout_pad + cl0;
-                    const int sg = all_taps ? -1 : 1;
+        if (border[i]) {
+            const int sg = all_taps ? -1 : 1;
+            uint64_t mk = tapmask[i];
+            while (mk) {
+                const int tp = __builtin_ctzll(mk);
+                mk &= mk - 1;
+                const int wt = all_taps ? tp : a.wtap[tp];   // every tap: the table is the identity
+                const int32_t *row = a.tapsum + (int64_t)wt * a.cout_pad + cl0;
 #pragma unroll
-                    for (int jj = 0; jj < 4; ++jj) T[jj] += sg * *reinterpret_cast<const v4i *>(row + 16 * jj);
-                }
+                for (int jj = 0; jj < 4; ++jj) T[jj] += sg * *reinterpret_cast<const v4i *>(row + 16 * jj);
             }
         }
 #pragma unroll
@@ -567,6 +580,40 @@ struct Epilogue {
                     v[4 * jj + 2] = __builtin_fmaf((float)c4[2], t4[jj].z, b4[jj].z);
                     v[4 * jj + 3] = __builtin_fmaf((float)c4[3], t4[jj].w, b4[jj].w);
                 }
+            }
+            if (zpair) {
+                // v holds z / b: scale back (exact, a power of two)
+                const float bsc = (float)a.hblock;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) v[r] *= bsc;
+                if (i8) {
+                    uint32_t w[4];
+                    quant16(v, qs, qr, q_fast, w);
+                    if (valid[i]) {
+                        const int m = row0 + 16 * i + p;
+                        int8_t *yq = reinterpret_cast<int8_t *>(a.y) +
+                                     out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW) * a.cout + t.n0;
+#pragma unroll
+                        for (int jj = 0; jj < 4; ++jj) {
+                            const int cl = 64 * k + 16 * jj + 4 * q;
+                            if (t.n0 + cl < a.cout) *reinterpret_cast<uint32_t *>(yq + cl) = w[jj];
+                        }
+                    }
+                } else {
+                    // the maximum of |z| over the valid pixels and channels
+                    const bool all = full && blk_full;
+                    float mm = 0.0f;
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int ch = t.n0 + 64 * k + 16 * jj + 4 * q + r;
+                            const bool in = all || (valid[i] && ch < a.cout);
+                            mm = fmaxf(mm, in ? fabsf(v[4 * jj + r]) : 0.0f);
+                        }
+                    wave_m = fmaxf(wave_m, mm);
+                }
+                continue;
             }
             // bound on this lane's share of max |B_next y| (see above)
             float zmax = 0.0f;
@@ -1861,7 +1908,7 @@ hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
                         a, [&](auto e) { return launch_pipe<8, 32, 128, 5, decltype(e)>(a, st); });
                 case 192:
                     if (a.sa == 2 && a.so == 1 && a.k >= 4 && a.k <= 6)
-                        return with_epilogue<Epi<0, 64, 2>, Epi<0, 1, 2>, HATQ_HOT_EPILOGUES>(
+                        return with_epilogue<Epi<0, 64, 2>, Epi<0, 1, 2>, Epi<0, 0, 3>, HATQ_HOT_EPILOGUES>(
                             a, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st); });
                     return with_epilogue<HATQ_HOT_EPILOGUES>(
                         a, [&](auto e) { return launch_pipe<8, 32, 192, 5, decltype(e)>(a, st); });

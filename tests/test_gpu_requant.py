@@ -11,6 +11,10 @@ its dynamic scale.
   activation kernel computes from the stored F32 output with the same absmax
   (same fp32 butterfly, same rounding), and the absmax-only call matches the
   F32 call's fused absmax exactly.
+* A WH layer whose next operand uses the same blocks takes the next operand as
+  z, the accumulators dequantized before the restore (B_next y = z exactly,
+  Table I): scale and codes bit for bit against the oracle's z, and within the
+  code rule against the two-kernel path (whose two fp32 butterflies round).
 * A static scale (next_absmax = NULL) gives the oracle's codes for that scale.
 """
 import numpy as np
@@ -36,6 +40,13 @@ def _oracle_next(orc, r, next_b):
     return q_ref, s_ref
 
 
+def _paired(c, next_b):
+    """A WH layer whose next operand uses the same blocks: the next operand is
+    the accumulator-basis z (B_next y = z exactly), taken without butterflies."""
+    n, h, w, cin, cout, k, s, p, tr, op, form, hb = c
+    return form == "WH" and next_b == hb and hb > 1 and cout % hb == 0
+
+
 @pytest.mark.parametrize("c", CONV, ids=CONV_IDS)
 @pytest.mark.parametrize("next_b", [1, 64])
 def test_requant_codes(orc, c, next_b):
@@ -43,7 +54,11 @@ def test_requant_codes(orc, c, next_b):
     rng, wt, b, ref, layer = _layer(orc, c, 81)
     x = synth.heavy_tailed_activations(rng, (n, h, w, cin))
     r = orc.layer_forward(x, ref)
-    q_ref, s_ref = _oracle_next(orc, r, next_b)
+    paired = _paired(c, next_b)
+    if paired:
+        q_ref, s_ref = orc.quantize_symmetric(orc.wh_z(r.acc, r.sx, ref)[..., :cout])
+    else:
+        q_ref, s_ref = _oracle_next(orc, r, next_b)
     xq, sx = dev(r.xq), dev(r.sx)
     # pass 1: the absmax alone; pass 2: the codes
     nam = torch.full((n,), -1.0, device="cuda")
@@ -51,16 +66,27 @@ def test_requant_codes(orc, c, next_b):
                                absmax_only=True) is None
     yq, sq = hatq.hatq_conv_int8_requant(layer, xq, sx, next_b, next_absmax=nam)
     assert yq.shape == q_ref.shape and yq.dtype == torch.int8
-    assert_scale_ulp(host(sq), s_ref)
-    exact = form == "DH" and next_b == 1
-    assert_codes(host(yq), q_ref, exact=exact, what=f"requant codes next_b={next_b}")
-    # the two-kernel GPU path on the stored output: identical absmax, scale, codes
+    if paired:
+        # the same fp32 z on both sides: scale and codes bit for bit
+        assert np.array_equal(host(sq), s_ref)
+        assert_codes(host(yq), q_ref, exact=True, what=f"paired requant codes next_b={next_b}")
+    else:
+        assert_scale_ulp(host(sq), s_ref)
+        exact = form == "DH" and next_b == 1
+        assert_codes(host(yq), q_ref, exact=exact, what=f"requant codes next_b={next_b}")
+    # the two-kernel GPU path on the stored output: identical absmax, scale and
+    # codes (paired: the stored y goes through two fp32 butterflies, so within
+    # their rounding)
     nam2 = torch.full((n,), -1.0, device="cuda")
     y = hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=next_b, next_absmax=nam2)
-    assert torch.equal(nam, nam2)
     q2, s2 = hatq.hatq_fwht_quant_act(y, next_b, absmax=nam2)
-    assert torch.equal(sq, s2)
-    assert torch.equal(yq, q2)
+    if paired:
+        assert_scale_ulp(host(sq), host(s2), ulps=2)
+        assert_codes(host(yq), host(q2), what="paired requant vs two-kernel path")
+    else:
+        assert torch.equal(nam, nam2)
+        assert torch.equal(sq, s2)
+        assert torch.equal(yq, q2)
 
 
 @pytest.mark.parametrize("ci", [1, 2, 4, 5, 16], ids=[CONV_IDS[i] for i in (1, 2, 4, 5, 16)])

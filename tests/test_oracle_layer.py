@@ -230,3 +230,19 @@ def test_weight_preparation(orc, form):
             assert np.abs(qc).max() == 127
     if form == "DH":
         assert pw.w_scale[7] == 1.0 and not pw.wq[7].any()
+
+
+@pytest.mark.parametrize("name", ["k5s2_wh_b64", "rgb_wh_b64", "tconv_wh_b64", "k3_wh_m320"])
+def test_paired_transition_is_the_accumulator_basis(orc, name):
+    """Table I: a WH layer followed by a DH transform of the same blocks gives
+    B_next y = z, the dequantized accumulators before the restore (the two
+    transforms cancel), up to the fp32 rounding of y and of the transform."""
+    L = next(l for l in LAYERS if l[0] == name)
+    rng = np.random.default_rng(21)
+    x, wt, b = _make(rng, L)
+    pw = _prep(orc, L, wt, b)
+    r = orc.layer_forward(x, pw)
+    z = orc.wh_z(r.acc, r.sx, pw)[..., : pw.cout]
+    S = orc.activation_transform(r.y, pw.hblock)
+    assert np.abs(S - z).max() <= 2e-6 * np.abs(z).max()
+    assert np.abs(S - z).max() > 0 or pw.hblock == 1          # not the same arithmetic
