@@ -249,7 +249,8 @@ __device__ __forceinline__ uint32_t int_code_hi(int64_t w, int s, int64_t bias_m
 // Q = 1: I8 output (the next operand's codes, NB its transform block); Q = 2:
 // the same codes by the integer transition (mode 3); Q = 3: output from affine
 // activation codes (fixed variants: F32 with no next-operand absmax, NB = 0;
-// the generic one also I32).
+// the generic one also I32); Q = 4: the next operand's absmax alone (F32 mode
+// with no output).
 template <int WB_, int NB_, int Q_ = 0>
 struct Epi {
     static constexpr int WB = WB_, NB = NB_, Q = Q_;
@@ -265,8 +266,10 @@ bool epi_matches(const ConvArgs &a) {
         return (a.mode == kModeIntTransition) == (E::Q == 2) && (a.zx != nullptr) == (E::Q == 3);
     } else {
         if ((a.zx != nullptr) != (E::Q == 3)) return false;
-        if (E::Q == 3) return a.mode == 1 && (a.form == 1 ? a.hblock : 0) == E::WB && a.next_absmax == nullptr;
         const int wb = a.form == 1 ? a.hblock : 0;
+        if (E::Q == 3) return a.mode == 1 && wb == E::WB && a.next_absmax == nullptr;
+        if (E::Q == 4)
+            return a.mode == 1 && a.y == nullptr && a.next_absmax != nullptr && wb == E::WB && a.next_hblock == E::NB;
         if (E::Q) return a.mode == (E::Q == 2 ? kModeIntTransition : 2) && wb == E::WB && a.next_hblock == E::NB;
         const int nb = a.next_absmax != nullptr ? a.next_hblock : 0;
         return a.mode == 1 && wb == E::WB && nb == E::NB;
@@ -284,9 +287,10 @@ struct EpiFlags {
         iq = E::Q == 2;   // integer transition (its own variants, generic ones included)
         f32 = !iq && (generic ? a.mode != 0 : true);   // the fp32 arithmetic (F32 and I8 modes)
         wh = generic ? a.mode != 0 && a.form == 1 : WB != 0;
-        want_abs = !iq && (generic ? a.mode == 1 && a.next_absmax != nullptr && a.next_hblock > 0 : E::Q == 0 && NB != 0);
+        want_abs = !iq && (generic ? a.mode == 1 && a.next_absmax != nullptr && a.next_hblock > 0
+                                   : (E::Q == 0 || E::Q == 4) && NB != 0);
         i8 = !iq && (generic ? a.mode == 2 : E::Q == 1);
-        store = !i8 && !iq && a.y != nullptr;   // I32 / F32 values
+        store = E::Q != 4 && !i8 && !iq && a.y != nullptr;   // I32 / F32 values
     }
 };
 
@@ -1126,7 +1130,7 @@ template <int CS>
 hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
     if (a.cout_pad % 192 == 0) {
         if constexpr (CS == 3)
-            return with_epilogue<Epi<64, 64, 1>, Epi<64, 64, 2>, HATQ_HOT_EPILOGUES>(
+            return with_epilogue<Epi<64, 64, 1>, Epi<64, 64, 2>, Epi<64, 64, 4>, HATQ_HOT_EPILOGUES>(
                 a, [&](auto e) { return launch_rowrun<2, 64, 192, CS, decltype(e)>(a, st); });
         return with_epilogue<HATQ_GENERIC_EPILOGUES>(
             a, [&](auto e) { return launch_rowrun<2, 64, 192, CS, decltype(e)>(a, st); });
