@@ -3,9 +3,15 @@
 Flags: -O3, gfx950 only, no fast-math, no FP contraction (the epilogue uses
 explicit fma where the arithmetic contract says fma), fp32 denormals kept, and
 packed-FP32 instructions disabled.
+
+Every source compiles to an object of its own, in parallel; conv_i8.hip is
+compiled once per part of its dispatch (HATQ_CONV_PART), since its kernel
+instantiations take most of the build time. The objects are linked into one
+shared library.
 """
 from __future__ import annotations
 
+import concurrent.futures
 import os
 import subprocess
 import sys
@@ -15,6 +21,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhatq.so")
 SOURCES = ["api.cpp", "act_quant.hip", "conv_i8.hip", "weights.hip"]
+CONV_PARTS = 12         # HATQ_CONV_PART = 0 .. 11 in conv_i8.hip
+OBJ_DIR = os.path.join(ROOT, "_build", "hatq")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -30,19 +38,44 @@ def sources():
     return [os.path.join(CSRC, s) for s in SOURCES]
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, *sources(), "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+def _units():
+    """(source, extra flags, object) for every compilation."""
+    units = []
+    for src in sources():
+        base = os.path.splitext(os.path.basename(src))[0]
+        if base == "conv_i8":
+            for k in range(CONV_PARTS):
+                units.append((src, [f"-DHATQ_CONV_PART={k}"], os.path.join(OBJ_DIR, f"{base}.part{k}.o")))
+        else:
+            units.append((src, [], os.path.join(OBJ_DIR, base + ".o")))
+    return units
+
+
+# hipcc's host pass does not know the packed-fp32 feature and says so
+_NOISE = "'-packed-fp32-ops' is not a recognized feature"
+
+
+def _run(cmd):
     r = subprocess.run(cmd, capture_output=True, text=True)
-    # hipcc's host pass does not know the packed-fp32 feature and says so
-    noise = "'-packed-fp32-ops' is not a recognized feature"
-    err = "\n".join(l for l in r.stderr.splitlines() if noise not in l)
+    err = "\n".join(l for l in r.stderr.splitlines() if _NOISE not in l)
     if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{err}")
-    if err.strip() and verbose:
-        print(err, file=sys.stderr)
+        raise RuntimeError(f"hipcc failed ({r.returncode}): {' '.join(cmd)}\n{err}")
+    return err
+
+
+def build(verbose: bool = False, jobs: int = 0) -> str:
+    os.makedirs(OBJ_DIR, exist_ok=True)
+    compile_flags = [f for f in FLAGS if f != "-shared"]
+    cmds = [[HIPCC, *compile_flags, *extra, "-c", src, "-o", obj] for src, extra, obj in _units()]
+    jobs = jobs or max(1, min(len(cmds), len(os.sched_getaffinity(0))))
+    with concurrent.futures.ThreadPoolExecutor(max_workers=jobs) as pool:
+        for cmd, err in zip(cmds, pool.map(_run, cmds)):
+            if verbose:
+                print(" ".join(cmd), flush=True)
+                if err.strip():
+                    print(err, file=sys.stderr)
+    tmp = LIB + ".tmp"
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *[o for _, _, o in _units()], "-o", tmp])
     os.replace(tmp, LIB)
     return LIB
 

@@ -1898,38 +1898,130 @@ hipError_t launch_pipe(const ConvArgs &a, hipStream_t st) {
     return hipGetLastError();
 }
 
+// Launch with the first epilogue variant of Es that matches; *hit = false,
+// and nothing launched, if none does.
+template <typename... Es, typename L>
+hipError_t try_epilogue(const ConvArgs &a, bool *hit, L &&launch) {
+    hipError_t r = hipSuccess;
+    *hit = ((epi_matches<Es>(a) && (r = launch(Es{}), true)) || ...);
+    return r;
+}
+
 }  // namespace
 
-hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
-    if (clear_next && a.next_absmax && a.next_hblock > 0)
-        fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(a.next_absmax), a.n, 0u);
-    switch (a.cin_p <= 4 ? a.cin_p : 0) {
-        case 0:
-            switch (a.cout_pad) {
-                case 64: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
-                        a, [&](auto e) { return launch_pipe<8, 32, 64, 5, decltype(e)>(a, st); });
-                case 128: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
-                        a, [&](auto e) { return launch_pipe<8, 32, 128, 5, decltype(e)>(a, st); });
-                case 192:
-                    if (a.sa == 2 && a.so == 1 && a.k >= 4 && a.k <= 6)
-                        return with_epilogue<Epi<0, 64, 2>, Epi<0, 1, 2>, Epi<0, 0, 3>, HATQ_HOT_EPILOGUES>(
-                            a, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st); });
-                    return with_epilogue<HATQ_HOT_EPILOGUES>(
-                        a, [&](auto e) { return launch_pipe<8, 32, 192, 5, decltype(e)>(a, st); });
-                case 256: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
-                        a, [&](auto e) { return launch_pipe<4, 32, 256, 5, decltype(e)>(a, st); });
-                case 320:
-                    return with_epilogue<HATQ_HOT_EPILOGUES>(
-                        a, [&](auto e) { return launch_pipe<4, 32, 320, 5, decltype(e)>(a, st); });
-                default: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
-                        a, [&](auto e) { return launch_pipe<8, 32, 64, 5, decltype(e)>(a, st); });
-            }
-        case 1: return a.rowrun ? launch_rowrun_n<1>(a, st) : launch_gather_n<1>(a, st);
-        case 2: return a.rowrun ? launch_rowrun_n<2>(a, st) : launch_gather_n<2>(a, st);
-        case 3: return a.rowrun ? launch_rowrun_n<3>(a, st) : launch_gather_n<3>(a, st);
-        case 4: return a.rowrun ? launch_rowrun_n<4>(a, st) : launch_gather_n<4>(a, st);
+// The dispatch is spread over several compilations of this file so that the
+// kernel instantiations build in parallel: HATQ_CONV_PART = k compiles part k
+// only (0 is the dispatcher), and without it every part is compiled.
+#ifndef HATQ_CONV_PART
+#define HATQ_CONV_PART -1
+#endif
+#define HATQ_PART(k) (HATQ_CONV_PART < 0 || HATQ_CONV_PART == (k))
+
+// 192 output channels, 5x5 (4x4, 6x6) stride 2: the window kernels.  The
+// variant list is split in two; the order of the combined list decides.
+hipError_t conv_part_halo192_a(const ConvArgs &a, bool *hit, hipStream_t st);
+hipError_t conv_part_halo192_b(const ConvArgs &a, hipStream_t st);
+hipError_t conv_part_pipe192(const ConvArgs &a, hipStream_t st);
+hipError_t conv_part_pipe320(const ConvArgs &a, hipStream_t st);
+hipError_t conv_part_pipe_other(const ConvArgs &a, hipStream_t st);
+hipError_t conv_part_rowrun3(const ConvArgs &a, hipStream_t st);
+hipError_t conv_part_rowrun_other(const ConvArgs &a, hipStream_t st);
+hipError_t conv_part_gather1(const ConvArgs &a, hipStream_t st);
+hipError_t conv_part_gather2(const ConvArgs &a, hipStream_t st);
+hipError_t conv_part_gather3(const ConvArgs &a, hipStream_t st);
+hipError_t conv_part_gather4(const ConvArgs &a, hipStream_t st);
+
+#if HATQ_PART(1)
+hipError_t conv_part_halo192_a(const ConvArgs &a, bool *hit, hipStream_t st) {
+    return try_epilogue<Epi<0, 64, 2>, Epi<0, 1, 2>, Epi<0, 0, 3>, Epi<0, 64>, Epi<0, 1>, Epi<0, 0>>(
+        a, hit, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st); });
+}
+#endif
+#if HATQ_PART(2)
+hipError_t conv_part_halo192_b(const ConvArgs &a, hipStream_t st) {
+    return with_epilogue<Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_GENERIC_EPILOGUES>(
+        a, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st); });
+}
+#endif
+#if HATQ_PART(3)
+hipError_t conv_part_pipe192(const ConvArgs &a, hipStream_t st) {
+    return with_epilogue<HATQ_HOT_EPILOGUES>(
+        a, [&](auto e) { return launch_pipe<8, 32, 192, 5, decltype(e)>(a, st); });
+}
+#endif
+#if HATQ_PART(4)
+hipError_t conv_part_pipe320(const ConvArgs &a, hipStream_t st) {
+    return with_epilogue<HATQ_HOT_EPILOGUES>(
+        a, [&](auto e) { return launch_pipe<4, 32, 320, 5, decltype(e)>(a, st); });
+}
+#endif
+#if HATQ_PART(5)
+hipError_t conv_part_pipe_other(const ConvArgs &a, hipStream_t st) {
+    switch (a.cout_pad) {
+        case 128: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+                a, [&](auto e) { return launch_pipe<8, 32, 128, 5, decltype(e)>(a, st); });
+        case 256: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+                a, [&](auto e) { return launch_pipe<4, 32, 256, 5, decltype(e)>(a, st); });
+        default: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+                a, [&](auto e) { return launch_pipe<8, 32, 64, 5, decltype(e)>(a, st); });
+    }
+}
+#endif
+#if HATQ_PART(6)
+hipError_t conv_part_rowrun3(const ConvArgs &a, hipStream_t st) { return launch_rowrun_n<3>(a, st); }
+#endif
+#if HATQ_PART(7)
+hipError_t conv_part_rowrun_other(const ConvArgs &a, hipStream_t st) {
+    switch (a.cin_p) {
+        case 1: return launch_rowrun_n<1>(a, st);
+        case 2: return launch_rowrun_n<2>(a, st);
+        case 4: return launch_rowrun_n<4>(a, st);
         default: return hipErrorInvalidValue;
     }
 }
+#endif
+// One part per small channel count for the gather kernel.
+#define HATQ_GATHER_PART(CS)                                                                 \
+    hipError_t conv_part_gather##CS(const ConvArgs &a, hipStream_t st) { return launch_gather_n<CS>(a, st); }
+#if HATQ_PART(8)
+HATQ_GATHER_PART(1)
+#endif
+#if HATQ_PART(9)
+HATQ_GATHER_PART(2)
+#endif
+#if HATQ_PART(10)
+HATQ_GATHER_PART(3)
+#endif
+#if HATQ_PART(11)
+HATQ_GATHER_PART(4)
+#endif
+
+#if HATQ_PART(0)
+hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
+    if (clear_next && a.next_absmax && a.next_hblock > 0)
+        fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(a.next_absmax), a.n, 0u);
+    if (a.cin_p <= 4) {
+        if (a.cin_p < 1) return hipErrorInvalidValue;
+        if (a.rowrun) return a.cin_p == 3 ? conv_part_rowrun3(a, st) : conv_part_rowrun_other(a, st);
+        switch (a.cin_p) {
+            case 1: return conv_part_gather1(a, st);
+            case 2: return conv_part_gather2(a, st);
+            case 3: return conv_part_gather3(a, st);
+            default: return conv_part_gather4(a, st);
+        }
+    }
+    switch (a.cout_pad) {
+        case 192:
+            if (a.sa == 2 && a.so == 1 && a.k >= 4 && a.k <= 6) {
+                bool hit = false;
+                const hipError_t r = conv_part_halo192_a(a, &hit, st);
+                return hit ? r : conv_part_halo192_b(a, st);
+            }
+            return conv_part_pipe192(a, st);
+        case 320: return conv_part_pipe320(a, st);
+        default: return conv_part_pipe_other(a, st);
+    }
+}
+#endif
 
 }  // namespace hatq
