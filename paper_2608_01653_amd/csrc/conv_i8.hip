@@ -68,25 +68,46 @@ __device__ __forceinline__ int64_t out_pixel(const ConvArgs &a, int nb, int gi, 
 // after, as the operator is defined.
 // In the integer transition (mode 3) the two slots carry the bits of the
 // fixed-point multiplier M_c and of the integer bias b_int,c instead.
-__device__ __forceinline__ void column_factor(const ConvArgs &a, float sxv, int c, float &t, float &b) {
+// The per-channel inputs of column c (scale and bias, or the integer
+// transition's two table entries as bits) and the factors formed from them.
+__device__ __forceinline__ void column_raw(const ConvArgs &a, int c, float &r0, float &r1) {
     if (a.mode == kModeIntTransition) {
-        t = __int_as_float(a.rq_table[c]);
-        b = __int_as_float(a.rq_table[a.cout_pad + c]);
-        return;
-    }
-    if (a.form == 1) {
-        const float inv_b = 1.0f / (float)a.hblock;
-        t = (sxv * a.w_scale[c]) * inv_b;
-        b = a.bias[c] * inv_b;
+        r0 = __int_as_float(a.rq_table[c]);
+        r1 = __int_as_float(a.rq_table[a.cout_pad + c]);
     } else {
-        t = (sxv * a.w_scale[c]) / (float)a.hblock;   // exact scaling for a power of two
-        b = a.bias[c];
+        r0 = a.w_scale[c];
+        r1 = a.bias[c];
     }
+}
+__device__ __forceinline__ void column_from_raw(const ConvArgs &a, float sxv, float r0, float r1, float &t, float &b) {
+    if (a.mode == kModeIntTransition) {
+        t = r0;
+        b = r1;
+    } else if (a.form == 1) {
+        const float inv_b = 1.0f / (float)a.hblock;
+        t = (sxv * r0) * inv_b;
+        b = r1 * inv_b;
+    } else {
+        t = (sxv * r0) / (float)a.hblock;   // exact scaling for a power of two
+        b = r1;
+    }
+}
+__device__ __forceinline__ void column_factor(const ConvArgs &a, float sxv, int c, float &t, float &b) {
+    float r0, r1;
+    column_raw(a, c, r0, r1);
+    column_from_raw(a, sxv, r0, r1, t, b);
 }
 
 // The tile's activation scale (the integer transition has none).
 __device__ __forceinline__ float tile_sx(const ConvArgs &a, int nb) {
     return a.mode == kModeIntTransition ? 0.0f : a.sx[nb];
+}
+// The same through the scalar unit (nb is wave-uniform): a scalar load is not
+// counted by vmcnt, so it does not wait for the LDS DMAs and stores in flight.
+__device__ __forceinline__ float tile_sx_uniform(const ConvArgs &a, int nb) {
+    if (a.mode == kModeIntTransition) return 0.0f;
+    const __attribute__((address_space(4))) float *p = (const __attribute__((address_space(4))) float *)a.sx;
+    return p[__builtin_amdgcn_readfirstlane(nb)];
 }
 
 // Written by the whole block.
@@ -707,13 +728,12 @@ __device__ __forceinline__ void epilogue_regs(const ConvArgs &a, const v4i (&acc
 
 // Block index -> tile, XCD aware: blocks bid, bid+8, ... run on one XCD; each
 // XCD gets a contiguous range of tiles so neighbouring tiles (which share input
-// rows) share its L2.
-__device__ __forceinline__ int xcd_logical_tile() {
-    const int nt = gridDim.x;
-    const int bid = blockIdx.x;
+// rows) share its L2.  xcd_tile maps a virtual block bid of a grid of nt.
+__device__ __forceinline__ int xcd_tile(int bid, int nt) {
     const int xcd = bid & 7, q8 = nt >> 3, rmd = nt & 7;
     return xcd * q8 + (xcd < rmd ? xcd : rmd) + (bid >> 3);
 }
+__device__ __forceinline__ int xcd_logical_tile() { return xcd_tile(blockIdx.x, gridDim.x); }
 
 // ---------------------------------------------------------------------------
 // Row-run path (regular convolution, cin_p <= 4, k*cin_p <= 16, k <= 8,
@@ -1198,6 +1218,8 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | 0x70 | 0xF00 | ((N >> 4) << 14));
 }
 // The same, and this wave's LDS accesses done (lgkmcnt 0).
+// This wave's LDS accesses done (lgkmcnt 0), memory operations left in flight.
+__device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xF | 0x70 | (3 << 14)); }
 template <int N>
 __device__ __forceinline__ void wait_vmcnt_lds() {
     static_assert(N >= 0 && N < 64, "vmcnt");
@@ -1635,6 +1657,16 @@ __device__ __forceinline__ void unroll(F &&f) {
 // refills are issued every chunk (the odd-row refill after the last chunk
 // reads zeros into rows no later step uses), and the even half of chunk 0 is
 // loaded at the first step like every other chunk's.
+//
+// Persistent: the grid holds one block per CU and block b walks the logical
+// tiles b, b + G, b + 2G, ... (G = gridDim.x, a multiple of 8, so each virtual
+// block keeps the XCD of the real one and each XCD a contiguous tile range).
+// The refills issued during a tile's last chunk (odd window rows and the
+// first weight steps of chunk 0) fetch the next tile's data instead of zeros,
+// so a tile's prologue overlaps the previous tile's last steps and epilogue.
+// The weights and the per-channel scale and bias are the same for every tile
+// (one column tile: BN = cout_pad); the raw scale and bias are staged once and
+// each tile's column factors are formed from them and the sample's s_x.
 template <int BN, typename E>
 __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvArgs a) {
     using G = HaloGeom;
@@ -1658,29 +1690,30 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     static_assert(2 * (TH - 1) + K <= 2 * G::HR && 2 * (TW - 1) + K <= 2 * G::HCC, "window size");
     // one LDS object (window halves, weight ring, the tile's column factors):
     // a second one makes the compiler wait for every LDS DMA before each read
-    __shared__ __attribute__((aligned(1024))) int8_t lds[2 * G::HALF_BYTES + SLOTS * B_BYTES + 2 * BN * 4];
+    __shared__ __attribute__((aligned(1024))) int8_t lds[2 * G::HALF_BYTES + SLOTS * B_BYTES + 4 * BN * 4];
     int8_t *const halo = lds;
     int8_t *const bring = lds + RING_BASE;
     float *const s_col = reinterpret_cast<float *>(lds + RING_BASE + SLOTS * B_BYTES);
+    float *const s_raw = s_col + 2 * BN;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const Tile tile = block_tile(a, xcd_logical_tile(), TH, TW, BN);
+    const int ntiles = a.n * a.tiles_h * a.tiles_w;   // one column tile
+    int v = blockIdx.x;
+    Tile tile = block_tile(a, xcd_tile(v, ntiles), TH, TW, BN);
     const int cin_p = a.cin_p;
     const int nchunks = cin_p >> 6;
     const int rows_used = 2 * (TH - 1) + K, cols_used = 2 * (TW - 1) + K;
-    const int ih0 = tile.gi0 * 2 + a.bah, iw0 = tile.gj0 * 2 + a.baw;
 
     const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int8_t *>(a.xq), (short)0, (int)((int64_t)a.n * a.h * a.w * cin_p), 0x00020000);
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int8_t *>(a.wp), (short)0, (int)((int64_t)a.cout_pad * a.pack_stride), 0x00020000);
 
-    // window DMA offsets (as in conv_halo_kernel)
-    uint32_t h_off[2][HB];
-#pragma unroll
-    for (int hp = 0; hp < 2; ++hp)
+    // window DMA offsets of parity half hp of tile t (as in conv_halo_kernel)
+    auto window_offsets = [&](const Tile &t, int hp, uint32_t(&o)[HB]) {
+        const int ih0 = t.gi0 * 2 + a.bah, iw0 = t.gj0 * 2 + a.baw;
 #pragma unroll
         for (int j = 0; j < HB; ++j) {
             const int f = 16 * halo_block(wave, j, W_BLK) + (lane >> 2);
@@ -1691,15 +1724,20 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
             const int ih = ih0 + row, iw = iw0 + col;
             const bool in = f < G::RECS && row < rows_used && col < cols_used && (unsigned)ih < (unsigned)a.h &&
                             (unsigned)iw < (unsigned)a.w;
-            h_off[hp][j] = in ? (uint32_t)(((tile.nb * a.h + ih) * a.w + iw) * cin_p + 16 * g) : kOobOffset;
+            o[j] = in ? (uint32_t)(((t.nb * a.h + ih) * a.w + iw) * cin_p + 16 * g) : kOobOffset;
         }
-    // refill of window half hp with chunk c; zero_fill: the same number of
-    // DMAs reading zeros
-    auto burst = [&](int hp, int chunk) {
+    };
+    uint32_t h_off[2][HB];
+    window_offsets(tile, 0, h_off[0]);
+    window_offsets(tile, 1, h_off[1]);
+    // refill of window half hp from the offsets o with chunk c; zero_fill: the
+    // same number of DMAs reading zeros
+    auto burst_from = [&](int hp, const uint32_t(&o)[HB], int chunk) {
         int8_t *dst = halo + hp * G::HALF_BYTES;
 #pragma unroll
-        for (int j = 0; j < HB; ++j) dma16s(rx, dst + 1024 * halo_block(wave, j, W_BLK), h_off[hp][j], (uint32_t)chunk * 64u);
+        for (int j = 0; j < HB; ++j) dma16s(rx, dst + 1024 * halo_block(wave, j, W_BLK), o[j], (uint32_t)chunk * 64u);
     };
+    auto burst = [&](int hp, int chunk) { burst_from(hp, h_off[hp], chunk); };
     auto zero_fill = [&](int hp) {
         int8_t *dst = halo + hp * G::HALF_BYTES;
 #pragma unroll
@@ -1763,10 +1801,6 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     };
 
     v4i acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
     constexpr int RING = 4;
     static_assert(FN % RING == 0 && 2 * FM <= FN, "ring");
@@ -1777,18 +1811,31 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     static_assert(SLOTS - 1 <= NTAP, "prologue within chunk 0");
     burst(1, 0);
     unroll<SLOTS - 1>([&](auto Jc) { issue_b(Jc, 0u); });
-    // the epilogue's column factors, while the first DMAs are in flight
-    column_factors<BN>(a, tile, s_col, s_col + BN);
+    // the raw per-channel scale and bias, while the first DMAs are in flight
+    for (int c = tid; c < BN; c += kHaloThreads) column_raw(a, tile.n0 + c, s_raw[c], s_raw[BN + c]);
     wait_vmcnt_lds<(SLOTS - 2) * PER>();
     __builtin_amdgcn_s_barrier();
+
+  for (;;) {
+    // step 0's fragments (odd window rows and weight step 0 of chunk 0 landed
+    // and were published by the last barrier: the prologue's, or the last
+    // step's of the previous tile, which prefetched the same values)
     fa0[0] = afrag(std::integral_constant<int, 0>{}, 0);
     fa0[1] = afrag(std::integral_constant<int, 0>{}, 1);
 #pragma unroll
     for (int r = 0; r < RING - 1; ++r) ring[r] = bfrag(std::integral_constant<int, 0>{}, r);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
+    const bool first_tile = v == (int)blockIdx.x;
     for (int c = 0; c < nchunks; ++c) {
         const uint32_t coff = (uint32_t)c * cp64, coff1 = coff + cp64;
         const bool more = c + 1 < nchunks;
+        // the block's next tile, if any: the refills of the last chunk fetch
+        // its odd window rows and first weight steps
+        const bool has_next = v + (int)gridDim.x < ntiles;
         unroll<NTAP>([&](auto Jc) {
             constexpr int J = decltype(Jc)::value;
             v4i(&acur)[FM] = (J & 1) ? fa1 : fa0;
@@ -1796,20 +1843,35 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
             // weight step J+1 (and the window halves read by steps J, J+1)
             // landed: all but the last two weight steps, plus a refill issued
             // in either of the two previous steps
-            if constexpr (J == 1 || J == 2 || J == NODD + 1 || J == NODD + 2)
+            // (steps 0-2 of a block's later tiles read data that was complete
+            // before the previous epilogue's stores: no wait, so the stores
+            // drain meanwhile; step 3's data comes after them)
+            if constexpr (J < 3) {
+                if (c != 0 || first_tile) {
+                    if constexpr (J == 1 || J == 2) wait_vmcnt<(SLOTS - 3) * PER + HB>();
+                    else wait_vmcnt<(SLOTS - 3) * PER>();
+                }
+            } else if constexpr (J == NODD + 1 || J == NODD + 2) {
                 wait_vmcnt<(SLOTS - 3) * PER + HB>();
-            else
+            } else {
                 wait_vmcnt<(SLOTS - 3) * PER>();
+            }
             __builtin_amdgcn_s_barrier();
             if constexpr (J == 0) burst(0, c);   // even rows of this chunk
-            if constexpr (J == NODD) {          // odd rows of the next chunk
-                if (more) burst(1, c + 1);
-                else zero_fill(1);
+            if constexpr (J == NODD) {          // odd rows of the next chunk (or tile)
+                if (more) {
+                    burst(1, c + 1);
+                } else if (has_next) {
+                    window_offsets(block_tile(a, xcd_tile(v + (int)gridDim.x, ntiles), TH, TW, BN), 1, h_off[1]);
+                    burst(1, 0);
+                } else {
+                    zero_fill(1);
+                }
             }
             if constexpr (J + SLOTS - 1 < NTAP) {
                 issue_b(std::integral_constant<int, J + SLOTS - 1>{}, coff);
             } else {
-                if (more) issue_b(std::integral_constant<int, J + SLOTS - 1 - NTAP>{}, coff1);
+                if (more || has_next) issue_b(std::integral_constant<int, J + SLOTS - 1 - NTAP>{}, more ? coff1 : 0u);
                 else issue_zero(std::integral_constant<int, J + SLOTS - 1 - NTAP>{});
             }
 #pragma unroll
@@ -1838,8 +1900,44 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
 #pragma unroll
         for (int i = 0; i < FM; ++i) fa0[i] = fa1[i];
     }
+    // this tile's column factors (every wave finished the previous epilogue
+    // many barriers ago); the DMAs of the next tile stay in flight
+    const float sxv = tile_sx_uniform(a, tile.nb);
+    for (int c = tid; c < BN; c += kHaloThreads) column_from_raw(a, sxv, s_raw[c], s_raw[BN + c], s_col[c], s_col[BN + c]);
+    wait_lds();
+    __builtin_amdgcn_s_barrier();
+    // the next tile's DMAs (its odd window rows, weight steps 0-3) complete
+    // before this wave issues stores: they are then not counted behind them
+    wait_vmcnt<0>();
+    {
+        // the epilogue reads the arguments afresh each tile (scalar loads from
+        // the kernel argument segment, through a pointer the compiler cannot
+        // see through): hoisted out of the tile loop they would stay live
+        // through the main loop and spill
+        const __attribute__((address_space(4))) ConvArgs *kargs =
+            (const __attribute__((address_space(4))) ConvArgs *)__builtin_amdgcn_kernarg_segment_ptr();
+        asm volatile("" : "+s"(kargs));
+        // the same for the lane-derived addresses and masks
+        int elane = lane;
+        asm volatile("" : "+v"(elane));
+        epilogue_regs<TW, FM, FN, E>(*(const ConvArgs *)kargs, acc, tile, wave * TM, elane, s_col, s_col + BN);
+    }
+    v += gridDim.x;
+    if (v >= ntiles) break;
+    // h_off[1] already holds the new tile's odd-row offsets
+    tile = block_tile(a, xcd_tile(v, ntiles), TH, TW, BN);
+    window_offsets(tile, 0, h_off[0]);
+  }
     wait_vmcnt<0>();   // no DMA may still be writing LDS when the block ends
-    epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, s_col, s_col + BN);
+}
+
+// Blocks of a persistent grid: the CU count of the current device rounded
+// down to a multiple of 8 (so a virtual block keeps its XCD), or 0 if unknown.
+int persistent_blocks() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    return cus >= 8 ? cus & ~7 : 0;
 }
 
 // The arguments of the launch over samples [s0, s0 + gn) of a.
@@ -1869,13 +1967,20 @@ hipError_t launch_halo(const ConvArgs &a, hipStream_t st) {
     if (group < 1) return hipErrorInvalidValue;
     if ((int64_t)a.cout_pad * a.pack_stride >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     if (a.sa != 2 || a.so != 1 || a.k < 4 || a.k > 6 || a.cin_p % 64) return hipErrorInvalidValue;
+    const int persist = persistent_blocks();
     for (int64_t s0 = 0; s0 < a.n; s0 += group) {
         const int gn = (int)(a.n - s0 < group ? a.n - s0 : group);
         ConvArgs b = sample_group(a, s0, gn);
         const int64_t tiles = set_tiles(b, HaloGeom::TH, HaloGeom::TW, BN);
         if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-        if (a.k == 5) conv_halo5_kernel<BN, E><<<(unsigned)tiles, kHaloThreads, 0, st>>>(b);
-        else conv_halo_kernel<BN, STAGES, E><<<(unsigned)tiles, kHaloThreads, 0, st>>>(b);
+        if (a.k == 5) {
+            // persistent: one block per CU (a multiple of 8), each walking tiles
+            if (b.tiles_n != 1) return hipErrorInvalidValue;
+            const int64_t grid = persist > 0 && persist < tiles ? persist : tiles;
+            conv_halo5_kernel<BN, E><<<(unsigned)grid, kHaloThreads, 0, st>>>(b);
+        } else {
+            conv_halo_kernel<BN, STAGES, E><<<(unsigned)tiles, kHaloThreads, 0, st>>>(b);
+        }
     }
     return hipGetLastError();
 }

@@ -168,6 +168,8 @@ CONV = [  # (n, h, w, cin, cout, k, stride, pad, transposed, out_pad, form, hblo
     (1, 30, 70, 192, 192, 4, 2, 1, False, 0, "DH", 64),   # LDS window path, k = 4
     (1, 26, 40, 128, 192, 6, 2, 2, False, 0, "WH", 64),   # LDS window path, k = 6, two chunks
     (2, 20, 21, 64, 192, 5, 2, 2, False, 0, "DH", 64),    # LDS window path, one chunk
+    (150, 18, 18, 192, 192, 5, 2, 2, False, 0, "DH", 64), # 300 ragged tiles: blocks walk several, across samples
+    (140, 17, 19, 192, 192, 5, 2, 2, False, 0, "WH", 64), # the same, WH
 ]
 CONV_IDS = [f"n{c[0]}-{c[1]}x{c[2]}-{c[3]}to{c[4]}-k{c[5]}s{c[6]}-{c[10]}{'-T' if c[8] else ''}" for c in CONV]
 
