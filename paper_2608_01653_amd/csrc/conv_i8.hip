@@ -1672,6 +1672,7 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     using G = HaloGeom;
     constexpr int K = 5, NTAP = K * K, NODD = (K >> 1) * K, SLOTS = 5;
     static_assert(NTAP % SLOTS == 0, "ring slot of a step is fixed within a chunk");
+    static_assert(NTAP % 2 == 1 && NODD % 2 == 0 && SLOTS == 5, "barrier schedule");
     constexpr int TH = G::TH, TW = G::TW;
     constexpr int BM = TH * TW;
     constexpr int TM = BM / kHaloWaves;
@@ -1836,43 +1837,63 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
         // the block's next tile, if any: the refills of the last chunk fetch
         // its odd window rows and first weight steps
         const bool has_next = v + (int)gridDim.x < ntiles;
+        // weight step S of this chunk (S < NTAP) or S - NTAP of the next chunk
+        // (or tile), zeros past the last
+        auto issue_step = [&](auto Sc) {
+            constexpr int S = decltype(Sc)::value;
+            if constexpr (S < NTAP) {
+                issue_b(std::integral_constant<int, S>{}, coff);
+            } else {
+                if (more || has_next) issue_b(std::integral_constant<int, S - NTAP>{}, more ? coff1 : 0u);
+                else issue_zero(std::integral_constant<int, S - NTAP>{});
+            }
+        };
         unroll<NTAP>([&](auto Jc) {
             constexpr int J = decltype(Jc)::value;
             v4i(&acur)[FM] = (J & 1) ? fa1 : fa0;
             v4i(&anext)[FM] = (J & 1) ? fa0 : fa1;
-            // weight step J+1 (and the window halves read by steps J, J+1)
-            // landed: all but the last two weight steps, plus a refill issued
-            // in either of the two previous steps
-            // (steps 0-2 of a block's later tiles read data that was complete
-            // before the previous epilogue's stores: no wait, so the stores
-            // drain meanwhile; step 3's data comes after them)
-            if constexpr (J < 3) {
-                if (c != 0 || first_tile) {
-                    if constexpr (J == 1 || J == 2) wait_vmcnt<(SLOTS - 3) * PER + HB>();
-                    else wait_vmcnt<(SLOTS - 3) * PER>();
-                }
-            } else if constexpr (J == NODD + 1 || J == NODD + 2) {
-                wait_vmcnt<(SLOTS - 3) * PER + HB>();
-            } else {
-                wait_vmcnt<(SLOTS - 3) * PER>();
-            }
-            __builtin_amdgcn_s_barrier();
-            if constexpr (J == 0) burst(0, c);   // even rows of this chunk
-            if constexpr (J == NODD) {          // odd rows of the next chunk (or tile)
-                if (more) {
-                    burst(1, c + 1);
-                } else if (has_next) {
-                    window_offsets(block_tile(a, xcd_tile(v + (int)gridDim.x, ntiles), TH, TW, BN), 1, h_off[1]);
-                    burst(1, 0);
+            // One barrier per two steps (at even J; steps 24 and 0 of the
+            // next chunk both have one, as a chunk has an odd number of steps).
+            // At a barrier every wave's DMAs of the weight steps read before
+            // the next barrier (up to J + 2, prefetches included; up to J + 1
+            // at J = 24) have landed; then the weight steps up to J + 4 are
+            // issued, whose slots were last read before this barrier.  A
+            // window refill is issued after the weights of its barrier, so
+            // the next barrier's wait may leave it in flight.
+            if constexpr ((J & 1) == 0) {
+                if constexpr (J == 0) {
+                    // a block's later tiles: the data of steps 0-2 was complete
+                    // before the previous epilogue's stores (no wait, so the
+                    // stores drain meanwhile)
+                    if (c != 0 || first_tile) wait_vmcnt<PER>();
+                } else if constexpr (J == 2 || J == NODD + 2) {
+                    wait_vmcnt<HB>();
+                } else if constexpr (J == NTAP - 1) {
+                    wait_vmcnt<PER>();
                 } else {
-                    zero_fill(1);
+                    wait_vmcnt<0>();
                 }
-            }
-            if constexpr (J + SLOTS - 1 < NTAP) {
-                issue_b(std::integral_constant<int, J + SLOTS - 1>{}, coff);
-            } else {
-                if (more || has_next) issue_b(std::integral_constant<int, J + SLOTS - 1 - NTAP>{}, more ? coff1 : 0u);
-                else issue_zero(std::integral_constant<int, J + SLOTS - 1 - NTAP>{});
+                __builtin_amdgcn_s_barrier();
+                if constexpr (J == 0) {
+                    issue_step(std::integral_constant<int, 4>{});
+                } else if constexpr (J == NTAP - 1) {
+                    issue_step(std::integral_constant<int, NTAP + 2>{});
+                    issue_step(std::integral_constant<int, NTAP + 3>{});
+                } else {
+                    issue_step(std::integral_constant<int, J + 3>{});
+                    issue_step(std::integral_constant<int, J + 4>{});
+                }
+                if constexpr (J == 0) burst(0, c);   // even rows of this chunk
+                if constexpr (J == NODD) {          // odd rows of the next chunk (or tile)
+                    if (more) {
+                        burst(1, c + 1);
+                    } else if (has_next) {
+                        window_offsets(block_tile(a, xcd_tile(v + (int)gridDim.x, ntiles), TH, TW, BN), 1, h_off[1]);
+                        burst(1, 0);
+                    } else {
+                        zero_fill(1);
+                    }
+                }
             }
 #pragma unroll
             for (int j = 0; j < FN; ++j) {
