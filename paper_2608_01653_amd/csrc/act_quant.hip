@@ -92,6 +92,7 @@ __device__ __forceinline__ void quant_store_item(const float (&vin)[4 * ItemShap
                                                  int64_t E, int t, float s, float r, bool fast_ok, float sigma) {
     constexpr int R = ItemShape<B>::R;
     constexpr int I = ItemShape<B>::I;
+    static_assert(R % 4 == 0, "groups of four words");
     const float rs = sigma * r;
     uint32_t u[4 * R];
     bool near = !fast_ok;
@@ -111,10 +112,36 @@ __device__ __forceinline__ void quant_store_item(const float (&vin)[4 * ItemShap
         }
     }
     const bool full = base + I <= E;
+    if (full) {
+        // Word i of lane t holds channels 16i + 4t .. +3.  A 4 x 4 transpose of
+        // words inside the quad (two DPP swap stages) gives lane t channels
+        // 64g + 16t .. +15 of each group g of four words, so every lane stores
+        // 16 contiguous bytes and the wave 1 KB per group.
+#pragma unroll
+        for (int g = 0; g < R / 4; ++g) {
+            int w[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int k = 4 * (4 * g + i);
+                w[i] = (int)pack_low_bytes(u[k], u[k + 1], u[k + 2], u[k + 3]);
+            }
+            int x[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) x[i] = __builtin_amdgcn_mov_dpp(w[i ^ 1], 0xB1, 0xF, 0xF, true);   // lane ^ 1
+#pragma unroll
+            for (int i = 0; i < 4; ++i) w[i] = ((t ^ i) & 1) ? x[i] : w[i];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) x[i] = __builtin_amdgcn_mov_dpp(w[i ^ 2], 0x4E, 0xF, 0xF, true);   // lane ^ 2
+#pragma unroll
+            for (int i = 0; i < 4; ++i) w[i] = ((t ^ i) & 2) ? x[i] : w[i];
+            *reinterpret_cast<int4 *>(qs + base + 64 * g + 16 * t) = make_int4(w[0], w[1], w[2], w[3]);
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < R; ++i) {
         const int64_t off = base + 16 * i + 4 * t;
-        if (full || off < E)
+        if (off < E)
             *reinterpret_cast<uint32_t *>(qs + off) = pack_low_bytes(u[4 * i], u[4 * i + 1], u[4 * i + 2], u[4 * i + 3]);
     }
 }
