@@ -9,8 +9,10 @@ the known copy size to what each counter reads scales the bench's counters to
 bytes.  Launches are identified by their order within one step of the
 four-layer stack: layer 1 runs the row-run convolution (an absmax pass, then the
 requantizing pass that writes layer 2's codes), so the first window
-convolution after a row-run launch is layer 2's convolution and the first
-``quant_kernel<64>`` after it is layer 3's quantization.  The output JSON
+convolution with the F32 epilogue that also forms the next blocks-of-64 absmax
+(``Epi<0, 64, 0>``; the integer stack's layer 2 uses another variant) after a
+row-run launch is layer 2's convolution and the first ``quant_kernel<64>`` after
+it is layer 3's quantization.  The output JSON
 carries a hash of the kernel sources; bench.py reports the traffic only while
 the sources are unchanged.
 """
@@ -52,7 +54,7 @@ def per_launch(d, factor):
         v = float(r["Counter_Value"]) * factor * 1024
         if "conv_rowrun_kernel" in name:
             want_c = True
-        elif "conv_halo5_kernel<192" in name and want_c:
+        elif "conv_halo5_kernel<192" in name and "Epi<0, 64, 0>" in name and want_c:
             conv.append(v)
             want_c = False
             want_q = True
