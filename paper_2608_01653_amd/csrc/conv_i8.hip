@@ -578,11 +578,19 @@ struct Epilogue {
         const bool f32 = fl.f32, wh = fl.wh, want_abs = fl.want_abs, i8 = fl.i8, store = fl.store;
         float4 t4[4], b4[4];
         if (f32) {
+            // zpair: the next operand is z itself, so the factors carry no 1/b
+            // (t and b~ times b: exact, a power of two), and
+            // fma(acc, t, b~) equals fma(acc, t/b, b~/b) * b
+            const float bsc = zpair ? (float)a.hblock : 1.0f;
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
                 const int cl = 64 * k + 16 * jj + 4 * q;
                 t4[jj] = *reinterpret_cast<const float4 *>(col_t + cl);
                 b4[jj] = *reinterpret_cast<const float4 *>(col_b + cl);
+                if (zpair) {
+                    t4[jj] = make_float4(t4[jj].x * bsc, t4[jj].y * bsc, t4[jj].z * bsc, t4[jj].w * bsc);
+                    b4[jj] = make_float4(b4[jj].x * bsc, b4[jj].y * bsc, b4[jj].z * bsc, b4[jj].w * bsc);
+                }
             }
         }
         const bool blk_full = t.n0 + 64 * k + 64 <= a.cout;
@@ -607,10 +615,7 @@ struct Epilogue {
                 }
             }
             if (zpair) {
-                // v holds z / b: scale back (exact, a power of two)
-                const float bsc = (float)a.hblock;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) v[r] *= bsc;
+                // v holds z
                 if (i8) {
                     uint32_t w[4];
                     quant16(v, qs, qr, q_fast, w);
@@ -626,16 +631,21 @@ struct Epilogue {
                     }
                 } else {
                     // the maximum of |z| over the valid pixels and channels
-                    const bool all = full && blk_full;
+                    // (wave-uniform branch: whole tiles take no masks)
                     float mm = 0.0f;
+                    if (full && blk_full) {
 #pragma unroll
-                    for (int jj = 0; jj < 4; ++jj)
+                        for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(v[r]));
+                    } else {
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const int ch = t.n0 + 64 * k + 16 * jj + 4 * q + r;
-                            const bool in = all || (valid[i] && ch < a.cout);
-                            mm = fmaxf(mm, in ? fabsf(v[4 * jj + r]) : 0.0f);
-                        }
+                        for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) {
+                                const int ch = t.n0 + 64 * k + 16 * jj + 4 * q + r;
+                                const bool in = valid[i] && ch < a.cout;
+                                mm = fmaxf(mm, in ? fabsf(v[4 * jj + r]) : 0.0f);
+                            }
+                    }
                     wave_m = fmaxf(wave_m, mm);
                 }
                 continue;
