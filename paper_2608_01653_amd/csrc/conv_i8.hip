@@ -961,7 +961,17 @@ __global__ void __launch_bounds__(kThreads, 2) conv_rowrun_kernel(const ConvArgs
                     acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fb, fa[i], acc[i][j], 0, 0, 0);
             }
         }
-        epilogue_regs<TW, FM, FN, E>(a, acc, tile, wave * TM, lane, s_col, s_col + BN);
+        {
+            // the epilogue reads the arguments and the lane afresh each tile
+            // (through values the compiler cannot see through): hoisted out of
+            // the tile loop they stay live through it and spill
+            const __attribute__((address_space(4))) ConvArgs *kargs =
+                (const __attribute__((address_space(4))) ConvArgs *)__builtin_amdgcn_kernarg_segment_ptr();
+            asm volatile("" : "+s"(kargs));
+            int elane = lane;
+            asm volatile("" : "+v"(elane));
+            epilogue_regs<TW, FM, FN, E>(*(const ConvArgs *)kargs, acc, tile, wave * TM, elane, s_col, s_col + BN);
+        }
         // the other buffer was last read before the previous barrier
         if (more) patch_store(tile_of(t_first + it + 1), pwd, s_patch[(it + 1) & 1]);
         __syncthreads();
