@@ -422,8 +422,9 @@ __global__ void __launch_bounds__(kThreads) scalar_kernel(const float *__restric
 
 // Blocks per sample: enough for the work, at most `total` over the whole batch.
 // The absmax kernels end in one same-address atomic per block, so they use a
-// smaller total than the quantization kernels.
-int grid_x(int64_t work_units, int per_block, int n, int total = 8192) {
+// smaller total (2048; 4096 and more measured slower) than the quantization
+// kernels (16384: 3 % faster than 8192 on 805 MB, no gain beyond).
+int grid_x(int64_t work_units, int per_block, int n, int total = 16384) {
     int64_t want = (work_units + per_block - 1) / per_block;
     int64_t cap = (total + n - 1) / n;
     if (cap < 1) cap = 1;
