@@ -14,8 +14,10 @@ Student-t weights).
 Prints one JSON line.  ``value`` is the whole step's algorithmic INT8 conv
 throughput (TOP/s, dense taps, 2 ops per MAC); per-layer time, TOP/s, GB/s and
 Mpixel/s are under ``layers``.  ``roofline`` is for the dominant kernel (layer-2
-convolution, INT8 MFMA bound); ``roofline_act_quant`` for layer 2's fused
-transform+quantization pass (HBM bound).  ``cpu_baseline`` times the CPU oracle
+convolution, INT8 MFMA bound); ``roofline_act_quant`` for layer 3's fused
+transform+quantization pass (HBM bound; the first layer quantized from a stored
+fp32 output, read once).  Both are timed inside the steps; their ``isolated``
+entries time the same kernel on the same resident input launched back to back.  ``cpu_baseline`` times the CPU oracle
 on one sample of the batch (rank 0, N = 1 only).
 """
 from __future__ import annotations
@@ -467,6 +469,32 @@ def main():
               "traffic_detail": measured_traffic(f"quant_l{qi + 1}"),
               "avg_us": round(t_q * 1e6, 2),
               "work": f"{eq * 5} bytes per launch = {eq} elements x (4 B fp32 in + 1 B int8 out)"}
+
+    # the same two kernels launched back to back on their resident inputs (the
+    # last step's buffers), with no producer kernel before them: in the step,
+    # the quantization reads the fp32 output the layer-2 conv has just written
+    # and competes with its write-back
+    def back_to_back(f, reps=20):
+        for _ in range(3):
+            f()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(reps):
+            f()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e-3
+    t_qi = back_to_back(lambda: hatq.hatq_fwht_quant_act(ys[qi - 1], act_hb[qi], absmax=amax[qi - 1],
+                                                        xq=xq[qi], scale=sc[qi], ws=ws))
+    roof_q["isolated"] = {"avg_us": round(t_qi * 1e6, 2), "achieved": round(eq * 5 / t_qi / 1e9, 1),
+                          "frac": round(eq * 5 / t_qi / 1e9 / PEAK_HBM_GBS, 4),
+                          "note": "20 launches back to back on the resident layer input after the timed steps"}
+    t_ci = back_to_back(lambda: hatq.hatq_conv_int8(layers[1], xq[1], sc[1], hatq.HATQ_OUT_F32,
+                                                   next_hblock=act_hb[2], next_absmax=amax[1], y=ys[1]))
+    roof["isolated"] = {"avg_us": round(t_ci * 1e6, 2), "achieved": round(ops2 / t_ci / 1e12, 1),
+                        "frac": round(ops2 / t_ci / 1e12 / PEAK_INT8_TOPS, 4),
+                        "note": "20 launches back to back on the resident layer input after the timed steps"}
 
     integer_stack = measure_integer_stack(args, wl, layers, x0, xq, sc, ys, ws, act_hb, total_ops, img_pix)
     form_selection = measure_form_selection(args, wl, layers, x0, xq, sc, ys)
