@@ -21,7 +21,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhatq.so")
 SOURCES = ["api.cpp", "act_quant.hip", "conv_i8.hip", "weights.hip"]
-CONV_PARTS = 12         # HATQ_CONV_PART = 0 .. 11 in conv_i8.hip
+CONV_PARTS = 13         # HATQ_CONV_PART = 0 .. 12 in conv_i8.hip
 OBJ_DIR = os.path.join(ROOT, "_build", "hatq")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -43,7 +43,7 @@ struct Tile {
 __device__ __forceinline__ Tile block_tile(const ConvArgs &a, int logical, int TH, int TW, int BN) {
     Tile t;
     const int tile_m = logical / a.tiles_n;
-    t.n0 = (logical - tile_m * a.tiles_n) * BN;
+    t.n0 = a.n_base + (logical - tile_m * a.tiles_n) * BN;
     const int per = a.tiles_h * a.tiles_w;
     t.nb = tile_m / per;
     const int rem = tile_m - t.nb * per;
@@ -1998,8 +1998,10 @@ ConvArgs sample_group(const ConvArgs &a, int64_t s0, int gn) {
     return b;
 }
 
+// split: one launch over output columns n_base .. n_base + BN - 1 of a wider
+// layer (k = 5 only)
 template <int BN, int STAGES, typename E>
-hipError_t launch_halo(const ConvArgs &a, hipStream_t st) {
+hipError_t launch_halo(const ConvArgs &a, hipStream_t st, int n_base = 0, bool split = false) {
     static_assert(STAGES == 5, "ring");
     // keep every buffer under 2 GiB (32-bit buffer offsets, kOobOffset out of
     // range): launch over groups of whole samples
@@ -2012,7 +2014,13 @@ hipError_t launch_halo(const ConvArgs &a, hipStream_t st) {
     for (int64_t s0 = 0; s0 < a.n; s0 += group) {
         const int gn = (int)(a.n - s0 < group ? a.n - s0 : group);
         ConvArgs b = sample_group(a, s0, gn);
-        const int64_t tiles = set_tiles(b, HaloGeom::TH, HaloGeom::TW, BN);
+        int64_t tiles = set_tiles(b, HaloGeom::TH, HaloGeom::TW, BN);
+        if (split) {
+            if (a.k != 5 || n_base < 0 || n_base + BN > a.cout_pad) return hipErrorInvalidValue;
+            b.tiles_n = 1;
+            b.n_base = n_base;
+            tiles = (int64_t)b.n * b.tiles_h * b.tiles_w;
+        }
         if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
         if (a.k == 5) {
             // persistent: one block per CU (a multiple of 8), each walking tiles
@@ -2065,8 +2073,9 @@ hipError_t try_epilogue(const ConvArgs &a, bool *hit, L &&launch) {
 
 // 192 output channels, 5x5 (4x4, 6x6) stride 2: the window kernels.  The
 // variant list is split in two; the order of the combined list decides.
-hipError_t conv_part_halo192_a(const ConvArgs &a, bool *hit, hipStream_t st);
-hipError_t conv_part_halo192_b(const ConvArgs &a, hipStream_t st);
+hipError_t conv_part_halo192_a(const ConvArgs &a, bool *hit, hipStream_t st, int n_base = 0, bool split = false);
+hipError_t conv_part_halo192_b(const ConvArgs &a, hipStream_t st, int n_base = 0, bool split = false);
+hipError_t conv_part_halo128(const ConvArgs &a, hipStream_t st, int n_base, bool split);
 hipError_t conv_part_pipe192(const ConvArgs &a, hipStream_t st);
 hipError_t conv_part_pipe320(const ConvArgs &a, hipStream_t st);
 hipError_t conv_part_pipe_other(const ConvArgs &a, hipStream_t st);
@@ -2078,15 +2087,22 @@ hipError_t conv_part_gather3(const ConvArgs &a, hipStream_t st);
 hipError_t conv_part_gather4(const ConvArgs &a, hipStream_t st);
 
 #if HATQ_PART(1)
-hipError_t conv_part_halo192_a(const ConvArgs &a, bool *hit, hipStream_t st) {
+hipError_t conv_part_halo192_a(const ConvArgs &a, bool *hit, hipStream_t st, int n_base, bool split) {
     return try_epilogue<Epi<0, 64, 2>, Epi<0, 1, 2>, Epi<0, 0, 3>, Epi<0, 64>, Epi<0, 1>, Epi<0, 0>>(
-        a, hit, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st); });
+        a, hit, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st, n_base, split); });
 }
 #endif
 #if HATQ_PART(2)
-hipError_t conv_part_halo192_b(const ConvArgs &a, hipStream_t st) {
+hipError_t conv_part_halo192_b(const ConvArgs &a, hipStream_t st, int n_base, bool split) {
     return with_epilogue<Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_GENERIC_EPILOGUES>(
-        a, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st); });
+        a, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st, n_base, split); });
+}
+#endif
+#if HATQ_PART(12)
+// 128 output columns of a wider 5x5 stride-2 layer (columns 192..319 of 320)
+hipError_t conv_part_halo128(const ConvArgs &a, hipStream_t st, int n_base, bool split) {
+    return with_epilogue<Epi<64, 0>, Epi<64, 64>, Epi<64, 1>, Epi<0, 0>, HATQ_GENERIC_EPILOGUES>(
+        a, [&](auto e) { return launch_halo<128, 5, decltype(e)>(a, st, n_base, split); });
 }
 #endif
 #if HATQ_PART(3)
@@ -2164,7 +2180,16 @@ hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
                 return hit ? r : conv_part_halo192_b(a, st);
             }
             return conv_part_pipe192(a, st);
-        case 320: return conv_part_pipe320(a, st);
+        case 320:
+            if (a.sa == 2 && a.so == 1 && a.k == 5 && a.cin_p % 64 == 0) {
+                // the window kernel over columns 0..191, then 192..319
+                bool hit = false;
+                hipError_t r = conv_part_halo192_a(a, &hit, st, 0, true);
+                if (!hit) r = conv_part_halo192_b(a, st, 0, true);
+                if (r != hipSuccess) return r;
+                return conv_part_halo128(a, st, 192, true);
+            }
+            return conv_part_pipe320(a, st);
         default: return conv_part_pipe_other(a, st);
     }
 }
