@@ -1725,11 +1725,6 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     Tile tile = block_tile(a, xcd_tile(v, ntiles), TH, TW, BN);
     const int cin_p = a.cin_p;
     const int nchunks = cin_p >> 6;
-    // The block takes the channel chunks of every tile in the order rot, rot+1,
-    // ... (mod nchunks): blocks with different rotations read different weight
-    // rows at the same time, which spreads the weight reads of the lockstep
-    // blocks over more of L2 (integer sums: any order gives the same result).
-    const int rot = (int)(blockIdx.x % (unsigned)nchunks);
     const int rows_used = 2 * (TH - 1) + K, cols_used = 2 * (TW - 1) + K;
 
     const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
@@ -1777,7 +1772,6 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
         b_off[j] = (uint32_t)((tile.n0 + nn) * 64 + 16 * g);
     }
     const uint32_t cp64 = (uint32_t)a.cout_pad * 64u;
-    const uint32_t rot_off = (uint32_t)rot * cp64;
     const uint32_t tap_w = (uint32_t)nchunks * cp64;
     // Step j of a chunk: odd kernel rows first (kh = 1, 3), then even (0, 2, 4).
     auto step_kh = [](int j) { return j < NODD ? 1 + 2 * (j / K) : 2 * ((j - NODD) / K); };
@@ -1836,8 +1830,8 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
 
     // prologue: odd half of chunk 0, weight steps 0 .. 3
     static_assert(SLOTS - 1 <= NTAP, "prologue within chunk 0");
-    burst(1, rot);
-    unroll<SLOTS - 1>([&](auto Jc) { issue_b(Jc, rot_off); });
+    burst(1, 0);
+    unroll<SLOTS - 1>([&](auto Jc) { issue_b(Jc, 0u); });
     // the raw per-channel scale and bias, while the first DMAs are in flight
     for (int c = tid; c < BN; c += kHaloThreads) column_raw(a, tile.n0 + c, s_raw[c], s_raw[BN + c]);
     wait_vmcnt_lds<(SLOTS - 2) * PER>();
@@ -1858,10 +1852,7 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
 
     const bool first_tile = v == (int)blockIdx.x;
     for (int c = 0; c < nchunks; ++c) {
-        // chunk cc of the tile (the block's rotation), and the next one
-        const int cc = c + rot < nchunks ? c + rot : c + rot - nchunks;
-        const int cn = cc + 1 < nchunks ? cc + 1 : 0;
-        const uint32_t coff = (uint32_t)cc * cp64, coff1 = (uint32_t)cn * cp64;
+        const uint32_t coff = (uint32_t)c * cp64, coff1 = coff + cp64;
         const bool more = c + 1 < nchunks;
         // the block's next tile, if any: the refills of the last chunk fetch
         // its odd window rows and first weight steps
@@ -1873,7 +1864,7 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
             if constexpr (S < NTAP) {
                 issue_b(std::integral_constant<int, S>{}, coff);
             } else {
-                if (more || has_next) issue_b(std::integral_constant<int, S - NTAP>{}, more ? coff1 : rot_off);
+                if (more || has_next) issue_b(std::integral_constant<int, S - NTAP>{}, more ? coff1 : 0u);
                 else issue_zero(std::integral_constant<int, S - NTAP>{});
             }
         };
@@ -1912,13 +1903,13 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
                     issue_step(std::integral_constant<int, J + 3>{});
                     issue_step(std::integral_constant<int, J + 4>{});
                 }
-                if constexpr (J == 0) burst(0, cc);   // even rows of this chunk
+                if constexpr (J == 0) burst(0, c);   // even rows of this chunk
                 if constexpr (J == NODD) {          // odd rows of the next chunk (or tile)
                     if (more) {
-                        burst(1, cn);
+                        burst(1, c + 1);
                     } else if (has_next) {
                         window_offsets(block_tile(a, xcd_tile(v + (int)gridDim.x, ntiles), TH, TW, BN), 1, h_off[1]);
-                        burst(1, rot);
+                        burst(1, 0);
                     } else {
                         zero_fill(1);
                     }
