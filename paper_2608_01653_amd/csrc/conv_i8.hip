@@ -769,7 +769,10 @@ struct RowRunPatch {
     static constexpr int PIT = (WORDS + kThreads - 1) / kThreads;
 };
 
-constexpr int kRowRunTiles = 4;   // tiles per block
+// Tiles per block (a run of one sample): at least kRowRunMin; the launch
+// raises it so the grid is about two blocks per CU (two fit a CU), one round
+// with no tail, up to kRowRunMax.
+constexpr int kRowRunMin = 4, kRowRunMax = 64;
 
 template <int TH, int TW, int BN, int CIN, typename E>
 __global__ void __launch_bounds__(kThreads, 2) conv_rowrun_kernel(const ConvArgs a) {
@@ -794,13 +797,14 @@ __global__ void __launch_bounds__(kThreads, 2) conv_rowrun_kernel(const ConvArgs
     // this block's run: sample nb, column tile n0, tiles t_first .. t_first+cnt-1
     // of the sample (row-major over tiles_h x tiles_w)
     const int per = a.tiles_h * a.tiles_w;
-    const int runs = (per + kRowRunTiles - 1) / kRowRunTiles;
+    const int run = a.run_tiles;
+    const int runs = (per + run - 1) / run;
     const int logical = xcd_logical_tile();
     const int rn = logical / a.tiles_n;
     const int n0 = (logical - rn * a.tiles_n) * BN;
     const int nb = rn / runs;
-    const int t_first = (rn - nb * runs) * kRowRunTiles;
-    const int cnt = per - t_first < kRowRunTiles ? per - t_first : kRowRunTiles;
+    const int t_first = (rn - nb * runs) * run;
+    const int cnt = per - t_first < run ? per - t_first : run;
     auto tile_of = [&](int t) {
         Tile tl;
         tl.nb = nb;
@@ -1152,6 +1156,8 @@ hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
 #define HATQ_HOT_EPILOGUES \
     Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_GENERIC_EPILOGUES
 
+int persistent_blocks();
+
 template <int TH, int TW, int BN, int CS, typename E>
 hipError_t launch_rowrun(const ConvArgs &a, hipStream_t st) {
     ConvArgs b = a;
@@ -1160,7 +1166,11 @@ hipError_t launch_rowrun(const ConvArgs &a, hipStream_t st) {
     // every byte offset of the input fits the 32-bit buffer range
     if ((int64_t)b.n * b.h * b.w * CS >= ((int64_t)1 << 31) - 64) return hipErrorInvalidValue;
     const int64_t per = (int64_t)b.tiles_h * b.tiles_w;
-    const int64_t blocks = (int64_t)b.n * ((per + kRowRunTiles - 1) / kRowRunTiles) * b.tiles_n;
+    const int64_t slots = 2 * (int64_t)persistent_blocks();   // resident blocks (0 if unknown)
+    int64_t run = slots > 0 ? (b.n * per * b.tiles_n + slots - 1) / slots : kRowRunMin;
+    run = run < kRowRunMin ? kRowRunMin : run > kRowRunMax ? kRowRunMax : run;
+    b.run_tiles = (int32_t)run;
+    const int64_t blocks = (int64_t)b.n * ((per + run - 1) / run) * b.tiles_n;
     if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     conv_rowrun_kernel<TH, TW, BN, CS, E><<<(unsigned)blocks, kThreads, 0, st>>>(b);
     return hipGetLastError();

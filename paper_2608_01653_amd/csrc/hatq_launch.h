@@ -64,6 +64,7 @@ struct ConvArgs {
     int32_t next_hblock;   // 0 = no next-operand absmax
     int32_t tiles_h, tiles_w, tiles_n;   // 2-D tiles of grid points per sample; column tiles
     int32_t n_base;        // first output column of a launch over a column range, else 0
+    int32_t run_tiles;     // row-run kernel: tiles per block (set at launch)
     int8_t dh[kMaxTaps], dw[kMaxTaps];
     int16_t wtap[kMaxTaps];
 };
