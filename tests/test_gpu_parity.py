@@ -171,6 +171,7 @@ CONV = [  # (n, h, w, cin, cout, k, stride, pad, transposed, out_pad, form, hblo
     (150, 18, 18, 192, 192, 5, 2, 2, False, 0, "DH", 64), # 300 ragged tiles: blocks walk several, across samples
     (140, 17, 19, 192, 192, 5, 2, 2, False, 0, "WH", 64), # the same, WH
     (130, 17, 18, 192, 320, 5, 2, 2, False, 0, "WH", 64), # 320 columns: two launches (192 + 128), 260 tiles each
+    (3, 21, 30, 192, 320, 5, 2, 2, False, 0, "DH", 64),   # the same split with the DH epilogues
 ]
 CONV_IDS = [f"n{c[0]}-{c[1]}x{c[2]}-{c[3]}to{c[4]}-k{c[5]}s{c[6]}-{c[10]}{'-T' if c[8] else ''}" for c in CONV]
 
