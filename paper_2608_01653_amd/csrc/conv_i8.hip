@@ -1695,8 +1695,10 @@ __device__ __forceinline__ void unroll(F &&f) {
 // first weight steps of chunk 0) fetch the next tile's data instead of zeros,
 // so a tile's prologue overlaps the previous tile's last steps and epilogue.
 // The weights and the per-channel scale and bias are the same for every tile
-// (one column tile: BN = cout_pad); the raw scale and bias are staged once and
-// each tile's column factors are formed from them and the sample's s_x.
+// (a launch covers one range of BN output columns, from n_base: all of them, or
+// 0-191 and 192-319 of a 320-column layer in two launches); the raw scale and
+// bias are staged once and each tile's column factors are formed from them and
+// the sample's s_x.
 template <int BN, typename E>
 __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvArgs a) {
     using G = HaloGeom;
@@ -1730,7 +1732,7 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int ntiles = a.n * a.tiles_h * a.tiles_w;   // one column tile
+    const int ntiles = a.n * a.tiles_h * a.tiles_w;   // one column range per launch
     int v = blockIdx.x;
     Tile tile = block_tile(a, xcd_tile(v, ntiles), TH, TW, BN);
     const int cin_p = a.cin_p;
