@@ -31,7 +31,9 @@
  *    DEVICE pointers owned by the caller; the library never allocates, frees or
  *    synchronizes, and keeps no global state.  Calls are reentrant; calls on one
  *    stream execute in order.
- *  - `stream` is a hipStream_t (NULL = the default stream).
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Some launch
+ *    shapes (the persistent convolution grids) follow the CU count of the
+ *    current device; results do not depend on them.
  *  - Arguments are validated on the host before any launch.  On error nothing
  *    is launched and outputs are untouched.  A launch failure is reported as
  *    HATQ_EHIP; faults inside kernels surface at the caller's next
