@@ -569,6 +569,38 @@ struct Epilogue {
         }
     }
 
+    // Codes of group (i, k): word jj of lane (p, q) holds channels 64k + 16jj + 4q
+    // .. +3.  A 4 x 4 transpose of words between jj and the lane bits of q (pair
+    // swaps across lane bits 5, then 4) gives lane (p, q) channels 64k + 16q ..
+    // +15, stored as one 16-byte write.
+    __device__ __forceinline__ void store_codes(uint32_t (&w)[4], int i, int k) const {
+        auto swap32 = [](uint32_t &x, uint32_t &y) {
+            const auto r = __builtin_amdgcn_permlane32_swap(x, y, false, false);
+            x = r[0];
+            y = r[1];
+        };
+        auto swap16 = [](uint32_t &x, uint32_t &y) {
+            const auto r = __builtin_amdgcn_permlane16_swap(x, y, false, false);
+            x = r[0];
+            y = r[1];
+        };
+        swap32(w[0], w[2]);
+        swap32(w[1], w[3]);
+        swap16(w[0], w[1]);
+        swap16(w[2], w[3]);
+        if (!valid[i]) return;
+        const int m = row0 + 16 * i + p;
+        int8_t *yq = reinterpret_cast<int8_t *>(a.y) + out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW) * a.cout + t.n0;
+        const int cl = 64 * k + 16 * q;
+        if ((a.cout & 15) == 0 && t.n0 + cl + 16 <= a.cout) {
+            *reinterpret_cast<uint4 *>(yq + cl) = make_uint4(w[0], w[1], w[2], w[3]);
+        } else {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj)
+                if (t.n0 + cl + 4 * jj < a.cout) *reinterpret_cast<uint32_t *>(yq + cl + 4 * jj) = w[jj];
+        }
+    }
+
     // 64-channel block k of every row group (one set of column factors serves all)
     __device__ __forceinline__ void block(const v4i (&acc)[FM][FN], int k) {
         if (fl.iq) {
@@ -619,16 +651,7 @@ struct Epilogue {
                 if (i8) {
                     uint32_t w[4];
                     quant16(v, qs, qr, q_fast, w);
-                    if (valid[i]) {
-                        const int m = row0 + 16 * i + p;
-                        int8_t *yq = reinterpret_cast<int8_t *>(a.y) +
-                                     out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW) * a.cout + t.n0;
-#pragma unroll
-                        for (int jj = 0; jj < 4; ++jj) {
-                            const int cl = 64 * k + 16 * jj + 4 * q;
-                            if (t.n0 + cl < a.cout) *reinterpret_cast<uint32_t *>(yq + cl) = w[jj];
-                        }
-                    }
+                    store_codes(w, i, k);
                 } else {
                     // the maximum of |z| over the valid pixels and channels
                     // (wave-uniform branch: whole tiles take no masks)
@@ -695,16 +718,7 @@ struct Epilogue {
                     fwht_acc<NB, true>(v, a.next_hblock);
                     uint32_t w[4];
                     quant16(v, qs, qr, q_fast, w);
-                    if (valid[i]) {
-                        const int m = row0 + 16 * i + p;
-                        int8_t *yq = reinterpret_cast<int8_t *>(a.y) +
-                                     out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW) * a.cout + t.n0;
-#pragma unroll
-                        for (int jj = 0; jj < 4; ++jj) {
-                            const int cl = 64 * k + 16 * jj + 4 * q;
-                            if (t.n0 + cl < a.cout) *reinterpret_cast<uint32_t *>(yq + cl) = w[jj];
-                        }
-                    }
+                    store_codes(w, i, k);
                 } else {
                     fwht_acc<NB, false>(v, a.next_hblock);
                     float mm = 0.0f;
