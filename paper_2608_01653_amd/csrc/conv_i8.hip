@@ -545,27 +545,20 @@ struct Epilogue {
                 if (fl.wh) fwht_acc_i64<WB>(v, a.hblock);
                 fwht_acc_i64<NB>(v, a.next_hblock);
             }
-            if (valid[i]) {
-                uint32_t c[16];
-                if (rq_n >= 32) {
+            // every lane forms its codes (the transpose in store_codes needs
+            // them all); rows past the grid are not stored
+            uint32_t c[16];
+            if (rq_n >= 32) {
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) c[r] = int_code_hi(v[r], rq_n - 32, rq_bias);
-                } else {
+                for (int r = 0; r < 16; ++r) c[r] = int_code_hi(v[r], rq_n - 32, rq_bias);
+            } else {
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) c[r] = int_code(v[r], rq_n, rq_bias);
-                }
-                uint32_t w[4];
-#pragma unroll
-                for (int jj = 0; jj < 4; ++jj) w[jj] = pack_low_bytes(c[4 * jj], c[4 * jj + 1], c[4 * jj + 2], c[4 * jj + 3]);
-                const int m = row0 + 16 * i + p;
-                int8_t *yq = reinterpret_cast<int8_t *>(a.y) +
-                             out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW) * a.cout + t.n0;
-#pragma unroll
-                for (int jj = 0; jj < 4; ++jj) {
-                    const int cl = 64 * k + 16 * jj + 4 * q;
-                    if (t.n0 + cl < a.cout) *reinterpret_cast<uint32_t *>(yq + cl) = w[jj];
-                }
+                for (int r = 0; r < 16; ++r) c[r] = int_code(v[r], rq_n, rq_bias);
             }
+            uint32_t w[4];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) w[jj] = pack_low_bytes(c[4 * jj], c[4 * jj + 1], c[4 * jj + 2], c[4 * jj + 3]);
+            store_codes(w, i, k);
         }
     }
 
