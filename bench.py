@@ -34,7 +34,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, GB/s
 PEAK_INT8_TOPS = 5000.0      # MI355X dense INT8 MFMA, TOP/s
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cfg4.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_analysis_stack_b16.json")
 
 
 def kernel_source_hash() -> str:
@@ -318,7 +318,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="cfg4")
+    ap.add_argument("--workload", default="analysis_stack4_rgb_b16_1024x1024")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device-to-device copy (scales the HBM byte counters)")
@@ -335,7 +335,7 @@ def main():
     if args.gpus != 1:
         print("bench.py: this operator is measured on one GPU only; --gpus must be 1 "
               f"(got {args.gpus}). Batch sharding across GPUs needs no communication and is "
-              "described in DESIGN.md, but is not run here.", file=sys.stderr)
+              "not run here.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

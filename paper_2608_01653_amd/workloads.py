@@ -82,22 +82,22 @@ def _k5s2(cin, cout, form, hb=64):
 
 
 # Single 1x1 (linear) layer, double-Hadamard with one 128-point block.
-CFG0 = Workload("linear1x1_dh_b128_64x64x128", (1, 64, 64, 128), "heavy",
+LINEAR_1X1 = Workload("linear1x1_dh_b128_64x64x128", (1, 64, 64, 128), "heavy",
                 [Layer(128, 128, 1, 1, 0, "DH", 128)])
 # One analysis 5x5 stride-2 conv, 192->192, three 64-blocks; run in both forms.
-CFG1_DH = Workload("analysis_k5s2_192_256x256_dh", (1, 256, 256, 192), "heavy",
+ANALYSIS_K5S2_DH = Workload("analysis_k5s2_192_256x256_dh", (1, 256, 256, 192), "heavy",
                    [_k5s2(192, 192, "DH")])
-CFG1_WH = Workload("analysis_k5s2_192_256x256_wh", (1, 256, 256, 192), "heavy",
+ANALYSIS_K5S2_WH = Workload("analysis_k5s2_192_256x256_wh", (1, 256, 256, 192), "heavy",
                    [_k5s2(192, 192, "WH")])
 # One synthesis 5x5 stride-2 transposed conv on a 1/16-resolution 1024x1536 latent.
-CFG2 = Workload("synthesis_tconv_k5s2_192_64x96_dh", (1, 64, 96, 192), "heavy",
+SYNTHESIS_TCONV = Workload("synthesis_tconv_k5s2_192_64x96_dh", (1, 64, 96, 192), "heavy",
                 [Layer(192, 192, 5, 2, 2, "DH", 64, transposed=True, out_pad=1)])
 # Four-layer analysis stack, form mask WH, DH, DH, WH, on a Kodak-size RGB image.
 _STACK = [_k5s2(3, 192, "WH"), _k5s2(192, 192, "DH"), _k5s2(192, 192, "DH"),
           _k5s2(192, 320, "WH")]
-CFG3 = Workload("analysis_stack4_rgb_512x768", (1, 512, 768, 3), "rgb", list(_STACK))
+STACK_KODAK = Workload("analysis_stack4_rgb_512x768", (1, 512, 768, 3), "rgb", list(_STACK))
 # The same stack at batch 16 on 1024x1024 RGB: the largest conv shapes.
-CFG4 = Workload("analysis_stack4_rgb_b16_1024x1024", (16, 1024, 1024, 3), "rgb", list(_STACK))
+STACK_B16 = Workload("analysis_stack4_rgb_b16_1024x1024", (16, 1024, 1024, 3), "rgb", list(_STACK))
 
-ALL = {"cfg0": CFG0, "cfg1_dh": CFG1_DH, "cfg1_wh": CFG1_WH, "cfg2": CFG2,
-       "cfg3": CFG3, "cfg4": CFG4}
+ALL = {w.name: w for w in (LINEAR_1X1, ANALYSIS_K5S2_DH, ANALYSIS_K5S2_WH, SYNTHESIS_TCONV,
+                             STACK_KODAK, STACK_B16)}

@@ -97,13 +97,13 @@ def test_int_params_no_shift_fits(orc):
     assert host(table)[-1] == -1
 
 
-def test_cfg4_layer1_int_transition_full_size(orc):
+def test_stack_b16_layer1_int_transition_full_size(orc):
     """The benchmark's layer-1 -> layer-2 transition at full size in integer
     form: sampled pixels bit-exact against the oracle's integer transition of
     its own accumulators, and every code within 1 LSB of the float requantizing
     epilogue at the same static scales (the integer bias and the fixed-point
     multiplier are the only differences)."""
-    wl = workloads.CFG4
+    wl = workloads.STACK_B16
     (ishape, oshape) = wl.shapes()[0]
     L, nxt = wl.layers[0], wl.layers[1]
     rng = np.random.default_rng(4200)
@@ -140,4 +140,4 @@ def test_cfg4_layer1_int_transition_full_size(orc):
         crop = _crop(xq, s_, oh * L.stride - L.pad, ow * L.stride - L.pad, L.k)
         acc = orc.conv_int8(crop, ref.wq, stride=L.stride, pad=0)
         exp[i] = orc.int_transition(acc, ref, rq, nb)[0, 0, 0]
-    assert_codes(got, exp, exact=True, what="cfg4 layer-1 integer transition vs oracle")
+    assert_codes(got, exp, exact=True, what="batch-16 stack layer-1 integer transition vs oracle")

@@ -1,11 +1,11 @@
 """GPU parity at the workload shapes.
 
-* cfg0-cfg3 (sizes the oracle finishes in seconds): every layer of the workload,
+* the single layers and the 512x768 stack (sizes the oracle finishes in seconds): every layer of the workload,
   each GPU stage fed the oracle's own inputs (the oracle's fp32 output of the
   previous layer, the oracle's codes and scales), so the comparison isolates each
   stage: codes and scales of the activation pass, the fp32 output of the
   convolution with its epilogue, and the fused next-layer absmax.
-* cfg4 (batch 16, 1024x1024; too large for the oracle): every convolution at its
+* the stack at batch 16 on 1024x1024 (too large for the oracle): every convolution at its
   full size, in the launch configuration the benchmark times, on random INT8
   codes; sampled output pixels are recomputed by the oracle from their 5x5
   input crop, and the fused absmax is checked against the two-pass activation
@@ -38,7 +38,9 @@ def _act_block(L):
     return L.hblock if L.form == "DH" else 1
 
 
-@pytest.mark.parametrize("name", ["cfg0", "cfg1_dh", "cfg1_wh", "cfg2", "cfg3"])
+@pytest.mark.parametrize("name", [w.name for w in (workloads.LINEAR_1X1, workloads.ANALYSIS_K5S2_DH,
+                                                    workloads.ANALYSIS_K5S2_WH, workloads.SYNTHESIS_TCONV,
+                                                    workloads.STACK_KODAK)])
 def test_workload_layers(orc, name):
     wl = workloads.ALL[name]
     x, params = wl.generate()
@@ -80,8 +82,8 @@ def _crop(xq, nb, ih0, iw0, k):
 
 
 @pytest.mark.parametrize("li", [0, 1, 2, 3], ids=["L1", "L2", "L3", "L4"])
-def test_cfg4_full_size_sampled(orc, li):
-    wl = workloads.CFG4
+def test_stack_b16_full_size_sampled(orc, li):
+    wl = workloads.STACK_B16
     (ishape, oshape) = wl.shapes()[li]
     L = wl.layers[li]
     rng = np.random.default_rng(4000 + li)
@@ -122,7 +124,7 @@ def test_cfg4_full_size_sampled(orc, li):
         del q1, q2
 
 
-def test_cfg4_layer1_requant_full_size(orc):
+def test_stack_b16_layer1_requant_full_size(orc):
     """The benchmark's layer-1 -> layer-2 transition at full size (WH 64 -> DH
     64, so the next operand is the accumulator-basis z): the absmax-only pass
     and the requantizing epilogue agree with the F32 output followed by the
@@ -130,7 +132,7 @@ def test_cfg4_layer1_requant_full_size(orc):
     property that holds at any size); sampled pixels' codes equal the oracle's
     quantization of its own z with the GPU's scale, bit for bit, and every
     sampled |z| lies under the fused absmax."""
-    wl = workloads.CFG4
+    wl = workloads.STACK_B16
     (ishape, oshape) = wl.shapes()[0]
     L, nxt = wl.layers[0], wl.layers[1]
     rng = np.random.default_rng(4100)
@@ -150,7 +152,7 @@ def test_cfg4_layer1_requant_full_size(orc):
     # WH 64 -> DH 64: the fused passes take z (B_next y = z exactly); the
     # two-kernel path rounds through two fp32 butterflies
     assert_scale_ulp(host(sq), host(s2), ulps=2)
-    assert_codes(host(yq), host(q2), what="cfg4 layer-1 requant vs two-kernel path")
+    assert_codes(host(yq), host(q2), what="batch-16 stack layer-1 requant vs two-kernel path")
     # oracle on sampled pixels, with the GPU's scale: codes of z_ref, bit for bit
     ho, wo = oshape[1], oshape[2]
     pts = [(int(rng.integers(n)), int(rng.integers(ho)), int(rng.integers(wo))) for _ in range(64)]
@@ -165,5 +167,5 @@ def test_cfg4_layer1_requant_full_size(orc):
         z = orc.wh_z(acc, sx[s_:s_ + 1], ref)[0, 0, 0, :L.cout]
         assert np.abs(z).max() <= host(nam)[s_]
         exp[t] = np.clip(np.rint(z / sh[s_]), -127, 127).astype(np.int8)
-    assert_codes(got, exp, exact=True, what="cfg4 layer-1 requant codes vs oracle")
+    assert_codes(got, exp, exact=True, what="batch-16 stack layer-1 requant codes vs oracle")
     del y, q2
