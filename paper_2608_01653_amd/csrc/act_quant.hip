@@ -134,7 +134,16 @@ __device__ __forceinline__ void quant_store_item(const float (&vin)[4 * ItemShap
             for (int i = 0; i < 4; ++i) x[i] = __builtin_amdgcn_mov_dpp(w[i ^ 2], 0x4E, 0xF, 0xF, true);   // lane ^ 2
 #pragma unroll
             for (int i = 0; i < 4; ++i) w[i] = ((t ^ i) & 2) ? x[i] : w[i];
-            *reinterpret_cast<int4 *>(qs + base + 64 * g + 16 * t) = make_int4(w[0], w[1], w[2], w[3]);
+            int8_t *dst = qs + base + 64 * g + 16 * t;
+            // (xq need only be 4-byte aligned and a sample's E only a multiple
+            // of 4; base is a multiple of 64, so the sample's start decides,
+            // uniformly for the block)
+            if ((reinterpret_cast<uintptr_t>(qs) & 15) == 0) {
+                *reinterpret_cast<int4 *>(dst) = make_int4(w[0], w[1], w[2], w[3]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) reinterpret_cast<int *>(dst)[i] = w[i];
+            }
         }
         return;
     }

@@ -585,7 +585,10 @@ struct Epilogue {
         const int m = row0 + 16 * i + p;
         int8_t *yq = reinterpret_cast<int8_t *>(a.y) + out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW) * a.cout + t.n0;
         const int cl = 64 * k + 16 * q;
-        if ((a.cout & 15) == 0 && t.n0 + cl + 16 <= a.cout) {
+        // (the caller's buffer need only be 4-byte aligned: 16-byte writes when
+        // every pixel's codes start 16-byte aligned, a launch-wide condition)
+        const bool a16 = ((reinterpret_cast<uintptr_t>(a.y) | (uintptr_t)a.cout | (uintptr_t)t.n0) & 15) == 0;
+        if (a16 && t.n0 + cl + 16 <= a.cout) {
             *reinterpret_cast<uint4 *>(yq + cl) = make_uint4(w[0], w[1], w[2], w[3]);
         } else {
 #pragma unroll

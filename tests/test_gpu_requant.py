@@ -134,3 +134,40 @@ def test_requant_zero_output():
     hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=64, next_absmax=nam, absmax_only=True)
     yq, sq = hatq.hatq_conv_int8_requant(layer, xq, sx, 64, next_absmax=nam)
     assert torch.all(nam == 0) and torch.all(sq == 1) and not torch.any(yq)
+
+
+@pytest.mark.gpu
+def test_codes_into_4_byte_aligned_buffers(orc):
+    """Code outputs at an address that is 4- but not 16-byte aligned (all the ABI
+    asks of them): the activation quantizer and the requantizing epilogue write
+    the same codes as into aligned buffers."""
+    rng = np.random.default_rng(91)
+    x = dev(synth.heavy_tailed_activations(rng, (2, 9, 11, 192)))
+    q_ref, s_ref = hatq.hatq_fwht_quant_act(x, 64)
+    buf = torch.zeros(q_ref.numel() + 32, dtype=torch.int8, device="cuda")
+    q_off = buf[4:4 + q_ref.numel()].view(q_ref.shape)
+    q_got, s_got = hatq.hatq_fwht_quant_act(x, 64, xq=q_off)
+    assert q_off.data_ptr() % 16 == 4
+    assert torch.equal(q_got, q_ref) and torch.equal(s_got, s_ref)
+    assert torch.equal(buf[:4], torch.zeros(4, dtype=torch.int8, device="cuda"))
+    assert torch.equal(buf[4 + q_ref.numel():], torch.zeros(28, dtype=torch.int8, device="cuda"))
+    # samples of 84 elements (one full item of 64 and a tail): every sample after
+    # the first starts 4, 8 or 12 bytes past a 16-byte boundary (original-domain
+    # codes, exact on both sides)
+    xs = synth.heavy_tailed_activations(rng, (5, 4, 7, 3))
+    q_small, _ = hatq.hatq_fwht_quant_act(dev(xs), 1)
+    q_exp, _ = orc.quantize_symmetric(xs)
+    assert np.array_equal(host(q_small), q_exp)
+
+    c = (2, 21, 23, 192, 192, 5, 2, 2, False, 0, "DH", 64)
+    _, _, _, _, layer = _layer(orc, c, 92)
+    nam = torch.full((2,), -1.0, device="cuda")
+    assert hatq.hatq_conv_int8(layer, q_ref, s_ref, hatq.HATQ_OUT_F32, next_hblock=64, next_absmax=nam,
+                               absmax_only=True) is None
+    y_ref, _ = hatq.hatq_conv_int8_requant(layer, q_ref, s_ref, 64, next_absmax=nam)
+    ybuf = torch.zeros(y_ref.numel() + 32, dtype=torch.int8, device="cuda")
+    y_off = ybuf[4:4 + y_ref.numel()].view(y_ref.shape)
+    y_got, _ = hatq.hatq_conv_int8_requant(layer, q_ref, s_ref, 64, next_absmax=nam, yq=y_off)
+    assert y_off.data_ptr() % 16 == 4
+    assert torch.equal(y_got, y_ref)
+    assert torch.equal(ybuf[4 + y_ref.numel():], torch.zeros(28, dtype=torch.int8, device="cuda"))
