@@ -82,6 +82,7 @@ def lib():
         L.orc_hadamard.argtypes = [i32, P]
         L.orc_hadamard_base.argtypes = [i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
         L.orc_order.argtypes = [i32, i32]
+        L.orc_hadamard_split.argtypes = [i32]
         L.orc_select_form.argtypes = [i64, i64, ctypes.c_double]
         _lib = L
     return _lib
@@ -388,7 +389,7 @@ def select_form(expansions: int, images: int, tau: float = 0.8) -> str:
 # --------------------------------------------------------------------------
 def paley(q: int, kind: int) -> np.ndarray:
     """Paley-I (kind 1, q = 3 mod 4, order q + 1) or Paley-II (kind 2, q = 1 mod 4,
-    order 2(q + 1)) for a prime q."""
+    order 2(q + 1)) for an odd prime power q, over the field F_q."""
     n = (q + 1) * (1 if kind == 1 else 2)
     H = np.empty((n, n), np.int8)
     if lib().orc_paley(q, kind, _p(H)) != 0:
@@ -398,10 +399,18 @@ def paley(q: int, kind: int) -> np.ndarray:
 
 def hadamard_base(m: int):
     """(b, kind, q): the base order of the construction of order m (P_b (x) H~_(m/b))
-    and its Paley kind and prime (kind 0: b = 1, Sylvester); None if unsupported."""
+    and its Paley kind and prime power (kind 0: b = 1, Sylvester); None if m has no
+    such form (it may still be a Kronecker product, see hadamard_split)."""
     kind, q = ctypes.c_int32(), ctypes.c_int32()
     b = lib().orc_hadamard_base(m, ctypes.byref(kind), ctypes.byref(q))
     return None if b < 0 else (int(b), int(kind.value), int(q.value))
+
+
+def hadamard_split(m: int):
+    """The smallest factor a of an order m = a * c reached only as a Kronecker
+    product H_a (x) H_c of two supported orders; None otherwise."""
+    a = lib().orc_hadamard_split(m)
+    return None if a < 0 else int(a)
 
 
 def hadamard(m: int) -> np.ndarray:

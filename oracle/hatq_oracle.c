@@ -59,56 +59,169 @@ int orc_sylvester(int b, int8_t *H)
     return 0;
 }
 
-/* Paley constructions (supplementary, Hadamard construction): chi is the     */
-/* quadratic character of the prime field F_q (chi(0) = 0) and Q the          */
-/* Jacobsthal matrix Q[i][j] = chi(j - i).                                    */
+/* Paley constructions (supplementary, Hadamard construction), for an odd    */
+/* prime power q = p^k.  chi is the quadratic character of the finite field   */
+/* F_q (chi(0) = 0, chi(a) = 1 for a nonzero square, -1 otherwise) and Q the  */
+/* Jacobsthal matrix Q[i][j] = chi(x_j - x_i) over the field elements x_i.    */
 /*  Paley-I  (q = 3 mod 4, order q + 1): H = I + [[0, 1^T], [-1, Q]].         */
 /*  Paley-II (q = 1 mod 4, order 2(q + 1)): with the symmetric conference     */
 /*           matrix C = [[0, 1^T], [1, Q]], every entry C[i][j] becomes the   */
 /*           2x2 block [[1, -1], [-1, -1]] where C[i][j] = 0 and              */
 /*           C[i][j] * [[1, 1], [1, -1]] otherwise.                           */
-/* Only prime q (no prime powers).  Returns 0, or -1 if q is not such a prime.*/
-static int is_prime(int q)
+/* Field elements: x_e for e = 0 .. q-1 is the polynomial sum_i d_i t^i with  */
+/* e = sum_i d_i p^i (0 <= d_i < p), arithmetic modulo p and modulo the       */
+/* smallest monic irreducible polynomial of degree k over F_p (smallest by    */
+/* its lower coefficients read as the base-p number sum_i f_i p^i).  For k = 1 */
+/* this is the integers modulo p.  Returns 0, or -1 if q is not such a power. */
+#define GF_MAXK 16
+
+/* q = p^k with p prime and k >= 1: returns 1 and sets p, k. */
+static int prime_power(int q, int *p, int *k)
 {
     if (q < 2) return 0;
-    for (int d = 2; d * d <= q; ++d)
-        if (q % d == 0) return 0;
+    int d = 2;
+    while (q % d) ++d;              /* the smallest prime factor */
+    int e = 0, r = q;
+    while (r % d == 0) { r /= d; ++e; }
+    if (r != 1) return 0;
+    *p = d;
+    *k = e;
     return 1;
 }
 
-static int chi(int a, int q)
+typedef struct {
+    int p, k, q;
+    int f[GF_MAXK + 1];             /* monic modulus, f[k] = 1 */
+} gf_t;
+
+static void gf_digits(const gf_t *F, int e, int *d)
 {
-    a = ((a % q) + q) % q;
-    if (a == 0) return 0;
-    for (int x = 1; x < q; ++x)
-        if ((x * x) % q == a) return 1;
+    for (int i = 0; i < F->k; ++i) { d[i] = e % F->p; e /= F->p; }
+}
+
+static int gf_pack(const gf_t *F, const int *d)
+{
+    int e = 0;
+    for (int i = F->k - 1; i >= 0; --i) e = e * F->p + d[i];
+    return e;
+}
+
+static int gf_sub(const gf_t *F, int a, int b)
+{
+    int da[GF_MAXK], db[GF_MAXK];
+    gf_digits(F, a, da);
+    gf_digits(F, b, db);
+    for (int i = 0; i < F->k; ++i) da[i] = ((da[i] - db[i]) % F->p + F->p) % F->p;
+    return gf_pack(F, da);
+}
+
+static int gf_mul(const gf_t *F, int a, int b)
+{
+    const int p = F->p, k = F->k;
+    int da[GF_MAXK], db[GF_MAXK], c[2 * GF_MAXK] = {0};
+    gf_digits(F, a, da);
+    gf_digits(F, b, db);
+    for (int i = 0; i < k; ++i)
+        for (int j = 0; j < k; ++j) c[i + j] = (c[i + j] + da[i] * db[j]) % p;
+    /* t^d = t^(d-k) * t^k and t^k = -(f_0 + ... + f_(k-1) t^(k-1)) */
+    for (int d = 2 * k - 2; d >= k; --d) {
+        const int v = c[d];
+        c[d] = 0;
+        for (int i = 0; i < k; ++i) c[d - k + i] = ((c[d - k + i] - v * F->f[i]) % p + p) % p;
+    }
+    return gf_pack(F, c);
+}
+
+/* Whether the monic g of degree dg divides the monic f of degree k over F_p. */
+static int poly_divides(const int *g, int dg, const int *f, int k, int p)
+{
+    int r[GF_MAXK + 1];
+    for (int i = 0; i <= k; ++i) r[i] = f[i];
+    for (int d = k; d >= dg; --d) {
+        const int v = r[d];
+        if (!v) continue;
+        for (int i = 0; i <= dg; ++i) r[d - dg + i] = ((r[d - dg + i] - v * g[i]) % p + p) % p;
+    }
+    for (int i = 0; i < dg; ++i)
+        if (r[i]) return 0;
+    return 1;
+}
+
+/* Irreducible: no monic divisor of degree 1 .. k/2. */
+static int poly_irreducible(const int *f, int k, int p)
+{
+    int g[GF_MAXK + 1];
+    for (int dg = 1; 2 * dg <= k; ++dg) {
+        int count = 1;
+        for (int i = 0; i < dg; ++i) count *= p;
+        for (int c = 0; c < count; ++c) {
+            int v = c;
+            for (int i = 0; i < dg; ++i) { g[i] = v % p; v /= p; }
+            g[dg] = 1;
+            if (poly_divides(g, dg, f, k, p)) return 0;
+        }
+    }
+    return 1;
+}
+
+static int gf_init(gf_t *F, int q)
+{
+    int p, k;
+    if (!prime_power(q, &p, &k) || k > GF_MAXK) return -1;
+    F->p = p;
+    F->k = k;
+    F->q = q;
+    for (int c = 0; c < q; ++c) {   /* lower coefficients as a base-p number, ascending */
+        int v = c;
+        for (int i = 0; i < k; ++i) { F->f[i] = v % p; v /= p; }
+        F->f[k] = 1;
+        if (poly_irreducible(F->f, k, p)) return 0;
+    }
     return -1;
+}
+
+/* chi[e] for every element e of F_q, from the set of squares. */
+static int *gf_quadratic_character(const gf_t *F)
+{
+    int *chi = (int *)malloc(sizeof(int) * (size_t)F->q);
+    for (int e = 0; e < F->q; ++e) chi[e] = -1;
+    for (int x = 1; x < F->q; ++x) chi[gf_mul(F, x, x)] = 1;
+    chi[0] = 0;
+    return chi;
+}
+
+/* q is an odd prime power of the residue the Paley kind needs. */
+static int paley_q_ok(int q, int kind)
+{
+    int p, k;
+    if (q < 3 || q % 2 == 0 || !prime_power(q, &p, &k)) return 0;
+    return kind == 1 ? q % 4 == 3 : kind == 2 ? q % 4 == 1 : 0;
 }
 
 int orc_paley(int q, int kind, int8_t *H)
 {
-    if (!is_prime(q) || q == 2) return -1;
+    if (!paley_q_ok(q, kind)) return -1;
+    gf_t F;
+    if (gf_init(&F, q)) return -1;
+    int *chi = gf_quadratic_character(&F);
     const int n = q + 1;
+    /* matrix index i >= 1 stands for the field element x_(i-1) */
     if (kind == 1) {
-        if (q % 4 != 3) return -1;
         for (int i = 0; i < n; ++i)
             for (int j = 0; j < n; ++j) {
                 int s;
                 if (i == 0) s = j == 0 ? 0 : 1;
                 else if (j == 0) s = -1;
-                else s = chi(j - i, q);
+                else s = chi[gf_sub(&F, j - 1, i - 1)];
                 H[i * n + j] = (int8_t)((i == j ? 1 : 0) + s);
             }
-        return 0;
-    }
-    if (kind == 2) {
-        if (q % 4 != 1) return -1;
+    } else {
         const int m = 2 * n;
         for (int i = 0; i < n; ++i)
             for (int j = 0; j < n; ++j) {
                 int c;
                 if (i == 0 || j == 0) c = (i == j) ? 0 : 1;
-                else c = chi(j - i, q);
+                else c = chi[gf_sub(&F, j - 1, i - 1)];
                 for (int a = 0; a < 2; ++a)
                     for (int b = 0; b < 2; ++b) {
                         int v;
@@ -117,46 +230,79 @@ int orc_paley(int q, int kind, int8_t *H)
                         H[(2 * i + a) * m + 2 * j + b] = (int8_t)v;
                     }
             }
-        return 0;
     }
-    return -1;
+    free(chi);
+    return 0;
 }
 
-/* Base orders of the supported set: 1 and the Paley orders (Paley-I first    */
-/* where both give the same order).  The construction of order m is          */
-/* P_b (x) H~_(m/b) with the smallest base b such that m/b is a power of two; */
-/* returns b and its construction (kind 0: b = 1, else the Paley kind and q), */
-/* or -1 when m is not in the supported set.                                  */
+/* The supported set M_H: the Sylvester orders, the Paley orders, and         */
+/* Kronecker products of supported orders.  The construction of order m:     */
+/*  (1) if m = b * 2^j with b = 1 or a Paley order: P_b (x) H~_(m/b) for the   */
+/*      smallest such b (Paley-I preferred over Paley-II for the same b);     */
+/*  (2) else, if m = a * c with a and c supported, 1 < a <= c: H_a (x) H_c    */
+/*      for the smallest such a, each factor by this rule.                    */
+/* orc_hadamard_base returns the b of form (1) with its construction (kind 0: */
+/* b = 1, else the Paley kind and q), or -1 when m has no form (1).           */
 int orc_hadamard_base(int m, int *kind, int *q)
 {
     if (m < 1) return -1;
     for (int b = 1; b <= m; ++b) {
         if (m % b || !is_pow2(m / b)) continue;
         if (b == 1) { *kind = 0; *q = 0; return 1; }
-        if (is_prime(b - 1) && (b - 1) % 4 == 3) { *kind = 1; *q = b - 1; return b; }
-        if (b % 2 == 0 && is_prime(b / 2 - 1) && (b / 2 - 1) % 4 == 1) { *kind = 2; *q = b / 2 - 1; return b; }
+        if (paley_q_ok(b - 1, 1)) { *kind = 1; *q = b - 1; return b; }
+        if (b % 2 == 0 && paley_q_ok(b / 2 - 1, 2)) { *kind = 2; *q = b / 2 - 1; return b; }
     }
     return -1;
 }
 
-/* The Hadamard matrix of order m (row-major m*m): the Kronecker product      */
-/* P_b (x) H~_(m/b), index (a, j) -> a * (m/b) + j.  -1 if unsupported.        */
+static int supported(int m);
+
+/* The smallest a of form (2), or -1. */
+int orc_hadamard_split(int m)
+{
+    int kind, q;
+    if (m < 1 || orc_hadamard_base(m, &kind, &q) > 0) return -1;
+    for (int a = 2; a * a <= m; ++a)
+        if (m % a == 0 && supported(a) && supported(m / a)) return a;
+    return -1;
+}
+
+static int supported(int m)
+{
+    int kind, q;
+    return orc_hadamard_base(m, &kind, &q) > 0 || orc_hadamard_split(m) > 0;
+}
+
+/* The Hadamard matrix of order m (row-major m*m): form (1), index (a, j) ->  */
+/* a * (m/b) + j; form (2), index (i, j) -> i * c + j.  -1 if unsupported.     */
 int orc_hadamard(int m, int8_t *H)
 {
     int kind, q;
     const int b = orc_hadamard_base(m, &kind, &q);
-    if (b < 0) return -1;
-    const int s = m / b;
-    int8_t *P = (int8_t *)malloc((size_t)b * b);
-    int8_t *S = (int8_t *)malloc((size_t)s * s);
-    if (kind == 0) P[0] = 1;
-    else orc_paley(q, kind, P);
-    orc_sylvester(s, S);
-    for (int a = 0; a < b; ++a)
+    int8_t *P, *S;
+    int s;
+    if (b > 0) {
+        s = m / b;
+        P = (int8_t *)malloc((size_t)b * b);
+        S = (int8_t *)malloc((size_t)s * s);
+        if (kind == 0) P[0] = 1;
+        else orc_paley(q, kind, P);
+        orc_sylvester(s, S);
+    } else {
+        const int a = orc_hadamard_split(m);
+        if (a < 0) return -1;
+        s = m / a;
+        P = (int8_t *)malloc((size_t)a * a);
+        S = (int8_t *)malloc((size_t)s * s);
+        orc_hadamard(a, P);
+        orc_hadamard(s, S);
+    }
+    const int pb = m / s;
+    for (int a = 0; a < pb; ++a)
         for (int j = 0; j < s; ++j)
-            for (int c = 0; c < b; ++c)
+            for (int c = 0; c < pb; ++c)
                 for (int l = 0; l < s; ++l)
-                    H[(a * s + j) * m + c * s + l] = (int8_t)(P[a * b + c] * S[j * s + l]);
+                    H[(a * s + j) * m + c * s + l] = (int8_t)(P[a * pb + c] * S[j * s + l]);
     free(P);
     free(S);
     return 0;
@@ -168,16 +314,9 @@ int orc_order(int C, int mmax)
 {
     if (C < 1) return -1;
     const int c4 = 4 * ((C + 3) / 4);
-    int kind, q;
     for (int m = c4; m <= mmax; ++m)
-        if (orc_hadamard_base(m, &kind, &q) > 0) return m;
+        if (supported(m)) return m;
     return -1;
-}
-
-static int supported(int m)
-{
-    int kind, q;
-    return orc_hadamard_base(m, &kind, &q) > 0;
 }
 
 /* Dense block-diagonal transform along the last axis, fp64 in and out:       */

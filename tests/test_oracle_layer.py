@@ -246,3 +246,12 @@ def test_paired_transition_is_the_accumulator_basis(orc, name):
     S = orc.activation_transform(r.y, pw.hblock)
     assert np.abs(S - z).max() <= 2e-6 * np.abs(z).max()
     assert np.abs(S - z).max() > 0 or pw.hblock == 1          # not the same arithmetic
+    # the codes: those of z against the oracle's composition, the codes of
+    # fl32(B_next y) (Table I with the two transforms explicit), under the code
+    # rule (<= 1 LSB on <= 1e-4 of the elements) with scales within 2 ulps
+    if pw.hblock > 1:
+        qz, sz = orc.quantize_symmetric(z.astype(np.float32))
+        qs, ss = orc.quantize_symmetric(S)
+        assert np.all(np.abs(sz.astype(np.float64) / ss - 1) <= 2.5e-7)
+        d = np.abs(qz.astype(np.int32) - qs.astype(np.int32))
+        assert d.max() <= 1 and np.count_nonzero(d) <= 1e-4 * d.size
