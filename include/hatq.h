@@ -28,9 +28,10 @@
  *
  * Conventions for every entry point:
  *  - Tensors are NHWC, row-major, densely packed.  All tensor pointers are
- *    DEVICE pointers owned by the caller; the library never allocates, frees or
- *    synchronizes, and keeps no global state.  Calls are reentrant; calls on one
- *    stream execute in order.
+ *    DEVICE pointers owned by the caller (hatq_export_weights also takes host
+ *    destinations); the library never allocates, frees or synchronizes, and
+ *    keeps no global state.  Calls are reentrant; calls on one stream execute
+ *    in order.
  *  - `stream` is a hipStream_t (NULL = the default stream).  Some launch
  *    shapes (the persistent convolution grids) follow the CU count of the
  *    current device; results do not depend on them.
@@ -64,9 +65,22 @@ typedef enum {
     HATQ_OUT_I32 = 0,       /* raw INT32 accumulators [n][ho][wo][cout_pad], no bias;
                                WH accumulators stay in the output Hadamard basis */
     HATQ_OUT_F32 = 1,       /* dequantized fp32 output [n][ho][wo][cout], original basis */
-    HATQ_OUT_I8 = 2         /* the next operand's INT8 codes [n][ho][wo][cout]: produced by
-                               hatq_conv_int8_requant (hatq_conv_int8 rejects this mode) */
+    HATQ_OUT_I8 = 2         /* the next operand's INT8 codes [n][ho][wo][cout] (requantization,
+                               Eq. integer_requantization) */
 } hatq_out_mode;
+
+/* Flags of the convolution entry points (bitwise or; 0 = none).
+ *   HATQ_PAIRED: a WH layer whose next operand uses the same transform blocks
+ *     (next_hblock == hblock > 1) with nothing applied between the layers
+ *     (identity nonlinearity) may take the next operand through the cancellation
+ *     of Table I: B_next y = B_next (B_Cout z) / b = z, z the dequantized
+ *     accumulators before the output restore (Sylvester blocks square to b I).
+ *     Neither butterfly then runs: the next operand's absmax is max|z|, its
+ *     codes are those of z, and the integer transition uses B_next B_Cout = b I.
+ *     Without the flag both transforms run explicitly (the general Table I
+ *     transition, which a nonlinearity between the layers needs).  Ignored for
+ *     every other layer and output. */
+typedef enum { HATQ_PAIRED = 1 } hatq_conv_flags;
 
 /* One layer's geometry.  Square kernels only.
  *   conv:        ho = (h + 2*pad - k)/stride + 1
@@ -142,6 +156,17 @@ int32_t hatq_prepare_weights(const hatq_conv_desc *d, int32_t form, const float 
                              const float *bias, void *dst, size_t dst_bytes,
                              hatq_weights *out, void *stream);
 
+/* Copy prepared weights out in their documented layout (Eq. hadamard_linear_equivalence
+ * and Eq. weight_only_hadamard_equivalence: the transformed, quantized operator):
+ *   wq:      int8 [cout_pad][k][k][cin_pad], the codes of W' (row co holds
+ *            d = (kh*k + kw)*cin_pad + ci, as W->wq without its zero K padding);
+ *   w_scale: fp32 [cout_pad], s_w,c;  bias: fp32 [cout_pad] (WH: b~ = B_Cout [b; 0]).
+ * Destinations may be host or device memory (any of them NULL to skip it); the
+ * copies are enqueued on `stream` and host destinations hold the data once the
+ * caller has synchronized the stream (with pageable host memory the HIP runtime
+ * may complete the copy before returning). */
+int32_t hatq_export_weights(const hatq_weights *W, int8_t *wq, float *w_scale, float *bias, void *stream);
+
 /* Rebuild W->wpack from the codes in W->wq, for callers that write codes into
  * wq themselves (codes quantized elsewhere, e.g. loaded from a deployment
  * checkpoint, with w_scale and bias filled to match).  W must be a view returned
@@ -181,22 +206,29 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
  *     WH: z_c = fma(float(acc), fl(s_x*s_w,c), b~_c) (scale before the basis
  *         change, Supplementary "General Nonlinearities"), y = (B_Cout z)/b,
  *         truncated to cout.
+ *   mode HATQ_OUT_I8: y is int8 [n][ho][wo][cout], the next layer's codes
+ *     clamp(rne(fl32(y' / s))), y' = B_next y with blocks of next_hblock (1: y'
+ *     = y) and s = out_scale[n], a static per-sample scale (Eq.
+ *     integer_requantization); exactly hatq_conv_int8_requant with that static
+ *     scale.  y (fp32) itself is never written.
+ *   out_scale: device fp32 [n], required in I8 mode, NULL otherwise.
  *   next_hblock / next_absmax (F32 mode only): if next_absmax is non-NULL it
  *     receives, per sample, max |B_{next} y| with block size next_hblock (1: max
  *     |y|), the exact value hatq_fwht_quant_act would compute from y; the next
  *     layer can then quantize y reading it once.  It is overwritten, not
  *     accumulated.  y may be NULL in F32 mode when next_absmax is given: the
  *     call then only produces next_absmax (the first pass of
- *     hatq_conv_int8_requant's dynamic scale).  With y = NULL, a WH layer whose
- *     block equals next_hblock (> 1) takes the maximum of |z| instead, z the
- *     dequantized accumulators before the output restore: B_next y = z exactly
- *     there (the two transforms cancel, Table I), and no butterfly runs.
+ *     hatq_conv_int8_requant's dynamic scale).  With HATQ_PAIRED (see above)
+ *     a WH layer whose block equals next_hblock takes max |z| instead.
+ *   next_hblock (I8 mode): the next operand's transform block.
+ *   flags:     0 or HATQ_PAIRED.
  * Supported: cin_pad % 64 == 0 with k <= 8, or cin_pad <= 4 with k*k*cin_pad <= 128;
- * cout_pad % 64 == 0; WH block and next_hblock at most 64.  Transposed: stride 2.
- * xq and y must be 16-byte aligned. */
+ * cout_pad % 64 == 0; WH block and next_hblock at most 64 (I8: as
+ * hatq_conv_int8_requant).  Transposed: stride 2.  xq and y (F32, I32) must be
+ * 16-byte aligned, y in I8 mode 4-byte aligned. */
 int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act_scale,
-                       int32_t n, int32_t h, int32_t w, int32_t out_mode, void *y,
-                       int32_t next_hblock, float *next_absmax, void *stream);
+                       int32_t n, int32_t h, int32_t w, int32_t out_mode, const float *out_scale, void *y,
+                       int32_t next_hblock, float *next_absmax, int32_t flags, void *stream);
 
 /* INT8 convolution with the requantizing epilogue (step a6, I8 output; Eq.
  * integer_requantization with the dynamic per-tensor scale of Eq. symmetric_q):
@@ -205,22 +237,23 @@ int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act
  * y' = y, the WH input case), and quantized in registers,
  *   yq = clamp(rne(fl(y' / s)), -127, 127),
  * exactly as hatq_fwht_quant_act(y, ..., next_hblock, absmax = next_absmax)
- * would from y; y itself is never written.  A WH layer whose block equals
- * next_hblock (> 1) quantizes z, the dequantized accumulators before the
- * output restore, which equals B_next y exactly (Table I): the codes are those
- * of z (no butterfly), and can differ from the two-kernel path's by its fp32
- * rounding.
+ * would from y (the same fp32 butterflies in the same order, the same
+ * rounding); y itself is never written.  With HATQ_PAIRED a WH layer whose
+ * block equals next_hblock quantizes z instead (B_next y = z in exact
+ * arithmetic, Table I): the codes are those of z, and can differ from the
+ * explicit path's by the rounding of its two fp32 butterflies.
  *   next_absmax: device fp32 [n] with max |B_next y| per sample (from an
  *     earlier hatq_conv_int8 call with y = NULL, or an upper bound of it); the
  *     scale is then s = fl32(next_absmax / 127) (1 if it is 0) and is written to
  *     next_scale.  NULL: next_scale [n] is an input, a static scale.
  *   next_scale: device fp32 [n], the next layer's act_scale.
  *   yq:        device int8 [n][ho][wo][cout], the next layer's xq.
+ *   flags:     0 or HATQ_PAIRED.
  * Supported: as hatq_conv_int8, with cout % 4 == 0 and cout % next_hblock == 0. */
 int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const float *act_scale,
                                int32_t n, int32_t h, int32_t w, int32_t next_hblock,
                                const float *next_absmax, float *next_scale, int8_t *yq,
-                               void *stream);
+                               int32_t flags, void *stream);
 
 /* Affine activation quantization (Eq. affine_q, Eq. uniform_q), the dynamic
  * per-sample form of the paper's PTQ setting, on the signed grid [-128, 127]
@@ -283,9 +316,10 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
  *   A_max = k*k*cin_pad*127^2 + max|b_int|, G = (WH: hblock) * next_hblock:
  *   every int64 sum of the transition is then exact.  fp64 arithmetic with
  *   correctly rounded division.
- *   shift: NULL or host int32 receiving n.
- *   Waits for the stream (the status depends on the result): HATQ_EUNSUPPORTED
- *   if no shift fits (or |b_int| >= 2^30), then n = -1 in the table.
+ *   Enqueued on `stream` like every other call (it does not wait): when no
+ *   shift fits (or |b_int| >= 2^30) the table holds n = -1 and every M_c = 0,
+ *   which the caller reads back after its own synchronization; a transition
+ *   with such a table writes all-zero codes.
  *
  * hatq_conv_int8_int_transition: convolution plus the integer epilogue,
  *   p = M (.) (acc + b_int) in int64, v = B_Cout p (WH; truncated to cout),
@@ -293,13 +327,15 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
  *   with rne rounding exact halves to even; no act_scale (it is inside M).
  *   table: as written by hatq_int_transition_params for W and next_hblock.
  *   yq:    device int8 [n][ho][wo][cout], the next layer's codes.
+ *   flags: 0 or HATQ_PAIRED (a WH layer whose block equals next_hblock then
+ *          uses B_next B_Cout = b I: bit-identical codes, no butterflies).
  *   Supported: as hatq_conv_int8_requant. */
 size_t hatq_int_table_len(const hatq_weights *W);
 int32_t hatq_int_transition_params(const hatq_weights *W, float s_x, float s_y, int32_t next_hblock,
-                                   int32_t *table, int32_t *shift, void *stream);
+                                   int32_t *table, void *stream);
 int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, int32_t n, int32_t h,
                                       int32_t w, int32_t next_hblock, const int32_t *table,
-                                      int8_t *yq, void *stream);
+                                      int8_t *yq, int32_t flags, void *stream);
 
 /* Range-expansion profiling (Eq. hadamard_sensitivity): for each sample k of
  * a layer's input x, whether the layer's input-side transform enlarges the

@@ -61,6 +61,7 @@ def lib():
         L = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p
         i32, i64 = ctypes.c_int, ctypes.c_int64
+        L.orc_set_threads.argtypes = [i32]
         L.orc_sylvester.argtypes = [i32, P]
         L.orc_block_transform_f64.argtypes = [i32, P, P, i64, i32]
         L.orc_activation_transform.argtypes = [P, i64, i32, i32, P]
@@ -94,6 +95,12 @@ def _p(a: Optional[np.ndarray]):
 
 def _c(a, dtype):
     return np.ascontiguousarray(a, dtype=dtype)
+
+
+def set_threads(n: int = 0) -> int:
+    """Set the OpenMP thread count of the oracle's loops (n <= 0: leave it);
+    returns the count in effect."""
+    return int(lib().orc_set_threads(int(n)))
 
 
 def round_up(v: int, m: int) -> int:

@@ -32,9 +32,19 @@
  * and quotient below is a single correctly rounded IEEE operation.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* Thread count of the OpenMP loops below (timing of the oracle as a CPU     */
+/* baseline; results do not depend on it: every parallel loop writes disjoint */
+/* outputs and reduces only with max).  Returns the count now in effect.      */
+int orc_set_threads(int n)
+{
+    if (n > 0) omp_set_num_threads(n);
+    return omp_get_max_threads();
+}
 
 static int is_pow2(int b) { return b >= 1 && (b & (b - 1)) == 0; }
 static int round_up(int v, int m) { return (v + m - 1) / m * m; }

@@ -126,7 +126,7 @@ int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next
 // row i + (ph + pad - kh)/2 (gather form of the transposed convolution).
 int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, int32_t n,
                       int32_t h, int32_t w, int32_t mode, void *y, int32_t next_hblock,
-                      float *next_absmax, hipStream_t st, const float *q_absmax = nullptr,
+                      float *next_absmax, int32_t flags, hipStream_t st, const float *q_absmax = nullptr,
                       float *q_scale = nullptr, const int32_t *rq_table = nullptr,
                       const int32_t *zx = nullptr, const int32_t *tapsum = nullptr) {
     const hatq_conv_desc &d = W->d;
@@ -162,6 +162,7 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
     a.mode = mode;
     a.hblock = d.hblock;
     a.next_hblock = (next_absmax || mode >= HATQ_OUT_I8) ? next_hblock : 0;
+    a.paired = (flags & HATQ_PAIRED) ? 1 : 0;
     const bool small = W->cin_pad <= 4 && W->k_total <= 128;
     if (!d.transposed) {
         a.gh = ho;
@@ -311,6 +312,19 @@ int32_t hatq_pack_weights(const hatq_weights *W, void *stream) {
     return hip_status(hatq::launch_pack(a, static_cast<hipStream_t>(stream)));
 }
 
+int32_t hatq_export_weights(const hatq_weights *W, int8_t *wq, float *w_scale, float *bias, void *stream) {
+    const int32_t s = check_weights(W);
+    if (s != HATQ_OK) return s;
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    if (wq && hipMemcpy2DAsync(wq, (size_t)W->k_total, W->wq, (size_t)W->k_stride, (size_t)W->k_total,
+                               (size_t)W->cout_pad, hipMemcpyDefault, st) != hipSuccess)
+        return HATQ_EHIP;
+    const size_t cb = (size_t)W->cout_pad * sizeof(float);
+    if (w_scale && hipMemcpyAsync(w_scale, W->w_scale, cb, hipMemcpyDefault, st) != hipSuccess) return HATQ_EHIP;
+    if (bias && hipMemcpyAsync(bias, W->bias, cb, hipMemcpyDefault, st) != hipSuccess) return HATQ_EHIP;
+    return HATQ_OK;
+}
+
 size_t hatq_fwht_quant_ws_bytes(int32_t n) { return n > 0 ? align256((size_t)n * 4) : 0; }
 
 int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
@@ -330,31 +344,17 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
                                              act_scale, static_cast<hipStream_t>(stream)));
 }
 
-int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act_scale, int32_t n, int32_t h,
-                       int32_t w, int32_t out_mode, void *y, int32_t next_hblock, float *next_absmax,
-                       void *stream) {
-    int32_t s = check_weights(W);
-    if (s != HATQ_OK) return s;
-    if (!xq || !act_scale || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
-    if (out_mode != HATQ_OUT_I32 && out_mode != HATQ_OUT_F32) return HATQ_EINVAL;
-    if (out_mode == HATQ_OUT_I32 && next_absmax) return HATQ_EINVAL;
-    // y may be NULL only when the call is for next_absmax alone
-    if (!y && !(out_mode == HATQ_OUT_F32 && next_absmax)) return HATQ_EINVAL;
-    if (!aligned(xq, 16) || (y && !aligned(y, 16)) || !aligned(act_scale, 4)) return HATQ_EINVAL;
-    if ((s = check_conv_supported(W)) != HATQ_OK) return s;
-    if ((s = check_next(W, next_hblock, next_absmax)) != HATQ_OK) return s;
-    int32_t ho, wo;
-    if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
-    return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, next_hblock, next_absmax,
-                         static_cast<hipStream_t>(stream));
-}
+namespace {
 
-int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const float *act_scale, int32_t n,
-                               int32_t h, int32_t w, int32_t next_hblock, const float *next_absmax,
-                               float *next_scale, int8_t *yq, void *stream) {
+// The requantizing epilogue (I8 output): dynamic scale from next_absmax, or the
+// static scale in next_scale.
+int32_t requant(const hatq_weights *W, const int8_t *xq, const float *act_scale, int32_t n, int32_t h, int32_t w,
+                int32_t next_hblock, const float *next_absmax, float *next_scale, int8_t *yq, int32_t flags,
+                void *stream) {
     int32_t s = check_weights(W);
     if (s != HATQ_OK) return s;
     if (!xq || !act_scale || !next_scale || !yq || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
+    if (flags & ~HATQ_PAIRED) return HATQ_EINVAL;
     if (!aligned(xq, 16) || !aligned(yq, 4) || !aligned(act_scale, 4) || !aligned(next_scale, 4))
         return HATQ_EINVAL;
     if (next_absmax && !aligned(next_absmax, 4)) return HATQ_EINVAL;
@@ -366,8 +366,43 @@ int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const fl
     if (W->d.cout % 4) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
-    return conv_launches(W, xq, act_scale, n, h, w, HATQ_OUT_I8, yq, next_hblock, nullptr,
+    return conv_launches(W, xq, act_scale, n, h, w, HATQ_OUT_I8, yq, next_hblock, nullptr, flags,
                          static_cast<hipStream_t>(stream), next_absmax, next_scale);
+}
+
+}  // namespace
+
+int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act_scale, int32_t n, int32_t h,
+                       int32_t w, int32_t out_mode, const float *out_scale, void *y, int32_t next_hblock,
+                       float *next_absmax, int32_t flags, void *stream) {
+    int32_t s = check_weights(W);
+    if (s != HATQ_OK) return s;
+    if (!xq || !act_scale || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
+    if (flags & ~HATQ_PAIRED) return HATQ_EINVAL;
+    if (out_mode == HATQ_OUT_I8) {
+        // requantization with a static per-sample scale (read, never written)
+        if (!out_scale || !y || next_absmax) return HATQ_EINVAL;
+        return requant(W, xq, act_scale, n, h, w, next_hblock, nullptr, const_cast<float *>(out_scale),
+                       static_cast<int8_t *>(y), flags, stream);
+    }
+    if (out_mode != HATQ_OUT_I32 && out_mode != HATQ_OUT_F32) return HATQ_EINVAL;
+    if (out_scale) return HATQ_EINVAL;
+    if (out_mode == HATQ_OUT_I32 && next_absmax) return HATQ_EINVAL;
+    // y may be NULL only when the call is for next_absmax alone
+    if (!y && !(out_mode == HATQ_OUT_F32 && next_absmax)) return HATQ_EINVAL;
+    if (!aligned(xq, 16) || (y && !aligned(y, 16)) || !aligned(act_scale, 4)) return HATQ_EINVAL;
+    if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    if ((s = check_next(W, next_hblock, next_absmax)) != HATQ_OK) return s;
+    int32_t ho, wo;
+    if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
+    return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, next_hblock, next_absmax, flags,
+                         static_cast<hipStream_t>(stream));
+}
+
+int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const float *act_scale, int32_t n,
+                               int32_t h, int32_t w, int32_t next_hblock, const float *next_absmax,
+                               float *next_scale, int8_t *yq, int32_t flags, void *stream) {
+    return requant(W, xq, act_scale, n, h, w, next_hblock, next_absmax, next_scale, yq, flags, stream);
 }
 
 size_t hatq_fwht_quant_affine_ws_bytes(int32_t n) { return n > 0 ? align256((size_t)n * 8) : 0; }
@@ -422,7 +457,7 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
     if (!is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
-    return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, 0, nullptr, static_cast<hipStream_t>(stream),
+    return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, 0, nullptr, 0, static_cast<hipStream_t>(stream),
                          nullptr, nullptr, nullptr, act_zero, tapsum);
 }
 
@@ -432,7 +467,7 @@ size_t hatq_int_table_len(const hatq_weights *W) {
 }
 
 int32_t hatq_int_transition_params(const hatq_weights *W, float s_x, float s_y, int32_t next_hblock,
-                                   int32_t *table, int32_t *shift, void *stream) {
+                                   int32_t *table, void *stream) {
     int32_t s = check_weights(W);
     if (s != HATQ_OK) return s;
     if (!table || !aligned(table, 16)) return HATQ_EINVAL;
@@ -451,21 +486,16 @@ int32_t hatq_int_transition_params(const hatq_weights *W, float s_x, float s_y, 
     a.beta_out = dh ? 1 : W->d.hblock;
     a.K = W->d.k * W->d.k * W->cin_pad;
     a.gain = a.beta_out * next_hblock;
-    const hipStream_t st = static_cast<hipStream_t>(stream);
-    if (hatq::launch_int_params(a, st) != hipSuccess) return HATQ_EHIP;
-    int32_t n = -1;
-    if (hipMemcpyAsync(&n, table + 2 * W->cout_pad, sizeof(n), hipMemcpyDeviceToHost, st) != hipSuccess ||
-        hipStreamSynchronize(st) != hipSuccess)
-        return HATQ_EHIP;
-    if (shift) *shift = n;
-    return n >= 0 ? HATQ_OK : HATQ_EUNSUPPORTED;
+    return hip_status(hatq::launch_int_params(a, static_cast<hipStream_t>(stream)));
 }
 
 int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, int32_t n, int32_t h, int32_t w,
-                                      int32_t next_hblock, const int32_t *table, int8_t *yq, void *stream) {
+                                      int32_t next_hblock, const int32_t *table, int8_t *yq, int32_t flags,
+                                      void *stream) {
     int32_t s = check_weights(W);
     if (s != HATQ_OK) return s;
     if (!xq || !table || !yq || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
+    if (flags & ~HATQ_PAIRED) return HATQ_EINVAL;
     if (!aligned(xq, 16) || !aligned(yq, 4) || !aligned(table, 16)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
     if (!is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
@@ -473,7 +503,7 @@ int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, i
     if (W->d.cout % 4) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
-    return conv_launches(W, xq, nullptr, n, h, w, hatq::kModeIntTransition, yq, next_hblock, nullptr,
+    return conv_launches(W, xq, nullptr, n, h, w, hatq::kModeIntTransition, yq, next_hblock, nullptr, flags,
                          static_cast<hipStream_t>(stream), nullptr, nullptr, table);
 }
 
@@ -528,7 +558,7 @@ int32_t hatq_layer_forward(const hatq_weights *W, int32_t form, const float *x, 
     hipStream_t st = static_cast<hipStream_t>(stream);
     const int64_t E = (int64_t)h * w * W->d.cin;
     if (hatq::launch_act_quant(x, n, E, hb_act, x_absmax, amax, xq, sx, st) != hipSuccess) return HATQ_EHIP;
-    return conv_launches(W, xq, sx, n, h, w, HATQ_OUT_F32, y, next_hblock, next_absmax, st);
+    return conv_launches(W, xq, sx, n, h, w, HATQ_OUT_F32, y, next_hblock, next_absmax, 0, st);
 }
 
 }  // extern "C"

@@ -409,10 +409,12 @@ struct Epilogue {
             seen = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(seen)));
         }
         nbk = generic ? a.next_hblock : NB;
-        // WH layer whose next operand uses the same blocks: B y = B (B z / b) = z
-        // exactly, so max|B y| <= max|z| (1 + 2 gamma_6 * 64) with gamma_6 the
-        // six-stage fp32 rounding factor (< 3.6e-7); 1 + 1e-4 covers it.
-        z_bound = fl.wh && (generic ? a.hblock == a.next_hblock : WB == NB);
+        // WH layer whose next operand uses the same blocks, with the paired
+        // cancellation allowed (identity between the layers): B y = B (B z / b)
+        // = z exactly, so max|B y| <= max|z| (1 + 2 gamma_6 * 64) with gamma_6
+        // the six-stage fp32 rounding factor (< 3.6e-7); 1 + 1e-4 covers it.
+        // Without it every group runs both transforms.
+        z_bound = a.paired && fl.wh && (generic ? a.hblock == a.next_hblock : WB == NB);
         // With no fp32 output to store, the next operand of such a layer is z
         // itself (B_next y = B B z / b = z in exact arithmetic): its maximum and
         // its codes are taken from z, and neither butterfly runs.
@@ -441,7 +443,7 @@ struct Epilogue {
         if (fl.iq) {
             int n = __builtin_amdgcn_readfirstlane(a.rq_table[2 * a.cout_pad]);
             n = n < 0 ? 0 : (n > 62 ? 62 : n);   // the parameter call keeps n in [0, 62]
-            rq_pair = fl.wh && (generic ? a.hblock == a.next_hblock : WB == NB) && a.hblock > 1;
+            rq_pair = a.paired && fl.wh && (generic ? a.hblock == a.next_hblock : WB == NB) && a.hblock > 1;
             if (rq_pair) {
                 const int lg = 31 - __builtin_clz(a.hblock);
                 rq_pre = lg > n ? lg - n : 0;

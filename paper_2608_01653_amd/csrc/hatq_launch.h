@@ -62,6 +62,9 @@ struct ConvArgs {
                            // 3 the same codes by the integer transition (rq_table)
     int32_t hblock;        // the layer's block size
     int32_t next_hblock;   // 0 = no next-operand absmax
+    int32_t paired;        // 1: a WH layer with next_hblock == hblock takes the next operand
+                           // as z (B_next B_Cout = b I with identity nonlinearity); 0: both
+                           // transforms run
     int32_t tiles_h, tiles_w, tiles_n;   // 2-D tiles of grid points per sample; column tiles
     int32_t n_base;        // first output column of a launch over a column range, else 0
     int32_t run_tiles;     // row-run kernel: tiles per block (set at launch)

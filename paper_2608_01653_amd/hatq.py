@@ -21,6 +21,7 @@ from . import build as _build
 HATQ_OK, HATQ_EINVAL, HATQ_EUNSUPPORTED, HATQ_EWORKSPACE, HATQ_EHIP = range(5)
 HATQ_DH, HATQ_WH = 0, 1
 HATQ_OUT_I32, HATQ_OUT_F32, HATQ_OUT_I8 = 0, 1, 2
+HATQ_PAIRED = 1
 FORMS = {"DH": HATQ_DH, "WH": HATQ_WH}
 
 
@@ -45,7 +46,7 @@ class Weights(ctypes.Structure):
 
 
 EXPORTS = ["hatq_status_string", "hatq_conv_out_hw", "hatq_weights_bytes", "hatq_prepare_weights",
-           "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act", "hatq_conv_int8",
+           "hatq_export_weights", "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act", "hatq_conv_int8",
            "hatq_conv_int8_requant", "hatq_int_table_len", "hatq_int_transition_params",
            "hatq_conv_int8_int_transition", "hatq_range_expansion", "hatq_select_form",
            "hatq_fwht_quant_affine_ws_bytes", "hatq_fwht_quant_act_affine", "hatq_tapsum_len",
@@ -79,22 +80,23 @@ def load(build_if_missing: bool = False):
     L.hatq_weights_bytes.restype = sz
     L.hatq_prepare_weights.argtypes = [ctypes.POINTER(ConvDesc), i32, P, P, P, sz, ctypes.POINTER(Weights), P]
     L.hatq_prepare_weights.restype = i32
+    L.hatq_export_weights.argtypes = [ctypes.POINTER(Weights), P, P, P, P]
+    L.hatq_export_weights.restype = i32
     L.hatq_pack_weights.argtypes = [ctypes.POINTER(Weights), P]
     L.hatq_pack_weights.restype = i32
     L.hatq_fwht_quant_ws_bytes.argtypes = [i32]
     L.hatq_fwht_quant_ws_bytes.restype = sz
     L.hatq_fwht_quant_act.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P, sz, P]
     L.hatq_fwht_quant_act.restype = i32
-    L.hatq_conv_int8.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, i32, P, P]
+    L.hatq_conv_int8.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, P, i32, P, i32, P]
     L.hatq_conv_int8.restype = i32
-    L.hatq_conv_int8_requant.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, P, P, P]
+    L.hatq_conv_int8_requant.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, P, P, i32, P]
     L.hatq_conv_int8_requant.restype = i32
     L.hatq_int_table_len.argtypes = [ctypes.POINTER(Weights)]
     L.hatq_int_table_len.restype = sz
-    L.hatq_int_transition_params.argtypes = [ctypes.POINTER(Weights), ctypes.c_float, ctypes.c_float, i32, P,
-                                             ctypes.POINTER(i32), P]
+    L.hatq_int_transition_params.argtypes = [ctypes.POINTER(Weights), ctypes.c_float, ctypes.c_float, i32, P, P]
     L.hatq_int_transition_params.restype = i32
-    L.hatq_conv_int8_int_transition.argtypes = [ctypes.POINTER(Weights), P, i32, i32, i32, i32, P, P, P]
+    L.hatq_conv_int8_int_transition.argtypes = [ctypes.POINTER(Weights), P, i32, i32, i32, i32, P, P, i32, P]
     L.hatq_conv_int8_int_transition.restype = i32
     L.hatq_range_expansion.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P]
     L.hatq_fwht_quant_affine_ws_bytes.argtypes = [i32]
@@ -136,6 +138,32 @@ def _ptr(t: Optional[torch.Tensor]):
     if not t.is_contiguous():
         raise ValueError("contiguous tensor expected")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _need(t: Optional[torch.Tensor], name: str, dtype: torch.dtype, numel: int, optional: bool = False):
+    """Raise ValueError unless t is a contiguous device tensor of `dtype` with at
+    least `numel` elements (the library trusts the pointers it is given)."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name}: tensor required")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: device tensor expected")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: {dtype} expected, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: contiguous tensor expected")
+    if t.numel() < numel:
+        raise ValueError(f"{name}: {numel} elements needed, got {t.numel()}")
+
+
+def _nhwc(t: torch.Tensor, name: str, dtype: torch.dtype, channels: Optional[int] = None):
+    if t.dim() != 4:
+        raise ValueError(f"{name}: NHWC tensor expected, got shape {tuple(t.shape)}")
+    if channels is not None and t.shape[3] != channels:
+        raise ValueError(f"{name}: {channels} channels expected, got {t.shape[3]}")
+    _need(t, name, dtype, 0)
+    return t.shape
 
 
 def _stream(stream=None):
@@ -208,9 +236,26 @@ def hatq_prepare_weights(d: ConvDesc, form, w: torch.Tensor, bias: Optional[torc
     out = Weights()
     w = w.contiguous().float()
     b = None if bias is None else bias.contiguous().float()
+    _need(w, "w", torch.float32, d.cout * d.cin * d.k * d.k)
+    _need(b, "bias", torch.float32, d.cout, optional=True)
     _check(load().hatq_prepare_weights(ctypes.byref(d), f, _ptr(w), _ptr(b), _ptr(buf), nbytes,
                                        ctypes.byref(out), _stream(stream)), "hatq_prepare_weights")
     return PreparedLayer(buf, out, f)
+
+
+def hatq_export_weights(layer: PreparedLayer, stream=None):
+    """Host copies of the prepared operator: (codes int8 [cout_pad, k, k, cin_pad],
+    w_scale fp32 [cout_pad], bias fp32 [cout_pad]); waits for the stream."""
+    k, cp, co = layer.w.d.k, layer.w.cin_pad, layer.w.cout_pad
+    wq = torch.empty((co, k, k, cp), dtype=torch.int8, pin_memory=True)
+    sc = torch.empty(co, dtype=torch.float32, pin_memory=True)
+    b = torch.empty(co, dtype=torch.float32, pin_memory=True)
+    s = stream if stream is not None else torch.cuda.current_stream()
+    _check(load().hatq_export_weights(ctypes.byref(layer.w), ctypes.c_void_p(wq.data_ptr()),
+                                      ctypes.c_void_p(sc.data_ptr()), ctypes.c_void_p(b.data_ptr()), _stream(s)),
+           "hatq_export_weights")
+    s.synchronize()
+    return wq, sc, b
 
 
 def hatq_pack_weights(layer: PreparedLayer, stream=None) -> None:
@@ -223,54 +268,77 @@ def hatq_fwht_quant_act(x: torch.Tensor, hblock: int, absmax: Optional[torch.Ten
                         ws: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """x fp32 NHWC -> (int8 codes NHWC, per-sample scale fp32 [n]).  Output and
     workspace tensors may be passed in to avoid allocation."""
-    n, h, w, c = x.shape
+    n, h, w, c = _nhwc(x, "x", torch.float32)
     if xq is None:
         xq = torch.empty((n, h, w, c), dtype=torch.int8, device=x.device)
     sc = scale if scale is not None else torch.empty(n, dtype=torch.float32, device=x.device)
+    _need(xq, "xq", torch.int8, x.numel())
+    _need(sc, "scale", torch.float32, n)
+    _need(absmax, "absmax", torch.float32, n, optional=True)
     wsb = int(load().hatq_fwht_quant_ws_bytes(n))
     if ws is None:
         ws = torch.empty(max(wsb, 4), dtype=torch.int8, device=x.device)
+    _need(ws, "ws", torch.int8, 0)
     wsb = ws.numel()
     _check(load().hatq_fwht_quant_act(_ptr(x), n, h, w, c, int(hblock), _ptr(absmax), _ptr(xq), _ptr(sc),
                                       _ptr(ws), wsb, _stream(stream)), "hatq_fwht_quant_act")
     return xq, sc
 
 
+def _flags(paired: bool) -> int:
+    return HATQ_PAIRED if paired else 0
+
+
 def hatq_conv_int8(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tensor, out_mode=HATQ_OUT_F32,
                    next_hblock: int = 0, next_absmax: Optional[torch.Tensor] = None, y=None, stream=None,
-                   absmax_only: bool = False):
-    """absmax_only: F32 mode with y = NULL, producing next_absmax alone (returns None)."""
-    n, h, w, _ = xq.shape
+                   absmax_only: bool = False, out_scale: Optional[torch.Tensor] = None, paired: bool = False):
+    """absmax_only: F32 mode with y = NULL, producing next_absmax alone (returns None).
+    out_mode HATQ_OUT_I8: y receives the next operand's codes with the static
+    per-sample scale out_scale.  paired: the HATQ_PAIRED flag."""
+    n, h, w, _ = _nhwc(xq, "xq", torch.int8, layer.w.cin_pad)
+    _need(act_scale, "act_scale", torch.float32, n)
+    _need(next_absmax, "next_absmax", torch.float32, n, optional=True)
+    _need(out_scale, "out_scale", torch.float32, n, optional=True)
     ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
     if absmax_only:
         _check(load().hatq_conv_int8(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), n, h, w, int(out_mode),
-                                     None, int(next_hblock), _ptr(next_absmax), _stream(stream)),
+                                     _ptr(out_scale), None, int(next_hblock), _ptr(next_absmax), _flags(paired),
+                                     _stream(stream)),
                "hatq_conv_int8")
         return None
+    if out_mode == HATQ_OUT_I32:
+        shape, dt = (n, ho, wo, layer.w.cout_pad), torch.int32
+    elif out_mode == HATQ_OUT_I8:
+        shape, dt = (n, ho, wo, layer.w.d.cout), torch.int8
+    else:
+        shape, dt = (n, ho, wo, layer.w.d.cout), torch.float32
     if y is None:
-        if out_mode == HATQ_OUT_I32:
-            y = torch.empty((n, ho, wo, layer.w.cout_pad), dtype=torch.int32, device=xq.device)
-        else:
-            y = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.float32, device=xq.device)
+        y = torch.empty(shape, dtype=dt, device=xq.device)
+    _need(y, "y", dt, n * ho * wo * shape[3])
     _check(load().hatq_conv_int8(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), n, h, w, int(out_mode),
-                                 _ptr(y), int(next_hblock), _ptr(next_absmax), _stream(stream)),
+                                 _ptr(out_scale), _ptr(y), int(next_hblock), _ptr(next_absmax), _flags(paired),
+                                 _stream(stream)),
            "hatq_conv_int8")
     return y
 
 
 def hatq_conv_int8_requant(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tensor, next_hblock: int,
                            next_absmax: Optional[torch.Tensor] = None, next_scale: Optional[torch.Tensor] = None,
-                           yq: Optional[torch.Tensor] = None, stream=None):
+                           yq: Optional[torch.Tensor] = None, stream=None, paired: bool = False):
     """Conv with the requantizing epilogue: returns (yq, next_scale), the next layer's codes and scale."""
-    n, h, w, _ = xq.shape
+    n, h, w, _ = _nhwc(xq, "xq", torch.int8, layer.w.cin_pad)
+    _need(act_scale, "act_scale", torch.float32, n)
+    _need(next_absmax, "next_absmax", torch.float32, n, optional=True)
     ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
     if yq is None:
         yq = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.int8, device=xq.device)
     if next_scale is None:
         next_scale = torch.empty((n,), dtype=torch.float32, device=xq.device)
+    _need(yq, "yq", torch.int8, n * ho * wo * layer.w.d.cout)
+    _need(next_scale, "next_scale", torch.float32, n)
     _check(load().hatq_conv_int8_requant(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), n, h, w,
                                          int(next_hblock), _ptr(next_absmax), _ptr(next_scale), _ptr(yq),
-                                         _stream(stream)),
+                                         _flags(paired), _stream(stream)),
            "hatq_conv_int8_requant")
     return yq, next_scale
 
@@ -281,25 +349,32 @@ def hatq_int_table_len(layer: PreparedLayer) -> int:
 
 def hatq_int_transition_params(layer: PreparedLayer, s_x: float, s_y: float, next_hblock: int,
                                table: Optional[torch.Tensor] = None, device="cuda", stream=None):
-    """Integer transition table (M, b_int, shift) from static scales: returns (table, shift)."""
+    """Integer transition table (M, b_int, shift) from static scales: returns
+    (table, shift).  The library call does not wait; this wrapper reads the shift
+    back (-1: none fits, then the call is reported as HATQ_EUNSUPPORTED here)."""
     if table is None:
         table = torch.empty((hatq_int_table_len(layer),), dtype=torch.int32, device=device)
-    n = ctypes.c_int32(-1)
+    _need(table, "table", torch.int32, hatq_int_table_len(layer))
     _check(load().hatq_int_transition_params(ctypes.byref(layer.w), float(s_x), float(s_y), int(next_hblock),
-                                             _ptr(table), ctypes.byref(n), _stream(stream)),
+                                             _ptr(table), _stream(stream)),
            "hatq_int_transition_params")
-    return table, int(n.value)
+    shift = int(table[2 * layer.w.cout_pad].item())
+    if shift < 0:
+        raise HatqError(HATQ_EUNSUPPORTED, "hatq_int_transition_params (no shift fits)")
+    return table, shift
 
 
 def hatq_conv_int8_int_transition(layer: PreparedLayer, xq: torch.Tensor, next_hblock: int, table: torch.Tensor,
-                                  yq: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+                                  yq: Optional[torch.Tensor] = None, stream=None, paired: bool = False) -> torch.Tensor:
     """Conv with the integer-only epilogue: the next layer's codes."""
-    n, h, w, _ = xq.shape
+    n, h, w, _ = _nhwc(xq, "xq", torch.int8, layer.w.cin_pad)
+    _need(table, "table", torch.int32, hatq_int_table_len(layer))
     ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
     if yq is None:
         yq = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.int8, device=xq.device)
+    _need(yq, "yq", torch.int8, n * ho * wo * layer.w.d.cout)
     _check(load().hatq_conv_int8_int_transition(ctypes.byref(layer.w), _ptr(xq), n, h, w, int(next_hblock),
-                                                _ptr(table), _ptr(yq), _stream(stream)),
+                                                _ptr(table), _ptr(yq), _flags(paired), _stream(stream)),
            "hatq_conv_int8_int_transition")
     return yq
 
@@ -308,7 +383,7 @@ def hatq_fwht_quant_act_affine(x: torch.Tensor, hblock: int, xq: Optional[torch.
                                scale: Optional[torch.Tensor] = None, zero: Optional[torch.Tensor] = None,
                                ws: Optional[torch.Tensor] = None, stream=None):
     """x fp32 NHWC -> (int8 codes, per-sample scale fp32 [n], zero point int32 [n])."""
-    n, h, w, c = x.shape
+    n, h, w, c = _nhwc(x, "x", torch.float32)
     if xq is None:
         xq = torch.empty((n, h, w, c), dtype=torch.int8, device=x.device)
     if scale is None:
@@ -317,27 +392,38 @@ def hatq_fwht_quant_act_affine(x: torch.Tensor, hblock: int, xq: Optional[torch.
         zero = torch.empty(n, dtype=torch.int32, device=x.device)
     if ws is None:
         ws = torch.empty(int(load().hatq_fwht_quant_affine_ws_bytes(n)), dtype=torch.int8, device=x.device)
+    _need(xq, "xq", torch.int8, x.numel())
+    _need(scale, "scale", torch.float32, n)
+    _need(zero, "zero", torch.int32, n)
+    _need(ws, "ws", torch.int8, 0)
     _check(load().hatq_fwht_quant_act_affine(_ptr(x), n, h, w, c, int(hblock), _ptr(xq), _ptr(scale), _ptr(zero),
                                              _ptr(ws), ws.numel(), _stream(stream)), "hatq_fwht_quant_act_affine")
     return xq, scale, zero
 
 
 def hatq_weight_tapsums(layer: PreparedLayer, tapsum: Optional[torch.Tensor] = None, device="cuda", stream=None):
+    need = int(load().hatq_tapsum_len(ctypes.byref(layer.w)))
     if tapsum is None:
-        tapsum = torch.empty(int(load().hatq_tapsum_len(ctypes.byref(layer.w))), dtype=torch.int32, device=device)
+        tapsum = torch.empty(need, dtype=torch.int32, device=device)
+    _need(tapsum, "tapsum", torch.int32, need)
     _check(load().hatq_weight_tapsums(ctypes.byref(layer.w), _ptr(tapsum), _stream(stream)), "hatq_weight_tapsums")
     return tapsum
 
 
 def hatq_conv_int8_affine(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tensor, act_zero: torch.Tensor,
                           tapsum: torch.Tensor, out_mode=HATQ_OUT_F32, y=None, stream=None) -> torch.Tensor:
-    n, h, w, _ = xq.shape
+    n, h, w, _ = _nhwc(xq, "xq", torch.int8, layer.w.cin_pad)
+    _need(act_scale, "act_scale", torch.float32, n)
+    _need(act_zero, "act_zero", torch.int32, n)
+    _need(tapsum, "tapsum", torch.int32, int(load().hatq_tapsum_len(ctypes.byref(layer.w))))
     ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
+    if out_mode == HATQ_OUT_I32:
+        shape, dt = (n, ho, wo, layer.w.cout_pad), torch.int32
+    else:
+        shape, dt = (n, ho, wo, layer.w.d.cout), torch.float32
     if y is None:
-        if out_mode == HATQ_OUT_I32:
-            y = torch.empty((n, ho, wo, layer.w.cout_pad), dtype=torch.int32, device=xq.device)
-        else:
-            y = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.float32, device=xq.device)
+        y = torch.empty(shape, dtype=dt, device=xq.device)
+    _need(y, "y", dt, n * ho * wo * shape[3])
     _check(load().hatq_conv_int8_affine(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), _ptr(act_zero),
                                         _ptr(tapsum), n, h, w, int(out_mode), _ptr(y), _stream(stream)),
            "hatq_conv_int8_affine")
@@ -349,11 +435,14 @@ def hatq_range_expansion(x: torch.Tensor, hblock: int, amax: Optional[torch.Tens
                          stream=None):
     """Per-sample range-expansion indicator of x (fp32 NHWC): returns (amax [2n], flags [n]).
     count, if given, accumulates the number of expanding samples."""
-    n, h, w, c = x.shape
+    n, h, w, c = _nhwc(x, "x", torch.float32)
     if amax is None:
         amax = torch.empty(2 * n, dtype=torch.float32, device=x.device)
     if flags is None:
         flags = torch.empty(n, dtype=torch.int32, device=x.device)
+    _need(amax, "amax", torch.float32, 2 * n)
+    _need(flags, "flags", torch.int32, n)
+    _need(count, "count", torch.int32, 1, optional=True)
     _check(load().hatq_range_expansion(_ptr(x), n, h, w, c, int(hblock), _ptr(amax), _ptr(flags), _ptr(count),
                                        _stream(stream)), "hatq_range_expansion")
     return amax, flags
@@ -373,13 +462,18 @@ def hatq_layer_forward(layer: PreparedLayer, form, x: torch.Tensor, x_absmax: Op
                        next_hblock: int = 0, next_absmax: Optional[torch.Tensor] = None,
                        act_scale: Optional[torch.Tensor] = None, y: Optional[torch.Tensor] = None,
                        ws: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    n, h, w, _ = x.shape
+    n, h, w, _ = _nhwc(x, "x", torch.float32, layer.w.d.cin)
+    _need(x_absmax, "x_absmax", torch.float32, n, optional=True)
+    _need(next_absmax, "next_absmax", torch.float32, n, optional=True)
+    _need(act_scale, "act_scale", torch.float32, n, optional=True)
     ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
     if y is None:
         y = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.float32, device=x.device)
+    _need(y, "y", torch.float32, n * ho * wo * layer.w.d.cout)
     need = hatq_layer_ws_bytes(layer, n, h, w)
     if ws is None:
         ws = torch.empty(max(need, 256), dtype=torch.int8, device=x.device)
+    _need(ws, "ws", torch.int8, 0)
     _check(load().hatq_layer_forward(ctypes.byref(layer.w), FORMS.get(form, form), _ptr(x), n, h, w,
                                      _ptr(x_absmax), _ptr(y), _ptr(act_scale), int(next_hblock),
                                      _ptr(next_absmax), _ptr(ws), ws.numel(), _stream(stream)),

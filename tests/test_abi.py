@@ -119,43 +119,67 @@ def test_pack_rejects_before_launch(L):
 
 def test_conv_rejects_before_launch(L):
     f = L.hatq_conv_int8
+
+    def c(W, n, h, w, mode, y, nh, na, out_scale=None, flags=0):
+        return f(W, FAKE, FAKE, n, h, w, mode, out_scale, y, nh, na, flags, None)
     W = _fake_weights()
-    assert f(None, FAKE, FAKE, 1, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EINVAL
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 5, FAKE, 0, None, None) == hatq.HATQ_EINVAL
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 0, FAKE, 64, FAKE, None) == hatq.HATQ_EINVAL  # I32 + absmax
+    assert c(None, 1, 8, 8, 1, FAKE, 0, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W), 1, 8, 8, 5, FAKE, 0, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W), 1, 8, 8, 0, FAKE, 64, FAKE) == hatq.HATQ_EINVAL          # I32 + absmax
+    assert c(ctypes.byref(W), 1, 8, 8, 1, FAKE, 0, None, flags=2) == hatq.HATQ_EINVAL  # unknown flag
+    assert c(ctypes.byref(W), 1, 8, 8, 1, FAKE, 0, None, out_scale=FAKE) == hatq.HATQ_EINVAL   # scale outside I8
     bad = _fake_weights()
     bad.k_total += 1                                   # inconsistent view
-    assert f(ctypes.byref(bad), FAKE, FAKE, 1, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(bad), 1, 8, 8, 1, FAKE, 0, None) == hatq.HATQ_EINVAL
     W32 = _fake_weights(cin=32, hb=32)                 # cin_pad 32: neither small nor a multiple of 64
-    assert f(ctypes.byref(W32), FAKE, FAKE, 1, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EUNSUPPORTED
+    assert c(ctypes.byref(W32), 1, 8, 8, 1, FAKE, 0, None) == hatq.HATQ_EUNSUPPORTED
     Wt3 = _fake_weights(transposed=1, s=3, out_pad=1)  # transposed needs stride 2
-    assert f(ctypes.byref(Wt3), FAKE, FAKE, 1, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EUNSUPPORTED
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 1, FAKE, 128, FAKE, None) == hatq.HATQ_EUNSUPPORTED
+    assert c(ctypes.byref(Wt3), 1, 8, 8, 1, FAKE, 0, None) == hatq.HATQ_EUNSUPPORTED
+    assert c(ctypes.byref(W), 1, 8, 8, 1, FAKE, 128, FAKE) == hatq.HATQ_EUNSUPPORTED
     W0 = _fake_weights(p=0)                            # 5x5, no padding: a 2x2 input gives no output
-    assert f(ctypes.byref(W0), FAKE, FAKE, 1, 2, 2, 1, FAKE, 0, None, None) == hatq.HATQ_EINVAL
-    assert f(ctypes.byref(W), FAKE, FAKE, 0, 8, 8, 1, FAKE, 0, None, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W0), 1, 2, 2, 1, FAKE, 0, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W), 0, 8, 8, 1, FAKE, 0, None) == hatq.HATQ_EINVAL
 
 
 def test_conv_absmax_only_needs_next_absmax(L):
     f = L.hatq_conv_int8
     W = _fake_weights()
     # y = NULL is only the absmax-only F32 call
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 1, None, 0, None, None) == hatq.HATQ_EINVAL
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 0, None, 0, None, None) == hatq.HATQ_EINVAL
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, hatq.HATQ_OUT_I8, FAKE, 0, None, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 1, None, None, 0, None, 0, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 0, None, None, 0, None, 0, None) == hatq.HATQ_EINVAL
+
+
+def test_conv_i8_mode_needs_static_scale(L):
+    """HATQ_OUT_I8 through hatq_conv_int8: the codes need out_scale (a static
+    per-sample scale) and an output; a next_absmax is not taken in this mode;
+    the next operand's block follows the requantizing entry point's rules."""
+    f = L.hatq_conv_int8
+    W = _fake_weights()
+    I8 = hatq.HATQ_OUT_I8
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, None, FAKE, 64, None, 0, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, FAKE, None, 64, None, 0, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, FAKE, FAKE, 64, FAKE, 0, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, FAKE, FAKE, 3, None, 0, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, FAKE, FAKE, 128, None, 0, None) == hatq.HATQ_EUNSUPPORTED
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, ctypes.c_void_p(FAKE.value + 2), FAKE, 64, None, 0,
+             None) == hatq.HATQ_EINVAL                                                   # misaligned scale
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, FAKE, FAKE, 64, None, 4, None) == hatq.HATQ_EINVAL
 
 
 def test_requant_rejects_before_launch(L):
     f = L.hatq_conv_int8_requant
     W = _fake_weights()
-    assert f(None, FAKE, FAKE, 1, 8, 8, 64, FAKE, FAKE, FAKE, None) == hatq.HATQ_EINVAL
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 64, FAKE, None, FAKE, None) == hatq.HATQ_EINVAL   # no scale
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 64, FAKE, FAKE, None, None) == hatq.HATQ_EINVAL   # no output
-    assert f(ctypes.byref(W), FAKE, FAKE, 0, 8, 8, 64, FAKE, FAKE, FAKE, None) == hatq.HATQ_EINVAL
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 3, FAKE, FAKE, FAKE, None) == hatq.HATQ_EINVAL    # block 3
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 128, FAKE, FAKE, FAKE, None) == hatq.HATQ_EUNSUPPORTED
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, 64, ctypes.c_void_p(FAKE.value + 2), FAKE, FAKE, None) \
-        == hatq.HATQ_EINVAL                                                                           # misaligned
+
+    def r(W, n, nh, na, sc, yq, flags=0):
+        return f(W, FAKE, FAKE, n, 8, 8, nh, na, sc, yq, flags, None)
+    assert r(None, 1, 64, FAKE, FAKE, FAKE) == hatq.HATQ_EINVAL
+    assert r(ctypes.byref(W), 1, 64, FAKE, None, FAKE) == hatq.HATQ_EINVAL   # no scale
+    assert r(ctypes.byref(W), 1, 64, FAKE, FAKE, None) == hatq.HATQ_EINVAL   # no output
+    assert r(ctypes.byref(W), 0, 64, FAKE, FAKE, FAKE) == hatq.HATQ_EINVAL
+    assert r(ctypes.byref(W), 1, 3, FAKE, FAKE, FAKE) == hatq.HATQ_EINVAL    # block 3
+    assert r(ctypes.byref(W), 1, 128, FAKE, FAKE, FAKE) == hatq.HATQ_EUNSUPPORTED
+    assert r(ctypes.byref(W), 1, 64, ctypes.c_void_p(FAKE.value + 2), FAKE, FAKE) == hatq.HATQ_EINVAL  # misaligned
+    assert r(ctypes.byref(W), 1, 64, FAKE, FAKE, FAKE, flags=8) == hatq.HATQ_EINVAL                   # unknown flag
 
 
 def test_int_transition_rejects_before_launch(L):
@@ -163,24 +187,35 @@ def test_int_transition_rejects_before_launch(L):
     assert L.hatq_int_table_len(ctypes.byref(W)) == 2 * W.cout_pad + 1
     assert L.hatq_int_table_len(None) == 0
     p = L.hatq_int_transition_params
-    assert p(None, 0.1, 0.1, 64, FAKE, None, None) == hatq.HATQ_EINVAL
-    assert p(ctypes.byref(W), 0.0, 0.1, 64, FAKE, None, None) == hatq.HATQ_EINVAL           # s_x not positive
-    assert p(ctypes.byref(W), 0.1, float("inf"), 64, FAKE, None, None) == hatq.HATQ_EINVAL  # s_y not finite
-    assert p(ctypes.byref(W), 0.1, float("nan"), 64, FAKE, None, None) == hatq.HATQ_EINVAL
-    assert p(ctypes.byref(W), 0.1, 0.1, 3, FAKE, None, None) == hatq.HATQ_EINVAL            # block 3
-    assert p(ctypes.byref(W), 0.1, 0.1, 128, FAKE, None, None) == hatq.HATQ_EINVAL          # above 64
-    assert p(ctypes.byref(W), 0.1, 0.1, 64, None, None, None) == hatq.HATQ_EINVAL           # no table
-    assert p(ctypes.byref(W), 0.1, 0.1, 64, ctypes.c_void_p(FAKE.value + 4), None, None) \
-        == hatq.HATQ_EINVAL                                                                   # misaligned
+    assert p(None, 0.1, 0.1, 64, FAKE, None) == hatq.HATQ_EINVAL
+    assert p(ctypes.byref(W), 0.0, 0.1, 64, FAKE, None) == hatq.HATQ_EINVAL           # s_x not positive
+    assert p(ctypes.byref(W), 0.1, float("inf"), 64, FAKE, None) == hatq.HATQ_EINVAL  # s_y not finite
+    assert p(ctypes.byref(W), 0.1, float("nan"), 64, FAKE, None) == hatq.HATQ_EINVAL
+    assert p(ctypes.byref(W), 0.1, 0.1, 3, FAKE, None) == hatq.HATQ_EINVAL            # block 3
+    assert p(ctypes.byref(W), 0.1, 0.1, 128, FAKE, None) == hatq.HATQ_EINVAL          # above 64
+    assert p(ctypes.byref(W), 0.1, 0.1, 64, None, None) == hatq.HATQ_EINVAL           # no table
+    assert p(ctypes.byref(W), 0.1, 0.1, 64, ctypes.c_void_p(FAKE.value + 4), None) \
+        == hatq.HATQ_EINVAL                                                             # misaligned
     c = L.hatq_conv_int8_int_transition
-    assert c(None, FAKE, 1, 8, 8, 64, FAKE, FAKE, None) == hatq.HATQ_EINVAL
-    assert c(ctypes.byref(W), FAKE, 0, 8, 8, 64, FAKE, FAKE, None) == hatq.HATQ_EINVAL
-    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, None, FAKE, None) == hatq.HATQ_EINVAL      # no table
-    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, FAKE, None, None) == hatq.HATQ_EINVAL      # no output
-    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 3, FAKE, FAKE, None) == hatq.HATQ_EINVAL       # block 3
-    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 128, FAKE, FAKE, None) == hatq.HATQ_EUNSUPPORTED
-    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, ctypes.c_void_p(FAKE.value + 4), FAKE, None) \
+    assert c(None, FAKE, 1, 8, 8, 64, FAKE, FAKE, 0, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W), FAKE, 0, 8, 8, 64, FAKE, FAKE, 0, None) == hatq.HATQ_EINVAL
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, None, FAKE, 0, None) == hatq.HATQ_EINVAL      # no table
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, FAKE, None, 0, None) == hatq.HATQ_EINVAL      # no output
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 3, FAKE, FAKE, 0, None) == hatq.HATQ_EINVAL       # block 3
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 128, FAKE, FAKE, 0, None) == hatq.HATQ_EUNSUPPORTED
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, ctypes.c_void_p(FAKE.value + 4), FAKE, 0, None) \
         == hatq.HATQ_EINVAL                                                                   # misaligned table
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, FAKE, FAKE, 2, None) == hatq.HATQ_EINVAL      # unknown flag
+
+
+def test_export_rejects_before_copy(L):
+    f = L.hatq_export_weights
+    assert f(None, None, None, None, None) == hatq.HATQ_EINVAL
+    bad = _fake_weights()
+    bad.k_stride += 64                                 # inconsistent view
+    assert f(ctypes.byref(bad), None, None, None, None) == hatq.HATQ_EINVAL
+    W = _fake_weights()
+    assert f(ctypes.byref(W), None, None, None, None) == hatq.HATQ_OK   # nothing to copy
 
 
 def test_range_expansion_rejects_before_launch(L):

@@ -57,6 +57,9 @@ def test_int_transition_bit_exact(orc, c, next_b):
     assert yq.shape == q_ref.shape and yq.dtype == torch.int8
     assert_codes(host(yq), q_ref, exact=True, what=f"integer transition next_b={next_b}")
     assert np.abs(q_ref.astype(np.int32)).max() == 127        # the static scale reaches the range end
+    # HATQ_PAIRED: B_next B_Cout = b I is exact in integers, so the codes are
+    # identical (and for every other layer the flag changes nothing)
+    assert torch.equal(hatq.hatq_conv_int8_int_transition(layer, dev(xq), next_b, table, paired=True), yq)
 
 
 @pytest.mark.parametrize("next_b", [1, 64])
@@ -79,6 +82,8 @@ def test_int_transition_small_shifts_and_reuse(orc, next_b, target):
     q_ref = orc.int_transition(acc, ref, rq, next_b)
     assert np.count_nonzero(np.abs(q_ref.astype(np.int32)) == 127) > 0.01 * q_ref.size
     assert_codes(host(hatq.hatq_conv_int8_int_transition(layer, dev(xq), next_b, table)), q_ref, exact=True)
+    assert_codes(host(hatq.hatq_conv_int8_int_transition(layer, dev(xq), next_b, table, paired=True)), q_ref,
+                 exact=True)
     small = np.ascontiguousarray(xq[:1, :17, :11])
     acc_s = orc.conv_int8(small, ref.wq, stride=c[6], pad=c[7])
     assert_codes(host(hatq.hatq_conv_int8_int_transition(layer, dev(small), next_b, table)),
@@ -86,15 +91,22 @@ def test_int_transition_small_shifts_and_reuse(orc, next_b, target):
 
 
 def test_int_params_no_shift_fits(orc):
-    """A scale ratio too large for any shift: the call reports it and the table
-    holds n = -1."""
+    """A scale ratio too large for any shift: the table holds n = -1 and zero
+    multipliers (the library call itself does not wait; the binding reads the
+    shift back and reports it), and a transition with that table writes
+    all-zero codes."""
     c = CONV[1]
     _, _, _, _, layer = _layer(orc, c, 93)
     table = torch.zeros(hatq.hatq_int_table_len(layer), dtype=torch.int32, device="cuda")
     with pytest.raises(hatq.HatqError) as e:
         hatq.hatq_int_transition_params(layer, 1.0, 1e-30, 64, table=table)
     assert e.value.status == hatq.HATQ_EUNSUPPORTED
-    assert host(table)[-1] == -1
+    t = host(table)
+    assert t[-1] == -1 and not t[:layer.w.cout_pad].any()
+    n, h, w = c[0], c[1], c[2]
+    xq = torch.randint(-127, 128, (n, h, w, layer.w.cin_pad), dtype=torch.int8, device="cuda")
+    yq = hatq.hatq_conv_int8_int_transition(layer, xq, 64, table)
+    assert not host(yq).any()
 
 
 def test_stack_b16_layer1_int_transition_full_size(orc):
@@ -125,6 +137,7 @@ def test_stack_b16_layer1_int_transition_full_size(orc):
     cp = layer.w.cout_pad
     assert n_shift == rq.shift and np.array_equal(t[:cp], rq.M) and np.array_equal(t[cp:2 * cp], rq.b_int)
     yq = hatq.hatq_conv_int8_int_transition(layer, xq_d, nb, table)
+    assert torch.equal(hatq.hatq_conv_int8_int_transition(layer, xq_d, nb, table, paired=True), yq)
     yf, _ = hatq.hatq_conv_int8_requant(layer, xq_d, sx_d, nb, next_absmax=None,
                                         next_scale=torch.full((n,), s_y, device="cuda"))
     d = (yq.to(torch.int16) - yf.to(torch.int16)).abs()

@@ -4,18 +4,22 @@ its dynamic scale.
 
 * Against the oracle: the oracle's own layer (codes, scales, fp32 output y_ref)
   fixes S_ref = B_next y_ref and its codes and per-sample scale (Eq.
-  symmetric_q); the GPU, fed the oracle's codes and scales, must produce the
-  same scale within 1 ulp and the same codes under the INT8 rule (bit-exact
+  symmetric_q, Table I with both transforms explicit); the GPU, fed the
+  oracle's codes and scales, must produce the same scale within the bound its
+  fp32 butterflies allow and the same codes under the INT8 rule (bit-exact
   where both sides see identical fp32 values: DH layers with next block 1).
 * Against the two-kernel GPU path: the codes equal, bit for bit, what the
   activation kernel computes from the stored F32 output with the same absmax
-  (same fp32 butterfly, same rounding), and the absmax-only call matches the
-  F32 call's fused absmax exactly.
-* A WH layer whose next operand uses the same blocks takes the next operand as
-  z, the accumulators dequantized before the restore (B_next y = z exactly,
-  Table I): scale and codes bit for bit against the oracle's z, and within the
-  code rule against the two-kernel path (whose two fp32 butterflies round).
-* A static scale (next_absmax = NULL) gives the oracle's codes for that scale.
+  (same fp32 butterflies, same rounding), and the absmax-only call matches the
+  F32 call's fused absmax exactly.  This includes the WH -> DH transition with
+  equal blocks, whose WH restore and next butterfly both run.
+* HATQ_PAIRED: a WH layer whose next operand uses the same blocks takes the
+  next operand as z, the accumulators dequantized before the restore (B_next y
+  = z in exact arithmetic, Table I): scale and codes bit for bit against the
+  oracle's z, and within the code rule against the oracle's composition (codes
+  of fl32(B_next y_ref)).  For every other layer the flag changes nothing.
+* A static scale (next_absmax = NULL) gives the oracle's codes for that scale,
+  through hatq_conv_int8_requant and through hatq_conv_int8 in I8 mode.
 """
 import numpy as np
 import pytest
@@ -41,10 +45,38 @@ def _oracle_next(orc, r, next_b):
 
 
 def _paired(c, next_b):
-    """A WH layer whose next operand uses the same blocks: the next operand is
-    the accumulator-basis z (B_next y = z exactly), taken without butterflies."""
+    """A WH layer whose next operand uses the same blocks (the HATQ_PAIRED case)."""
     n, h, w, cin, cout, k, s, p, tr, op, form, hb = c
     return form == "WH" and next_b == hb and hb > 1 and cout % hb == 0
+
+
+def _gamma(k):
+    u = 2.0 ** -24
+    return k * u / (1 - k * u)
+
+
+def _scale_tol(orc, r, ref, next_b, s_ref, form):
+    """Bound on |s_gpu - s_ref| for the scale of B_next y.  The GPU forms B_next y
+    with log2(b) rounded fp32 butterfly stages (the oracle in fp64 with one
+    rounding), so each value differs by at most gamma_k * (sum of |y| over its
+    block).  A WH layer's y itself differs from the oracle's: the GPU restores
+    z / b (exact) with six rounded stages, the oracle rounds (B z) / b once, so
+    |dy| <= gamma_6 * (sum of |z| over the restored block) / b + u |y|; a value
+    of the next operand sums next_b of them.  The maxima differ by at most the
+    largest value difference; over 127, plus two ulps (the roundings of both
+    scales and of the oracle's transformed values)."""
+    n = r.y.shape[0]
+    k = int(np.log2(next_b)) if next_b > 1 else 0
+    ya = np.abs(r.y.astype(np.float64))
+    ya = np.pad(ya, [(0, 0)] * 3 + [(0, (-ya.shape[-1]) % next_b)])
+    tol = _gamma(k) * ya.reshape(n, -1, next_b).sum(-1).max(-1)
+    if form == "WH":
+        hb = ref.hblock
+        za = np.abs(orc.wh_z(r.acc, r.sx, ref).astype(np.float64))
+        dy = _gamma(int(np.log2(hb))) * za.reshape(n, -1, hb).sum(-1).max(-1) / hb
+        dy = dy + 2.0 ** -24 * np.abs(r.y.astype(np.float64)).reshape(n, -1).max(-1)
+        tol = tol + max(next_b, 1) * dy
+    return tol / 127 + 2 * np.spacing(s_ref.astype(np.float32)).astype(np.float64)
 
 
 @pytest.mark.parametrize("c", CONV, ids=CONV_IDS)
@@ -54,58 +86,43 @@ def test_requant_codes(orc, c, next_b):
     rng, wt, b, ref, layer = _layer(orc, c, 81)
     x = synth.heavy_tailed_activations(rng, (n, h, w, cin))
     r = orc.layer_forward(x, ref)
-    paired = _paired(c, next_b)
-    if paired:
-        q_ref, s_ref = orc.quantize_symmetric(orc.wh_z(r.acc, r.sx, ref)[..., :cout])
-    else:
-        q_ref, s_ref = _oracle_next(orc, r, next_b)
+    q_ref, s_ref = _oracle_next(orc, r, next_b)
     xq, sx = dev(r.xq), dev(r.sx)
-    # pass 1: the absmax alone; pass 2: the codes
+    # pass 1: the absmax alone; pass 2: the codes (both transforms explicit)
     nam = torch.full((n,), -1.0, device="cuda")
     assert hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=next_b, next_absmax=nam,
                                absmax_only=True) is None
     yq, sq = hatq.hatq_conv_int8_requant(layer, xq, sx, next_b, next_absmax=nam)
     assert yq.shape == q_ref.shape and yq.dtype == torch.int8
-    if paired:
-        # the same fp32 z on both sides: scale and codes bit for bit
-        assert np.array_equal(host(sq), s_ref)
-        assert_codes(host(yq), q_ref, exact=True, what=f"paired requant codes next_b={next_b}")
-    elif form == "WH":
-        # y is restored by an fp32 butterfly here and in fp64 by the oracle, so
-        # max|y| and the scale agree to the WH output tolerance (1e-6 of the
-        # range); over many samples a few differ by 2 ulps
-        np.testing.assert_allclose(host(sq), s_ref, rtol=1e-6, atol=0)
-        assert_codes(host(yq), q_ref, exact=False, what=f"requant codes next_b={next_b}")
-    elif next_b == 1:
+    if form == "DH" and next_b == 1:
         assert_scale_ulp(host(sq), s_ref)
         assert_codes(host(yq), q_ref, exact=True, what=f"requant codes next_b={next_b}")
     else:
-        # B_next y by log2(b) fp32 butterfly stages here, by an fp64 transform
-        # with one rounding in the oracle: each value differs by at most
-        # gamma_k * (sum of |y| over its block), so the scale by that over 127
-        # plus one ulp of its own rounding
-        k = int(np.log2(next_b))
-        u = 2.0 ** -24
-        gamma = k * u / (1 - k * u)
-        ya = np.abs(r.y.astype(np.float64))
-        ya = np.pad(ya, [(0, 0)] * 3 + [(0, (-ya.shape[-1]) % next_b)])
-        blk = ya.reshape(n, -1, next_b).sum(-1).max(-1)
-        tol = gamma * blk / 127 + np.spacing(s_ref.astype(np.float32)).astype(np.float64)
-        assert np.all(np.abs(host(sq).astype(np.float64) - s_ref) <= tol)
+        tol = _scale_tol(orc, r, ref, next_b, s_ref, form)
+        assert np.all(np.abs(host(sq).astype(np.float64) - s_ref) <= tol), (host(sq), s_ref, tol)
         assert_codes(host(yq), q_ref, exact=False, what=f"requant codes next_b={next_b}")
-    # the two-kernel GPU path on the stored output: identical absmax, scale and
-    # codes (paired: the stored y goes through two fp32 butterflies, so within
-    # their rounding)
+    # the two-kernel GPU path on the stored output: identical absmax, scale and codes
     nam2 = torch.full((n,), -1.0, device="cuda")
     y = hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=next_b, next_absmax=nam2)
     q2, s2 = hatq.hatq_fwht_quant_act(y, next_b, absmax=nam2)
-    if paired:
-        assert_scale_ulp(host(sq), host(s2), ulps=2)
-        assert_codes(host(yq), host(q2), what="paired requant vs two-kernel path")
+    assert torch.equal(nam, nam2)
+    assert torch.equal(sq, s2)
+    assert torch.equal(yq, q2)
+    # the same two passes with HATQ_PAIRED
+    namp = torch.full((n,), -1.0, device="cuda")
+    hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=next_b, next_absmax=namp,
+                        absmax_only=True, paired=True)
+    yqp, sqp = hatq.hatq_conv_int8_requant(layer, xq, sx, next_b, next_absmax=namp, paired=True)
+    if _paired(c, next_b):
+        qz, sz = orc.quantize_symmetric(orc.wh_z(r.acc, r.sx, ref)[..., :cout])
+        # the same fp32 z on both sides: scale and codes bit for bit
+        assert np.array_equal(host(sqp), sz)
+        assert_codes(host(yqp), qz, exact=True, what=f"paired requant codes next_b={next_b}")
+        # and the oracle's composition within the code rule
+        assert np.all(np.abs(host(sqp).astype(np.float64) - s_ref) <= _scale_tol(orc, r, ref, next_b, s_ref, form))
+        assert_codes(host(yqp), q_ref, what="paired requant codes vs the oracle's composition")
     else:
-        assert torch.equal(nam, nam2)
-        assert torch.equal(sq, s2)
-        assert torch.equal(yq, q2)
+        assert torch.equal(namp, nam) and torch.equal(sqp, sq) and torch.equal(yqp, yq)
 
 
 @pytest.mark.parametrize("ci", [1, 2, 4, 5, 16], ids=[CONV_IDS[i] for i in (1, 2, 4, 5, 16)])
@@ -120,6 +137,10 @@ def test_requant_static_scale(orc, ci):
     yq, sq = hatq.hatq_conv_int8_requant(layer, dev(r.xq), dev(r.sx), 64, next_absmax=None, next_scale=sc)
     assert np.array_equal(host(sq), s_ref)      # an input: left as given
     assert_codes(host(yq), q_ref, what="requant codes, static scale")
+    # hatq_conv_int8 in I8 mode with out_scale: the same kernel, the same codes
+    y8 = hatq.hatq_conv_int8(layer, dev(r.xq), dev(r.sx), hatq.HATQ_OUT_I8, next_hblock=64, out_scale=sc)
+    assert y8.dtype == torch.int8 and torch.equal(y8, yq)
+    assert np.array_equal(host(sc), s_ref)
 
 
 def test_requant_zero_output():

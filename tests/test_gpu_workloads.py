@@ -124,14 +124,7 @@ def test_stack_b16_full_size_sampled(orc, li):
         del q1, q2
 
 
-def test_stack_b16_layer1_requant_full_size(orc):
-    """The benchmark's layer-1 -> layer-2 transition at full size (WH 64 -> DH
-    64, so the next operand is the accumulator-basis z): the absmax-only pass
-    and the requantizing epilogue agree with the F32 output followed by the
-    activation kernel within the rounding of its two fp32 butterflies (a
-    property that holds at any size); sampled pixels' codes equal the oracle's
-    quantization of its own z with the GPU's scale, bit for bit, and every
-    sampled |z| lies under the fused absmax."""
+def _layer1_case(orc):
     wl = workloads.STACK_B16
     (ishape, oshape) = wl.shapes()[0]
     L, nxt = wl.layers[0], wl.layers[1]
@@ -141,7 +134,26 @@ def test_stack_b16_layer1_requant_full_size(orc):
     n = ishape[0]
     xq = synth.int8_codes(rng, ishape)
     sx = rng.uniform(1e-3, 1e-2, n).astype(np.float32)
-    nb = _act_block(nxt)
+    ho, wo = oshape[1], oshape[2]
+    pts = [(int(rng.integers(n)), int(rng.integers(ho)), int(rng.integers(wo))) for _ in range(64)]
+    pts += [(0, 0, 0), (n - 1, ho - 1, wo - 1)]
+    return L, ref, layer, n, xq, sx, _act_block(nxt), pts
+
+
+def _sample(t, pts):
+    return host(t[torch.tensor([p[0] for p in pts]), torch.tensor([p[1] for p in pts]),
+                  torch.tensor([p[2] for p in pts])])
+
+
+def test_stack_b16_layer1_requant_full_size(orc):
+    """The benchmark's layer-1 -> layer-2 transition at full size (WH 64 -> DH
+    64) with both transforms explicit: the absmax-only pass and the
+    requantizing epilogue equal, bit for bit, the F32 output followed by the
+    activation kernel (a property that holds at any size); on sampled pixels
+    the codes are those of the oracle's composition, fl32(B_next y_ref) with
+    y_ref restored in fp64, quantized with the GPU's scale (code rule), and
+    every sampled |B_next y_ref| lies under the fused absmax."""
+    L, ref, layer, n, xq, sx, nb, pts = _layer1_case(orc)
     xq_d, sx_d = dev(xq), dev(sx)
     nam = torch.full((n,), -1.0, device="cuda")
     hatq.hatq_conv_int8(layer, xq_d, sx_d, hatq.HATQ_OUT_F32, next_hblock=nb, next_absmax=nam, absmax_only=True)
@@ -149,23 +161,48 @@ def test_stack_b16_layer1_requant_full_size(orc):
     nam2 = torch.full((n,), -1.0, device="cuda")
     y = hatq.hatq_conv_int8(layer, xq_d, sx_d, hatq.HATQ_OUT_F32, next_hblock=nb, next_absmax=nam2)
     q2, s2 = hatq.hatq_fwht_quant_act(y, nb, absmax=nam2)
-    # WH 64 -> DH 64: the fused passes take z (B_next y = z exactly); the
-    # two-kernel path rounds through two fp32 butterflies
-    assert_scale_ulp(host(sq), host(s2), ulps=2)
-    assert_codes(host(yq), host(q2), what="batch-16 stack layer-1 requant vs two-kernel path")
-    # oracle on sampled pixels, with the GPU's scale: codes of z_ref, bit for bit
-    ho, wo = oshape[1], oshape[2]
-    pts = [(int(rng.integers(n)), int(rng.integers(ho)), int(rng.integers(wo))) for _ in range(64)]
-    pts += [(0, 0, 0), (n - 1, ho - 1, wo - 1)]
-    sh = host(sq)
-    got = host(yq[torch.tensor([p[0] for p in pts]), torch.tensor([p[1] for p in pts]),
-                  torch.tensor([p[2] for p in pts])])
+    assert torch.equal(nam, nam2) and torch.equal(sq, s2)
+    assert torch.equal(yq, q2)
+    del y, q2
+    sh, A = host(sq), host(nam)
+    got = _sample(yq, pts)
+    exp = np.empty_like(got)
+    for t, (s_, oh, ow) in enumerate(pts):
+        crop = _crop(xq, s_, oh * L.stride - L.pad, ow * L.stride - L.pad, L.k)
+        acc = orc.conv_int8(crop, ref.wq, stride=L.stride, pad=0)
+        y_ref = orc.epilogue(acc, sx[s_:s_ + 1], ref)
+        S = orc.activation_transform(y_ref, nb)[0, 0, 0]
+        assert np.abs(S.astype(np.float64)).max() <= A[s_] * (1 + 1e-5)
+        exp[t] = np.clip(np.rint(S / sh[s_]), -127, 127).astype(np.int8)
+    assert_codes(got, exp, what="batch-16 stack layer-1 requant codes vs oracle composition")
+
+
+def test_stack_b16_layer1_requant_paired_full_size(orc):
+    """The same transition with HATQ_PAIRED (the next operand taken as z, B_next
+    y = z in exact arithmetic): sampled pixels' codes equal the oracle's
+    quantization of its own z with the GPU's scale, bit for bit, every sampled
+    |z| lies under the fused absmax, and the codes stay within the code rule of
+    the explicit path."""
+    L, ref, layer, n, xq, sx, nb, pts = _layer1_case(orc)
+    xq_d, sx_d = dev(xq), dev(sx)
+    nam = torch.full((n,), -1.0, device="cuda")
+    hatq.hatq_conv_int8(layer, xq_d, sx_d, hatq.HATQ_OUT_F32, next_hblock=nb, next_absmax=nam, absmax_only=True,
+                        paired=True)
+    yq, sq = hatq.hatq_conv_int8_requant(layer, xq_d, sx_d, nb, next_absmax=nam, paired=True)
+    nam2 = torch.full((n,), -1.0, device="cuda")
+    hatq.hatq_conv_int8(layer, xq_d, sx_d, hatq.HATQ_OUT_F32, next_hblock=nb, next_absmax=nam2, absmax_only=True)
+    yq2, sq2 = hatq.hatq_conv_int8_requant(layer, xq_d, sx_d, nb, next_absmax=nam2)
+    assert_scale_ulp(host(sq), host(sq2), ulps=2)
+    d = (yq.to(torch.int16) - yq2.to(torch.int16)).abs()
+    assert int(d.max()) <= 1 and int(torch.count_nonzero(d)) <= 1e-4 * d.numel()
+    del yq2, d
+    sh, A = host(sq), host(nam)
+    got = _sample(yq, pts)
     exp = np.empty_like(got)
     for t, (s_, oh, ow) in enumerate(pts):
         crop = _crop(xq, s_, oh * L.stride - L.pad, ow * L.stride - L.pad, L.k)
         acc = orc.conv_int8(crop, ref.wq, stride=L.stride, pad=0)
         z = orc.wh_z(acc, sx[s_:s_ + 1], ref)[0, 0, 0, :L.cout]
-        assert np.abs(z).max() <= host(nam)[s_]
+        assert np.abs(z).max() <= A[s_]
         exp[t] = np.clip(np.rint(z / sh[s_]), -127, 127).astype(np.int8)
-    assert_codes(got, exp, exact=True, what="batch-16 stack layer-1 requant codes vs oracle")
-    del y, q2
+    assert_codes(got, exp, exact=True, what="batch-16 stack layer-1 paired requant codes vs oracle z")
