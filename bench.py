@@ -175,13 +175,38 @@ def layer_report(st, dur, img_pix):
     return out
 
 
+_SLEEP_CYCLES_PER_US = None
+
+
+def gpu_hold(us):
+    """Keep the GPU busy for about `us` microseconds with a spin kernel that
+    touches no memory, so the launches the host enqueues meanwhile run back to
+    back (host launch overhead then adds no idle time between them)."""
+    import torch
+    global _SLEEP_CYCLES_PER_US
+    if _SLEEP_CYCLES_PER_US is None:
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(1000)
+        a.record()
+        torch.cuda._sleep(1 << 20)
+        b.record()
+        torch.cuda.synchronize()
+        _SLEEP_CYCLES_PER_US = (1 << 20) / max(a.elapsed_time(b) * 1e3, 1.0)
+    torch.cuda._sleep(int(us * _SLEEP_CYCLES_PER_US))
+
+
 def run_steps(st, x0, steps, warmup, paired=False, flush=None):
+    """Time `steps` steps.  Warm: back to back, the whole run between two events
+    (and each kernel by the marks).  Flushed: a 1 GiB write before every step;
+    the step is timed from its first mark to its last.  Either way the GPU is
+    held busy while the host enqueues, so host overhead does not show."""
     import torch
     for _ in range(warmup):
         st.step(x0, paired=paired)
     torch.cuda.synchronize()
     mk = Marks()
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    gpu_hold(3000 + 600 * steps * st.nL)
     if flush is None:
         t0.record()
     for _ in range(steps):
