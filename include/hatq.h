@@ -196,6 +196,20 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
                             int32_t hblock, const float *absmax, int8_t *xq, float *act_scale,
                             void *ws, size_t ws_bytes, void *stream);
 
+/* hatq_fwht_quant_act without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation): the two-pass form (absmax, then codes) keeps the
+ * per-sample absmax in a static array inside the library, one copy per GPU,
+ * of HATQ_NOALLOC_MAX_SAMPLES floats (16 KB), held until the process ends.
+ * Arguments, results and support as hatq_fwht_quant_act with absmax = NULL;
+ * n > HATQ_NOALLOC_MAX_SAMPLES returns HATQ_EUNSUPPORTED.  Allocates nothing.
+ * Every call on one GPU shares that GPU's array (it is cleared by the call
+ * itself on the stream), so calls that overlap on one GPU (on different
+ * streams, or from several threads) race and must not be issued. */
+#define HATQ_NOALLOC_MAX_SAMPLES 4096
+int32_t hatq_fwht_quant_act_noalloc(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
+                                    int8_t *xq, float *act_scale, void *stream);
+
 /* INT8 convolution with INT32 accumulation and the fused epilogue, steps a5-a6
  * (Eq. integer_accumulation, Eq. accumulator_scale, Table I).
  *   xq:        device int8 [n][h][w][cin_pad] (codes from hatq_fwht_quant_act).

@@ -15,8 +15,17 @@
 //   quant_kernel : transform again, quantize with s = fl32(A / 127), store codes.
 // When the producer of x already computed A (next_absmax of the convolution),
 // only quant_kernel runs and x is read once.
+#include <mutex>
+
 #include "hatq_device.h"
 #include "hatq_launch.h"
+
+// Scratch of the no-allocation entry point: the per-sample absmax of the
+// two-pass quantization for callers that cannot allocate.  Every GPU the
+// library runs on holds its own copy until the process ends.  In host code the
+// name is a stand-in, not a device address: the address comes from
+// hipGetSymbolAddress, looked up once per device (scratch_absmax below).
+static __device__ __align__(256) float scratch[hatq::kNoAllocMaxSamples];
 
 namespace hatq {
 
@@ -535,6 +544,42 @@ hipError_t launch_range_expansion(const float *x, int n, int64_t P, int C, int h
     if (e != hipSuccess) return e;
     expansion_flags_kernel<<<(n + 255) / 256, 256, 0, st>>>(amax, n, hblock, flags, count);
     return hipGetLastError();
+}
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float *g_scratch[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, looked up on the first call on that
+// device (with it current) and kept.
+hipError_t scratch_absmax(float **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch[dev] = static_cast<float *>(p);
+    }
+    *out = g_scratch[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_act_quant_noalloc(const float *x, int n, int64_t E, int hblock, int8_t *xq, float *act_scale,
+                                    hipStream_t st) {
+    if (n <= 0 || n > kNoAllocMaxSamples) return hipErrorInvalidValue;
+    float *ws = nullptr;
+    const hipError_t e = scratch_absmax(&ws);
+    if (e != hipSuccess) return e;
+    // the two-pass path clears ws[0 .. n) with a fill kernel before its atomics
+    return launch_act_quant(x, n, E, hblock, nullptr, ws, xq, act_scale, st);
 }
 
 hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,

@@ -344,6 +344,18 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
                                              act_scale, static_cast<hipStream_t>(stream)));
 }
 
+int32_t hatq_fwht_quant_act_noalloc(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
+                                    int8_t *xq, float *act_scale, void *stream) {
+    static_assert(HATQ_NOALLOC_MAX_SAMPLES == hatq::kNoAllocMaxSamples, "one limit");
+    if (!x || !xq || !act_scale || n <= 0 || h <= 0 || w <= 0 || c <= 0) return HATQ_EINVAL;
+    if (!supported_order(hblock)) return HATQ_EINVAL;
+    if (c % hblock) return HATQ_EUNSUPPORTED;
+    if (!aligned(x, 16) || !aligned(xq, 4) || !aligned(act_scale, 4)) return HATQ_EINVAL;
+    if (n > HATQ_NOALLOC_MAX_SAMPLES) return HATQ_EUNSUPPORTED;
+    const int64_t E = (int64_t)h * w * c;
+    return hip_status(hatq::launch_act_quant_noalloc(x, n, E, hblock, xq, act_scale, static_cast<hipStream_t>(stream)));
+}
+
 namespace {
 
 // The requantizing epilogue (I8 output): dynamic scale from next_absmax, or the

@@ -11,6 +11,12 @@ namespace hatq {
 hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,
                             float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st);
 
+// The same two-pass quantization with the per-sample absmax in the library's
+// static device scratch (no caller workspace, no allocation): n <= kNoAllocMaxSamples.
+constexpr int kNoAllocMaxSamples = 4096;
+hipError_t launch_act_quant_noalloc(const float *x, int n, int64_t E, int hblock, int8_t *xq, float *act_scale,
+                                    hipStream_t st);
+
 // Affine activation quantization (signed grid [-128, 127]) of n samples of E
 // floats each (E % 4 == 0, the channel count a multiple of hblock): ws holds 2n
 // floats (per-sample max(S, 0), then max(-S, 0)); per-sample scale and zero point out.

@@ -46,7 +46,8 @@ class Weights(ctypes.Structure):
 
 
 EXPORTS = ["hatq_status_string", "hatq_conv_out_hw", "hatq_weights_bytes", "hatq_prepare_weights",
-           "hatq_export_weights", "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act", "hatq_conv_int8",
+           "hatq_export_weights", "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act",
+           "hatq_fwht_quant_act_noalloc", "hatq_conv_int8",
            "hatq_conv_int8_requant", "hatq_int_table_len", "hatq_int_transition_params",
            "hatq_conv_int8_int_transition", "hatq_range_expansion", "hatq_select_form",
            "hatq_fwht_quant_affine_ws_bytes", "hatq_fwht_quant_act_affine", "hatq_tapsum_len",
@@ -88,6 +89,8 @@ def load(build_if_missing: bool = False):
     L.hatq_fwht_quant_ws_bytes.restype = sz
     L.hatq_fwht_quant_act.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P, sz, P]
     L.hatq_fwht_quant_act.restype = i32
+    L.hatq_fwht_quant_act_noalloc.argtypes = [P, i32, i32, i32, i32, i32, P, P, P]
+    L.hatq_fwht_quant_act_noalloc.restype = i32
     L.hatq_conv_int8.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, P, i32, P, i32, P]
     L.hatq_conv_int8.restype = i32
     L.hatq_conv_int8_requant.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, P, P, i32, P]
@@ -283,6 +286,21 @@ def hatq_fwht_quant_act(x: torch.Tensor, hblock: int, absmax: Optional[torch.Ten
     _check(load().hatq_fwht_quant_act(_ptr(x), n, h, w, c, int(hblock), _ptr(absmax), _ptr(xq), _ptr(sc),
                                       _ptr(ws), wsb, _stream(stream)), "hatq_fwht_quant_act")
     return xq, sc
+
+
+HATQ_NOALLOC_MAX_SAMPLES = 4096
+
+
+def hatq_fwht_quant_act_noalloc(x: torch.Tensor, hblock: int, xq: torch.Tensor, scale: torch.Tensor,
+                                stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """hatq_fwht_quant_act (two passes) with the library's static scratch: the
+    caller passes the outputs; nothing is allocated."""
+    n, h, w, c = _nhwc(x, "x", torch.float32)
+    _need(xq, "xq", torch.int8, x.numel())
+    _need(scale, "scale", torch.float32, n)
+    _check(load().hatq_fwht_quant_act_noalloc(_ptr(x), n, h, w, c, int(hblock), _ptr(xq), _ptr(scale),
+                                              _stream(stream)), "hatq_fwht_quant_act_noalloc")
+    return xq, scale
 
 
 def _flags(paired: bool) -> int:

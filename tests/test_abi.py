@@ -208,6 +208,18 @@ def test_int_transition_rejects_before_launch(L):
     assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, FAKE, FAKE, 2, None) == hatq.HATQ_EINVAL      # unknown flag
 
 
+def test_noalloc_rejects_before_launch(L):
+    f = L.hatq_fwht_quant_act_noalloc
+    assert f(None, 1, 4, 4, 64, 64, FAKE, FAKE, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 1, 4, 4, 64, 64, None, FAKE, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 0, 4, 4, 64, 64, FAKE, FAKE, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 1, 4, 4, 64, 48, FAKE, FAKE, None) == hatq.HATQ_EINVAL           # not a supported order
+    assert f(FAKE, 1, 4, 4, 96, 64, FAKE, FAKE, None) == hatq.HATQ_EUNSUPPORTED     # c % b
+    assert f(ctypes.c_void_p(FAKE.value + 4), 1, 4, 4, 64, 64, FAKE, FAKE, None) == hatq.HATQ_EINVAL
+    n = hatq.HATQ_NOALLOC_MAX_SAMPLES
+    assert f(FAKE, n + 1, 4, 4, 64, 64, FAKE, FAKE, None) == hatq.HATQ_EUNSUPPORTED  # past the scratch
+
+
 def test_export_rejects_before_copy(L):
     f = L.hatq_export_weights
     assert f(None, None, None, None, None) == hatq.HATQ_EINVAL
