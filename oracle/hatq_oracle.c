@@ -758,8 +758,10 @@ int orc_int_requant_params(int cout_p, float s_x, const float *s_w, const float 
 static int64_t rne_shift(int64_t w, int n)
 {
     if (n == 0) return w;
-    const int64_t q = w >> n;                         /* floor */
-    const int64_t r = w - (q << n);                   /* 0 <= r < 2^n */
+    const int64_t p = (int64_t)1 << n;
+    int64_t q = w / p;                                /* truncated toward zero */
+    if (w % p != 0 && w < 0) q -= 1;                  /* floor */
+    const int64_t r = w - q * p;                      /* 0 <= r < 2^n */
     const int64_t half = (int64_t)1 << (n - 1);
     if (r > half || (r == half && (q & 1))) return q + 1;
     return q;

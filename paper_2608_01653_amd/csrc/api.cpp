@@ -13,6 +13,19 @@
 namespace {
 
 bool is_pow2(int v) { return v >= 1 && (v & (v - 1)) == 0; }
+
+constexpr int32_t kMaxChannels = 1 << 16;   // per layer, in and out
+constexpr int64_t kMaxElems = (int64_t)1 << 40;   // elements of one tensor
+
+// a * b * c * d (all >= 1) without overflow, or -1 when above kMaxElems.
+int64_t elems(int64_t a, int64_t b, int64_t c, int64_t d = 1) {
+    int64_t v = 1;
+    for (int64_t f : {a, b, c, d}) {
+        if (f < 1 || v > kMaxElems / f) return -1;
+        v *= f;
+    }
+    return v;
+}
 int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -26,6 +39,10 @@ int32_t check_desc(const hatq_conv_desc *d, int32_t form) {
     if (!d) return HATQ_EINVAL;
     if (form != HATQ_DH && form != HATQ_WH) return HATQ_EINVAL;
     if (d->cin <= 0 || d->cout <= 0 || d->k <= 0 || d->stride <= 0 || d->pad < 0 || d->out_pad < 0)
+        return HATQ_EINVAL;
+    // bounds that keep every derived size (k*k*cin_pad, cout_pad * k_stride) in range
+    if (d->cin > kMaxChannels || d->cout > kMaxChannels || d->k > 64 || d->stride > 64 || d->pad > 64 ||
+        d->out_pad > 64)
         return HATQ_EINVAL;
     if (!supported_order(d->hblock)) return HATQ_EINVAL;
     if (d->transposed != 0 && d->transposed != 1) return HATQ_EINVAL;
@@ -58,13 +75,14 @@ Dims dims_of(const hatq_conv_desc *d, int32_t form) {
 
 int32_t out_hw(const hatq_conv_desc *d, int32_t h, int32_t w, int32_t *ho, int32_t *wo) {
     int64_t a, b;
+    const int64_t H = h, Wd = w, p = d->pad, k = d->k, st = d->stride;
     if (d->transposed) {
-        a = (int64_t)(h - 1) * d->stride - 2 * d->pad + d->k + d->out_pad;
-        b = (int64_t)(w - 1) * d->stride - 2 * d->pad + d->k + d->out_pad;
+        a = (H - 1) * st - 2 * p + k + d->out_pad;
+        b = (Wd - 1) * st - 2 * p + k + d->out_pad;
     } else {
-        if (h + 2 * d->pad < d->k || w + 2 * d->pad < d->k) return HATQ_EINVAL;
-        a = (h + 2 * d->pad - d->k) / d->stride + 1;
-        b = (w + 2 * d->pad - d->k) / d->stride + 1;
+        if (H + 2 * p < k || Wd + 2 * p < k) return HATQ_EINVAL;
+        a = (H + 2 * p - k) / st + 1;
+        b = (Wd + 2 * p - k) / st + 1;
     }
     if (a <= 0 || b <= 0 || a > INT32_MAX || b > INT32_MAX) return HATQ_EINVAL;
     *ho = (int32_t)a;
@@ -132,6 +150,7 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
     const hatq_conv_desc &d = W->d;
     int32_t ho, wo;
     if (out_hw(&d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
+    if (elems(n, h, w, W->cin_pad) < 0 || elems(n, ho, wo, W->cout_pad) < 0) return HATQ_EINVAL;
     hatq::ConvArgs a;
     std::memset(&a, 0, sizeof(a));
     a.xq = xq;
@@ -335,6 +354,7 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
     if (c % hblock) return HATQ_EUNSUPPORTED;
     if (!aligned(x, 16) || !aligned(xq, 4) || !aligned(act_scale, 4)) return HATQ_EINVAL;
     if (absmax && !aligned(absmax, 4)) return HATQ_EINVAL;
+    if (elems(n, h, w, c) < 0) return HATQ_EINVAL;
     if (!absmax) {
         if (!ws) return HATQ_EINVAL;
         if (ws_bytes < hatq_fwht_quant_ws_bytes(n) || !aligned(ws, 4)) return HATQ_EWORKSPACE;
@@ -352,6 +372,7 @@ int32_t hatq_fwht_quant_act_noalloc(const float *x, int32_t n, int32_t h, int32_
     if (c % hblock) return HATQ_EUNSUPPORTED;
     if (!aligned(x, 16) || !aligned(xq, 4) || !aligned(act_scale, 4)) return HATQ_EINVAL;
     if (n > HATQ_NOALLOC_MAX_SAMPLES) return HATQ_EUNSUPPORTED;
+    if (elems(n, h, w, c) < 0) return HATQ_EINVAL;
     const int64_t E = (int64_t)h * w * c;
     return hip_status(hatq::launch_act_quant_noalloc(x, n, E, hblock, xq, act_scale, static_cast<hipStream_t>(stream)));
 }
@@ -428,8 +449,9 @@ int32_t hatq_fwht_quant_act_affine(const float *x, int32_t n, int32_t h, int32_t
     if (!aligned(x, 16) || !aligned(xq, 4) || !aligned(act_scale, 4) || !aligned(act_zero, 4) || !aligned(ws, 4))
         return HATQ_EINVAL;
     if (ws_bytes < (size_t)n * 8) return HATQ_EWORKSPACE;
+    if (elems(n, h, w, c) < 0) return HATQ_EINVAL;
     const int64_t E = (int64_t)h * w * c;
-    if (c % hblock != 0 || E % 4 != 0 || E > ((int64_t)1 << 40)) return HATQ_EUNSUPPORTED;
+    if (c % hblock != 0 || E % 4 != 0) return HATQ_EUNSUPPORTED;
     return hip_status(hatq::launch_act_quant_affine(x, n, E, hblock, static_cast<float *>(ws), xq, act_scale,
                                                     act_zero, static_cast<hipStream_t>(stream)));
 }
@@ -525,8 +547,8 @@ int32_t hatq_range_expansion(const float *x, int32_t n, int32_t h, int32_t w, in
     if (!is_pow2(hblock) || hblock > 128) return HATQ_EINVAL;
     if (!aligned(x, 16) || !aligned(amax, 4)) return HATQ_EINVAL;
     if ((flags && !aligned(flags, 4)) || (count && !aligned(count, 4))) return HATQ_EINVAL;
+    if (elems(n, h, w, c) < 0) return HATQ_EINVAL;
     const int64_t P = (int64_t)h * w;
-    if (P * c > ((int64_t)1 << 40)) return HATQ_EINVAL;
     return hip_status(hatq::launch_range_expansion(x, n, P, c, hblock, amax, flags, count,
                                                    static_cast<hipStream_t>(stream)));
 }
@@ -540,6 +562,7 @@ int32_t hatq_select_form(int64_t expansions, int64_t images, double tau, int32_t
 
 size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w) {
     if (check_weights(W) != HATQ_OK || n <= 0 || h <= 0 || w <= 0) return 0;
+    if (elems(n, h, w, W->cin_pad) < 0) return 0;
     const size_t codes = (size_t)n * h * w * W->cin_pad;
     return align256(codes) + align256((size_t)n * 4) + hatq_fwht_quant_ws_bytes(n);
 }
@@ -561,6 +584,7 @@ int32_t hatq_layer_forward(const hatq_weights *W, int32_t form, const float *x, 
     if (W->d.cin % hb_act) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
+    if (elems(n, h, w, W->cin_pad) < 0 || elems(n, ho, wo, W->cout_pad) < 0) return HATQ_EINVAL;
     const size_t need = hatq_layer_ws_bytes(W, n, h, w);
     if (ws_bytes < need) return HATQ_EWORKSPACE;
     int8_t *xq = static_cast<int8_t *>(ws);

@@ -190,6 +190,31 @@ __device__ __forceinline__ void fwht_acc(float (&v)[16], int b) {
     }
 }
 
+// max |B v| over the 16 values after fwht_acc<B, false>.  For B = 64 the last
+// stage (registers r and r + 8) is fused with the maximum: of a + c and a - c,
+// the one whose operands agree in sign has magnitude |a| + |c| and the other
+// is no larger, and rounding is monotone, so max(|fl(a + c)|, |fl(a - c)|) =
+// fl(|a| + |c|) exactly -- one add with absolute-value operands and one max
+// per pair instead of an add, a subtract and two maxima.
+template <int B>
+__device__ __forceinline__ float fwht_acc_absmax(float (&v)[16], int b) {
+    float mm = 0.0f;
+    if constexpr (B == 64) {
+        reg_stage<1>(v);
+        reg_stage<2>(v);
+        cross_stage_pairs<16, false>(v);
+        cross_stage_pairs<32, false>(v);
+        reg_stage<4>(v);
+#pragma unroll
+        for (int r = 0; r < 8; ++r) mm = fmaxf(mm, fabsf(v[r]) + fabsf(v[r + 8]));
+    } else {
+        fwht_acc<B, false>(v, b);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(v[r]));
+    }
+    return mm;
+}
+
 // ---- integer transition: the same butterflies on int64 values ---------------
 // Integer butterflies are exact, so any stage order gives the Sylvester
 // transform of the block; the layout and the lane pairing are those above.
@@ -591,7 +616,9 @@ struct Epilogue {
         // every pixel's codes start 16-byte aligned, a launch-wide condition)
         const bool a16 = ((reinterpret_cast<uintptr_t>(a.y) | (uintptr_t)a.cout | (uintptr_t)t.n0) & 15) == 0;
         if (a16 && t.n0 + cl + 16 <= a.cout) {
-            *reinterpret_cast<uint4 *>(yq + cl) = make_uint4(w[0], w[1], w[2], w[3]);
+            // streaming store: the next layer's convolution reads the codes
+            __builtin_nontemporal_store(v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]},
+                                        reinterpret_cast<v4i *>(yq + cl));
         } else {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj)
@@ -606,8 +633,12 @@ struct Epilogue {
             return;
         }
         const bool f32 = fl.f32, wh = fl.wh, want_abs = fl.want_abs, i8 = fl.i8, store = fl.store;
+        // The small-cin layer's two passes read the factors per group (LDS
+        // reads are cheap next to its two transforms; kept across the row
+        // groups they took 32 registers and the kernel spilled).
+        constexpr bool serial = E::Q == 1 || E::Q == 4;
         float4 t4[4], b4[4];
-        if (f32) {
+        auto load_factors = [&]() {
             // zpair: the next operand is z itself, so the factors carry no 1/b
             // (t and b~ times b: exact, a power of two), and
             // fma(acc, t, b~) equals fma(acc, t/b, b~/b) * b
@@ -622,10 +653,18 @@ struct Epilogue {
                     b4[jj] = make_float4(b4[jj].x * bsc, b4[jj].y * bsc, b4[jj].z * bsc, b4[jj].w * bsc);
                 }
             }
-        }
+        };
+        if (f32 && !serial) load_factors();
         const bool blk_full = t.n0 + 64 * k + 64 <= a.cout;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
+            // The requantizing and absmax-only variants (the small-cin layer's
+            // two passes, with both transforms) keep one group's values live
+            // at a time: interleaving groups spilled registers.
+            if constexpr (serial) {
+                __builtin_amdgcn_sched_barrier(0);
+                if (f32) load_factors();
+            }
             float v[16];
             v4i cc[4];
 #pragma unroll
@@ -718,11 +757,7 @@ struct Epilogue {
                     quant16(v, qs, qr, q_fast, w);
                     store_codes(w, i, k);
                 } else {
-                    fwht_acc<NB, false>(v, a.next_hblock);
-                    float mm = 0.0f;
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(v[r]));
-                    wave_m = fmaxf(wave_m, mm);
+                    wave_m = fmaxf(wave_m, fwht_acc_absmax<NB>(v, a.next_hblock));
                 }
             }
         }
@@ -786,8 +821,8 @@ struct RowRunPatch {
 // with no tail, up to kRowRunMax.
 constexpr int kRowRunMin = 4, kRowRunMax = 64;
 
-template <int TH, int TW, int BN, int CIN, typename E>
-__global__ void __launch_bounds__(kThreads, 2) conv_rowrun_kernel(const ConvArgs a) {
+template <int TH, int TW, int BN, int CIN, typename E, int MINB = 2>
+__global__ void __launch_bounds__(kThreads, MINB) conv_rowrun_kernel(const ConvArgs a) {
     constexpr int BM = TH * TW;
     constexpr int TM = BM / 4;
     constexpr int FM = TM / 16;
@@ -1170,7 +1205,7 @@ hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
 
 int persistent_blocks();
 
-template <int TH, int TW, int BN, int CS, typename E>
+template <int TH, int TW, int BN, int CS, typename E, int MINB = 2>
 hipError_t launch_rowrun(const ConvArgs &a, hipStream_t st) {
     ConvArgs b = a;
     const int64_t tiles = set_tiles(b, TH, TW, BN);
@@ -1178,22 +1213,40 @@ hipError_t launch_rowrun(const ConvArgs &a, hipStream_t st) {
     // every byte offset of the input fits the 32-bit buffer range
     if ((int64_t)b.n * b.h * b.w * CS >= ((int64_t)1 << 31) - 64) return hipErrorInvalidValue;
     const int64_t per = (int64_t)b.tiles_h * b.tiles_w;
-    const int64_t slots = 2 * (int64_t)persistent_blocks();   // resident blocks (0 if unknown)
+    const int64_t slots = MINB * (int64_t)persistent_blocks();   // resident blocks (0 if unknown)
     int64_t run = slots > 0 ? (b.n * per * b.tiles_n + slots - 1) / slots : kRowRunMin;
     run = run < kRowRunMin ? kRowRunMin : run > kRowRunMax ? kRowRunMax : run;
     b.run_tiles = (int32_t)run;
     const int64_t blocks = (int64_t)b.n * ((per + run - 1) / run) * b.tiles_n;
     if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-    conv_rowrun_kernel<TH, TW, BN, CS, E><<<(unsigned)blocks, kThreads, 0, st>>>(b);
+    conv_rowrun_kernel<TH, TW, BN, CS, E, MINB><<<(unsigned)blocks, kThreads, 0, st>>>(b);
     return hipGetLastError();
 }
+
+// Tile of the 3-channel layer with 192 outputs (the RGB input layer): rows x
+// columns of output pixels per block and blocks per CU.
+#ifndef HATQ_RR_TH
+#define HATQ_RR_TH 2
+#endif
+#ifndef HATQ_RR_TW
+#define HATQ_RR_TW 64
+#endif
+#ifndef HATQ_RR_MINB
+#define HATQ_RR_MINB 2
+#endif
 
 template <int CS>
 hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
     if (a.cout_pad % 192 == 0) {
         if constexpr (CS == 3)
-            return with_epilogue<Epi<64, 64, 1>, Epi<64, 64, 2>, Epi<64, 64, 4>, HATQ_HOT_EPILOGUES>(
-                a, [&](auto e) { return launch_rowrun<2, 64, 192, CS, decltype(e)>(a, st); });
+            return with_epilogue<Epi<64, 64, 1>, Epi<64, 64, 2>, Epi<64, 64, 4>, HATQ_HOT_EPILOGUES>(a, [&](auto e) {
+                // the requantizing pass (two transforms and the quantizer per
+                // value) keeps one row group per wave: with two it spilled
+                if constexpr (decltype(e)::Q == 1)
+                    return launch_rowrun<HATQ_RR_TH, HATQ_RR_TW / 2, 192, CS, decltype(e), HATQ_RR_MINB>(a, st);
+                else
+                    return launch_rowrun<HATQ_RR_TH, HATQ_RR_TW, 192, CS, decltype(e), HATQ_RR_MINB>(a, st);
+            });
         return with_epilogue<HATQ_GENERIC_EPILOGUES>(
             a, [&](auto e) { return launch_rowrun<2, 64, 192, CS, decltype(e)>(a, st); });
     }

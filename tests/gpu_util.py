@@ -81,3 +81,26 @@ def unpack_codes(layer, k, cin_p):
     kt = layer.w.k_total
     assert not w[:, kt:].any(), "K padding must be zero"
     return w[:, :kt].reshape(layer.w.cout_pad, k, k, cin_p)
+
+
+GUARD_BYTES = 256
+GUARD_BYTE = 0x5A
+
+
+class Guarded:
+    """An output buffer with canary bytes before and after it: `view` is the
+    tensor to hand to the library (256-byte aligned, as torch allocates), and
+    check() asserts that no byte outside it was written."""
+
+    def __init__(self, shape, dtype):
+        nbytes = int(np.prod(shape)) * torch.empty((), dtype=dtype).element_size()
+        self.raw = torch.full((GUARD_BYTES + nbytes + GUARD_BYTES,), GUARD_BYTE, dtype=torch.uint8, device=DEV)
+        self.nbytes = nbytes
+        self.view = self.raw[GUARD_BYTES:GUARD_BYTES + nbytes].view(dtype).view(shape)
+
+    def check(self, what="output"):
+        torch.cuda.synchronize()
+        head = self.raw[:GUARD_BYTES]
+        tail = self.raw[GUARD_BYTES + self.nbytes:]
+        assert bool(torch.all(head == GUARD_BYTE)), f"{what}: bytes before the buffer were written"
+        assert bool(torch.all(tail == GUARD_BYTE)), f"{what}: bytes after the buffer were written"
