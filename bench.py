@@ -39,6 +39,10 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, GB/s
 PEAK_INT8_TOPS = 5000.0      # MI355X dense INT8 MFMA, TOP/s
+# fp32 vector ALU, one lane-operation per lane per clock: 256 CUs x 4 SIMDs x
+# 16 lanes x 2.4 GHz (the 157.3 TFLOP/s figure counts an FMA as two flops and
+# packed dual-rate issue twice)
+PEAK_ALU_TLOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 RIDGE = PEAK_INT8_TOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # ops per byte
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_analysis_stack_b16.json")
 DEFAULT_WORKLOAD = "analysis_stack4_rgb_b16_1024x1024"
@@ -127,6 +131,60 @@ def kernel_label(st, key):
     return f"{name}<Epi<{wb},{nb}>> ({shape})"
 
 
+def _log2(b):
+    return max(int(b).bit_length() - 1, 0)
+
+
+# Algorithmic vector-ALU lane-operations of the method per element:
+QUANT_OPS = 4          # scale, round, clamp, convert of one code
+DEQUANT_OPS = 2        # int -> fp32 conversion and the fused scale-and-bias
+
+
+def kernel_work(st, key):
+    """Algorithmic work of the kernel(s) behind a mark label: INT8 MFMA ops,
+    HBM bytes and vector-ALU lane-operations (butterfly stages log2(b) add/sub
+    per element, dequantization, quantization, maxima)."""
+    import numpy as np
+    from paper_2608_01653_amd import stack as stk, workloads
+    li, part = key.split(".")
+    i = int(li[1:]) - 1
+    L = st.wl.layers[i]
+    (ishape, oshape) = st.shapes[i]
+    if part == "quant":
+        e = int(np.prod(ishape))
+        passes = st.quant_passes(i)
+        ops = e * (_log2(st.act_hb[i]) + QUANT_OPS) + (e * (_log2(st.act_hb[i]) + 1) if passes == 2 else 0)
+        return {"mfma_ops": 0, "hbm_bytes": e * 5, "alu_lane_ops": ops}
+    outs = int(np.prod(oshape[:3])) * L.cout
+    wb = L.hblock if L.form == "WH" else 1
+    nxt = i + 1 < st.nL
+    nb = st.act_hb[i + 1] if nxt else 1
+    base = DEQUANT_OPS + _log2(wb)
+    mf = workloads.conv_ops(st.wl, i)
+    wbytes = st.layers[i].cout_pad * st.layers[i].k_stride
+    xin = int(np.prod(ishape))
+    if part == "absmax":
+        return {"mfma_ops": mf, "hbm_bytes": xin + wbytes, "alu_lane_ops": outs * (base + _log2(nb) + 1)}
+    if part == "requant":
+        return {"mfma_ops": mf, "hbm_bytes": xin + wbytes + outs,
+                "alu_lane_ops": outs * (base + _log2(nb) + QUANT_OPS)}
+    alu = outs * (base + ((_log2(nb) + 1) if nxt else 0))
+    return {"mfma_ops": mf, "hbm_bytes": stk.conv_bytes(st, i), "alu_lane_ops": alu}
+
+
+def roofline_of(work, us):
+    """The bound with the longest ideal time, and the achieved fraction of it."""
+    t = us * 1e-6
+    cands = [("mfma", work["mfma_ops"] / (PEAK_INT8_TOPS * 1e12), work["mfma_ops"] / t / 1e12, PEAK_INT8_TOPS,
+              "TOP/s"),
+             ("hbm", work["hbm_bytes"] / (PEAK_HBM_GBS * 1e9), work["hbm_bytes"] / t / 1e9, PEAK_HBM_GBS, "GB/s"),
+             ("alu", work["alu_lane_ops"] / (PEAK_ALU_TLOPS * 1e12), work["alu_lane_ops"] / t / 1e12, PEAK_ALU_TLOPS,
+              "T lane-op/s")]
+    bound, ideal, ach, peak, unit = max(cands, key=lambda c: c[1])
+    return {"bound": bound, "achieved": round(ach, 1), "peak": round(peak, 1), "unit": unit,
+            "frac": round(ach / peak, 4), "ideal_us": round(ideal * 1e6, 2)}
+
+
 def layer_report(st, dur, img_pix):
     """Per-layer figures from the per-kernel durations (us)."""
     import numpy as np
@@ -138,16 +196,15 @@ def layer_report(st, dur, img_pix):
         passes = st.quant_passes(i)
         tq = dur.get(f"L{i + 1}.quant", 0.0)
         if st.requant[i]:
-            parts = {"absmax_pass_us": round(dur[f"L{i + 1}.absmax"], 2),
-                     "requant_pass_us": round(dur[f"L{i + 1}.requant"], 2)}
+            parts = {f"{p}_pass": dict(us=round(dur[f"L{i + 1}.{p}"], 2),
+                                       **roofline_of(kernel_work(st, f"L{i + 1}.{p}"), dur[f"L{i + 1}.{p}"]))
+                     for p in ("absmax", "requant")}
             tc = dur[f"L{i + 1}.absmax"] + dur[f"L{i + 1}.requant"]
         else:
-            parts = {}
+            parts = {"conv_roofline": roofline_of(kernel_work(st, f"L{i + 1}.conv"), dur[f"L{i + 1}.conv"])}
             tc = dur[f"L{i + 1}.conv"]
         ops = workloads.conv_ops(st.wl, i)
         cb = stk.conv_bytes(st, i)
-        ai = ops / cb
-        bound = "mfma" if ai >= RIDGE else "hbm"
         tops = ops / (tc * 1e-6) / 1e12
         gbs = cb / (tc * 1e-6) / 1e9
         out_pix = oshape[0] * oshape[1] * oshape[2]
@@ -161,10 +218,9 @@ def layer_report(st, dur, img_pix):
             "conv_us": round(tc, 2),
             "conv_output": "int8 codes of the next operand" if st.requant[i] else "fp32",
             "conv_tops": round(tops, 1),
+            "conv_mfma_frac": round(tops / PEAK_INT8_TOPS, 4),
             "conv_gbs_alg": round(gbs, 1),
-            "conv_ops_per_byte": round(ai, 1),
-            "conv_bound": bound,
-            "conv_roofline_frac": round(tops / PEAK_INT8_TOPS if bound == "mfma" else gbs / PEAK_HBM_GBS, 4),
+            "conv_ops_per_byte": round(ops / cb, 1),
             "mpix_per_s_image": round(img_pix / ((tq + tc) * 1e-6) / 1e6, 1),
             "mpix_per_s_output": round(out_pix / ((tq + tc) * 1e-6) / 1e6, 1),
         }
@@ -546,22 +602,18 @@ def main():
     dur = mk.durations_us()
     per_layer = layer_report(st, dur, img_pix)
 
-    # the step's longest kernel, against its roofline
-    key = max((k for k in dur if k != "end" and not k.endswith(".quant")), key=lambda k: dur[k])
-    li = int(key.split(".")[0][1:]) - 1
-    ops_k = workloads.conv_ops(wl, li)
-    cb = stack.conv_bytes(st, li)
-    t_k = dur[key] * 1e-6
-    if ops_k / cb >= RIDGE:
-        ach, peak, unit, bound = ops_k / t_k / 1e12, PEAK_INT8_TOPS, "TOP/s", "mfma"
-        work = f"{ops_k} ops per launch (2 x outputs x cout x k*k*cin, dense taps)"
-    else:
-        ach, peak, unit, bound = cb / t_k / 1e9, PEAK_HBM_GBS, "GB/s", "hbm"
-        work = f"{cb} bytes per launch (int8 input + weights + output)"
+    # the step's longest kernel, against its roofline (the bound with the
+    # longest ideal time: INT8 MFMA ops, HBM bytes or vector-ALU lane-ops)
+    key = max((k for k in dur if k != "end"), key=lambda k: dur[k])
+    work = kernel_work(st, key)
     tkey = "conv_l2" if key == "L2.conv" else None
-    roof = {"kernel": kernel_label(st, key), "bound": bound, "achieved": round(ach, 1), "peak": peak,
-            "unit": unit, "frac": round(ach / peak, 4), "traffic": traffic_bytes(tkey) if tkey else None,
-            "traffic_detail": measured_traffic(tkey) if tkey else None, "avg_us": round(dur[key], 2), "work": work}
+    roof = {"kernel": kernel_label(st, key), **roofline_of(work, dur[key]),
+            "traffic": traffic_bytes(tkey) if tkey else None,
+            "traffic_detail": measured_traffic(tkey) if tkey else None, "avg_us": round(dur[key], 2),
+            "work": {**work, "per": "launch"}}
+    kernels = [{"kernel": kernel_label(st, k), "us": round(v, 2), **roofline_of(kernel_work(st, k), v)}
+               for k, v in dur.items() if k != "end" and v > 0 and not (k.endswith(".quant") and
+                                                                         not st.quant_passes(int(k[1]) - 1))]
     out = {
         "metric": "Hadamard-INT8 conv TOPS + Mpixel/s per layer; % of INT8 MFMA / HBM peak",
         "value": round(total_ops / (step_us * 1e-6) / 1e12, 2),
@@ -580,7 +632,7 @@ def main():
                    "parallelism": "none"},
         "mpix_per_s": round(img_pix / (step_us * 1e-6) / 1e6, 1),
         "layers": per_layer,
-        "kernel_us": {kernel_label(st, k): round(v, 2) for k, v in dur.items() if k != "end"},
+        "kernels": kernels,
         "roofline": roof,
     }
     # the fused transform + quantization pass in the step (first single-read layer)

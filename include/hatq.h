@@ -93,8 +93,10 @@ typedef enum { HATQ_PAIRED = 1 } hatq_conv_flags;
  * 320 = P_20 (x) H~_16, index a*16 + l (Paley index a, Sylvester index l).
  * Those two are supported for DH layers in hatq_fwht_quant_act,
  * hatq_prepare_weights, hatq_conv_int8 and hatq_layer_forward (the DH
- * dequantization factor is fl(s_x s_w / b)); the requantizing, integer,
- * affine and profiling entry points and WH layers take powers of two. */
+ * dequantization factor is fl(s_x s_w / b)), and by the activation-side
+ * profiling and affine entry points (hatq_range_expansion,
+ * hatq_fwht_quant_act_affine) for whole blocks (c % b == 0); the entry points
+ * below that say so take 192 also for the convolution epilogues. */
 typedef struct {
     int32_t cin, cout;
     int32_t k;
@@ -237,7 +239,9 @@ int32_t hatq_fwht_quant_act_noalloc(const float *x, int32_t n, int32_t h, int32_
  *   next_hblock (I8 mode): the next operand's transform block.
  *   flags:     0 or HATQ_PAIRED.
  * Supported: cin_pad % 64 == 0 with k <= 8, or cin_pad <= 4 with k*k*cin_pad <= 128;
- * cout_pad % 64 == 0; WH block and next_hblock at most 64 (I8: as
+ * cout_pad % 64 == 0; WH block and next_hblock a power of two at most 64, or
+ * the Kronecker order 192 (P_12 (x) H~_16, applied as H~_16 then the Paley
+ * factor; the WH restore multiplies by B^T) when cout_pad == 192 (I8: as
  * hatq_conv_int8_requant).  Transposed: stride 2.  xq and y (F32, I32) must be
  * 16-byte aligned, y in I8 mode 4-byte aligned. */
 int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act_scale,
@@ -279,6 +283,7 @@ int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const fl
  *   s = 1, z = 0;  xq = clamp(rne(fl32(S / s)) + z, -128, 127).
  *   act_scale, act_zero: device fp32 / int32 [n], written.
  *   ws: device workspace of hatq_fwht_quant_affine_ws_bytes(n) bytes.
+ * hblock: a power of two <= 128 or a Kronecker order (192, 320).
  * Supported: c % hblock == 0, h*w*c % 4 == 0, n <= 65535. */
 size_t hatq_fwht_quant_affine_ws_bytes(int32_t n);
 int32_t hatq_fwht_quant_act_affine(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
@@ -300,7 +305,7 @@ int32_t hatq_weight_tapsums(const hatq_weights *W, int32_t *tapsum, void *stream
  * accumulators; HATQ_OUT_F32: the same epilogue with s_x = act_scale).
  *   act_zero: device int32 [n] (from hatq_fwht_quant_act_affine).
  *   tapsum:   from hatq_weight_tapsums for W.
- * Supported: as hatq_conv_int8 (no next-operand absmax). */
+ * Supported: as hatq_conv_int8 (no next-operand absmax; WH blocks Sylvester). */
 int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const float *act_scale,
                               const int32_t *act_zero, const int32_t *tapsum, int32_t n, int32_t h, int32_t w,
                               int32_t out_mode, void *y, void *stream);
@@ -317,8 +322,8 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
  *   s_x:   the static scale of W's input codes (unnormalized domain).
  *   s_y:   the static scale of the next operand's codes.
  *   next_hblock: the next operand's transform block (1: none), a power of two
- *          <= 64; the overflow bound depends on it, so the table serves only
- *          calls with this next_hblock.
+ *          <= 64 or 192; the overflow bound depends on it, so the table serves
+ *          only calls with this next_hblock.
  *   table: device int32 [2*cout_pad + 1], 16-byte aligned, written as
  *     M[c]         = rne(2^n rho_c), rho_c = u_c / (beta_out s_y),
  *     b_int[c]     = rne(b_c / u_c),  u_c = s_x s_w,c / beta_in,
@@ -336,7 +341,7 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
  *   with such a table writes all-zero codes.
  *
  * hatq_conv_int8_int_transition: convolution plus the integer epilogue,
- *   p = M (.) (acc + b_int) in int64, v = B_Cout p (WH; truncated to cout),
+ *   p = M (.) (acc + b_int) in int64, v = B_Cout^T p (WH; truncated to cout),
  *   w = B_next v (blocks of next_hblock), yq = clamp(rne(w / 2^n), -127, 127)
  *   with rne rounding exact halves to even; no act_scale (it is inside M).
  *   table: as written by hatq_int_transition_params for W and next_hblock.
@@ -358,7 +363,8 @@ int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, i
  * multiple of hblock).  Decided exactly as max|S|^2 > hblock * max|x|^2 in
  * fp64, S the fp32 butterfly transform hatq_fwht_quant_act applies.
  *   x:      device fp32 [n][h][w][c], 16-byte aligned; n <= 65535.
- *   hblock: power of two <= 128 (1: no transform, never an expansion).
+ *   hblock: a supported order (1: no transform, never an expansion); the
+ *           Kronecker orders 192 and 320 need c % hblock == 0 and h*w*c % 4 == 0.
  *   amax:   device fp32 [2n], written: max|x_k| at [k], max|S_k| at [n + k].
  *   flags:  NULL, or device int32 [n] receiving 1 (expands) or 0.
  *   count:  NULL, or device int32 [1] to which the number of expanding samples

@@ -775,11 +775,11 @@ static int64_t rne_shift(int64_t w, int n)
 int orc_int_transition(const int32_t *acc, int64_t P, int cout, int cout_p, const int32_t *M,
                        const int32_t *b_int, int n, int wb, int nb, int8_t *q)
 {
-    if (!is_pow2(wb) || !is_pow2(nb) || cout_p % wb || cout % nb || n < 0 || n > 62) return -1;
+    if (!supported(wb) || !supported(nb) || cout_p % wb || cout % nb || n < 0 || n > 62) return -1;
     int8_t *Ho = (int8_t *)malloc((size_t)wb * wb);
     int8_t *Hi = (int8_t *)malloc((size_t)nb * nb);
-    orc_sylvester(wb, Ho);
-    orc_sylvester(nb, Hi);
+    orc_hadamard(wb, Ho);               /* Sylvester for powers of two */
+    orc_hadamard(nb, Hi);
     #pragma omp parallel
     {
         int64_t *p = (int64_t *)malloc(sizeof(int64_t) * cout_p);
@@ -788,10 +788,11 @@ int orc_int_transition(const int32_t *acc, int64_t P, int cout, int cout_p, cons
         for (int64_t px = 0; px < P; ++px) {
             const int32_t *a = acc + px * cout_p;
             for (int c = 0; c < cout_p; ++c) p[c] = (int64_t)M[c] * ((int64_t)a[c] + b_int[c]);
+            /* the WH output restore multiplies by the transposed block (B^T B = b I) */
             for (int blk = 0; blk < cout_p; blk += wb)
                 for (int i = 0; i < wb; ++i) {
                     int64_t s = 0;
-                    for (int j = 0; j < wb; ++j) s += Ho[i * wb + j] * p[blk + j];
+                    for (int j = 0; j < wb; ++j) s += Ho[j * wb + i] * p[blk + j];
                     v[blk + i] = s;
                 }
             for (int blk = 0; blk < cout; blk += nb)
@@ -825,10 +826,10 @@ int orc_int_transition(const int32_t *acc, int64_t P, int cout, int cout_p, cons
 /* ------------------------------------------------------------------------- */
 int orc_range_expansion(const float *x, int n, int64_t P, int C, int b, float *ax, float *ah, int32_t *flags)
 {
-    if (!is_pow2(b) || C <= 0 || n <= 0 || P <= 0) return -1;
+    if (!supported(b) || C <= 0 || n <= 0 || P <= 0) return -1;
     const int Cp = round_up(C, b);
     int8_t *H = (int8_t *)malloc((size_t)b * b);
-    orc_sylvester(b, H);
+    orc_hadamard(b, H);                 /* Sylvester for a power of two */
     for (int k = 0; k < n; ++k) {
         const float *xs = x + (int64_t)k * P * C;
         float mx = 0.0f, mh = 0.0f;

@@ -501,9 +501,11 @@ hipError_t launch_range_b(const float *x, int n, int64_t P, int C, float *amax, 
         constexpr int I = ItemShape<B>::I;
         const int64_t items = (E + I - 1) / I;
         range_kernel<B><<<dim3(grid_x(items, kQuadsPerBlock, n, 2048), n), kThreads, 0, st>>>(x, E, amax);
-    } else {
+    } else if constexpr (kron_q(B) == 0) {
         const int64_t units = P * ((C + B - 1) / B);
         range_pad_kernel<B><<<dim3(grid_x(units, kThreads, n, 2048), n), kThreads, 0, st>>>(x, P, C, amax);
+    } else {
+        return hipErrorInvalidValue;   // Kronecker orders: whole blocks only
     }
     return hipGetLastError();
 }
@@ -534,6 +536,8 @@ hipError_t launch_act_quant_affine(const float *x, int n, int64_t E, int hblock,
         case 32: return launch_affine_b<32>(x, n, E, ws, xq, act_scale, act_zero, st);
         case 64: return launch_affine_b<64>(x, n, E, ws, xq, act_scale, act_zero, st);
         case 128: return launch_affine_b<128>(x, n, E, ws, xq, act_scale, act_zero, st);
+        case 192: return launch_affine_b<192>(x, n, E, ws, xq, act_scale, act_zero, st);
+        case 320: return launch_affine_b<320>(x, n, E, ws, xq, act_scale, act_zero, st);
         default: return hipErrorInvalidValue;
     }
 }
@@ -551,6 +555,8 @@ hipError_t launch_range_expansion(const float *x, int n, int64_t P, int C, int h
         case 32: e = launch_range_b<32>(x, n, P, C, amax, st); break;
         case 64: e = launch_range_b<64>(x, n, P, C, amax, st); break;
         case 128: e = launch_range_b<128>(x, n, P, C, amax, st); break;
+        case 192: e = launch_range_b<192>(x, n, P, C, amax, st); break;
+        case 320: e = launch_range_b<320>(x, n, P, C, amax, st); break;
         default: return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;

@@ -107,7 +107,13 @@ int32_t check_conv_supported(const hatq_weights *W) {
     bool fixed = false;
     for (int t : tiles) fixed |= (W->cout_pad == t);
     const int bn = fixed ? W->cout_pad : 64;
-    if (W->form == HATQ_WH && (bn % W->d.hblock != 0 || W->d.hblock > 64)) return HATQ_EUNSUPPORTED;
+    // the WH restore runs inside one wave: a Sylvester block up to 64 that tiles
+    // the columns, or the Kronecker order 192 on a 192-column tile
+    if (W->form == HATQ_WH) {
+        const int b = W->d.hblock;
+        const bool ok = (is_pow2(b) && b <= 64 && bn % b == 0) || (b == 192 && bn == 192);
+        if (!ok) return HATQ_EUNSUPPORTED;
+    }
     return HATQ_OK;
 }
 
@@ -126,13 +132,20 @@ int32_t check_weights(const hatq_weights *W) {
 
 int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next_absmax) {
     if (!next_absmax) return HATQ_OK;
-    if (!is_pow2(next_hblock) || next_hblock > 128) return HATQ_EINVAL;
+    if (!supported_order(next_hblock)) return HATQ_EINVAL;
     if (W->d.cout % next_hblock != 0) return HATQ_EUNSUPPORTED;
     const int tiles[] = {64, 128, 192, 256, 320};
     bool fixed = false;
     for (int t : tiles) fixed |= (W->cout_pad == t);
     const int bn = fixed ? W->cout_pad : 64;
-    if (next_hblock > 64 || (bn % next_hblock != 0 && next_hblock > 1)) return HATQ_EUNSUPPORTED;
+    // the next operand's transform runs inside one wave: a Sylvester block up
+    // to 64 that tiles the columns, or the Kronecker order 192 on a 192-column
+    // tile (320 would span the two launches of a 320-column layer)
+    if (hatq::kron_q(next_hblock)) {
+        if (next_hblock != 192 || bn != 192) return HATQ_EUNSUPPORTED;
+    } else if (next_hblock > 64 || (bn % next_hblock != 0 && next_hblock > 1)) {
+        return HATQ_EUNSUPPORTED;
+    }
     if (!aligned(next_absmax, 4)) return HATQ_EINVAL;
     return HATQ_OK;
 }
@@ -392,7 +405,6 @@ int32_t requant(const hatq_weights *W, const int8_t *xq, const float *act_scale,
         return HATQ_EINVAL;
     if (next_absmax && !aligned(next_absmax, 4)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
-    if (!is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
     // the transform and the code layout follow the next operand's blocks
     const float *probe = next_absmax ? next_absmax : next_scale;
     if ((s = check_next(W, next_hblock, probe)) != HATQ_OK) return s;
@@ -445,7 +457,7 @@ int32_t hatq_fwht_quant_act_affine(const float *x, int32_t n, int32_t h, int32_t
                                    void *stream) {
     if (!x || !xq || !act_scale || !act_zero || !ws || n <= 0 || n > 65535 || h <= 0 || w <= 0 || c <= 0)
         return HATQ_EINVAL;
-    if (!is_pow2(hblock) || hblock > 128) return HATQ_EINVAL;
+    if (!supported_order(hblock)) return HATQ_EINVAL;
     if (!aligned(x, 16) || !aligned(xq, 4) || !aligned(act_scale, 4) || !aligned(act_zero, 4) || !aligned(ws, 4))
         return HATQ_EINVAL;
     if (ws_bytes < (size_t)n * 8) return HATQ_EWORKSPACE;
@@ -488,7 +500,8 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
         !aligned(tapsum, 16))
         return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
-    if (!is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
+    // (the zero-point correction has no Kronecker variant: WH layers take Sylvester blocks)
+    if (W->form == HATQ_WH && !is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
     return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, 0, nullptr, 0, static_cast<hipStream_t>(stream),
@@ -506,8 +519,7 @@ int32_t hatq_int_transition_params(const hatq_weights *W, float s_x, float s_y, 
     if (s != HATQ_OK) return s;
     if (!table || !aligned(table, 16)) return HATQ_EINVAL;
     if (!(s_x > 0.0f) || !(s_y > 0.0f) || !std::isfinite(s_x) || !std::isfinite(s_y)) return HATQ_EINVAL;
-    if (!is_pow2(next_hblock) || next_hblock > 64) return HATQ_EINVAL;
-    if (!is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
+    if (!((is_pow2(next_hblock) && next_hblock <= 64) || next_hblock == 192)) return HATQ_EINVAL;
     const bool dh = W->form == HATQ_DH;
     hatq::IntParamArgs a;
     a.w_scale = W->w_scale;
@@ -532,7 +544,6 @@ int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, i
     if (flags & ~HATQ_PAIRED) return HATQ_EINVAL;
     if (!aligned(xq, 16) || !aligned(yq, 4) || !aligned(table, 16)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
-    if (!is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
     if ((s = check_next(W, next_hblock, reinterpret_cast<const float *>(table))) != HATQ_OK) return s;
     if (W->d.cout % 4) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;
@@ -544,11 +555,13 @@ int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, i
 int32_t hatq_range_expansion(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
                              float *amax, int32_t *flags, int32_t *count, void *stream) {
     if (!x || !amax || n <= 0 || n > 65535 || h <= 0 || w <= 0 || c <= 0) return HATQ_EINVAL;
-    if (!is_pow2(hblock) || hblock > 128) return HATQ_EINVAL;
+    if (!supported_order(hblock)) return HATQ_EINVAL;
     if (!aligned(x, 16) || !aligned(amax, 4)) return HATQ_EINVAL;
     if ((flags && !aligned(flags, 4)) || (count && !aligned(count, 4))) return HATQ_EINVAL;
     if (elems(n, h, w, c) < 0) return HATQ_EINVAL;
     const int64_t P = (int64_t)h * w;
+    // Kronecker orders: whole blocks and float4-aligned samples only
+    if (!is_pow2(hblock) && (c % hblock != 0 || (P * c) % 4 != 0)) return HATQ_EUNSUPPORTED;
     return hip_status(hatq::launch_range_expansion(x, n, P, c, hblock, amax, flags, count,
                                                    static_cast<hipStream_t>(stream)));
 }

@@ -304,11 +304,24 @@ struct Epi {
 using EpiGeneric = Epi<-1, -1>;
 using EpiGenericInt = Epi<-1, -1, 2>;   // the integer transition, blocks at run time
 using EpiGenericAffine = Epi<-1, -1, 3>;   // affine activations: zero-point correction
+// A Kronecker order (192) for the WH restore or the next operand, on a
+// 192-column tile: float modes (Q = 5) and the integer transition (Q = 6).
+using EpiKron = Epi<-1, -1, 5>;
+using EpiKronInt = Epi<-1, -1, 6>;
+
+// Whether a launch needs the Kronecker epilogue.
+inline bool kron_epilogue(const ConvArgs &a) {
+    const bool next = a.next_hblock == 192 && (a.next_absmax != nullptr || a.mode == 2 || a.mode == kModeIntTransition);
+    const bool restore = a.form == 1 && a.hblock == 192 && a.mode != 0;
+    return a.zx == nullptr && (next || restore);
+}
 
 // The variant a launch needs, or the generic one.
 template <typename E>
 bool epi_matches(const ConvArgs &a) {
     if constexpr (E::WB == -1) {
+        if constexpr (E::Q == 5 || E::Q == 6)
+            return kron_epilogue(a) && a.cout_pad == 192 && (a.mode == kModeIntTransition) == (E::Q == 6);
         return (a.mode == kModeIntTransition) == (E::Q == 2) && (a.zx != nullptr) == (E::Q == 3);
     } else {
         if ((a.zx != nullptr) != (E::Q == 3)) return false;
@@ -330,7 +343,7 @@ struct EpiFlags {
     bool f32, wh, want_abs, i8, iq, affine, store;
     __device__ explicit EpiFlags(const ConvArgs &a) {
         affine = E::Q == 3;
-        iq = E::Q == 2;   // integer transition (its own variants, generic ones included)
+        iq = E::Q == 2 || E::Q == 6;   // integer transition (its own variants, generic ones included)
         f32 = !iq && (generic ? a.mode != 0 : true);   // the fp32 arithmetic (F32 and I8 modes)
         wh = generic ? a.mode != 0 && a.form == 1 : WB != 0;
         want_abs = !iq && (generic ? a.mode == 1 && a.next_absmax != nullptr && a.next_hblock > 0
@@ -404,12 +417,13 @@ struct Epilogue {
     static constexpr int WB = E::WB, NB = E::NB;
     static constexpr bool generic = WB == -1;
     static constexpr int NBLK = FN / 4;
+    static constexpr bool kKron = (E::Q == 5 || E::Q == 6) && FN == 12;
     const ConvArgs &a;
     const Tile &t;
     const int row0, lane, p, q;
     const float *col_t, *col_b;
     const EpiFlags<E> fl;
-    bool full, z_bound, zpair, q_fast;
+    bool full, z_bound, zpair, q_fast, kron;
     float wave_m, seen, qs, qr;
     int nbk, rq_n, rq_pre, zp;
     int64_t rq_bias;
@@ -444,6 +458,15 @@ struct Epilogue {
         // itself (B_next y = B B z / b = z in exact arithmetic): its maximum and
         // its codes are taken from z, and neither butterfly runs.
         zpair = !fl.affine && z_bound && !fl.store && nbk > 1 && (fl.want_abs || fl.i8);
+        // A Kronecker order (192 = P_12 (x) H~_16) for the next operand or the
+        // WH restore spans the tile's three 64-channel blocks (a 192-column
+        // tile: a lane holds all twelve 16-channel groups of its pixel), so
+        // the Kronecker variants handle it after the last block (block_kron).
+        kron = false;
+        if constexpr (kKron) {
+            const bool nk = a.next_hblock == 192 && (fl.want_abs || fl.i8 || fl.iq);
+            kron = nk || (fl.wh && a.hblock == 192);
+        }
         // I8 mode: the sample's scale (from the absmax as the activation quantizer
         // derives it, or given), published by the sample's first tile
         qs = 1.0f;
@@ -468,7 +491,8 @@ struct Epilogue {
         if (fl.iq) {
             int n = __builtin_amdgcn_readfirstlane(a.rq_table[2 * a.cout_pad]);
             n = n < 0 ? 0 : (n > 62 ? 62 : n);   // the parameter call keeps n in [0, 62]
-            rq_pair = a.paired && fl.wh && (generic ? a.hblock == a.next_hblock : WB == NB) && a.hblock > 1;
+            rq_pair = a.paired && fl.wh && (generic ? a.hblock == a.next_hblock : WB == NB) && a.hblock > 1 &&
+                      (a.hblock & (a.hblock - 1)) == 0;
             if (rq_pair) {
                 const int lg = 31 - __builtin_clz(a.hblock);
                 rq_pre = lg > n ? lg - n : 0;
@@ -626,8 +650,168 @@ struct Epilogue {
         }
     }
 
+    // The sixteen values of 64-channel block k inside a row group's 48.
+    static __device__ __forceinline__ float (&grp(float (&v)[48], int k))[16] {
+        return *reinterpret_cast<float (*)[16]>(v + 16 * k);
+    }
+    static __device__ __forceinline__ int64_t (&grp(int64_t (&v)[48], int k))[16] {
+        return *reinterpret_cast<int64_t (*)[16]>(v + 16 * k);
+    }
+
+    // Float modes with a Kronecker order on the tile's 192 columns.  Channel c
+    // = 16 j + 4 q + r of the lane's pixel sits in v[4 j + r] (j = 4 k + jj the
+    // fragment): the Kronecker index a * 16 + l has a = j (the Paley factor over
+    // the twelve fragments, in registers) and l = 4 q + r (the H~_16 factor:
+    // register bits and lane bits 4-5, the first four stages of fwht_acc).  The
+    // stage order is the activation kernel's (H~_16, then the Paley factor,
+    // summed in ascending order), so the values are the ones it computes.
+    __device__ void block_kron(const v4i (&acc)[FM][FN]) {
+        const bool wh = fl.wh, want_abs = fl.want_abs, i8 = fl.i8, store = fl.store;
+        const int nb = a.next_hblock;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            float v[48];
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                v4i cc[4];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) cc[jj] = acc[i][4 * k + jj];
+                if (fl.affine) zero_point_fix(cc, i, k);
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int cl = 64 * k + 16 * jj + 4 * q;
+                    const float4 t4 = *reinterpret_cast<const float4 *>(col_t + cl);
+                    const float4 b4 = *reinterpret_cast<const float4 *>(col_b + cl);
+                    v[16 * k + 4 * jj + 0] = __builtin_fmaf((float)cc[jj][0], t4.x, b4.x);
+                    v[16 * k + 4 * jj + 1] = __builtin_fmaf((float)cc[jj][1], t4.y, b4.y);
+                    v[16 * k + 4 * jj + 2] = __builtin_fmaf((float)cc[jj][2], t4.z, b4.z);
+                    v[16 * k + 4 * jj + 3] = __builtin_fmaf((float)cc[jj][3], t4.w, b4.w);
+                }
+            }
+            if (wh) {
+                // the output restore: B^T z (the column factors carry 1/b)
+                if (a.hblock == 192) {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k) fwht_acc<16, true>(grp(v, k), 16);
+                    paley_stage_t<11>(v);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k) fwht_acc<-1, true>(grp(v, k), a.hblock);
+                }
+            }
+            if (store && valid[i]) {
+#pragma unroll
+                for (int k = 0; k < 3; ++k) store_group(a, t, row0, lane, i, k, grp(v, k));
+            }
+            if (!(want_abs || i8)) continue;
+            // rows past the grid are not part of the next operand (cout is a
+            // multiple of the next block, so every channel is)
+            if (!valid[i]) {
+#pragma unroll
+                for (int r = 0; r < 48; ++r) v[r] = 0.0f;
+            }
+            if (nb == 192) {
+                // channel order matters for the codes only
+                if (i8) {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k) fwht_acc<16, true>(grp(v, k), 16);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k) fwht_acc<16, false>(grp(v, k), 16);
+                }
+                paley_stage<11>(v);
+            } else if (nb > 1) {
+                if (i8) {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k) fwht_acc<-1, true>(grp(v, k), nb);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k) fwht_acc<-1, false>(grp(v, k), nb);
+                }
+            }
+            if (i8) {
+#pragma unroll
+                for (int k = 0; k < 3; ++k) {
+                    uint32_t w[4];
+                    quant16(grp(v, k), qs, qr, q_fast, w);
+                    store_codes(w, i, k);
+                }
+            } else {
+                float mm = 0.0f;
+#pragma unroll
+                for (int r = 0; r < 48; ++r) mm = fmaxf(mm, fabsf(v[r]));
+                wave_m = fmaxf(wave_m, mm);
+            }
+        }
+    }
+
+    // The integer transition with a Kronecker order (same layout; int64 is
+    // exact, so the stage order is free).
+    __device__ void block_int_kron(const v4i (&acc)[FM][FN]) {
+        const int nb = a.next_hblock;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            int64_t v[48];
+#pragma unroll
+            for (int k = 0; k < 3; ++k)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int cl = 64 * k + 16 * jj + 4 * q;
+                    const v4i m4 = *reinterpret_cast<const v4i *>(col_t + cl);
+                    const v4i b4 = *reinterpret_cast<const v4i *>(col_b + cl);
+                    const v4i c4 = acc[i][4 * k + jj];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        v[16 * k + 4 * jj + r] = (int64_t)m4[r] * (int64_t)(c4[r] + b4[r]);
+                }
+            if (fl.wh) {
+                if (a.hblock == 192) {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k) fwht_acc_i64<16>(grp(v, k), 16);
+                    paley_stage_i64<11, true>(v);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k) fwht_acc_i64<-1>(grp(v, k), a.hblock);
+                }
+            }
+            if (nb == 192) {
+#pragma unroll
+                for (int k = 0; k < 3; ++k) fwht_acc_i64<16>(grp(v, k), 16);
+                paley_stage_i64<11, false>(v);
+            } else {
+#pragma unroll
+                for (int k = 0; k < 3; ++k) fwht_acc_i64<-1>(grp(v, k), nb);
+            }
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                uint32_t c[16];
+                if (rq_n >= 32) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) c[r] = int_code_hi(v[16 * k + r], rq_n - 32, rq_bias);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) c[r] = int_code(v[16 * k + r], rq_n, rq_bias);
+                }
+                uint32_t w[4];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+                    w[jj] = pack_low_bytes(c[4 * jj], c[4 * jj + 1], c[4 * jj + 2], c[4 * jj + 3]);
+                store_codes(w, i, k);
+            }
+        }
+    }
+
     // 64-channel block k of every row group (one set of column factors serves all)
     __device__ __forceinline__ void block(const v4i (&acc)[FM][FN], int k) {
+        if constexpr (kKron) {
+            if (kron) {
+                if (k == NBLK - 1) {
+                    if (fl.iq) block_int_kron(acc);
+                    else block_kron(acc);
+                }
+                return;
+            }
+        }
         if (fl.iq) {
             block_int(acc, k);
             return;
@@ -1200,6 +1384,7 @@ hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
 // Variants compiled for the layer shapes of the analysis transforms: DH or WH
 // blocks of 64, next operand blocked by 64 (DH next), 1 (WH next) or none.
 #define HATQ_GENERIC_EPILOGUES EpiGenericInt, EpiGenericAffine, EpiGeneric
+#define HATQ_KRON_EPILOGUES EpiKron, EpiKronInt
 #define HATQ_HOT_EPILOGUES \
     Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_GENERIC_EPILOGUES
 
@@ -1239,7 +1424,9 @@ template <int CS>
 hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
     if (a.cout_pad % 192 == 0) {
         if constexpr (CS == 3)
-            return with_epilogue<Epi<64, 64, 1>, Epi<64, 64, 2>, Epi<64, 64, 4>, HATQ_HOT_EPILOGUES>(a, [&](auto e) {
+            return with_epilogue<Epi<64, 64, 1>, Epi<64, 64, 2>, Epi<64, 64, 4>, Epi<0, 64>, Epi<0, 1>, Epi<0, 0>,
+                                 Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_KRON_EPILOGUES, HATQ_GENERIC_EPILOGUES>(
+                a, [&](auto e) {
                 // the requantizing pass (two transforms and the quantizer per
                 // value) keeps one row group per wave: with two it spilled
                 if constexpr (decltype(e)::Q == 1)
@@ -1247,7 +1434,7 @@ hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
                 else
                     return launch_rowrun<HATQ_RR_TH, HATQ_RR_TW, 192, CS, decltype(e), HATQ_RR_MINB>(a, st);
             });
-        return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+        return with_epilogue<HATQ_KRON_EPILOGUES, HATQ_GENERIC_EPILOGUES>(
             a, [&](auto e) { return launch_rowrun<2, 64, 192, CS, decltype(e)>(a, st); });
     }
     if (a.cout_pad % 128 == 0)
@@ -1257,15 +1444,17 @@ hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
         a, [&](auto e) { return launch_rowrun<2, 64, 64, CS, decltype(e)>(a, st); });
 }
 
-template <int TH, int TW, int BN, int CS>
+template <int TH, int TW, int BN, int CS, bool KRON = false>
 hipError_t launch_gather(const ConvArgs &a, hipStream_t st) {
     ConvArgs b = a;
     const int64_t tiles = set_tiles(b, TH, TW, BN);
     if (tiles <= 0 || tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-    return with_epilogue<HATQ_GENERIC_EPILOGUES>(b, [&](auto e) {
+    auto launch = [&](auto e) {
         conv_gather_kernel<TH, TW, BN, CS, decltype(e)><<<(unsigned)tiles, kThreads, 0, st>>>(b);
         return hipGetLastError();
-    });
+    };
+    if constexpr (KRON) return with_epilogue<HATQ_KRON_EPILOGUES, HATQ_GENERIC_EPILOGUES>(b, launch);
+    else return with_epilogue<HATQ_GENERIC_EPILOGUES>(b, launch);
 }
 
 template <int CS>
@@ -1273,7 +1462,7 @@ hipError_t launch_gather_n(const ConvArgs &a, hipStream_t st) {
     switch (a.cout_pad) {
         case 64: return launch_gather<8, 32, 64, CS>(a, st);
         case 128: return launch_gather<8, 32, 128, CS>(a, st);
-        case 192: return launch_gather<8, 32, 192, CS>(a, st);
+        case 192: return launch_gather<8, 32, 192, CS, true>(a, st);
         case 256: return launch_gather<4, 32, 256, CS>(a, st);
         case 320: return launch_gather<4, 32, 320, CS>(a, st);
         default: return launch_gather<8, 32, 64, CS>(a, st);
@@ -2171,7 +2360,7 @@ hipError_t conv_part_halo192_a(const ConvArgs &a, bool *hit, hipStream_t st, int
 #endif
 #if HATQ_PART(2)
 hipError_t conv_part_halo192_b(const ConvArgs &a, hipStream_t st, int n_base, bool split) {
-    return with_epilogue<Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_GENERIC_EPILOGUES>(
+    return with_epilogue<Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_KRON_EPILOGUES, HATQ_GENERIC_EPILOGUES>(
         a, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st, n_base, split); });
 }
 #endif
@@ -2184,7 +2373,8 @@ hipError_t conv_part_halo128(const ConvArgs &a, hipStream_t st, int n_base, bool
 #endif
 #if HATQ_PART(3)
 hipError_t conv_part_pipe192(const ConvArgs &a, hipStream_t st) {
-    return with_epilogue<HATQ_HOT_EPILOGUES>(
+    return with_epilogue<Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_KRON_EPILOGUES,
+                         HATQ_GENERIC_EPILOGUES>(
         a, [&](auto e) { return launch_pipe<8, 32, 192, 5, decltype(e)>(a, st); });
 }
 #endif

@@ -174,6 +174,53 @@ __device__ __forceinline__ void paley_stage(float (&v)[R4]) {
     for (int r = 0; r < R4; ++r) v[r] = out[r];
 }
 
+// The transposed factor, out[a] = sum over c, ascending, of P[c][a] * v[c]: the
+// WH output restore of a Kronecker order multiplies by B^T (B^T B = m I; a
+// Paley-I matrix is not symmetric).
+template <int Q, int R4>
+__device__ __forceinline__ void paley_stage_t(float (&v)[R4]) {
+    constexpr int P = Q + 1;
+    static_assert(R4 == 4 * P, "one register group per Paley index");
+    constexpr Paley1Table<Q> H{};
+    float out[R4];
+#pragma unroll
+    for (int a = 0; a < P; ++a)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float acc = H.s[0][a] > 0 ? v[j] : -v[j];
+#pragma unroll
+            for (int c = 1; c < P; ++c) acc = H.s[c][a] > 0 ? acc + v[4 * c + j] : acc - v[4 * c + j];
+            out[4 * a + j] = acc;
+        }
+#pragma unroll
+    for (int r = 0; r < R4; ++r) v[r] = out[r];
+}
+
+// The same on int64 values (exact, so any summation order), one register
+// position j at a time to keep the temporaries small.
+template <int Q, bool TRANSPOSED, int R4>
+__device__ __forceinline__ void paley_stage_i64(int64_t (&v)[R4]) {
+    constexpr int P = Q + 1;
+    static_assert(R4 == 4 * P, "one register group per Paley index");
+    constexpr Paley1Table<Q> H{};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        int64_t out[P];
+#pragma unroll
+        for (int a = 0; a < P; ++a) {
+            int64_t acc = 0;
+#pragma unroll
+            for (int c = 0; c < P; ++c) {
+                const int sgn = TRANSPOSED ? H.s[c][a] : H.s[a][c];
+                acc = sgn > 0 ? acc + v[4 * c + j] : acc - v[4 * c + j];
+            }
+            out[a] = acc;
+        }
+#pragma unroll
+        for (int a = 0; a < P; ++a) v[4 * a + j] = out[a];
+    }
+}
+
 // Quad layout: one quad (4 consecutive lanes) owns an item of I = max(64, b)
 // consecutive floats; lane t of the quad holds channels 16*i + 4*t + j in
 // v[4*i + j].  Channel bits 0-1 (j) and 4+ (i) are inside the thread, bits 2-3

@@ -102,17 +102,183 @@ def test_layer_forward_heavy_tailed(orc, c):
 
 
 def test_unsupported_uses_are_rejected(orc):
-    c = LAYERS[0]
-    n, h, w, cin, cout, k, s, p, tr, op, form, hb = c
-    _, ref, layer = _layer(orc, c, 323)
-    xq = torch.zeros((n, h, w, cin), dtype=torch.int8, device="cuda")
-    sx = torch.ones(n, device="cuda")
-    with pytest.raises(hatq.HatqError):
-        hatq.hatq_conv_int8_requant(layer, xq, sx, 64, next_scale=torch.ones(n, device="cuda"))
-    with pytest.raises(hatq.HatqError):
-        hatq.hatq_range_expansion(torch.zeros((1, 2, 2, 192), device="cuda"), 192)
-    wh = hatq.hatq_prepare_weights(hatq.desc(64, 192, 3, 1, 1, 192), "WH",
-                                   torch.ones(192, 64, 3, 3, device="cuda"), torch.zeros(192, device="cuda"))
-    with pytest.raises(hatq.HatqError):      # the WH restore runs power-of-two blocks only
-        hatq.hatq_conv_int8(wh, torch.zeros((1, 8, 8, 64), dtype=torch.int8, device="cuda"),
-                            torch.ones(1, device="cuda"), hatq.HATQ_OUT_F32)
+    """What stays outside the kernels: the order 320 in a convolution epilogue
+    (a 320-column layer runs as two launches, so a 320 block would span both),
+    192 on a 320-column layer, a Kronecker block cut by the channel count in the
+    profiling pass, and the affine zero-point correction with a Kronecker WH
+    restore.  Each is rejected before any launch."""
+    wt = torch.ones(320, 192, 5, 5, device="cuda")
+    b0 = torch.zeros(320, device="cuda")
+    wh320 = hatq.hatq_prepare_weights(hatq.desc(192, 320, 5, 2, 2, 320), "WH", wt, b0)
+    xq = torch.zeros((1, 9, 9, 192), dtype=torch.int8, device="cuda")
+    sx = torch.ones(1, device="cuda")
+    with pytest.raises(hatq.HatqError) as e:
+        hatq.hatq_conv_int8(wh320, xq, sx, hatq.HATQ_OUT_F32)
+    assert e.value.status == hatq.HATQ_EUNSUPPORTED
+    dh320 = hatq.hatq_prepare_weights(hatq.desc(192, 320, 5, 2, 2, 64), "DH", wt, b0)
+    for nb in (192, 320):
+        with pytest.raises(hatq.HatqError) as e:
+            hatq.hatq_conv_int8(dh320, xq, sx, hatq.HATQ_OUT_F32, next_hblock=nb,
+                                next_absmax=torch.zeros(1, device="cuda"))
+        assert e.value.status == hatq.HATQ_EUNSUPPORTED
+    with pytest.raises(hatq.HatqError) as e:
+        hatq.hatq_range_expansion(torch.zeros((1, 2, 2, 200), device="cuda"), 192)
+    assert e.value.status == hatq.HATQ_EUNSUPPORTED
+    wh192 = hatq.hatq_prepare_weights(hatq.desc(192, 192, 5, 2, 2, 192), "WH", wt[:192], b0[:192])
+    zx = torch.zeros(1, dtype=torch.int32, device="cuda")
+    with pytest.raises(hatq.HatqError) as e:
+        hatq.hatq_conv_int8_affine(wh192, xq, sx, zx, hatq.hatq_weight_tapsums(wh192), hatq.HATQ_OUT_F32)
+    assert e.value.status == hatq.HATQ_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("m", [192, 320])
+def test_range_expansion_kronecker(orc, m):
+    """The profiling statistic with a Kronecker order: the per-sample maxima
+    against the oracle's dense transform (bit-exact on dyadic inputs, within
+    the butterfly's rounding on heavy-tailed ones), the indicator and count."""
+    rng = np.random.default_rng(330 + m)
+    x = synth.dyadic_integers(rng, (3, 5, 7, 2 * m))
+    x[1] = 5.0                                          # a constant sample: expands (Paley-I first row)
+    ax, ah, fl = orc.range_expansion(x, m)
+    count = torch.zeros(1, dtype=torch.int32, device="cuda")
+    amax, flags = hatq.hatq_range_expansion(dev(x), m, count=count)
+    a = host(amax)
+    assert np.array_equal(a[:3], ax) and np.array_equal(a[3:], ah)
+    assert np.array_equal(host(flags), fl) and int(host(count)[0]) == int(fl.sum()) and fl[1] == 1
+    xh = synth.heavy_tailed_activations(rng, (2, 9, 11, m))
+    ax, ah, fl = orc.range_expansion(xh, m)
+    amax, flags = hatq.hatq_range_expansion(dev(xh), m)
+    a = host(amax)
+    assert np.array_equal(a[:2], ax)
+    # each transformed value: 4 rounded butterfly stages, then a Paley sum of
+    # m/16 terms (m/16 - 1 rounded additions), against one rounding in fp64
+    k = 4 + m // 16 - 1
+    u = 2.0 ** -24
+    blk = np.abs(xh.astype(np.float64)).reshape(2, -1, m).sum(-1).max(-1)
+    tol = k * u / (1 - k * u) * blk + u * ah
+    assert np.all(np.abs(a[2:].astype(np.float64) - ah) <= tol)
+    decided = np.abs(ah.astype(np.float64) ** 2 - m * ax.astype(np.float64) ** 2) > 2 * ah * tol
+    assert np.array_equal(host(flags)[decided], fl[decided])
+
+
+@pytest.mark.parametrize("m", [192, 320])
+def test_affine_quant_kronecker(orc, m):
+    """Affine activation codes with a Kronecker order: scale and zero point
+    bit-exact and codes bit-exact on dyadic inputs (identical fp32 transform
+    outputs); the code rule on heavy-tailed inputs."""
+    rng = np.random.default_rng(340 + m)
+    x = synth.dyadic_integers(rng, (2, 5, 9, m))
+    S = orc.activation_transform(x, m)
+    q_ref, s_ref, z_ref = orc.quantize_affine(S)
+    q, s, z = hatq.hatq_fwht_quant_act_affine(dev(x), m)
+    assert np.array_equal(host(s), s_ref) and np.array_equal(host(z), z_ref)
+    assert np.array_equal(host(q), q_ref)                # affine codes span [-128, 127]
+    xh = synth.heavy_tailed_activations(rng, (2, 13, 17, m))
+    q_ref, s_ref, z_ref = orc.quantize_affine(orc.activation_transform(xh, m))
+    q, s, z = hatq.hatq_fwht_quant_act_affine(dev(xh), m)
+    assert_scale_ulp(host(s), s_ref, ulps=2)
+    assert np.all(np.abs(host(z).astype(np.int64) - z_ref) <= 1)
+    if np.array_equal(host(z), z_ref):
+        d = np.abs(host(q).astype(np.int32) - q_ref.astype(np.int32))
+        assert d.max() <= 1 and np.count_nonzero(d) <= 1e-4 * d.size
+
+
+# The Kronecker order 192 in the convolution epilogues (192-column tiles):
+# (n, h, w, cin, cout, k, stride, pad, transposed, out_pad, form, hblock, next block)
+KCONV = [(2, 17, 21, 192, 192, 5, 2, 2, False, 0, "DH", 64, 192),     # window kernel, next operand 192
+         (1, 13, 15, 192, 192, 5, 2, 2, False, 0, "WH", 192, 1),      # window kernel, WH restore 192
+         (1, 11, 9, 192, 192, 5, 2, 2, False, 0, "WH", 192, 192),     # both
+         (1, 9, 13, 192, 192, 3, 1, 1, False, 0, "DH", 192, 192),     # pipeline kernel
+         (2, 13, 17, 3, 192, 5, 2, 2, False, 0, "WH", 192, 64),       # row-run kernel (3 input channels)
+         (1, 6, 7, 192, 192, 5, 2, 2, True, 1, "DH", 64, 192)]        # transposed phases
+KIDS = [f"{c[10]}{c[11]}-{c[3]}to{c[4]}k{c[5]}{'T' if c[8] else ''}-next{c[12]}" for c in KCONV]
+
+
+def _kron_layer(orc, c, seed):
+    n, h, w, cin, cout, k, s, p, tr, op, form, hb, nb = c
+    rng = np.random.default_rng(seed)
+    wt, b = synth.layer_params(rng, cin, cout, k, tr)
+    ref = orc.prepare_weights(wt, b, cin=cin, cout=cout, k=k, stride=s, pad=p, form=form, hblock=hb,
+                              transposed=tr, out_pad=op)
+    layer = hatq.hatq_prepare_weights(hatq.desc(cin, cout, k, s, p, hb, tr, op), form, dev(wt), dev(b))
+    x = synth.heavy_tailed_activations(rng, (n, h, w, cin))
+    return ref, layer, orc.layer_forward(x, ref), nb
+
+
+def _gamma(k):
+    u = 2.0 ** -24
+    return k * u / (1 - k * u)
+
+
+def _transform_stages(b):
+    """Rounded fp32 stages between an input value and a transformed one."""
+    return 4 + b // 16 - 1 if b == 192 else int(np.log2(b)) if b > 1 else 0
+
+
+@pytest.mark.parametrize("c", KCONV, ids=KIDS)
+def test_kron_epilogue_f32_and_absmax(orc, c):
+    ref, layer, r, nb = _kron_layer(orc, c, 400)
+    n = r.y.shape[0]
+    y0 = host(hatq.hatq_conv_int8(layer, dev(r.xq), dev(r.sx), hatq.HATQ_OUT_F32))
+    nam = torch.full((n,), -1.0, device="cuda")
+    yd = hatq.hatq_conv_int8(layer, dev(r.xq), dev(r.sx), hatq.HATQ_OUT_F32, next_hblock=nb, next_absmax=nam)
+    y = host(yd)
+    assert np.array_equal(y, y0)
+    if c[10] == "DH":
+        assert np.array_equal(y, r.y)
+    else:
+        assert_range_rel(y, r.y)
+    # the fused absmax: what the activation kernel computes from the stored output
+    _, s2 = hatq.hatq_fwht_quant_act(yd, nb)
+    assert torch.equal(hatq.hatq_fwht_quant_act(yd, nb, absmax=nam)[1], s2)
+    S = orc.activation_transform(y, nb)
+    A = np.abs(S.astype(np.float64)).reshape(n, -1).max(1)
+    blk = np.abs(y.astype(np.float64)).reshape(n, -1, nb).sum(-1).max(-1)
+    assert np.all(np.abs(host(nam) - A) <= _gamma(_transform_stages(nb)) * blk + 2.0 ** -24 * A)
+    # the absmax alone (no fp32 output) gives the same value
+    nam2 = torch.full((n,), -1.0, device="cuda")
+    hatq.hatq_conv_int8(layer, dev(r.xq), dev(r.sx), hatq.HATQ_OUT_F32, next_hblock=nb, next_absmax=nam2,
+                        absmax_only=True)
+    assert torch.equal(nam, nam2)
+
+
+@pytest.mark.parametrize("c", KCONV, ids=KIDS)
+def test_kron_epilogue_requant(orc, c):
+    ref, layer, r, nb = _kron_layer(orc, c, 410)
+    n = r.y.shape[0]
+    xq, sx = dev(r.xq), dev(r.sx)
+    nam = torch.full((n,), -1.0, device="cuda")
+    hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=nb, next_absmax=nam, absmax_only=True)
+    yq, sq = hatq.hatq_conv_int8_requant(layer, xq, sx, nb, next_absmax=nam)
+    # the two-kernel GPU path: identical (same fp32 stages in the same order)
+    y = hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32)
+    q2, s2 = hatq.hatq_fwht_quant_act(y, nb, absmax=nam)
+    assert torch.equal(sq, s2) and torch.equal(yq, q2)
+    # the oracle's composition: codes of fl32(B_next y_ref) within the code rule
+    q_ref, s_ref = orc.quantize_symmetric(orc.activation_transform(r.y, nb))
+    d = np.abs(host(sq).astype(np.float64) / s_ref - 1)
+    assert np.all(d <= 2e-5), d
+    assert_codes(host(yq), q_ref, what=f"requant codes next {nb}")
+    # a static scale through hatq_conv_int8's I8 mode
+    y8 = hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_I8, next_hblock=nb, out_scale=sq)
+    assert torch.equal(y8, yq)
+
+
+@pytest.mark.parametrize("c", KCONV, ids=KIDS)
+def test_kron_int_transition_bit_exact(orc, c):
+    ref, layer, r, nb = _kron_layer(orc, c, 420)
+    s_x = float(r.sx.max())
+    xq_b = np.clip(np.rint(r.S / s_x), -127, 127).astype(np.int8)      # one static scale for the batch
+    acc = orc.conv_int8(xq_b, ref.wq, stride=ref.stride, pad=ref.pad, transposed=ref.transposed,
+                        out_pad=ref.out_pad)
+    y = orc.epilogue(acc, np.full(r.y.shape[0], s_x, np.float32), ref)
+    s_y = float(np.float32(np.abs(orc.activation_transform(y, nb)).max() / np.float32(127.0)))
+    rq = orc.int_requant_params(ref, s_x, s_y, nb)
+    table, shift = hatq.hatq_int_transition_params(layer, s_x, s_y, nb)
+    t = host(table)
+    cp = layer.w.cout_pad
+    assert shift == rq.shift and np.array_equal(t[:cp], rq.M) and np.array_equal(t[cp:2 * cp], rq.b_int)
+    q_ref = orc.int_transition(acc, ref, rq, nb)
+    yq = hatq.hatq_conv_int8_int_transition(layer, dev(xq_b), nb, table)
+    assert_codes(host(yq), q_ref, exact=True, what=f"integer transition next {nb}")
+    assert np.abs(q_ref.astype(np.int32)).max() == 127

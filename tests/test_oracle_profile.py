@@ -88,3 +88,29 @@ def test_select_form_rule():
     for bad in [(1, 0), (-1, 4), (5, 4)]:
         with pytest.raises(ValueError):
             oracle.select_form(*bad)
+
+
+@pytest.mark.parametrize("b", [12, 20, 52, 192])
+def test_kronecker_orders_statistic(orc, b):
+    """The statistic with the paper's non-power-of-two orders (the supplementary
+    Hadamard construction).  Paley-I matrices (q + 1 = 12, 20; 192 = P_12 (x)
+    H~_16) have an all-ones first row, so a constant block lands on it (max|S|
+    = b|c|, an expansion); for every order a one-hot block gives a column of
+    +-1 entries (max|S| = |x|, no expansion), and a random input equals the
+    dense transform by numpy with the same matrix."""
+    H = orc.hadamard(b).astype(np.float64)
+    if orc.hadamard_base(b)[1] != 2:                   # Paley-I based
+        assert np.all(H[0] == 1)
+        x = np.full((1, 2, 3, b), -0.75, np.float32)
+        ax, ah, fl = orc.range_expansion(x, b)
+        assert ah[0] == np.float32(0.75 * b) and fl[0] == 1
+    e = np.zeros((1, 1, 1, b), np.float32)
+    e[0, 0, 0, b // 3] = 2.5
+    ax, ah, fl = orc.range_expansion(e, b)
+    assert ax[0] == 2.5 and ah[0] == 2.5 and fl[0] == 0
+    rng = np.random.default_rng(b)
+    x = rng.standard_normal((2, 3, 4, 2 * b)).astype(np.float32)
+    ax, ah, fl = orc.range_expansion(x, b)
+    S = (x.reshape(2, -1, b).astype(np.float64) @ H.T).astype(np.float32)
+    np.testing.assert_array_equal(ah, np.abs(S).reshape(2, -1).max(1))
+    np.testing.assert_array_equal(fl, (ah.astype(np.float64) ** 2 > b * ax.astype(np.float64) ** 2).astype(np.int32))
