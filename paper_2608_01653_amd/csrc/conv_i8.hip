@@ -329,6 +329,8 @@ bool epi_matches(const ConvArgs &a) {
         if (E::Q == 3) return a.mode == 1 && wb == E::WB && a.next_absmax == nullptr;
         if (E::Q == 4)
             return a.mode == 1 && a.y == nullptr && a.next_absmax != nullptr && wb == E::WB && a.next_hblock == E::NB;
+        if (E::Q == 1)   // the codes with the dynamic scale (from the next operand's absmax)
+            return a.mode == 2 && a.q_absmax != nullptr && wb == E::WB && a.next_hblock == E::NB;
         if (E::Q) return a.mode == (E::Q == 2 ? kModeIntTransition : 2) && wb == E::WB && a.next_hblock == E::NB;
         const int nb = a.next_absmax != nullptr ? a.next_hblock : 0;
         return a.mode == 1 && wb == E::WB && nb == E::NB;
@@ -369,6 +371,8 @@ __device__ __forceinline__ void store_group_impl(const ConvArgs &a, const Tile &
     for (int jj = 0; jj < 4; ++jj) {
         const int cl = 64 * k + 16 * jj + 4 * q;
         if ((ycols & 3) == 0) {
+            // (plain stores: streaming ones made the layer-2 conv 5 % slower and
+            // the next quantization 9 % faster, the step slower overall)
             if (cl < ncols)
                 *reinterpret_cast<float4 *>(yp + cl) = make_float4(v[4 * jj], v[4 * jj + 1], v[4 * jj + 2], v[4 * jj + 3]);
         } else {
@@ -386,12 +390,16 @@ __device__ __forceinline__ void store_group_impl(const ConvArgs &a, const Tile &
 // the fast path's range); w[jj] packs the codes of registers 4*jj .. 4*jj+3.
 // (A per-register exact path behind a wave vote was measured slower: the
 // branches split the straight-line code.)
+// CLAMP = false when the scale comes from the values' own maximum (or an upper
+// bound of it): then |u / s| <= 127 (1 + 2^-23) and every rounding stays in
+// [-127, 127] without the clamp.
+template <bool CLAMP = true>
 __device__ __forceinline__ void quant16(const float (&u)[16], float s, float r, bool fast_ok, uint32_t (&w)[4]) {
     uint32_t c[16];
     bool near = !fast_ok;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
-        const float tq = clamp127(u[k] * r);
+        const float tq = CLAMP ? clamp127(u[k] * r) : u[k] * r;
         const float uf = tq + HATQ_MAGIC;
         const float kf = uf - HATQ_MAGIC;
         near |= fabsf(tq - kf) > HATQ_NEAR_TIE;
@@ -418,6 +426,8 @@ struct Epilogue {
     static constexpr bool generic = WB == -1;
     static constexpr int NBLK = FN / 4;
     static constexpr bool kKron = (E::Q == 5 || E::Q == 6) && FN == 12;
+    // the fixed I8 variants take the dynamic scale only (epi_matches): no clamp
+    static constexpr bool kClamp = E::Q != 1;
     const ConvArgs &a;
     const Tile &t;
     const int row0, lane, p, q;
@@ -871,7 +881,7 @@ struct Epilogue {
                 // v holds z
                 if (i8) {
                     uint32_t w[4];
-                    quant16(v, qs, qr, q_fast, w);
+                    quant16<kClamp>(v, qs, qr, q_fast, w);
                     store_codes(w, i, k);
                 } else {
                     // the maximum of |z| over the valid pixels and channels
@@ -938,7 +948,7 @@ struct Epilogue {
                     // codes of B_next y in channel order (restoring butterflies)
                     fwht_acc<NB, true>(v, a.next_hblock);
                     uint32_t w[4];
-                    quant16(v, qs, qr, q_fast, w);
+                    quant16<kClamp>(v, qs, qr, q_fast, w);
                     store_codes(w, i, k);
                 } else {
                     wave_m = fmaxf(wave_m, fwht_acc_absmax<NB>(v, a.next_hblock));
