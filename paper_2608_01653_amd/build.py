@@ -21,7 +21,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhatq.so")
 SOURCES = ["api.cpp", "act_quant.hip", "conv_i8.hip", "weights.hip"]
-CONV_PARTS = 13         # HATQ_CONV_PART = 0 .. 12 in conv_i8.hip
+CONV_PARTS = 14         # HATQ_CONV_PART = 0 .. 13 in conv_i8.hip
 OBJ_DIR = os.path.join(ROOT, "_build", "hatq")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -75,7 +75,10 @@ def build(verbose: bool = False, jobs: int = 0) -> str:
                 if err.strip():
                     print(err, file=sys.stderr)
     tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *[o for _, _, o in _units()], "-o", tmp])
+    # -z defs: a symbol left unresolved (a part's entry point that another
+    # compilation of conv_i8.hip does not define) fails the link, not the load
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,-z,defs", *[o for _, _, o in _units()],
+          "-o", tmp])
     os.replace(tmp, LIB)
     return LIB
 

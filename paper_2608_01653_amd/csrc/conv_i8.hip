@@ -1000,6 +1000,14 @@ __device__ __forceinline__ int xcd_logical_tile() { return xcd_tile(blockIdx.x, 
 // patch buffers).  Accumulators stay small (two 16-point groups per wave) so
 // two blocks share a CU.
 // ---------------------------------------------------------------------------
+// The input patch of a TH x TW tile of one sample nb in LDS: patch row r holds
+// the input bytes of row ih0 + r from the 4-aligned address at or below its
+// first byte (pixel iw0), fetched as aligned dwords; the row's alignment shift
+// is (first byte address) mod 4.  load() issues every global load of a patch at
+// once (no branches: rows outside the image use an out-of-range offset and
+// read 0); store() applies the masks (bytes of columns inside both the patch
+// and the image) and writes the LDS copy.  The range check drops the whole
+// dword that straddles the end of the input; its bytes are read one by one.
 template <int TH, int TW, int CIN>
 struct RowRunPatch {
     static constexpr int PH = (TH - 1) * 2 + 8;                 // patch rows (stride <= 2, k <= 8)
@@ -1008,6 +1016,62 @@ struct RowRunPatch {
     static constexpr int RW = RS / 4;
     static constexpr int WORDS = PH * RW;
     static constexpr int PIT = (WORDS + kThreads - 1) / kThreads;
+
+    const ConvArgs &a;
+    const int nb;
+    const int prow, pcols;   // patch rows and columns in use
+    const int64_t in_bytes;
+    const __amdgpu_buffer_rsrc_t rx;
+
+    __device__ __forceinline__ RowRunPatch(const ConvArgs &a_, int nb_)
+        : a(a_), nb(nb_), prow((TH - 1) * a_.sa + a_.k), pcols((TW - 1) * a_.sa + a_.k),
+          in_bytes((int64_t)a_.n * a_.h * a_.w * CIN),
+          rx(__builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t *>(a_.xq), (short)0, (int)in_bytes, 0x00020000)) {}
+
+    __device__ __forceinline__ int row_shift(int ih, int iw0) const {
+        const uint32_t g = ((uint32_t)(nb * a.h + ih) * (uint32_t)a.w + (uint32_t)iw0) * (uint32_t)CIN;
+        return (int)(g & 3u);
+    }
+
+    __device__ __forceinline__ void load(const Tile &tl, uint32_t (&pwd)[PIT]) const {
+        const int tid = threadIdx.x;
+        const int ih0 = tl.gi0 * a.sa + a.bah, iw0 = tl.gj0 * a.sa + a.baw;
+#pragma unroll
+        for (int it = 0; it < PIT; ++it) {
+            const int e4 = tid + it * kThreads;
+            const int r = e4 / RW, wi = e4 - r * RW;
+            const int ih = ih0 + r;
+            const bool live = e4 < WORDS && r < prow && (unsigned)ih < (unsigned)a.h;
+            const int64_t ga = ((int64_t)(nb * a.h + ih) * a.w + iw0) * CIN + 4 * wi - row_shift(ih, iw0);
+            pwd[it] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rx, (int)(live ? (uint32_t)ga : 0xFFFFFFFFu),
+                                                                     0, 0);
+        }
+    }
+
+    __device__ __forceinline__ void store(const Tile &tl, const uint32_t (&pwd)[PIT], uint32_t *dst) const {
+        const int tid = threadIdx.x;
+        const int ih0 = tl.gi0 * a.sa + a.bah, iw0 = tl.gj0 * a.sa + a.baw;
+        const int vlo = (iw0 < 0 ? -iw0 : 0) * CIN;
+        const int vhi = (pcols < a.w - iw0 ? pcols : a.w - iw0) * CIN;
+#pragma unroll
+        for (int it = 0; it < PIT; ++it) {
+            const int e4 = tid + it * kThreads;
+            const int r = e4 / RW, wi = e4 - r * RW;
+            const int ih = ih0 + r;
+            const bool live = e4 < WORDS && r < prow && (unsigned)ih < (unsigned)a.h;
+            const int rel0 = 4 * wi - row_shift(ih, iw0);   // byte index of byte 0 from pixel iw0
+            const int64_t ga = ((int64_t)(nb * a.h + ih) * a.w + iw0) * CIN + rel0;
+            uint32_t word = pwd[it];
+            if (live && ga + 4 > in_bytes) {
+                word = 0;
+                for (int e = 0; e < 4 && ga + e < in_bytes; ++e)
+                    word |= (uint32_t)(uint8_t)a.xq[ga + e] << (8 * e);
+            }
+            const int lo = live ? min(max(vlo - rel0, 0), 4) : 4, hi = min(max(vhi - rel0, 0), 4);
+            const uint64_t keep = ((1ull << (8 * hi)) - 1) & ~((1ull << (8 * lo)) - 1);
+            if (e4 < WORDS) dst[e4] = word & (uint32_t)keep;
+        }
+    }
 };
 
 // Tiles per block (a run of one sample): at least kRowRunMin; the launch
@@ -1022,7 +1086,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rowrun_kernel(const ConvA
     constexpr int FM = TM / 16;
     constexpr int FN = BN / 16;
     using P = RowRunPatch<TH, TW, CIN>;
-    constexpr int RS = P::RS, RW = P::RW, PWORDS = P::WORDS, PIT = P::PIT;
+    constexpr int RS = P::RS, PWORDS = P::WORDS, PIT = P::PIT;
     constexpr int BIT = 2 * BN * 4 / kThreads;
     static_assert(TM % 16 == 0 && TW % 16 == 0 && BN % 64 == 0 && 2 * BN * 4 % kThreads == 0, "tile");
     static_assert(BN <= kThreads, "one column per thread");
@@ -1056,59 +1120,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rowrun_kernel(const ConvA
         return tl;
     };
 
-    const int prow = (TH - 1) * a.sa + a.k;   // patch rows in use
-    const int pcols = (TW - 1) * a.sa + a.k;  // patch columns in use
-    const int64_t in_bytes = (int64_t)a.n * a.h * a.w * CIN;
-    const __amdgpu_buffer_rsrc_t rx =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t *>(a.xq), (short)0, (int)in_bytes, 0x00020000);
-    // Patch row r of a tile holds the input bytes of row ih0 + r from the
-    // 4-aligned address at or below its first byte (pixel iw0), fetched as
-    // aligned dwords; the row's alignment shift is (first byte address) mod 4.
-    auto row_shift = [&](int ih, int iw0) -> int {
-        const uint32_t g = ((uint32_t)(nb * a.h + ih) * (uint32_t)a.w + (uint32_t)iw0) * (uint32_t)CIN;
-        return (int)(g & 3u);
-    };
-    // every load of a patch at once (no branches): rows outside the image use an
-    // out-of-range offset and read 0
-    auto patch_load = [&](const Tile &tl, uint32_t (&pwd)[PIT]) {
-        const int ih0 = tl.gi0 * a.sa + a.bah, iw0 = tl.gj0 * a.sa + a.baw;
-#pragma unroll
-        for (int it = 0; it < PIT; ++it) {
-            const int e4 = tid + it * kThreads;
-            const int r = e4 / RW, wi = e4 - r * RW;
-            const int ih = ih0 + r;
-            const bool live = e4 < PWORDS && r < prow && (unsigned)ih < (unsigned)a.h;
-            const int64_t ga = ((int64_t)(nb * a.h + ih) * a.w + iw0) * CIN + 4 * wi - row_shift(ih, iw0);
-            pwd[it] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rx, (int)(live ? (uint32_t)ga : 0xFFFFFFFFu),
-                                                                     0, 0);
-        }
-    };
-    // then the masks (bytes of columns inside both the patch and the image) and
-    // the LDS copy.  The range check drops the whole dword that straddles the end
-    // of the input; its bytes are read one by one.
-    auto patch_store = [&](const Tile &tl, uint32_t (&pwd)[PIT], uint32_t *dst) {
-        const int ih0 = tl.gi0 * a.sa + a.bah, iw0 = tl.gj0 * a.sa + a.baw;
-        const int vlo = (iw0 < 0 ? -iw0 : 0) * CIN;
-        const int vhi = (pcols < a.w - iw0 ? pcols : a.w - iw0) * CIN;
-#pragma unroll
-        for (int it = 0; it < PIT; ++it) {
-            const int e4 = tid + it * kThreads;
-            const int r = e4 / RW, wi = e4 - r * RW;
-            const int ih = ih0 + r;
-            const bool live = e4 < PWORDS && r < prow && (unsigned)ih < (unsigned)a.h;
-            const int rel0 = 4 * wi - row_shift(ih, iw0);   // byte index of byte 0 from pixel iw0
-            const int64_t ga = ((int64_t)(nb * a.h + ih) * a.w + iw0) * CIN + rel0;
-            uint32_t word = pwd[it];
-            if (live && ga + 4 > in_bytes) {
-                word = 0;
-                for (int e = 0; e < 4 && ga + e < in_bytes; ++e)
-                    word |= (uint32_t)(uint8_t)a.xq[ga + e] << (8 * e);
-            }
-            const int lo = live ? min(max(vlo - rel0, 0), 4) : 4, hi = min(max(vhi - rel0, 0), 4);
-            const uint64_t keep = ((1ull << (8 * hi)) - 1) & ~((1ull << (8 * lo)) - 1);
-            if (e4 < PWORDS) dst[e4] = word & (uint32_t)keep;
-        }
-    };
+    const P pp(a, nb);
 
     // ---- once per block: weight tile, column factors, first patch ----
     uint32_t pwd[PIT];
@@ -1123,7 +1135,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rowrun_kernel(const ConvA
                 wb[it] = *reinterpret_cast<const v4i *>(a.wp + ((int64_t)ks * a.cout_pad + n0 + (rem >> 2)) * 64 +
                                                         16 * (rem & 3));
         }
-        patch_load(tile_of(t_first), pwd);
+        pp.load(tile_of(t_first), pwd);
         float colv_t = 0.0f, colv_b = 0.0f;
         if (tid < BN) column_factor(a, tile_sx(a, nb), n0 + tid, colv_t, colv_b);
 #pragma unroll
@@ -1137,7 +1149,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rowrun_kernel(const ConvA
             s_col[tid] = colv_t;
             s_col[BN + tid] = colv_b;
         }
-        patch_store(tile_of(t_first), pwd, s_patch[0]);
+        pp.store(tile_of(t_first), pwd, s_patch[0]);
     }
     __syncthreads();
 
@@ -1145,7 +1157,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rowrun_kernel(const ConvA
     for (int it = 0; it < cnt; ++it) {
         const Tile tile = tile_of(t_first + it);
         const bool more = it + 1 < cnt;
-        if (more) patch_load(tile_of(t_first + it + 1), pwd);   // lands during this tile's work
+        if (more) pp.load(tile_of(t_first + it + 1), pwd);   // lands during this tile's work
         const uint32_t *patch = s_patch[it & 1];
         const int ih0 = tile.gi0 * a.sa + a.bah, iw0 = tile.gj0 * a.sa + a.baw;
         v4i acc[FM][FN];
@@ -1165,7 +1177,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rowrun_kernel(const ConvA
                     const int m = wave * TM + 16 * i + fr;
                     const int ohl = m / TW, owl = m - ohl * TW;
                     const int row = a.sa * ohl + kh;
-                    const int off = row * RS + a.sa * owl * CIN + b0 + row_shift(ih0 + row, iw0);
+                    const int off = row * RS + a.sa * owl * CIN + b0 + pp.row_shift(ih0 + row, iw0);
                     const uint32_t *pw = patch + (off >> 2);
                     const uint32_t sh = off & 3;
                     const uint32_t d0 = pw[0], d1 = pw[1], d2 = pw[2];
@@ -1190,7 +1202,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rowrun_kernel(const ConvA
                 const int m = wave * TM + 16 * i + fr;
                 const int ohl = m / TW, owl = m - ohl * TW;
                 const int row = a.sa * ohl + kh;
-                const int off = row * RS + a.sa * owl * CIN + row_shift(ih0 + row, iw0);
+                const int off = row * RS + a.sa * owl * CIN + pp.row_shift(ih0 + row, iw0);
                 const uint32_t *pw = patch + (off >> 2);
                 const uint32_t sh = off & 3;
                 const uint32_t d0 = pw[0], d1 = pw[1], d2 = pw[2], d3 = pw[3], d4 = pw[4];
@@ -1218,8 +1230,278 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rowrun_kernel(const ConvA
             epilogue_regs<TW, FM, FN, E>(*(const ConvArgs *)kargs, acc, tile, wave * TM, elane, s_col, s_col + BN);
         }
         // the other buffer was last read before the previous barrier
-        if (more) patch_store(tile_of(t_first + it + 1), pwd, s_patch[(it + 1) & 1]);
+        if (more) pp.store(tile_of(t_first + it + 1), pwd, s_patch[(it + 1) & 1]);
         __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// The small-cin layer's two passes with both Table I transforms, on 32 x 32
+// MFMA tiles: a WH layer with blocks of 64 whose output feeds a DH operand with
+// blocks of 64, 192 output channels.  PASS 0 forms the next operand's
+// per-sample max |B_next y| (no output); PASS 1 writes its codes with the scale
+// derived from that maximum.  The contraction is the row-run one (one 16-byte
+// run per kernel row) on v_mfma_i32_32x32x32_i8 with the weights as the first
+// operand: lane (j, h), j = lane % 32 and h = lane / 32, supplies kernel row
+// 2s + h of pixel j to MFMA s, and register r of 32-channel tile u holds
+// channel 32u + 8(r/4) + 4h + r%4 of pixel j.
+//
+// A 64-channel block of one pixel is then 32 registers, index rho = 16u + r,
+// of the lane pair (j, 0), (j, 1): channel bits 0, 1, 3, 4, 5 are bits 0-4 of
+// rho and channel bit 2 is h, so each 64-point transform has five stages in
+// registers and one across the lane halves (v_permlane32_swap).  That stage is
+// left unrestored: pairing registers that differ in bit m, it leaves the stage's
+// channel bit in register bit m and the lane half holding what bit m held.
+// The WH restore pairs them by bit 1 (channel bit 1, already done), which
+// leaves h = channel bit 1; the next transform's stage on channel bit 1 (now h)
+// pairs them by bit 0, which leaves h = channel bit 0 and rho = channel bits
+// 1-5: lane (j, h) ends with channels h + 2 rho of the block.  Both transforms
+// keep the ascending stage order and the (a, c) -> (a + c, a - c) roundings of
+// fwht_item, so the values are the ones the other kernels compute.
+// ---------------------------------------------------------------------------
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+// Butterfly across the lane halves on register pairs (rho, rho | M): after one
+// swap the lanes with h = 0 hold both halves of register rho and those with
+// h = 1 both halves of rho | M; a + c and a - c are formed in place.
+template <int M>
+__device__ __forceinline__ void half_stage(float (&v)[32]) {
+#pragma unroll
+    for (int r = 0; r < 32; ++r)
+        if (!(r & M)) pair_swap<32>(v[r], v[r | M]);
+#pragma unroll
+    for (int r = 0; r < 32; ++r) {
+        if (r & M) continue;
+        const float s = v[r] + v[r | M], d = v[r] - v[r | M];
+        v[r] = s;
+        v[r | M] = d;
+    }
+}
+
+// Output columns of a tile: one MFMA column set.
+constexpr int kRr32W = 32;
+
+template <int TH, int CIN, int NS, int PASS, int MINB>
+__global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArgs a) {
+    constexpr int TW = kRr32W, BN = 192, NBLK = BN / 64, RPW = TH / 4;
+    using P = RowRunPatch<TH, TW, CIN>;
+    constexpr int RS = P::RS, PWORDS = P::WORDS, PIT = P::PIT;
+    constexpr int WROWS = 2 * NS;   // kernel rows the MFMAs cover
+    static_assert(TH % 4 == 0 && NS >= 1 && NS <= 4, "tile");
+    __shared__ __attribute__((aligned(16))) int8_t s_w[WROWS * BN * 16];   // [kernel row][channel][16 B]
+    __shared__ uint32_t s_patch[2][PWORDS];
+    __shared__ __attribute__((aligned(16))) float s_col[2 * BN];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int j = lane & 31, h = lane >> 5;
+
+    // this block's run: sample nb, tiles t_first .. t_first+cnt-1 of the sample
+    const int per = a.tiles_h * a.tiles_w;
+    const int run = a.run_tiles;
+    const int runs = (per + run - 1) / run;
+    const int rn = xcd_logical_tile();
+    const int nb = rn / runs;
+    const int t_first = (rn - nb * runs) * run;
+    const int cnt = per - t_first < run ? per - t_first : run;
+    auto tile_of = [&](int t) {
+        Tile tl;
+        tl.nb = nb;
+        tl.n0 = 0;
+        const int th = t / a.tiles_w;
+        tl.gi0 = th * TH;
+        tl.gj0 = (t - th * a.tiles_w) * TW;
+        return tl;
+    };
+    const P pp(a, nb);
+
+    // PASS 1: the sample's scale as the activation quantizer derives it,
+    // published by the block whose run starts the sample
+    const float qs = PASS == 1 ? act_scale_from_absmax(a.q_absmax[nb]) : 1.0f;
+    const float qr = 1.0f / qs;
+    const bool q_fast = qs >= 0x1p-125f && qs <= 0x1p125f;
+    if (PASS == 1 && t_first == 0 && tid == 0) a.q_scale[nb] = qs;
+
+    // ---- once per block: weights, column factors, first patch ----
+    uint32_t pwd[PIT];
+    {
+        // kernel row kh of channel c: 16 bytes of K-step kh / 4 of the packed weights
+        constexpr int WIT = (WROWS * BN + kThreads - 1) / kThreads;
+        v4i wb[WIT];
+#pragma unroll
+        for (int it = 0; it < WIT; ++it) {
+            const int e = tid + it * kThreads;
+            const int kh = e / BN, c = e - kh * BN;
+            wb[it] = v4i{0, 0, 0, 0};
+            if (e < WROWS * BN && kh < 4 * a.nksteps)
+                wb[it] = *reinterpret_cast<const v4i *>(a.wp + ((int64_t)(kh >> 2) * a.cout_pad + c) * 64 +
+                                                        16 * (kh & 3));
+        }
+        pp.load(tile_of(t_first), pwd);
+        float colv_t = 0.0f, colv_b = 0.0f;
+        if (tid < BN) column_factor(a, tile_sx(a, nb), tid, colv_t, colv_b);
+#pragma unroll
+        for (int it = 0; it < WIT; ++it) {
+            const int e = tid + it * kThreads;
+            if (e < WROWS * BN) *reinterpret_cast<v4i *>(s_w + 16 * e) = wb[it];
+        }
+        if (tid < BN) {
+            s_col[tid] = colv_t;
+            s_col[BN + tid] = colv_b;
+        }
+        pp.store(tile_of(t_first), pwd, s_patch[0]);
+    }
+    __syncthreads();
+
+    // 16-byte code stores when every pixel's codes start 16-byte aligned
+    const bool a16 = PASS == 1 && ((reinterpret_cast<uintptr_t>(a.y) | (uintptr_t)a.cout) & 15) == 0;
+    float wave_m = 0.0f;
+    for (int it = 0; it < cnt; ++it) {
+        const Tile tile = tile_of(t_first + it);
+        const bool more = it + 1 < cnt;
+        if (more) pp.load(tile_of(t_first + it + 1), pwd);   // lands during this tile's work
+        const uint32_t *patch = s_patch[it & 1];
+        const int ih0 = tile.gi0 * a.sa + a.bah, iw0 = tile.gj0 * a.sa + a.baw;
+#pragma unroll 1
+        for (int rr = 0; rr < RPW; ++rr) {
+            const int ohl = wave + 4 * rr;   // the wave's output row in the tile
+            // pixel operand: kernel row 2s + h of pixel j, from the patch
+            v4i fb[NS];
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                const int row = a.sa * ohl + 2 * s + h;
+                const int off = row * RS + a.sa * j * CIN + pp.row_shift(ih0 + row, iw0);
+                const uint32_t *pw = patch + (off >> 2);
+                const uint32_t sh = off & 3;
+                const uint32_t d0 = pw[0], d1 = pw[1], d2 = pw[2], d3 = pw[3], d4 = pw[4];
+                fb[s] = v4i{(int)__builtin_amdgcn_alignbyte(d1, d0, sh), (int)__builtin_amdgcn_alignbyte(d2, d1, sh),
+                            (int)__builtin_amdgcn_alignbyte(d3, d2, sh), (int)__builtin_amdgcn_alignbyte(d4, d3, sh)};
+            }
+            const int gi = tile.gi0 + ohl, gj = tile.gj0 + j;
+            const bool valid = gi < a.gh && gj < a.gw;
+#pragma unroll 1
+            for (int k = 0; k < NBLK; ++k) {
+                v16i acc[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    acc[u] = v16i{};
+#pragma unroll
+                    for (int s = 0; s < NS; ++s) {
+                        const v4i fa =
+                            *reinterpret_cast<const v4i *>(s_w + ((2 * s + h) * BN + 64 * k + 32 * u + j) * 16);
+                        acc[u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa, fb[s], acc[u], 0, 0, 0);
+                    }
+                }
+                // dequantization (the factors carry 1/b), then the WH output
+                // restore B^T (z / b)
+                float v[32];
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+#pragma unroll
+                    for (int q4 = 0; q4 < 4; ++q4) {
+                        const int c0 = 64 * k + 32 * u + 8 * q4 + 4 * h;
+                        const float4 t4 = *reinterpret_cast<const float4 *>(s_col + c0);
+                        const float4 b4 = *reinterpret_cast<const float4 *>(s_col + BN + c0);
+                        const int r0 = 16 * u + 4 * q4;
+                        v[r0 + 0] = __builtin_fmaf((float)acc[u][4 * q4 + 0], t4.x, b4.x);
+                        v[r0 + 1] = __builtin_fmaf((float)acc[u][4 * q4 + 1], t4.y, b4.y);
+                        v[r0 + 2] = __builtin_fmaf((float)acc[u][4 * q4 + 2], t4.z, b4.z);
+                        v[r0 + 3] = __builtin_fmaf((float)acc[u][4 * q4 + 3], t4.w, b4.w);
+                    }
+                reg_stage<1>(v);
+                reg_stage<2>(v);
+                half_stage<2>(v);
+                reg_stage<4>(v);
+                reg_stage<8>(v);
+                reg_stage<16>(v);
+                // the next operand: B_next y (pixels outside the grid are not
+                // part of it: their maximum is dropped and their codes not stored)
+                reg_stage<1>(v);
+                half_stage<1>(v);
+                reg_stage<2>(v);
+                reg_stage<4>(v);
+                reg_stage<8>(v);
+                if constexpr (PASS == 0) {
+                    // last stage fused with the maximum: of a + c and a - c, the one
+                    // whose operands agree in sign has magnitude |a| + |c| and the
+                    // other is no larger; rounding is monotone, so
+                    // max(|fl(a + c)|, |fl(a - c)|) = fl(|a| + |c|)
+                    float mm = 0.0f;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(v[r]) + fabsf(v[r + 16]));
+                    wave_m = fmaxf(wave_m, valid ? mm : 0.0f);
+                } else {
+                    reg_stage<16>(v);
+                    // Codes rne(fl(v / s)) (the scale comes from the values' own
+                    // maximum, so |v / s| <= 127 (1 + 2^-23) and no clamp is
+                    // needed).  Fast path: u = fl(v r + MAGIC) rounds the exact
+                    // product v r to an integer k, and d = fl(v r - k) measures how
+                    // far it lies from k; |v r - v / s| <= 127 * 2^-24, so with
+                    // |d| <= 0.5 - 2^-15 the quotient fl(v / s) lies strictly
+                    // inside (k - 1/2, k + 1/2).  A lane with any value closer to a
+                    // half-integer (or a scale outside the fast path's range) takes
+                    // the IEEE quotient for all of them.
+                    uint32_t c[32];
+                    float dm = 0.0f;
+#pragma unroll
+                    for (int r = 0; r < 32; ++r) {
+                        const float uf = __builtin_fmaf(v[r], qr, HATQ_MAGIC);
+                        const float kf = uf - HATQ_MAGIC;
+                        dm = fmaxf(dm, fabsf(__builtin_fmaf(v[r], qr, -kf)));
+                        c[r] = __float_as_uint(uf);
+                    }
+                    if (!q_fast || dm > HATQ_NEAR_TIE) {
+#pragma unroll
+                        for (int r = 0; r < 32; ++r) c[r] = __float_as_uint(rintf(clamp127(v[r] / qs)) + HATQ_MAGIC);
+                    }
+                    // word w holds channels h + 8w + {0, 2, 4, 6}; one exchange
+                    // across the halves gives each lane the odd (h = 0) or even
+                    // (h = 1) channels it lacks, and a byte interleave the 32
+                    // channels 32h .. 32h + 31 in order
+                    uint32_t w[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) w[q] = pack_low_bytes(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const auto x = __builtin_amdgcn_permlane32_swap(w[q], w[4 + q], false, false);
+                        w[q] = x[0];
+                        w[4 + q] = x[1];
+                    }
+                    uint32_t o[8];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        o[2 * q] = __builtin_amdgcn_perm(w[4 + q], w[q], 0x05010400u);       // [e0, o0, e1, o1]
+                        o[2 * q + 1] = __builtin_amdgcn_perm(w[4 + q], w[q], 0x07030602u);   // [e2, o2, e3, o3]
+                    }
+                    if (valid) {
+                        int8_t *yq = reinterpret_cast<int8_t *>(a.y) +
+                                     out_pixel(a, nb, gi, gj) * a.cout + 64 * k + 32 * h;
+                        if (a16) {
+                            // streaming stores: the next layer's convolution reads the codes
+                            __builtin_nontemporal_store(v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]},
+                                                        reinterpret_cast<v4i *>(yq));
+                            __builtin_nontemporal_store(v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]},
+                                                        reinterpret_cast<v4i *>(yq + 16));
+                        } else {
+#pragma unroll
+                            for (int q = 0; q < 8; ++q) *reinterpret_cast<uint32_t *>(yq + 4 * q) = o[q];
+                        }
+                    }
+                }
+            }
+        }
+        // the other buffer was last read before the previous barrier
+        if (more) pp.store(tile_of(t_first + it + 1), pwd, s_patch[(it + 1) & 1]);
+        __syncthreads();
+    }
+    if constexpr (PASS == 0) {
+        // one atomic per wave and run (a run is one sample); the running maximum
+        // only grows, so a wave that does not exceed the published value skips it
+        const float m = wave_max(wave_m);
+        if (lane == 0 && m > __uint_as_float(__hip_atomic_load(reinterpret_cast<unsigned int *>(a.next_absmax + nb),
+                                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)))
+            atomic_max_nonneg(a.next_absmax + nb, m);
     }
 }
 
@@ -1418,6 +1700,49 @@ hipError_t launch_rowrun(const ConvArgs &a, hipStream_t st) {
     return hipGetLastError();
 }
 
+// The launch conv_rr32_kernel implements: 0 (absmax pass), 1 (codes), or -1.
+// Three input channels, 192 output channels, 5x5 or 6x6 kernels (kernel rows
+// 0-5 on three MFMAs), a WH layer with blocks of 64 and both transforms run
+// (no paired shortcut) into a next operand with blocks of 64.
+inline int rr32_pass(const ConvArgs &a) {
+    if (!a.rowrun || a.cin_p != 3 || a.cout != 192 || a.cout_pad != 192 || a.n_base != 0) return -1;
+    if (a.k < 5 || a.k > 6 || a.sa > 2 || a.nksteps != 2) return -1;
+    if (a.form != 1 || a.hblock != 64 || a.next_hblock != 64 || a.paired || a.zx != nullptr) return -1;
+    if (a.mode == 1 && a.y == nullptr && a.next_absmax != nullptr) return 0;
+    if (a.mode == 2 && a.q_absmax != nullptr) return 1;
+    return -1;
+}
+
+#ifndef HATQ_RR32_TH
+#define HATQ_RR32_TH 8
+#endif
+#ifndef HATQ_RR32_MINB
+#define HATQ_RR32_MINB 4
+#endif
+
+template <int TH, int NS, int PASS, int MINB>
+hipError_t launch_rr32(const ConvArgs &a, hipStream_t st) {
+    ConvArgs b = a;
+    const int64_t tiles = set_tiles(b, TH, kRr32W, 192);
+    if (tiles <= 0 || rr32_pass(b) != PASS) return hipErrorInvalidValue;
+    // every byte offset of the input fits the 32-bit buffer range
+    if ((int64_t)b.n * b.h * b.w * 3 >= ((int64_t)1 << 31) - 64) return hipErrorInvalidValue;
+    const int64_t per = (int64_t)b.tiles_h * b.tiles_w;
+    const int64_t slots = MINB * (int64_t)persistent_blocks();   // resident blocks (0 if unknown)
+    int64_t run = slots > 0 ? (b.n * per + slots - 1) / slots : kRowRunMin;
+    run = run < kRowRunMin ? kRowRunMin : run > kRowRunMax ? kRowRunMax : run;
+    b.run_tiles = (int32_t)run;
+    const int64_t blocks = (int64_t)b.n * ((per + run - 1) / run);
+    if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    conv_rr32_kernel<TH, 3, NS, PASS, MINB><<<(unsigned)blocks, kThreads, 0, st>>>(b);
+    return hipGetLastError();
+}
+
+}  // namespace
+// (defined in its own compilation of this file, below)
+hipError_t conv_part_rr32(const ConvArgs &a, int pass, hipStream_t st);
+namespace {
+
 // Tile of the 3-channel layer with 192 outputs (the RGB input layer): rows x
 // columns of output pixels per block and blocks per CU.
 #ifndef HATQ_RR_TH
@@ -1433,6 +1758,10 @@ hipError_t launch_rowrun(const ConvArgs &a, hipStream_t st) {
 template <int CS>
 hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
     if (a.cout_pad % 192 == 0) {
+        if constexpr (CS == 3) {
+            const int pass = rr32_pass(a);
+            if (pass >= 0) return conv_part_rr32(a, pass, st);
+        }
         if constexpr (CS == 3)
             return with_epilogue<Epi<64, 64, 1>, Epi<64, 64, 2>, Epi<64, 64, 4>, Epi<0, 64>, Epi<0, 1>, Epi<0, 0>,
                                  Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_KRON_EPILOGUES, HATQ_GENERIC_EPILOGUES>(
@@ -2408,6 +2737,12 @@ hipError_t conv_part_pipe_other(const ConvArgs &a, hipStream_t st) {
 #endif
 #if HATQ_PART(6)
 hipError_t conv_part_rowrun3(const ConvArgs &a, hipStream_t st) { return launch_rowrun_n<3>(a, st); }
+#endif
+#if HATQ_PART(13)
+hipError_t conv_part_rr32(const ConvArgs &a, int pass, hipStream_t st) {
+    return pass == 0 ? launch_rr32<HATQ_RR32_TH, 3, 0, HATQ_RR32_MINB>(a, st)
+                     : launch_rr32<HATQ_RR32_TH, 3, 1, HATQ_RR32_MINB>(a, st);
+}
 #endif
 #if HATQ_PART(7)
 hipError_t conv_part_rowrun_other(const ConvArgs &a, hipStream_t st) {

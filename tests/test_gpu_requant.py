@@ -192,3 +192,40 @@ def test_codes_into_4_byte_aligned_buffers(orc):
     assert y_off.data_ptr() % 16 == 4
     assert torch.equal(y_got, y_ref)
     assert torch.equal(ybuf[4 + y_ref.numel():], torch.zeros(28, dtype=torch.int8, device="cuda"))
+
+
+# The small-cin layer with 192 WH outputs into a next operand with blocks of 64
+# (the RGB input layer of the analysis transform): its two passes run on 32 x 32
+# MFMA tiles of 8 output rows x 32 columns.  Ragged tiles in both directions,
+# k = 6, stride 1, and many one-tile samples.
+SMALL_CIN = [
+    (3, 45, 141, 3, 192, 5, 2, 2, False, 0, "WH", 64),
+    (2, 30, 40, 3, 192, 6, 2, 2, False, 0, "WH", 64),
+    (1, 20, 70, 3, 192, 5, 1, 2, False, 0, "WH", 64),
+    (40, 9, 11, 3, 192, 5, 2, 2, False, 0, "WH", 64),
+]
+
+
+@pytest.mark.parametrize("c", SMALL_CIN, ids=[f"n{c[0]}-{c[1]}x{c[2]}-k{c[5]}s{c[6]}" for c in SMALL_CIN])
+def test_requant_small_cin_tiles(orc, c):
+    n, h, w, cin, cout, k, s, p, tr, op, form, hb = c
+    rng, wt, b, ref, layer = _layer(orc, c, 83)
+    x = synth.heavy_tailed_activations(rng, (n, h, w, cin))
+    r = orc.layer_forward(x, ref)
+    q_ref, s_ref = _oracle_next(orc, r, 64)
+    xq, sx = dev(r.xq), dev(r.sx)
+    nam = torch.full((n,), -1.0, device="cuda")
+    assert hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=64, next_absmax=nam,
+                               absmax_only=True) is None
+    yq, sq = hatq.hatq_conv_int8_requant(layer, xq, sx, 64, next_absmax=nam)
+    tol = _scale_tol(orc, r, ref, 64, s_ref, form)
+    assert np.all(np.abs(host(sq).astype(np.float64) - s_ref) <= tol), (host(sq), s_ref, tol)
+    assert_codes(host(yq), q_ref, exact=False, what="small-cin requant codes")
+    # the F32 output with its fused absmax, then the activation kernel: the same
+    # absmax, scale and codes bit for bit
+    nam2 = torch.full((n,), -1.0, device="cuda")
+    y = hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=64, next_absmax=nam2)
+    q2, s2 = hatq.hatq_fwht_quant_act(y, 64, absmax=nam2)
+    assert torch.equal(nam, nam2)
+    assert torch.equal(sq, s2)
+    assert torch.equal(yq, q2)
