@@ -454,6 +454,10 @@ __global__ void __launch_bounds__(kThreads) scalar_kernel(const float *__restric
 #ifndef HATQ_QUANT_GRID
 #define HATQ_QUANT_GRID 32768
 #endif
+// Blocks of the vector absmax kernels over the whole batch.
+#ifndef HATQ_ABSMAX_GRID
+#define HATQ_ABSMAX_GRID 2048
+#endif
 int grid_x(int64_t work_units, int per_block, int n, int total = HATQ_QUANT_GRID) {
     int64_t want = (work_units + per_block - 1) / per_block;
     int64_t cap = (total + n - 1) / n;
@@ -469,7 +473,7 @@ hipError_t launch_vector(const float *x, int n, int64_t E, const float *absmax_i
     const int64_t items = (E + I - 1) / I;
     const float *A = absmax_in;
     if (!A) {
-        dim3 grid(grid_x(items, kQuadsPerBlock, n, 2048), n);
+        dim3 grid(grid_x(items, kQuadsPerBlock, n, HATQ_ABSMAX_GRID), n);
         fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(ws_absmax), n, 0u);
         absmax_kernel<B><<<grid, kThreads, 0, st>>>(x, E, ws_absmax);
         A = ws_absmax;

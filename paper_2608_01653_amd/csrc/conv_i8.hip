@@ -1437,23 +1437,32 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
                     // maximum, so |v / s| <= 127 (1 + 2^-23) and no clamp is
                     // needed).  Fast path: u = fl(v r + MAGIC) rounds the exact
                     // product v r to an integer k, and d = fl(v r - k) measures how
-                    // far it lies from k; |v r - v / s| <= 127 * 2^-24, so with
-                    // |d| <= 0.5 - 2^-15 the quotient fl(v / s) lies strictly
-                    // inside (k - 1/2, k + 1/2).  A lane with any value closer to a
-                    // half-integer (or a scale outside the fast path's range) takes
-                    // the IEEE quotient for all of them.
+                    // far it lies from k.  With Q = v / s: |v r - Q| <= 127 * 2^-24
+                    // (7.6e-6, r = fl(1/s)), |d - (v r - k)| <= 2^-25, and fl(Q)
+                    // lies within half an ulp (<= 2^-18) of Q; so |d| <= 0.5 -
+                    // 2^-16 puts fl(Q) strictly inside (k - 1/2, k + 1/2), and
+                    // rne(fl(Q)) = k.  Values closer to a half-integer (or every
+                    // value, for a scale outside the fast path's range) take the
+                    // IEEE quotient, by groups of eight registers (one maximum of
+                    // |d| per group), so a wave divides only the groups in which
+                    // some lane needs it.
                     uint32_t c[32];
-                    float dm = 0.0f;
+                    float dm[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
                     for (int r = 0; r < 32; ++r) {
                         const float uf = __builtin_fmaf(v[r], qr, HATQ_MAGIC);
                         const float kf = uf - HATQ_MAGIC;
-                        dm = fmaxf(dm, fabsf(__builtin_fmaf(v[r], qr, -kf)));
+                        dm[r >> 3] = fmaxf(dm[r >> 3], fabsf(__builtin_fmaf(v[r], qr, -kf)));
                         c[r] = __float_as_uint(uf);
                     }
-                    if (!q_fast || dm > HATQ_NEAR_TIE) {
+                    constexpr float kTie = 0.5f - 0x1p-16f;
 #pragma unroll
-                        for (int r = 0; r < 32; ++r) c[r] = __float_as_uint(rintf(clamp127(v[r] / qs)) + HATQ_MAGIC);
+                    for (int g = 0; g < 4; ++g) {
+                        if (!q_fast || dm[g] > kTie) {
+#pragma unroll
+                            for (int r = 8 * g; r < 8 * g + 8; ++r)
+                                c[r] = __float_as_uint(rintf(clamp127(v[r] / qs)) + HATQ_MAGIC);
+                        }
                     }
                     // word w holds channels h + 8w + {0, 2, 4, 6}; one exchange
                     // across the halves gives each lane the odd (h = 0) or even
@@ -1714,7 +1723,7 @@ inline int rr32_pass(const ConvArgs &a) {
 }
 
 #ifndef HATQ_RR32_TH
-#define HATQ_RR32_TH 8
+#define HATQ_RR32_TH 16
 #endif
 #ifndef HATQ_RR32_MINB
 #define HATQ_RR32_MINB 4
