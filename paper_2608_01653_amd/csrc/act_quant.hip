@@ -445,18 +445,19 @@ __global__ void __launch_bounds__(kThreads) scalar_kernel(const float *__restric
 }
 
 // Blocks per sample: enough for the work, at most `total` over the whole batch.
-// The absmax kernels end in one same-address atomic per block, so they use a
-// smaller total (2048; 4096 and more measured slower) than the quantization
-// kernels (16384: 3 % faster than 8192 on 805 MB, no gain beyond).
 // Blocks of the quantization kernels over the whole batch (measured on the
 // 805 M-element layer-2-shaped tensor: 16384 -> 32768 blocks 801 -> 782 us;
 // 65536 no faster).
 #ifndef HATQ_QUANT_GRID
 #define HATQ_QUANT_GRID 32768
 #endif
-// Blocks of the vector absmax kernels over the whole batch.
+// The absmax kernels end in one same-address atomic per block (they serialize
+// per sample), so they use a much smaller total.  Two-pass quantization, all
+// else equal: 8192 / 4096 / 2048 / 1024 / 512 blocks 148 / 107 / 90 / 84 /
+// 81 us on 16 x 1024 x 1024 x 3 (no transform) and 1269 (2048) -> 1238 us
+// (512) on 16 x 512 x 512 x 192 (blocks of 64).
 #ifndef HATQ_ABSMAX_GRID
-#define HATQ_ABSMAX_GRID 2048
+#define HATQ_ABSMAX_GRID 512
 #endif
 int grid_x(int64_t work_units, int per_block, int n, int total = HATQ_QUANT_GRID) {
     int64_t want = (work_units + per_block - 1) / per_block;

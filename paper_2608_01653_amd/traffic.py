@@ -7,12 +7,13 @@ pass (FETCH_SIZE or WRITE_SIZE, in KiB per dispatch).  The two calibration
 passes profile ``bench.py --calibrate-copy`` (1 GiB device copies); the ratio of
 the known copy size to what each counter reads scales the bench's counters to
 bytes.  Launches are identified by their order within one step of the
-four-layer stack: layer 1 runs the row-run convolution (an absmax pass, then the
-requantizing pass that writes layer 2's codes), so the first window
+four-layer stack: layer 1 runs the small-cin convolution twice
+(``conv_rr32_kernel``: the absmax pass, then the requantizing pass that writes
+layer 2's codes; ``conv_rowrun_kernel`` in the paired leg), so the first window
 convolution with the F32 epilogue that also forms the next blocks-of-64 absmax
-(``Epi<0, 64, 0>``; the integer stack's layer 2 uses another variant) after a
-row-run launch is layer 2's convolution and the first ``quant_kernel<64>`` after
-it is layer 3's quantization.  The output JSON
+(``Epi<0, 64, 0>``; the integer stack's layer 2 uses another variant) after such
+a launch is layer 2's convolution and the first ``quant_kernel<64>`` after it is
+layer 3's quantization.  Layer 1's two passes are reported too.  The output JSON
 carries a hash of the kernel sources; bench.py reports the traffic only while
 the sources are unchanged.
 """
@@ -45,14 +46,18 @@ def copy_factor(d):
 
 
 def per_launch(d, factor):
-    """KiB counter -> bytes, median over the steps, for the layer-2 conv and the
-    layer-3 quantization."""
-    conv, quant = [], []
+    """KiB counter -> bytes, median over the steps, for layer 1's two passes, the
+    layer-2 conv and the layer-3 quantization."""
+    conv, quant, l1a, l1q = [], [], [], []
     want_q = want_c = False
     for r in rows(d):
         name = r["Kernel_Name"]
         v = float(r["Counter_Value"]) * factor * 1024
-        if "conv_rowrun_kernel" in name:
+        if "conv_rr32_kernel" in name:
+            # template arguments <TH, CIN, NS, PASS, MINB>: PASS 0 absmax, 1 codes
+            (l1a if name.split("<")[1].split(",")[3].strip() == "0" else l1q).append(v)
+            want_c = True
+        elif "conv_rowrun_kernel" in name:
             want_c = True
         elif "conv_halo5_kernel<192" in name and "Epi<0, 64, 0>" in name and want_c:
             conv.append(v)
@@ -61,8 +66,8 @@ def per_launch(d, factor):
         elif "quant_kernel<64>" in name and want_q:
             quant.append(v)
             want_q = False
-    return {"conv_l2": statistics.median(conv) if conv else None,
-            "quant_l3": statistics.median(quant) if quant else None}
+    med = lambda xs: statistics.median(xs) if xs else None
+    return {"conv_l2": med(conv), "quant_l3": med(quant), "absmax_pass_l1": med(l1a), "codes_pass_l1": med(l1q)}
 
 
 def main():
