@@ -1278,10 +1278,92 @@ __device__ __forceinline__ void half_stage(float (&v)[32]) {
     }
 }
 
+// Codes rne(fl(v / s)) of N values whose scale comes from their own maximum, so
+// |v / s| <= 127 (1 + 2^-23) and no clamp is needed.  Fast path: u = fl(v r +
+// MAGIC) rounds the exact product v r to an integer k, and d = fl(v r - k)
+// measures how far it lies from k.  With Q = v / s: |v r - Q| <= 127 * 2^-24
+// (7.6e-6, r = fl(1/s)), |d - (v r - k)| <= 2^-25, and fl(Q) lies within half an
+// ulp (<= 2^-18) of Q; so |d| <= 0.5 - 2^-16 puts fl(Q) strictly inside (k - 1/2,
+// k + 1/2), and rne(fl(Q)) = k.  Values closer to a half-integer (or every value,
+// for a scale outside the fast path's range) take the IEEE quotient, by groups
+// of eight (one maximum of |d| per group), so a wave divides only the groups in
+// which some lane needs it.  c[r] holds the code in its low byte.
+template <int N>
+__device__ __forceinline__ void rr32_codes(const float (&v)[N], float s, float r, bool fast_ok, uint32_t (&c)[N]) {
+    static_assert(N % 8 == 0, "groups of eight");
+    float dm[N / 8];
+#pragma unroll
+    for (int g = 0; g < N / 8; ++g) dm[g] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const float uf = __builtin_fmaf(v[i], r, HATQ_MAGIC);
+        const float kf = uf - HATQ_MAGIC;
+        dm[i >> 3] = fmaxf(dm[i >> 3], fabsf(__builtin_fmaf(v[i], r, -kf)));
+        c[i] = __float_as_uint(uf);
+    }
+    constexpr float kTie = 0.5f - 0x1p-16f;
+#pragma unroll
+    for (int g = 0; g < N / 8; ++g) {
+        if (!fast_ok || dm[g] > kTie) {
+#pragma unroll
+            for (int i = 8 * g; i < 8 * g + 8; ++i) c[i] = __float_as_uint(rintf(clamp127(v[i] / s)) + HATQ_MAGIC);
+        }
+    }
+}
+
+// The codes of 64-channel block k of grid point (nb, gi, gj) held by lane half h:
+// o[0..3] channels 64k + 16h .. +15, o[4..7] channels 64k + 32 + 16h .. +15, so
+// each store instruction writes 32 contiguous bytes per pixel (the two lanes of
+// the pixel side by side).  16-byte stores where every pixel's codes start
+// 16-byte aligned, else 4-byte ones.  NT: streaming stores (the next layer's
+// convolution reads the codes, not this kernel).  The codes pass with both
+// transforms measured 516 (streaming) against 532 us (plain); the paired pass,
+// which issues its stores four times as densely, 623 against 307 us.
+template <bool NT>
+__device__ __forceinline__ void rr32_store(const ConvArgs &a, int nb, int gi, int gj, int k, int h, bool a16,
+                                           const uint32_t (&o)[8]) {
+    int8_t *yq = reinterpret_cast<int8_t *>(a.y) + out_pixel(a, nb, gi, gj) * a.cout + 64 * k + 16 * h;
+    if (a16) {
+        const v4i lo = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]}, hi = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
+        if constexpr (NT) {
+            __builtin_nontemporal_store(lo, reinterpret_cast<v4i *>(yq));
+            __builtin_nontemporal_store(hi, reinterpret_cast<v4i *>(yq + 32));
+        } else {
+            *reinterpret_cast<v4i *>(yq) = lo;
+            *reinterpret_cast<v4i *>(yq + 32) = hi;
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            *reinterpret_cast<uint32_t *>(yq + 4 * q) = o[q];
+            *reinterpret_cast<uint32_t *>(yq + 32 + 4 * q) = o[4 + q];
+        }
+    }
+}
+
+// Word exchange across the lane halves on the pairs (0, 2), (1, 3), (4, 6),
+// (5, 7): the lanes with h = 0 then hold both halves' words 0, 1, 4, 5 (own in
+// the first of each pair), those with h = 1 both halves' words 2, 3, 6, 7 (own
+// in the second).
+__device__ __forceinline__ void rr32_exchange(uint32_t (&w)[8]) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        if (q & 2) continue;
+        const auto x = __builtin_amdgcn_permlane32_swap(w[q], w[q + 2], false, false);
+        w[q] = x[0];
+        w[q + 2] = x[1];
+    }
+}
+
 // Output columns of a tile: one MFMA column set.
 constexpr int kRr32W = 32;
 
-template <int TH, int CIN, int NS, int PASS, int MINB>
+// PAIRED (HATQ_PAIRED, the blocks equal): the next operand is z itself (B_next
+// B_Cout = b I), so neither transform runs: the factors carry no 1/b (times b,
+// exact), the maximum is max |z|, and the codes are those of z in the MFMA
+// layout, where one swap of words across the lane halves gives each lane 32
+// contiguous channels.
+template <int TH, int CIN, int NS, int PASS, bool PAIRED, int MINB>
 __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArgs a) {
     constexpr int TW = kRr32W, BN = 192, NBLK = BN / 64, RPW = TH / 4;
     using P = RowRunPatch<TH, TW, CIN>;
@@ -1341,6 +1423,11 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
         pp.load(tile_of(t_first), pwd);
         float colv_t = 0.0f, colv_b = 0.0f;
         if (tid < BN) column_factor(a, tile_sx(a, nb), tid, colv_t, colv_b);
+        if constexpr (PAIRED) {
+            // z = fma(acc, t b, b~_c / b * b): the factors without the 1/b (b = 64)
+            colv_t *= 64.0f;
+            colv_b *= 64.0f;
+        }
 #pragma unroll
         for (int it = 0; it < WIT; ++it) {
             const int e = tid + it * kThreads;
@@ -1393,6 +1480,38 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
                         acc[u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa, fb[s], acc[u], 0, 0, 0);
                     }
                 }
+                if constexpr (PASS == 1 && PAIRED) {
+                    // the codes of z, one 32-channel tile at a time (no stage
+                    // mixes the tiles; all 32 values at once spilled)
+                    uint32_t w[8];
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        float z[16];
+#pragma unroll
+                        for (int q4 = 0; q4 < 4; ++q4) {
+                            const int c0 = 64 * k + 32 * u + 8 * q4 + 4 * h;
+                            const float4 t4 = *reinterpret_cast<const float4 *>(s_col + c0);
+                            const float4 b4 = *reinterpret_cast<const float4 *>(s_col + BN + c0);
+                            z[4 * q4 + 0] = __builtin_fmaf((float)acc[u][4 * q4 + 0], t4.x, b4.x);
+                            z[4 * q4 + 1] = __builtin_fmaf((float)acc[u][4 * q4 + 1], t4.y, b4.y);
+                            z[4 * q4 + 2] = __builtin_fmaf((float)acc[u][4 * q4 + 2], t4.z, b4.z);
+                            z[4 * q4 + 3] = __builtin_fmaf((float)acc[u][4 * q4 + 3], t4.w, b4.w);
+                        }
+                        uint32_t c[16];
+                        rr32_codes<16>(z, qs, qr, q_fast, c);
+#pragma unroll
+                        for (int q4 = 0; q4 < 4; ++q4)
+                            w[4 * u + q4] = pack_low_bytes(c[4 * q4], c[4 * q4 + 1], c[4 * q4 + 2], c[4 * q4 + 3]);
+                    }
+                    // word 4u + q holds channels 32u + 8q + 4h .. +3; after the
+                    // exchange the pairs (0, 2), (1, 3), (4, 6), (5, 7) hold the
+                    // channels 32u + 16h + 8q' .. +7 in order
+                    rr32_exchange(w);
+                    if (valid)
+                        rr32_store<false>(a, nb, gi, gj, k, h, a16,
+                                          {w[0], w[2], w[1], w[3], w[4], w[6], w[5], w[7]});
+                    continue;
+                }
                 // dequantization (the factors carry 1/b), then the WH output
                 // restore B^T (z / b)
                 float v[32];
@@ -1409,20 +1528,27 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
                         v[r0 + 2] = __builtin_fmaf((float)acc[u][4 * q4 + 2], t4.z, b4.z);
                         v[r0 + 3] = __builtin_fmaf((float)acc[u][4 * q4 + 3], t4.w, b4.w);
                     }
-                reg_stage<1>(v);
-                reg_stage<2>(v);
-                half_stage<2>(v);
-                reg_stage<4>(v);
-                reg_stage<8>(v);
-                reg_stage<16>(v);
-                // the next operand: B_next y (pixels outside the grid are not
-                // part of it: their maximum is dropped and their codes not stored)
-                reg_stage<1>(v);
-                half_stage<1>(v);
-                reg_stage<2>(v);
-                reg_stage<4>(v);
-                reg_stage<8>(v);
-                if constexpr (PASS == 0) {
+                if constexpr (!PAIRED) {
+                    reg_stage<1>(v);
+                    reg_stage<2>(v);
+                    half_stage<2>(v);
+                    reg_stage<4>(v);
+                    reg_stage<8>(v);
+                    reg_stage<16>(v);
+                    // the next operand: B_next y (pixels outside the grid are not
+                    // part of it: their maximum is dropped and their codes not stored)
+                    reg_stage<1>(v);
+                    half_stage<1>(v);
+                    reg_stage<2>(v);
+                    reg_stage<4>(v);
+                    reg_stage<8>(v);
+                }
+                if constexpr (PASS == 0 && PAIRED) {
+                    float mm = 0.0f;
+#pragma unroll
+                    for (int r = 0; r < 32; ++r) mm = fmaxf(mm, fabsf(v[r]));
+                    wave_m = fmaxf(wave_m, valid ? mm : 0.0f);
+                } else if constexpr (PASS == 0) {
                     // last stage fused with the maximum: of a + c and a - c, the one
                     // whose operands agree in sign has magnitude |a| + |c| and the
                     // other is no larger; rounding is monotone, so
@@ -1432,71 +1558,26 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
                     for (int r = 0; r < 16; ++r) mm = fmaxf(mm, fabsf(v[r]) + fabsf(v[r + 16]));
                     wave_m = fmaxf(wave_m, valid ? mm : 0.0f);
                 } else {
-                    reg_stage<16>(v);
-                    // Codes rne(fl(v / s)) (the scale comes from the values' own
-                    // maximum, so |v / s| <= 127 (1 + 2^-23) and no clamp is
-                    // needed).  Fast path: u = fl(v r + MAGIC) rounds the exact
-                    // product v r to an integer k, and d = fl(v r - k) measures how
-                    // far it lies from k.  With Q = v / s: |v r - Q| <= 127 * 2^-24
-                    // (7.6e-6, r = fl(1/s)), |d - (v r - k)| <= 2^-25, and fl(Q)
-                    // lies within half an ulp (<= 2^-18) of Q; so |d| <= 0.5 -
-                    // 2^-16 puts fl(Q) strictly inside (k - 1/2, k + 1/2), and
-                    // rne(fl(Q)) = k.  Values closer to a half-integer (or every
-                    // value, for a scale outside the fast path's range) take the
-                    // IEEE quotient, by groups of eight registers (one maximum of
-                    // |d| per group), so a wave divides only the groups in which
-                    // some lane needs it.
+                    if constexpr (!PAIRED) reg_stage<16>(v);
                     uint32_t c[32];
-                    float dm[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-                    for (int r = 0; r < 32; ++r) {
-                        const float uf = __builtin_fmaf(v[r], qr, HATQ_MAGIC);
-                        const float kf = uf - HATQ_MAGIC;
-                        dm[r >> 3] = fmaxf(dm[r >> 3], fabsf(__builtin_fmaf(v[r], qr, -kf)));
-                        c[r] = __float_as_uint(uf);
-                    }
-                    constexpr float kTie = 0.5f - 0x1p-16f;
-#pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        if (!q_fast || dm[g] > kTie) {
-#pragma unroll
-                            for (int r = 8 * g; r < 8 * g + 8; ++r)
-                                c[r] = __float_as_uint(rintf(clamp127(v[r] / qs)) + HATQ_MAGIC);
-                        }
-                    }
-                    // word w holds channels h + 8w + {0, 2, 4, 6}; one exchange
-                    // across the halves gives each lane the odd (h = 0) or even
-                    // (h = 1) channels it lacks, and a byte interleave the 32
-                    // channels 32h .. 32h + 31 in order
+                    rr32_codes<32>(v, qs, qr, q_fast, c);
+                    // word w holds channels h + 8w + {0, 2, 4, 6}; after the
+                    // exchange each pair (0, 2), (1, 3), (4, 6), (5, 7) holds the
+                    // even and the odd channels of 8 consecutive ones, 16h + 8w'
+                    // (+ 32 for the last two pairs), and a byte interleave puts
+                    // them in order
                     uint32_t w[8];
 #pragma unroll
                     for (int q = 0; q < 8; ++q) w[q] = pack_low_bytes(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const auto x = __builtin_amdgcn_permlane32_swap(w[q], w[4 + q], false, false);
-                        w[q] = x[0];
-                        w[4 + q] = x[1];
-                    }
+                    rr32_exchange(w);
                     uint32_t o[8];
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        o[2 * q] = __builtin_amdgcn_perm(w[4 + q], w[q], 0x05010400u);       // [e0, o0, e1, o1]
-                        o[2 * q + 1] = __builtin_amdgcn_perm(w[4 + q], w[q], 0x07030602u);   // [e2, o2, e3, o3]
+                        const int e = q + (q & 2), d = e + 2;   // pairs (0, 2), (1, 3), (4, 6), (5, 7)
+                        o[2 * q] = __builtin_amdgcn_perm(w[d], w[e], 0x05010400u);       // [e0, o0, e1, o1]
+                        o[2 * q + 1] = __builtin_amdgcn_perm(w[d], w[e], 0x07030602u);   // [e2, o2, e3, o3]
                     }
-                    if (valid) {
-                        int8_t *yq = reinterpret_cast<int8_t *>(a.y) +
-                                     out_pixel(a, nb, gi, gj) * a.cout + 64 * k + 32 * h;
-                        if (a16) {
-                            // streaming stores: the next layer's convolution reads the codes
-                            __builtin_nontemporal_store(v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]},
-                                                        reinterpret_cast<v4i *>(yq));
-                            __builtin_nontemporal_store(v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]},
-                                                        reinterpret_cast<v4i *>(yq + 16));
-                        } else {
-#pragma unroll
-                            for (int q = 0; q < 8; ++q) *reinterpret_cast<uint32_t *>(yq + 4 * q) = o[q];
-                        }
-                    }
+                    if (valid) rr32_store<true>(a, nb, gi, gj, k, h, a16, o);
                 }
             }
         }
@@ -1711,12 +1792,12 @@ hipError_t launch_rowrun(const ConvArgs &a, hipStream_t st) {
 
 // The launch conv_rr32_kernel implements: 0 (absmax pass), 1 (codes), or -1.
 // Three input channels, 192 output channels, 5x5 or 6x6 kernels (kernel rows
-// 0-5 on three MFMAs), a WH layer with blocks of 64 and both transforms run
-// (no paired shortcut) into a next operand with blocks of 64.
+// 0-5 on three MFMAs), a WH layer with blocks of 64 into a next operand with
+// blocks of 64 (both transforms, or with HATQ_PAIRED neither).
 inline int rr32_pass(const ConvArgs &a) {
     if (!a.rowrun || a.cin_p != 3 || a.cout != 192 || a.cout_pad != 192 || a.n_base != 0) return -1;
     if (a.k < 5 || a.k > 6 || a.sa > 2 || a.nksteps != 2) return -1;
-    if (a.form != 1 || a.hblock != 64 || a.next_hblock != 64 || a.paired || a.zx != nullptr) return -1;
+    if (a.form != 1 || a.hblock != 64 || a.next_hblock != 64 || a.zx != nullptr) return -1;
     if (a.mode == 1 && a.y == nullptr && a.next_absmax != nullptr) return 0;
     if (a.mode == 2 && a.q_absmax != nullptr) return 1;
     return -1;
@@ -1729,11 +1810,11 @@ inline int rr32_pass(const ConvArgs &a) {
 #define HATQ_RR32_MINB 4
 #endif
 
-template <int TH, int NS, int PASS, int MINB>
+template <int TH, int NS, int PASS, bool PAIRED, int MINB>
 hipError_t launch_rr32(const ConvArgs &a, hipStream_t st) {
     ConvArgs b = a;
     const int64_t tiles = set_tiles(b, TH, kRr32W, 192);
-    if (tiles <= 0 || rr32_pass(b) != PASS) return hipErrorInvalidValue;
+    if (tiles <= 0 || rr32_pass(b) != PASS || (b.paired != 0) != PAIRED) return hipErrorInvalidValue;
     // every byte offset of the input fits the 32-bit buffer range
     if ((int64_t)b.n * b.h * b.w * 3 >= ((int64_t)1 << 31) - 64) return hipErrorInvalidValue;
     const int64_t per = (int64_t)b.tiles_h * b.tiles_w;
@@ -1743,7 +1824,7 @@ hipError_t launch_rr32(const ConvArgs &a, hipStream_t st) {
     b.run_tiles = (int32_t)run;
     const int64_t blocks = (int64_t)b.n * ((per + run - 1) / run);
     if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-    conv_rr32_kernel<TH, 3, NS, PASS, MINB><<<(unsigned)blocks, kThreads, 0, st>>>(b);
+    conv_rr32_kernel<TH, 3, NS, PASS, PAIRED, MINB><<<(unsigned)blocks, kThreads, 0, st>>>(b);
     return hipGetLastError();
 }
 
@@ -2749,8 +2830,11 @@ hipError_t conv_part_rowrun3(const ConvArgs &a, hipStream_t st) { return launch_
 #endif
 #if HATQ_PART(13)
 hipError_t conv_part_rr32(const ConvArgs &a, int pass, hipStream_t st) {
-    return pass == 0 ? launch_rr32<HATQ_RR32_TH, 3, 0, HATQ_RR32_MINB>(a, st)
-                     : launch_rr32<HATQ_RR32_TH, 3, 1, HATQ_RR32_MINB>(a, st);
+    if (a.paired)
+        return pass == 0 ? launch_rr32<HATQ_RR32_TH, 3, 0, true, HATQ_RR32_MINB>(a, st)
+                         : launch_rr32<HATQ_RR32_TH, 3, 1, true, HATQ_RR32_MINB>(a, st);
+    return pass == 0 ? launch_rr32<HATQ_RR32_TH, 3, 0, false, HATQ_RR32_MINB>(a, st)
+                     : launch_rr32<HATQ_RR32_TH, 3, 1, false, HATQ_RR32_MINB>(a, st);
 }
 #endif
 #if HATQ_PART(7)

@@ -229,3 +229,15 @@ def test_requant_small_cin_tiles(orc, c):
     assert torch.equal(nam, nam2)
     assert torch.equal(sq, s2)
     assert torch.equal(yq, q2)
+    # HATQ_PAIRED: the next operand is z itself (no transform): scale and codes
+    # bit for bit against the oracle's z, and within the code rule against its
+    # composition
+    namp = torch.full((n,), -1.0, device="cuda")
+    hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=64, next_absmax=namp, absmax_only=True,
+                        paired=True)
+    yqp, sqp = hatq.hatq_conv_int8_requant(layer, xq, sx, 64, next_absmax=namp, paired=True)
+    qz, sz = orc.quantize_symmetric(orc.wh_z(r.acc, r.sx, ref)[..., :cout])
+    assert np.array_equal(host(sqp), sz)
+    assert_codes(host(yqp), qz, exact=True, what="paired small-cin codes")
+    assert np.all(np.abs(host(sqp).astype(np.float64) - s_ref) <= tol)
+    assert_codes(host(yqp), q_ref, what="paired small-cin codes vs the oracle's composition")
