@@ -389,7 +389,7 @@ def measure_integer_stack(st, x0, args, total_ops, img_pix):
         for i in range(nL - 1):
             m(f"conv_l{i + 1}_int_transition")
             hatq.hatq_conv_int8_int_transition(st.layers[i], st.xq[i], st.act_hb[i + 1], tables[i],
-                                               yq=st.xq[i + 1], paired=paired)
+                                               yq=st.xq[i + 1], paired=paired, yq_c64=st.c64[i + 1])
         m(f"conv_l{nL}_f32")
         hatq.hatq_conv_int8(st.layers[-1], st.xq[-1], s_last, hatq.HATQ_OUT_F32, y=y_last)
         m("end")
@@ -452,8 +452,9 @@ def measure_act_quant_l2_input(st, y1, am):
     from paper_2608_01653_amd import hatq
     hb = st.act_hb[1]
     e = y1.numel()
-    t1 = back_to_back(lambda: hatq.hatq_fwht_quant_act(y1, hb, absmax=am, xq=st.xq[1], scale=st.sc[1], ws=st.ws))
-    t2 = back_to_back(lambda: hatq.hatq_fwht_quant_act(y1, hb, xq=st.xq[1], scale=st.sc[1], ws=st.ws))
+    q1 = st.nhwc_buf(1)
+    t1 = back_to_back(lambda: hatq.hatq_fwht_quant_act(y1, hb, absmax=am, xq=q1, scale=st.sc[1], ws=st.ws))
+    t2 = back_to_back(lambda: hatq.hatq_fwht_quant_act(y1, hb, xq=q1, scale=st.sc[1], ws=st.ws))
     alg = e * 5
     log(f"layer-2 input quantization: {t1:.1f} us single read, {t2:.1f} us two-pass")
     return {"tensor": list(y1.shape), "elements": e, "algorithmic_bytes": alg,
@@ -513,9 +514,10 @@ def measure_affine_layer(st, per_layer, li=2, reps=20):
     ws = torch.empty(int(hatq.load().hatq_fwht_quant_affine_ws_bytes(n)), dtype=torch.int8, device=st.dev)
     tapsum = hatq.hatq_weight_tapsums(st.layers[li], device=st.dev)
     hb = st.act_hb[li]
-    tq = back_to_back(lambda: hatq.hatq_fwht_quant_act_affine(x, hb, xq=st.xq[li], scale=scale, zero=zero, ws=ws),
+    q = st.nhwc_buf(li)
+    tq = back_to_back(lambda: hatq.hatq_fwht_quant_act_affine(x, hb, xq=q, scale=scale, zero=zero, ws=ws),
                       reps)
-    tc = back_to_back(lambda: hatq.hatq_conv_int8_affine(st.layers[li], st.xq[li], scale, zero, tapsum,
+    tc = back_to_back(lambda: hatq.hatq_conv_int8_affine(st.layers[li], q, scale, zero, tapsum,
                                                          hatq.HATQ_OUT_F32, y=st.ys[li]), reps)
     ops = workloads.conv_ops(st.wl, li)
     z = zero.cpu().tolist()
@@ -544,8 +546,9 @@ def measure_order_layer(st, params, per_layer, li=2, reps=20):
     layer = hatq.hatq_prepare_weights(hatq.desc(L.cin, L.cout, L.k, L.stride, L.pad, m, L.transposed, L.out_pad),
                                       "DH", torch.from_numpy(w).to(st.dev), torch.from_numpy(b).to(st.dev))
     x = st.ys[li - 1]
-    tq = back_to_back(lambda: hatq.hatq_fwht_quant_act(x, m, xq=st.xq[li], scale=st.sc[li], ws=st.ws), reps)
-    tc = back_to_back(lambda: hatq.hatq_conv_int8(layer, st.xq[li], st.sc[li], hatq.HATQ_OUT_F32, y=st.ys[li]),
+    q = st.nhwc_buf(li)
+    tq = back_to_back(lambda: hatq.hatq_fwht_quant_act(x, m, xq=q, scale=st.sc[li], ws=st.ws), reps)
+    tc = back_to_back(lambda: hatq.hatq_conv_int8(layer, q, st.sc[li], hatq.HATQ_OUT_F32, y=st.ys[li]),
                       reps)
     log(f"order-{m} layer {li + 1}: quant {tq:.1f} us, conv {tc:.1f} us")
     return {"layer": per_layer[li]["layer"], "order": m, "construction": "P_12 (x) H~_16 (Paley-I q = 11)",

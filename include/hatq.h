@@ -80,7 +80,19 @@ typedef enum {
  *     Without the flag both transforms run explicitly (the general Table I
  *     transition, which a nonlinearity between the layers needs).  Ignored for
  *     every other layer and output. */
-typedef enum { HATQ_PAIRED = 1 } hatq_conv_flags;
+/*   HATQ_XQ_C64: the input codes xq are in the chunk-major layout
+ *     [n][cin_pad/64][h][w][64] (64-channel planes) instead of [n][h][w][cin_pad],
+ *     as hatq_fwht_quant_act_c64 and HATQ_YQ_C64 write them.  Same codes, same
+ *     results; the window refills of the 5x5 stride-2 kernel then read whole
+ *     128-byte lines (Eq. linear_operator: the contraction is unchanged, only
+ *     where each code sits).  Supported for regular (not transposed) 5x5 stride-2
+ *     layers with cin_pad % 64 == 0 and cout_pad 192 or 320; HATQ_EUNSUPPORTED
+ *     otherwise.
+ *   HATQ_YQ_C64: code outputs (HATQ_OUT_I8, hatq_conv_int8_requant,
+ *     hatq_conv_int8_int_transition) go out chunk-major,
+ *     [n][cout/64][ho][wo][64]; needs cout % 64 == 0 (HATQ_EUNSUPPORTED
+ *     otherwise), HATQ_EINVAL for F32 and I32 outputs. */
+typedef enum { HATQ_PAIRED = 1, HATQ_XQ_C64 = 2, HATQ_YQ_C64 = 4 } hatq_conv_flags;
 
 /* One layer's geometry.  Square kernels only.
  *   conv:        ho = (h + 2*pad - k)/stride + 1
@@ -198,6 +210,15 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
                             int32_t hblock, const float *absmax, int8_t *xq, float *act_scale,
                             void *ws, size_t ws_bytes, void *stream);
 
+/* hatq_fwht_quant_act with the codes in the chunk-major layout of HATQ_XQ_C64:
+ *   xq: device int8 [n][c/64][h][w][64], 16-byte aligned; the code of channel
+ *       64m + j of pixel p at ((i*(c/64) + m)*h*w + p)*64 + j for sample i.
+ * Same codes and scales as hatq_fwht_quant_act.  Supported: c % 64 == 0 and
+ * hblock a power of two at most 64 (HATQ_EUNSUPPORTED otherwise). */
+int32_t hatq_fwht_quant_act_c64(const float *x, int32_t n, int32_t h, int32_t w, int32_t c,
+                                int32_t hblock, const float *absmax, int8_t *xq, float *act_scale,
+                                void *ws, size_t ws_bytes, void *stream);
+
 /* hatq_fwht_quant_act without a workspace, for callers that cannot allocate
  * device memory (code under HIP graph capture, tight serving loops, harnesses
  * that forbid allocation): the two-pass form (absmax, then codes) keeps the
@@ -237,7 +258,7 @@ int32_t hatq_fwht_quant_act_noalloc(const float *x, int32_t n, int32_t h, int32_
  *     hatq_conv_int8_requant's dynamic scale).  With HATQ_PAIRED (see above)
  *     a WH layer whose block equals next_hblock takes max |z| instead.
  *   next_hblock (I8 mode): the next operand's transform block.
- *   flags:     0 or HATQ_PAIRED.
+ *   flags:     HATQ_PAIRED, HATQ_XQ_C64, HATQ_YQ_C64 (I8 mode only), or 0.
  * Supported: cin_pad % 64 == 0 with k <= 8, or cin_pad <= 4 with k*k*cin_pad <= 128;
  * cout_pad % 64 == 0; WH block and next_hblock a power of two at most 64, or
  * the Kronecker order 192 (P_12 (x) H~_16, applied as H~_16 then the Paley
@@ -265,8 +286,9 @@ int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act
  *     scale is then s = fl32(next_absmax / 127) (1 if it is 0) and is written to
  *     next_scale.  NULL: next_scale [n] is an input, a static scale.
  *   next_scale: device fp32 [n], the next layer's act_scale.
- *   yq:        device int8 [n][ho][wo][cout], the next layer's xq.
- *   flags:     0 or HATQ_PAIRED.
+ *   yq:        device int8 [n][ho][wo][cout], the next layer's xq (with
+ *              HATQ_YQ_C64: [n][cout/64][ho][wo][64]).
+ *   flags:     HATQ_PAIRED, HATQ_XQ_C64, HATQ_YQ_C64, or 0.
  * Supported: as hatq_conv_int8, with cout % 4 == 0 and cout % next_hblock == 0. */
 int32_t hatq_conv_int8_requant(const hatq_weights *W, const int8_t *xq, const float *act_scale,
                                int32_t n, int32_t h, int32_t w, int32_t next_hblock,
@@ -346,8 +368,9 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
  *   with rne rounding exact halves to even; no act_scale (it is inside M).
  *   table: as written by hatq_int_transition_params for W and next_hblock.
  *   yq:    device int8 [n][ho][wo][cout], the next layer's codes.
- *   flags: 0 or HATQ_PAIRED (a WH layer whose block equals next_hblock then
- *          uses B_next B_Cout = b I: bit-identical codes, no butterflies).
+ *   flags: HATQ_PAIRED (a WH layer whose block equals next_hblock then uses
+ *          B_next B_Cout = b I: bit-identical codes, no butterflies),
+ *          HATQ_XQ_C64, HATQ_YQ_C64, or 0.
  *   Supported: as hatq_conv_int8_requant. */
 size_t hatq_int_table_len(const hatq_weights *W);
 int32_t hatq_int_transition_params(const hatq_weights *W, float s_x, float s_y, int32_t next_hblock,

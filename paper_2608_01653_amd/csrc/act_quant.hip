@@ -99,9 +99,13 @@ struct QuantUnroll {
 };
 
 // Quantize one transformed item (s = act scale, r = fl(1/s)) and store its codes.
+// cc > 0: codes in the chunk-major layout of a sample of cc channels (items of
+// 64 channels, cc % 64 == 0): the item of pixel p, channels 64m .. 64m + 63, goes
+// to ((m * (E / cc)) + p) * 64.
 template <int B>
 __device__ __forceinline__ void quant_store_item(const float (&vin)[4 * ItemShape<B>::R], int8_t *qs, int64_t base,
-                                                 int64_t E, int t, float s, float r, bool fast_ok, float sigma) {
+                                                 int64_t E, int t, float s, float r, bool fast_ok, float sigma,
+                                                 int cc) {
     constexpr int R = ItemShape<B>::R;
     constexpr int I = ItemShape<B>::I;
     static_assert(R % 4 == 0, "groups of four words");
@@ -147,6 +151,10 @@ __device__ __forceinline__ void quant_store_item(const float (&vin)[4 * ItemShap
 #pragma unroll
             for (int i = 0; i < 4; ++i) w[i] = ((t ^ i) & 2) ? x[i] : w[i];
             int8_t *dst = qs + base + 64 * g + 16 * t;
+            if (I == 64 && cc > 0) {
+                const int64_t p = base / cc;
+                dst = qs + (((base - p * cc) >> 6) * (E / cc) + p) * 64 + 16 * t;
+            }
             // (xq need only be 4-byte aligned and a sample's E only a multiple
             // of 4; base is a multiple of 64, so the sample's start decides,
             // uniformly for the block)
@@ -174,7 +182,7 @@ template <int B>
 __global__ void __launch_bounds__(kThreads) quant_kernel(const float *__restrict__ x, int64_t E,
                                                          const float *__restrict__ absmax,
                                                          int8_t *__restrict__ xq,
-                                                         float *__restrict__ act_scale) {
+                                                         float *__restrict__ act_scale, int cc) {
     constexpr int I = ItemShape<B>::I;
     constexpr int R = ItemShape<B>::R;
     constexpr int UN = QuantUnroll<B>::UN;
@@ -203,7 +211,7 @@ __global__ void __launch_bounds__(kThreads) quant_kernel(const float *__restrict
             const int64_t it = it0 + u * kQuadsPerBlock;
             if (it >= items) break;
             const float sigma = fwht_item<B>(v[u], t);
-            quant_store_item<B>(v[u], qs, it * I, E, t, s, r, fast_ok, sigma);
+            quant_store_item<B>(v[u], qs, it * I, E, t, s, r, fast_ok, sigma, cc);
         }
     }
 }
@@ -469,7 +477,7 @@ int grid_x(int64_t work_units, int per_block, int n, int total = HATQ_QUANT_GRID
 
 template <int B>
 hipError_t launch_vector(const float *x, int n, int64_t E, const float *absmax_in, float *ws_absmax,
-                         int8_t *xq, float *act_scale, hipStream_t st) {
+                         int8_t *xq, float *act_scale, hipStream_t st, int c64 = 0) {
     constexpr int I = ItemShape<B>::I;
     const int64_t items = (E + I - 1) / I;
     const float *A = absmax_in;
@@ -480,7 +488,7 @@ hipError_t launch_vector(const float *x, int n, int64_t E, const float *absmax_i
         A = ws_absmax;
     }
     dim3 grid(grid_x(items, kQuadsPerBlock * QuantUnroll<B>::UN, n), n);
-    quant_kernel<B><<<grid, kThreads, 0, st>>>(x, E, A, xq, act_scale);
+    quant_kernel<B><<<grid, kThreads, 0, st>>>(x, E, A, xq, act_scale, c64);
     return hipGetLastError();
 }
 
@@ -606,7 +614,21 @@ hipError_t launch_act_quant_noalloc(const float *x, int n, int64_t E, int hblock
 }
 
 hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,
-                            float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st) {
+                            float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st, int c64) {
+    if (c64 > 0) {
+        // items of 64 channels, one chunk each
+        if (c64 % 64 != 0 || E % c64 != 0) return hipErrorInvalidValue;
+        switch (hblock) {
+            case 1: return launch_vector<1>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st, c64);
+            case 2: return launch_vector<2>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st, c64);
+            case 4: return launch_vector<4>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st, c64);
+            case 8: return launch_vector<8>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st, c64);
+            case 16: return launch_vector<16>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st, c64);
+            case 32: return launch_vector<32>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st, c64);
+            case 64: return launch_vector<64>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st, c64);
+            default: return hipErrorInvalidValue;
+        }
+    }
     if (E % 4 != 0) {
         if (hblock == 1) return launch_scalar<1>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);
         return launch_scalar<2>(x, n, E, absmax_in, ws_absmax, xq, act_scale, st);

@@ -130,6 +130,20 @@ int32_t check_weights(const hatq_weights *W) {
     return HATQ_OK;
 }
 
+// The chunk-major layouts: HATQ_XQ_C64 for the 5x5 stride-2 window kernel,
+// HATQ_YQ_C64 for code outputs with whole 64-channel planes.
+constexpr int32_t kConvFlags = HATQ_PAIRED | HATQ_XQ_C64 | HATQ_YQ_C64;
+int32_t check_layouts(const hatq_weights *W, int32_t flags, bool codes_out) {
+    const hatq_conv_desc &d = W->d;
+    if ((flags & HATQ_YQ_C64) && !codes_out) return HATQ_EINVAL;
+    if ((flags & HATQ_YQ_C64) && d.cout % 64 != 0) return HATQ_EUNSUPPORTED;
+    if ((flags & HATQ_XQ_C64) &&
+        (d.transposed || d.k != 5 || d.stride != 2 || W->cin_pad % 64 != 0 ||
+         (W->cout_pad != 192 && W->cout_pad != 320)))
+        return HATQ_EUNSUPPORTED;
+    return HATQ_OK;
+}
+
 int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next_absmax) {
     if (!next_absmax) return HATQ_OK;
     if (!supported_order(next_hblock)) return HATQ_EINVAL;
@@ -195,6 +209,8 @@ int32_t conv_launches(const hatq_weights *W, const int8_t *xq, const float *sx, 
     a.hblock = d.hblock;
     a.next_hblock = (next_absmax || mode >= HATQ_OUT_I8) ? next_hblock : 0;
     a.paired = (flags & HATQ_PAIRED) ? 1 : 0;
+    a.xq_c64 = (flags & HATQ_XQ_C64) ? 1 : 0;
+    a.yq_c64 = (flags & HATQ_YQ_C64) ? 1 : 0;
     const bool small = W->cin_pad <= 4 && W->k_total <= 128;
     if (!d.transposed) {
         a.gh = ho;
@@ -377,6 +393,24 @@ int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int
                                              act_scale, static_cast<hipStream_t>(stream)));
 }
 
+int32_t hatq_fwht_quant_act_c64(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
+                                const float *absmax, int8_t *xq, float *act_scale, void *ws, size_t ws_bytes,
+                                void *stream) {
+    if (!x || !xq || !act_scale || n <= 0 || h <= 0 || w <= 0 || c <= 0) return HATQ_EINVAL;
+    if (!supported_order(hblock)) return HATQ_EINVAL;
+    if (c % 64 != 0 || hblock > 64 || (hblock & (hblock - 1)) != 0) return HATQ_EUNSUPPORTED;
+    if (!aligned(x, 16) || !aligned(xq, 16) || !aligned(act_scale, 4)) return HATQ_EINVAL;
+    if (absmax && !aligned(absmax, 4)) return HATQ_EINVAL;
+    if (elems(n, h, w, c) < 0) return HATQ_EINVAL;
+    if (!absmax) {
+        if (!ws) return HATQ_EINVAL;
+        if (ws_bytes < hatq_fwht_quant_ws_bytes(n) || !aligned(ws, 4)) return HATQ_EWORKSPACE;
+    }
+    const int64_t E = (int64_t)h * w * c;
+    return hip_status(hatq::launch_act_quant(x, n, E, hblock, absmax, static_cast<float *>(ws), xq, act_scale,
+                                             static_cast<hipStream_t>(stream), c));
+}
+
 int32_t hatq_fwht_quant_act_noalloc(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
                                     int8_t *xq, float *act_scale, void *stream) {
     static_assert(HATQ_NOALLOC_MAX_SAMPLES == hatq::kNoAllocMaxSamples, "one limit");
@@ -400,11 +434,13 @@ int32_t requant(const hatq_weights *W, const int8_t *xq, const float *act_scale,
     int32_t s = check_weights(W);
     if (s != HATQ_OK) return s;
     if (!xq || !act_scale || !next_scale || !yq || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
-    if (flags & ~HATQ_PAIRED) return HATQ_EINVAL;
-    if (!aligned(xq, 16) || !aligned(yq, 4) || !aligned(act_scale, 4) || !aligned(next_scale, 4))
+    if (flags & ~kConvFlags) return HATQ_EINVAL;
+    if (!aligned(xq, 16) || !aligned(yq, (flags & HATQ_YQ_C64) ? 16 : 4) || !aligned(act_scale, 4) ||
+        !aligned(next_scale, 4))
         return HATQ_EINVAL;
     if (next_absmax && !aligned(next_absmax, 4)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    if ((s = check_layouts(W, flags, true)) != HATQ_OK) return s;
     // the transform and the code layout follow the next operand's blocks
     const float *probe = next_absmax ? next_absmax : next_scale;
     if ((s = check_next(W, next_hblock, probe)) != HATQ_OK) return s;
@@ -423,7 +459,7 @@ int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act
     int32_t s = check_weights(W);
     if (s != HATQ_OK) return s;
     if (!xq || !act_scale || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
-    if (flags & ~HATQ_PAIRED) return HATQ_EINVAL;
+    if (flags & ~kConvFlags) return HATQ_EINVAL;
     if (out_mode == HATQ_OUT_I8) {
         // requantization with a static per-sample scale (read, never written)
         if (!out_scale || !y || next_absmax) return HATQ_EINVAL;
@@ -437,6 +473,7 @@ int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act
     if (!y && !(out_mode == HATQ_OUT_F32 && next_absmax)) return HATQ_EINVAL;
     if (!aligned(xq, 16) || (y && !aligned(y, 16)) || !aligned(act_scale, 4)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    if ((s = check_layouts(W, flags, false)) != HATQ_OK) return s;
     if ((s = check_next(W, next_hblock, next_absmax)) != HATQ_OK) return s;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
@@ -541,9 +578,10 @@ int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, i
     int32_t s = check_weights(W);
     if (s != HATQ_OK) return s;
     if (!xq || !table || !yq || n <= 0 || h <= 0 || w <= 0) return HATQ_EINVAL;
-    if (flags & ~HATQ_PAIRED) return HATQ_EINVAL;
-    if (!aligned(xq, 16) || !aligned(yq, 4) || !aligned(table, 16)) return HATQ_EINVAL;
+    if (flags & ~kConvFlags) return HATQ_EINVAL;
+    if (!aligned(xq, 16) || !aligned(yq, (flags & HATQ_YQ_C64) ? 16 : 4) || !aligned(table, 16)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    if ((s = check_layouts(W, flags, true)) != HATQ_OK) return s;
     if ((s = check_next(W, next_hblock, reinterpret_cast<const float *>(table))) != HATQ_OK) return s;
     if (W->d.cout % 4) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;

@@ -644,7 +644,14 @@ struct Epilogue {
         swap16(w[2], w[3]);
         if (!valid[i]) return;
         const int m = row0 + 16 * i + p;
-        int8_t *yq = reinterpret_cast<int8_t *>(a.y) + out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW) * a.cout + t.n0;
+        const int64_t pix = out_pixel(a, t.nb, t.gi0 + m / TW, t.gj0 + m % TW);
+        int8_t *yq = reinterpret_cast<int8_t *>(a.y) + pix * a.cout + t.n0;
+        if (a.yq_c64) {
+            // chunk-major: block k of the tile is the plane (n0 + 64 k) / 64 of its sample
+            const int64_t hw = (int64_t)a.ho * a.wo;
+            yq = reinterpret_cast<int8_t *>(a.y) + ((int64_t)t.nb * (a.cout - 64) + t.n0 + 64 * k) * hw +
+                 pix * 64 - 64 * k;
+        }
         const int cl = 64 * k + 16 * q;
         // (the caller's buffer need only be 4-byte aligned: 16-byte writes when
         // every pixel's codes start 16-byte aligned, a launch-wide condition)
@@ -1322,7 +1329,11 @@ __device__ __forceinline__ void rr32_codes(const float (&v)[N], float s, float r
 template <bool NT>
 __device__ __forceinline__ void rr32_store(const ConvArgs &a, int nb, int gi, int gj, int k, int h, bool a16,
                                            const uint32_t (&o)[8]) {
-    int8_t *yq = reinterpret_cast<int8_t *>(a.y) + out_pixel(a, nb, gi, gj) * a.cout + 64 * k + 16 * h;
+    const int64_t pix = out_pixel(a, nb, gi, gj);
+    int8_t *yq = reinterpret_cast<int8_t *>(a.y) + pix * a.cout + 64 * k + 16 * h;
+    if (a.yq_c64)   // chunk-major: the plane of block k
+        yq = reinterpret_cast<int8_t *>(a.y) + ((int64_t)nb * (a.cout - 64) + 64 * k) * ((int64_t)a.ho * a.wo) +
+             pix * 64 + 16 * h;
     if (a16) {
         const v4i lo = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]}, hi = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
         if constexpr (NT) {
@@ -2440,18 +2451,24 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
             const int ih = ih0 + row, iw = iw0 + col;
             const bool in = f < G::RECS && row < rows_used && col < cols_used && (unsigned)ih < (unsigned)a.h &&
                             (unsigned)iw < (unsigned)a.w;
-            o[j] = in ? (uint32_t)(((t.nb * a.h + ih) * a.w + iw) * cin_p + 16 * g) : kOobOffset;
+            // NHWC: 64 bytes of chunk c at pixel * cin_p + 64 c; chunk-major: a
+            // plane of h * w * 64 bytes per chunk (whole 128-byte lines per refill)
+            const uint32_t pix = (uint32_t)((t.nb * a.h + ih) * a.w + iw);
+            const uint32_t off = a.xq_c64 ? (uint32_t)(t.nb * (cin_p - 64) * a.h * a.w) + pix * 64u : pix * (uint32_t)cin_p;
+            o[j] = in ? off + 16u * g : kOobOffset;
         }
     };
     uint32_t h_off[2][HB];
     window_offsets(tile, 0, h_off[0]);
     window_offsets(tile, 1, h_off[1]);
+    const uint32_t chunk_stride = a.xq_c64 ? (uint32_t)(a.h * a.w * 64) : 64u;
     // refill of window half hp from the offsets o with chunk c; zero_fill: the
     // same number of DMAs reading zeros
     auto burst_from = [&](int hp, const uint32_t(&o)[HB], int chunk) {
         int8_t *dst = halo + hp * G::HALF_BYTES;
 #pragma unroll
-        for (int j = 0; j < HB; ++j) dma16s(rx, dst + 1024 * halo_block(wave, j, W_BLK), o[j], (uint32_t)chunk * 64u);
+        for (int j = 0; j < HB; ++j)
+            dma16s(rx, dst + 1024 * halo_block(wave, j, W_BLK), o[j], (uint32_t)chunk * chunk_stride);
     };
     auto burst = [&](int hp, int chunk) { burst_from(hp, h_off[hp], chunk); };
     auto zero_fill = [&](int hp) {

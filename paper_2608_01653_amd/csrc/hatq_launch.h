@@ -8,8 +8,10 @@ namespace hatq {
 
 // Activation transform + quantization of n samples of E floats each.
 // absmax_in == nullptr: two passes through ws_absmax (n floats of scratch).
+// c64 > 0: the codes go out in the chunk-major layout of a sample of c64
+// channels ([E / c64 pixels] per 64-channel plane; c64 % 64 == 0, hblock <= 64).
 hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,
-                            float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st);
+                            float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st, int c64 = 0);
 
 // The same two-pass quantization with the per-sample absmax in the library's
 // static device scratch (no caller workspace, no allocation): n <= kNoAllocMaxSamples.
@@ -71,6 +73,8 @@ struct ConvArgs {
     int32_t paired;        // 1: a WH layer with next_hblock == hblock takes the next operand
                            // as z (B_next B_Cout = b I with identity nonlinearity); 0: both
                            // transforms run
+    int32_t xq_c64;        // 1: xq in the chunk-major layout [n][cin_p/64][h][w][64]
+    int32_t yq_c64;        // 1: code outputs in the chunk-major layout [n][cout/64][ho][wo][64]
     int32_t tiles_h, tiles_w, tiles_n;   // 2-D tiles of grid points per sample; column tiles
     int32_t n_base;        // first output column of a launch over a column range, else 0
     int32_t run_tiles;     // row-run kernel: tiles per block (set at launch)

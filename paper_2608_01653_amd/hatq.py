@@ -21,7 +21,7 @@ from . import build as _build
 HATQ_OK, HATQ_EINVAL, HATQ_EUNSUPPORTED, HATQ_EWORKSPACE, HATQ_EHIP = range(5)
 HATQ_DH, HATQ_WH = 0, 1
 HATQ_OUT_I32, HATQ_OUT_F32, HATQ_OUT_I8 = 0, 1, 2
-HATQ_PAIRED = 1
+HATQ_PAIRED, HATQ_XQ_C64, HATQ_YQ_C64 = 1, 2, 4
 FORMS = {"DH": HATQ_DH, "WH": HATQ_WH}
 
 
@@ -47,7 +47,7 @@ class Weights(ctypes.Structure):
 
 EXPORTS = ["hatq_status_string", "hatq_conv_out_hw", "hatq_weights_bytes", "hatq_prepare_weights",
            "hatq_export_weights", "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act",
-           "hatq_fwht_quant_act_noalloc", "hatq_conv_int8",
+           "hatq_fwht_quant_act_noalloc", "hatq_fwht_quant_act_c64", "hatq_conv_int8",
            "hatq_conv_int8_requant", "hatq_int_table_len", "hatq_int_transition_params",
            "hatq_conv_int8_int_transition", "hatq_range_expansion", "hatq_select_form",
            "hatq_fwht_quant_affine_ws_bytes", "hatq_fwht_quant_act_affine", "hatq_tapsum_len",
@@ -91,6 +91,8 @@ def load(build_if_missing: bool = False):
     L.hatq_fwht_quant_act.restype = i32
     L.hatq_fwht_quant_act_noalloc.argtypes = [P, i32, i32, i32, i32, i32, P, P, P]
     L.hatq_fwht_quant_act_noalloc.restype = i32
+    L.hatq_fwht_quant_act_c64.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P, sz, P]
+    L.hatq_fwht_quant_act_c64.restype = i32
     L.hatq_conv_int8.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, P, i32, P, i32, P]
     L.hatq_conv_int8.restype = i32
     L.hatq_conv_int8_requant.argtypes = [ctypes.POINTER(Weights), P, P, i32, i32, i32, i32, P, P, P, i32, P]
@@ -303,38 +305,91 @@ def hatq_fwht_quant_act_noalloc(x: torch.Tensor, hblock: int, xq: torch.Tensor, 
     return xq, scale
 
 
+def hatq_fwht_quant_act_c64(x: torch.Tensor, hblock: int, absmax: Optional[torch.Tensor] = None,
+                            xq: Optional[torch.Tensor] = None, scale: Optional[torch.Tensor] = None,
+                            ws: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """hatq_fwht_quant_act with the codes chunk-major: int8 [n, c/64, h, w, 64]."""
+    n, h, w, c = _nhwc(x, "x", torch.float32)
+    if c % 64:
+        raise HatqError(HATQ_EUNSUPPORTED, "hatq_fwht_quant_act_c64 (c % 64)")
+    if xq is None:
+        xq = torch.empty((n, c // 64, h, w, 64), dtype=torch.int8, device=x.device)
+    sc = scale if scale is not None else torch.empty(n, dtype=torch.float32, device=x.device)
+    _need(xq, "xq", torch.int8, x.numel())
+    _need(sc, "scale", torch.float32, n)
+    _need(absmax, "absmax", torch.float32, n, optional=True)
+    if ws is None:
+        ws = torch.empty(max(int(load().hatq_fwht_quant_ws_bytes(n)), 4), dtype=torch.int8, device=x.device)
+    _need(ws, "ws", torch.int8, 0)
+    _check(load().hatq_fwht_quant_act_c64(_ptr(x), n, h, w, c, int(hblock), _ptr(absmax), _ptr(xq), _ptr(sc),
+                                          _ptr(ws), ws.numel(), _stream(stream)), "hatq_fwht_quant_act_c64")
+    return xq, sc
+
+
+def to_c64(q: torch.Tensor) -> torch.Tensor:
+    """NHWC codes [n, h, w, c] -> chunk-major [n, c/64, h, w, 64] (a copy)."""
+    n, h, w, c = q.shape
+    return q.view(n, h, w, c // 64, 64).permute(0, 3, 1, 2, 4).contiguous()
+
+
+def from_c64(q: torch.Tensor) -> torch.Tensor:
+    """Chunk-major codes [n, c/64, h, w, 64] -> NHWC [n, h, w, c] (a copy)."""
+    n, m, h, w, _ = q.shape
+    return q.permute(0, 2, 3, 1, 4).reshape(n, h, w, m * 64).contiguous()
+
+
+def _codes_in(xq: torch.Tensor, cin_pad: int):
+    """(n, h, w, flag) of a layer's input codes: NHWC [n, h, w, cin_pad], or
+    chunk-major [n, cin_pad/64, h, w, 64] (HATQ_XQ_C64)."""
+    if xq.dim() == 5:
+        n, m, h, w, c64 = xq.shape
+        if m * 64 != cin_pad or c64 != 64:
+            raise ValueError(f"xq: chunk-major shape {tuple(xq.shape)} for cin_pad {cin_pad}")
+        _need(xq, "xq", torch.int8, n * h * w * cin_pad)
+        return n, h, w, HATQ_XQ_C64
+    n, h, w, _ = _nhwc(xq, "xq", torch.int8, cin_pad)
+    return n, h, w, 0
+
+
+def _codes_out_shape(n: int, ho: int, wo: int, c: int, c64: bool):
+    return (n, c // 64, ho, wo, 64) if c64 else (n, ho, wo, c)
+
+
 def _flags(paired: bool) -> int:
     return HATQ_PAIRED if paired else 0
 
 
 def hatq_conv_int8(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tensor, out_mode=HATQ_OUT_F32,
                    next_hblock: int = 0, next_absmax: Optional[torch.Tensor] = None, y=None, stream=None,
-                   absmax_only: bool = False, out_scale: Optional[torch.Tensor] = None, paired: bool = False):
+                   absmax_only: bool = False, out_scale: Optional[torch.Tensor] = None, paired: bool = False,
+                   yq_c64: bool = False):
     """absmax_only: F32 mode with y = NULL, producing next_absmax alone (returns None).
     out_mode HATQ_OUT_I8: y receives the next operand's codes with the static
-    per-sample scale out_scale.  paired: the HATQ_PAIRED flag."""
-    n, h, w, _ = _nhwc(xq, "xq", torch.int8, layer.w.cin_pad)
+    per-sample scale out_scale (chunk-major with yq_c64).  paired: the
+    HATQ_PAIRED flag.  A 5-d xq is chunk-major (HATQ_XQ_C64)."""
+    n, h, w, xf = _codes_in(xq, layer.w.cin_pad)
+    fl = _flags(paired) | xf | (HATQ_YQ_C64 if yq_c64 else 0)
     _need(act_scale, "act_scale", torch.float32, n)
     _need(next_absmax, "next_absmax", torch.float32, n, optional=True)
     _need(out_scale, "out_scale", torch.float32, n, optional=True)
     ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
     if absmax_only:
         _check(load().hatq_conv_int8(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), n, h, w, int(out_mode),
-                                     _ptr(out_scale), None, int(next_hblock), _ptr(next_absmax), _flags(paired),
+                                     _ptr(out_scale), None, int(next_hblock), _ptr(next_absmax), fl,
                                      _stream(stream)),
                "hatq_conv_int8")
         return None
     if out_mode == HATQ_OUT_I32:
         shape, dt = (n, ho, wo, layer.w.cout_pad), torch.int32
     elif out_mode == HATQ_OUT_I8:
-        shape, dt = (n, ho, wo, layer.w.d.cout), torch.int8
+        shape, dt = _codes_out_shape(n, ho, wo, layer.w.d.cout, yq_c64), torch.int8
     else:
         shape, dt = (n, ho, wo, layer.w.d.cout), torch.float32
     if y is None:
         y = torch.empty(shape, dtype=dt, device=xq.device)
-    _need(y, "y", dt, n * ho * wo * shape[3])
+    _need(y, "y", dt, n * ho * wo * (layer.w.cout_pad if out_mode == HATQ_OUT_I32 else layer.w.d.cout))
     _check(load().hatq_conv_int8(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), n, h, w, int(out_mode),
-                                 _ptr(out_scale), _ptr(y), int(next_hblock), _ptr(next_absmax), _flags(paired),
+                                 _ptr(out_scale), _ptr(y), int(next_hblock), _ptr(next_absmax), fl,
                                  _stream(stream)),
            "hatq_conv_int8")
     return y
@@ -342,21 +397,23 @@ def hatq_conv_int8(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tens
 
 def hatq_conv_int8_requant(layer: PreparedLayer, xq: torch.Tensor, act_scale: torch.Tensor, next_hblock: int,
                            next_absmax: Optional[torch.Tensor] = None, next_scale: Optional[torch.Tensor] = None,
-                           yq: Optional[torch.Tensor] = None, stream=None, paired: bool = False):
-    """Conv with the requantizing epilogue: returns (yq, next_scale), the next layer's codes and scale."""
-    n, h, w, _ = _nhwc(xq, "xq", torch.int8, layer.w.cin_pad)
+                           yq: Optional[torch.Tensor] = None, stream=None, paired: bool = False,
+                           yq_c64: bool = False):
+    """Conv with the requantizing epilogue: returns (yq, next_scale), the next
+    layer's codes (chunk-major with yq_c64) and scale.  A 5-d xq is chunk-major."""
+    n, h, w, xf = _codes_in(xq, layer.w.cin_pad)
     _need(act_scale, "act_scale", torch.float32, n)
     _need(next_absmax, "next_absmax", torch.float32, n, optional=True)
     ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
     if yq is None:
-        yq = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.int8, device=xq.device)
+        yq = torch.empty(_codes_out_shape(n, ho, wo, layer.w.d.cout, yq_c64), dtype=torch.int8, device=xq.device)
     if next_scale is None:
         next_scale = torch.empty((n,), dtype=torch.float32, device=xq.device)
     _need(yq, "yq", torch.int8, n * ho * wo * layer.w.d.cout)
     _need(next_scale, "next_scale", torch.float32, n)
     _check(load().hatq_conv_int8_requant(ctypes.byref(layer.w), _ptr(xq), _ptr(act_scale), n, h, w,
                                          int(next_hblock), _ptr(next_absmax), _ptr(next_scale), _ptr(yq),
-                                         _flags(paired), _stream(stream)),
+                                         _flags(paired) | xf | (HATQ_YQ_C64 if yq_c64 else 0), _stream(stream)),
            "hatq_conv_int8_requant")
     return yq, next_scale
 
@@ -383,16 +440,19 @@ def hatq_int_transition_params(layer: PreparedLayer, s_x: float, s_y: float, nex
 
 
 def hatq_conv_int8_int_transition(layer: PreparedLayer, xq: torch.Tensor, next_hblock: int, table: torch.Tensor,
-                                  yq: Optional[torch.Tensor] = None, stream=None, paired: bool = False) -> torch.Tensor:
-    """Conv with the integer-only epilogue: the next layer's codes."""
-    n, h, w, _ = _nhwc(xq, "xq", torch.int8, layer.w.cin_pad)
+                                  yq: Optional[torch.Tensor] = None, stream=None, paired: bool = False,
+                                  yq_c64: bool = False) -> torch.Tensor:
+    """Conv with the integer-only epilogue: the next layer's codes (chunk-major
+    with yq_c64).  A 5-d xq is chunk-major."""
+    n, h, w, xf = _codes_in(xq, layer.w.cin_pad)
     _need(table, "table", torch.int32, hatq_int_table_len(layer))
     ho, wo = hatq_conv_out_hw(layer.w.d, h, w)
     if yq is None:
-        yq = torch.empty((n, ho, wo, layer.w.d.cout), dtype=torch.int8, device=xq.device)
+        yq = torch.empty(_codes_out_shape(n, ho, wo, layer.w.d.cout, yq_c64), dtype=torch.int8, device=xq.device)
     _need(yq, "yq", torch.int8, n * ho * wo * layer.w.d.cout)
     _check(load().hatq_conv_int8_int_transition(ctypes.byref(layer.w), _ptr(xq), n, h, w, int(next_hblock),
-                                                _ptr(table), _ptr(yq), _flags(paired), _stream(stream)),
+                                                _ptr(table), _ptr(yq), _flags(paired) | xf |
+                                                (HATQ_YQ_C64 if yq_c64 else 0), _stream(stream)),
            "hatq_conv_int8_int_transition")
     return yq
 

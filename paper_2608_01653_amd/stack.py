@@ -16,6 +16,13 @@ Composition (identity nonlinearity between layers, fp32 between layers):
   * Every other layer writes fp32 and the next layer's per-sample absmax in its
     epilogue, so the next layer's quantization reads its input once.
 
+Code layout: with ``c64`` (the default) a layer's input codes are kept in the
+chunk-major layout [n][cin/64][h][w][64] (HATQ_XQ_C64) wherever the layer's
+convolution reads it (5x5 stride 2, cin a multiple of 64) and its producer
+writes it (the requantizing epilogue, HATQ_YQ_C64, or
+hatq_fwht_quant_act_c64): the same codes, placed so the convolution's input
+window refills read whole 128-byte lines.  ``codes(i)`` returns them NHWC.
+
 Every step of the path runs in the library's kernels; this module only
 allocates and sequences the calls.
 """
@@ -30,7 +37,7 @@ from . import hatq, workloads
 
 
 class Stack:
-    def __init__(self, wl: workloads.Workload, params, device="cuda:0"):
+    def __init__(self, wl: workloads.Workload, params, device="cuda:0", c64: bool = True):
         self.wl = wl
         self.dev = torch.device(device)
         self.shapes = wl.shapes()
@@ -45,9 +52,23 @@ class Stack:
         self.act_hb = [L.hblock if L.form == "DH" else 1 for L in wl.layers]
         # layer i writes layer i+1's codes (small-cin producer: the row-run path)
         self.requant = [i + 1 < self.nL and wl.layers[i].cin <= 4 for i in range(self.nL)]
+        # chunk-major input codes: read by the 5x5 stride-2 window kernel, written
+        # by the requantizing epilogue or the chunk-major quantizer
+        def c64_ok(i):
+            L = wl.layers[i]
+            pl = self.layers[i]
+            reads = (not L.transposed and L.k == 5 and L.stride == 2 and pl.cin_pad % 64 == 0
+                     and pl.cout_pad in (192, 320))
+            hb = self.act_hb[i]
+            writes = hb <= 64 and (hb & (hb - 1)) == 0 if not (i > 0 and self.requant[i - 1]) else True
+            return i > 0 and reads and writes
+        self.c64 = [c64 and c64_ok(i) for i in range(self.nL)]
         n = self.n
         self.xq, self.sc, self.amax, self.ys = [], [], [], []
         for i, (ishape, oshape) in enumerate(self.shapes):
+            if self.c64[i]:
+                nn, h, w, c = ishape
+                ishape = (nn, c // 64, h, w, 64)
             self.xq.append(torch.empty(ishape, dtype=torch.int8, device=self.dev))
             self.sc.append(torch.empty(n, dtype=torch.float32, device=self.dev))
             self.amax.append(torch.empty(n, dtype=torch.float32, device=self.dev))
@@ -74,8 +95,9 @@ class Stack:
         for i in range(self.nL):
             m(f"L{i + 1}.quant")
             if self.quant_passes(i):
-                hatq.hatq_fwht_quant_act(x, self.act_hb[i], absmax=None if i == 0 else self.amax[i - 1],
-                                         xq=self.xq[i], scale=self.sc[i], ws=self.ws)
+                quant = hatq.hatq_fwht_quant_act_c64 if self.c64[i] else hatq.hatq_fwht_quant_act
+                quant(x, self.act_hb[i], absmax=None if i == 0 else self.amax[i - 1], xq=self.xq[i],
+                      scale=self.sc[i], ws=self.ws)
             nxt = i + 1 < self.nL
             if self.requant[i]:
                 m(f"L{i + 1}.absmax")
@@ -85,7 +107,7 @@ class Stack:
                 m(f"L{i + 1}.requant")
                 hatq.hatq_conv_int8_requant(self.layers[i], self.xq[i], self.sc[i], self.act_hb[i + 1],
                                             next_absmax=self.amax[i], next_scale=self.sc[i + 1],
-                                            yq=self.xq[i + 1], paired=paired)
+                                            yq=self.xq[i + 1], paired=paired, yq_c64=self.c64[i + 1])
             else:
                 m(f"L{i + 1}.conv")
                 hatq.hatq_conv_int8(self.layers[i], self.xq[i], self.sc[i], hatq.HATQ_OUT_F32,
@@ -97,6 +119,15 @@ class Stack:
 
     def output(self) -> torch.Tensor:
         return self.ys[-1]
+
+    def nhwc_buf(self, i: int) -> torch.Tensor:
+        """Layer i's code buffer viewed NHWC (the same memory, for calls that
+        write and read it in that layout themselves)."""
+        return self.xq[i].view(self.shapes[i][0])
+
+    def codes(self, i: int) -> torch.Tensor:
+        """Layer i's input codes, NHWC (a copy when they are kept chunk-major)."""
+        return hatq.from_c64(self.xq[i]) if self.c64[i] else self.xq[i]
 
 
 def conv_bytes(st: Stack, i: int) -> int:

@@ -6,7 +6,7 @@
 
 namespace hatq {
 [[noreturn]] static void reached() { std::abort(); }
-hipError_t launch_act_quant(const float *, int, int64_t, int, const float *, float *, int8_t *, float *, hipStream_t) { reached(); }
+hipError_t launch_act_quant(const float *, int, int64_t, int, const float *, float *, int8_t *, float *, hipStream_t, int) { reached(); }
 hipError_t launch_act_quant_noalloc(const float *, int, int64_t, int, int8_t *, float *, hipStream_t) { reached(); }
 hipError_t launch_act_quant_affine(const float *, int, int64_t, int, float *, int8_t *, float *, int32_t *, hipStream_t) { reached(); }
 hipError_t launch_range_expansion(const float *, int, int64_t, int, int, float *, int32_t *, int32_t *, hipStream_t) { reached(); }

@@ -84,6 +84,17 @@ def test_prepare_rejects_before_launch(L):
              None) == hatq.HATQ_EINVAL    # dst not 256-aligned
 
 
+def test_fwht_quant_c64_rejects_before_launch(L):
+    f = L.hatq_fwht_quant_act_c64
+    assert f(None, 1, 4, 4, 64, 64, None, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EINVAL
+    assert f(FAKE, 1, 4, 4, 96, 32, None, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EUNSUPPORTED   # c % 64
+    assert f(FAKE, 1, 4, 4, 128, 128, None, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EUNSUPPORTED  # block 128
+    assert f(FAKE, 1, 4, 4, 192, 192, None, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EUNSUPPORTED  # Kronecker
+    assert f(FAKE, 1, 4, 4, 64, 64, None, ctypes.c_void_p(FAKE.value + 4), FAKE, FAKE, 256,
+             None) == hatq.HATQ_EINVAL                                                            # xq not 16-aligned
+    assert f(FAKE, 2, 4, 4, 64, 64, None, FAKE, FAKE, FAKE, 0, None) == hatq.HATQ_EWORKSPACE
+
+
 def test_fwht_quant_rejects_before_launch(L):
     f = L.hatq_fwht_quant_act
     assert f(None, 1, 4, 4, 64, 64, None, FAKE, FAKE, FAKE, 256, None) == hatq.HATQ_EINVAL
@@ -126,7 +137,15 @@ def test_conv_rejects_before_launch(L):
     assert c(None, 1, 8, 8, 1, FAKE, 0, None) == hatq.HATQ_EINVAL
     assert c(ctypes.byref(W), 1, 8, 8, 5, FAKE, 0, None) == hatq.HATQ_EINVAL
     assert c(ctypes.byref(W), 1, 8, 8, 0, FAKE, 64, FAKE) == hatq.HATQ_EINVAL          # I32 + absmax
-    assert c(ctypes.byref(W), 1, 8, 8, 1, FAKE, 0, None, flags=2) == hatq.HATQ_EINVAL  # unknown flag
+    assert c(ctypes.byref(W), 1, 8, 8, 1, FAKE, 0, None, flags=8) == hatq.HATQ_EINVAL  # unknown flag
+    # chunk-major codes: outputs only in code modes; input only for the 5x5 stride-2 window kernel
+    assert c(ctypes.byref(W), 1, 8, 8, 1, FAKE, 0, None, flags=hatq.HATQ_YQ_C64) == hatq.HATQ_EINVAL
+    W3 = _fake_weights(k=3, p=1)
+    assert c(ctypes.byref(W3), 1, 8, 8, 1, FAKE, 0, None, flags=hatq.HATQ_XQ_C64) == hatq.HATQ_EUNSUPPORTED
+    Wt = _fake_weights(transposed=1, out_pad=1)
+    assert c(ctypes.byref(Wt), 1, 8, 8, 1, FAKE, 0, None, flags=hatq.HATQ_XQ_C64) == hatq.HATQ_EUNSUPPORTED
+    W128 = _fake_weights(cout=128)
+    assert c(ctypes.byref(W128), 1, 8, 8, 1, FAKE, 0, None, flags=hatq.HATQ_XQ_C64) == hatq.HATQ_EUNSUPPORTED
     assert c(ctypes.byref(W), 1, 8, 8, 1, FAKE, 0, None, out_scale=FAKE) == hatq.HATQ_EINVAL   # scale outside I8
     bad = _fake_weights()
     bad.k_total += 1                                   # inconsistent view
@@ -163,7 +182,7 @@ def test_conv_i8_mode_needs_static_scale(L):
     assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, FAKE, FAKE, 128, None, 0, None) == hatq.HATQ_EUNSUPPORTED
     assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, ctypes.c_void_p(FAKE.value + 2), FAKE, 64, None, 0,
              None) == hatq.HATQ_EINVAL                                                   # misaligned scale
-    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, FAKE, FAKE, 64, None, 4, None) == hatq.HATQ_EINVAL
+    assert f(ctypes.byref(W), FAKE, FAKE, 1, 8, 8, I8, FAKE, FAKE, 64, None, 8, None) == hatq.HATQ_EINVAL
 
 
 def test_requant_rejects_before_launch(L):
@@ -180,6 +199,10 @@ def test_requant_rejects_before_launch(L):
     assert r(ctypes.byref(W), 1, 128, FAKE, FAKE, FAKE) == hatq.HATQ_EUNSUPPORTED
     assert r(ctypes.byref(W), 1, 64, ctypes.c_void_p(FAKE.value + 2), FAKE, FAKE) == hatq.HATQ_EINVAL  # misaligned
     assert r(ctypes.byref(W), 1, 64, FAKE, FAKE, FAKE, flags=8) == hatq.HATQ_EINVAL                   # unknown flag
+    W96 = _fake_weights(cout=96, hb=32)
+    assert r(ctypes.byref(W96), 1, 32, FAKE, FAKE, FAKE, flags=hatq.HATQ_YQ_C64) == hatq.HATQ_EUNSUPPORTED  # cout % 64
+    assert r(ctypes.byref(W), 1, 64, FAKE, FAKE, ctypes.c_void_p(FAKE.value + 4),
+             flags=hatq.HATQ_YQ_C64) == hatq.HATQ_EINVAL                                            # yq not 16-aligned
 
 
 def test_int_transition_rejects_before_launch(L):
@@ -205,7 +228,9 @@ def test_int_transition_rejects_before_launch(L):
     assert c(ctypes.byref(W), FAKE, 1, 8, 8, 128, FAKE, FAKE, 0, None) == hatq.HATQ_EUNSUPPORTED
     assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, ctypes.c_void_p(FAKE.value + 4), FAKE, 0, None) \
         == hatq.HATQ_EINVAL                                                                   # misaligned table
-    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, FAKE, FAKE, 2, None) == hatq.HATQ_EINVAL      # unknown flag
+    assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, FAKE, FAKE, 8, None) == hatq.HATQ_EINVAL      # unknown flag
+    W3 = _fake_weights(k=3, p=1)
+    assert c(ctypes.byref(W3), FAKE, 1, 8, 8, 64, FAKE, FAKE, hatq.HATQ_XQ_C64, None) == hatq.HATQ_EUNSUPPORTED
 
 
 def test_noalloc_rejects_before_launch(L):

@@ -68,10 +68,10 @@ def _check_sample(orc, st, refs, x0, s, paired):
     # layer 1 activation pass (WH: original domain)
     q_ref, s_ref = orc.quantize_symmetric(orc.activation_transform(x0[sl], st.act_hb[0]))
     assert np.array_equal(g(st.sc[0]), s_ref)
-    assert_codes(g(st.xq[0]), q_ref, exact=True, what=f"sample {s} layer 1 codes")
+    assert_codes(g(st.codes(0)), q_ref, exact=True, what=f"sample {s} layer 1 codes")
     for i in range(st.nL):
         pw = refs[i]
-        xq_i, sx_i = g(st.xq[i]), g(st.sc[i])
+        xq_i, sx_i = g(st.codes(i)), g(st.sc[i])
         acc = _conv(orc, xq_i, pw)
         y_ref = orc.epilogue(acc, sx_i, pw)
         if i + 1 == st.nL:
@@ -90,7 +90,7 @@ def _check_sample(orc, st, refs, x0, s, paired):
                 tol += max(nb, 1) * (dy + 2.0 ** -24 * np.abs(y_ref).max())
             s_tol = tol / 127 + 2 * np.spacing(np.float32(s_ref[0]))
             assert abs(float(g(st.sc[i + 1])[0]) - float(s_ref[0])) <= s_tol
-            assert_codes(g(st.xq[i + 1]), q_ref, what=f"sample {s} layer {i + 1} -> {i + 2} codes"
+            assert_codes(g(st.codes(i + 1)), q_ref, what=f"sample {s} layer {i + 1} -> {i + 2} codes"
                          + (" (paired)" if paired else ""))
             continue
         y_gpu = g(st.ys[i])
@@ -105,11 +105,11 @@ def _check_sample(orc, st, refs, x0, s, paired):
         q_ref, s_ref = orc.quantize_symmetric(S)
         if nb == 1:
             assert np.array_equal(g(st.sc[i + 1]), s_ref)
-            assert_codes(g(st.xq[i + 1]), q_ref, exact=True, what=f"sample {s} layer {i + 2} codes")
+            assert_codes(g(st.codes(i + 1)), q_ref, exact=True, what=f"sample {s} layer {i + 2} codes")
         else:
             s_tol = _butterfly_absmax_tol(y_gpu, nb) / 127 + 2 * np.spacing(np.float32(s_ref[0]))
             assert abs(float(g(st.sc[i + 1])[0]) - float(s_ref[0])) <= s_tol
-            assert_codes(g(st.xq[i + 1]), q_ref, what=f"sample {s} layer {i + 2} codes")
+            assert_codes(g(st.codes(i + 1)), q_ref, what=f"sample {s} layer {i + 2} codes")
 
 
 @pytest.mark.parametrize("name,samples", [("analysis_stack4_rgb_512x768", [0]),
@@ -126,7 +126,7 @@ def test_stack_step_teacher_forced(orc, name, samples, paired):
     for i in range(st.nL - 1):
         if not st.requant[i]:
             q1, s1 = hatq.hatq_fwht_quant_act(st.ys[i], st.act_hb[i + 1])
-            assert torch.equal(s1, st.sc[i + 1]) and torch.equal(q1, st.xq[i + 1])
+            assert torch.equal(s1, st.sc[i + 1]) and torch.equal(q1, st.codes(i + 1))
             del q1
     refs = _oracle_prepared(orc, wl, params)
     for s in samples:
