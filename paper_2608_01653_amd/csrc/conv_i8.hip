@@ -1318,22 +1318,17 @@ __device__ __forceinline__ void rr32_codes(const float (&v)[N], float s, float r
     }
 }
 
-// The codes of 64-channel block k of grid point (nb, gi, gj) held by lane half h:
-// o[0..3] channels 64k + 16h .. +15, o[4..7] channels 64k + 32 + 16h .. +15, so
-// each store instruction writes 32 contiguous bytes per pixel (the two lanes of
-// the pixel side by side).  16-byte stores where every pixel's codes start
-// 16-byte aligned, else 4-byte ones.  NT: streaming stores (the next layer's
-// convolution reads the codes, not this kernel).  The codes pass with both
-// transforms measured 516 (streaming) against 532 us (plain); the paired pass,
-// which issues its stores four times as densely, 623 against 307 us.
+// The codes of one 64-channel block of a grid point held by lane half h, from yq
+// = the address of the block's first code + 16h: o[0..3] channels 16h .. +15,
+// o[4..7] channels 32 + 16h .. +15, so each store instruction writes 32
+// contiguous bytes per pixel (the two lanes of the pixel side by side).  16-byte
+// stores where every pixel's codes start 16-byte aligned, else 4-byte ones.  NT:
+// streaming stores (the next layer's convolution reads the codes, not this
+// kernel).  The codes pass with both transforms measured 516 (streaming) against
+// 532 us (plain); the paired pass, which issues its stores four times as
+// densely, 623 against 307 us.
 template <bool NT>
-__device__ __forceinline__ void rr32_store(const ConvArgs &a, int nb, int gi, int gj, int k, int h, bool a16,
-                                           const uint32_t (&o)[8]) {
-    const int64_t pix = out_pixel(a, nb, gi, gj);
-    int8_t *yq = reinterpret_cast<int8_t *>(a.y) + pix * a.cout + 64 * k + 16 * h;
-    if (a.yq_c64)   // chunk-major: the plane of block k
-        yq = reinterpret_cast<int8_t *>(a.y) + ((int64_t)nb * (a.cout - 64) + 64 * k) * ((int64_t)a.ho * a.wo) +
-             pix * 64 + 16 * h;
+__device__ __forceinline__ void rr32_store(int8_t *yq, bool a16, const uint32_t (&o)[8]) {
     if (a16) {
         const v4i lo = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]}, hi = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
         if constexpr (NT) {
@@ -1363,6 +1358,34 @@ __device__ __forceinline__ void rr32_exchange(uint32_t (&w)[8]) {
         const auto x = __builtin_amdgcn_permlane32_swap(w[q], w[q + 2], false, false);
         w[q] = x[0];
         w[q + 2] = x[1];
+    }
+}
+
+// The same stages on int64 values (the integer transition): in registers, and
+// across the lane halves with both 32-bit words swapped.
+template <int STRIDE, int N>
+__device__ __forceinline__ void reg_stage_i64n(int64_t (&v)[N]) {
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        if (r & STRIDE) continue;
+        const int64_t x = v[r], y = v[r + STRIDE];
+        v[r] = x + y;
+        v[r + STRIDE] = x - y;
+    }
+}
+template <int M>
+__device__ __forceinline__ void half_stage_i64(int64_t (&v)[32]) {
+#pragma unroll
+    for (int r = 0; r < 32; ++r) {
+        if (r & M) continue;
+        uint32_t xl = (uint32_t)v[r], xh = (uint32_t)((uint64_t)v[r] >> 32);
+        uint32_t yl = (uint32_t)v[r | M], yh = (uint32_t)((uint64_t)v[r | M] >> 32);
+        const auto lo = __builtin_amdgcn_permlane32_swap(xl, yl, false, false);
+        const auto hi = __builtin_amdgcn_permlane32_swap(xh, yh, false, false);
+        const int64_t x = (int64_t)(((uint64_t)hi[0] << 32) | lo[0]);
+        const int64_t y = (int64_t)(((uint64_t)hi[1] << 32) | lo[1]);
+        v[r] = x + y;
+        v[r | M] = x - y;
     }
 }
 
@@ -1411,6 +1434,20 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
 
     // PASS 1: the sample's scale as the activation quantizer derives it,
     // published by the block whose run starts the sample
+    // PASS 2: the shared shift n of the table (in [0, 62]); PAIRED: B_next B_Cout
+    // = 64 I, so w = 64 p and the shift absorbs log2 64 (a left shift where n < 6)
+    int rq_n = 0, rq_pre = 0;
+    int64_t rq_bias = 0;
+    if constexpr (PASS == 2) {
+        int n = __builtin_amdgcn_readfirstlane(a.rq_table[2 * a.cout_pad]);
+        n = n < 0 ? 0 : (n > 62 ? 62 : n);
+        if constexpr (PAIRED) {
+            rq_pre = 6 > n ? 6 - n : 0;
+            n = 6 > n ? 0 : n - 6;
+        }
+        rq_n = n;
+        rq_bias = n ? ((int64_t)1 << (n - 1)) - 1 : 0;
+    }
     const float qs = PASS == 1 ? act_scale_from_absmax(a.q_absmax[nb]) : 1.0f;
     const float qr = 1.0f / qs;
     const bool q_fast = qs >= 0x1p-125f && qs <= 0x1p125f;
@@ -1434,7 +1471,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
         pp.load(tile_of(t_first), pwd);
         float colv_t = 0.0f, colv_b = 0.0f;
         if (tid < BN) column_factor(a, tile_sx(a, nb), tid, colv_t, colv_b);
-        if constexpr (PAIRED) {
+        if constexpr (PAIRED && PASS != 2) {
             // z = fma(acc, t b, b~_c / b * b): the factors without the 1/b (b = 64)
             colv_t *= 64.0f;
             colv_b *= 64.0f;
@@ -1453,7 +1490,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
     __syncthreads();
 
     // 16-byte code stores when every pixel's codes start 16-byte aligned
-    const bool a16 = PASS == 1 && ((reinterpret_cast<uintptr_t>(a.y) | (uintptr_t)a.cout) & 15) == 0;
+    const bool a16 = PASS >= 1 && ((reinterpret_cast<uintptr_t>(a.y) | (uintptr_t)a.cout) & 15) == 0;
     float wave_m = 0.0f;
     for (int it = 0; it < cnt; ++it) {
         const Tile tile = tile_of(t_first + it);
@@ -1478,6 +1515,15 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
             }
             const int gi = tile.gi0 + ohl, gj = tile.gj0 + j;
             const bool valid = gi < a.gh && gj < a.gw;
+            // codes of block k at ybase + k * kstride (NHWC, or the chunk-major plane of block k)
+            int8_t *ybase = nullptr;
+            int64_t kstride = 64;
+            if constexpr (PASS >= 1) {
+                const int64_t pix = out_pixel(a, nb, gi, gj), hw = (int64_t)a.ho * a.wo;
+                ybase = reinterpret_cast<int8_t *>(a.y) + 16 * h +
+                        (a.yq_c64 ? (int64_t)nb * (a.cout - 64) * hw + pix * 64 : pix * a.cout);
+                kstride = a.yq_c64 ? 64 * hw : 64;
+            }
 #pragma unroll 1
             for (int k = 0; k < NBLK; ++k) {
                 v16i acc[2];
@@ -1490,6 +1536,69 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
                             *reinterpret_cast<const v4i *>(s_w + ((2 * s + h) * BN + 64 * k + 32 * u + j) * 16);
                         acc[u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa, fb[s], acc[u], 0, 0, 0);
                     }
+                }
+                if constexpr (PASS == 2) {
+                    // The integer transition (Table I, integer form): p = M_c (acc +
+                    // b_int,c) in int64, the WH output transform, the next operand's
+                    // transform, codes clamp(rne(w / 2^n)).  Integer butterflies are
+                    // exact, so the stage order is free; the layout moves as in the
+                    // float passes.  PAIRED: w = 64 p, no transform.
+                    int64_t v[32];
+#pragma unroll
+                    for (int u = 0; u < 2; ++u)
+#pragma unroll
+                        for (int q4 = 0; q4 < 4; ++q4) {
+                            const int c0 = 64 * k + 32 * u + 8 * q4 + 4 * h;
+                            const v4i m4 = *reinterpret_cast<const v4i *>(s_col + c0);
+                            const v4i b4 = *reinterpret_cast<const v4i *>(s_col + BN + c0);
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                v[16 * u + 4 * q4 + e] = (int64_t)m4[e] * (int64_t)(acc[u][4 * q4 + e] + b4[e]);
+                        }
+                    if constexpr (PAIRED) {
+#pragma unroll
+                        for (int r = 0; r < 32; ++r) v[r] = (int64_t)((uint64_t)v[r] << rq_pre);
+                    } else {
+                        reg_stage_i64n<1>(v);
+                        reg_stage_i64n<2>(v);
+                        half_stage_i64<2>(v);
+                        reg_stage_i64n<4>(v);
+                        reg_stage_i64n<8>(v);
+                        reg_stage_i64n<16>(v);
+                        reg_stage_i64n<1>(v);
+                        half_stage_i64<1>(v);
+                        reg_stage_i64n<2>(v);
+                        reg_stage_i64n<4>(v);
+                        reg_stage_i64n<8>(v);
+                        reg_stage_i64n<16>(v);
+                    }
+                    uint32_t c[32];
+                    if (rq_n >= 32) {
+#pragma unroll
+                        for (int r = 0; r < 32; ++r) c[r] = int_code_hi(v[r], rq_n - 32, rq_bias);
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 32; ++r) c[r] = int_code(v[r], rq_n, rq_bias);
+                    }
+                    uint32_t w[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) w[q] = pack_low_bytes(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
+                    rr32_exchange(w);
+                    if constexpr (PAIRED) {
+                        if (valid)
+                            rr32_store<false>(ybase + k * kstride, a16,
+                                              {w[0], w[2], w[1], w[3], w[4], w[6], w[5], w[7]});
+                    } else {
+                        uint32_t o[8];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const int e = q + (q & 2), d = e + 2;
+                            o[2 * q] = __builtin_amdgcn_perm(w[d], w[e], 0x05010400u);
+                            o[2 * q + 1] = __builtin_amdgcn_perm(w[d], w[e], 0x07030602u);
+                        }
+                        if (valid) rr32_store<true>(ybase + k * kstride, a16, o);
+                    }
+                    continue;
                 }
                 if constexpr (PASS == 1 && PAIRED) {
                     // the codes of z, one 32-channel tile at a time (no stage
@@ -1519,7 +1628,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
                     // channels 32u + 16h + 8q' .. +7 in order
                     rr32_exchange(w);
                     if (valid)
-                        rr32_store<false>(a, nb, gi, gj, k, h, a16,
+                        rr32_store<false>(ybase + k * kstride, a16,
                                           {w[0], w[2], w[1], w[3], w[4], w[6], w[5], w[7]});
                     continue;
                 }
@@ -1588,7 +1697,7 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
                         o[2 * q] = __builtin_amdgcn_perm(w[d], w[e], 0x05010400u);       // [e0, o0, e1, o1]
                         o[2 * q + 1] = __builtin_amdgcn_perm(w[d], w[e], 0x07030602u);   // [e2, o2, e3, o3]
                     }
-                    if (valid) rr32_store<true>(a, nb, gi, gj, k, h, a16, o);
+                    if (valid) rr32_store<true>(ybase + k * kstride, a16, o);
                 }
             }
         }
@@ -1811,6 +1920,7 @@ inline int rr32_pass(const ConvArgs &a) {
     if (a.form != 1 || a.hblock != 64 || a.next_hblock != 64 || a.zx != nullptr) return -1;
     if (a.mode == 1 && a.y == nullptr && a.next_absmax != nullptr) return 0;
     if (a.mode == 2 && a.q_absmax != nullptr) return 1;
+    if (a.mode == kModeIntTransition) return 2;
     return -1;
 }
 
@@ -1819,6 +1929,11 @@ inline int rr32_pass(const ConvArgs &a) {
 #endif
 #ifndef HATQ_RR32_MINB
 #define HATQ_RR32_MINB 4
+#endif
+// the integer transition (int64 values: twice the registers; 159 VGPRs, three
+// blocks per CU)
+#ifndef HATQ_RR32_MINB_INT
+#define HATQ_RR32_MINB_INT 3
 #endif
 
 template <int TH, int NS, int PASS, bool PAIRED, int MINB>
@@ -2847,6 +2962,9 @@ hipError_t conv_part_rowrun3(const ConvArgs &a, hipStream_t st) { return launch_
 #endif
 #if HATQ_PART(13)
 hipError_t conv_part_rr32(const ConvArgs &a, int pass, hipStream_t st) {
+    if (pass == 2)
+        return a.paired ? launch_rr32<HATQ_RR32_TH, 3, 2, true, HATQ_RR32_MINB_INT>(a, st)
+                        : launch_rr32<HATQ_RR32_TH, 3, 2, false, HATQ_RR32_MINB_INT>(a, st);
     if (a.paired)
         return pass == 0 ? launch_rr32<HATQ_RR32_TH, 3, 0, true, HATQ_RR32_MINB>(a, st)
                          : launch_rr32<HATQ_RR32_TH, 3, 1, true, HATQ_RR32_MINB>(a, st);

@@ -154,3 +154,26 @@ def test_stack_b16_layer1_int_transition_full_size(orc):
         acc = orc.conv_int8(crop, ref.wq, stride=L.stride, pad=0)
         exp[i] = orc.int_transition(acc, ref, rq, nb)[0, 0, 0]
     assert_codes(got, exp, exact=True, what="batch-16 stack layer-1 integer transition vs oracle")
+
+
+@pytest.mark.parametrize("target", [None, 20, 3])
+@pytest.mark.parametrize("c", [(3, 45, 141, 3, 192, 5, 2, 2, False, 0, "WH", 64),
+                               (40, 9, 11, 3, 192, 5, 2, 2, False, 0, "WH", 64)], ids=["3x45x141", "40x9x11"])
+def test_int_transition_small_cin(orc, c, target):
+    """The small-cin layer with 192 WH outputs (the RGB input layer; its integer
+    transition runs on 32 x 32 MFMA tiles, int64 butterflies, ragged tiles): its
+    own shift, 20, and 3 (below log2 of the block: the paired form shifts left);
+    bit-exact against the oracle, paired and explicit, NHWC and chunk-major."""
+    ref, layer, xq, acc, s_x, s_y = _static_case(orc, c, 64, 94)
+    n1 = orc.int_requant_params(ref, s_x, s_y, 64).shift
+    shrink = 1.0 if target is None else 2.0 ** (n1 - target)
+    rq = orc.int_requant_params(ref, s_x, s_y / shrink, 64)
+    assert target is None or rq.shift == target
+    table, n_shift = hatq.hatq_int_transition_params(layer, s_x, s_y / shrink, 64)
+    assert n_shift == rq.shift
+    q_ref = orc.int_transition(acc, ref, rq, 64)
+    yq = hatq.hatq_conv_int8_int_transition(layer, dev(xq), 64, table)
+    assert_codes(host(yq), q_ref, exact=True, what=f"small-cin integer transition, shift {rq.shift}")
+    assert torch.equal(hatq.hatq_conv_int8_int_transition(layer, dev(xq), 64, table, paired=True), yq)
+    y64 = hatq.hatq_conv_int8_int_transition(layer, dev(xq), 64, table, yq_c64=True)
+    assert torch.equal(hatq.from_c64(y64), yq)
