@@ -86,7 +86,9 @@ typedef enum {
  *     results; the window refills of the 5x5 stride-2 kernel then read whole
  *     128-byte lines (Eq. linear_operator: the contraction is unchanged, only
  *     where each code sits).  Supported for regular (not transposed) 5x5 stride-2
- *     layers with cin_pad % 64 == 0 and cout_pad 192 or 320; HATQ_EUNSUPPORTED
+ *     layers with cin_pad % 64 == 0 and cout_pad 192 or 320, except a call
+ *     whose epilogue transforms by the order 320 (a WH restore of order 320 or
+ *     next_hblock 320 with a float or code output); HATQ_EUNSUPPORTED
  *     otherwise.
  *   HATQ_YQ_C64: code outputs (HATQ_OUT_I8, hatq_conv_int8_requant,
  *     hatq_conv_int8_int_transition) go out chunk-major,
@@ -108,7 +110,8 @@ typedef enum { HATQ_PAIRED = 1, HATQ_XQ_C64 = 2, HATQ_YQ_C64 = 4 } hatq_conv_fla
  * dequantization factor is fl(s_x s_w / b)), and by the activation-side
  * profiling and affine entry points (hatq_range_expansion,
  * hatq_fwht_quant_act_affine) for whole blocks (c % b == 0); the entry points
- * below that say so take 192 also for the convolution epilogues. */
+ * below that say so take them also for the convolution epilogues (192 with
+ * cout_pad 192, 320 with cout_pad 320 and cin_pad % 64 == 0). */
 typedef struct {
     int32_t cin, cout;
     int32_t k;
@@ -261,9 +264,9 @@ int32_t hatq_fwht_quant_act_noalloc(const float *x, int32_t n, int32_t h, int32_
  *   flags:     HATQ_PAIRED, HATQ_XQ_C64, HATQ_YQ_C64 (I8 mode only), or 0.
  * Supported: cin_pad % 64 == 0 with k <= 8, or cin_pad <= 4 with k*k*cin_pad <= 128;
  * cout_pad % 64 == 0; WH block and next_hblock a power of two at most 64, or
- * the Kronecker order 192 (P_12 (x) H~_16, applied as H~_16 then the Paley
- * factor; the WH restore multiplies by B^T) when cout_pad == 192 (I8: as
- * hatq_conv_int8_requant).  Transposed: stride 2.  xq and y (F32, I32) must be
+ * a Kronecker order equal to cout_pad: 192 (P_12 (x) H~_16), or 320
+ * (P_20 (x) H~_16) when cin_pad % 64 == 0 (applied as H~_16 then the Paley
+ * factor; the WH restore multiplies by B^T) (I8: as hatq_conv_int8_requant).  Transposed: stride 2.  xq and y (F32, I32) must be
  * 16-byte aligned, y in I8 mode 4-byte aligned. */
 int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act_scale,
                        int32_t n, int32_t h, int32_t w, int32_t out_mode, const float *out_scale, void *y,
@@ -344,7 +347,7 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
  *   s_x:   the static scale of W's input codes (unnormalized domain).
  *   s_y:   the static scale of the next operand's codes.
  *   next_hblock: the next operand's transform block (1: none), a power of two
- *          <= 64 or 192; the overflow bound depends on it, so the table serves
+ *          <= 64, 192 or 320; the overflow bound depends on it, so the table serves
  *          only calls with this next_hblock.
  *   table: device int32 [2*cout_pad + 1], 16-byte aligned, written as
  *     M[c]         = rne(2^n rho_c), rho_c = u_c / (beta_out s_y),

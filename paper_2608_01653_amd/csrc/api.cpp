@@ -92,6 +92,12 @@ int32_t out_hw(const hatq_conv_desc *d, int32_t h, int32_t w, int32_t *ho, int32
 
 int32_t hip_status(hipError_t e) { return e == hipSuccess ? HATQ_OK : HATQ_EHIP; }
 
+// A Kronecker order b on the layer's tile of bn columns.
+bool kron_tile(const hatq_weights *W, int b, int bn) {
+    const bool small = W->cin_pad <= 4 && W->k_total <= 128;
+    return (b == 192 && bn == 192) || (b == 320 && bn == 320 && !small);
+}
+
 // Kernel geometry the conv kernels implement.
 int32_t check_conv_supported(const hatq_weights *W) {
     const hatq_conv_desc &d = W->d;
@@ -108,10 +114,12 @@ int32_t check_conv_supported(const hatq_weights *W) {
     for (int t : tiles) fixed |= (W->cout_pad == t);
     const int bn = fixed ? W->cout_pad : 64;
     // the WH restore runs inside one wave: a Sylvester block up to 64 that tiles
-    // the columns, or the Kronecker order 192 on a 192-column tile
+    // the columns, or a Kronecker order on a tile of that many columns (192;
+    // 320 on the general kernel's 320-column tile, which the small-channel
+    // kernels do not have)
     if (W->form == HATQ_WH) {
         const int b = W->d.hblock;
-        const bool ok = (is_pow2(b) && b <= 64 && bn % b == 0) || (b == 192 && bn == 192);
+        const bool ok = (is_pow2(b) && b <= 64 && bn % b == 0) || kron_tile(W, b, bn);
         if (!ok) return HATQ_EUNSUPPORTED;
     }
     return HATQ_OK;
@@ -133,15 +141,25 @@ int32_t check_weights(const hatq_weights *W) {
 // The chunk-major layouts: HATQ_XQ_C64 for the 5x5 stride-2 window kernel,
 // HATQ_YQ_C64 for code outputs with whole 64-channel planes.
 constexpr int32_t kConvFlags = HATQ_PAIRED | HATQ_XQ_C64 | HATQ_YQ_C64;
-int32_t check_layouts(const hatq_weights *W, int32_t flags, bool codes_out) {
+// order320: the launch applies an order-320 transform in its epilogue (the WH
+// restore of a float or code output, or the next operand's), which runs on the
+// general kernel's 320-column tile, not on the window kernel that reads
+// chunk-major codes.
+int32_t check_layouts(const hatq_weights *W, int32_t flags, bool codes_out, bool order320 = false) {
     const hatq_conv_desc &d = W->d;
     if ((flags & HATQ_YQ_C64) && !codes_out) return HATQ_EINVAL;
     if ((flags & HATQ_YQ_C64) && d.cout % 64 != 0) return HATQ_EUNSUPPORTED;
     if ((flags & HATQ_XQ_C64) &&
         (d.transposed || d.k != 5 || d.stride != 2 || W->cin_pad % 64 != 0 ||
-         (W->cout_pad != 192 && W->cout_pad != 320)))
+         (W->cout_pad != 192 && W->cout_pad != 320) || order320))
         return HATQ_EUNSUPPORTED;
     return HATQ_OK;
+}
+
+// Whether a launch with a float or code output (not I32) transforms by the
+// order 320 in its epilogue.
+bool order320(const hatq_weights *W, int32_t next_hblock, bool next_used) {
+    return (W->form == HATQ_WH && W->d.hblock == 320) || (next_used && next_hblock == 320);
 }
 
 int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next_absmax) {
@@ -153,10 +171,10 @@ int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next
     for (int t : tiles) fixed |= (W->cout_pad == t);
     const int bn = fixed ? W->cout_pad : 64;
     // the next operand's transform runs inside one wave: a Sylvester block up
-    // to 64 that tiles the columns, or the Kronecker order 192 on a 192-column
-    // tile (320 would span the two launches of a 320-column layer)
+    // to 64 that tiles the columns, or a Kronecker order on a tile of that many
+    // columns
     if (hatq::kron_q(next_hblock)) {
-        if (next_hblock != 192 || bn != 192) return HATQ_EUNSUPPORTED;
+        if (!kron_tile(W, next_hblock, bn)) return HATQ_EUNSUPPORTED;
     } else if (next_hblock > 64 || (bn % next_hblock != 0 && next_hblock > 1)) {
         return HATQ_EUNSUPPORTED;
     }
@@ -440,7 +458,7 @@ int32_t requant(const hatq_weights *W, const int8_t *xq, const float *act_scale,
         return HATQ_EINVAL;
     if (next_absmax && !aligned(next_absmax, 4)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
-    if ((s = check_layouts(W, flags, true)) != HATQ_OK) return s;
+    if ((s = check_layouts(W, flags, true, order320(W, next_hblock, true))) != HATQ_OK) return s;
     // the transform and the code layout follow the next operand's blocks
     const float *probe = next_absmax ? next_absmax : next_scale;
     if ((s = check_next(W, next_hblock, probe)) != HATQ_OK) return s;
@@ -473,7 +491,10 @@ int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act
     if (!y && !(out_mode == HATQ_OUT_F32 && next_absmax)) return HATQ_EINVAL;
     if (!aligned(xq, 16) || (y && !aligned(y, 16)) || !aligned(act_scale, 4)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
-    if ((s = check_layouts(W, flags, false)) != HATQ_OK) return s;
+    if ((s = check_layouts(W, flags, false,
+                           out_mode == HATQ_OUT_F32 && order320(W, next_hblock, next_absmax != nullptr))) !=
+        HATQ_OK)
+        return s;
     if ((s = check_next(W, next_hblock, next_absmax)) != HATQ_OK) return s;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
@@ -556,7 +577,7 @@ int32_t hatq_int_transition_params(const hatq_weights *W, float s_x, float s_y, 
     if (s != HATQ_OK) return s;
     if (!table || !aligned(table, 16)) return HATQ_EINVAL;
     if (!(s_x > 0.0f) || !(s_y > 0.0f) || !std::isfinite(s_x) || !std::isfinite(s_y)) return HATQ_EINVAL;
-    if (!((is_pow2(next_hblock) && next_hblock <= 64) || next_hblock == 192)) return HATQ_EINVAL;
+    if (!((is_pow2(next_hblock) && next_hblock <= 64) || hatq::kron_q(next_hblock) != 0)) return HATQ_EINVAL;
     const bool dh = W->form == HATQ_DH;
     hatq::IntParamArgs a;
     a.w_scale = W->w_scale;
@@ -581,7 +602,7 @@ int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, i
     if (flags & ~kConvFlags) return HATQ_EINVAL;
     if (!aligned(xq, 16) || !aligned(yq, (flags & HATQ_YQ_C64) ? 16 : 4) || !aligned(table, 16)) return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
-    if ((s = check_layouts(W, flags, true)) != HATQ_OK) return s;
+    if ((s = check_layouts(W, flags, true, order320(W, next_hblock, true))) != HATQ_OK) return s;
     if ((s = check_next(W, next_hblock, reinterpret_cast<const float *>(table))) != HATQ_OK) return s;
     if (W->d.cout % 4) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;

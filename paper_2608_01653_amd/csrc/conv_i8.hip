@@ -304,15 +304,17 @@ struct Epi {
 using EpiGeneric = Epi<-1, -1>;
 using EpiGenericInt = Epi<-1, -1, 2>;   // the integer transition, blocks at run time
 using EpiGenericAffine = Epi<-1, -1, 3>;   // affine activations: zero-point correction
-// A Kronecker order (192) for the WH restore or the next operand, on a
-// 192-column tile: float modes (Q = 5) and the integer transition (Q = 6).
+// A Kronecker order (192 or 320) for the WH restore or the next operand, on a
+// tile of that many columns: float modes (Q = 5) and the integer transition
+// (Q = 6).
 using EpiKron = Epi<-1, -1, 5>;
 using EpiKronInt = Epi<-1, -1, 6>;
 
 // Whether a launch needs the Kronecker epilogue.
 inline bool kron_epilogue(const ConvArgs &a) {
-    const bool next = a.next_hblock == 192 && (a.next_absmax != nullptr || a.mode == 2 || a.mode == kModeIntTransition);
-    const bool restore = a.form == 1 && a.hblock == 192 && a.mode != 0;
+    const bool next = kron_q(a.next_hblock) != 0 &&
+                      (a.next_absmax != nullptr || a.mode == 2 || a.mode == kModeIntTransition);
+    const bool restore = a.form == 1 && kron_q(a.hblock) != 0 && a.mode != 0;
     return a.zx == nullptr && (next || restore);
 }
 
@@ -321,7 +323,8 @@ template <typename E>
 bool epi_matches(const ConvArgs &a) {
     if constexpr (E::WB == -1) {
         if constexpr (E::Q == 5 || E::Q == 6)
-            return kron_epilogue(a) && a.cout_pad == 192 && (a.mode == kModeIntTransition) == (E::Q == 6);
+            return kron_epilogue(a) && (a.cout_pad == 192 || a.cout_pad == 320) &&
+                   (a.mode == kModeIntTransition) == (E::Q == 6);
         return (a.mode == kModeIntTransition) == (E::Q == 2) && (a.zx != nullptr) == (E::Q == 3);
     } else {
         if ((a.zx != nullptr) != (E::Q == 3)) return false;
@@ -425,7 +428,11 @@ struct Epilogue {
     static constexpr int WB = E::WB, NB = E::NB;
     static constexpr bool generic = WB == -1;
     static constexpr int NBLK = FN / 4;
-    static constexpr bool kKron = (E::Q == 5 || E::Q == 6) && FN == 12;
+    // the Kronecker order of a tile of 16 FN columns (192 = P_12 (x) H~_16,
+    // 320 = P_20 (x) H~_16): its Paley q, and the values a lane holds per pixel
+    static constexpr int KQ = FN == 12 ? 11 : FN == 20 ? 19 : 0;
+    static constexpr int KB = 16 * FN, KV = 4 * FN;
+    static constexpr bool kKron = (E::Q == 5 || E::Q == 6) && KQ != 0;
     // the fixed I8 variants take the dynamic scale only (epi_matches): no clamp
     static constexpr bool kClamp = E::Q != 1;
     const ConvArgs &a;
@@ -468,14 +475,15 @@ struct Epilogue {
         // itself (B_next y = B B z / b = z in exact arithmetic): its maximum and
         // its codes are taken from z, and neither butterfly runs.
         zpair = !fl.affine && z_bound && !fl.store && nbk > 1 && (fl.want_abs || fl.i8);
-        // A Kronecker order (192 = P_12 (x) H~_16) for the next operand or the
-        // WH restore spans the tile's three 64-channel blocks (a 192-column
-        // tile: a lane holds all twelve 16-channel groups of its pixel), so
-        // the Kronecker variants handle it after the last block (block_kron).
+        // A Kronecker order (192 = P_12 (x) H~_16, 320 = P_20 (x) H~_16) for the
+        // next operand or the WH restore spans all the tile's 64-channel blocks
+        // (a tile of that many columns: a lane holds every 16-channel group of
+        // its pixel), so the Kronecker variants handle it after the last block
+        // (block_kron).
         kron = false;
         if constexpr (kKron) {
-            const bool nk = a.next_hblock == 192 && (fl.want_abs || fl.i8 || fl.iq);
-            kron = nk || (fl.wh && a.hblock == 192);
+            const bool nk = a.next_hblock == KB && (fl.want_abs || fl.i8 || fl.iq);
+            kron = nk || (fl.wh && a.hblock == KB);
         }
         // I8 mode: the sample's scale (from the absmax as the activation quantizer
         // derives it, or given), published by the sample's first tile
@@ -668,17 +676,15 @@ struct Epilogue {
     }
 
     // The sixteen values of 64-channel block k inside a row group's 48.
-    static __device__ __forceinline__ float (&grp(float (&v)[48], int k))[16] {
-        return *reinterpret_cast<float (*)[16]>(v + 16 * k);
-    }
-    static __device__ __forceinline__ int64_t (&grp(int64_t (&v)[48], int k))[16] {
-        return *reinterpret_cast<int64_t (*)[16]>(v + 16 * k);
+    template <typename T>
+    static __device__ __forceinline__ T (&grp(T (&v)[KV], int k))[16] {
+        return *reinterpret_cast<T (*)[16]>(v + 16 * k);
     }
 
-    // Float modes with a Kronecker order on the tile's 192 columns.  Channel c
+    // Float modes with a Kronecker order on the tile's KB columns.  Channel c
     // = 16 j + 4 q + r of the lane's pixel sits in v[4 j + r] (j = 4 k + jj the
     // fragment): the Kronecker index a * 16 + l has a = j (the Paley factor over
-    // the twelve fragments, in registers) and l = 4 q + r (the H~_16 factor:
+    // the FN fragments, in registers) and l = 4 q + r (the H~_16 factor:
     // register bits and lane bits 4-5, the first four stages of fwht_acc).  The
     // stage order is the activation kernel's (H~_16, then the Paley factor,
     // summed in ascending order), so the values are the ones it computes.
@@ -687,9 +693,9 @@ struct Epilogue {
         const int nb = a.next_hblock;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
-            float v[48];
+            float v[KV];
 #pragma unroll
-            for (int k = 0; k < 3; ++k) {
+            for (int k = 0; k < NBLK; ++k) {
                 v4i cc[4];
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) cc[jj] = acc[i][4 * k + jj];
@@ -707,48 +713,48 @@ struct Epilogue {
             }
             if (wh) {
                 // the output restore: B^T z (the column factors carry 1/b)
-                if (a.hblock == 192) {
+                if (a.hblock == KB) {
 #pragma unroll
-                    for (int k = 0; k < 3; ++k) fwht_acc<16, true>(grp(v, k), 16);
-                    paley_stage_t<11>(v);
+                    for (int k = 0; k < NBLK; ++k) fwht_acc<16, true>(grp(v, k), 16);
+                    paley_stage_t<KQ>(v);
                 } else {
 #pragma unroll
-                    for (int k = 0; k < 3; ++k) fwht_acc<-1, true>(grp(v, k), a.hblock);
+                    for (int k = 0; k < NBLK; ++k) fwht_acc<-1, true>(grp(v, k), a.hblock);
                 }
             }
             if (store && valid[i]) {
 #pragma unroll
-                for (int k = 0; k < 3; ++k) store_group(a, t, row0, lane, i, k, grp(v, k));
+                for (int k = 0; k < NBLK; ++k) store_group(a, t, row0, lane, i, k, grp(v, k));
             }
             if (!(want_abs || i8)) continue;
             // rows past the grid are not part of the next operand (cout is a
             // multiple of the next block, so every channel is)
             if (!valid[i]) {
 #pragma unroll
-                for (int r = 0; r < 48; ++r) v[r] = 0.0f;
+                for (int r = 0; r < KV; ++r) v[r] = 0.0f;
             }
-            if (nb == 192) {
+            if (nb == KB) {
                 // channel order matters for the codes only
                 if (i8) {
 #pragma unroll
-                    for (int k = 0; k < 3; ++k) fwht_acc<16, true>(grp(v, k), 16);
+                    for (int k = 0; k < NBLK; ++k) fwht_acc<16, true>(grp(v, k), 16);
                 } else {
 #pragma unroll
-                    for (int k = 0; k < 3; ++k) fwht_acc<16, false>(grp(v, k), 16);
+                    for (int k = 0; k < NBLK; ++k) fwht_acc<16, false>(grp(v, k), 16);
                 }
-                paley_stage<11>(v);
+                paley_stage<KQ>(v);
             } else if (nb > 1) {
                 if (i8) {
 #pragma unroll
-                    for (int k = 0; k < 3; ++k) fwht_acc<-1, true>(grp(v, k), nb);
+                    for (int k = 0; k < NBLK; ++k) fwht_acc<-1, true>(grp(v, k), nb);
                 } else {
 #pragma unroll
-                    for (int k = 0; k < 3; ++k) fwht_acc<-1, false>(grp(v, k), nb);
+                    for (int k = 0; k < NBLK; ++k) fwht_acc<-1, false>(grp(v, k), nb);
                 }
             }
             if (i8) {
 #pragma unroll
-                for (int k = 0; k < 3; ++k) {
+                for (int k = 0; k < NBLK; ++k) {
                     uint32_t w[4];
                     quant16(grp(v, k), qs, qr, q_fast, w);
                     store_codes(w, i, k);
@@ -756,7 +762,7 @@ struct Epilogue {
             } else {
                 float mm = 0.0f;
 #pragma unroll
-                for (int r = 0; r < 48; ++r) mm = fmaxf(mm, fabsf(v[r]));
+                for (int r = 0; r < KV; ++r) mm = fmaxf(mm, fabsf(v[r]));
                 wave_m = fmaxf(wave_m, mm);
             }
         }
@@ -768,9 +774,9 @@ struct Epilogue {
         const int nb = a.next_hblock;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
-            int64_t v[48];
+            int64_t v[KV];
 #pragma unroll
-            for (int k = 0; k < 3; ++k)
+            for (int k = 0; k < NBLK; ++k)
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) {
                     const int cl = 64 * k + 16 * jj + 4 * q;
@@ -782,25 +788,25 @@ struct Epilogue {
                         v[16 * k + 4 * jj + r] = (int64_t)m4[r] * (int64_t)(c4[r] + b4[r]);
                 }
             if (fl.wh) {
-                if (a.hblock == 192) {
+                if (a.hblock == KB) {
 #pragma unroll
-                    for (int k = 0; k < 3; ++k) fwht_acc_i64<16>(grp(v, k), 16);
-                    paley_stage_i64<11, true>(v);
+                    for (int k = 0; k < NBLK; ++k) fwht_acc_i64<16>(grp(v, k), 16);
+                    paley_stage_i64<KQ, true>(v);
                 } else {
 #pragma unroll
-                    for (int k = 0; k < 3; ++k) fwht_acc_i64<-1>(grp(v, k), a.hblock);
+                    for (int k = 0; k < NBLK; ++k) fwht_acc_i64<-1>(grp(v, k), a.hblock);
                 }
             }
-            if (nb == 192) {
+            if (nb == KB) {
 #pragma unroll
-                for (int k = 0; k < 3; ++k) fwht_acc_i64<16>(grp(v, k), 16);
-                paley_stage_i64<11, false>(v);
+                for (int k = 0; k < NBLK; ++k) fwht_acc_i64<16>(grp(v, k), 16);
+                paley_stage_i64<KQ, false>(v);
             } else {
 #pragma unroll
-                for (int k = 0; k < 3; ++k) fwht_acc_i64<-1>(grp(v, k), nb);
+                for (int k = 0; k < NBLK; ++k) fwht_acc_i64<-1>(grp(v, k), nb);
             }
 #pragma unroll
-            for (int k = 0; k < 3; ++k) {
+            for (int k = 0; k < NBLK; ++k) {
                 uint32_t c[16];
                 if (rq_n >= 32) {
 #pragma unroll
@@ -1887,8 +1893,6 @@ hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
 // blocks of 64, next operand blocked by 64 (DH next), 1 (WH next) or none.
 #define HATQ_GENERIC_EPILOGUES EpiGenericInt, EpiGenericAffine, EpiGeneric
 #define HATQ_KRON_EPILOGUES EpiKron, EpiKronInt
-#define HATQ_HOT_EPILOGUES \
-    Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_GENERIC_EPILOGUES
 
 int persistent_blocks();
 
@@ -2941,7 +2945,8 @@ hipError_t conv_part_pipe192(const ConvArgs &a, hipStream_t st) {
 #endif
 #if HATQ_PART(4)
 hipError_t conv_part_pipe320(const ConvArgs &a, hipStream_t st) {
-    return with_epilogue<HATQ_HOT_EPILOGUES>(
+    return with_epilogue<Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_KRON_EPILOGUES,
+                         HATQ_GENERIC_EPILOGUES>(
         a, [&](auto e) { return launch_pipe<4, 32, 320, 5, decltype(e)>(a, st); });
 }
 #endif
@@ -3021,8 +3026,10 @@ hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
             }
             return conv_part_pipe192(a, st);
         case 320:
-            if (a.sa == 2 && a.so == 1 && a.k == 5 && a.cin_p % 64 == 0) {
-                // the window kernel over columns 0..191, then 192..319
+            if (a.sa == 2 && a.so == 1 && a.k == 5 && a.cin_p % 64 == 0 && !kron_epilogue(a)) {
+                // the window kernel over columns 0..191, then 192..319 (an
+                // order-320 transform spans both: the pipeline kernel's
+                // 320-column tile takes those)
                 bool hit = false;
                 hipError_t r = conv_part_halo192_a(a, &hit, st, 0, true);
                 if (!hit) r = conv_part_halo192_b(a, st, 0, true);

@@ -146,6 +146,17 @@ def test_conv_rejects_before_launch(L):
     assert c(ctypes.byref(Wt), 1, 8, 8, 1, FAKE, 0, None, flags=hatq.HATQ_XQ_C64) == hatq.HATQ_EUNSUPPORTED
     W128 = _fake_weights(cout=128)
     assert c(ctypes.byref(W128), 1, 8, 8, 1, FAKE, 0, None, flags=hatq.HATQ_XQ_C64) == hatq.HATQ_EUNSUPPORTED
+    # an order-320 transform in the epilogue runs on the general kernel's
+    # 320-column tile: not with chunk-major codes, not for 3 input channels
+    Wwh = _fake_weights(cout=320, hb=320, form=1)
+    assert c(ctypes.byref(Wwh), 1, 8, 8, 1, FAKE, 0, None, flags=hatq.HATQ_XQ_C64) == hatq.HATQ_EUNSUPPORTED
+    Wdh = _fake_weights(cout=320)
+    assert c(ctypes.byref(Wdh), 1, 8, 8, 1, FAKE, 320, FAKE, flags=hatq.HATQ_XQ_C64) == hatq.HATQ_EUNSUPPORTED
+    assert c(ctypes.byref(Wdh), 1, 8, 8, 1, FAKE, 192, FAKE) == hatq.HATQ_EUNSUPPORTED   # 192 does not tile 320
+    Wrgb = _fake_weights(cin=3, cout=320, hb=320, form=1)
+    assert c(ctypes.byref(Wrgb), 1, 8, 8, 1, FAKE, 0, None) == hatq.HATQ_EUNSUPPORTED
+    Wrgb64 = _fake_weights(cin=3, cout=320, hb=64, form=1)
+    assert c(ctypes.byref(Wrgb64), 1, 8, 8, 1, FAKE, 320, FAKE) == hatq.HATQ_EUNSUPPORTED
     assert c(ctypes.byref(W), 1, 8, 8, 1, FAKE, 0, None, out_scale=FAKE) == hatq.HATQ_EINVAL   # scale outside I8
     bad = _fake_weights()
     bad.k_total += 1                                   # inconsistent view

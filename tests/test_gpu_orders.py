@@ -89,6 +89,29 @@ def test_layer_forward_exact_inputs(orc, c):
     assert np.array_equal(y, r.y)
 
 
+WH_LAYERS = [(1, 15, 13, 192, 192, 5, 2, 2, False, 0, "WH", 192),
+             (2, 11, 13, 192, 320, 5, 2, 2, False, 0, "WH", 320)]
+
+
+@pytest.mark.parametrize("c", WH_LAYERS, ids=[f"WH{c[11]}" for c in WH_LAYERS])
+def test_layer_forward_wh_kronecker(orc, c):
+    """A WH layer with the paper's order m(cout) through hatq_layer_forward: the
+    input quantized in the original domain (the same scale as the oracle's),
+    the output restored by B^T in the epilogue, within 1e-6 of the range (192
+    on the window kernel, 320 on the general kernel's 320-column tile)."""
+    n, h, w, cin, cout, k, s, p, tr, op, form, hb = c
+    rng, ref, layer = _layer(orc, c, 323)
+    x = synth.heavy_tailed_activations(rng, (n, h, w, cin))
+    r = orc.layer_forward(x, ref)
+    sc = torch.empty(n, device="cuda")
+    y = host(hatq.hatq_layer_forward(layer, form, dev(x), act_scale=sc))
+    # no input transform: the scale and the codes are the oracle's exactly
+    assert np.array_equal(host(sc), r.sx)
+    yc = host(hatq.hatq_conv_int8(layer, dev(r.xq), dev(r.sx), hatq.HATQ_OUT_F32))
+    assert np.array_equal(y, yc)
+    assert_range_rel(y, r.y)
+
+
 @pytest.mark.parametrize("c", LAYERS[:2], ids=IDS[:2])
 def test_layer_forward_heavy_tailed(orc, c):
     """The oracle's codes and scale fed to the GPU convolution: fp32 output
@@ -102,9 +125,11 @@ def test_layer_forward_heavy_tailed(orc, c):
 
 
 def test_unsupported_uses_are_rejected(orc):
-    """What stays outside the kernels: the order 320 in a convolution epilogue
-    (a 320-column layer runs as two launches, so a 320 block would span both),
-    192 on a 320-column layer, a Kronecker block cut by the channel count in the
+    """What stays outside the kernels: an order-320 epilogue with chunk-major
+    input codes (the window kernel splits a 320-column layer over two launches;
+    the order 320 runs on the general kernel's 320-column tile) or with three
+    input channels (the small-channel kernels have no 320-column tile), 192 on a
+    320-column layer, a Kronecker block cut by the channel count in the
     profiling pass, and the affine zero-point correction with a Kronecker WH
     restore.  Each is rejected before any launch."""
     wt = torch.ones(320, 192, 5, 5, device="cuda")
@@ -113,14 +138,22 @@ def test_unsupported_uses_are_rejected(orc):
     xq = torch.zeros((1, 9, 9, 192), dtype=torch.int8, device="cuda")
     sx = torch.ones(1, device="cuda")
     with pytest.raises(hatq.HatqError) as e:
-        hatq.hatq_conv_int8(wh320, xq, sx, hatq.HATQ_OUT_F32)
+        hatq.hatq_conv_int8(wh320, hatq.to_c64(xq), sx, hatq.HATQ_OUT_F32)
+    assert e.value.status == hatq.HATQ_EUNSUPPORTED
+    rgb = hatq.hatq_prepare_weights(hatq.desc(3, 320, 5, 2, 2, 320), "WH", wt[:, :3].contiguous(), b0)
+    with pytest.raises(hatq.HatqError) as e:
+        hatq.hatq_conv_int8(rgb, torch.zeros((1, 9, 9, 3), dtype=torch.int8, device="cuda"), sx,
+                            hatq.HATQ_OUT_F32)
     assert e.value.status == hatq.HATQ_EUNSUPPORTED
     dh320 = hatq.hatq_prepare_weights(hatq.desc(192, 320, 5, 2, 2, 64), "DH", wt, b0)
-    for nb in (192, 320):
-        with pytest.raises(hatq.HatqError) as e:
-            hatq.hatq_conv_int8(dh320, xq, sx, hatq.HATQ_OUT_F32, next_hblock=nb,
-                                next_absmax=torch.zeros(1, device="cuda"))
-        assert e.value.status == hatq.HATQ_EUNSUPPORTED
+    with pytest.raises(hatq.HatqError) as e:
+        hatq.hatq_conv_int8(dh320, xq, sx, hatq.HATQ_OUT_F32, next_hblock=192,
+                            next_absmax=torch.zeros(1, device="cuda"))
+    assert e.value.status == hatq.HATQ_EUNSUPPORTED
+    with pytest.raises(hatq.HatqError) as e:
+        hatq.hatq_conv_int8(dh320, hatq.to_c64(xq), sx, hatq.HATQ_OUT_F32, next_hblock=320,
+                            next_absmax=torch.zeros(1, device="cuda"))
+    assert e.value.status == hatq.HATQ_EUNSUPPORTED
     with pytest.raises(hatq.HatqError) as e:
         hatq.hatq_range_expansion(torch.zeros((1, 2, 2, 200), device="cuda"), 192)
     assert e.value.status == hatq.HATQ_EUNSUPPORTED
@@ -183,14 +216,19 @@ def test_affine_quant_kronecker(orc, m):
         assert d.max() <= 1 and np.count_nonzero(d) <= 1e-4 * d.size
 
 
-# The Kronecker order 192 in the convolution epilogues (192-column tiles):
+# The Kronecker orders in the convolution epilogues (192 on 192-column tiles,
+# 320 on the general kernel's 320-column tile):
 # (n, h, w, cin, cout, k, stride, pad, transposed, out_pad, form, hblock, next block)
 KCONV = [(2, 17, 21, 192, 192, 5, 2, 2, False, 0, "DH", 64, 192),     # window kernel, next operand 192
          (1, 13, 15, 192, 192, 5, 2, 2, False, 0, "WH", 192, 1),      # window kernel, WH restore 192
          (1, 11, 9, 192, 192, 5, 2, 2, False, 0, "WH", 192, 192),     # both
          (1, 9, 13, 192, 192, 3, 1, 1, False, 0, "DH", 192, 192),     # pipeline kernel
          (2, 13, 17, 3, 192, 5, 2, 2, False, 0, "WH", 192, 64),       # row-run kernel (3 input channels)
-         (1, 6, 7, 192, 192, 5, 2, 2, True, 1, "DH", 64, 192)]        # transposed phases
+         (1, 6, 7, 192, 192, 5, 2, 2, True, 1, "DH", 64, 192),        # transposed phases
+         (1, 13, 11, 192, 320, 5, 2, 2, False, 0, "WH", 320, 1),      # 320-column tile, WH restore 320
+         (2, 11, 9, 192, 320, 5, 2, 2, False, 0, "DH", 64, 320),      # next operand 320
+         (1, 9, 13, 192, 320, 3, 1, 1, False, 0, "WH", 320, 320),     # both, stride 1
+         (1, 6, 7, 192, 320, 5, 2, 2, True, 1, "WH", 320, 64)]        # transposed phases, WH restore 320
 KIDS = [f"{c[10]}{c[11]}-{c[3]}to{c[4]}k{c[5]}{'T' if c[8] else ''}-next{c[12]}" for c in KCONV]
 
 
@@ -212,7 +250,7 @@ def _gamma(k):
 
 def _transform_stages(b):
     """Rounded fp32 stages between an input value and a transformed one."""
-    return 4 + b // 16 - 1 if b == 192 else int(np.log2(b)) if b > 1 else 0
+    return 4 + b // 16 - 1 if b in (192, 320) else int(np.log2(b)) if b > 1 else 0
 
 
 @pytest.mark.parametrize("c", KCONV, ids=KIDS)
