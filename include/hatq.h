@@ -330,7 +330,7 @@ int32_t hatq_weight_tapsums(const hatq_weights *W, int32_t *tapsum, void *stream
  * accumulators; HATQ_OUT_F32: the same epilogue with s_x = act_scale).
  *   act_zero: device int32 [n] (from hatq_fwht_quant_act_affine).
  *   tapsum:   from hatq_weight_tapsums for W.
- * Supported: as hatq_conv_int8 (no next-operand absmax; WH blocks Sylvester). */
+ * Supported: as hatq_conv_int8 (no next-operand absmax). */
 int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const float *act_scale,
                               const int32_t *act_zero, const int32_t *tapsum, int32_t n, int32_t h, int32_t w,
                               int32_t out_mode, void *y, void *stream);

@@ -558,8 +558,6 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
         !aligned(tapsum, 16))
         return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
-    // (the zero-point correction has no Kronecker variant: WH layers take Sylvester blocks)
-    if (W->form == HATQ_WH && !is_pow2(W->d.hblock)) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
     return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, 0, nullptr, 0, static_cast<hipStream_t>(stream),

@@ -309,14 +309,17 @@ using EpiGenericAffine = Epi<-1, -1, 3>;   // affine activations: zero-point cor
 // (Q = 6).
 using EpiKron = Epi<-1, -1, 5>;
 using EpiKronInt = Epi<-1, -1, 6>;
+using EpiKronAffine = Epi<-1, -1, 7>;   // the WH restore after the zero-point correction
 
-// Whether a launch needs the Kronecker epilogue.
-inline bool kron_epilogue(const ConvArgs &a) {
+// Whether a launch applies a Kronecker order in its epilogue (any activation
+// kind), and whether it takes the symmetric Kronecker variants.
+inline bool kron_needed(const ConvArgs &a) {
     const bool next = kron_q(a.next_hblock) != 0 &&
                       (a.next_absmax != nullptr || a.mode == 2 || a.mode == kModeIntTransition);
     const bool restore = a.form == 1 && kron_q(a.hblock) != 0 && a.mode != 0;
-    return a.zx == nullptr && (next || restore);
+    return next || restore;
 }
+inline bool kron_epilogue(const ConvArgs &a) { return a.zx == nullptr && kron_needed(a); }
 
 // The variant a launch needs, or the generic one.
 template <typename E>
@@ -325,7 +328,11 @@ bool epi_matches(const ConvArgs &a) {
         if constexpr (E::Q == 5 || E::Q == 6)
             return kron_epilogue(a) && (a.cout_pad == 192 || a.cout_pad == 320) &&
                    (a.mode == kModeIntTransition) == (E::Q == 6);
-        return (a.mode == kModeIntTransition) == (E::Q == 2) && (a.zx != nullptr) == (E::Q == 3);
+        if constexpr (E::Q == 7)
+            return a.zx != nullptr && a.mode == 1 && kron_needed(a) && (a.cout_pad == 192 || a.cout_pad == 320);
+        // (never a launch with a Kronecker order: a list without its variants
+        // then finds no match and the launch fails)
+        return (a.mode == kModeIntTransition) == (E::Q == 2) && (a.zx != nullptr) == (E::Q == 3) && !kron_needed(a);
     } else {
         if ((a.zx != nullptr) != (E::Q == 3)) return false;
         const int wb = a.form == 1 ? a.hblock : 0;
@@ -347,7 +354,7 @@ struct EpiFlags {
     static constexpr bool generic = WB == -1;
     bool f32, wh, want_abs, i8, iq, affine, store;
     __device__ explicit EpiFlags(const ConvArgs &a) {
-        affine = E::Q == 3;
+        affine = E::Q == 3 || E::Q == 7;
         iq = E::Q == 2 || E::Q == 6;   // integer transition (its own variants, generic ones included)
         f32 = !iq && (generic ? a.mode != 0 : true);   // the fp32 arithmetic (F32 and I8 modes)
         wh = generic ? a.mode != 0 && a.form == 1 : WB != 0;
@@ -432,7 +439,7 @@ struct Epilogue {
     // 320 = P_20 (x) H~_16): its Paley q, and the values a lane holds per pixel
     static constexpr int KQ = FN == 12 ? 11 : FN == 20 ? 19 : 0;
     static constexpr int KB = 16 * FN, KV = 4 * FN;
-    static constexpr bool kKron = (E::Q == 5 || E::Q == 6) && KQ != 0;
+    static constexpr bool kKron = (E::Q == 5 || E::Q == 6 || E::Q == 7) && KQ != 0;
     // the fixed I8 variants take the dynamic scale only (epi_matches): no clamp
     static constexpr bool kClamp = E::Q != 1;
     const ConvArgs &a;
@@ -1882,6 +1889,7 @@ template <typename E, typename... Es, typename L>
 hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
     if constexpr (sizeof...(Es) == 0) {
         static_assert(E::WB == -1 && E::Q == 0, "the generic variant comes last");
+        if (!epi_matches<E>(a)) return hipErrorInvalidValue;   // a Kronecker order this list lacks
         return launch(E{});
     } else {
         if (epi_matches<E>(a)) return launch(E{});
@@ -1892,7 +1900,7 @@ hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
 // Variants compiled for the layer shapes of the analysis transforms: DH or WH
 // blocks of 64, next operand blocked by 64 (DH next), 1 (WH next) or none.
 #define HATQ_GENERIC_EPILOGUES EpiGenericInt, EpiGenericAffine, EpiGeneric
-#define HATQ_KRON_EPILOGUES EpiKron, EpiKronInt
+#define HATQ_KRON_EPILOGUES EpiKron, EpiKronInt, EpiKronAffine
 
 int persistent_blocks();
 
@@ -3026,7 +3034,7 @@ hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
             }
             return conv_part_pipe192(a, st);
         case 320:
-            if (a.sa == 2 && a.so == 1 && a.k == 5 && a.cin_p % 64 == 0 && !kron_epilogue(a)) {
+            if (a.sa == 2 && a.so == 1 && a.k == 5 && a.cin_p % 64 == 0 && !kron_needed(a)) {
                 // the window kernel over columns 0..191, then 192..319 (an
                 // order-320 transform spans both: the pipeline kernel's
                 // 320-column tile takes those)

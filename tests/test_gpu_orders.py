@@ -129,9 +129,8 @@ def test_unsupported_uses_are_rejected(orc):
     input codes (the window kernel splits a 320-column layer over two launches;
     the order 320 runs on the general kernel's 320-column tile) or with three
     input channels (the small-channel kernels have no 320-column tile), 192 on a
-    320-column layer, a Kronecker block cut by the channel count in the
-    profiling pass, and the affine zero-point correction with a Kronecker WH
-    restore.  Each is rejected before any launch."""
+    320-column layer, and a Kronecker block cut by the channel count in the
+    profiling pass.  Each is rejected before any launch."""
     wt = torch.ones(320, 192, 5, 5, device="cuda")
     b0 = torch.zeros(320, device="cuda")
     wh320 = hatq.hatq_prepare_weights(hatq.desc(192, 320, 5, 2, 2, 320), "WH", wt, b0)
@@ -156,11 +155,6 @@ def test_unsupported_uses_are_rejected(orc):
     assert e.value.status == hatq.HATQ_EUNSUPPORTED
     with pytest.raises(hatq.HatqError) as e:
         hatq.hatq_range_expansion(torch.zeros((1, 2, 2, 200), device="cuda"), 192)
-    assert e.value.status == hatq.HATQ_EUNSUPPORTED
-    wh192 = hatq.hatq_prepare_weights(hatq.desc(192, 192, 5, 2, 2, 192), "WH", wt[:192], b0[:192])
-    zx = torch.zeros(1, dtype=torch.int32, device="cuda")
-    with pytest.raises(hatq.HatqError) as e:
-        hatq.hatq_conv_int8_affine(wh192, xq, sx, zx, hatq.hatq_weight_tapsums(wh192), hatq.HATQ_OUT_F32)
     assert e.value.status == hatq.HATQ_EUNSUPPORTED
 
 
@@ -251,6 +245,36 @@ def _gamma(k):
 def _transform_stages(b):
     """Rounded fp32 stages between an input value and a transformed one."""
     return 4 + b // 16 - 1 if b in (192, 320) else int(np.log2(b)) if b > 1 else 0
+
+
+# Affine activations with a Kronecker WH restore (the zero-point correction,
+# then B^T): (n, h, w, cin, cout, k, stride, pad, transposed, out_pad, form, hblock)
+KAFF = [(2, 13, 15, 192, 192, 5, 2, 2, False, 0, "WH", 192),     # window kernel
+        (1, 11, 9, 192, 320, 5, 2, 2, False, 0, "WH", 320),      # 320-column tile
+        (2, 13, 17, 3, 192, 5, 2, 2, False, 0, "WH", 192),       # row-run kernel (3 input channels)
+        (1, 6, 7, 192, 192, 5, 2, 2, True, 1, "WH", 192)]        # transposed phases
+
+
+@pytest.mark.parametrize("c", KAFF, ids=[f"{c[3]}to{c[4]}k{c[5]}{'T' if c[8] else ''}" for c in KAFF])
+def test_affine_conv_wh_kronecker(orc, c):
+    """The oracle's affine codes, scale and zero point (original domain: a WH
+    layer) into the GPU convolution with the Kronecker WH restore; the fp32
+    output within 1e-6 of the range of the oracle's epilogue of its centered
+    accumulators, and the centered INT32 accumulators bit-exact."""
+    n, h, w, cin, cout, k, s, p, tr, op, form, hb = c
+    rng, ref, layer = _layer(orc, c, 330)
+    x = synth.heavy_tailed_activations(rng, (n, h, w, cin))
+    x[0] += np.float32(1.0) * np.abs(x[0]).mean()
+    x[-1] = np.abs(x[-1])
+    xq, sx, zx = orc.quantize_affine(x)
+    if xq.shape[-1] < ref.cin_p:
+        xq = np.concatenate([xq, np.zeros(xq.shape[:-1] + (ref.cin_p - xq.shape[-1],), np.int8)], axis=-1)
+    acc_ref = orc.conv_int8(xq, ref.wq, stride=s, pad=p, transposed=tr, out_pad=op, zx=zx)
+    tapsum = hatq.hatq_weight_tapsums(layer)
+    acc = hatq.hatq_conv_int8_affine(layer, dev(xq), dev(sx), dev(zx), tapsum, hatq.HATQ_OUT_I32)
+    assert np.array_equal(host(acc), acc_ref)
+    y = hatq.hatq_conv_int8_affine(layer, dev(xq), dev(sx), dev(zx), tapsum, hatq.HATQ_OUT_F32)
+    assert_range_rel(host(y), orc.epilogue(acc_ref, sx, ref), what="affine WH Kronecker y")
 
 
 @pytest.mark.parametrize("c", KCONV, ids=KIDS)
