@@ -125,19 +125,26 @@ def kernel_label(st, key):
         what = "next-operand absmax only" if part == "absmax" else "codes of the next operand"
         return f"{name} ({shape}; {what}, WH restore + B_{nb} explicit)"
     nxt = i + 1 < st.nL
-    if L.cin <= 4:
-        name = "conv_rowrun_kernel"
-    elif L.k == 5 and L.stride == 2 and not L.transposed:
-        name = "conv_halo5_kernel"
-    else:
-        name = "conv_pipe_kernel"
     wb = L.hblock if L.form == "WH" else 0
     nb = st.act_hb[i + 1] if nxt else 0
+    if L.cin <= 4:
+        name = "conv_rowrun_kernel"
+    elif L.k == 5 and L.stride == 2 and not L.transposed and 320 not in (wb, nb):
+        name = "conv_halo5_kernel"
+    else:
+        name = "conv_pipe_kernel"    # (an order-320 epilogue: the 320-column tile)
     return f"{name}<Epi<{wb},{nb}>> ({shape})"
 
 
 def _log2(b):
     return max(int(b).bit_length() - 1, 0)
+
+
+def _stages(b):
+    """Add/sub passes over each element of a transform of order b: log2(b) for
+    a Sylvester block; for P_q+1 (x) H~_16 the four butterfly stages, then q
+    sums per output of the Paley factor."""
+    return 4 + int(b) // 16 - 1 if int(b) in (192, 320) else _log2(b)
 
 
 # Algorithmic vector-ALU lane-operations of the method per element:
@@ -147,8 +154,8 @@ DEQUANT_OPS = 2        # int -> fp32 conversion and the fused scale-and-bias
 
 def kernel_work(st, key):
     """Algorithmic work of the kernel(s) behind a mark label: INT8 MFMA ops,
-    HBM bytes and vector-ALU lane-operations (butterfly stages log2(b) add/sub
-    per element, dequantization, quantization, maxima)."""
+    HBM bytes and vector-ALU lane-operations (a transform's add/sub passes per
+    element, _stages, dequantization, quantization, maxima)."""
     import numpy as np
     from paper_2608_01653_amd import stack as stk, workloads
     li, part = key.split(".")
@@ -158,22 +165,22 @@ def kernel_work(st, key):
     if part == "quant":
         e = int(np.prod(ishape))
         passes = st.quant_passes(i)
-        ops = e * (_log2(st.act_hb[i]) + QUANT_OPS) + (e * (_log2(st.act_hb[i]) + 1) if passes == 2 else 0)
+        ops = e * (_stages(st.act_hb[i]) + QUANT_OPS) + (e * (_stages(st.act_hb[i]) + 1) if passes == 2 else 0)
         return {"mfma_ops": 0, "hbm_bytes": e * 5, "alu_lane_ops": ops}
     outs = int(np.prod(oshape[:3])) * L.cout
     wb = L.hblock if L.form == "WH" else 1
     nxt = i + 1 < st.nL
     nb = st.act_hb[i + 1] if nxt else 1
-    base = DEQUANT_OPS + _log2(wb)
+    base = DEQUANT_OPS + _stages(wb)
     mf = workloads.conv_ops(st.wl, i)
     wbytes = st.layers[i].cout_pad * st.layers[i].k_stride
     xin = int(np.prod(ishape))
     if part == "absmax":
-        return {"mfma_ops": mf, "hbm_bytes": xin + wbytes, "alu_lane_ops": outs * (base + _log2(nb) + 1)}
+        return {"mfma_ops": mf, "hbm_bytes": xin + wbytes, "alu_lane_ops": outs * (base + _stages(nb) + 1)}
     if part == "requant":
         return {"mfma_ops": mf, "hbm_bytes": xin + wbytes + outs,
-                "alu_lane_ops": outs * (base + _log2(nb) + QUANT_OPS)}
-    alu = outs * (base + ((_log2(nb) + 1) if nxt else 0))
+                "alu_lane_ops": outs * (base + _stages(nb) + QUANT_OPS)}
+    alu = outs * (base + ((_stages(nb) + 1) if nxt else 0))
     return {"mfma_ops": mf, "hbm_bytes": stk.conv_bytes(st, i), "alu_lane_ops": alu}
 
 
@@ -561,6 +568,30 @@ def measure_order_layer(st, params, per_layer, li=2, reps=20):
                     "element (4 B fp32 read + 1 B int8 written)"}
 
 
+def measure_paper_order_stack(wl, params, x0, steps, warmup, dev, block64_step_us):
+    """The same four layers with one block of the paper's order m(C) per
+    transformed axis (Eq. hadamard_order: 192, 192, 192, 320), the rest of the
+    step unchanged (explicit transforms, dynamic per-sample scales)."""
+    from paper_2608_01653_amd import hatq, stack, workloads
+    owl = workloads.with_orders(wl, hatq.hatq_hadamard_order)
+    ost = stack.Stack(owl, params, dev)
+    mk, us = run_steps(ost, x0, steps, warmup)
+    n, H, W = owl.input_shape[:3]
+    img_pix = n * H * W
+    ops = sum(workloads.conv_ops(owl, i) for i in range(ost.nL))
+    res = {"workload": owl.name, "orders": [L.hblock for L in owl.layers],
+           "layers_desc": [f"{L.form} {L.cin}->{L.cout} k{L.k}s{L.stride} b{L.hblock}" for L in owl.layers],
+           "ms_per_step": round(us / 1e3, 4), "tops": round(ops / (us * 1e-6) / 1e12, 2),
+           "mpix_per_s": round(img_pix / (us * 1e-6) / 1e6, 1),
+           "block64_ms_per_step": round(block64_step_us / 1e3, 4),
+           "layers": layer_report(ost, mk.durations_us(), img_pix),
+           "note": "192 = P_12 (x) H~_16, 320 = P_20 (x) H~_16; layer 1's two passes on the row-run kernel "
+                   "(the 32x32 variant takes blocks of 64), layer 4 on the general kernel's 320-column tile"}
+    log(f"paper-order stack {res['orders']}: {us / 1e3:.3f} ms/step")
+    del ost
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -682,6 +713,8 @@ def main():
             st.step(x0)
             out["affine_layer"] = measure_affine_layer(st, per_layer)
             out["paper_order_layer"] = measure_order_layer(st, params, per_layer)
+            out["paper_order_stack"] = measure_paper_order_stack(wl, params, x0, args.steps, args.warmup, dev,
+                                                                 step_us)
             flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
             others = []
             for name in OTHER_WORKLOADS:

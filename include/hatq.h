@@ -406,6 +406,16 @@ int32_t hatq_range_expansion(const float *x, int32_t n, int32_t h, int32_t w, in
  * tau.  Host only. */
 int32_t hatq_select_form(int64_t expansions, int64_t images, double tau, int32_t *form);
 
+/* Transform order rule (Eq. hadamard_order with the supplementary Hadamard
+ * construction): m(c) = the smallest order m >= 4 ceil(c/4) for which a
+ * Hadamard matrix is built, the orders being 1 and 2, q + 1 (Paley-I, q an odd
+ * prime power, q = 3 mod 4), 2(q + 1) (Paley-II, q = 1 mod 4), and every
+ * product of two of them (Kronecker products); m(192) = 192 and m(320) = 320.
+ * Returns m(c), or 0 for c < 1 or c > 4096.  Whether the kernels take the
+ * order is a separate question: hblock documents that (the powers of two up to
+ * 128, 192 and 320).  Host only. */
+int32_t hatq_hadamard_order(int32_t c);
+
 /* Workspace bytes of hatq_layer_forward for an input of n x h x w. */
 size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w);
 

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <vector>
 #include <cstdint>
 #include <cstring>
 
@@ -628,6 +629,35 @@ int32_t hatq_select_form(int64_t expansions, int64_t images, double tau, int32_t
     const double p = (double)expansions / (double)images;
     *form = p > tau ? HATQ_WH : HATQ_DH;
     return HATQ_OK;
+}
+
+int32_t hatq_hadamard_order(int32_t c) {
+    constexpr int kMax = 4096;
+    if (c < 1 || c > kMax) return 0;
+    // orders with a construction: 1, 2, Paley-I q + 1 (q = 3 mod 4) and
+    // Paley-II 2(q + 1) (q = 1 mod 4) for odd prime powers q, and products
+    static const std::vector<bool> built = [] {
+        std::vector<bool> ok(kMax + 1, false);
+        auto prime_power = [](int q) {
+            int p = 2;
+            while (q % p) ++p;
+            while (q % p == 0) q /= p;
+            return q == 1;
+        };
+        ok[1] = ok[2] = true;
+        for (int q = 3; q < kMax; q += 2) {
+            if (!prime_power(q)) continue;
+            if (q % 4 == 3 && q + 1 <= kMax) ok[q + 1] = true;
+            if (q % 4 == 1 && 2 * (q + 1) <= kMax) ok[2 * (q + 1)] = true;
+        }
+        for (int m = 4; m <= kMax; ++m)
+            for (int a = 2; a * a <= m && !ok[m]; ++a)
+                if (m % a == 0 && ok[a] && ok[m / a]) ok[m] = true;
+        return ok;
+    }();
+    for (int m = 4 * ((c + 3) / 4); m <= kMax; m += 4)
+        if (built[m]) return m;
+    return 0;
 }
 
 size_t hatq_layer_ws_bytes(const hatq_weights *W, int32_t n, int32_t h, int32_t w) {

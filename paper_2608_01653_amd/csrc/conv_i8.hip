@@ -334,6 +334,12 @@ bool epi_matches(const ConvArgs &a) {
         // then finds no match and the launch fails)
         return (a.mode == kModeIntTransition) == (E::Q == 2) && (a.zx != nullptr) == (E::Q == 3) && !kron_needed(a);
     } else {
+        if constexpr (E::Q == 5) {   // a Kronecker order at compile time (float modes)
+            const int wb = a.form == 1 ? a.hblock : 0;
+            const int nb = a.next_absmax != nullptr || a.mode == 2 ? a.next_hblock : 0;
+            return kron_epilogue(a) && a.mode != kModeIntTransition && (a.cout_pad == 192 || a.cout_pad == 320) &&
+                   wb == E::WB && nb == E::NB;
+        }
         if ((a.zx != nullptr) != (E::Q == 3)) return false;
         const int wb = a.form == 1 ? a.hblock : 0;
         if (E::Q == 3) return a.mode == 1 && wb == E::WB && a.next_absmax == nullptr;
@@ -352,15 +358,17 @@ template <typename E>
 struct EpiFlags {
     static constexpr int WB = E::WB, NB = E::NB;
     static constexpr bool generic = WB == -1;
+    // the Kronecker variants with fixed orders take the output mode at run time
+    static constexpr bool flex = generic || E::Q == 5;
     bool f32, wh, want_abs, i8, iq, affine, store;
     __device__ explicit EpiFlags(const ConvArgs &a) {
         affine = E::Q == 3 || E::Q == 7;
         iq = E::Q == 2 || E::Q == 6;   // integer transition (its own variants, generic ones included)
         f32 = !iq && (generic ? a.mode != 0 : true);   // the fp32 arithmetic (F32 and I8 modes)
         wh = generic ? a.mode != 0 && a.form == 1 : WB != 0;
-        want_abs = !iq && (generic ? a.mode == 1 && a.next_absmax != nullptr && a.next_hblock > 0
-                                   : (E::Q == 0 || E::Q == 4) && NB != 0);
-        i8 = !iq && (generic ? a.mode == 2 : E::Q == 1);
+        want_abs = !iq && (flex ? a.mode == 1 && a.next_absmax != nullptr && a.next_hblock > 0
+                                : (E::Q == 0 || E::Q == 4) && NB != 0);
+        i8 = !iq && (flex ? a.mode == 2 : E::Q == 1);
         store = E::Q != 4 && !i8 && !iq && a.y != nullptr;   // I32 / F32 values
     }
 };
@@ -697,7 +705,15 @@ struct Epilogue {
     // summed in ascending order), so the values are the ones it computes.
     __device__ void block_kron(const v4i (&acc)[FM][FN]) {
         const bool wh = fl.wh, want_abs = fl.want_abs, i8 = fl.i8, store = fl.store;
-        const int nb = a.next_hblock;
+        // orders fixed at compile time (E::Q == 5 with WB, NB given): the WH
+        // block 0 or the tile's order or a Sylvester block up to 64, the next
+        // operand's 0, 1, the tile's order or a Sylvester block up to 64
+        constexpr bool kFixed = E::WB != -1;
+        constexpr int kWB = kFixed ? E::WB : 1, kNB = kFixed ? E::NB : 1;
+        static_assert(!kFixed || ((kWB == 0 || kWB == KB || (kWB <= 64 && (kWB & (kWB - 1)) == 0)) &&
+                                  (kNB <= 1 || kNB == KB || (kNB <= 64 && (kNB & (kNB - 1)) == 0))),
+                      "fixed Kronecker variant orders");
+        const int nb = kFixed ? kNB : a.next_hblock;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
             float v[KV];
@@ -720,10 +736,20 @@ struct Epilogue {
             }
             if (wh) {
                 // the output restore: B^T z (the column factors carry 1/b)
-                if (a.hblock == KB) {
+                auto restore_kron = [&]() {
 #pragma unroll
                     for (int k = 0; k < NBLK; ++k) fwht_acc<16, true>(grp(v, k), 16);
                     paley_stage_t<KQ>(v);
+                };
+                if constexpr (kFixed) {
+                    if constexpr (kWB == KB) {
+                        restore_kron();
+                    } else if constexpr (kWB > 1) {
+#pragma unroll
+                        for (int k = 0; k < NBLK; ++k) fwht_acc<kWB, true>(grp(v, k), kWB);
+                    }
+                } else if (a.hblock == KB) {
+                    restore_kron();
                 } else {
 #pragma unroll
                     for (int k = 0; k < NBLK; ++k) fwht_acc<-1, true>(grp(v, k), a.hblock);
@@ -740,8 +766,8 @@ struct Epilogue {
 #pragma unroll
                 for (int r = 0; r < KV; ++r) v[r] = 0.0f;
             }
-            if (nb == KB) {
-                // channel order matters for the codes only
+            // channel order matters for the codes only
+            auto next_kron = [&]() {
                 if (i8) {
 #pragma unroll
                     for (int k = 0; k < NBLK; ++k) fwht_acc<16, true>(grp(v, k), 16);
@@ -750,6 +776,21 @@ struct Epilogue {
                     for (int k = 0; k < NBLK; ++k) fwht_acc<16, false>(grp(v, k), 16);
                 }
                 paley_stage<KQ>(v);
+            };
+            if constexpr (kFixed) {
+                if constexpr (kNB == KB) {
+                    next_kron();
+                } else if constexpr (kNB > 1) {
+                    if (i8) {
+#pragma unroll
+                        for (int k = 0; k < NBLK; ++k) fwht_acc<kNB, true>(grp(v, k), kNB);
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < NBLK; ++k) fwht_acc<kNB, false>(grp(v, k), kNB);
+                    }
+                }
+            } else if (nb == KB) {
+                next_kron();
             } else if (nb > 1) {
                 if (i8) {
 #pragma unroll
@@ -833,15 +874,25 @@ struct Epilogue {
 
     // 64-channel block k of every row group (one set of column factors serves all)
     __device__ __forceinline__ void block(const v4i (&acc)[FM][FN], int k) {
-        if constexpr (kKron) {
-            if (kron) {
-                if (k == NBLK - 1) {
-                    if (fl.iq) block_int_kron(acc);
-                    else block_kron(acc);
+        if constexpr (kKron && E::Q == 5 && E::WB != -1) {
+            // orders fixed at compile time: always the Kronecker path
+            if (k == NBLK - 1) block_kron(acc);
+        } else {
+            if constexpr (kKron) {
+                if (kron) {
+                    if (k == NBLK - 1) {
+                        if (fl.iq) block_int_kron(acc);
+                        else block_kron(acc);
+                    }
+                    return;
                 }
-                return;
             }
+            block_plain(acc, k);
         }
+    }
+
+    // One 64-channel block of every row group, no Kronecker order.
+    __device__ __forceinline__ void block_plain(const v4i (&acc)[FM][FN], int k) {
         if (fl.iq) {
             block_int(acc, k);
             return;
@@ -1901,6 +1952,11 @@ hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
 // blocks of 64, next operand blocked by 64 (DH next), 1 (WH next) or none.
 #define HATQ_GENERIC_EPILOGUES EpiGenericInt, EpiGenericAffine, EpiGeneric
 #define HATQ_KRON_EPILOGUES EpiKron, EpiKronInt, EpiKronAffine
+// The float-mode Kronecker variants with the orders at compile time, per tile
+// width (the paper's orders on every layer of a stack: order 192 on both sides
+// of a 192-column layer, 320 on a 320-column one).
+#define HATQ_KRON192_FIXED Epi<0, 192, 5>, Epi<192, 192, 5>, Epi<192, 1, 5>, Epi<192, 0, 5>
+#define HATQ_KRON320_FIXED Epi<0, 320, 5>, Epi<320, 1, 5>, Epi<320, 0, 5>
 
 int persistent_blocks();
 
@@ -1992,7 +2048,8 @@ hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
         }
         if constexpr (CS == 3)
             return with_epilogue<Epi<64, 64, 1>, Epi<64, 64, 2>, Epi<64, 64, 4>, Epi<0, 64>, Epi<0, 1>, Epi<0, 0>,
-                                 Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_KRON_EPILOGUES, HATQ_GENERIC_EPILOGUES>(
+                                 Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, Epi<192, 192, 5>, HATQ_KRON_EPILOGUES,
+                                 HATQ_GENERIC_EPILOGUES>(
                 a, [&](auto e) {
                 // the requantizing pass (two transforms and the quantizer per
                 // value) keeps one row group per wave: with two it spilled
@@ -2933,7 +2990,8 @@ hipError_t conv_part_halo192_a(const ConvArgs &a, bool *hit, hipStream_t st, int
 #endif
 #if HATQ_PART(2)
 hipError_t conv_part_halo192_b(const ConvArgs &a, hipStream_t st, int n_base, bool split) {
-    return with_epilogue<Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_KRON_EPILOGUES, HATQ_GENERIC_EPILOGUES>(
+    return with_epilogue<Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_KRON192_FIXED, HATQ_KRON_EPILOGUES,
+                         HATQ_GENERIC_EPILOGUES>(
         a, [&](auto e) { return launch_halo<192, 5, decltype(e)>(a, st, n_base, split); });
 }
 #endif
@@ -2953,8 +3011,8 @@ hipError_t conv_part_pipe192(const ConvArgs &a, hipStream_t st) {
 #endif
 #if HATQ_PART(4)
 hipError_t conv_part_pipe320(const ConvArgs &a, hipStream_t st) {
-    return with_epilogue<Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_KRON_EPILOGUES,
-                         HATQ_GENERIC_EPILOGUES>(
+    return with_epilogue<Epi<0, 64>, Epi<0, 1>, Epi<0, 0>, Epi<64, 64>, Epi<64, 1>, Epi<64, 0>, HATQ_KRON320_FIXED,
+                         HATQ_KRON_EPILOGUES, HATQ_GENERIC_EPILOGUES>(
         a, [&](auto e) { return launch_pipe<4, 32, 320, 5, decltype(e)>(a, st); });
 }
 #endif

@@ -154,24 +154,26 @@ struct ItemShape {
 
 // The Paley factor of a Kronecker order on the register groups of an item:
 // out[a] = sum over c, ascending, of P[a][c] * v[c] for each of the four values
-// j of group c (v[4*c + j]).
+// j of group c (v[4*c + j]).  One position j at a time, so only P temporaries
+// are live next to the values.
 template <int Q, int R4>
 __device__ __forceinline__ void paley_stage(float (&v)[R4]) {
     constexpr int P = Q + 1;
     static_assert(R4 == 4 * P, "one register group per Paley index");
     constexpr Paley1Table<Q> H{};
-    float out[R4];
 #pragma unroll
-    for (int a = 0; a < P; ++a)
+    for (int j = 0; j < 4; ++j) {
+        float out[P];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int a = 0; a < P; ++a) {
             float acc = H.s[a][0] > 0 ? v[j] : -v[j];
 #pragma unroll
             for (int c = 1; c < P; ++c) acc = H.s[a][c] > 0 ? acc + v[4 * c + j] : acc - v[4 * c + j];
-            out[4 * a + j] = acc;
+            out[a] = acc;
         }
 #pragma unroll
-    for (int r = 0; r < R4; ++r) v[r] = out[r];
+        for (int a = 0; a < P; ++a) v[4 * a + j] = out[a];
+    }
 }
 
 // The transposed factor, out[a] = sum over c, ascending, of P[c][a] * v[c]: the
@@ -182,18 +184,19 @@ __device__ __forceinline__ void paley_stage_t(float (&v)[R4]) {
     constexpr int P = Q + 1;
     static_assert(R4 == 4 * P, "one register group per Paley index");
     constexpr Paley1Table<Q> H{};
-    float out[R4];
 #pragma unroll
-    for (int a = 0; a < P; ++a)
+    for (int j = 0; j < 4; ++j) {
+        float out[P];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int a = 0; a < P; ++a) {
             float acc = H.s[0][a] > 0 ? v[j] : -v[j];
 #pragma unroll
             for (int c = 1; c < P; ++c) acc = H.s[c][a] > 0 ? acc + v[4 * c + j] : acc - v[4 * c + j];
-            out[4 * a + j] = acc;
+            out[a] = acc;
         }
 #pragma unroll
-    for (int r = 0; r < R4; ++r) v[r] = out[r];
+        for (int a = 0; a < P; ++a) v[4 * a + j] = out[a];
+    }
 }
 
 // The same on int64 values (exact, so any summation order), one register

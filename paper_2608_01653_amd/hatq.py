@@ -49,7 +49,7 @@ EXPORTS = ["hatq_status_string", "hatq_conv_out_hw", "hatq_weights_bytes", "hatq
            "hatq_export_weights", "hatq_pack_weights", "hatq_fwht_quant_ws_bytes", "hatq_fwht_quant_act",
            "hatq_fwht_quant_act_noalloc", "hatq_fwht_quant_act_c64", "hatq_conv_int8",
            "hatq_conv_int8_requant", "hatq_int_table_len", "hatq_int_transition_params",
-           "hatq_conv_int8_int_transition", "hatq_range_expansion", "hatq_select_form",
+           "hatq_conv_int8_int_transition", "hatq_range_expansion", "hatq_select_form", "hatq_hadamard_order",
            "hatq_fwht_quant_affine_ws_bytes", "hatq_fwht_quant_act_affine", "hatq_tapsum_len",
            "hatq_weight_tapsums", "hatq_conv_int8_affine",
            "hatq_layer_ws_bytes", "hatq_layer_forward"]
@@ -117,6 +117,8 @@ def load(build_if_missing: bool = False):
     L.hatq_range_expansion.restype = i32
     L.hatq_select_form.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_double, ctypes.POINTER(i32)]
     L.hatq_select_form.restype = i32
+    L.hatq_hadamard_order.argtypes = [i32]
+    L.hatq_hadamard_order.restype = i32
     L.hatq_layer_ws_bytes.argtypes = [ctypes.POINTER(Weights), i32, i32, i32]
     L.hatq_layer_ws_bytes.restype = sz
     L.hatq_layer_forward.argtypes = [ctypes.POINTER(Weights), i32, P, i32, i32, i32, P, P, P, i32, P, P,
@@ -530,6 +532,11 @@ def hatq_select_form(expansions: int, images: int, tau: float = 0.8) -> str:
     f = ctypes.c_int32(-1)
     _check(load().hatq_select_form(int(expansions), int(images), float(tau), ctypes.byref(f)), "hatq_select_form")
     return "WH" if f.value == HATQ_WH else "DH"
+
+
+def hatq_hadamard_order(c: int) -> int:
+    """m(c) of the transform order rule (0: c outside [1, 4096])."""
+    return int(load().hatq_hadamard_order(int(c)))
 
 
 def hatq_layer_ws_bytes(layer: PreparedLayer, n: int, h: int, w: int) -> int:

@@ -57,8 +57,12 @@ class Stack:
         def c64_ok(i):
             L = wl.layers[i]
             pl = self.layers[i]
+            # (an epilogue with an order-320 transform runs on the general
+            # kernel, which reads NHWC codes)
+            nxt = wl.layers[i + 1] if i + 1 < self.nL else None
+            o320 = (L.form == "WH" and L.hblock == 320) or (nxt is not None and self.act_hb[i + 1] == 320)
             reads = (not L.transposed and L.k == 5 and L.stride == 2 and pl.cin_pad % 64 == 0
-                     and pl.cout_pad in (192, 320))
+                     and pl.cout_pad in (192, 320) and not o320)
             hb = self.act_hb[i]
             writes = hb <= 64 and (hb & (hb - 1)) == 0 if not (i > 0 and self.requant[i - 1]) else True
             return i > 0 and reads and writes

@@ -4,12 +4,14 @@ Shapes only; no arithmetic of the method lives here.  Each workload is a list of
 layers run in order; a layer's fp32 output is the next layer's input (identity
 nonlinearity between layers).  ``form`` is the per-layer Hadamard form: "DH"
 (double-Hadamard, Sec. IV-B) or "WH" (weight-only Hadamard, Sec. IV-B).  ``hblock``
-is the Sylvester block size of the block-diagonal transform; it acts on C_in for DH
-and on C_out for WH.
+is the block order of the block-diagonal transform (Sylvester blocks of 64 in the
+specified workloads); it acts on C_in for DH and on C_out for WH.
+``with_orders`` gives the same stack with one block of the paper's order m(C)
+over each transformed axis (Eq. hadamard_order).
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field
+from dataclasses import dataclass, field, replace
 from typing import List, Optional, Tuple
 
 import numpy as np
@@ -66,6 +68,15 @@ class Workload:
         params = [synth.layer_params(rng, L.cin, L.cout, L.k, L.transposed, with_bias)
                   for L in self.layers]
         return x, params
+
+
+def with_orders(wl: Workload, order) -> Workload:
+    """The workload with each layer's block replaced by order(C), C the channel
+    count of the transformed axis (C_in for DH, C_out for WH); ``order`` is the
+    order rule m(C), passed in so this module stays free of the method."""
+    layers = [replace(L, hblock=int(order(L.cin if L.form == "DH" else L.cout))) for L in wl.layers]
+    return Workload(wl.name + "_paper_orders", wl.input_shape, wl.input_kind, layers, wl.seed,
+                    "one block of order m(C) per transformed axis")
 
 
 def conv_ops(wl: Workload, i: int) -> int:

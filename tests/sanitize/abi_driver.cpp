@@ -67,6 +67,11 @@ int main() {
     int32_t form = -1;
     EXPECT(hatq_select_form(3, 2, 0.8, &form), HATQ_EINVAL);
     EXPECT(hatq_select_form(1, 2, 0.8, &form), HATQ_OK);
+    EXPECT(hatq_hadamard_order(0), 0);
+    EXPECT(hatq_hadamard_order(4097), 0);
+    EXPECT(hatq_hadamard_order(3), 4);
+    EXPECT(hatq_hadamard_order(192), 192);
+    EXPECT(hatq_hadamard_order(4096), 4096);
     EXPECT(hatq_layer_forward(&W, HATQ_WH, xf, 1, 16, 16, nullptr, fl, nullptr, 0, nullptr, F, 1u << 30, nullptr),
            HATQ_EINVAL);
     EXPECT(hatq_export_weights(&W, nullptr, nullptr, nullptr, nullptr), HATQ_OK);

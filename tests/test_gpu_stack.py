@@ -39,14 +39,21 @@ def _gamma(k):
     return k * u / (1 - k * u)
 
 
+def _stages(b):
+    """Rounded fp32 stages between a value and its transform: log2(b) for a
+    Sylvester block; the 16-point butterfly then the Paley factor's b/16 - 1
+    sums for the Kronecker orders."""
+    return 4 + b // 16 - 1 if b in (192, 320) else int(np.log2(b)) if b > 1 else 0
+
+
 def _butterfly_absmax_tol(y, b):
     """|max|B y|_fp32-butterfly - max|fl32(B y)|_fp64| bound for one sample: each
-    value differs by at most gamma_log2(b) * (sum of |y| over its block) plus the
-    oracle's own rounding."""
+    value differs by at most gamma_stages(b) * (sum of |y| over its block) plus
+    the oracle's own rounding."""
     if b == 1:
         return 0.0
     ya = np.abs(y.astype(np.float64)).reshape(-1, b).sum(-1).max()
-    return _gamma(int(np.log2(b))) * ya + 2.0 ** -24 * np.abs(y).max() * b
+    return _gamma(_stages(b)) * ya + 2.0 ** -24 * np.abs(y).max() * b
 
 
 def _oracle_prepared(orc, wl, params):
@@ -86,7 +93,7 @@ def _check_sample(orc, st, refs, x0, s, paired):
             if pw.form == "WH":
                 za = np.abs(orc.wh_z(acc, sx_i, pw).astype(np.float64))
                 hb = pw.hblock
-                dy = _gamma(int(np.log2(hb))) * za.reshape(-1, hb).sum(-1).max() / hb
+                dy = _gamma(_stages(hb)) * za.reshape(-1, hb).sum(-1).max() / hb
                 tol += max(nb, 1) * (dy + 2.0 ** -24 * np.abs(y_ref).max())
             s_tol = tol / 127 + 2 * np.spacing(np.float32(s_ref[0]))
             assert abs(float(g(st.sc[i + 1])[0]) - float(s_ref[0])) <= s_tol
@@ -131,3 +138,23 @@ def test_stack_step_teacher_forced(orc, name, samples, paired):
     refs = _oracle_prepared(orc, wl, params)
     for s in samples:
         _check_sample(orc, st, refs, x_np, s, paired)
+
+
+def test_stack_paper_orders_teacher_forced(orc):
+    """The 512x768 stack with one block of the paper's order m(C) per transformed
+    axis (Eq. hadamard_order: 192, 192, 192, 320) instead of blocks of 64: the
+    WH restore of order 192 and the next operand's order 192 in layer 1's two
+    passes, order 192 in the quantizer and in the fused absmax, and the order-320
+    WH restore of layer 4 on the 320-column tile; same rules per stage."""
+    wl = workloads.with_orders(workloads.ALL["analysis_stack4_rgb_512x768"], hatq.hatq_hadamard_order)
+    assert [L.hblock for L in wl.layers] == [192, 192, 192, 320]
+    x_np, params = wl.generate()
+    st = stack.Stack(wl, params)
+    x0 = torch.from_numpy(x_np).to(st.dev)
+    st.step(x0)
+    torch.cuda.synchronize()
+    for i in range(st.nL - 1):
+        if not st.requant[i]:
+            q1, s1 = hatq.hatq_fwht_quant_act(st.ys[i], st.act_hb[i + 1])
+            assert torch.equal(s1, st.sc[i + 1]) and torch.equal(q1, st.codes(i + 1))
+    _check_sample(orc, st, _oracle_prepared(orc, wl, params), x_np, 0, False)
