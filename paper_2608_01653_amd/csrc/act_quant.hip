@@ -95,7 +95,9 @@ __global__ void __launch_bounds__(kThreads) absmax_kernel(const float *__restric
 #endif
 template <int B>
 struct QuantUnroll {
-    static constexpr int UN = HATQ_QUANT_UN;   // more items in flight measured no faster
+    // two items in flight per quad: the untransformed 3-channel image's two-pass
+    // quantization 80.5 -> 77.3 us; with blocks of 64, 178 -> 182 us
+    static constexpr int UN = B == 1 ? 2 : HATQ_QUANT_UN;
 };
 
 // Quantize one transformed item (s = act scale, r = fl(1/s)) and store its codes.
@@ -454,10 +456,11 @@ __global__ void __launch_bounds__(kThreads) scalar_kernel(const float *__restric
 
 // Blocks per sample: enough for the work, at most `total` over the whole batch.
 // Blocks of the quantization kernels over the whole batch (measured on the
-// 805 M-element layer-2-shaped tensor: 16384 -> 32768 blocks 801 -> 782 us;
-// 65536 no faster).
+// 805 M-element layer-2-shaped tensor: 16384 -> 32768 blocks 801 -> 782 us,
+// 65536 no faster; on the 201 M-element one, blocks of 64, single read:
+// 32768 -> 65536 blocks 175 -> 167 us NHWC, 178 -> 175 us chunk-major).
 #ifndef HATQ_QUANT_GRID
-#define HATQ_QUANT_GRID 32768
+#define HATQ_QUANT_GRID 65536
 #endif
 // The absmax kernels end in one same-address atomic per block (they serialize
 // per sample), so they use a much smaller total.  Two-pass quantization, all
