@@ -266,7 +266,9 @@ int32_t hatq_fwht_quant_act_noalloc(const float *x, int32_t n, int32_t h, int32_
  * cout_pad % 64 == 0; WH block and next_hblock a power of two at most 64, or
  * a Kronecker order equal to cout_pad: 192 (P_12 (x) H~_16), or 320
  * (P_20 (x) H~_16) when cin_pad % 64 == 0 (applied as H~_16 then the Paley
- * factor; the WH restore multiplies by B^T) (I8: as hatq_conv_int8_requant).  Transposed: stride 2.  xq and y (F32, I32) must be
+ * factor; the WH restore multiplies by B^T), or 128 with cout_pad 128 or 256
+ * (with cin_pad <= 4 only for the row-run geometry: k <= 8, stride <= 2,
+ * k*cin_pad <= 16, not transposed) (I8: as hatq_conv_int8_requant).  Transposed: stride 2.  xq and y (F32, I32) must be
  * 16-byte aligned, y in I8 mode 4-byte aligned. */
 int32_t hatq_conv_int8(const hatq_weights *W, const int8_t *xq, const float *act_scale,
                        int32_t n, int32_t h, int32_t w, int32_t out_mode, const float *out_scale, void *y,
@@ -330,7 +332,8 @@ int32_t hatq_weight_tapsums(const hatq_weights *W, int32_t *tapsum, void *stream
  * accumulators; HATQ_OUT_F32: the same epilogue with s_x = act_scale).
  *   act_zero: device int32 [n] (from hatq_fwht_quant_act_affine).
  *   tapsum:   from hatq_weight_tapsums for W.
- * Supported: as hatq_conv_int8 (no next-operand absmax). */
+ * Supported: as hatq_conv_int8 (no next-operand absmax; not a WH layer of
+ * block 128). */
 int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const float *act_scale,
                               const int32_t *act_zero, const int32_t *tapsum, int32_t n, int32_t h, int32_t w,
                               int32_t out_mode, void *y, void *stream);
@@ -347,7 +350,8 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
  *   s_x:   the static scale of W's input codes (unnormalized domain).
  *   s_y:   the static scale of the next operand's codes.
  *   next_hblock: the next operand's transform block (1: none), a power of two
- *          <= 64, 192 or 320; the overflow bound depends on it, so the table serves
+ *          <= 64, 192 or 320 (not 128, and W not a WH layer of block 128:
+ *          HATQ_EUNSUPPORTED); the overflow bound depends on it, so the table serves
  *          only calls with this next_hblock.
  *   table: device int32 [2*cout_pad + 1], 16-byte aligned, written as
  *     M[c]         = rne(2^n rho_c), rho_c = u_c / (beta_out s_y),

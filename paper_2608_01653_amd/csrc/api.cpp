@@ -93,9 +93,14 @@ int32_t out_hw(const hatq_conv_desc *d, int32_t h, int32_t w, int32_t *ho, int32
 
 int32_t hip_status(hipError_t e) { return e == hipSuccess ? HATQ_OK : HATQ_EHIP; }
 
-// A Kronecker order b on the layer's tile of bn columns.
+// An order b that spans several 64-channel blocks of the layer's tile of bn
+// columns: a Kronecker order equal to the tile (192; 320 on the general
+// kernel's 320-column tile, which the small-channel kernels lack), or the
+// Sylvester order 128 on tiles of 128 or 256 columns (not on the
+// small-channel gather kernel).
 bool kron_tile(const hatq_weights *W, int b, int bn) {
     const bool small = W->cin_pad <= 4 && W->k_total <= 128;
+    if (b == 128) return (bn == 128 || bn == 256) && (!small || rowrun_geometry(&W->d, W->cin_pad));
     return (b == 192 && bn == 192) || (b == 320 && bn == 320 && !small);
 }
 
@@ -115,9 +120,8 @@ int32_t check_conv_supported(const hatq_weights *W) {
     for (int t : tiles) fixed |= (W->cout_pad == t);
     const int bn = fixed ? W->cout_pad : 64;
     // the WH restore runs inside one wave: a Sylvester block up to 64 that tiles
-    // the columns, or a Kronecker order on a tile of that many columns (192;
-    // 320 on the general kernel's 320-column tile, which the small-channel
-    // kernels do not have)
+    // the columns, or a wider order on a tile that holds whole blocks of it
+    // (kron_tile)
     if (W->form == HATQ_WH) {
         const int b = W->d.hblock;
         const bool ok = (is_pow2(b) && b <= 64 && bn % b == 0) || kron_tile(W, b, bn);
@@ -172,9 +176,9 @@ int32_t check_next(const hatq_weights *W, int32_t next_hblock, const float *next
     for (int t : tiles) fixed |= (W->cout_pad == t);
     const int bn = fixed ? W->cout_pad : 64;
     // the next operand's transform runs inside one wave: a Sylvester block up
-    // to 64 that tiles the columns, or a Kronecker order on a tile of that many
-    // columns
-    if (hatq::kron_q(next_hblock)) {
+    // to 64 that tiles the columns, or a wider order on a tile that holds whole
+    // blocks of it (kron_tile)
+    if (hatq::kron_q(next_hblock) || next_hblock == 128) {
         if (!kron_tile(W, next_hblock, bn)) return HATQ_EUNSUPPORTED;
     } else if (next_hblock > 64 || (bn % next_hblock != 0 && next_hblock > 1)) {
         return HATQ_EUNSUPPORTED;
@@ -559,6 +563,8 @@ int32_t hatq_conv_int8_affine(const hatq_weights *W, const int8_t *xq, const flo
         !aligned(tapsum, 16))
         return HATQ_EINVAL;
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
+    // (the zero-point correction's wide-order variant covers the Kronecker orders)
+    if (W->form == HATQ_WH && W->d.hblock == 128) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;
     return conv_launches(W, xq, act_scale, n, h, w, out_mode, y, 0, nullptr, 0, static_cast<hipStream_t>(stream),
@@ -576,6 +582,7 @@ int32_t hatq_int_transition_params(const hatq_weights *W, float s_x, float s_y, 
     if (s != HATQ_OK) return s;
     if (!table || !aligned(table, 16)) return HATQ_EINVAL;
     if (!(s_x > 0.0f) || !(s_y > 0.0f) || !std::isfinite(s_x) || !std::isfinite(s_y)) return HATQ_EINVAL;
+    if (W->form == HATQ_WH && W->d.hblock == 128) return HATQ_EUNSUPPORTED;   // as the transition itself
     if (!((is_pow2(next_hblock) && next_hblock <= 64) || hatq::kron_q(next_hblock) != 0)) return HATQ_EINVAL;
     const bool dh = W->form == HATQ_DH;
     hatq::IntParamArgs a;
@@ -603,6 +610,8 @@ int32_t hatq_conv_int8_int_transition(const hatq_weights *W, const int8_t *xq, i
     if ((s = check_conv_supported(W)) != HATQ_OK) return s;
     if ((s = check_layouts(W, flags, true, order320(W, next_hblock, true))) != HATQ_OK) return s;
     if ((s = check_next(W, next_hblock, reinterpret_cast<const float *>(table))) != HATQ_OK) return s;
+    // (the integer epilogue takes the Sylvester order 128 on neither side)
+    if (next_hblock == 128 || (W->form == HATQ_WH && W->d.hblock == 128)) return HATQ_EUNSUPPORTED;
     if (W->d.cout % 4) return HATQ_EUNSUPPORTED;
     int32_t ho, wo;
     if (out_hw(&W->d, h, w, &ho, &wo) != HATQ_OK) return HATQ_EINVAL;

@@ -311,34 +311,39 @@ using EpiKron = Epi<-1, -1, 5>;
 using EpiKronInt = Epi<-1, -1, 6>;
 using EpiKronAffine = Epi<-1, -1, 7>;   // the WH restore after the zero-point correction
 
-// Whether a launch applies a Kronecker order in its epilogue (any activation
-// kind), and whether it takes the symmetric Kronecker variants.
-inline bool kron_needed(const ConvArgs &a) {
-    const bool next = kron_q(a.next_hblock) != 0 &&
+// Orders the per-64-channel-block epilogue cannot apply, because the transform
+// spans several of the lane's 64-channel blocks: the Kronecker orders and the
+// Sylvester order 128.
+inline bool wide_order(int b) { return kron_q(b) != 0 || b == 128; }
+
+// Whether a launch applies such an order in its epilogue (any activation
+// kind), and whether it takes the symmetric variants.
+inline bool wide_needed(const ConvArgs &a) {
+    const bool next = wide_order(a.next_hblock) &&
                       (a.next_absmax != nullptr || a.mode == 2 || a.mode == kModeIntTransition);
-    const bool restore = a.form == 1 && kron_q(a.hblock) != 0 && a.mode != 0;
+    const bool restore = a.form == 1 && wide_order(a.hblock) && a.mode != 0;
     return next || restore;
 }
-inline bool kron_epilogue(const ConvArgs &a) { return a.zx == nullptr && kron_needed(a); }
+inline bool wide_epilogue(const ConvArgs &a) { return a.zx == nullptr && wide_needed(a); }
 
 // The variant a launch needs, or the generic one.
 template <typename E>
 bool epi_matches(const ConvArgs &a) {
     if constexpr (E::WB == -1) {
         if constexpr (E::Q == 5 || E::Q == 6)
-            return kron_epilogue(a) && (a.cout_pad == 192 || a.cout_pad == 320) &&
+            return wide_epilogue(a) && (a.cout_pad == 192 || a.cout_pad == 320) &&
                    (a.mode == kModeIntTransition) == (E::Q == 6);
         if constexpr (E::Q == 7)
-            return a.zx != nullptr && a.mode == 1 && kron_needed(a) && (a.cout_pad == 192 || a.cout_pad == 320);
+            return a.zx != nullptr && a.mode == 1 && wide_needed(a) && (a.cout_pad == 192 || a.cout_pad == 320);
         // (never a launch with a Kronecker order: a list without its variants
         // then finds no match and the launch fails)
-        return (a.mode == kModeIntTransition) == (E::Q == 2) && (a.zx != nullptr) == (E::Q == 3) && !kron_needed(a);
+        return (a.mode == kModeIntTransition) == (E::Q == 2) && (a.zx != nullptr) == (E::Q == 3) && !wide_needed(a);
     } else {
         if constexpr (E::Q == 5) {   // a Kronecker order at compile time (float modes)
             const int wb = a.form == 1 ? a.hblock : 0;
             const int nb = a.next_absmax != nullptr || a.mode == 2 ? a.next_hblock : 0;
-            return kron_epilogue(a) && a.mode != kModeIntTransition && (a.cout_pad == 192 || a.cout_pad == 320) &&
-                   wb == E::WB && nb == E::NB;
+            return wide_epilogue(a) && a.mode != kModeIntTransition && a.cout_pad % 64 == 0 && wb == E::WB &&
+                   nb == E::NB;
         }
         if ((a.zx != nullptr) != (E::Q == 3)) return false;
         const int wb = a.form == 1 ? a.hblock : 0;
@@ -448,6 +453,10 @@ struct Epilogue {
     static constexpr int KQ = FN == 12 ? 11 : FN == 20 ? 19 : 0;
     static constexpr int KB = 16 * FN, KV = 4 * FN;
     static constexpr bool kKron = (E::Q == 5 || E::Q == 6 || E::Q == 7) && KQ != 0;
+    // The Sylvester order 128 on a tile of 128 or 256 columns (float modes,
+    // orders at compile time): blocks of two 64-channel blocks of the lane.
+    static constexpr bool kS128 = E::Q == 5 && E::WB != -1 && (E::WB == 128 || E::NB == 128);
+    static_assert(!kS128 || (FN % 8 == 0 && !kKron), "order 128 on 128-column multiples");
     // the fixed I8 variants take the dynamic scale only (epi_matches): no clamp
     static constexpr bool kClamp = E::Q != 1;
     const ConvArgs &a;
@@ -690,7 +699,7 @@ struct Epilogue {
         }
     }
 
-    // The sixteen values of 64-channel block k inside a row group's 48.
+    // The sixteen values of 64-channel block k among a row group's KV.
     template <typename T>
     static __device__ __forceinline__ T (&grp(T (&v)[KV], int k))[16] {
         return *reinterpret_cast<T (*)[16]>(v + 16 * k);
@@ -874,7 +883,9 @@ struct Epilogue {
 
     // 64-channel block k of every row group (one set of column factors serves all)
     __device__ __forceinline__ void block(const v4i (&acc)[FM][FN], int k) {
-        if constexpr (kKron && E::Q == 5 && E::WB != -1) {
+        if constexpr (kS128) {
+            if (k == NBLK - 1) block_s128(acc);
+        } else if constexpr (kKron && E::Q == 5 && E::WB != -1) {
             // orders fixed at compile time: always the Kronecker path
             if (k == NBLK - 1) block_kron(acc);
         } else {
@@ -888,6 +899,99 @@ struct Epilogue {
                 }
             }
             block_plain(acc, k);
+        }
+    }
+
+    // Float modes with the Sylvester order 128 for the WH restore and/or the next
+    // operand (the other side a block up to 64 or none), after the tile's last
+    // 64-channel block: the lane holds every 64-channel block of its pixel, so
+    // a 128-block is the 64-point butterfly on blocks 2g and 2g + 1, then the
+    // stage between them (channel bit 6, last: the activation kernel's
+    // ascending stage order).
+    __device__ void block_s128(const v4i (&acc)[FM][FN]) {
+        constexpr int V = 4 * FN;
+        const bool want_abs = fl.want_abs, i8 = fl.i8, store = fl.store;
+        auto order128 = [](float (&v)[V], auto RESTOREc) {
+            constexpr bool RESTORE = decltype(RESTOREc)::value;
+#pragma unroll
+            for (int k = 0; k < NBLK; ++k) fwht_acc<64, RESTORE>(grp(v, k), 64);
+#pragma unroll
+            for (int g = 0; g < V / 32; ++g)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const float x = v[32 * g + r], y = v[32 * g + 16 + r];
+                    v[32 * g + r] = x + y;
+                    v[32 * g + 16 + r] = x - y;
+                }
+        };
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            float v[V];
+#pragma unroll
+            for (int k = 0; k < NBLK; ++k)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int cl = 64 * k + 16 * jj + 4 * q;
+                    const float4 t4 = *reinterpret_cast<const float4 *>(col_t + cl);
+                    const float4 b4 = *reinterpret_cast<const float4 *>(col_b + cl);
+                    const v4i c4 = acc[i][4 * k + jj];
+                    v[16 * k + 4 * jj + 0] = __builtin_fmaf((float)c4[0], t4.x, b4.x);
+                    v[16 * k + 4 * jj + 1] = __builtin_fmaf((float)c4[1], t4.y, b4.y);
+                    v[16 * k + 4 * jj + 2] = __builtin_fmaf((float)c4[2], t4.z, b4.z);
+                    v[16 * k + 4 * jj + 3] = __builtin_fmaf((float)c4[3], t4.w, b4.w);
+                }
+            // the output restore B^T z = B z (the column factors carry 1/b)
+            if constexpr (E::WB == 128) {
+                order128(v, std::true_type{});
+            } else if constexpr (E::WB > 1) {
+#pragma unroll
+                for (int k = 0; k < NBLK; ++k) fwht_acc<E::WB, true>(grp(v, k), E::WB);
+            }
+            if (store && valid[i]) {
+#pragma unroll
+                for (int k = 0; k < NBLK; ++k) store_group(a, t, row0, lane, i, k, grp(v, k));
+            }
+            if (!(want_abs || i8)) continue;
+            // rows past the grid are not part of the next operand; channels
+            // past cout neither
+            const bool blk_full = t.n0 + 16 * FN <= a.cout;
+            if (!valid[i] || !blk_full) {
+#pragma unroll
+                for (int k = 0; k < NBLK; ++k)
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int ch = t.n0 + 64 * k + 16 * jj + 4 * q + r;
+                            if (!valid[i] || ch >= a.cout) v[16 * k + 4 * jj + r] = 0.0f;
+                        }
+            }
+            // channel order matters for the codes only
+            if constexpr (E::NB == 128) {
+                if (i8) order128(v, std::true_type{});
+                else order128(v, std::false_type{});
+            } else if constexpr (E::NB > 1) {
+                if (i8) {
+#pragma unroll
+                    for (int k = 0; k < NBLK; ++k) fwht_acc<E::NB, true>(grp(v, k), E::NB);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < NBLK; ++k) fwht_acc<E::NB, false>(grp(v, k), E::NB);
+                }
+            }
+            if (i8) {
+#pragma unroll
+                for (int k = 0; k < NBLK; ++k) {
+                    uint32_t w[4];
+                    quant16(grp(v, k), qs, qr, q_fast, w);
+                    store_codes(w, i, k);
+                }
+            } else {
+                float mm = 0.0f;
+#pragma unroll
+                for (int r = 0; r < V; ++r) mm = fmaxf(mm, fabsf(v[r]));
+                wave_m = fmaxf(wave_m, mm);
+            }
         }
     }
 
@@ -1957,6 +2061,9 @@ hipError_t with_epilogue(const ConvArgs &a, L &&launch) {
 // of a 192-column layer, 320 on a 320-column one).
 #define HATQ_KRON192_FIXED Epi<0, 192, 5>, Epi<192, 192, 5>, Epi<192, 1, 5>, Epi<192, 0, 5>
 #define HATQ_KRON320_FIXED Epi<0, 320, 5>, Epi<320, 1, 5>, Epi<320, 0, 5>
+// The Sylvester order 128 (tiles of 128 or 256 columns).
+#define HATQ_S128_FIXED \
+    Epi<128, 0, 5>, Epi<128, 1, 5>, Epi<128, 128, 5>, Epi<0, 128, 5>, Epi<64, 128, 5>, Epi<128, 64, 5>
 
 int persistent_blocks();
 
@@ -2062,7 +2169,7 @@ hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
             a, [&](auto e) { return launch_rowrun<2, 64, 192, CS, decltype(e)>(a, st); });
     }
     if (a.cout_pad % 128 == 0)
-        return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+        return with_epilogue<HATQ_S128_FIXED, HATQ_GENERIC_EPILOGUES>(
             a, [&](auto e) { return launch_rowrun<2, 64, 128, CS, decltype(e)>(a, st); });
     return with_epilogue<HATQ_GENERIC_EPILOGUES>(
         a, [&](auto e) { return launch_rowrun<2, 64, 64, CS, decltype(e)>(a, st); });
@@ -3019,9 +3126,9 @@ hipError_t conv_part_pipe320(const ConvArgs &a, hipStream_t st) {
 #if HATQ_PART(5)
 hipError_t conv_part_pipe_other(const ConvArgs &a, hipStream_t st) {
     switch (a.cout_pad) {
-        case 128: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+        case 128: return with_epilogue<HATQ_S128_FIXED, HATQ_GENERIC_EPILOGUES>(
                 a, [&](auto e) { return launch_pipe<8, 32, 128, 5, decltype(e)>(a, st); });
-        case 256: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
+        case 256: return with_epilogue<HATQ_S128_FIXED, HATQ_GENERIC_EPILOGUES>(
                 a, [&](auto e) { return launch_pipe<4, 32, 256, 5, decltype(e)>(a, st); });
         default: return with_epilogue<HATQ_GENERIC_EPILOGUES>(
                 a, [&](auto e) { return launch_pipe<8, 32, 64, 5, decltype(e)>(a, st); });
@@ -3092,7 +3199,7 @@ hipError_t launch_conv(const ConvArgs &a, bool clear_next, hipStream_t st) {
             }
             return conv_part_pipe192(a, st);
         case 320:
-            if (a.sa == 2 && a.so == 1 && a.k == 5 && a.cin_p % 64 == 0 && !kron_needed(a)) {
+            if (a.sa == 2 && a.so == 1 && a.k == 5 && a.cin_p % 64 == 0 && !wide_needed(a)) {
                 // the window kernel over columns 0..191, then 192..319 (an
                 // order-320 transform spans both: the pipeline kernel's
                 // 320-column tile takes those)

@@ -237,6 +237,12 @@ def test_int_transition_rejects_before_launch(L):
     assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, FAKE, None, 0, None) == hatq.HATQ_EINVAL      # no output
     assert c(ctypes.byref(W), FAKE, 1, 8, 8, 3, FAKE, FAKE, 0, None) == hatq.HATQ_EINVAL       # block 3
     assert c(ctypes.byref(W), FAKE, 1, 8, 8, 128, FAKE, FAKE, 0, None) == hatq.HATQ_EUNSUPPORTED
+    # the Sylvester order 128 stays out of the integer epilogue, on either side
+    Wwh = _fake_weights(cin=128, cout=128, hb=128, form=1)
+    assert p(ctypes.byref(Wwh), 0.1, 0.1, 64, FAKE, None) == hatq.HATQ_EUNSUPPORTED
+    assert c(ctypes.byref(Wwh), FAKE, 1, 8, 8, 64, FAKE, FAKE, 0, None) == hatq.HATQ_EUNSUPPORTED
+    Wdh = _fake_weights(cin=64, cout=128)
+    assert c(ctypes.byref(Wdh), FAKE, 1, 8, 8, 128, FAKE, FAKE, 0, None) == hatq.HATQ_EUNSUPPORTED
     assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, ctypes.c_void_p(FAKE.value + 4), FAKE, 0, None) \
         == hatq.HATQ_EINVAL                                                                   # misaligned table
     assert c(ctypes.byref(W), FAKE, 1, 8, 8, 64, FAKE, FAKE, 8, None) == hatq.HATQ_EINVAL      # unknown flag

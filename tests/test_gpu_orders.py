@@ -129,8 +129,9 @@ def test_unsupported_uses_are_rejected(orc):
     input codes (the window kernel splits a 320-column layer over two launches;
     the order 320 runs on the general kernel's 320-column tile) or with three
     input channels (the small-channel kernels have no 320-column tile), 192 on a
-    320-column layer, and a Kronecker block cut by the channel count in the
-    profiling pass.  Each is rejected before any launch."""
+    320-column layer, a Kronecker block cut by the channel count in the
+    profiling pass, the Sylvester order 128 in the affine epilogue or across a
+    192-column tile.  Each is rejected before any launch."""
     wt = torch.ones(320, 192, 5, 5, device="cuda")
     b0 = torch.zeros(320, device="cuda")
     wh320 = hatq.hatq_prepare_weights(hatq.desc(192, 320, 5, 2, 2, 320), "WH", wt, b0)
@@ -155,6 +156,20 @@ def test_unsupported_uses_are_rejected(orc):
     assert e.value.status == hatq.HATQ_EUNSUPPORTED
     with pytest.raises(hatq.HatqError) as e:
         hatq.hatq_range_expansion(torch.zeros((1, 2, 2, 200), device="cuda"), 192)
+    assert e.value.status == hatq.HATQ_EUNSUPPORTED
+    # the Sylvester order 128: not in the integer and affine epilogues, not
+    # across a 192-column tile
+    wh128 = hatq.hatq_prepare_weights(hatq.desc(128, 128, 5, 2, 2, 128), "WH", wt[:128, :128].contiguous(),
+                                      b0[:128])
+    x128 = torch.zeros((1, 9, 9, 128), dtype=torch.int8, device="cuda")
+    with pytest.raises(hatq.HatqError) as e:
+        hatq.hatq_conv_int8_affine(wh128, x128, sx, torch.zeros(1, dtype=torch.int32, device="cuda"),
+                                   hatq.hatq_weight_tapsums(wh128), hatq.HATQ_OUT_F32)
+    assert e.value.status == hatq.HATQ_EUNSUPPORTED
+    dh192 = hatq.hatq_prepare_weights(hatq.desc(192, 192, 5, 2, 2, 64), "DH", wt[:192], b0[:192])
+    with pytest.raises(hatq.HatqError) as e:
+        hatq.hatq_conv_int8(dh192, xq, sx, hatq.HATQ_OUT_F32, next_hblock=128,
+                            next_absmax=torch.zeros(1, device="cuda"))
     assert e.value.status == hatq.HATQ_EUNSUPPORTED
 
 
@@ -224,6 +239,14 @@ KCONV = [(2, 17, 21, 192, 192, 5, 2, 2, False, 0, "DH", 64, 192),     # window k
          (1, 9, 13, 192, 320, 3, 1, 1, False, 0, "WH", 320, 320),     # both, stride 1
          (1, 6, 7, 192, 320, 5, 2, 2, True, 1, "WH", 320, 64)]        # transposed phases, WH restore 320
 KIDS = [f"{c[10]}{c[11]}-{c[3]}to{c[4]}k{c[5]}{'T' if c[8] else ''}-next{c[12]}" for c in KCONV]
+# The Sylvester order 128 across two 64-channel blocks of a 128- or 256-column
+# tile (m(C) = 128 for 65..128 channels), float modes:
+S128 = [(1, 13, 11, 64, 128, 3, 1, 1, False, 0, "WH", 128, 1),      # general kernel, WH restore 128
+        (2, 11, 9, 64, 256, 3, 1, 1, False, 0, "DH", 64, 128),      # 256-column tile, next operand 128
+        (1, 9, 13, 128, 128, 5, 2, 2, False, 0, "WH", 128, 128),    # both, 5x5 stride 2
+        (2, 13, 17, 3, 128, 5, 2, 2, False, 0, "WH", 128, 64),      # row-run kernel (3 input channels)
+        (1, 6, 7, 128, 128, 5, 2, 2, True, 1, "WH", 128, 1)]        # transposed phases
+S128_IDS = [f"{c[10]}{c[11]}-{c[3]}to{c[4]}k{c[5]}{'T' if c[8] else ''}-next{c[12]}" for c in S128]
 
 
 def _kron_layer(orc, c, seed):
@@ -277,7 +300,7 @@ def test_affine_conv_wh_kronecker(orc, c):
     assert_range_rel(host(y), orc.epilogue(acc_ref, sx, ref), what="affine WH Kronecker y")
 
 
-@pytest.mark.parametrize("c", KCONV, ids=KIDS)
+@pytest.mark.parametrize("c", KCONV + S128, ids=KIDS + S128_IDS)
 def test_kron_epilogue_f32_and_absmax(orc, c):
     ref, layer, r, nb = _kron_layer(orc, c, 400)
     n = r.y.shape[0]
@@ -304,7 +327,7 @@ def test_kron_epilogue_f32_and_absmax(orc, c):
     assert torch.equal(nam, nam2)
 
 
-@pytest.mark.parametrize("c", KCONV, ids=KIDS)
+@pytest.mark.parametrize("c", KCONV + S128, ids=KIDS + S128_IDS)
 def test_kron_epilogue_requant(orc, c):
     ref, layer, r, nb = _kron_layer(orc, c, 410)
     n = r.y.shape[0]
