@@ -226,7 +226,8 @@ int32_t hatq_fwht_quant_act_c64(const float *x, int32_t n, int32_t h, int32_t w,
  * device memory (code under HIP graph capture, tight serving loops, harnesses
  * that forbid allocation): the two-pass form (absmax, then codes) keeps the
  * per-sample absmax in a static array inside the library, one copy per GPU,
- * of HATQ_NOALLOC_MAX_SAMPLES floats (16 KB), held until the process ends.
+ * of HATQ_NOALLOC_MAX_SAMPLES x 32 floats (512 KB: the per-block maxima of a
+ * sample spread over 32 slots), held until the process ends.
  * Arguments, results and support as hatq_fwht_quant_act with absmax = NULL;
  * n > HATQ_NOALLOC_MAX_SAMPLES returns HATQ_EUNSUPPORTED.  Allocates nothing.
  * Every call on one GPU shares that GPU's array (it is cleared by the call

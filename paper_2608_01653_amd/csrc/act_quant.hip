@@ -25,7 +25,7 @@
 // library runs on holds its own copy until the process ends.  In host code the
 // name is a stand-in, not a device address: the address comes from
 // hipGetSymbolAddress, looked up once per device (scratch_absmax below).
-static __device__ __align__(256) float scratch[hatq::kNoAllocMaxSamples];
+static __device__ __align__(256) float scratch[hatq::kNoAllocMaxSamples * hatq::kAbsSlots];
 
 namespace hatq {
 
@@ -85,7 +85,7 @@ __global__ void __launch_bounds__(kThreads) absmax_kernel(const float *__restric
         float b = red[0];
 #pragma unroll
         for (int k = 1; k < kThreads / 64; ++k) b = fmaxf(b, red[k]);
-        atomic_max_nonneg(absmax + n, b);
+        atomic_max_nonneg(absmax + (int64_t)n * kAbsSlots + blockIdx.x % kAbsSlots, b);
     }
 }
 
@@ -184,7 +184,7 @@ template <int B>
 __global__ void __launch_bounds__(kThreads) quant_kernel(const float *__restrict__ x, int64_t E,
                                                          const float *__restrict__ absmax,
                                                          int8_t *__restrict__ xq,
-                                                         float *__restrict__ act_scale, int cc) {
+                                                         float *__restrict__ act_scale, int cc, int slots) {
     constexpr int I = ItemShape<B>::I;
     constexpr int R = ItemShape<B>::R;
     constexpr int UN = QuantUnroll<B>::UN;
@@ -205,7 +205,10 @@ __global__ void __launch_bounds__(kThreads) quant_kernel(const float *__restrict
     const float *xs = x + (int64_t)n * E;
     int8_t *qs = xq + (int64_t)n * E;
     const int t = threadIdx.x & 3;
-    const float s = act_scale_from_absmax(absmax[n]);
+    // the sample's absmax: one value (given), or the maximum of its slots
+    float am = absmax[(int64_t)n * slots];
+    for (int k = 1; k < slots; ++k) am = fmaxf(am, absmax[(int64_t)n * slots + k]);
+    const float s = act_scale_from_absmax(am);
     if (blockIdx.x == 0 && threadIdx.x == 0) act_scale[n] = s;
     const float r = 1.0f / s;
     // The fast path needs r and every t finite and normal-range; a scale below
@@ -475,13 +478,10 @@ __global__ void __launch_bounds__(kThreads) scalar_kernel(const float *__restric
 #ifndef HATQ_QUANT_GRID
 #define HATQ_QUANT_GRID 65536
 #endif
-// The absmax kernels end in one same-address atomic per block (they serialize
-// per sample), so they use a much smaller total.  Two-pass quantization, all
-// else equal: 8192 / 4096 / 2048 / 1024 / 512 blocks 148 / 107 / 90 / 84 /
-// 81 us on 16 x 1024 x 1024 x 3 (no transform) and 1269 (2048) -> 1238 us
-// (512) on 16 x 512 x 512 x 192 (blocks of 64).
+// The absmax kernels end in one atomic per block on one of the sample's
+// kAbsSlots slots.
 #ifndef HATQ_ABSMAX_GRID
-#define HATQ_ABSMAX_GRID 512
+#define HATQ_ABSMAX_GRID 4096
 #endif
 int grid_x(int64_t work_units, int per_block, int n, int total = HATQ_QUANT_GRID) {
     int64_t want = (work_units + per_block - 1) / per_block;
@@ -499,12 +499,13 @@ hipError_t launch_vector(const float *x, int n, int64_t E, const float *absmax_i
     const float *A = absmax_in;
     if (!A) {
         dim3 grid(grid_x(items, kQuadsPerBlock, n, HATQ_ABSMAX_GRID), n);
-        fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(ws_absmax), n, 0u);
+        fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(ws_absmax), n * kAbsSlots, 0u);
         absmax_kernel<B><<<grid, kThreads, 0, st>>>(x, E, ws_absmax);
         A = ws_absmax;
     }
+    const int slots = absmax_in ? 1 : kAbsSlots;
     dim3 grid(grid_x(items, kQuadsPerBlock * QuantUnroll<B>::UN, n), n);
-    quant_kernel<B><<<grid, kThreads, 0, st>>>(x, E, A, xq, act_scale, c64);
+    quant_kernel<B><<<grid, kThreads, 0, st>>>(x, E, A, xq, act_scale, c64, slots);
     return hipGetLastError();
 }
 
@@ -625,7 +626,8 @@ hipError_t launch_act_quant_noalloc(const float *x, int n, int64_t E, int hblock
     float *ws = nullptr;
     const hipError_t e = scratch_absmax(&ws);
     if (e != hipSuccess) return e;
-    // the two-pass path clears ws[0 .. n) with a fill kernel before its atomics
+    // the two-pass path clears the n * kAbsSlots slots with a fill kernel
+    // before its atomics
     return launch_act_quant(x, n, E, hblock, nullptr, ws, xq, act_scale, st);
 }
 

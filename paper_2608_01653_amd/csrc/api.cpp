@@ -396,7 +396,7 @@ int32_t hatq_export_weights(const hatq_weights *W, int8_t *wq, float *w_scale, f
     return HATQ_OK;
 }
 
-size_t hatq_fwht_quant_ws_bytes(int32_t n) { return n > 0 ? align256((size_t)n * 4) : 0; }
+size_t hatq_fwht_quant_ws_bytes(int32_t n) { return n > 0 ? align256((size_t)n * 4 * hatq::kAbsSlots) : 0; }
 
 int32_t hatq_fwht_quant_act(const float *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t hblock,
                             const float *absmax, int8_t *xq, float *act_scale, void *ws, size_t ws_bytes,

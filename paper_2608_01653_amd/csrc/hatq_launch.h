@@ -7,14 +7,19 @@
 namespace hatq {
 
 // Activation transform + quantization of n samples of E floats each.
-// absmax_in == nullptr: two passes through ws_absmax (n floats of scratch).
+// absmax_in == nullptr: two passes through ws_absmax (n * kAbsSlots floats of
+// scratch: the absmax pass's blocks of a sample spread their maxima over
+// kAbsSlots slots, so no address takes more than a few atomics, and the
+// quantization takes the maximum of the slots).
+constexpr int kAbsSlots = 32;
 // c64 > 0: the codes go out in the chunk-major layout of a sample of c64
 // channels ([E / c64 pixels] per 64-channel plane; c64 % 64 == 0, hblock <= 64).
 hipError_t launch_act_quant(const float *x, int n, int64_t E, int hblock, const float *absmax_in,
                             float *ws_absmax, int8_t *xq, float *act_scale, hipStream_t st, int c64 = 0);
 
 // The same two-pass quantization with the per-sample absmax in the library's
-// static device scratch (no caller workspace, no allocation): n <= kNoAllocMaxSamples.
+// static device scratch (no caller workspace, no allocation): n <= kNoAllocMaxSamples
+// (kNoAllocMaxSamples * kAbsSlots floats, 512 KB).
 constexpr int kNoAllocMaxSamples = 4096;
 hipError_t launch_act_quant_noalloc(const float *x, int n, int64_t E, int hblock, int8_t *xq, float *act_scale,
                                     hipStream_t st);
