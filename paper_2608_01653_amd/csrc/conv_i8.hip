@@ -2425,6 +2425,12 @@ __device__ __forceinline__ int halo_block(int wave, int j, int nblk) {
     const int bi = wave + kHaloWaves * j;
     return bi < nblk ? bi : bi - kHaloWaves;
 }
+// The same over the NW waves of one DMA role (nblk >= NW).
+template <int NW>
+__device__ __forceinline__ int role_block(int w, int j, int nblk) {
+    const int bi = w + NW * j;
+    return bi < nblk ? bi : bi - NW;
+}
 
 template <int BN, int STAGES, typename E>
 __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo_kernel(const ConvArgs a) {
@@ -2696,13 +2702,17 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     constexpr int FM = TM / 16;
     constexpr int FN = BN / 16;
     constexpr int B_BLK = BN / 16;
-    constexpr int PER = (B_BLK + kHaloWaves - 1) / kHaloWaves;
+    // the DMA roles: waves 0-3 refill the weight ring, waves 4-7 the window
+    // (one of each per SIMD), so a wave's vmcnt counts one kind of refill
+    constexpr int RW = kHaloWaves / 2;
+    constexpr int PER = (B_BLK + RW - 1) / RW;                      // weight DMAs per weight wave per step
     constexpr int W_BLK = (G::RECS + 15) / 16;
-    constexpr int HB = (W_BLK + kHaloWaves - 1) / kHaloWaves;
+    constexpr int HB = (W_BLK + RW - 1) / RW;                       // window DMAs per window wave per half
     constexpr int B_BYTES = BN * 64;
     constexpr uint32_t RING_BASE = 2 * G::HALF_BYTES;
     static_assert(BN % 64 == 0 && FM == 2 && TM == TW, "tile");
-    static_assert(B_BLK >= kHaloWaves && W_BLK >= kHaloWaves && W_BLK * 1024 <= G::HALF_BYTES, "DMA blocks");
+    static_assert(B_BLK >= RW && W_BLK >= RW && W_BLK * 1024 <= G::HALF_BYTES && PER <= HB && 2 * HB <= 32,
+                  "DMA blocks");
     static_assert((G::HALF_BYTES & 0x1FF) == 0 && (RING_BASE & 0x1FF) == 0 && (B_BYTES & 0x1FF) == 0, "swizzle bits");
     static_assert(G::HALF_BYTES + 1024 < 65536 && (SLOTS - 1) * B_BYTES + (FN - 1) * 1024 < 65536, "read offsets");
     static_assert(2 * (TH - 1) + K <= 2 * G::HR && 2 * (TW - 1) + K <= 2 * G::HCC, "window size");
@@ -2717,6 +2727,8 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const bool wwave = wave < RW;               // refills the weights (else the window)
+    const int ri = wwave ? wave : wave - RW;    // index within the role
     const int ntiles = a.n * a.tiles_h * a.tiles_w;   // one column range per launch
     int v = blockIdx.x;
     Tile tile = block_tile(a, xcd_tile(v, ntiles), TH, TW, BN);
@@ -2729,70 +2741,84 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int8_t *>(a.wp), (short)0, (int)((int64_t)a.cout_pad * a.pack_stride), 0x00020000);
 
-    // window DMA offsets of parity half hp of tile t (as in conv_halo_kernel)
-    auto window_offsets = [&](const Tile &t, int hp, uint32_t(&o)[HB]) {
+    // DMA offsets.  A window wave: doff[j] is the offset of its record j in the
+    // even-row half (rows 2 rr), the odd-row record (2 rr + 1) one input row
+    // further, and bit hp * HB + j of dmask says whether the record of half hp
+    // lies in the image (else its DMA reads zeros).  A weight wave: doff[j],
+    // j < PER.  One array, so the roles share the registers.
+    uint32_t doff[HB];
+    uint32_t dmask = 0;
+    // NHWC: 64 bytes of chunk c at pixel * cin_p + 64 c; chunk-major: a plane of
+    // h * w * 64 bytes per chunk (whole 128-byte lines per refill)
+    const uint32_t row_stride = (uint32_t)a.w * (a.xq_c64 ? 64u : (uint32_t)cin_p);
+    const uint32_t chunk_stride = a.xq_c64 ? (uint32_t)(a.h * a.w * 64) : 64u;
+    auto window_offsets = [&](const Tile &t) {
         const int ih0 = t.gi0 * 2 + a.bah, iw0 = t.gj0 * 2 + a.baw;
+        uint32_t m = 0;
 #pragma unroll
         for (int j = 0; j < HB; ++j) {
-            const int f = 16 * halo_block(wave, j, W_BLK) + (lane >> 2);
+            const int f = 16 * role_block<RW>(ri, j, W_BLK) + (lane >> 2);
             const int g = (lane & 3) ^ swz(f);
             const int rr = f / (2 * G::HCC), rem = f - rr * (2 * G::HCC);
             const int cp = rem / G::HCC, cc = rem - cp * G::HCC;
-            const int row = 2 * rr + hp, col = 2 * cc + cp;
+            const int row = 2 * rr, col = 2 * cc + cp;
             const int ih = ih0 + row, iw = iw0 + col;
-            const bool in = f < G::RECS && row < rows_used && col < cols_used && (unsigned)ih < (unsigned)a.h &&
-                            (unsigned)iw < (unsigned)a.w;
-            // NHWC: 64 bytes of chunk c at pixel * cin_p + 64 c; chunk-major: a
-            // plane of h * w * 64 bytes per chunk (whole 128-byte lines per refill)
-            const uint32_t pix = (uint32_t)((t.nb * a.h + ih) * a.w + iw);
+            const bool cin = f < G::RECS && col < cols_used && (unsigned)iw < (unsigned)a.w;
+            const bool in0 = cin && row < rows_used && (unsigned)ih < (unsigned)a.h;
+            const bool in1 = cin && row + 1 < rows_used && (unsigned)(ih + 1) < (unsigned)a.h;
+            // modulo 2^32 (ih may be -1 or -2 here, with its odd row inside)
+            const uint32_t pix = (uint32_t)(t.nb * a.h + ih) * (uint32_t)a.w + (uint32_t)iw;
             const uint32_t off = a.xq_c64 ? (uint32_t)(t.nb * (cin_p - 64) * a.h * a.w) + pix * 64u : pix * (uint32_t)cin_p;
-            o[j] = in ? off + 16u * g : kOobOffset;
+            doff[j] = off + 16u * g;
+            m |= (in0 ? 1u << j : 0u) | (in1 ? 1u << (HB + j) : 0u);
         }
+        dmask = m;
     };
-    uint32_t h_off[2][HB];
-    window_offsets(tile, 0, h_off[0]);
-    window_offsets(tile, 1, h_off[1]);
-    const uint32_t chunk_stride = a.xq_c64 ? (uint32_t)(a.h * a.w * 64) : 64u;
-    // refill of window half hp from the offsets o with chunk c; zero_fill: the
+    // (window waves) refill of window half hp with chunk c; zero_fill: the
     // same number of DMAs reading zeros
-    auto burst_from = [&](int hp, const uint32_t(&o)[HB], int chunk) {
+    auto burst = [&](int hp, int chunk) {
         int8_t *dst = halo + hp * G::HALF_BYTES;
 #pragma unroll
-        for (int j = 0; j < HB; ++j)
-            dma16s(rx, dst + 1024 * halo_block(wave, j, W_BLK), o[j], (uint32_t)chunk * chunk_stride);
+        for (int j = 0; j < HB; ++j) {
+            const uint32_t o = (dmask >> (hp * HB + j)) & 1u ? doff[j] + (hp ? row_stride : 0u) : kOobOffset;
+            dma16s(rx, dst + 1024 * role_block<RW>(ri, j, W_BLK), o, (uint32_t)chunk * chunk_stride);
+        }
     };
-    auto burst = [&](int hp, int chunk) { burst_from(hp, h_off[hp], chunk); };
     auto zero_fill = [&](int hp) {
         int8_t *dst = halo + hp * G::HALF_BYTES;
 #pragma unroll
-        for (int j = 0; j < HB; ++j) dma16s(rx, dst + 1024 * halo_block(wave, j, W_BLK), kOobOffset, 0u);
+        for (int j = 0; j < HB; ++j) dma16s(rx, dst + 1024 * role_block<RW>(ri, j, W_BLK), kOobOffset, 0u);
     };
-    uint32_t b_off[PER];
+    if (wwave) {
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int nn = 16 * halo_block(wave, j, B_BLK) + (lane >> 2);
-        const int g = (lane & 3) ^ swz(nn);
-        b_off[j] = (uint32_t)((tile.n0 + nn) * 64 + 16 * g);
+        for (int j = 0; j < PER; ++j) {
+            const int nn = 16 * role_block<RW>(ri, j, B_BLK) + (lane >> 2);
+            const int g = (lane & 3) ^ swz(nn);
+            doff[j] = (uint32_t)((tile.n0 + nn) * 64 + 16 * g);
+        }
+    } else {
+        window_offsets(tile);
     }
     const uint32_t cp64 = (uint32_t)a.cout_pad * 64u;
     const uint32_t tap_w = (uint32_t)nchunks * cp64;
     // Step j of a chunk: odd kernel rows first (kh = 1, 3), then even (0, 2, 4).
     auto step_kh = [](int j) { return j < NODD ? 1 + 2 * (j / K) : 2 * ((j - NODD) / K); };
     auto step_kw = [](int j) { return j < NODD ? j % K : (j - NODD) % K; };
-    // weight step J of the chunk at chunk_off into its slot; or zeros into it
+    // (weight waves) weight step J of the chunk at chunk_off into its slot; or
+    // zeros into it
     auto issue_b = [&](auto Jc, uint32_t chunk_off) {
         constexpr int J = decltype(Jc)::value;
         constexpr int TAP = step_kh(J) * K + step_kw(J);
         int8_t *sb = bring + (J % SLOTS) * B_BYTES;
         const uint32_t woff = (uint32_t)TAP * tap_w + chunk_off;
 #pragma unroll
-        for (int j = 0; j < PER; ++j) dma16s(rw, sb + 1024 * halo_block(wave, j, B_BLK), b_off[j], woff);
+        for (int j = 0; j < PER; ++j) dma16s(rw, sb + 1024 * role_block<RW>(ri, j, B_BLK), doff[j], woff);
     };
     auto issue_zero = [&](auto Jc) {
         constexpr int J = decltype(Jc)::value;
         int8_t *sb = bring + (J % SLOTS) * B_BYTES;
 #pragma unroll
-        for (int j = 0; j < PER; ++j) dma16s(rw, sb + 1024 * halo_block(wave, j, B_BLK), kOobOffset, 0u);
+        for (int j = 0; j < PER; ++j) dma16s(rw, sb + 1024 * role_block<RW>(ri, j, B_BLK), kOobOffset, 0u);
     };
 
     // per-lane A fragment addresses of the 15 window offsets (kh >> 1, kw):
@@ -2833,11 +2859,16 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
 
     // prologue: odd half of chunk 0, weight steps 0 .. 3
     static_assert(SLOTS - 1 <= NTAP, "prologue within chunk 0");
-    burst(1, 0);
-    unroll<SLOTS - 1>([&](auto Jc) { issue_b(Jc, 0u); });
+    if (wwave)
+        unroll<SLOTS - 1>([&](auto Jc) { issue_b(Jc, 0u); });
+    else
+        burst(1, 0);
     // the raw per-channel scale and bias, while the first DMAs are in flight
     for (int c = tid; c < BN; c += kHaloThreads) column_raw(a, tile.n0 + c, s_raw[c], s_raw[BN + c]);
-    wait_vmcnt_lds<(SLOTS - 2) * PER>();
+    if (wwave)
+        wait_vmcnt_lds<(SLOTS - 2) * PER>();
+    else
+        wait_vmcnt_lds<0>();
     __builtin_amdgcn_s_barrier();
 
   for (;;) {
@@ -2864,6 +2895,7 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
         // (or tile), zeros past the last
         auto issue_step = [&](auto Sc) {
             constexpr int S = decltype(Sc)::value;
+            if (!wwave) return;
             if constexpr (S < NTAP) {
                 issue_b(std::integral_constant<int, S>{}, coff);
             } else {
@@ -2877,23 +2909,31 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
             v4i(&anext)[FM] = (J & 1) ? fa0 : fa1;
             // One barrier per two steps (at even J; steps 24 and 0 of the
             // next chunk both have one, as a chunk has an odd number of steps).
-            // At a barrier every wave's DMAs of the weight steps read before
-            // the next barrier (up to J + 2, prefetches included; up to J + 1
-            // at J = 24) have landed; then the weight steps up to J + 4 are
-            // issued, whose slots were last read before this barrier.  A
-            // window refill is issued after the weights of its barrier, so
-            // the next barrier's wait may leave it in flight.
+            // At a barrier the weight waves' DMAs of the weight steps read
+            // before the next barrier (up to J + 2, prefetches included; up to
+            // J + 1 at J = 24) have landed; then the weight steps up to J + 4
+            // are issued, whose slots were last read before this barrier.  A
+            // window half is refilled right after the barrier past its last
+            // read (even rows at step 0, odd rows of the next chunk at step
+            // NODD) and must have landed at the barrier before its first read
+            // (step NODD - 2, as step NODD - 1 prefetches step NODD's
+            // fragments; step 24, which prefetches the next chunk's step 0):
+            // 8 and 14 steps later.  Loads retire in issue order, so a window
+            // refill in the same wave's count as the weights would have to land
+            // at the weights' next wait.
             if constexpr ((J & 1) == 0) {
-                if constexpr (J == 0) {
-                    // a block's later tiles: the data of steps 0-2 was complete
-                    // before the previous epilogue's stores (no wait, so the
-                    // stores drain meanwhile)
-                    if (c != 0 || first_tile) wait_vmcnt<PER>();
-                } else if constexpr (J == 2 || J == NODD + 2) {
-                    wait_vmcnt<HB>();
-                } else if constexpr (J == NTAP - 1) {
-                    wait_vmcnt<PER>();
-                } else {
+                if (wwave) {
+                    if constexpr (J == 0) {
+                        // a block's later tiles: the data of steps 0-2 was
+                        // complete before the previous epilogue's stores (no
+                        // wait, so the stores drain meanwhile)
+                        if (c != 0 || first_tile) wait_vmcnt<PER>();
+                    } else if constexpr (J == NTAP - 1) {
+                        wait_vmcnt<PER>();
+                    } else {
+                        wait_vmcnt<0>();
+                    }
+                } else if constexpr (J == NODD - 2 || J == NTAP - 1) {
                     wait_vmcnt<0>();
                 }
                 __builtin_amdgcn_s_barrier();
@@ -2906,15 +2946,20 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
                     issue_step(std::integral_constant<int, J + 3>{});
                     issue_step(std::integral_constant<int, J + 4>{});
                 }
-                if constexpr (J == 0) burst(0, c);   // even rows of this chunk
+                if constexpr (J == 0) {             // even rows of this chunk
+                    if (!wwave) burst(0, c);
+                }
                 if constexpr (J == NODD) {          // odd rows of the next chunk (or tile)
-                    if (more) {
-                        burst(1, c + 1);
-                    } else if (has_next) {
-                        window_offsets(block_tile(a, xcd_tile(v + (int)gridDim.x, ntiles), TH, TW, BN), 1, h_off[1]);
-                        burst(1, 0);
-                    } else {
-                        zero_fill(1);
+                    if (!wwave) {
+                        if (more) {
+                            burst(1, c + 1);
+                        } else if (has_next) {
+                            // the even rows of this tile were fetched at step 0
+                            window_offsets(block_tile(a, xcd_tile(v + (int)gridDim.x, ntiles), TH, TW, BN));
+                            burst(1, 0);
+                        } else {
+                            zero_fill(1);
+                        }
                     }
                 }
             }
@@ -2944,33 +2989,34 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
 #pragma unroll
         for (int i = 0; i < FM; ++i) fa0[i] = fa1[i];
     }
-    // this tile's column factors (every wave finished the previous epilogue
-    // many barriers ago); the DMAs of the next tile stay in flight
-    const float sxv = tile_sx_uniform(a, tile.nb);
-    for (int c = tid; c < BN; c += kHaloThreads) column_from_raw(a, sxv, s_raw[c], s_raw[BN + c], s_col[c], s_col[BN + c]);
-    wait_lds();
-    __builtin_amdgcn_s_barrier();
-    // the next tile's DMAs (its odd window rows, weight steps 0-3) complete
-    // before this wave issues stores: they are then not counted behind them
-    wait_vmcnt<0>();
     {
-        // the epilogue reads the arguments afresh each tile (scalar loads from
-        // the kernel argument segment, through a pointer the compiler cannot
-        // see through): hoisted out of the tile loop they would stay live
-        // through the main loop and spill
+        // the column factors and the epilogue read the arguments afresh each
+        // tile (scalar loads from the kernel argument segment, through a
+        // pointer the compiler cannot see through): hoisted out of the tile
+        // loop they would stay live through the main loop and spill
         const __attribute__((address_space(4))) ConvArgs *kargs =
             (const __attribute__((address_space(4))) ConvArgs *)__builtin_amdgcn_kernarg_segment_ptr();
         asm volatile("" : "+s"(kargs));
+        const ConvArgs &ka = *(const ConvArgs *)kargs;
+        // this tile's column factors (every wave finished the previous
+        // epilogue many barriers ago); the DMAs of the next tile stay in flight
+        const float sxv = tile_sx_uniform(ka, tile.nb);
+        for (int c = tid; c < BN; c += kHaloThreads)
+            column_from_raw(ka, sxv, s_raw[c], s_raw[BN + c], s_col[c], s_col[BN + c]);
+        wait_lds();
+        __builtin_amdgcn_s_barrier();
+        // the next tile's DMAs (its odd window rows, weight steps 0-3) complete
+        // before this wave issues stores: they are then not counted behind them
+        wait_vmcnt<0>();
         // the same for the lane-derived addresses and masks
         int elane = lane;
         asm volatile("" : "+v"(elane));
-        epilogue_regs<TW, FM, FN, E>(*(const ConvArgs *)kargs, acc, tile, wave * TM, elane, s_col, s_col + BN);
+        epilogue_regs<TW, FM, FN, E>(ka, acc, tile, wave * TM, elane, s_col, s_col + BN);
     }
     v += gridDim.x;
     if (v >= ntiles) break;
-    // h_off[1] already holds the new tile's odd-row offsets
+    // a window wave's offsets are already the new tile's
     tile = block_tile(a, xcd_tile(v, ntiles), TH, TW, BN);
-    window_offsets(tile, 0, h_off[0]);
   }
     wait_vmcnt<0>();   // no DMA may still be writing LDS when the block ends
 }
