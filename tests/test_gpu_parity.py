@@ -170,6 +170,7 @@ CONV = [  # (n, h, w, cin, cout, k, stride, pad, transposed, out_pad, form, hblo
     (2, 20, 21, 64, 192, 5, 2, 2, False, 0, "DH", 64),    # LDS window path, one chunk
     (150, 18, 18, 192, 192, 5, 2, 2, False, 0, "DH", 64), # 300 ragged tiles: blocks walk several, across samples
     (140, 17, 19, 192, 192, 5, 2, 2, False, 0, "WH", 64), # the same, WH
+    (150, 18, 18, 64, 192, 5, 2, 2, False, 0, "DH", 64),  # one chunk, 300 tiles (the static tile order)
     (130, 17, 18, 192, 320, 5, 2, 2, False, 0, "WH", 64), # 320 columns: two launches (192 + 128), 260 tiles each
     (3, 21, 30, 192, 320, 5, 2, 2, False, 0, "DH", 64),   # the same split with the DH epilogues
 ]
