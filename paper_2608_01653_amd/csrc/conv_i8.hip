@@ -1560,14 +1560,57 @@ __device__ __forceinline__ void half_stage_i64(int64_t (&v)[32]) {
 // Output columns of a tile: one MFMA column set.
 constexpr int kRr32W = 32;
 
+// Codes of one 64-channel block of a pixel whose lane pair (j, 0), (j, 1)
+// holds channel h + 2 rho in v[rho] (both transforms done), stored at yq: word
+// w holds channels h + 8w + {0, 2, 4, 6}; after the exchange each pair (0, 2),
+// (1, 3), (4, 6), (5, 7) holds the even and the odd channels of 8 consecutive
+// ones, 16h + 8w' (+ 32 for the last two pairs), and a byte interleave puts them
+// in order.
+__device__ __forceinline__ void rr32_block_codes(const float (&v)[32], float qs, float qr, bool q_fast, bool valid,
+                                                 int8_t *yq, bool a16) {
+    uint32_t c[32];
+    rr32_codes<32>(v, qs, qr, q_fast, c);
+    uint32_t w[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) w[q] = pack_low_bytes(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
+    rr32_exchange(w);
+    uint32_t o[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = q + (q & 2), d = e + 2;   // pairs (0, 2), (1, 3), (4, 6), (5, 7)
+        o[2 * q] = __builtin_amdgcn_perm(w[d], w[e], 0x05010400u);       // [e0, o0, e1, o1]
+        o[2 * q + 1] = __builtin_amdgcn_perm(w[d], w[e], 0x07030602u);   // [e2, o2, e3, o3]
+    }
+    if (valid) rr32_store<true>(yq, a16, o);
+}
+
+// half_stage<M> on each 32-value block of a lane's N values.
+template <int M, int N>
+__device__ __forceinline__ void half_stage_blocks(float (&v)[N]) {
+    static_assert(N % 32 == 0, "32-value blocks");
+#pragma unroll
+    for (int r = 0; r < N; ++r)
+        if (!(r & M)) pair_swap<32>(v[r], v[r | M]);
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        if (r & M) continue;
+        const float s = v[r] + v[r | M], d = v[r] - v[r | M];
+        v[r] = s;
+        v[r | M] = d;
+    }
+}
+
 // PAIRED (HATQ_PAIRED, the blocks equal): the next operand is z itself (B_next
 // B_Cout = b I), so neither transform runs: the factors carry no 1/b (times b,
 // exact), the maximum is max |z|, and the codes are those of z in the MFMA
 // layout, where one swap of words across the lane halves gives each lane 32
 // contiguous channels.
-template <int TH, int CIN, int NS, int PASS, bool PAIRED, int MINB>
+template <int TH, int CIN, int NS, int PASS, bool PAIRED, int MINB, int ORD = 64>
 __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArgs a) {
     constexpr int TW = kRr32W, BN = 192, NBLK = BN / 64, RPW = TH / 4;
+    // ORD: the order of both transforms (blocks of 64, or the order 192 on
+    // all 192 channels: float passes only, both transforms explicit)
+    static_assert(ORD == 64 || (ORD == 192 && PASS <= 1 && !PAIRED), "transform order");
     using P = RowRunPatch<TH, TW, CIN>;
     constexpr int RS = P::RS, PWORDS = P::WORDS, PIT = P::PIT;
     constexpr int WROWS = 2 * NS;   // kernel rows the MFMAs cover
@@ -1692,6 +1735,76 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
                         (a.yq_c64 ? (int64_t)nb * (a.cout - 64) * hw + pix * 64 : pix * a.cout);
                 kstride = a.yq_c64 ? 64 * hw : 64;
             }
+            if constexpr (ORD == 192) {
+                // Order 192 = P_12 (x) H~_16 on both sides (the WH restore and
+                // the next operand): all six 32-channel tiles of the pixel
+                // first.  Register r of tile u holds channel c = 32u + 8
+                // floor(r/4) + 4h + r mod 4: the H~_16 index l = c mod 16 has
+                // bits 0-1 = r bits 0-1, bit 2 = h and bit 3 = r bit 2; the
+                // Paley index a = c / 16 = 2u + r bit 3, so v[16u + r] is value
+                // r mod 8 of group a at v[8a + r mod 8].  The stages are the
+                // other kernels' (H~_16 in ascending bit order, then the Paley
+                // factor summed in ascending order; transposed for the
+                // restore), the lane-half stage left unrestored as for blocks of
+                // 64, so each 64-channel block ends in the layout the codes
+                // store takes (channel h + 2 rho).
+                float v[96];
+                // the weight fragments are the same for every row: an opaque
+                // base keeps the compiler from holding all 18 (72 registers)
+                // across the row loop
+                int wbase = (h * BN + j) * 16;
+                asm volatile("" : "+v"(wbase));
+#pragma unroll
+                for (int u = 0; u < 6; ++u) {
+                    // one tile at a time: the dequantized values replace its
+                    // accumulators
+                    v16i acc = v16i{};
+#pragma unroll
+                    for (int s = 0; s < NS; ++s) {
+                        const v4i fa = *reinterpret_cast<const v4i *>(s_w + wbase + (2 * s * BN + 32 * u) * 16);
+                        acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa, fb[s], acc, 0, 0, 0);
+                    }
+#pragma unroll
+                    for (int q4 = 0; q4 < 4; ++q4) {
+                        const int c0 = 32 * u + 8 * q4 + 4 * h;
+                        const float4 t4 = *reinterpret_cast<const float4 *>(s_col + c0);
+                        const float4 b4 = *reinterpret_cast<const float4 *>(s_col + BN + c0);
+                        const int r0 = 16 * u + 4 * q4;
+                        v[r0 + 0] = __builtin_fmaf((float)acc[4 * q4 + 0], t4.x, b4.x);
+                        v[r0 + 1] = __builtin_fmaf((float)acc[4 * q4 + 1], t4.y, b4.y);
+                        v[r0 + 2] = __builtin_fmaf((float)acc[4 * q4 + 2], t4.z, b4.z);
+                        v[r0 + 3] = __builtin_fmaf((float)acc[4 * q4 + 3], t4.w, b4.w);
+                    }
+                }
+                // the WH restore B^T (z / b) (the factors carry 1/b): H~_16,
+                // then the transposed Paley factor
+                reg_stage<1>(v);
+                reg_stage<2>(v);
+                half_stage_blocks<2>(v);   // l bit 2; then h = l bit 1
+                reg_stage<4>(v);
+                paley_stage_t<11>(v);
+                // the next operand B_next y: H~_16 (l bit 1 now in h), then the
+                // Paley factor
+                reg_stage<1>(v);
+                half_stage_blocks<1>(v);   // l bit 1; then h = l bit 0
+                reg_stage<2>(v);
+                reg_stage<4>(v);
+                paley_stage<11>(v);
+                if constexpr (PASS == 0) {
+                    float mm = 0.0f;
+#pragma unroll
+                    for (int r = 0; r < 96; ++r) mm = fmaxf(mm, fabsf(v[r]));
+                    wave_m = fmaxf(wave_m, valid ? mm : 0.0f);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < NBLK; ++k) {
+                        float vk[32];
+#pragma unroll
+                        for (int r = 0; r < 32; ++r) vk[r] = v[32 * k + r];
+                        rr32_block_codes(vk, qs, qr, q_fast, valid, ybase + k * kstride, a16);
+                    }
+                }
+            } else {
 #pragma unroll 1
             for (int k = 0; k < NBLK; ++k) {
                 v16i acc[2];
@@ -1847,26 +1960,9 @@ __global__ void __launch_bounds__(kThreads, MINB) conv_rr32_kernel(const ConvArg
                     wave_m = fmaxf(wave_m, valid ? mm : 0.0f);
                 } else {
                     if constexpr (!PAIRED) reg_stage<16>(v);
-                    uint32_t c[32];
-                    rr32_codes<32>(v, qs, qr, q_fast, c);
-                    // word w holds channels h + 8w + {0, 2, 4, 6}; after the
-                    // exchange each pair (0, 2), (1, 3), (4, 6), (5, 7) holds the
-                    // even and the odd channels of 8 consecutive ones, 16h + 8w'
-                    // (+ 32 for the last two pairs), and a byte interleave puts
-                    // them in order
-                    uint32_t w[8];
-#pragma unroll
-                    for (int q = 0; q < 8; ++q) w[q] = pack_low_bytes(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
-                    rr32_exchange(w);
-                    uint32_t o[8];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int e = q + (q & 2), d = e + 2;   // pairs (0, 2), (1, 3), (4, 6), (5, 7)
-                        o[2 * q] = __builtin_amdgcn_perm(w[d], w[e], 0x05010400u);       // [e0, o0, e1, o1]
-                        o[2 * q + 1] = __builtin_amdgcn_perm(w[d], w[e], 0x07030602u);   // [e2, o2, e3, o3]
-                    }
-                    if (valid) rr32_store<true>(ybase + k * kstride, a16, o);
+                    rr32_block_codes(v, qs, qr, q_fast, valid, ybase + k * kstride, a16);
                 }
+            }
             }
         }
         // the other buffer was last read before the previous barrier
@@ -2099,6 +2195,17 @@ inline int rr32_pass(const ConvArgs &a) {
     return -1;
 }
 
+// The same with the order 192 = P_12 (x) H~_16 (m(192), the paper's order for
+// 192 channels) on both sides instead of blocks of 64: 0, 1, or -1.
+inline int rr32_kron_pass(const ConvArgs &a) {
+    if (!a.rowrun || a.cin_p != 3 || a.cout != 192 || a.cout_pad != 192 || a.n_base != 0) return -1;
+    if (a.k < 5 || a.k > 6 || a.sa > 2 || a.nksteps != 2) return -1;
+    if (a.form != 1 || a.hblock != 192 || a.next_hblock != 192 || a.zx != nullptr || a.paired) return -1;
+    if (a.mode == 1 && a.y == nullptr && a.next_absmax != nullptr) return 0;
+    if (a.mode == 2 && a.q_absmax != nullptr) return 1;
+    return -1;
+}
+
 #ifndef HATQ_RR32_TH
 #define HATQ_RR32_TH 16
 #endif
@@ -2110,12 +2217,17 @@ inline int rr32_pass(const ConvArgs &a) {
 #ifndef HATQ_RR32_MINB_INT
 #define HATQ_RR32_MINB_INT 3
 #endif
+// the order 192 (a pixel's 96 values per lane at once)
+#ifndef HATQ_RR32_MINB_KRON
+#define HATQ_RR32_MINB_KRON 2
+#endif
 
-template <int TH, int NS, int PASS, bool PAIRED, int MINB>
+template <int TH, int NS, int PASS, bool PAIRED, int MINB, int ORD = 64>
 hipError_t launch_rr32(const ConvArgs &a, hipStream_t st) {
     ConvArgs b = a;
     const int64_t tiles = set_tiles(b, TH, kRr32W, 192);
-    if (tiles <= 0 || rr32_pass(b) != PASS || (b.paired != 0) != PAIRED) return hipErrorInvalidValue;
+    if (tiles <= 0 || (ORD == 64 ? rr32_pass(b) : rr32_kron_pass(b)) != PASS || (b.paired != 0) != PAIRED)
+        return hipErrorInvalidValue;
     // every byte offset of the input fits the 32-bit buffer range
     if ((int64_t)b.n * b.h * b.w * 3 >= ((int64_t)1 << 31) - 64) return hipErrorInvalidValue;
     const int64_t per = (int64_t)b.tiles_h * b.tiles_w;
@@ -2125,7 +2237,7 @@ hipError_t launch_rr32(const ConvArgs &a, hipStream_t st) {
     b.run_tiles = (int32_t)run;
     const int64_t blocks = (int64_t)b.n * ((per + run - 1) / run);
     if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-    conv_rr32_kernel<TH, 3, NS, PASS, PAIRED, MINB><<<(unsigned)blocks, kThreads, 0, st>>>(b);
+    conv_rr32_kernel<TH, 3, NS, PASS, PAIRED, MINB, ORD><<<(unsigned)blocks, kThreads, 0, st>>>(b);
     return hipGetLastError();
 }
 
@@ -2152,6 +2264,8 @@ hipError_t launch_rowrun_n(const ConvArgs &a, hipStream_t st) {
         if constexpr (CS == 3) {
             const int pass = rr32_pass(a);
             if (pass >= 0) return conv_part_rr32(a, pass, st);
+            const int kpass = rr32_kron_pass(a);
+            if (kpass >= 0) return conv_part_rr32(a, 3 + kpass, st);
         }
         if constexpr (CS == 3)
             return with_epilogue<Epi<64, 64, 1>, Epi<64, 64, 2>, Epi<64, 64, 4>, Epi<0, 64>, Epi<0, 1>, Epi<0, 0>,
@@ -3186,6 +3300,9 @@ hipError_t conv_part_rowrun3(const ConvArgs &a, hipStream_t st) { return launch_
 #endif
 #if HATQ_PART(13)
 hipError_t conv_part_rr32(const ConvArgs &a, int pass, hipStream_t st) {
+    // 3, 4: the absmax and codes passes with the order 192 on both sides
+    if (pass == 3) return launch_rr32<HATQ_RR32_TH, 3, 0, false, HATQ_RR32_MINB_KRON, 192>(a, st);
+    if (pass == 4) return launch_rr32<HATQ_RR32_TH, 3, 1, false, HATQ_RR32_MINB_KRON, 192>(a, st);
     if (pass == 2)
         return a.paired ? launch_rr32<HATQ_RR32_TH, 3, 2, true, HATQ_RR32_MINB_INT>(a, st)
                         : launch_rr32<HATQ_RR32_TH, 3, 2, false, HATQ_RR32_MINB_INT>(a, st);

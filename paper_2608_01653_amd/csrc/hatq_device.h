@@ -18,6 +18,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 #include "hatq_launch.h"
 
 namespace hatq {
@@ -134,6 +136,16 @@ constexpr int paley1_entry(int q, int i, int j) {
     return (i == j ? 1 : 0) + s;
 }
 
+// f(integral_constant<int, J>) for J = 0 .. N-1, unrolled at compile time.
+template <typename F, int... J>
+__device__ __forceinline__ void static_for_seq(F &&f, std::integer_sequence<int, J...>) {
+    (f(std::integral_constant<int, J>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
 template <int Q>
 struct Paley1Table {
     int8_t s[Q + 1][Q + 1];
@@ -153,27 +165,30 @@ struct ItemShape {
 };
 
 // The Paley factor of a Kronecker order on the register groups of an item:
-// out[a] = sum over c, ascending, of P[a][c] * v[c] for each of the four values
-// j of group c (v[4*c + j]).  One position j at a time, so only P temporaries
-// are live next to the values.
+// out[a] = sum over c, ascending, of P[a][c] * v[c] for each of the G values j
+// of group c (v[G*c + j]; G = 4 in the quad and 16 x 16 MFMA layouts, 8 in the
+// 32 x 32 one).  One position j at a time, so only P temporaries are live next
+// to the values.
 template <int Q, int R4>
 __device__ __forceinline__ void paley_stage(float (&v)[R4]) {
-    constexpr int P = Q + 1;
-    static_assert(R4 == 4 * P, "one register group per Paley index");
+    constexpr int P = Q + 1, G = R4 / P;   // G registers per Paley index
+    static_assert(R4 == G * P && (G == 4 || G == 8), "one register group per Paley index");
     constexpr Paley1Table<Q> H{};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    // positions by a compile-time loop: with eight of them a counted loop was
+    // left rolled, and its run-time register index sent v to scratch memory
+    static_for<G>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
         float out[P];
 #pragma unroll
         for (int a = 0; a < P; ++a) {
             float acc = H.s[a][0] > 0 ? v[j] : -v[j];
 #pragma unroll
-            for (int c = 1; c < P; ++c) acc = H.s[a][c] > 0 ? acc + v[4 * c + j] : acc - v[4 * c + j];
+            for (int c = 1; c < P; ++c) acc = H.s[a][c] > 0 ? acc + v[G * c + j] : acc - v[G * c + j];
             out[a] = acc;
         }
 #pragma unroll
-        for (int a = 0; a < P; ++a) v[4 * a + j] = out[a];
-    }
+        for (int a = 0; a < P; ++a) v[G * a + j] = out[a];
+    });
 }
 
 // The transposed factor, out[a] = sum over c, ascending, of P[c][a] * v[c]: the
@@ -181,33 +196,33 @@ __device__ __forceinline__ void paley_stage(float (&v)[R4]) {
 // Paley-I matrix is not symmetric).
 template <int Q, int R4>
 __device__ __forceinline__ void paley_stage_t(float (&v)[R4]) {
-    constexpr int P = Q + 1;
-    static_assert(R4 == 4 * P, "one register group per Paley index");
+    constexpr int P = Q + 1, G = R4 / P;   // G registers per Paley index
+    static_assert(R4 == G * P && (G == 4 || G == 8), "one register group per Paley index");
     constexpr Paley1Table<Q> H{};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    static_for<G>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
         float out[P];
 #pragma unroll
         for (int a = 0; a < P; ++a) {
             float acc = H.s[0][a] > 0 ? v[j] : -v[j];
 #pragma unroll
-            for (int c = 1; c < P; ++c) acc = H.s[c][a] > 0 ? acc + v[4 * c + j] : acc - v[4 * c + j];
+            for (int c = 1; c < P; ++c) acc = H.s[c][a] > 0 ? acc + v[G * c + j] : acc - v[G * c + j];
             out[a] = acc;
         }
 #pragma unroll
-        for (int a = 0; a < P; ++a) v[4 * a + j] = out[a];
-    }
+        for (int a = 0; a < P; ++a) v[G * a + j] = out[a];
+    });
 }
 
 // The same on int64 values (exact, so any summation order), one register
 // position j at a time to keep the temporaries small.
 template <int Q, bool TRANSPOSED, int R4>
 __device__ __forceinline__ void paley_stage_i64(int64_t (&v)[R4]) {
-    constexpr int P = Q + 1;
-    static_assert(R4 == 4 * P, "one register group per Paley index");
+    constexpr int P = Q + 1, G = R4 / P;   // G registers per Paley index
+    static_assert(R4 == G * P && (G == 4 || G == 8), "one register group per Paley index");
     constexpr Paley1Table<Q> H{};
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < G; ++j) {
         int64_t out[P];
 #pragma unroll
         for (int a = 0; a < P; ++a) {
@@ -215,12 +230,12 @@ __device__ __forceinline__ void paley_stage_i64(int64_t (&v)[R4]) {
 #pragma unroll
             for (int c = 0; c < P; ++c) {
                 const int sgn = TRANSPOSED ? H.s[c][a] : H.s[a][c];
-                acc = sgn > 0 ? acc + v[4 * c + j] : acc - v[4 * c + j];
+                acc = sgn > 0 ? acc + v[G * c + j] : acc - v[G * c + j];
             }
             out[a] = acc;
         }
 #pragma unroll
-        for (int a = 0; a < P; ++a) v[4 * a + j] = out[a];
+        for (int a = 0; a < P; ++a) v[G * a + j] = out[a];
     }
 }
 

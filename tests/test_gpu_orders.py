@@ -239,6 +239,13 @@ KCONV = [(2, 17, 21, 192, 192, 5, 2, 2, False, 0, "DH", 64, 192),     # window k
          (1, 9, 13, 192, 320, 3, 1, 1, False, 0, "WH", 320, 320),     # both, stride 1
          (1, 6, 7, 192, 320, 5, 2, 2, True, 1, "WH", 320, 64)]        # transposed phases, WH restore 320
 KIDS = [f"{c[10]}{c[11]}-{c[3]}to{c[4]}k{c[5]}{'T' if c[8] else ''}-next{c[12]}" for c in KCONV]
+# Order 192 on both sides of the 3-channel layer (the paper's order for 192
+# channels): the 32 x 32 small-cin kernel's absmax and codes passes, against the
+# 16 x 16 row-run kernel's fp32-output path (the same fp32 stages) and the oracle
+KRR = [(2, 13, 17, 3, 192, 5, 2, 2, False, 0, "WH", 192, 192),      # one tile
+       (2, 70, 100, 3, 192, 5, 2, 2, False, 0, "WH", 192, 192),     # ragged tiles, runs of several
+       (1, 64, 96, 3, 192, 6, 2, 2, False, 0, "WH", 192, 192)]      # 6 x 6 kernel
+KRR_IDS = [f"rr32-{c[1]}x{c[2]}k{c[5]}" for c in KRR]
 # The Sylvester order 128 across two 64-channel blocks of a 128- or 256-column
 # tile (m(C) = 128 for 65..128 channels), float modes:
 S128 = [(1, 13, 11, 64, 128, 3, 1, 1, False, 0, "WH", 128, 1),      # general kernel, WH restore 128
@@ -300,7 +307,7 @@ def test_affine_conv_wh_kronecker(orc, c):
     assert_range_rel(host(y), orc.epilogue(acc_ref, sx, ref), what="affine WH Kronecker y")
 
 
-@pytest.mark.parametrize("c", KCONV + S128, ids=KIDS + S128_IDS)
+@pytest.mark.parametrize("c", KCONV + S128 + KRR, ids=KIDS + S128_IDS + KRR_IDS)
 def test_kron_epilogue_f32_and_absmax(orc, c):
     ref, layer, r, nb = _kron_layer(orc, c, 400)
     n = r.y.shape[0]
@@ -327,7 +334,7 @@ def test_kron_epilogue_f32_and_absmax(orc, c):
     assert torch.equal(nam, nam2)
 
 
-@pytest.mark.parametrize("c", KCONV + S128, ids=KIDS + S128_IDS)
+@pytest.mark.parametrize("c", KCONV + S128 + KRR, ids=KIDS + S128_IDS + KRR_IDS)
 def test_kron_epilogue_requant(orc, c):
     ref, layer, r, nb = _kron_layer(orc, c, 410)
     n = r.y.shape[0]
