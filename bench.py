@@ -119,8 +119,9 @@ def kernel_label(st, key):
     if part in ("absmax", "requant"):
         nb = st.act_hb[i + 1]
         # the 32 x 32 MFMA variant: 3 -> 192 channels, 5x5 or 6x6, WH blocks of 64
-        # into a next operand with blocks of 64
-        rr32 = L.cin == 3 and L.cout == 192 and L.k in (5, 6) and L.form == "WH" and L.hblock == 64 and nb == 64
+        # into a next operand with blocks of 64, or the order 192 on both sides
+        rr32 = (L.cin == 3 and L.cout == 192 and L.k in (5, 6) and L.form == "WH"
+                and (L.hblock, nb) in ((64, 64), (192, 192)))
         name = "conv_rr32_kernel" if rr32 else "conv_rowrun_kernel"
         what = "next-operand absmax only" if part == "absmax" else "codes of the next operand"
         return f"{name} ({shape}; {what}, WH restore + B_{nb} explicit)"

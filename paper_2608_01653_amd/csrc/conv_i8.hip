@@ -723,6 +723,14 @@ struct Epilogue {
                                   (kNB <= 1 || kNB == KB || (kNB <= 64 && (kNB & (kNB - 1)) == 0))),
                       "fixed Kronecker variant orders");
         const int nb = kFixed ? kNB : a.next_hblock;
+        // the lane's column-factor base (channel 4q of each 16), on the
+        // 192-column tiles with a value the compiler cannot see through: with
+        // its known low bits it turned base + offset into an or and kept one
+        // address per channel group (spills in the window kernel; the 320-column
+        // tile, with its accumulators in AGPRs, does better without)
+        int qo = 4 * q;
+        if constexpr (FN == 12) asm volatile("" : "+v"(qo));
+        const float *ctq = col_t + qo, *cbq = col_b + qo;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
             float v[KV];
@@ -734,9 +742,9 @@ struct Epilogue {
                 if (fl.affine) zero_point_fix(cc, i, k);
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) {
-                    const int cl = 64 * k + 16 * jj + 4 * q;
-                    const float4 t4 = *reinterpret_cast<const float4 *>(col_t + cl);
-                    const float4 b4 = *reinterpret_cast<const float4 *>(col_b + cl);
+                    const int cl = 64 * k + 16 * jj;
+                    const float4 t4 = *reinterpret_cast<const float4 *>(ctq + cl);
+                    const float4 b4 = *reinterpret_cast<const float4 *>(cbq + cl);
                     v[16 * k + 4 * jj + 0] = __builtin_fmaf((float)cc[jj][0], t4.x, b4.x);
                     v[16 * k + 4 * jj + 1] = __builtin_fmaf((float)cc[jj][1], t4.y, b4.y);
                     v[16 * k + 4 * jj + 2] = __builtin_fmaf((float)cc[jj][2], t4.z, b4.z);
