@@ -89,6 +89,36 @@ __global__ void __launch_bounds__(kThreads) absmax_kernel(const float *__restric
     }
 }
 
+// The same for blocks of 1 (no transform): max |x| over the sample read as
+// float4 (E % 4 == 0), four loads per thread in flight per iteration.
+__global__ void __launch_bounds__(kThreads) absmax_flat_kernel(const float *__restrict__ x, int64_t E,
+                                                               float *__restrict__ absmax) {
+    const int n = blockIdx.y;
+    const float4 *xs = reinterpret_cast<const float4 *>(x + (int64_t)n * E);
+    const int64_t E4 = E >> 2;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    auto m4 = [](float m, const float4 &f) {
+        return fmaxf(fmaxf(fmaxf(m, fabsf(f.x)), fabsf(f.y)), fmaxf(fabsf(f.z), fabsf(f.w)));
+    };
+    float m = 0.0f;
+    for (; i + 3 * stride < E4; i += 4 * stride) {
+        const float4 a = xs[i], b = xs[i + stride], c = xs[i + 2 * stride], d = xs[i + 3 * stride];
+        m = m4(m4(m4(m4(m, a), b), c), d);
+    }
+    for (; i < E4; i += stride) m = m4(m, xs[i]);
+    m = wave_max(m);
+    __shared__ float red[kThreads / 64];
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float b = red[0];
+#pragma unroll
+        for (int k = 1; k < kThreads / 64; ++k) b = fmaxf(b, red[k]);
+        atomic_max_nonneg(absmax + (int64_t)n * kAbsSlots + blockIdx.x % kAbsSlots, b);
+    }
+}
+
 // Items per quad per loop iteration (all their loads issued before first use).
 #ifndef HATQ_QUANT_UN
 #define HATQ_QUANT_UN 1
@@ -498,9 +528,15 @@ hipError_t launch_vector(const float *x, int n, int64_t E, const float *absmax_i
     const int64_t items = (E + I - 1) / I;
     const float *A = absmax_in;
     if (!A) {
-        dim3 grid(grid_x(items, kQuadsPerBlock, n, HATQ_ABSMAX_GRID), n);
         fill_u32_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t *>(ws_absmax), n * kAbsSlots, 0u);
-        absmax_kernel<B><<<grid, kThreads, 0, st>>>(x, E, ws_absmax);
+        if constexpr (B == 1) {
+            // sixteen float4 per thread
+            const dim3 grid(grid_x(E / 4, kThreads * 16, n, HATQ_ABSMAX_GRID), n);
+            absmax_flat_kernel<<<grid, kThreads, 0, st>>>(x, E, ws_absmax);
+        } else {
+            const dim3 grid(grid_x(items, kQuadsPerBlock, n, HATQ_ABSMAX_GRID), n);
+            absmax_kernel<B><<<grid, kThreads, 0, st>>>(x, E, ws_absmax);
+        }
         A = ws_absmax;
     }
     const int slots = absmax_in ? 1 : kAbsSlots;
