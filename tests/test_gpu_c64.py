@@ -88,6 +88,27 @@ def test_small_cin_codes_c64(orc, c, paired):
     assert torch.equal(hatq.from_c64(yq64), yq)
 
 
+@pytest.mark.parametrize("c", [(3, 45, 141, 3, 192, 5, 2, 2, False, 0, "WH", 192)], ids=["3x45x141"])
+def test_small_cin_codes_c64_order192(orc, c):
+    """The same with the order 192 on both sides (the paper's order for 192
+    channels: the 32 x 32 small-cin kernel's order-192 passes)."""
+    n, h, w, cin, cout, k, s, p, tr, op, form, hb = c
+    rng, wt, b, ref, layer = _layer(orc, c, 104)
+    x = synth.heavy_tailed_activations(rng, (n, h, w, cin))
+    r = orc.layer_forward(x, ref)
+    xq, sx = dev(r.xq), dev(r.sx)
+    nam = torch.full((n,), -1.0, device="cuda")
+    hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32, next_hblock=192, next_absmax=nam, absmax_only=True)
+    yq, sq = hatq.hatq_conv_int8_requant(layer, xq, sx, 192, next_absmax=nam)
+    yq64, sq64 = hatq.hatq_conv_int8_requant(layer, xq, sx, 192, next_absmax=nam, yq_c64=True)
+    assert torch.equal(sq64, sq)
+    assert torch.equal(hatq.from_c64(yq64), yq)
+    # and the codes are the two-kernel path's (fp32 output, then the activation kernel)
+    y = hatq.hatq_conv_int8(layer, xq, sx, hatq.HATQ_OUT_F32)
+    q2, s2 = hatq.hatq_fwht_quant_act(y, 192, absmax=nam)
+    assert torch.equal(sq, s2) and torch.equal(yq, q2)
+
+
 def test_int_transition_c64(orc):
     """The integer transition between two window-kernel layers, both layouts in and out."""
     c = (2, 37, 29, 192, 192, 5, 2, 2, False, 0, "DH", 64)
