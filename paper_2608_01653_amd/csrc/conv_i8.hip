@@ -2876,11 +2876,17 @@ __global__ void __launch_bounds__(kHaloThreads, 1) conv_halo5_kernel(const ConvA
     const uint32_t chunk_stride = a.xq_c64 ? (uint32_t)(a.h * a.w * 64) : 64u;
     auto window_offsets = [&](const Tile &t) {
         const int ih0 = t.gi0 * 2 + a.bah, iw0 = t.gj0 * 2 + a.baw;
+        // the record positions afresh for each tile (a lane value the compiler
+        // cannot see through): hoisted out of the tile loop, its eleven records'
+        // rows and columns stayed live through the main loop and spilled in
+        // the epilogue variants with the most registers
+        int wl = lane;
+        asm volatile("" : "+v"(wl));
         uint32_t m = 0;
 #pragma unroll
         for (int j = 0; j < HB; ++j) {
-            const int f = 16 * role_block<RW>(ri, j, W_BLK) + (lane >> 2);
-            const int g = (lane & 3) ^ swz(f);
+            const int f = 16 * role_block<RW>(ri, j, W_BLK) + (wl >> 2);
+            const int g = (wl & 3) ^ swz(f);
             const int rr = f / (2 * G::HCC), rem = f - rr * (2 * G::HCC);
             const int cp = rem / G::HCC, cc = rem - cp * G::HCC;
             const int row = 2 * rr, col = 2 * cc + cp;
