@@ -140,13 +140,16 @@ def test_stack_step_teacher_forced(orc, name, samples, paired):
         _check_sample(orc, st, refs, x_np, s, paired)
 
 
-def test_stack_paper_orders_teacher_forced(orc):
-    """The 512x768 stack with one block of the paper's order m(C) per transformed
-    axis (Eq. hadamard_order: 192, 192, 192, 320) instead of blocks of 64: the
-    WH restore of order 192 and the next operand's order 192 in layer 1's two
+@pytest.mark.parametrize("name,samples", [("analysis_stack4_rgb_512x768", [0]),
+                                          ("analysis_stack4_rgb_b16_1024x1024", [0, 15])])
+def test_stack_paper_orders_teacher_forced(orc, name, samples):
+    """The stack with one block of the paper's order m(C) per transformed axis
+    (Eq. hadamard_order: 192, 192, 192, 320) instead of blocks of 64: the WH
+    restore of order 192 and the next operand's order 192 in layer 1's two
     passes, order 192 in the quantizer and in the fused absmax, and the order-320
-    WH restore of layer 4 on the 320-column tile; same rules per stage."""
-    wl = workloads.with_orders(workloads.ALL["analysis_stack4_rgb_512x768"], hatq.hatq_hadamard_order)
+    WH restore of layer 4 on the 320-column tile; same rules per stage (at the
+    batch-16 size, the step the bench's paper-order leg times)."""
+    wl = workloads.with_orders(workloads.ALL[name], hatq.hatq_hadamard_order)
     assert [L.hblock for L in wl.layers] == [192, 192, 192, 320]
     x_np, params = wl.generate()
     st = stack.Stack(wl, params)
@@ -157,4 +160,6 @@ def test_stack_paper_orders_teacher_forced(orc):
         if not st.requant[i]:
             q1, s1 = hatq.hatq_fwht_quant_act(st.ys[i], st.act_hb[i + 1])
             assert torch.equal(s1, st.sc[i + 1]) and torch.equal(q1, st.codes(i + 1))
-    _check_sample(orc, st, _oracle_prepared(orc, wl, params), x_np, 0, False)
+    refs = _oracle_prepared(orc, wl, params)
+    for s in samples:
+        _check_sample(orc, st, refs, x_np, s, False)
